@@ -1,0 +1,204 @@
+"""ctypes wrapper of the fp64 oracle (``liblirpa_ref.so``) -- test infrastructure only.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import this module.
+Networks are given as lists of layer dicts (``kind``, shapes, fp32 ``W`` and ``b``), the format
+of ``paper_2011_13824_amd.workloads``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "lirpa_ref.c")
+LIB = os.path.join(HERE, "liblirpa_ref.so")
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP)."""
+    if force or not os.path.exists(LIB):
+        tmp = LIB + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, SRC,
+                        "-lm"], check=True)
+        os.replace(tmp, LIB)
+    return LIB
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("in_c", ctypes.c_int), ("in_h", ctypes.c_int),
+                ("in_w", ctypes.c_int), ("out_c", ctypes.c_int), ("out_h", ctypes.c_int),
+                ("out_w", ctypes.c_int), ("k", ctypes.c_int), ("stride", ctypes.c_int),
+                ("pad", ctypes.c_int), ("W", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build(force=False)
+        L = ctypes.CDLL(LIB)
+        i, f, d, l = ctypes.c_int, ctypes.c_float, ctypes.c_double, ctypes.c_long
+        L.ref_num_relu.argtypes = [_P, i]
+        L.ref_num_relu.restype = l
+        L.ref_bound.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, _P, _P, _P, _P, i]
+        L.ref_bound_grad.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, i, _P, _P, i]
+        L.ref_optimize.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, _P, _P, i, d, d, d, d, i, _P,
+                                   _P, i]
+        L.ref_linear_bound_fn.argtypes = [_P, i, _P, f, _P, i, _P, _P, _P, _P]
+        L.ref_forward.argtypes = [_P, i, _P, l, _P, _P]
+        L.ref_layer_T.argtypes = [_P, _P, l, _P]
+        L.ref_layer_fwd.argtypes = [_P, _P, l, _P]
+        L.ref_relax.argtypes = [d, d, i, i, d, _P]
+        for fn in ("ref_bound", "ref_bound_grad", "ref_optimize", "ref_linear_bound_fn",
+                   "ref_forward", "ref_layer_T", "ref_layer_fwd", "ref_relax"):
+            getattr(L, fn).restype = i
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class RefNet:
+    """Holds the fp32 weights and the ctypes layer array for one network."""
+
+    def __init__(self, layers: list[dict]):
+        self.layers = layers
+        self._keep = []
+        self.arr = (_Layer * len(layers))()
+        for i, t in enumerate(layers):
+            W = np.ascontiguousarray(t["W"], dtype=np.float32)
+            b = np.ascontiguousarray(t["b"], dtype=np.float32)
+            self._keep += [W, b]
+            self.arr[i] = _Layer(t["kind"], t["in_c"], t["in_h"], t["in_w"], t["out_c"],
+                                 t["out_h"], t["out_w"], t.get("k", 0), t.get("stride", 1),
+                                 t.get("pad", 0), W.ctypes.data, b.ctypes.data)
+        self.L = len(layers)
+        self.n_relu = int(lib().ref_num_relu(self.arr, self.L))
+        if self.n_relu < 0:
+            raise ValueError("invalid layer chain")
+        self.n0 = layers[0]["in_c"] * layers[0]["in_h"] * layers[0]["in_w"]
+        self.nL = layers[-1]["out_c"] * layers[-1]["out_h"] * layers[-1]["out_w"]
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise RuntimeError(f"{what} failed with code {rc}")
+
+
+def _f32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i8(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int8)
+
+
+def bound(net: RefNet, x0, eps, C, split=None, alpha=None, B=None, nthreads=0):
+    """lb [B,S], l [B,n_relu], u [B,n_relu], stability codes [B,n_relu] (all fp64/int8)."""
+    x0, C, split, alpha = _f32(x0), _f32(C), _i8(split), _f32(alpha)
+    if B is None:
+        B = split.shape[0] if split is not None else (alpha.shape[0] if alpha is not None else 1)
+    S = C.shape[0]
+    lb = np.zeros((B, S))
+    l = np.zeros((B, net.n_relu))
+    u = np.zeros((B, net.n_relu))
+    code = np.zeros((B, net.n_relu), dtype=np.int8)
+    _check(lib().ref_bound(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S, B, _ptr(split),
+                           _ptr(alpha), _ptr(lb), _ptr(l), _ptr(u), _ptr(code), nthreads),
+           "ref_bound")
+    return lb, l, u, code
+
+
+def bound_grad(net: RefNet, x0, eps, C, split, alpha, full=True, nthreads=0):
+    """lb [B,S] and d(sum_s lb)/d alpha [B,n_relu] at the given alpha."""
+    x0, C, split, alpha = _f32(x0), _f32(C), _i8(split), _f32(alpha)
+    B, S = alpha.shape[0], C.shape[0]
+    lb = np.zeros((B, S))
+    g = np.zeros((B, net.n_relu))
+    _check(lib().ref_bound_grad(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S, B,
+                                _ptr(split), _ptr(alpha), int(full), _ptr(lb), _ptr(g),
+                                nthreads), "ref_bound_grad")
+    return lb, g
+
+
+def optimize(net: RefNet, x0, eps, C, split, alpha0, steps, lr=0.1, beta1=0.9, beta2=0.999,
+             eps_adam=1e-8, m=None, v=None, t0=0, nthreads=0):
+    """Projected Adam on alpha; returns dict(alpha, m, v, lb_best, lb_trace)."""
+    x0, C, split = _f32(x0), _f32(C), _i8(split)
+    alpha = np.array(alpha0, dtype=np.float64, copy=True)
+    B, S = alpha.shape[0], C.shape[0]
+    m = np.zeros_like(alpha) if m is None else np.array(m, dtype=np.float64, copy=True)
+    v = np.zeros_like(alpha) if v is None else np.array(v, dtype=np.float64, copy=True)
+    best = np.zeros((B, S))
+    trace = np.zeros((steps + 1, B, S))
+    _check(lib().ref_optimize(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S, B, _ptr(split),
+                              _ptr(alpha), _ptr(m), _ptr(v), steps, lr, beta1, beta2, eps_adam,
+                              t0, _ptr(best), _ptr(trace), nthreads), "ref_optimize")
+    return dict(alpha=alpha, m=m, v=v, lb_best=best, lb_trace=trace)
+
+
+def linear_bound_fn(net: RefNet, x0, eps, C, split=None, alpha=None):
+    """A [S,n0], beta [S] of the final linear lower-bounding functions of one sub-domain."""
+    x0, C, split, alpha = _f32(x0), _f32(C), _i8(split), _f32(alpha)
+    S = C.shape[0]
+    A = np.zeros((S, net.n0))
+    beta = np.zeros(S)
+    _check(lib().ref_linear_bound_fn(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S,
+                                     _ptr(split), _ptr(alpha), _ptr(A), _ptr(beta)),
+           "ref_linear_bound_fn")
+    return A, beta
+
+
+def forward(net: RefNet, x, split=None):
+    x = np.ascontiguousarray(np.atleast_2d(x), dtype=np.float64)
+    out = np.zeros((x.shape[0], net.nL))
+    _check(lib().ref_forward(net.arr, net.L, _ptr(x), x.shape[0], _ptr(_i8(split)), _ptr(out)),
+           "ref_forward")
+    return out
+
+
+def layer_T(net: RefNet, m: int, a_out):
+    """Rows a_out [R, n_out(T_m)] -> a_out W_m [R, n_in(T_m)] (m is 1-based)."""
+    t = net.layers[m - 1]
+    a_out = np.ascontiguousarray(np.atleast_2d(a_out), dtype=np.float64)
+    nin = t["in_c"] * t["in_h"] * t["in_w"]
+    a_in = np.zeros((a_out.shape[0], nin))
+    _check(lib().ref_layer_T(ctypes.byref(net.arr[m - 1]), _ptr(a_out), a_out.shape[0],
+                             _ptr(a_in)), "ref_layer_T")
+    return a_in
+
+
+def layer_fwd(net: RefNet, m: int, g):
+    t = net.layers[m - 1]
+    g = np.ascontiguousarray(np.atleast_2d(g), dtype=np.float64)
+    nout = t["out_c"] * t["out_h"] * t["out_w"]
+    h = np.zeros((g.shape[0], nout))
+    _check(lib().ref_layer_fwd(ctypes.byref(net.arr[m - 1]), _ptr(g), g.shape[0], _ptr(h)),
+           "ref_layer_fwd")
+    return h
+
+
+def relax(l, u, split=0, alpha=None):
+    """(a_lo, a_up, b_up), stability code of one neuron."""
+    out = np.zeros(3)
+    code = lib().ref_relax(float(l), float(u), int(split), int(alpha is not None),
+                           0.0 if alpha is None else float(alpha), _ptr(out))
+    return tuple(out), code
+
+
+ST_SPLIT_ACTIVE, ST_SPLIT_INACTIVE, ST_INACTIVE, ST_ACTIVE, ST_UNSTABLE = 1, 2, 3, 4, 5
+
+
+def root_unstable(net: RefNet, x0, eps, C):
+    """Flat indices of the ReLU neurons that are unstable at the root (no splits, heuristic)."""
+    _, _, _, code = bound(net, x0, eps, C, B=1)
+    return np.flatnonzero(code[0] == ST_UNSTABLE)
