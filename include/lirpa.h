@@ -1,0 +1,132 @@
+/*
+ * lirpa.h -- C ABI of the MI355X (gfx950) batched LiRPA bound library.
+ *
+ * Computes sound lower bounds of linear properties of a ReLU network over an l_inf input box,
+ * for a whole batch of branch-and-bound sub-domains at once: backward-mode linear relaxation
+ * based perturbation analysis (CROWN) as described in Xu et al., "Fast and Complete: Enabling
+ * Complete Neural Network Verification with Rapid and Massively Parallel Incomplete Verifiers"
+ * (ICLR 2021), Sec. 2.3 (Eq. 2-7) and Sec. 3.1 (Eq. 8-9, ReLU split constraints).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All tensor arguments are DEVICE pointers owned by the caller; the library reads them
+ *   during the enqueued work only and never keeps them past the call (except the weights
+ *   borrowed by a lirpa_net, which must outlive it).  The library never allocates or frees
+ *   device memory: every scratch buffer comes from the caller's workspace `ws`.
+ * - Calls validate their arguments on the host, enqueue kernels on `stream` and return without
+ *   synchronising.  Return 0 (LIRPA_OK) on success, a negative lirpa_status otherwise; on error
+ *   nothing is enqueued and lirpa_last_error() returns a thread-local message.
+ * - Flattening is C order: a conv activation is [C][H][W]; a Linear layer after a conv reads the
+ *   flattened [C][H][W] vector.  Per-neuron arrays (split, alpha, l, u, gradients) concatenate
+ *   the ReLU layers 1..L-1 in layer order: n_relu = sum_{m<L} n_m values per sub-domain.
+ * - Floating point is fp32 (round to nearest).  Device contents are not validated: a split
+ *   value outside {-1, 0, 1} or an alpha outside [0, 1] gives undefined (but memory-safe)
+ *   results.
+ */
+#ifndef LIRPA_H_
+#define LIRPA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LIRPA_OK = 0,
+  LIRPA_EINVAL = -1,      /* bad argument: shape, null pointer, eps, S, B            */
+  LIRPA_ENOMEM = -2,      /* the workspace cannot hold even one sub-domain            */
+  LIRPA_EDEVICE = -3,     /* a HIP launch or runtime call failed                      */
+  LIRPA_EUNSUPPORTED = -4 /* a layer shape outside the supported set                  */
+} lirpa_status;
+
+typedef enum { LIRPA_LINEAR = 0, LIRPA_CONV2D = 1 } lirpa_layer_kind;
+
+/* One affine layer T_m: h^(m) = W g^(m-1) + b (Sec. 2.1; the paper drops biases for brevity,
+ * they are kept here).  ReLU follows every layer except the last.
+ * LINEAR : in_c = input features, out_c = output features, in_h = in_w = out_h = out_w = 1;
+ *          W is [out_c][in_c] row-major.
+ * CONV2D : cross-correlation with zero padding, W is [out_c][in_c][k][k], b is per output
+ *          channel, out_h = (in_h + 2 pad - k) / stride + 1 (same for w).
+ * W and b are device pointers borrowed by the net. */
+typedef struct {
+  int kind;
+  int in_c, in_h, in_w;
+  int out_c, out_h, out_w;
+  int k, stride, pad;
+  const float* W;
+  const float* b;
+} lirpa_layer;
+
+typedef struct lirpa_net lirpa_net; /* opaque host object */
+
+/* Build a network from n_layers >= 1 layers (copied; W/b pointers borrowed).  EINVAL if the
+ * chain is inconsistent (n_in of T_m != n_out of T_{m-1}, a conv output size that does not
+ * follow the formula above, null W/b) and EUNSUPPORTED for shapes the kernels do not handle
+ * (kernel size > 7, stride > 4, more than 32 layers). */
+int lirpa_net_create(const lirpa_layer* layers, int n_layers, lirpa_net** out);
+void lirpa_net_destroy(lirpa_net* net);
+
+/* n_relu = sum over ReLU layers of their sizes; -1 for a null net. */
+int64_t lirpa_net_num_relu(const lirpa_net* net);
+
+/* Workspace bytes for one call processing up to B_chunk sub-domains at a time with S spec
+ * rows.  mode 0 = lirpa_bound, 1 = lirpa_bound_grad / lirpa_optimize.  A call given a
+ * smaller workspace processes its batch in chunks of as many sub-domains as fit. */
+size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode);
+
+/* Batched bound (Sec. 2.3 Eq. 2-7, concretised by Eq. 8; split constraints of Sec. 3.1).
+ *   x0      [n0]          centre of the box ||x - x0||_inf <= eps (eps >= 0, finite)
+ *   C       [S][n_L]      spec rows; the property C f(x) >= 0 is merged into the last layer
+ *   split   [B][n_relu]   int8 per neuron: +1 enforces h >= 0 (ReLU = identity), -1 enforces
+ *                         h < 0 (ReLU = 0), 0 leaves it free; NULL = no splits
+ *   alpha   [B][n_relu]   lower slopes of unstable neurons in [0,1] (Eq. 5); NULL = use the
+ *                         upper slope u/(u-l) of each neuron's own bounds
+ *   lb      [B][S]        out: lb[b][s] <= min_{x in box} (C f_b(x))_s, f_b = the network
+ *                         under sub-domain b's splits
+ *   l_out, u_out [B][n_relu] optional out: intermediate pre-activation bounds (layer-1 bounds
+ *                         are exact; split neurons report their bounds before the split)
+ * Intermediate bounds of every layer are recomputed per sub-domain under its own splits. */
+int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
+                void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* As lirpa_bound, plus grad[b][:] = d(sum_s lb[b][s]) / d alpha[b][:] (alpha required).
+ * full != 0 differentiates through the recomputed intermediate bounds (Sec. 3.1: they depend on
+ * the alphas of earlier layers); full == 0 holds them fixed.  Split and stable neurons get
+ * exactly 0. */
+int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                     const int8_t* split, const float* alpha, int full, float* lb, float* grad,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+typedef struct {
+  int steps;      /* number of Adam updates (>= 0)                       */
+  float lr;       /* step size                                           */
+  float beta1;    /* first-moment decay, in [0,1)                        */
+  float beta2;    /* second-moment decay, in [0,1)                       */
+  float eps_adam; /* denominator guard, > 0                              */
+  int t0;         /* updates already taken (bias correction on resume)   */
+} lirpa_opt_params;
+
+/* Optimised bounds (Sec. 3.1, Eq. 9 read as a maximisation over alpha): projected Adam ascent
+ * on J_b = sum_s lb[b][s], alpha clipped to [0,1] after each step, intermediate bounds
+ * recomputed at every iterate.  alpha, adam_m, adam_v [B][n_relu] are in/out (the caller
+ * initialises them; m = v = 0 and t0 = 0 for a fresh start).  lb_best [B][S] is out: the
+ * elementwise maximum of lb over the steps+1 iterates (each a sound bound).  lb_trace
+ * ([steps+1][B][S], optional) receives every iterate's lb. */
+int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                   const int8_t* split, float* alpha, float* adam_m, float* adam_v,
+                   const lirpa_opt_params* params, float* lb_best, float* lb_trace, void* ws,
+                   size_t ws_bytes, hipStream_t stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* lirpa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIRPA_H_ */

@@ -1,0 +1,647 @@
+// Batched backward-mode LiRPA (CROWN) bounds for gfx950 -- host API and kernels.
+//
+// Method: Xu et al., "Fast and Complete" (ICLR 2021), Sec. 2.3 Eq. 3-7 (backward propagation
+// of the bound matrix through affine layers and the ReLU relaxation of Eq. 5), Sec. 3.1 Eq. 8
+// (concretisation by Hoelder's inequality over the l_inf box) and the ReLU split constraints of
+// Sec. 3.1.
+//
+// Data layout.  A "pass" bounds Q = (sub-domains in the chunk) x R rows at once; every bound
+// matrix slab is stored [n][Qp] with the row index q = b*R + r fastest (Qp = Q rounded up to
+// 64), so one lane owns one row for the whole pass: loads and stores of a slab are coalesced
+// across the wave, weights are wave-uniform (scalar loads), and the per-row sums of the
+// relaxation (bias accumulation) and of the concretisation need no cross-lane reduction.
+//
+// Pass structure (one chunk of sub-domains):
+//   pass 1       rows +-e_j of h^(1), once per call: exact layer-1 bounds (shared);
+//   pass k       rows +-e_j of h^(k), 2 <= k <= L-1: init writes relax_{k-1}(+-W_k rows),
+//                then stage m = k-1..1 applies T_m^T with the relaxation of layer m-1 fused in
+//                its epilogue, and the last stage concretises into l^(k), u^(k);
+//   final pass   spec rows C over h^(L): stage L..1 as above, concretising into lb.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "lirpa.h"
+
+namespace {
+
+// ---------------------------------------------------------------------------------------------
+// Errors
+// ---------------------------------------------------------------------------------------------
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define LIRPA_LAUNCH_CHECK(what)                                                          \
+  do {                                                                                    \
+    hipError_t e_ = hipGetLastError();                                                    \
+    if (e_ != hipSuccess) return fail(LIRPA_EDEVICE, "%s: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kMaxLayers = 32;
+constexpr int kBlock = 256;
+
+long n_in_of(const lirpa_layer& t) { return (long)t.in_c * t.in_h * t.in_w; }
+long n_out_of(const lirpa_layer& t) { return (long)t.out_c * t.out_h * t.out_w; }
+long round_up(long x, long m) { return (x + m - 1) / m * m; }
+
+}  // namespace
+
+struct lirpa_net {
+  std::vector<lirpa_layer> T;  // T[0..L-1] = T_1..T_L
+  int L = 0;
+  long n[kMaxLayers + 1] = {};    // n[0] input size, n[m] size of h^(m)
+  long off[kMaxLayers + 1] = {};  // offset of ReLU layer m in per-neuron arrays
+  long n_relu = 0;
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------------------------
+// Device-side descriptors
+// ---------------------------------------------------------------------------------------------
+struct DLayer {
+  int kind, in_c, in_h, in_w, out_c, out_h, out_w, k, stride, pad;
+  const float* W;
+  const float* b;
+};
+
+DLayer dlayer(const lirpa_layer& t) {
+  return DLayer{t.kind, t.in_c, t.in_h, t.in_w, t.out_c, t.out_h, t.out_w,
+                t.k,    t.stride, t.pad, t.W,  t.b};
+}
+
+enum { MODE_SLAB = 0, MODE_BOUND = 1 };
+
+// Where a stage's output row goes.
+//  MODE_SLAB : coefficients over g^(m) are relaxed with layer m's (a_lo, a_up, b_up) of the
+//              row's sub-domain (Eq. 6: non-negative entries take the lower line, negative ones
+//              the upper line and its intercept), the bias of layer m is dotted in, and the
+//              relaxed row is stored in out[i*ldq + q].
+//  MODE_BOUND: coefficients over the input x are concretised (Eq. 8):
+//              value = A x0 - eps ||A||_1 + beta; row r < n_half goes to lo[b*bstride + r],
+//              a row r >= n_half to hi[b*bstride + r - n_half] negated (an upper bound).
+struct Sink {
+  float* out;
+  long ldq;
+  const float* a_lo;
+  const float* a_up;
+  const float* b_up;
+  long pstride;  // per-sub-domain stride of the relaxation parameters
+  const float* bias;
+  int bias_hw;
+  const float* x0;
+  float eps;
+  float* beta;  // running bias of each row, [Qp]
+  long R;       // rows per sub-domain
+  float* lo;
+  float* hi;
+  long bstride;
+  long n_half;
+};
+
+struct Acc {
+  float beta, lin, l1;
+};
+
+template <int MODE>
+__device__ __forceinline__ void sink_put(const Sink& s, Acc& acc, long i, float a, long q,
+                                         long b) {
+  if constexpr (MODE == MODE_SLAB) {
+    long pi = b * s.pstride + i;
+    float ah;
+    if (a >= 0.f) {
+      ah = a * s.a_lo[pi];
+    } else {
+      acc.beta = fmaf(a, s.b_up[pi], acc.beta);
+      ah = a * s.a_up[pi];
+    }
+    acc.beta = fmaf(ah, s.bias[i / s.bias_hw], acc.beta);
+    s.out[i * s.ldq + q] = ah;
+  } else {
+    acc.lin = fmaf(a, s.x0[i], acc.lin);
+    acc.l1 += fabsf(a);
+  }
+}
+
+// use_beta: add the row's running bias kept in s.beta (stages after an init).
+template <int MODE>
+__device__ __forceinline__ void sink_finish(const Sink& s, const Acc& acc, long q, long b, long r,
+                                            bool first) {
+  if constexpr (MODE == MODE_SLAB) {
+    s.beta[q] = first ? acc.beta : s.beta[q] + acc.beta;
+  } else {
+    float beta = first ? acc.beta : s.beta[q] + acc.beta;
+    float v = acc.lin - s.eps * acc.l1 + beta;
+    if (r < s.n_half)
+      s.lo[b * s.bstride + r] = v;
+    else
+      s.hi[b * s.bstride + (r - s.n_half)] = -v;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------------------------
+
+// Rows +-e_j over h^(k) (j = r mod n_k, sign + for r < n_k): carried through T_k (Eq. 4) they
+// become +-(row j of W_k) over g^(k-1), with bias +-b_k[j].
+template <int MODE>
+__global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, long Q, Sink s) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  long b = q / s.R, r = q % s.R;
+  long nk = (long)t.out_c * t.out_h * t.out_w;
+  long j = r % nk;
+  float sgn = r < nk ? 1.f : -1.f;
+  int hw = t.out_h * t.out_w;
+  Acc acc{sgn * t.b[j / hw], 0.f, 0.f};
+  if (t.kind == LIRPA_LINEAR) {
+    for (int i = 0; i < t.in_c; ++i) sink_put<MODE>(s, acc, i, sgn * t.W[j * t.in_c + i], q, b);
+  } else {
+    int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
+    int y0 = yo * t.stride - t.pad, x0 = xo * t.stride - t.pad;
+    for (int ci = 0; ci < t.in_c; ++ci)
+      for (int yi = 0; yi < t.in_h; ++yi)
+        for (int xi = 0; xi < t.in_w; ++xi) {
+          int ky = yi - y0, kx = xi - x0;
+          float a = 0.f;
+          if (ky >= 0 && ky < t.k && kx >= 0 && kx < t.k)
+            a = sgn * t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx];
+          sink_put<MODE>(s, acc, ((long)ci * t.in_h + yi) * t.in_w + xi, a, q, b);
+        }
+  }
+  sink_finish<MODE>(s, acc, q, b, r, true);
+}
+
+// Spec rows C_s over h^(L) (the property merged into the last layer): written to the slab as
+// they are, with the bias C_s . b_L.
+__global__ void __launch_bounds__(kBlock) k_spec_rows(const float* __restrict__ C, long nL,
+                                                      const float* __restrict__ bL, int hwL,
+                                                      long Q, long S, float* __restrict__ out,
+                                                      long ldq, float* __restrict__ beta) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  long s = q % S;
+  float acc = 0.f;
+  for (long o = 0; o < nL; ++o) {
+    float c = C[s * nL + o];
+    out[o * ldq + q] = c;
+    acc = fmaf(c, bL[o / hwL], acc);
+  }
+  beta[q] = acc;
+}
+
+// One backward step through a fully connected layer: a_in[i] = sum_o a_out[o] W[o][i].
+template <int MODE>
+__global__ void __launch_bounds__(kBlock) k_fcT(DLayer t, const float* __restrict__ in, long ldq,
+                                                long Q, Sink s) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  long b = q / s.R, r = q % s.R;
+  Acc acc{0.f, 0.f, 0.f};
+  for (int i = 0; i < t.in_c; ++i) {
+    float a = 0.f;
+    for (int o = 0; o < t.out_c; ++o) a = fmaf(t.W[(long)o * t.in_c + i], in[o * ldq + q], a);
+    sink_put<MODE>(s, acc, i, a, q, b);
+  }
+  sink_finish<MODE>(s, acc, q, b, r, false);
+}
+
+// One backward step through a convolution: the transposed convolution with the layer's own
+// weights, stride and padding, gathered per input position.
+template <int MODE>
+__global__ void __launch_bounds__(kBlock) k_convT(DLayer t, const float* __restrict__ in,
+                                                  long ldq, long Q, Sink s) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  long b = q / s.R, r = q % s.R;
+  Acc acc{0.f, 0.f, 0.f};
+  const int K = t.k, St = t.stride, P = t.pad;
+  const long ohw = (long)t.out_h * t.out_w;
+  const long wco = (long)t.in_c * K * K;
+  for (int ci = 0; ci < t.in_c; ++ci)
+    for (int yi = 0; yi < t.in_h; ++yi)
+      for (int xi = 0; xi < t.in_w; ++xi) {
+        float a = 0.f;
+        for (int ky = 0; ky < K; ++ky) {
+          int yn = yi + P - ky;
+          if (yn < 0 || yn % St) continue;
+          int yo = yn / St;
+          if (yo >= t.out_h) continue;
+          for (int kx = 0; kx < K; ++kx) {
+            int xn = xi + P - kx;
+            if (xn < 0 || xn % St) continue;
+            int xo = xn / St;
+            if (xo >= t.out_w) continue;
+            const float* wp = t.W + ((long)ci * K + ky) * K + kx;
+            const float* ip = in + ((long)yo * t.out_w + xo) * ldq + q;
+            for (int co = 0; co < t.out_c; ++co) a = fmaf(wp[co * wco], ip[co * ohw * ldq], a);
+          }
+        }
+        sink_put<MODE>(s, acc, ((long)ci * t.in_h + yi) * t.in_w + xi, a, q, b);
+      }
+  sink_finish<MODE>(s, acc, q, b, r, false);
+}
+
+// Relaxation parameters of ReLU layer m for every sub-domain of the chunk (Eq. 5 with the split
+// override of Sec. 3.1, checked in the order: split, u <= 0, l >= 0, unstable).
+__global__ void __launch_bounds__(kBlock)
+    k_relax_params(long nb, long nm, long stride, long off, const float* __restrict__ l,
+                   const float* __restrict__ u, const int8_t* __restrict__ split,
+                   const float* __restrict__ alpha, float* __restrict__ a_lo,
+                   float* __restrict__ a_up, float* __restrict__ b_up,
+                   int8_t* __restrict__ code) {
+  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= nb * nm) return;
+  long b = idx / nm, j = idx % nm;
+  long p = b * stride + off + j;
+  int sp = split ? split[p] : 0;
+  float lo = 0.f, up = 0.f, bu = 0.f;
+  int c;
+  if (sp > 0) {
+    lo = 1.f; up = 1.f; c = 1;
+  } else if (sp < 0) {
+    c = 2;
+  } else {
+    float lj = l[p], uj = u[p];
+    if (uj <= 0.f) {
+      c = 3;
+    } else if (lj >= 0.f) {
+      lo = 1.f; up = 1.f; c = 4;
+    } else {
+      float d = uj - lj;
+      up = uj / d;
+      bu = -(uj * lj) / d;
+      lo = alpha ? alpha[p] : up;
+      c = 5;
+    }
+  }
+  a_lo[p] = lo;
+  a_up[p] = up;
+  b_up[p] = bu;
+  code[p] = (int8_t)c;
+}
+
+// Copies the shared layer-1 bounds into every sub-domain's row of l, u.
+__global__ void __launch_bounds__(kBlock) k_bcast_l1(long nb, long n1, long stride,
+                                                     const float* __restrict__ l1,
+                                                     const float* __restrict__ u1,
+                                                     float* __restrict__ l, float* __restrict__ u) {
+  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= nb * n1) return;
+  long b = idx / n1, j = idx % n1;
+  l[b * stride + j] = l1[j];
+  u[b * stride + j] = u1[j];
+}
+
+// ---------------------------------------------------------------------------------------------
+// Workspace plan
+// ---------------------------------------------------------------------------------------------
+struct Plan {
+  long Bc = 0;
+  size_t off_l = 0, off_u = 0, off_alo = 0, off_aup = 0, off_bup = 0, off_code = 0;
+  size_t off_l1u1 = 0, off_slab0 = 0, off_slab1 = 0, off_beta = 0, total = 0;
+  long slab_floats = 0, qp_max = 0;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+Plan make_plan(const lirpa_net* net, long S, long Bc) {
+  Plan p;
+  p.Bc = Bc;
+  const int L = net->L;
+  long slab = 0, qpmax = round_up(2 * net->n[1], 64);
+  for (int k = 2; k <= L; ++k) {
+    long R = (k < L) ? 2 * net->n[k] : S;
+    long qp = round_up(Bc * R, 64);
+    qpmax = std::max(qpmax, qp);
+    int mtop = (k < L) ? k - 1 : L;  // slabs hold A over h^(m), m = mtop..1
+    for (int m = 1; m <= mtop; ++m) slab = std::max(slab, net->n[m] * qp);
+  }
+  if (L == 1) {
+    long qp = round_up(Bc * S, 64);
+    qpmax = std::max(qpmax, qp);
+    slab = std::max(slab, net->n[1] * qp);
+  }
+  p.slab_floats = slab;
+  p.qp_max = qpmax;
+  size_t o = 0;
+  size_t per = (size_t)Bc * (net->n_relu ? net->n_relu : 1);
+  p.off_l = o;    o = align256(o + per * 4);
+  p.off_u = o;    o = align256(o + per * 4);
+  p.off_alo = o;  o = align256(o + per * 4);
+  p.off_aup = o;  o = align256(o + per * 4);
+  p.off_bup = o;  o = align256(o + per * 4);
+  p.off_code = o; o = align256(o + per);
+  p.off_l1u1 = o; o = align256(o + 2 * (size_t)net->n[1] * 4);
+  p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
+  p.off_slab0 = o; o = align256(o + (size_t)slab * 4);
+  p.off_slab1 = o; o = align256(o + (size_t)slab * 4);
+  p.total = o;
+  return p;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+dim3 grid_for(long n) { return dim3((unsigned)((n + kBlock - 1) / kBlock)); }
+
+// One backward stage through layer m (1-based) applied to Q rows held in `in` ([n_m][ldq]).
+template <int MODE>
+int launch_stage(const lirpa_net* net, int m, const float* in, long ldq, long Q, const Sink& s,
+                 hipStream_t st) {
+  DLayer t = dlayer(net->T[m - 1]);
+  if (t.kind == LIRPA_LINEAR)
+    hipLaunchKernelGGL(k_fcT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
+  else
+    hipLaunchKernelGGL(k_convT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
+  LIRPA_LAUNCH_CHECK("backward stage");
+  return LIRPA_OK;
+}
+
+struct Chunk {
+  const lirpa_net* net;
+  const Plan* p;
+  void* ws;
+  const float* x0;
+  float eps;
+  long S;
+  long nb;             // sub-domains in this chunk
+  float* L;            // l rows of the chunk, stride n_relu
+  float* U;
+  const int8_t* split; // chunk's first row or null
+  const float* alpha;
+  hipStream_t st;
+};
+
+// Sink that relaxes onto ReLU layer m and stores into `out`.
+Sink slab_sink(const Chunk& c, int m, float* out, long ldq, long R) {
+  const lirpa_net* net = c.net;
+  const lirpa_layer& t = net->T[m - 1];
+  Sink s{};
+  s.out = out;
+  s.ldq = ldq;
+  s.a_lo = at<float>(c.ws, c.p->off_alo) + net->off[m];
+  s.a_up = at<float>(c.ws, c.p->off_aup) + net->off[m];
+  s.b_up = at<float>(c.ws, c.p->off_bup) + net->off[m];
+  s.pstride = net->n_relu;
+  s.bias = t.b;
+  s.bias_hw = t.out_h * t.out_w;
+  s.beta = at<float>(c.ws, c.p->off_beta);
+  s.R = R;
+  return s;
+}
+
+Sink bound_sink(const Chunk& c, long R, float* lo, float* hi, long bstride, long n_half) {
+  Sink s{};
+  s.x0 = c.x0;
+  s.eps = c.eps;
+  s.beta = at<float>(c.ws, c.p->off_beta);
+  s.R = R;
+  s.lo = lo;
+  s.hi = hi;
+  s.bstride = bstride;
+  s.n_half = n_half;
+  return s;
+}
+
+int relax_layer(const Chunk& c, int m) {
+  const lirpa_net* net = c.net;
+  long nm = net->n[m];
+  long off = net->off[m];
+  hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
+                     net->n_relu, off, c.L, c.U, c.split, c.alpha, at<float>(c.ws, c.p->off_alo),
+                     at<float>(c.ws, c.p->off_aup), at<float>(c.ws, c.p->off_bup),
+                     at<int8_t>(c.ws, c.p->off_code));
+  LIRPA_LAUNCH_CHECK("relaxation parameters");
+  return LIRPA_OK;
+}
+
+// Stages m = mtop .. 1 on rows already in slab 0 (relaxed onto layer mtop when mtop < L, raw
+// spec rows when mtop == L), ending with the concretisation into (lo, hi).
+int run_stages(const Chunk& c, int mtop, long R, long Q, long ldq, float* lo, float* hi,
+               long bstride, long n_half) {
+  float* slab[2] = {at<float>(c.ws, c.p->off_slab0), at<float>(c.ws, c.p->off_slab1)};
+  int cur = 0;
+  for (int m = mtop; m >= 1; --m) {
+    int e;
+    if (m > 1) {
+      Sink s = slab_sink(c, m - 1, slab[1 - cur], ldq, R);
+      e = launch_stage<MODE_SLAB>(c.net, m, slab[cur], ldq, Q, s, c.st);
+      cur ^= 1;
+    } else {
+      Sink s = bound_sink(c, R, lo, hi, bstride, n_half);
+      e = launch_stage<MODE_BOUND>(c.net, m, slab[cur], ldq, Q, s, c.st);
+    }
+    if (e) return e;
+  }
+  return LIRPA_OK;
+}
+
+int bound_chunk(const Chunk& c, const float* C, float* lb) {
+  const lirpa_net* net = c.net;
+  const int L = net->L;
+  long n1 = net->n[1];
+  if (L >= 2) {
+    const float* l1u1 = at<float>(c.ws, c.p->off_l1u1);
+    hipLaunchKernelGGL(k_bcast_l1, grid_for(c.nb * n1), dim3(kBlock), 0, c.st, c.nb, n1,
+                       net->n_relu, l1u1, l1u1 + n1, c.L, c.U);
+    LIRPA_LAUNCH_CHECK("layer-1 bounds broadcast");
+    if (int e = relax_layer(c, 1)) return e;
+  }
+  for (int k = 2; k <= L - 1; ++k) {
+    long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
+    Sink s = slab_sink(c, k - 1, at<float>(c.ws, c.p->off_slab0), ldq, R);
+    hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
+                       dlayer(net->T[k - 1]), Q, s);
+    LIRPA_LAUNCH_CHECK("pass initialisation");
+    if (int e = run_stages(c, k - 1, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
+                           net->n_relu, nk))
+      return e;
+    if (int e = relax_layer(c, k)) return e;
+  }
+  // final pass
+  long R = c.S, Q = c.nb * R, ldq = round_up(Q, 64);
+  const lirpa_layer& tL = net->T[L - 1];
+  hipLaunchKernelGGL(k_spec_rows, grid_for(Q), dim3(kBlock), 0, c.st, C, net->n[L], tL.b,
+                     tL.out_h * tL.out_w, Q, c.S, at<float>(c.ws, c.p->off_slab0), ldq,
+                     at<float>(c.ws, c.p->off_beta));
+  LIRPA_LAUNCH_CHECK("spec rows");
+  return run_stages(c, L, R, Q, ldq, lb, lb, c.S, c.S);
+}
+
+// Exact layer-1 bounds, shared by every sub-domain: rows +-e_j of h^(1) through T_1, then
+// concretised (no relaxation in front of layer 1).
+int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0, float eps,
+                  hipStream_t st) {
+  long n1 = net->n[1], R = 2 * n1, Q = R;
+  float* l1u1 = at<float>(ws, p.off_l1u1);
+  Sink s{};
+  s.x0 = x0;
+  s.eps = eps;
+  s.R = R;
+  s.lo = l1u1;
+  s.hi = l1u1 + n1;
+  s.bstride = 0;
+  s.n_half = n1;
+  hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
+                     dlayer(net->T[0]), Q, s);
+  LIRPA_LAUNCH_CHECK("layer-1 bounds");
+  return LIRPA_OK;
+}
+
+int check_common(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                 void* ws) {
+  if (!net) return fail(LIRPA_EINVAL, "net is null");
+  if (!x0) return fail(LIRPA_EINVAL, "x0 is null");
+  if (!C) return fail(LIRPA_EINVAL, "C is null");
+  if (S < 1) return fail(LIRPA_EINVAL, "S must be >= 1 (got %d)", S);
+  if (B < 1) return fail(LIRPA_EINVAL, "B must be >= 1 (got %d)", B);
+  if (!std::isfinite(eps) || eps < 0.f) return fail(LIRPA_EINVAL, "eps must be finite and >= 0");
+  if (!ws) return fail(LIRPA_EINVAL, "workspace is null");
+  return LIRPA_OK;
+}
+
+// Largest chunk whose workspace fits.
+long fit_chunk(const lirpa_net* net, long S, long B, size_t ws_bytes, Plan* out) {
+  long lo = 0, hi = B;
+  while (lo < hi) {
+    long mid = (lo + hi + 1) / 2;
+    if (make_plan(net, S, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+  }
+  if (lo > 0) *out = make_plan(net, S, lo);
+  return lo;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------------------------
+extern "C" {
+
+int lirpa_net_create(const lirpa_layer* layers, int n_layers, lirpa_net** out) {
+  if (!out) return fail(LIRPA_EINVAL, "out is null");
+  *out = nullptr;
+  if (!layers || n_layers < 1) return fail(LIRPA_EINVAL, "need at least one layer");
+  if (n_layers > kMaxLayers) return fail(LIRPA_EUNSUPPORTED, "at most %d layers", kMaxLayers);
+  lirpa_net* net = new lirpa_net;
+  net->L = n_layers;
+  net->T.assign(layers, layers + n_layers);
+  net->n[0] = n_in_of(layers[0]);
+  for (int m = 1; m <= n_layers; ++m) {
+    const lirpa_layer& t = layers[m - 1];
+    int e = LIRPA_OK;
+    if (!t.W || !t.b) e = fail(LIRPA_EINVAL, "layer %d: null W or b", m);
+    else if (t.in_c < 1 || t.in_h < 1 || t.in_w < 1 || t.out_c < 1 || t.out_h < 1 || t.out_w < 1)
+      e = fail(LIRPA_EINVAL, "layer %d: non-positive dimension", m);
+    else if (t.kind == LIRPA_LINEAR) {
+      if (t.in_h != 1 || t.in_w != 1 || t.out_h != 1 || t.out_w != 1)
+        e = fail(LIRPA_EINVAL, "layer %d: a linear layer has unit spatial dims", m);
+    } else if (t.kind == LIRPA_CONV2D) {
+      if (t.k < 1 || t.stride < 1 || t.pad < 0)
+        e = fail(LIRPA_EINVAL, "layer %d: bad conv geometry", m);
+      else if (t.out_h != (t.in_h + 2 * t.pad - t.k) / t.stride + 1 ||
+               t.out_w != (t.in_w + 2 * t.pad - t.k) / t.stride + 1)
+        e = fail(LIRPA_EINVAL, "layer %d: conv output size does not match", m);
+      else if (t.k > 7 || t.stride > 4 || t.pad >= t.k)
+        e = fail(LIRPA_EUNSUPPORTED, "layer %d: conv with k<=7, stride<=4, pad<k supported", m);
+    } else {
+      e = fail(LIRPA_EINVAL, "layer %d: unknown kind %d", m, t.kind);
+    }
+    if (!e && m > 1 && n_in_of(t) != net->n[m - 1])
+      e = fail(LIRPA_EINVAL, "layer %d: input size %ld != previous output size %ld", m,
+               n_in_of(t), net->n[m - 1]);
+    if (e) {
+      delete net;
+      return e;
+    }
+    net->n[m] = n_out_of(t);
+    if (m < n_layers) {
+      net->off[m] = net->n_relu;
+      net->n_relu += net->n[m];
+    }
+  }
+  *out = net;
+  return LIRPA_OK;
+}
+
+void lirpa_net_destroy(lirpa_net* net) { delete net; }
+
+int64_t lirpa_net_num_relu(const lirpa_net* net) { return net ? net->n_relu : -1; }
+
+size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode) {
+  if (!net || S < 1 || B_chunk < 1 || (mode != 0 && mode != 1)) return 0;
+  return make_plan(net, S, B_chunk).total;
+}
+
+int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
+                void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!lb) return fail(LIRPA_EINVAL, "lb is null");
+  if ((l_out == nullptr) != (u_out == nullptr))
+    return fail(LIRPA_EINVAL, "l_out and u_out must both be given or both be null");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                make_plan(net, S, 1).total);
+  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c;
+    c.net = net;
+    c.p = &p;
+    c.ws = ws;
+    c.x0 = x0;
+    c.eps = eps;
+    c.S = S;
+    c.nb = std::min(Bc, (long)B - b0);
+    c.L = l_out ? l_out + b0 * net->n_relu : at<float>(ws, p.off_l);
+    c.U = u_out ? u_out + b0 * net->n_relu : at<float>(ws, p.off_u);
+    c.split = split ? split + b0 * net->n_relu : nullptr;
+    c.alpha = alpha ? alpha + b0 * net->n_relu : nullptr;
+    c.st = stream;
+    if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
+  }
+  return LIRPA_OK;
+}
+
+int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                     const int8_t* split, const float* alpha, int full, float* lb, float* grad,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)net; (void)x0; (void)eps; (void)C; (void)S; (void)B; (void)split; (void)alpha;
+  (void)full; (void)lb; (void)grad; (void)ws; (void)ws_bytes; (void)stream;
+  return fail(LIRPA_EUNSUPPORTED, "lirpa_bound_grad is not implemented yet");
+}
+
+int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                   const int8_t* split, float* alpha, float* adam_m, float* adam_v,
+                   const lirpa_opt_params* params, float* lb_best, float* lb_trace, void* ws,
+                   size_t ws_bytes, hipStream_t stream) {
+  (void)net; (void)x0; (void)eps; (void)C; (void)S; (void)B; (void)split; (void)alpha;
+  (void)adam_m; (void)adam_v; (void)params; (void)lb_best; (void)lb_trace; (void)ws;
+  (void)ws_bytes; (void)stream;
+  return fail(LIRPA_EUNSUPPORTED, "lirpa_optimize is not implemented yet");
+}
+
+const char* lirpa_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

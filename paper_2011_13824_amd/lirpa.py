@@ -1,0 +1,212 @@
+"""Thin ctypes binding of ``liblirpa.so`` (the C ABI declared in include/lirpa.h).
+
+The functions below carry the C names and only marshal arguments: torch CUDA tensors become
+device pointers and the current torch stream becomes the ``hipStream_t``.  Every step of the
+bound computation runs in the HIP library; there is no fallback.  ``Network`` is a small
+convenience owner of device weights, a net handle and a workspace.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblirpa.so")
+
+LIRPA_OK, LIRPA_EINVAL, LIRPA_ENOMEM, LIRPA_EDEVICE, LIRPA_EUNSUPPORTED = 0, -1, -2, -3, -4
+LINEAR, CONV2D = 0, 1
+
+
+class lirpa_layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("in_c", ctypes.c_int), ("in_h", ctypes.c_int),
+                ("in_w", ctypes.c_int), ("out_c", ctypes.c_int), ("out_h", ctypes.c_int),
+                ("out_w", ctypes.c_int), ("k", ctypes.c_int), ("stride", ctypes.c_int),
+                ("pad", ctypes.c_int), ("W", ctypes.c_void_p), ("b", ctypes.c_void_p)]
+
+
+class lirpa_opt_params(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps_adam", ctypes.c_float), ("t0", ctypes.c_int)]
+
+
+SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
+           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_grad", "lirpa_optimize",
+           "lirpa_last_error")
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built (no CPU fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    L.lirpa_net_create.argtypes = [ctypes.POINTER(lirpa_layer), i, ctypes.POINTER(P)]
+    L.lirpa_net_create.restype = i
+    L.lirpa_net_destroy.argtypes = [P]
+    L.lirpa_net_destroy.restype = None
+    L.lirpa_net_num_relu.argtypes = [P]
+    L.lirpa_net_num_relu.restype = ctypes.c_int64
+    L.lirpa_workspace_bytes.argtypes = [P, i, i, i]
+    L.lirpa_workspace_bytes.restype = sz
+    L.lirpa_bound.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, sz, P]
+    L.lirpa_bound.restype = i
+    L.lirpa_bound_grad.argtypes = [P, P, f, P, i, i, P, P, i, P, P, P, sz, P]
+    L.lirpa_bound_grad.restype = i
+    L.lirpa_optimize.argtypes = [P, P, f, P, i, i, P, P, P, P, ctypes.POINTER(lirpa_opt_params),
+                                 P, P, P, sz, P]
+    L.lirpa_optimize.restype = i
+    L.lirpa_last_error.argtypes = []
+    L.lirpa_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+class LirpaError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"lirpa error {code}: {msg}")
+        self.code = code
+
+
+def _check(rc):
+    if rc != LIRPA_OK:
+        raise LirpaError(rc, load().lirpa_last_error().decode())
+
+
+def _dev(t, dtype=None, what="tensor"):
+    """Device pointer of a contiguous CUDA tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{what} must be a CUDA tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def lirpa_last_error() -> str:
+    return load().lirpa_last_error().decode()
+
+
+def lirpa_net_create(layers):
+    """layers: list of dicts with the layer fields and device tensors ``W``, ``b``."""
+    arr = (lirpa_layer * len(layers))()
+    for i, t in enumerate(layers):
+        arr[i] = lirpa_layer(t["kind"], t["in_c"], t["in_h"], t["in_w"], t["out_c"], t["out_h"],
+                             t["out_w"], t.get("k", 0), t.get("stride", 1), t.get("pad", 0),
+                             _dev(t["W"], torch.float32, "W"), _dev(t["b"], torch.float32, "b"))
+    h = ctypes.c_void_p()
+    _check(load().lirpa_net_create(arr, len(layers), ctypes.byref(h)))
+    return h
+
+
+def lirpa_net_destroy(net):
+    load().lirpa_net_destroy(net)
+
+
+def lirpa_net_num_relu(net) -> int:
+    return int(load().lirpa_net_num_relu(net))
+
+
+def lirpa_workspace_bytes(net, S, B_chunk, mode=0) -> int:
+    return int(load().lirpa_workspace_bytes(net, S, B_chunk, mode))
+
+
+def lirpa_bound(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, ws, ws_bytes,
+                stream=None):
+    _check(load().lirpa_bound(net, _dev(x0, torch.float32, "x0"), float(eps),
+                              _dev(C, torch.float32, "C"), int(S), int(B),
+                              _dev(split, torch.int8, "split"),
+                              _dev(alpha, torch.float32, "alpha"),
+                              _dev(lb, torch.float32, "lb"), _dev(l_out, torch.float32, "l_out"),
+                              _dev(u_out, torch.float32, "u_out"), _dev(ws, None, "ws"),
+                              int(ws_bytes), _stream(stream)))
+
+
+def lirpa_bound_grad(net, x0, eps, C, S, B, split, alpha, full, lb, grad, ws, ws_bytes,
+                     stream=None):
+    _check(load().lirpa_bound_grad(net, _dev(x0, torch.float32, "x0"), float(eps),
+                                   _dev(C, torch.float32, "C"), int(S), int(B),
+                                   _dev(split, torch.int8, "split"),
+                                   _dev(alpha, torch.float32, "alpha"), int(full),
+                                   _dev(lb, torch.float32, "lb"),
+                                   _dev(grad, torch.float32, "grad"), _dev(ws, None, "ws"),
+                                   int(ws_bytes), _stream(stream)))
+
+
+def lirpa_optimize(net, x0, eps, C, S, B, split, alpha, adam_m, adam_v, params, lb_best,
+                   lb_trace, ws, ws_bytes, stream=None):
+    p = params if isinstance(params, lirpa_opt_params) else lirpa_opt_params(**params)
+    _check(load().lirpa_optimize(net, _dev(x0, torch.float32, "x0"), float(eps),
+                                 _dev(C, torch.float32, "C"), int(S), int(B),
+                                 _dev(split, torch.int8, "split"),
+                                 _dev(alpha, torch.float32, "alpha"),
+                                 _dev(adam_m, torch.float32, "adam_m"),
+                                 _dev(adam_v, torch.float32, "adam_v"), ctypes.byref(p),
+                                 _dev(lb_best, torch.float32, "lb_best"),
+                                 _dev(lb_trace, torch.float32, "lb_trace"), _dev(ws, None, "ws"),
+                                 int(ws_bytes), _stream(stream)))
+
+
+class Network:
+    """Device copy of a network (layer dicts with numpy W, b), its handle and a workspace."""
+
+    def __init__(self, layers, device="cuda"):
+        self.layers = []
+        for t in layers:
+            d = dict(t)
+            d["W"] = torch.as_tensor(np.ascontiguousarray(t["W"], dtype=np.float32)).to(device)
+            d["b"] = torch.as_tensor(np.ascontiguousarray(t["b"], dtype=np.float32)).to(device)
+            self.layers.append(d)
+        self.device = device
+        self.handle = lirpa_net_create(self.layers)
+        self.n_relu = lirpa_net_num_relu(self.handle)
+        self._ws = None
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib is not None:
+            lirpa_net_destroy(h)
+            self.handle = None
+
+    def workspace(self, S, B, mode=0, max_bytes=None):
+        """A workspace for up to B sub-domains per chunk (capped at max_bytes), reused."""
+        need = lirpa_workspace_bytes(self.handle, S, B, mode)
+        if max_bytes is not None and need > max_bytes:
+            need = max_bytes
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self._ws, need
+
+    def bound(self, x0, eps, C, split=None, alpha=None, B=None, want_lu=False, ws=None,
+              ws_bytes=None, max_ws_bytes=16 << 30):
+        S = C.shape[0]
+        if B is None:
+            B = split.shape[0] if split is not None else (alpha.shape[0] if alpha is not None
+                                                            else 1)
+        lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        l = u = None
+        if want_lu:
+            l = torch.empty((B, self.n_relu), dtype=torch.float32, device=self.device)
+            u = torch.empty_like(l)
+        if ws is None:
+            ws, ws_bytes = self.workspace(S, B, 0, max_ws_bytes)
+        lirpa_bound(self.handle, x0, eps, C, S, B, split, alpha, lb, l, u, ws, ws_bytes)
+        return (lb, l, u) if want_lu else lb

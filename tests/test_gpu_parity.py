@@ -1,0 +1,166 @@
+"""GPU parity: the HIP library against the fp64 oracle on the same seeded inputs.
+
+Tolerance (fp32 GPU vs fp64 oracle): |gpu - ref| <= 1e-4 + 1e-4 |ref| for every bound, and for
+the intermediate bounds l, u.  Full-size batches run on the GPU exactly as the benchmark runs
+them; the oracle recomputes a sample of their sub-domains one by one."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ref
+from paper_2011_13824_amd import lirpa
+from paper_2011_13824_amd import workloads as wl
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+ATOL = RTOL = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lirpa.load()
+
+
+def dev(a):
+    return None if a is None else torch.as_tensor(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_bound(layers, x0, eps, C, split=None, alpha=None, B=None, max_ws_bytes=16 << 30,
+              net=None):
+    net = net or lirpa.Network(layers)
+    lb, l, u = net.bound(dev(x0), eps, dev(C), dev(split), dev(alpha), B=B, want_lu=True,
+                         max_ws_bytes=max_ws_bytes)
+    torch.cuda.synchronize()
+    return (lb.cpu().double().numpy(), l.cpu().double().numpy(), u.cpu().double().numpy())
+
+
+def check(name, got, want):
+    excess = np.abs(got - want) - (ATOL + RTOL * np.abs(want))
+    worst = float(np.abs(got - want).max()) if got.size else 0.0
+    print(f"{name}: max |gpu - oracle| = {worst:.3g}", flush=True)
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    assert np.all(excess <= 0), f"{name}: exceeds tolerance by {excess.max():.3g}"
+
+
+def test_tiny_every_subdomain():
+    w = wl.tiny()
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C))
+    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split)
+    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, split)
+    check("tiny lb", lb, lr)
+    check("tiny l", l, llr)
+    check("tiny u", u, ulr)
+
+
+# batch sizes run here; None = the workload's full batch
+BATCH = {"base": None, "wide": 128, "deep": 128}
+
+
+@pytest.mark.parametrize("name", ["base", "wide", "deep"])
+def test_full_size_batches_sampled(name):
+    w = wl.get(name)
+    B = BATCH[name] or w.B
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=B)
+    print(f"{name}: B={B} S={w.S} n_relu={w.n_relu}", flush=True)
+    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split)
+    rng = np.random.default_rng(7)
+    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 14, replace=False)]))
+    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, split[idx])
+    check(f"{name} lb", lb[idx], lr)
+    check(f"{name} l", l[idx], llr)
+    check(f"{name} u", u[idx], ulr)
+
+
+def test_small_conv_ragged_batch_with_alpha():
+    layers = wl.random_net(H.small_conv_arch(), 21)
+    rng = np.random.default_rng(21)
+    x0 = rng.uniform(0, 1, wl.n_in(layers[0])).astype(np.float32)
+    C = wl.margin_spec(3, 2)
+    rnet = ref.RefNet(layers)
+    B = 37
+    split = wl.make_splits(B, rnet.n_relu, 5, 21, ref.root_unstable(rnet, x0, 0.05, C))
+    alpha = rng.uniform(0, 1, (B, rnet.n_relu)).astype(np.float32)
+    for a in (None, alpha):
+        lb, l, u = gpu_bound(layers, x0, 0.05, C, split, a)
+        lr, llr, ulr, _ = ref.bound(rnet, x0, 0.05, C, split, a)
+        check("small lb", lb, lr)
+        check("small l", l, llr)
+        check("small u", u, ulr)
+
+
+def test_alpha_on_base():
+    w = wl.base()
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=6)
+    alpha = np.random.default_rng(3).uniform(0, 1, (6, rnet.n_relu)).astype(np.float32)
+    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split, alpha)
+    lr, llr, ulr, code = ref.bound(rnet, w.x0, w.eps, w.C, split, alpha)
+    check("base+alpha lb", lb, lr)
+    check("base+alpha l", l, llr)
+    check("base+alpha u", u, ulr)
+
+
+@pytest.mark.parametrize("name", ["tiny", "base"])
+def test_all_split_matches_closed_form(name):
+    w = wl.get(name)
+    rng = np.random.default_rng(5)
+    split = rng.choice(np.array([-1, 1], dtype=np.int8), size=(3, w.n_relu))
+    lb, _, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split)
+    for b in range(3):
+        M, c = H.affine_map_of_split_net(w.layers, split[b])
+        check(f"{name} all-split", lb[b], H.box_min_of_affine(w.C, M, c, w.x0, w.eps))
+
+
+def test_edge_cases():
+    w = wl.tiny()
+    rnet = ref.RefNet(w.layers)
+    # one sub-domain, no split mask at all
+    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, None, B=1)
+    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, B=1)
+    check("B=1 lb", lb, lr)
+    check("B=1 l", l, llr)
+    # eps = 0: the bound is the network value at x0
+    lb, _, _ = gpu_bound(w.layers, w.x0, 0.0, w.C, None, B=2)
+    f0 = H.torch_forward(w.layers, w.x0[None].astype(np.float64)) @ w.C.T.astype(np.float64)
+    check("eps=0", lb, np.repeat(f0, 2, axis=0))
+    # a single affine layer (no ReLU)
+    one = wl.random_net([wl.conv(2, 6, 3, 3, 1, 1)], 4)
+    x0 = np.random.default_rng(4).uniform(0, 1, 72).astype(np.float32)
+    C = np.random.default_rng(5).normal(size=(4, 108)).astype(np.float32)
+    lb, _, _ = gpu_bound(one, x0, 0.1, C, None, B=3)
+    lr, *_ = ref.bound(ref.RefNet(one), x0, 0.1, C, B=3)
+    check("single conv layer", lb, lr)
+    # a convolution as the last layer, spec over its feature map
+    arch = [wl.conv(1, 8, 2, 3, 1, 1), wl.conv(2, 8, 2, 3, 2, 0)]
+    net2 = wl.random_net(arch, 6)
+    x0 = np.random.default_rng(6).uniform(0, 1, 64).astype(np.float32)
+    C = np.random.default_rng(7).normal(size=(5, 18)).astype(np.float32)
+    rn2 = ref.RefNet(net2)
+    split = wl.make_splits(9, rn2.n_relu, 4, 6)
+    lb, l, u = gpu_bound(net2, x0, 0.2, C, split)
+    lr, llr, ulr, _ = ref.bound(rn2, x0, 0.2, C, split)
+    check("conv-last lb", lb, lr)
+    check("conv-last l", l, llr)
+
+
+def test_chunking_permutation_determinism():
+    w = wl.base()
+    rnet = ref.RefNet(w.layers)
+    B = 50
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=B)
+    net = lirpa.Network(w.layers)
+    lb1, l1, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split, net=net)
+    lb2, l2, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split, net=net)
+    assert np.array_equal(lb1, lb2) and np.array_equal(l1, l2), "run-to-run difference"
+    small = lirpa.lirpa_workspace_bytes(net.handle, w.S, 7, 0)
+    lb3, l3, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split, max_ws_bytes=small,
+                           net=lirpa.Network(w.layers))
+    assert np.array_equal(lb1, lb3) and np.array_equal(l1, l3), "chunk size changed results"
+    perm = np.random.default_rng(1).permutation(B)
+    lb4, _, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split[perm], net=net)
+    assert np.array_equal(lb4, lb1[perm]), "sub-domain order changed results"
