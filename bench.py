@@ -1,0 +1,216 @@
+#!/usr/bin/env python
+"""Throughput of batched LiRPA sub-domain bounds on one MI355X.
+
+One step = one lirpa_bound call over the whole batch of the workload (default: the Base conv
+net, 400 sub-domains, 9 margin specs): layer-1 bounds, every intermediate pass (rows +-e_j of
+each hidden layer, per sub-domain under its own splits) and the final pass, each backward stage
+with its relaxation or concretisation fused.  Inputs are synthetic and resident in HBM before
+the timed region.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "subdomain lower bounds/sec (batched LiRPA) + % MFMA / HBM roofline"
+PEAK_FP32_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+
+def stage_work(layers, S, B):
+    """Algorithmic work of one step per kernel class: {class: (flop, bytes)}.
+
+    A backward stage through layer m carries Q = B*R rows (R = 2 n_k for pass k, S for the final
+    pass).  Its flops are 2 * Q * MACs(T_m) with MACs(T_m) = n_out * in_c * k^2 for a conv
+    (every kernel tap, the dense count of the forward convolution) and out_c * in_c for a
+    linear layer.  Its bytes are the fp32 slab it reads ([n_m, Q]) plus, for a relaxing stage,
+    the slab it writes ([n_{m-1}, Q]); a concretising stage writes Q floats.  The pass
+    initialisation writes its relaxed [n_{k-1}, Q] slab."""
+    from paper_2011_13824_amd import workloads as wl
+    L = len(layers)
+    n = [wl.n_in(layers[0])] + [wl.n_out(t) for t in layers]
+
+    def macs(t):
+        if t["kind"] == wl.CONV:
+            return wl.n_out(t) * t["in_c"] * t["k"] * t["k"]
+        return t["out_c"] * t["in_c"]
+
+    work = {}
+
+    def add(cls, flop, byt):
+        f, b = work.get(cls, (0.0, 0.0))
+        work[cls] = (f + flop, b + byt)
+
+    for k in range(2, L + 1):
+        R = 2 * n[k] if k < L else S
+        Q = B * R
+        mtop = k - 1 if k < L else L
+        if k < L:
+            add(f"init_rows[layer{k},pass{k}]", 0.0, 4.0 * n[k - 1] * Q)
+        for m in range(mtop, 0, -1):
+            t = layers[m - 1]
+            kind = "fcT" if t["kind"] == wl.FC else "convT"
+            sfx = "_relax" if m > 1 else "_bound"
+            out_bytes = 4.0 * n[m - 1] * Q if m > 1 else 4.0 * Q
+            add(f"{kind}{sfx}[layer{m},pass{k}]", 2.0 * Q * macs(t), 4.0 * n[m] * Q + out_bytes)
+    return work
+
+
+def total_flops(layers, S, B):
+    return sum(f for f, _ in stage_work(layers, S, B).values())
+
+
+def cpu_baseline(w, budget_s=20.0):
+    """The fp64 oracle, as it is, on a bounded sample of the same workload recipe."""
+    from oracle import ref
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    rnet = ref.RefNet(w.layers)
+    cand = ref.root_unstable(rnet, w.x0, w.eps, w.C)
+    split = w.splits(cand)
+    probe = min(8, w.B)
+    t0 = time.perf_counter()
+    ref.bound(rnet, w.x0, w.eps, w.C, split[:probe], nthreads=threads)
+    per = (time.perf_counter() - t0) / probe
+    n = int(min(w.B, max(probe, budget_s / max(per, 1e-9))))
+    t0 = time.perf_counter()
+    ref.bound(rnet, w.x0, w.eps, w.C, split[:n], nthreads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 3), "unit": "subdomains/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"first {n} of the {w.B} sub-domains of the {w.name} batch "
+                      f"(fp64 C oracle, OpenMP, {dt:.1f} s wall)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="base", choices=["tiny", "base", "wide", "deep"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
+    ap.add_argument("--max-ws-gib", type=float, default=64.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only copy a device buffer of this many MiB 3 times (a known-size "
+                         "kernel for scaling HBM byte counters) and exit")
+    args = ap.parse_args()
+
+    if args.copy_calibration_mib > 0:
+        import torch
+        n = args.copy_calibration_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 3}), flush=True)
+        return
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(sub-domains shard across GPUs with no exchange; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2011_13824_amd import lirpa, workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = wl.get(args.workload)
+    B, S = w.B, w.S
+    net = lirpa.Network(w.layers, device=dev)
+    x0 = torch.as_tensor(w.x0).to(dev)
+    C = torch.as_tensor(w.C).to(dev)
+
+    # split masks: neurons unstable at the root, from this library's own root bound
+    _, l0, u0 = net.bound(x0, w.eps, C, B=1, want_lu=True)
+    l0, u0 = l0.cpu().numpy()[0], u0.cpu().numpy()[0]
+    cand = np.flatnonzero((l0 < 0) & (u0 > 0))
+    split = torch.as_tensor(w.splits(cand)).to(dev)
+
+    ws, ws_bytes = net.workspace(S, B, 0, int(args.max_ws_gib * (1 << 30)))
+    lb = torch.empty((B, S), dtype=torch.float32, device=dev)
+
+    def step():
+        lirpa.lirpa_bound(net.handle, x0, w.eps, C, S, B, split, None, lb, None, None, ws,
+                          ws_bytes)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    value = B / (ms / 1e3)
+
+    # per-kernel event timing over the same number of steps
+    lirpa.lirpa_timing_begin()
+    for _ in range(args.steps):
+        step()
+    times = lirpa.lirpa_timing_end()
+    torch.cuda.synchronize()
+    work = stage_work(w.layers, S, B)
+    stages = {}
+    for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):
+        f, b = work.get(cls, (0.0, 0.0))
+        f, b = f * args.steps, b * args.steps
+        sec = tot_ms / 1e3
+        stages[cls] = {"ms_per_step": round(tot_ms / args.steps, 4),
+                       "launches_per_step": launches / args.steps,
+                       "tflops": round(f / sec / 1e12, 3) if f else None,
+                       "gbs": round(b / sec / 1e9, 1) if b else None}
+    dom = max(times, key=lambda c: times[c][0])
+    tot_ms, launches = times[dom]
+    f, b = work.get(dom, (0.0, 0.0))
+    f, b = f * args.steps, b * args.steps
+    if f > 0:
+        achieved = f / launches / (tot_ms / launches / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
+    else:
+        achieved = b / (tot_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dom
+    roof["avg_launch_ms"] = round(tot_ms / launches, 4)
+    roof["traffic"] = None
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "subdomains/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "net": w.extra.get("arch"), "B": B, "S": S,
+                   "n_relu": w.n_relu, "max_splits": w.max_splits, "eps": w.eps,
+                   "alpha": "upper slope", "ws_gib": round(ws_bytes / 2**30, 2)},
+        "path_tflops": round(total_flops(w.layers, S, B) / (ms / 1e3) / 1e12, 3),
+        "roofline": roof,
+        "stages": stages,
+        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_budget),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

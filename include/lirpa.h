@@ -122,6 +122,20 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
                    const lirpa_opt_params* params, float* lb_best, float* lb_trace, void* ws,
                    size_t ws_bytes, hipStream_t stream);
 
+/* Kernel timing, for profiling harnesses.  Between lirpa_timing_begin() and
+ * lirpa_timing_end() every kernel the calls of this thread enqueue is bracketed by a pair of
+ * hipEvents recorded on the call's own stream.  lirpa_timing_end() waits for those events and
+ * fills up to max_entries records, one per kernel class (summed over its launches), returning
+ * the number of classes in *n.  Timing adds two event records per launch. */
+typedef struct {
+  char name[48];     /* kernel class, e.g. "convT_bound" */
+  double total_ms;   /* summed event-to-event time of its launches */
+  int64_t launches;
+} lirpa_kernel_time;
+
+int lirpa_timing_begin(void);
+int lirpa_timing_end(lirpa_kernel_time* out, int max_entries, int* n);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* lirpa_last_error(void);
 

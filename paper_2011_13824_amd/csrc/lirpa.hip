@@ -46,11 +46,50 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
-#define LIRPA_LAUNCH_CHECK(what)                                                          \
-  do {                                                                                    \
-    hipError_t e_ = hipGetLastError();                                                    \
-    if (e_ != hipSuccess) return fail(LIRPA_EDEVICE, "%s: %s", what, hipGetErrorString(e_)); \
-  } while (0)
+// Kernel timing (lirpa_timing_begin / lirpa_timing_end): event pairs around every launch.
+struct TimingRec {
+  std::string cls;
+  size_t ev;  // index of the first event of the pair in the pool
+};
+struct TimingState {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<TimingRec> recs;
+};
+thread_local TimingState g_tim;
+
+// Enqueue one kernel through `launch`, bracketed by events when timing is on.
+template <typename F>
+int launch_k(const std::string& cls, hipStream_t st, F&& launch) {
+  size_t ev = 0;
+  if (g_tim.on) {
+    while (g_tim.pool.size() < g_tim.used + 2) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return fail(LIRPA_EDEVICE, "hipEventCreate failed");
+      g_tim.pool.push_back(e);
+    }
+    ev = g_tim.used;
+    g_tim.used += 2;
+    if (hipEventRecord(g_tim.pool[ev], st) != hipSuccess)
+      return fail(LIRPA_EDEVICE, "hipEventRecord failed");
+  }
+  launch();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(LIRPA_EDEVICE, "%s: %s", cls.c_str(), hipGetErrorString(e));
+  if (g_tim.on) {
+    if (hipEventRecord(g_tim.pool[ev + 1], st) != hipSuccess)
+      return fail(LIRPA_EDEVICE, "hipEventRecord failed");
+    g_tim.recs.push_back(TimingRec{cls, ev});
+  }
+  return LIRPA_OK;
+}
+
+std::string tag(const char* kind, int m, int k) {
+  char b[64];
+  snprintf(b, sizeof b, "%s[layer%d,pass%d]", kind, m, k);
+  return b;
+}
 
 constexpr int kMaxLayers = 32;
 constexpr int kBlock = 256;
@@ -365,15 +404,17 @@ dim3 grid_for(long n) { return dim3((unsigned)((n + kBlock - 1) / kBlock)); }
 
 // One backward stage through layer m (1-based) applied to Q rows held in `in` ([n_m][ldq]).
 template <int MODE>
-int launch_stage(const lirpa_net* net, int m, const float* in, long ldq, long Q, const Sink& s,
-                 hipStream_t st) {
+int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ldq, long Q,
+                 const Sink& s, hipStream_t st) {
   DLayer t = dlayer(net->T[m - 1]);
+  const char* sfx = MODE == MODE_SLAB ? "_relax" : "_bound";
   if (t.kind == LIRPA_LINEAR)
-    hipLaunchKernelGGL(k_fcT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
-  else
+    return launch_k(tag((std::string("fcT") + sfx).c_str(), m, pass), st, [&] {
+      hipLaunchKernelGGL(k_fcT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
+    });
+  return launch_k(tag((std::string("convT") + sfx).c_str(), m, pass), st, [&] {
     hipLaunchKernelGGL(k_convT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
-  LIRPA_LAUNCH_CHECK("backward stage");
-  return LIRPA_OK;
+  });
 }
 
 struct Chunk {
@@ -426,29 +467,29 @@ int relax_layer(const Chunk& c, int m) {
   const lirpa_net* net = c.net;
   long nm = net->n[m];
   long off = net->off[m];
-  hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
-                     net->n_relu, off, c.L, c.U, c.split, c.alpha, at<float>(c.ws, c.p->off_alo),
-                     at<float>(c.ws, c.p->off_aup), at<float>(c.ws, c.p->off_bup),
-                     at<int8_t>(c.ws, c.p->off_code));
-  LIRPA_LAUNCH_CHECK("relaxation parameters");
-  return LIRPA_OK;
+  return launch_k(tag("relax_params", m, m), c.st, [&] {
+    hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
+                       net->n_relu, off, c.L, c.U, c.split, c.alpha,
+                       at<float>(c.ws, c.p->off_alo), at<float>(c.ws, c.p->off_aup),
+                       at<float>(c.ws, c.p->off_bup), at<int8_t>(c.ws, c.p->off_code));
+  });
 }
 
 // Stages m = mtop .. 1 on rows already in slab 0 (relaxed onto layer mtop when mtop < L, raw
 // spec rows when mtop == L), ending with the concretisation into (lo, hi).
-int run_stages(const Chunk& c, int mtop, long R, long Q, long ldq, float* lo, float* hi,
-               long bstride, long n_half) {
+int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, float* lo,
+               float* hi, long bstride, long n_half) {
   float* slab[2] = {at<float>(c.ws, c.p->off_slab0), at<float>(c.ws, c.p->off_slab1)};
   int cur = 0;
   for (int m = mtop; m >= 1; --m) {
     int e;
     if (m > 1) {
       Sink s = slab_sink(c, m - 1, slab[1 - cur], ldq, R);
-      e = launch_stage<MODE_SLAB>(c.net, m, slab[cur], ldq, Q, s, c.st);
+      e = launch_stage<MODE_SLAB>(c.net, m, pass, slab[cur], ldq, Q, s, c.st);
       cur ^= 1;
     } else {
       Sink s = bound_sink(c, R, lo, hi, bstride, n_half);
-      e = launch_stage<MODE_BOUND>(c.net, m, slab[cur], ldq, Q, s, c.st);
+      e = launch_stage<MODE_BOUND>(c.net, m, pass, slab[cur], ldq, Q, s, c.st);
     }
     if (e) return e;
   }
@@ -461,18 +502,22 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   long n1 = net->n[1];
   if (L >= 2) {
     const float* l1u1 = at<float>(c.ws, c.p->off_l1u1);
-    hipLaunchKernelGGL(k_bcast_l1, grid_for(c.nb * n1), dim3(kBlock), 0, c.st, c.nb, n1,
-                       net->n_relu, l1u1, l1u1 + n1, c.L, c.U);
-    LIRPA_LAUNCH_CHECK("layer-1 bounds broadcast");
+    if (int e = launch_k(tag("bcast_l1", 1, 1), c.st, [&] {
+          hipLaunchKernelGGL(k_bcast_l1, grid_for(c.nb * n1), dim3(kBlock), 0, c.st, c.nb, n1,
+                             net->n_relu, l1u1, l1u1 + n1, c.L, c.U);
+        }))
+      return e;
     if (int e = relax_layer(c, 1)) return e;
   }
   for (int k = 2; k <= L - 1; ++k) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
     Sink s = slab_sink(c, k - 1, at<float>(c.ws, c.p->off_slab0), ldq, R);
-    hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
-                       dlayer(net->T[k - 1]), Q, s);
-    LIRPA_LAUNCH_CHECK("pass initialisation");
-    if (int e = run_stages(c, k - 1, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
+    if (int e = launch_k(tag("init_rows", k, k), c.st, [&] {
+          hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
+                             dlayer(net->T[k - 1]), Q, s);
+        }))
+      return e;
+    if (int e = run_stages(c, k, k - 1, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
                            net->n_relu, nk))
       return e;
     if (int e = relax_layer(c, k)) return e;
@@ -480,11 +525,13 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   // final pass
   long R = c.S, Q = c.nb * R, ldq = round_up(Q, 64);
   const lirpa_layer& tL = net->T[L - 1];
-  hipLaunchKernelGGL(k_spec_rows, grid_for(Q), dim3(kBlock), 0, c.st, C, net->n[L], tL.b,
-                     tL.out_h * tL.out_w, Q, c.S, at<float>(c.ws, c.p->off_slab0), ldq,
-                     at<float>(c.ws, c.p->off_beta));
-  LIRPA_LAUNCH_CHECK("spec rows");
-  return run_stages(c, L, R, Q, ldq, lb, lb, c.S, c.S);
+  if (int e = launch_k(tag("spec_rows", L, L), c.st, [&] {
+        hipLaunchKernelGGL(k_spec_rows, grid_for(Q), dim3(kBlock), 0, c.st, C, net->n[L], tL.b,
+                           tL.out_h * tL.out_w, Q, c.S, at<float>(c.ws, c.p->off_slab0), ldq,
+                           at<float>(c.ws, c.p->off_beta));
+      }))
+    return e;
+  return run_stages(c, L, L, R, Q, ldq, lb, lb, c.S, c.S);
 }
 
 // Exact layer-1 bounds, shared by every sub-domain: rows +-e_j of h^(1) through T_1, then
@@ -501,10 +548,10 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
   s.hi = l1u1 + n1;
   s.bstride = 0;
   s.n_half = n1;
-  hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
-                     dlayer(net->T[0]), Q, s);
-  LIRPA_LAUNCH_CHECK("layer-1 bounds");
-  return LIRPA_OK;
+  return launch_k(tag("init_rows_bound", 1, 1), st, [&] {
+    hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
+                       dlayer(net->T[0]), Q, s);
+  });
 }
 
 int check_common(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
@@ -640,6 +687,42 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
   (void)adam_m; (void)adam_v; (void)params; (void)lb_best; (void)lb_trace; (void)ws;
   (void)ws_bytes; (void)stream;
   return fail(LIRPA_EUNSUPPORTED, "lirpa_optimize is not implemented yet");
+}
+
+int lirpa_timing_begin(void) {
+  g_tim.on = true;
+  g_tim.used = 0;
+  g_tim.recs.clear();
+  return LIRPA_OK;
+}
+
+int lirpa_timing_end(lirpa_kernel_time* out, int max_entries, int* n) {
+  g_tim.on = false;
+  std::vector<lirpa_kernel_time> acc;
+  int rc = LIRPA_OK;
+  for (const TimingRec& r : g_tim.recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(g_tim.pool[r.ev + 1]) != hipSuccess ||
+        hipEventElapsedTime(&ms, g_tim.pool[r.ev], g_tim.pool[r.ev + 1]) != hipSuccess) {
+      rc = fail(LIRPA_EDEVICE, "timing events failed");
+      break;
+    }
+    auto it = std::find_if(acc.begin(), acc.end(),
+                           [&](const lirpa_kernel_time& k) { return r.cls == k.name; });
+    if (it == acc.end()) {
+      lirpa_kernel_time k{};
+      snprintf(k.name, sizeof k.name, "%s", r.cls.c_str());
+      acc.push_back(k);
+      it = acc.end() - 1;
+    }
+    it->total_ms += ms;
+    it->launches += 1;
+  }
+  g_tim.recs.clear();
+  g_tim.used = 0;
+  if (n) *n = (int)acc.size();
+  for (int i = 0; out && i < (int)acc.size() && i < max_entries; ++i) out[i] = acc[i];
+  return rc;
 }
 
 const char* lirpa_last_error(void) { return g_err.c_str(); }

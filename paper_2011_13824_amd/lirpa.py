@@ -32,9 +32,14 @@ class lirpa_opt_params(ctypes.Structure):
                 ("beta2", ctypes.c_float), ("eps_adam", ctypes.c_float), ("t0", ctypes.c_int)]
 
 
+class lirpa_kernel_time(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("total_ms", ctypes.c_double),
+                ("launches", ctypes.c_int64)]
+
+
 SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
            "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_grad", "lirpa_optimize",
-           "lirpa_last_error")
+           "lirpa_timing_begin", "lirpa_timing_end", "lirpa_last_error")
 
 _lib = None
 
@@ -64,6 +69,10 @@ def load() -> ctypes.CDLL:
     L.lirpa_optimize.argtypes = [P, P, f, P, i, i, P, P, P, P, ctypes.POINTER(lirpa_opt_params),
                                  P, P, P, sz, P]
     L.lirpa_optimize.restype = i
+    L.lirpa_timing_begin.argtypes = []
+    L.lirpa_timing_begin.restype = i
+    L.lirpa_timing_end.argtypes = [ctypes.POINTER(lirpa_kernel_time), i, ctypes.POINTER(i)]
+    L.lirpa_timing_end.restype = i
     L.lirpa_last_error.argtypes = []
     L.lirpa_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -102,6 +111,19 @@ def _stream(stream):
 
 def lirpa_last_error() -> str:
     return load().lirpa_last_error().decode()
+
+
+def lirpa_timing_begin():
+    _check(load().lirpa_timing_begin())
+
+
+def lirpa_timing_end(max_entries=256):
+    """{kernel class: (total_ms, launches)} of the kernels enqueued since lirpa_timing_begin."""
+    arr = (lirpa_kernel_time * max_entries)()
+    n = ctypes.c_int(0)
+    _check(load().lirpa_timing_end(arr, max_entries, ctypes.byref(n)))
+    return {arr[i].name.decode(): (arr[i].total_ms, int(arr[i].launches))
+            for i in range(min(n.value, max_entries))}
 
 
 def lirpa_net_create(layers):
