@@ -151,6 +151,7 @@ struct Sink {
   float* hi;
   long bstride;
   long n_half;
+  float* tape;  // optional: the coefficient before relaxation (or over x), [i*ldq + q]
 };
 
 struct Acc {
@@ -160,6 +161,7 @@ struct Acc {
 template <int MODE>
 __device__ __forceinline__ void sink_put(const Sink& s, Acc& acc, long i, float a, long q,
                                          long b) {
+  if (s.tape) s.tape[i * s.ldq + q] = a;
   if constexpr (MODE == MODE_SLAB) {
     long pi = b * s.pstride + i;
     float ah;
@@ -349,20 +351,172 @@ __global__ void __launch_bounds__(kBlock) k_bcast_l1(long nb, long n1, long stri
 }
 
 // ---------------------------------------------------------------------------------------------
+// Gradient kernels (reverse sweep of one pass)
+// ---------------------------------------------------------------------------------------------
+
+// Row weights of pass P: 1 for the spec rows of the final pass (J = sum_s lb_s); for pass P < L
+// the adjoints of the bounds it produced: row +e_j carries g_l[j], row -e_j carries -g_u[j]
+// (u_j = -lb of that row).
+__global__ void __launch_bounds__(kBlock) k_row_weights(long Q, long R, long nP, long n_relu,
+                                                        long offP, int final_pass,
+                                                        const float* __restrict__ gl,
+                                                        const float* __restrict__ gu,
+                                                        float* __restrict__ w) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  if (final_pass) {
+    w[q] = 1.f;
+    return;
+  }
+  long b = q / R, r = q % R;
+  w[q] = r < nP ? gl[b * n_relu + offP + r] : -gu[b * n_relu + offP + (r - nP)];
+}
+
+// Forward step of the witness pass through layer m for every row with a non-zero weight.
+// The row's bound equals its linear lower function at the box vertex x* = x0 - eps sign(A_x);
+// that function is the network with each ReLU replaced, per row, by the line the backward pass
+// chose for it (lower line where the row's coefficient was >= 0, upper line otherwise).
+// G = W_m z + b_m is the pre-activation along that network; z_out = chosen line applied to G.
+// WITNESS: the input z is built on the fly from the tape of A_x.
+template <bool WITNESS>
+__global__ void __launch_bounds__(kBlock)
+    k_fwd(DLayer t, const float* __restrict__ zin, long ldq, long Q, long R,
+          const float* __restrict__ w, const float* __restrict__ x0, float eps,
+          const float* __restrict__ tape, const float* __restrict__ a_lo,
+          const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+          float* __restrict__ G, float* __restrict__ zout) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q || w[q] == 0.f) return;
+  long b = q / R;
+  auto in = [&](long i) -> float {
+    float v = zin[i * ldq + q];
+    if constexpr (WITNESS) return x0[i] - eps * (v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f));
+    return v;
+  };
+  const int hw = t.out_h * t.out_w;
+  const long nout = (long)t.out_c * hw;
+  for (long o = 0; o < nout; ++o) {
+    float g = t.b[o / hw];
+    if (t.kind == LIRPA_LINEAR) {
+      for (int i = 0; i < t.in_c; ++i) g = fmaf(t.W[o * t.in_c + i], in(i), g);
+    } else {
+      int co = (int)(o / hw), yo = (int)((o / t.out_w) % t.out_h), xo = (int)(o % t.out_w);
+      for (int ci = 0; ci < t.in_c; ++ci)
+        for (int ky = 0; ky < t.k; ++ky) {
+          int yi = yo * t.stride - t.pad + ky;
+          if (yi < 0 || yi >= t.in_h) continue;
+          for (int kx = 0; kx < t.k; ++kx) {
+            int xi = xo * t.stride - t.pad + kx;
+            if (xi < 0 || xi >= t.in_w) continue;
+            g = fmaf(t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx],
+                     in(((long)ci * t.in_h + yi) * t.in_w + xi), g);
+          }
+        }
+    }
+    G[o * ldq + q] = g;
+    if (zout) {
+      long pi = b * pstride + o;
+      float tv = tape[o * ldq + q];
+      zout[o * ldq + q] = tv >= 0.f ? a_lo[pi] * g : fmaf(a_up[pi], g, b_up[pi]);
+    }
+  }
+}
+
+// Adjoint accumulation for ReLU layer m: one wave per (sub-domain, neuron) sums over the rows of
+// the pass, w * max(A~,0) G (-> alpha), w * min(A~,0) G (-> upper slope) and w * min(A~,0)
+// (-> upper intercept), and for unstable neurons turns the last two into adjoints of l and u
+// through a_up = u/(u-l), b_up = -u l/(u-l).  Deterministic: fixed lane order and tree.
+__global__ void __launch_bounds__(kBlock)
+    k_grad_reduce(long nb, long nm, long R, long ldq, const float* __restrict__ w,
+                  const float* __restrict__ tape, const float* __restrict__ G,
+                  const int8_t* __restrict__ code, const float* __restrict__ l,
+                  const float* __restrict__ u, long n_relu, float* __restrict__ ga,
+                  float* __restrict__ gl, float* __restrict__ gu) {
+  long pair = blockIdx.x * (long)(blockDim.x / 64) + threadIdx.x / 64;
+  int lane = threadIdx.x % 64;
+  if (pair >= nb * nm) return;  // uniform per wave
+  long b = pair / nm, j = pair % nm;
+  float sa = 0.f, da = 0.f, db = 0.f;
+  for (long r = lane; r < R; r += 64) {
+    long q = b * R + r;
+    float wr = w[q];
+    if (wr == 0.f) continue;
+    float tv = tape[j * ldq + q], g = G[j * ldq + q];
+    float tp = fmaxf(tv, 0.f), tn = fminf(tv, 0.f);
+    sa = fmaf(wr * tp, g, sa);
+    da = fmaf(wr * tn, g, da);
+    db = fmaf(wr, tn, db);
+  }
+  for (int o = 32; o >= 1; o >>= 1) {
+    sa += __shfl_xor(sa, o, 64);
+    da += __shfl_xor(da, o, 64);
+    db += __shfl_xor(db, o, 64);
+  }
+  if (lane != 0) return;
+  long p = b * n_relu + j;
+  if (code[p] != 5) return;
+  float lj = l[p], uj = u[p], d = uj - lj, d2 = d * d;
+  ga[p] += sa;
+  gl[p] += (da * uj - db * uj * uj) / d2;
+  gu[p] += (-da * lj + db * lj * lj) / d2;
+}
+
+// Projected Adam ascent step (bias-corrected), alpha clipped to [0, 1].
+__global__ void __launch_bounds__(kBlock) k_adam(long n, float* __restrict__ alpha,
+                                                 float* __restrict__ m, float* __restrict__ v,
+                                                 const float* __restrict__ g, float lr,
+                                                 float b1, float b2, float eps, float c1,
+                                                 float c2) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float gi = g[i];
+  float mi = b1 * m[i] + (1.f - b1) * gi;
+  float vi = b2 * v[i] + (1.f - b2) * gi * gi;
+  m[i] = mi;
+  v[i] = vi;
+  float a = alpha[i] + lr * (mi / c1) / (sqrtf(vi / c2) + eps);
+  alpha[i] = fminf(fmaxf(a, 0.f), 1.f);
+}
+
+// Best bound so far (elementwise max over iterates) and optional trace copy.
+__global__ void __launch_bounds__(kBlock) k_best(long n, const float* __restrict__ lb,
+                                                 float* __restrict__ best,
+                                                 float* __restrict__ trace, int first) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float v = lb[i];
+  best[i] = first ? v : fmaxf(best[i], v);
+  if (trace) trace[i] = v;
+}
+
+__global__ void __launch_bounds__(kBlock) k_zero(long n, float* __restrict__ p) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+// ---------------------------------------------------------------------------------------------
 // Workspace plan
 // ---------------------------------------------------------------------------------------------
 struct Plan {
   long Bc = 0;
+  int mode = 0;
   size_t off_l = 0, off_u = 0, off_alo = 0, off_aup = 0, off_bup = 0, off_code = 0;
   size_t off_l1u1 = 0, off_slab0 = 0, off_slab1 = 0, off_beta = 0, total = 0;
   long slab_floats = 0, qp_max = 0;
+  // mode 1 (gradient): tape[k][m] holds, for pass k, the coefficients over g^(m) before their
+  // relaxation (m >= 1) and over x (m = 0), [n_m][qp_k]; adjoints; row weights; forward slabs.
+  size_t off_tape[kMaxLayers + 1][kMaxLayers + 1] = {};
+  size_t off_ga = 0, off_gl = 0, off_gu = 0, off_w = 0, off_za = 0, off_zb = 0, off_G = 0;
+  size_t off_lbt = 0, off_grad = 0;
+  long fwd_floats = 0;
 };
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-Plan make_plan(const lirpa_net* net, long S, long Bc) {
+Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   Plan p;
   p.Bc = Bc;
+  p.mode = mode;
   const int L = net->L;
   long slab = 0, qpmax = round_up(2 * net->n[1], 64);
   for (int k = 2; k <= L; ++k) {
@@ -391,6 +545,28 @@ Plan make_plan(const lirpa_net* net, long S, long Bc) {
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
   p.off_slab0 = o; o = align256(o + (size_t)slab * 4);
   p.off_slab1 = o; o = align256(o + (size_t)slab * 4);
+  if (mode == 1) {
+    long fwd = 0;
+    for (int k = 2; k <= L; ++k) {
+      long R = (k < L) ? 2 * net->n[k] : S;
+      long qp = round_up(Bc * R, 64);
+      for (int m = 0; m <= k - 1; ++m) {
+        p.off_tape[k][m] = o;
+        o = align256(o + (size_t)net->n[m] * qp * 4);
+        if (m >= 1) fwd = std::max(fwd, net->n[m] * qp);
+      }
+    }
+    p.fwd_floats = fwd;
+    p.off_ga = o; o = align256(o + per * 4);
+    p.off_gl = o; o = align256(o + per * 4);
+    p.off_gu = o; o = align256(o + per * 4);
+    p.off_grad = o; o = align256(o + per * 4);
+    p.off_w = o;  o = align256(o + (size_t)qpmax * 4);
+    p.off_za = o; o = align256(o + (size_t)fwd * 4);
+    p.off_zb = o; o = align256(o + (size_t)fwd * 4);
+    p.off_G = o;  o = align256(o + (size_t)fwd * 4);
+    p.off_lbt = o; o = align256(o + (size_t)Bc * S * 4);
+  }
   p.total = o;
   return p;
 }
@@ -430,6 +606,7 @@ struct Chunk {
   const int8_t* split; // chunk's first row or null
   const float* alpha;
   hipStream_t st;
+  bool tape = false;   // record the gradient tape (mode-1 plan)
 };
 
 // Sink that relaxes onto ReLU layer m and stores into `out`.
@@ -477,6 +654,10 @@ int relax_layer(const Chunk& c, int m) {
 
 // Stages m = mtop .. 1 on rows already in slab 0 (relaxed onto layer mtop when mtop < L, raw
 // spec rows when mtop == L), ending with the concretisation into (lo, hi).
+float* tape_of(const Chunk& c, int pass, int m) {
+  return c.tape ? at<float>(c.ws, c.p->off_tape[pass][m]) : nullptr;
+}
+
 int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, float* lo,
                float* hi, long bstride, long n_half) {
   float* slab[2] = {at<float>(c.ws, c.p->off_slab0), at<float>(c.ws, c.p->off_slab1)};
@@ -485,10 +666,13 @@ int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, flo
     int e;
     if (m > 1) {
       Sink s = slab_sink(c, m - 1, slab[1 - cur], ldq, R);
+      s.tape = tape_of(c, pass, m - 1);
       e = launch_stage<MODE_SLAB>(c.net, m, pass, slab[cur], ldq, Q, s, c.st);
       cur ^= 1;
     } else {
       Sink s = bound_sink(c, R, lo, hi, bstride, n_half);
+      s.ldq = ldq;
+      s.tape = tape_of(c, pass, 0);
       e = launch_stage<MODE_BOUND>(c.net, m, pass, slab[cur], ldq, Q, s, c.st);
     }
     if (e) return e;
@@ -512,6 +696,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   for (int k = 2; k <= L - 1; ++k) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
     Sink s = slab_sink(c, k - 1, at<float>(c.ws, c.p->off_slab0), ldq, R);
+    s.tape = tape_of(c, k, k - 1);
     if (int e = launch_k(tag("init_rows", k, k), c.st, [&] {
           hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
                              dlayer(net->T[k - 1]), Q, s);
@@ -554,6 +739,70 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
   });
 }
 
+// Gradient of J_b = sum_s lb[b][s] with respect to alpha for every sub-domain of the chunk,
+// after bound_chunk has recorded the tape (passes visited in descending order; the adjoints of
+// l^(P), u^(P) are complete once every later pass has been visited).  full == 0 visits the
+// final pass only (intermediate bounds held fixed).  Result in ga ([nb][n_relu]).
+int grad_chunk(const Chunk& c, int full) {
+  const lirpa_net* net = c.net;
+  const Plan& p = *c.p;
+  const int L = net->L;
+  long per = c.nb * net->n_relu;
+  float* ga = at<float>(c.ws, p.off_ga);
+  float* gl = at<float>(c.ws, p.off_gl);
+  float* gu = at<float>(c.ws, p.off_gu);
+  float* w = at<float>(c.ws, p.off_w);
+  float* za = at<float>(c.ws, p.off_za);
+  float* zb = at<float>(c.ws, p.off_zb);
+  float* G = at<float>(c.ws, p.off_G);
+  for (float* g : {ga, gl, gu})
+    if (int e = launch_k("zero", c.st, [&] {
+          hipLaunchKernelGGL(k_zero, grid_for(per), dim3(kBlock), 0, c.st, per, g);
+        }))
+      return e;
+  for (int P = L; P >= 2; --P) {
+    if (!full && P < L) break;
+    long R = (P < L) ? 2 * net->n[P] : c.S, Q = c.nb * R, ldq = round_up(Q, 64);
+    long offP = (P < L) ? net->off[P] : 0;
+    if (int e = launch_k(tag("row_weights", P, P), c.st, [&] {
+          hipLaunchKernelGGL(k_row_weights, grid_for(Q), dim3(kBlock), 0, c.st, Q, R, net->n[P],
+                             net->n_relu, offP, (int)(P == L), gl, gu, w);
+        }))
+      return e;
+    const float* zin = tape_of(c, P, 0);
+    float* zbuf[2] = {za, zb};
+    for (int m = 1; m <= P - 1; ++m) {
+      const float* tp = tape_of(c, P, m);
+      long off = net->off[m];
+      float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
+      DLayer t = dlayer(net->T[m - 1]);
+      int e = launch_k(tag("fwd", m, P), c.st, [&] {
+        if (m == 1)
+          hipLaunchKernelGGL(k_fwd<true>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
+                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + off,
+                             at<float>(c.ws, p.off_aup) + off, at<float>(c.ws, p.off_bup) + off,
+                             net->n_relu, G, zout);
+        else
+          hipLaunchKernelGGL(k_fwd<false>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
+                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + off,
+                             at<float>(c.ws, p.off_aup) + off, at<float>(c.ws, p.off_bup) + off,
+                             net->n_relu, G, zout);
+      });
+      if (e) return e;
+      long pairs = c.nb * net->n[m];
+      e = launch_k(tag("grad_reduce", m, P), c.st, [&] {
+        hipLaunchKernelGGL(k_grad_reduce, dim3((unsigned)((pairs + 3) / 4)), dim3(kBlock), 0,
+                           c.st, c.nb, net->n[m], R, ldq, w, tp, G,
+                           at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off, net->n_relu,
+                           ga + off, gl + off, gu + off);
+      });
+      if (e) return e;
+      zin = zout;
+    }
+  }
+  return LIRPA_OK;
+}
+
 int check_common(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
                  void* ws) {
   if (!net) return fail(LIRPA_EINVAL, "net is null");
@@ -567,14 +816,40 @@ int check_common(const lirpa_net* net, const float* x0, float eps, const float* 
 }
 
 // Largest chunk whose workspace fits.
-long fit_chunk(const lirpa_net* net, long S, long B, size_t ws_bytes, Plan* out) {
+long fit_chunk(const lirpa_net* net, long S, long B, size_t ws_bytes, Plan* out, int mode = 0) {
   long lo = 0, hi = B;
   while (lo < hi) {
     long mid = (lo + hi + 1) / 2;
-    if (make_plan(net, S, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+    if (make_plan(net, S, mid, mode).total <= ws_bytes) lo = mid; else hi = mid - 1;
   }
-  if (lo > 0) *out = make_plan(net, S, lo);
+  if (lo > 0) *out = make_plan(net, S, lo, mode);
   return lo;
+}
+
+Chunk make_chunk(lirpa_net* net, const Plan& p, void* ws, const float* x0, float eps, long S,
+                 long B, long b0, const int8_t* split, const float* alpha, float* l_out,
+                 float* u_out, hipStream_t stream) {
+  Chunk c;
+  c.net = net;
+  c.p = &p;
+  c.ws = ws;
+  c.x0 = x0;
+  c.eps = eps;
+  c.S = S;
+  c.nb = std::min(p.Bc, B - b0);
+  c.L = l_out ? l_out + b0 * net->n_relu : at<float>(ws, p.off_l);
+  c.U = u_out ? u_out + b0 * net->n_relu : at<float>(ws, p.off_u);
+  c.split = split ? split + b0 * net->n_relu : nullptr;
+  c.alpha = alpha ? alpha + b0 * net->n_relu : nullptr;
+  c.st = stream;
+  c.tape = (p.mode == 1);
+  return c;
+}
+
+int copy_d2d(void* dst, const void* src, size_t bytes, hipStream_t st) {
+  if (hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return fail(LIRPA_EDEVICE, "hipMemcpyAsync failed");
+  return LIRPA_OK;
 }
 
 }  // namespace
@@ -636,7 +911,7 @@ int64_t lirpa_net_num_relu(const lirpa_net* net) { return net ? net->n_relu : -1
 
 size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode) {
   if (!net || S < 1 || B_chunk < 1 || (mode != 0 && mode != 1)) return 0;
-  return make_plan(net, S, B_chunk).total;
+  return make_plan(net, S, B_chunk, mode).total;
 }
 
 int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
@@ -653,19 +928,7 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
                 make_plan(net, S, 1).total);
   if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
-    Chunk c;
-    c.net = net;
-    c.p = &p;
-    c.ws = ws;
-    c.x0 = x0;
-    c.eps = eps;
-    c.S = S;
-    c.nb = std::min(Bc, (long)B - b0);
-    c.L = l_out ? l_out + b0 * net->n_relu : at<float>(ws, p.off_l);
-    c.U = u_out ? u_out + b0 * net->n_relu : at<float>(ws, p.off_u);
-    c.split = split ? split + b0 * net->n_relu : nullptr;
-    c.alpha = alpha ? alpha + b0 * net->n_relu : nullptr;
-    c.st = stream;
+    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
     if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
   }
   return LIRPA_OK;
@@ -674,19 +937,72 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
 int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
                      const int8_t* split, const float* alpha, int full, float* lb, float* grad,
                      void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)net; (void)x0; (void)eps; (void)C; (void)S; (void)B; (void)split; (void)alpha;
-  (void)full; (void)lb; (void)grad; (void)ws; (void)ws_bytes; (void)stream;
-  return fail(LIRPA_EUNSUPPORTED, "lirpa_bound_grad is not implemented yet");
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!alpha) return fail(LIRPA_EINVAL, "alpha is required for the gradient");
+  if (!lb || !grad) return fail(LIRPA_EINVAL, "lb and grad must be given");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p, 1);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                make_plan(net, S, 1, 1).total);
+  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
+    if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
+    if (int e = grad_chunk(c, full)) return e;
+    if (int e = copy_d2d(grad + b0 * net->n_relu, at<float>(ws, p.off_ga),
+                         sizeof(float) * c.nb * net->n_relu, stream))
+      return e;
+  }
+  return LIRPA_OK;
 }
 
 int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
                    const int8_t* split, float* alpha, float* adam_m, float* adam_v,
                    const lirpa_opt_params* params, float* lb_best, float* lb_trace, void* ws,
                    size_t ws_bytes, hipStream_t stream) {
-  (void)net; (void)x0; (void)eps; (void)C; (void)S; (void)B; (void)split; (void)alpha;
-  (void)adam_m; (void)adam_v; (void)params; (void)lb_best; (void)lb_trace; (void)ws;
-  (void)ws_bytes; (void)stream;
-  return fail(LIRPA_EUNSUPPORTED, "lirpa_optimize is not implemented yet");
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!alpha || !adam_m || !adam_v || !params || !lb_best)
+    return fail(LIRPA_EINVAL, "alpha, adam_m, adam_v, params and lb_best must be given");
+  const lirpa_opt_params& op = *params;
+  if (op.steps < 0 || op.t0 < 0 || !(op.lr >= 0.f) || !(op.beta1 >= 0.f && op.beta1 < 1.f) ||
+      !(op.beta2 >= 0.f && op.beta2 < 1.f) || !(op.eps_adam > 0.f))
+    return fail(LIRPA_EINVAL, "bad optimiser parameters");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p, 1);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                make_plan(net, S, 1, 1).total);
+  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
+    long na = c.nb * net->n_relu, ns = c.nb * S;
+    float* a = alpha + b0 * net->n_relu;
+    float* lbt = at<float>(ws, p.off_lbt);
+    for (int t = 0; t <= op.steps; ++t) {
+      c.tape = (t < op.steps);
+      if (int e = bound_chunk(c, C, lbt)) return e;
+      float* tr = lb_trace ? lb_trace + ((long)t * B + b0) * S : nullptr;
+      if (int e = launch_k("best", stream, [&] {
+            hipLaunchKernelGGL(k_best, grid_for(ns), dim3(kBlock), 0, stream, ns, lbt,
+                               lb_best + b0 * S, tr, (int)(t == 0));
+          }))
+        return e;
+      if (t == op.steps) break;
+      if (int e = grad_chunk(c, 1)) return e;
+      int tt = op.t0 + t + 1;
+      float c1 = (float)(1.0 - std::pow((double)op.beta1, tt));
+      float c2 = (float)(1.0 - std::pow((double)op.beta2, tt));
+      if (int e = launch_k("adam", stream, [&] {
+            hipLaunchKernelGGL(k_adam, grid_for(na), dim3(kBlock), 0, stream, na, a,
+                               adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu,
+                               at<float>(ws, p.off_ga), op.lr, op.beta1, op.beta2, op.eps_adam,
+                               c1, c2);
+          }))
+        return e;
+    }
+  }
+  return LIRPA_OK;
 }
 
 int lirpa_timing_begin(void) {

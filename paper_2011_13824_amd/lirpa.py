@@ -232,3 +232,30 @@ class Network:
             ws, ws_bytes = self.workspace(S, B, 0, max_ws_bytes)
         lirpa_bound(self.handle, x0, eps, C, S, B, split, alpha, lb, l, u, ws, ws_bytes)
         return (lb, l, u) if want_lu else lb
+
+    def bound_grad(self, x0, eps, C, split, alpha, full=True, max_ws_bytes=16 << 30):
+        S, B = C.shape[0], alpha.shape[0]
+        lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        grad = torch.empty((B, self.n_relu), dtype=torch.float32, device=self.device)
+        ws, ws_bytes = self.workspace(S, B, 1, max_ws_bytes)
+        lirpa_bound_grad(self.handle, x0, eps, C, S, B, split, alpha, int(full), lb, grad, ws,
+                         ws_bytes)
+        return lb, grad
+
+    def optimize(self, x0, eps, C, split, alpha, adam_m=None, adam_v=None, steps=20, lr=0.1,
+                 beta1=0.9, beta2=0.999, eps_adam=1e-8, t0=0, trace=False,
+                 max_ws_bytes=16 << 30):
+        """In place on alpha (and adam_m, adam_v); returns lb_best (and the lb trace)."""
+        S, B = C.shape[0], alpha.shape[0]
+        if adam_m is None:
+            adam_m = torch.zeros_like(alpha)
+        if adam_v is None:
+            adam_v = torch.zeros_like(alpha)
+        best = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        tr = torch.empty((steps + 1, B, S), dtype=torch.float32, device=self.device) \
+            if trace else None
+        ws, ws_bytes = self.workspace(S, B, 1, max_ws_bytes)
+        lirpa_optimize(self.handle, x0, eps, C, S, B, split, alpha, adam_m, adam_v,
+                       lirpa_opt_params(steps, lr, beta1, beta2, eps_adam, t0), best, tr, ws,
+                       ws_bytes)
+        return (best, tr) if trace else best

@@ -1,0 +1,146 @@
+"""GPU parity of the alpha gradient and the projected Adam loop against the fp64 oracle.
+
+Gates: bounds within 1e-4 abs + 1e-4 rel; gradients normwise per sub-domain,
+||g_gpu - g_ref||_inf <= 1e-4 (1 + ||g_ref||_inf); split neurons get exactly 0 on both sides;
+each Adam step is replayed in fp64 from the GPU's own (alpha, m, v, g)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ref
+from paper_2011_13824_amd import lirpa
+from paper_2011_13824_amd import workloads as wl
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lirpa.load()
+
+
+def dev(a):
+    return None if a is None else torch.as_tensor(np.ascontiguousarray(a)).cuda()
+
+
+def check_bound(name, got, want):
+    excess = np.abs(got - want) - (1e-4 + 1e-4 * np.abs(want))
+    print(f"{name}: max |gpu - oracle| = {np.abs(got - want).max():.3g}", flush=True)
+    assert np.all(excess <= 0), f"{name}: bound off by {excess.max():.3g} beyond tolerance"
+
+
+def check_grad(name, got, want, split):
+    for b in range(got.shape[0]):
+        ref_inf = np.abs(want[b]).max()
+        err = np.abs(got[b] - want[b]).max()
+        assert err <= 1e-4 * (1 + ref_inf), f"{name}[{b}]: |dg| {err:.3g} vs |g| {ref_inf:.3g}"
+    print(f"{name}: max |g_gpu - g_ref| = {np.abs(got - want).max():.3g}", flush=True)
+    if split is not None:
+        s = split != 0
+        assert np.all(got[s] == 0.0) and np.all(want[s] == 0.0), f"{name}: split neuron grad"
+
+
+def setup(layers, x0, eps, C, B, max_splits, seed):
+    rnet = ref.RefNet(layers)
+    split = wl.make_splits(B, rnet.n_relu, max_splits, seed,
+                           ref.root_unstable(rnet, x0, eps, C))
+    alpha = np.random.default_rng(seed).uniform(0.05, 0.95, (B, rnet.n_relu)).astype(np.float32)
+    return rnet, split, alpha
+
+
+@pytest.mark.parametrize("full", [True, False])
+def test_grad_tiny(full):
+    w = wl.tiny()
+    rnet, split, alpha = setup(w.layers, w.x0, w.eps, w.C, 64, 6, 1)
+    net = lirpa.Network(w.layers)
+    lb, g = net.bound_grad(dev(w.x0), w.eps, dev(w.C), dev(split), dev(alpha), full=full)
+    lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, alpha, full=full)
+    check_bound("tiny lb", lb.cpu().double().numpy(), lr)
+    check_grad("tiny grad", g.cpu().double().numpy(), gr, split)
+
+
+def test_grad_small_conv():
+    layers = wl.random_net(H.small_conv_arch(), 31)
+    x0 = np.random.default_rng(31).uniform(0, 1, wl.n_in(layers[0])).astype(np.float32)
+    C = wl.margin_spec(3, 0)
+    rnet, split, alpha = setup(layers, x0, 0.05, C, 19, 4, 2)
+    net = lirpa.Network(layers)
+    lb, g = net.bound_grad(dev(x0), 0.05, dev(C), dev(split), dev(alpha))
+    lr, gr = ref.bound_grad(rnet, x0, 0.05, C, split, alpha)
+    check_bound("small lb", lb.cpu().double().numpy(), lr)
+    check_grad("small grad", g.cpu().double().numpy(), gr, split)
+
+
+@pytest.mark.parametrize("name", ["base", "deep"])
+def test_grad_conv_nets(name):
+    w = wl.get(name)
+    rnet, split, alpha = setup(w.layers, w.x0, w.eps, w.C, 4, w.max_splits, 3)
+    net = lirpa.Network(w.layers)
+    lb, g = net.bound_grad(dev(w.x0), w.eps, dev(w.C), dev(split), dev(alpha))
+    lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, alpha)
+    check_bound(f"{name} lb", lb.cpu().double().numpy(), lr)
+    check_grad(f"{name} grad", g.cpu().double().numpy(), gr, split)
+
+
+def test_optimize_replay_wide():
+    """Wide net as in the alpha-optimised workload, a few sub-domains, 3 Adam steps replayed."""
+    w = wl.wide_opt()
+    B = 4
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=B)
+    net = lirpa.Network(w.layers)
+    x0, C, sp = dev(w.x0), dev(w.C), dev(split)
+    _, l, u = net.bound(x0, w.eps, C, sp, want_lu=True)
+    l, u = l.cpu().numpy(), u.cpu().numpy()
+    a0 = np.where((l < 0) & (u > 0), u / np.where(u - l > 0, u - l, 1), np.where(l >= 0, 1, 0))
+    alpha = dev(a0.astype(np.float32))
+    m = torch.zeros_like(alpha)
+    v = torch.zeros_like(alpha)
+    lb0 = None
+    for t in range(3):
+        a_t, m_t, v_t = (x.cpu().double().numpy() for x in (alpha, m, v))
+        lb, g = net.bound_grad(x0, w.eps, C, sp, alpha)
+        lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, a_t.astype(np.float32))
+        check_bound(f"step {t} lb", lb.cpu().double().numpy(), lr)
+        check_grad(f"step {t} grad", g.cpu().double().numpy(), gr, split)
+        if lb0 is None:
+            lb0 = lb.cpu().double().numpy()
+        best = net.optimize(x0, w.eps, C, sp, alpha, m, v, steps=1, lr=0.1, t0=t)
+        gg = g.cpu().double().numpy()
+        tt = t + 1
+        # the optimiser's parameters cross the ABI as fp32
+        b1, b2, lr, ea = (np.float64(np.float32(x)) for x in (0.9, 0.999, 0.1, 1e-8))
+        m_e = b1 * m_t + (1 - b1) * gg
+        v_e = b2 * v_t + (1 - b2) * gg * gg
+        a_e = np.clip(a_t + lr * (m_e / (1 - b1 ** tt)) / (np.sqrt(v_e / (1 - b2 ** tt)) + ea),
+                      0, 1)
+        np.testing.assert_allclose(m.cpu().double().numpy(), m_e, rtol=1e-5, atol=1e-7)
+        np.testing.assert_allclose(v.cpu().double().numpy(), v_e, rtol=1e-5, atol=1e-9)
+        np.testing.assert_allclose(alpha.cpu().double().numpy(), a_e, rtol=0, atol=2e-6)
+        assert np.all(best.cpu().double().numpy() >= lb.cpu().double().numpy())
+
+
+def test_optimize_improves_and_is_sound():
+    """20 Adam steps on the tiny net: best-so-far never below the start, never above the
+    sampled minimum of the split network."""
+    w = wl.tiny()
+    rnet, split, _ = setup(w.layers, w.x0, w.eps, w.C, 64, 6, 5)
+    net = lirpa.Network(w.layers)
+    x0, C, sp = dev(w.x0), dev(w.C), dev(split)
+    lb0, l, u = net.bound(x0, w.eps, C, sp, want_lu=True)
+    l, u = l.cpu().numpy(), u.cpu().numpy()
+    a0 = np.where((l < 0) & (u > 0), u / np.where(u - l > 0, u - l, 1), np.where(l >= 0, 1, 0))
+    alpha = dev(a0.astype(np.float32))
+    best, trace = net.optimize(x0, w.eps, C, sp, alpha, steps=20, lr=0.1, trace=True)
+    best, trace = best.cpu().double().numpy(), trace.cpu().double().numpy()
+    lb0 = lb0.cpu().double().numpy()
+    check_bound("trace[0] vs heuristic", trace[0], lb0)
+    assert np.array_equal(best, trace.max(0))
+    assert np.all(best >= trace[0]) and best.sum() > trace[0].sum()
+    X = H.box_samples(w.x0, w.eps, 20000, np.random.default_rng(0))
+    for b in range(0, 64, 9):
+        vals = H.torch_forward(w.layers, X, split[b]) @ w.C.T.astype(np.float64)
+        assert np.all(best[b] <= vals.min(0) + 1e-5)
