@@ -106,6 +106,10 @@ struct lirpa_net {
   long n[kMaxLayers + 1] = {};    // n[0] input size, n[m] size of h^(m)
   long off[kMaxLayers + 1] = {};  // offset of ReLU layer m in per-neuron arrays
   long n_relu = 0;
+  // internal layout of the relaxation parameters: every layer segment starts on a 16-byte
+  // boundary so that rows of a feature map load as float4
+  long poff[kMaxLayers + 1] = {};
+  long pstride = 0;
 };
 
 namespace {
@@ -299,18 +303,320 @@ __global__ void __launch_bounds__(kBlock) k_convT(DLayer t, const float* __restr
   sink_finish<MODE>(s, acc, q, b, r, false);
 }
 
+// ---------------------------------------------------------------------------------------------
+// MFMA stage kernels (fp32 32x32x2 matrix cores).
+//
+// Lane layout of v_mfma_f32_32x32x2_f32 (measured on gfx950): lane l supplies A[l%32][l/32] and
+// B[l/32][l%32]; accumulator register r of lane l holds D[8(r/4) + 4(l/32) + r%4][l%32].
+// ---------------------------------------------------------------------------------------------
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+// Reduce (beta, lin, l1) of the two lane halves and of the waves of the block, then finish the
+// rows q0..q0+31.  red: LDS scratch of nw*3*32 floats.
+template <int MODE>
+__device__ __forceinline__ void block_finish(const Sink& s, Acc acc, float* red, long q0, long Q,
+                                             bool add_beta_from_acc) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  acc.beta += __shfl_xor(acc.beta, 32, 64);
+  acc.lin += __shfl_xor(acc.lin, 32, 64);
+  acc.l1 += __shfl_xor(acc.l1, 32, 64);
+  if (lane < 32) {
+    red[(wave * 3 + 0) * 32 + lane] = acc.beta;
+    red[(wave * 3 + 1) * 32 + lane] = acc.lin;
+    red[(wave * 3 + 2) * 32 + lane] = acc.l1;
+  }
+  __syncthreads();
+  if (wave != 0 || lane >= 32) return;
+  long q = q0 + lane;
+  if (q >= Q) return;
+  Acc t{0.f, 0.f, 0.f};
+  for (int w = 0; w < nw; ++w) {
+    t.beta += red[(w * 3 + 0) * 32 + lane];
+    t.lin += red[(w * 3 + 1) * 32 + lane];
+    t.l1 += red[(w * 3 + 2) * 32 + lane];
+  }
+  (void)add_beta_from_acc;
+  sink_finish<MODE>(s, t, q, q / s.R, q % s.R, false);
+}
+
+// Transposed convolution as a scatter-form implicit GEMM on 16x16x4 MFMA.
+//
+// Lane layout of v_mfma_f32_16x16x4_f32 (measured on gfx950): lane l supplies A[l%16][l/16] and
+// B[l/16][l%16]; accumulator register r of lane l holds D[4(l/16) + r][l%16].
+//
+// Block: 16 rows q (N) and one wave per CPW output channels ci.  M = 16 tap slots (G, kx): lane
+// group G = l/16, kx = register r; K = 4 of the layer's output channels co per MFMA.  Input
+// positions are visited row by row (y1) from a double-buffered LDS tile.  Output row y always
+// lives in lane group (y + P) mod K, so at input row y1 group G takes tap row
+// ky = (G - y1*S) mod K (the A operand rotates, the accumulators stay put) and collects in its
+// own registers the whole contribution of row y1 to output row y1*S - P + ky, including the
+// overlap along x.  Rows with ky < S are complete after row y1 and go to the epilogue
+// (relaxation of layer m-1 plus bias, or concretisation) before the group starts its next row.
+// The y1 loop is unrolled over the rotation period so every register index is static.
+template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CPW, int NW,
+          int MODE, bool TAPE>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
+k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
+  static_assert(K <= 4 && S <= K && CO % 4 == 0 && W0 % 4 == 0, "unsupported geometry");
+  constexpr int KS = CO / 4;
+  constexpr int NT = 64 * NW;
+  constexpr int PER = (K % S == 0) ? K / S : K;  // rotation period of the tap rows
+  constexpr int TILE = CO * W1 * 16;  // floats per input-row tile
+  constexpr int NV4 = TILE / 4;       // float4 per tile
+  extern __shared__ float lds[];
+  float* tiles = lds;                  // 2 x [CO][W1][16]
+  float* xs = lds + 2 * TILE;          // MODE_BOUND: x0 [in_c*H0*W0]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, G = lane >> 4;
+  const unsigned q0 = blockIdx.x * 16u;
+  const unsigned q = q0 + n;
+  const bool qok = q < Q;
+  const unsigned b = qok ? q / (unsigned)s.R : 0u;
+  float* red = xs + (MODE == MODE_BOUND ? t.in_c * H0 * W0 : 0);  // [NW][3][16]
+
+  if constexpr (MODE == MODE_BOUND) {
+    const int nx = t.in_c * H0 * W0;
+    for (int e = threadIdx.x; e < nx; e += NT) xs[e] = s.x0[e];
+  }
+
+  // A operands, one set per rotation phase: slot (M/4, M%4) of lane l (M = l%16) takes tap
+  // ((M/4 - ph*S) mod K, M%4) of co = 4*ks + l/16
+  float wreg[PER][CPW][KS];
+  int cis[CPW];
+  bool cok[CPW];
+#pragma unroll
+  for (int c = 0; c < CPW; ++c) {
+    cis[c] = wave * CPW + c;
+    cok[c] = cis[c] < t.in_c;
+  }
+  {
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER; ++ph) {
+      const int ky = ((slot - ph * S) % K + K) % K;
+#pragma unroll
+      for (int c = 0; c < CPW; ++c)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int co = 4 * ks + G;
+          wreg[ph][c][ks] = (cok[c] && slot < K && kx < K)
+                                ? t.W[((co * t.in_c + cis[c]) * K + ky) * K + kx] : 0.f;
+        }
+    }
+  }
+
+  float beta = 0.f, lin = 0.f, l1 = 0.f;
+  auto emit = [&](int c, int y, const float* vals) {
+    if (!cok[c] || !qok || y < 0 || y >= H0) return;
+    const unsigned rowi = ((unsigned)cis[c] * H0 + y) * W0;
+    if constexpr (MODE == MODE_BOUND) {
+#pragma unroll
+      for (int x = 0; x < W0; ++x) {
+        const float a = vals[x];
+        if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = a;
+        lin = fmaf(a, xs[rowi + x], lin);
+        l1 += fabsf(a);
+      }
+    } else {
+      const long pb = (long)b * s.pstride + rowi;
+      const float bias_c = s.bias[cis[c]];
+#pragma unroll
+      for (int x4 = 0; x4 < W0; x4 += 4) {
+        const float4v lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + x4);
+        const float4v up = *reinterpret_cast<const float4v*>(s.a_up + pb + x4);
+        const float4v bu = *reinterpret_cast<const float4v*>(s.b_up + pb + x4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float a = vals[x4 + j];
+          const unsigned idx = (rowi + x4 + j) * ldq + q;
+          if constexpr (TAPE) s.tape[idx] = a;
+          const float ah = a >= 0.f ? a * lo[j] : a * up[j];
+          beta = fmaf(fminf(a, 0.f), bu[j], beta);
+          beta = fmaf(ah, bias_c, beta);
+          s.out[idx] = ah;
+        }
+      }
+    }
+  };
+
+  float acc[CPW][W0];
+#pragma unroll
+  for (int c = 0; c < CPW; ++c)
+#pragma unroll
+    for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+
+  auto gaddr = [&](int y1, int v4) {
+    const int cx = v4 >> 2, j4 = v4 & 3;
+    const int co = cx / W1, x1 = cx - co * W1;
+    return in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4;
+  };
+  for (int v4 = threadIdx.x; v4 < NV4; v4 += NT)
+    *reinterpret_cast<float4v*>(tiles + v4 * 4) = *reinterpret_cast<const float4v*>(gaddr(0, v4));
+  __syncthreads();
+
+  constexpr int PF = (NV4 + NT - 1) / NT;  // prefetched float4 per thread
+  for (int ybase = 0; ybase < H1; ybase += PER) {
+#pragma unroll
+    for (int ph = 0; ph < PER; ++ph) {
+      const int y1 = ybase + ph;
+      if (H1 % PER != 0 && y1 >= H1) break;
+      const float* tile = tiles + (y1 & 1) * TILE;
+      const bool more = y1 + 1 < H1;
+      float4v pf[PF];
+      {
+        // next input row: loaded now, stored to the other LDS buffer after the MFMAs
+        const int yn = more ? y1 + 1 : y1;
+#pragma unroll
+        for (int k = 0; k < PF; ++k) {
+          const int v4 = min((int)threadIdx.x + k * NT, NV4 - 1);
+          pf[k] = *reinterpret_cast<const float4v*>(gaddr(yn, v4));
+        }
+      }
+#pragma unroll
+      for (int x1 = 0; x1 < W1; ++x1) {
+        float bv[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[((4 * ks + G) * W1 + x1) * 16 + n];
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) {
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+#pragma unroll
+          for (int kx = 0; kx < K; ++kx) {
+            const int col = x1 * S - P + kx;
+            if (col >= 0 && col < W0) acc[c][col] += d[kx];
+          }
+        }
+      }
+      // this lane group's tap row at this phase; rows with ky < S are complete
+      const int ky = ((G - ph * S) % K + K) % K;
+      if (G < K && ky < S) {
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) {
+          emit(c, y1 * S - P + ky, acc[c]);
+#pragma unroll
+          for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+        }
+      }
+      if (more) {
+        float* nt = tiles + ((y1 + 1) & 1) * TILE;
+#pragma unroll
+        for (int k = 0; k < PF; ++k) {
+          const int v4 = (int)threadIdx.x + k * NT;
+          if (v4 < NV4) *reinterpret_cast<float4v*>(nt + v4 * 4) = pf[k];
+        }
+        __syncthreads();
+      }
+    }
+  }
+  {
+    // rows still open after the last input row are complete too
+    constexpr int ph_last = (H1 - 1) % PER;
+    const int ky = ((G - ph_last * S) % K + K) % K;
+    if (G < K && ky >= S) {
+#pragma unroll
+      for (int c = 0; c < CPW; ++c) emit(c, (H1 - 1) * S - P + ky, acc[c]);
+    }
+  }
+  // output rows no input row reaches (zero coefficients)
+  constexpr int YZ = (H1 - 1) * S - P + K;
+  if constexpr (YZ < H0) {
+    if (G == 0) {
+      float zero[W0];
+#pragma unroll
+      for (int x = 0; x < W0; ++x) zero[x] = 0.f;
+#pragma unroll
+      for (int y = YZ; y < H0; ++y)
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) emit(c, y, zero);
+    }
+  }
+
+  // sum over lane groups and waves, then finish rows q0..q0+15
+  beta += __shfl_xor(beta, 16, 64);
+  lin += __shfl_xor(lin, 16, 64);
+  l1 += __shfl_xor(l1, 16, 64);
+  beta += __shfl_xor(beta, 32, 64);
+  lin += __shfl_xor(lin, 32, 64);
+  l1 += __shfl_xor(l1, 32, 64);
+  __syncthreads();
+  if (lane < 16) {
+    red[(wave * 3 + 0) * 16 + lane] = beta;
+    red[(wave * 3 + 1) * 16 + lane] = lin;
+    red[(wave * 3 + 2) * 16 + lane] = l1;
+  }
+  __syncthreads();
+  if (wave != 0 || lane >= 16 || !qok) return;
+  Acc tot{0.f, 0.f, 0.f};
+  for (int w = 0; w < NW; ++w) {
+    tot.beta += red[(w * 3 + 0) * 16 + lane];
+    tot.lin += red[(w * 3 + 1) * 16 + lane];
+    tot.l1 += red[(w * 3 + 2) * 16 + lane];
+  }
+  sink_finish<MODE>(s, tot, q, b, q % (unsigned)s.R, false);
+}
+
+// Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q and
+// 4 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 4th tile of 32
+// output features i, K runs over o two at a time.  Epilogue as in the other stages.
+template <int MODE>
+__global__ void __launch_bounds__(256) k_fcT_mfma(DLayer t, const float* __restrict__ in,
+                                                  long ldq, long Q, Sink s) {
+  extern __shared__ float lds[];
+  float* tile = lds;                            // [out_c][32]
+  float* red = lds + (long)t.out_c * 32;        // [4][3][32]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int n = lane & 31, h = lane >> 5;
+  const long q0 = (long)blockIdx.x * 32;
+  const long q = q0 + n;
+  const long b = q < Q ? q / s.R : 0;
+  const int nin = t.in_c, nout = t.out_c;
+  for (int e = threadIdx.x; e < nout * 8; e += blockDim.x) {
+    const int j4 = e & 7, o = e >> 3;
+    *reinterpret_cast<float4*>(tile + o * 32 + j4 * 4) =
+        *reinterpret_cast<const float4*>(in + (long)o * ldq + q0 + j4 * 4);
+  }
+  __syncthreads();
+  Acc sum{0.f, 0.f, 0.f};
+  const int KS = (nout + 1) / 2;
+  for (int mt = wave; mt * 32 < nin; mt += nw) {
+    floatx16 d;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) d[r] = 0.f;
+    const int ia = mt * 32 + (lane & 31);
+    for (int k = 0; k < KS; ++k) {
+      const int o = 2 * k + h;
+      const float a = (o < nout && ia < nin) ? t.W[(long)o * nin + ia] : 0.f;
+      const float bv = o < nout ? tile[o * 32 + n] : 0.f;
+      d = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, d, 0, 0, 0);
+    }
+    if (q < Q) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = mt * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (i < nin) sink_put<MODE>(s, sum, i, d[r], q, b);
+      }
+    }
+  }
+  block_finish<MODE>(s, sum, red, q0, Q, false);
+}
+
 // Relaxation parameters of ReLU layer m for every sub-domain of the chunk (Eq. 5 with the split
 // override of Sec. 3.1, checked in the order: split, u <= 0, l >= 0, unstable).
 __global__ void __launch_bounds__(kBlock)
-    k_relax_params(long nb, long nm, long stride, long off, const float* __restrict__ l,
-                   const float* __restrict__ u, const int8_t* __restrict__ split,
-                   const float* __restrict__ alpha, float* __restrict__ a_lo,
-                   float* __restrict__ a_up, float* __restrict__ b_up,
+    k_relax_params(long nb, long nm, long stride, long off, long pstride, long poff,
+                   const float* __restrict__ l, const float* __restrict__ u,
+                   const int8_t* __restrict__ split, const float* __restrict__ alpha,
+                   float* __restrict__ a_lo, float* __restrict__ a_up, float* __restrict__ b_up,
                    int8_t* __restrict__ code) {
   long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
   if (idx >= nb * nm) return;
   long b = idx / nm, j = idx % nm;
   long p = b * stride + off + j;
+  long pp = b * pstride + poff + j;
   int sp = split ? split[p] : 0;
   float lo = 0.f, up = 0.f, bu = 0.f;
   int c;
@@ -332,9 +638,9 @@ __global__ void __launch_bounds__(kBlock)
       c = 5;
     }
   }
-  a_lo[p] = lo;
-  a_up[p] = up;
-  b_up[p] = bu;
+  a_lo[pp] = lo;
+  a_up[pp] = up;
+  b_up[pp] = bu;
   code[p] = (int8_t)c;
 }
 
@@ -535,11 +841,12 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   p.qp_max = qpmax;
   size_t o = 0;
   size_t per = (size_t)Bc * (net->n_relu ? net->n_relu : 1);
+  size_t perp = (size_t)Bc * (net->pstride ? net->pstride : 4);
   p.off_l = o;    o = align256(o + per * 4);
   p.off_u = o;    o = align256(o + per * 4);
-  p.off_alo = o;  o = align256(o + per * 4);
-  p.off_aup = o;  o = align256(o + per * 4);
-  p.off_bup = o;  o = align256(o + per * 4);
+  p.off_alo = o;  o = align256(o + perp * 4);
+  p.off_aup = o;  o = align256(o + perp * 4);
+  p.off_bup = o;  o = align256(o + perp * 4);
   p.off_code = o; o = align256(o + per);
   p.off_l1u1 = o; o = align256(o + 2 * (size_t)net->n[1] * 4);
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
@@ -568,6 +875,12 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
     p.off_lbt = o; o = align256(o + (size_t)Bc * S * 4);
   }
   p.total = o;
+  // kernels address a slab with 32-bit element offsets
+  long big = std::max(slab, p.fwd_floats);
+  if (mode == 1)
+    for (int k = 2; k <= L; ++k)
+      big = std::max(big, net->n[0] * round_up(Bc * ((k < L) ? 2 * net->n[k] : S), 64));
+  if (big >= (1L << 31)) p.total = (size_t)-1;
   return p;
 }
 
@@ -579,16 +892,87 @@ T* at(void* ws, size_t off) {
 dim3 grid_for(long n) { return dim3((unsigned)((n + kBlock - 1) / kBlock)); }
 
 // One backward stage through layer m (1-based) applied to Q rows held in `in` ([n_m][ldq]).
+// Geometries with an MFMA transposed-convolution kernel: (k, stride, pad, out_h, out_w, in_h,
+// in_w) of the forward layer.  Other shapes use the per-lane gather kernel.
+template <int MODE>
+using ConvTKernel = void (*)(DLayer, const float*, unsigned, unsigned, Sink);
+
+// Block size limit per instantiation: 256 threads (one wave per SIMD, so the unified register
+// file can hold the 32-wide ring of accumulators) for in_c <= 8, else 512.
+// Geometry / channel combinations with an MFMA kernel (those of the Base, Wide and Deep
+// shapes); everything else uses the per-lane gather kernel.  One wave per channel ci, two
+// channels per wave above 8.
+template <int MODE, bool TAPE>
+ConvTKernel<MODE> convT_mfma_pick(const DLayer& t, int* nwaves) {
+  const bool g_s2_32 = t.k == 4 && t.stride == 2 && t.pad == 1 && t.out_h == 16 &&
+                       t.out_w == 16 && t.in_h == 32 && t.in_w == 32;
+  const bool g_s2_16 = t.k == 4 && t.stride == 2 && t.pad == 1 && t.out_h == 8 && t.out_w == 8 &&
+                       t.in_h == 16 && t.in_w == 16;
+  const bool g_s1_16 = t.k == 3 && t.stride == 1 && t.pad == 1 && t.out_h == 16 &&
+                       t.out_w == 16 && t.in_h == 16 && t.in_w == 16;
+  if (g_s2_32 && t.in_c == 3 && t.out_c == 8) {
+    *nwaves = 3;
+    return k_convT_mfma<4, 2, 1, 16, 16, 32, 32, 8, 1, 3, MODE, TAPE>;
+  }
+  if (g_s2_32 && t.in_c == 3 && t.out_c == 16) {
+    *nwaves = 3;
+    return k_convT_mfma<4, 2, 1, 16, 16, 32, 32, 16, 1, 3, MODE, TAPE>;
+  }
+  if (g_s2_16 && t.in_c == 8 && t.out_c == 16) {
+    *nwaves = 8;
+    return k_convT_mfma<4, 2, 1, 8, 8, 16, 16, 16, 1, 8, MODE, TAPE>;
+  }
+  if (g_s2_16 && t.in_c == 8 && t.out_c == 8) {
+    *nwaves = 8;
+    return k_convT_mfma<4, 2, 1, 8, 8, 16, 16, 8, 1, 8, MODE, TAPE>;
+  }
+  if (g_s2_16 && t.in_c == 16 && t.out_c == 32) {
+    *nwaves = 8;
+    return k_convT_mfma<4, 2, 1, 8, 8, 16, 16, 32, 2, 8, MODE, TAPE>;
+  }
+  if (g_s1_16 && t.in_c == 8 && t.out_c == 8) {
+    *nwaves = 8;
+    return k_convT_mfma<3, 1, 1, 16, 16, 16, 16, 8, 1, 8, MODE, TAPE>;
+  }
+  return nullptr;
+}
+
+// Geometry / channel combinations with an MFMA kernel (those of the Base, Wide and Deep
+// shapes); everything else uses the per-lane gather kernel.  One wave per channel ci, two
+// channels per wave above 8.
+template <int MODE>
+ConvTKernel<MODE> convT_mfma_for(const DLayer& t, bool tape, int* nwaves) {
+  return tape ? convT_mfma_pick<MODE, true>(t, nwaves) : convT_mfma_pick<MODE, false>(t, nwaves);
+}
+
 template <int MODE>
 int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ldq, long Q,
                  const Sink& s, hipStream_t st) {
   DLayer t = dlayer(net->T[m - 1]);
   const char* sfx = MODE == MODE_SLAB ? "_relax" : "_bound";
-  if (t.kind == LIRPA_LINEAR)
-    return launch_k(tag((std::string("fcT") + sfx).c_str(), m, pass), st, [&] {
+  const unsigned nblk32 = (unsigned)((Q + 31) / 32);
+  if (t.kind == LIRPA_LINEAR) {
+    if (t.out_c <= 448) {
+      size_t lds = ((size_t)t.out_c * 32 + 4 * 3 * 32) * sizeof(float);
+      return launch_k(tag((std::string("fcT") + sfx).c_str(), m, pass), st, [&] {
+        hipLaunchKernelGGL(k_fcT_mfma<MODE>, dim3(nblk32), dim3(256), lds, st, t, in, ldq, Q, s);
+      });
+    }
+    return launch_k(tag((std::string("fcT_lane") + sfx).c_str(), m, pass), st, [&] {
       hipLaunchKernelGGL(k_fcT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
     });
-  return launch_k(tag((std::string("convT") + sfx).c_str(), m, pass), st, [&] {
+  }
+  int nw = 0;
+  if (ConvTKernel<MODE> kern = convT_mfma_for<MODE>(t, s.tape != nullptr, &nw)) {
+    const unsigned nblk16 = (unsigned)((Q + 15) / 16);
+    size_t lds = (2 * (size_t)t.out_c * t.out_w * 16 + (size_t)nw * 3 * 16 +
+                  (MODE == MODE_BOUND ? (size_t)t.in_c * t.in_h * t.in_w : 0)) * sizeof(float);
+    return launch_k(tag((std::string("convT") + sfx).c_str(), m, pass), st, [&] {
+      hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, st, t, in, (unsigned)ldq,
+                         (unsigned)Q, s);
+    });
+  }
+  return launch_k(tag((std::string("convT_lane") + sfx).c_str(), m, pass), st, [&] {
     hipLaunchKernelGGL(k_convT<MODE>, grid_for(Q), dim3(kBlock), 0, st, t, in, ldq, Q, s);
   });
 }
@@ -616,10 +1000,10 @@ Sink slab_sink(const Chunk& c, int m, float* out, long ldq, long R) {
   Sink s{};
   s.out = out;
   s.ldq = ldq;
-  s.a_lo = at<float>(c.ws, c.p->off_alo) + net->off[m];
-  s.a_up = at<float>(c.ws, c.p->off_aup) + net->off[m];
-  s.b_up = at<float>(c.ws, c.p->off_bup) + net->off[m];
-  s.pstride = net->n_relu;
+  s.a_lo = at<float>(c.ws, c.p->off_alo) + net->poff[m];
+  s.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[m];
+  s.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[m];
+  s.pstride = net->pstride;
   s.bias = t.b;
   s.bias_hw = t.out_h * t.out_w;
   s.beta = at<float>(c.ws, c.p->off_beta);
@@ -646,7 +1030,7 @@ int relax_layer(const Chunk& c, int m) {
   long off = net->off[m];
   return launch_k(tag("relax_params", m, m), c.st, [&] {
     hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
-                       net->n_relu, off, c.L, c.U, c.split, c.alpha,
+                       net->n_relu, off, net->pstride, net->poff[m], c.L, c.U, c.split, c.alpha,
                        at<float>(c.ws, c.p->off_alo), at<float>(c.ws, c.p->off_aup),
                        at<float>(c.ws, c.p->off_bup), at<int8_t>(c.ws, c.p->off_code));
   });
@@ -773,20 +1157,20 @@ int grad_chunk(const Chunk& c, int full) {
     float* zbuf[2] = {za, zb};
     for (int m = 1; m <= P - 1; ++m) {
       const float* tp = tape_of(c, P, m);
-      long off = net->off[m];
+      long off = net->off[m], poff = net->poff[m];
       float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
       DLayer t = dlayer(net->T[m - 1]);
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
         if (m == 1)
           hipLaunchKernelGGL(k_fwd<true>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
-                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + off,
-                             at<float>(c.ws, p.off_aup) + off, at<float>(c.ws, p.off_bup) + off,
-                             net->n_relu, G, zout);
+                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + poff,
+                             at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
+                             net->pstride, G, zout);
         else
           hipLaunchKernelGGL(k_fwd<false>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
-                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + off,
-                             at<float>(c.ws, p.off_aup) + off, at<float>(c.ws, p.off_bup) + off,
-                             net->n_relu, G, zout);
+                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + poff,
+                             at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
+                             net->pstride, G, zout);
       });
       if (e) return e;
       long pairs = c.nb * net->n[m];
@@ -899,6 +1283,8 @@ int lirpa_net_create(const lirpa_layer* layers, int n_layers, lirpa_net** out) {
     if (m < n_layers) {
       net->off[m] = net->n_relu;
       net->n_relu += net->n[m];
+      net->poff[m] = net->pstride;
+      net->pstride += round_up(net->n[m], 4);
     }
   }
   *out = net;
