@@ -559,6 +559,164 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   sink_finish<MODE>(s, tot, q, b, q % (unsigned)s.R, false);
 }
 
+// Pass 2 restricted to each row's receptive field, when T_2 and T_1 are convolutions.
+// Row +-e_j of h^(2), j = (c2, y2, x2), carried through T_2 is +-W_2[c2] placed on the window
+// (y2*S2 - P2 + ky2, x2*S2 - P2 + kx2) of g^(1) and zero elsewhere, so its image under the
+// relaxation of layer 1 and T_1^T is confined to that window's footprint on the input.  One
+// block takes 16 rows that share a window -- one sub-domain, one sign, 16 consecutive c2 -- and
+//  (1) writes their relaxed window coefficients to LDS (Eq. 6), accumulating the intercept and
+//      layer-1 bias terms of each row in a fixed order,
+//  (2) applies T_1^T to the window on 16x16x4 MFMA (one wave per input channel of T_1, the
+//      same rotating lane-group scheme as k_convT_mfma), and
+//  (3) concretises the footprint (Eq. 8; positions outside the image are zero padding) and
+//      writes l_j (sign +) or u_j (sign -) of the sub-domain.
+// The result equals the dense pass exactly in arithmetic terms: the skipped products are zeros.
+template <int K1, int S1, int P1, int K2, int C1, int NW>
+__global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
+               const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+               const float* __restrict__ x0, float eps, float* __restrict__ L,
+               float* __restrict__ U, long n_relu, long off2) {
+  static_assert(C1 % 4 == 0 && K1 <= 4 && K2 <= 4, "unsupported geometry");
+  constexpr int KS = C1 / 4;
+  constexpr int NT = 64 * NW;
+  constexpr int NPOS = K2 * K2;
+  constexpr int WO = (K2 - 1) * S1 + K1;           // footprint width on the input
+  constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int NEL = C1 * NPOS * 16;               // relaxed window tile
+  constexpr int RPT = NT / 16;                      // threads per row in phase 1
+  __shared__ float tile[NEL];
+  __shared__ float red[NW * 3 * 16 + RPT * 16];
+  float* bred = red + NW * 3 * 16;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, G = lane >> 4;
+  // block -> (sub-domain, sign, c2 block, y2, x2)
+  const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
+  const int ncb = C2 / 16;
+  long blk = blockIdx.x;
+  const int x2 = (int)(blk % W2); blk /= W2;
+  const int y2 = (int)(blk % H2); blk /= H2;
+  const int cb = (int)(blk % ncb); blk /= ncb;
+  const int sgn_neg = (int)(blk % 2); blk /= 2;
+  const long b = blk;
+  const float sgn = sgn_neg ? -1.f : 1.f;
+  const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;  // window origin on g^(1)
+  const int H1 = t1.out_h, Wd1 = t1.out_w;
+
+  // (1) relaxed window coefficients of the 16 rows, and their bias terms
+  {
+    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const int c2 = cb * 16 + row;
+    float bpart = 0.f;
+    const long pb = b * pstride;
+    for (int e = part; e < C1 * NPOS; e += RPT) {
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
+      const int y1 = Y1 + ky2, x1 = X1 + kx2;
+      float v = 0.f;
+      if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
+        const float w = sgn * t2.W[(((long)c2 * t2.in_c + c1) * t2.k + ky2) * t2.k + kx2];
+        const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
+        v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
+        bpart = fmaf(fminf(w, 0.f), b_up[pi], bpart);
+        bpart = fmaf(v, t1.b[c1], bpart);
+      }
+      tile[(c1 * NPOS + pos) * 16 + row] = v;
+    }
+    bred[part * 16 + row] = bpart;
+  }
+  __syncthreads();
+
+  // (2) T_1^T on the window, one wave per input channel c0 of T_1
+  const int c0 = wave;
+  const bool cok = c0 < t1.in_c;
+  float wreg[PER][KS];
+  {
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER; ++ph) {
+      const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c1 = 4 * ks + G;
+        wreg[ph][ks] = (cok && slot < K1 && kx < K1)
+                           ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
+      }
+    }
+  }
+  const int Hi = t1.in_h, Wi = t1.in_w;
+  const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;  // footprint origin on the input
+  float lin = 0.f, l1 = 0.f;
+  float acc[WO];
+#pragma unroll
+  for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+  auto emit = [&](int yl) {  // local footprint row yl of channel c0
+    const int y = OY + yl;
+    if (!cok || y < 0 || y >= Hi) return;
+    const float* xr = x0 + ((long)c0 * Hi + y) * Wi;
+#pragma unroll
+    for (int x = 0; x < WO; ++x) {
+      const int xi = OX + x;
+      if (xi >= 0 && xi < Wi) {
+        lin = fmaf(acc[x], xr[xi], lin);
+        l1 += fabsf(acc[x]);
+      }
+    }
+  };
+#pragma unroll
+  for (int j = 0; j < K2; ++j) {
+    const int ph = j % PER;
+#pragma unroll
+    for (int i = 0; i < K2; ++i) {
+      const int pos = j * K2 + i;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
+                                                tile[((4 * ks + G) * NPOS + pos) * 16 + n], d,
+                                                0, 0, 0);
+#pragma unroll
+      for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+    }
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    if (G < K1 && ky < S1) {
+      emit(j * S1 + ky);
+#pragma unroll
+      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+    }
+  }
+  {
+    const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
+    if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
+  }
+
+  // (3) reduce over lane groups and waves; add the bias terms; write the bound
+  lin += __shfl_xor(lin, 16, 64);
+  l1 += __shfl_xor(l1, 16, 64);
+  lin += __shfl_xor(lin, 32, 64);
+  l1 += __shfl_xor(l1, 32, 64);
+  if (lane < 16) {
+    red[(wave * 2 + 0) * 16 + lane] = lin;
+    red[(wave * 2 + 1) * 16 + lane] = l1;
+  }
+  __syncthreads();
+  if (threadIdx.x >= 16) return;
+  const int row = threadIdx.x;
+  const int c2 = cb * 16 + row;
+  float tl = 0.f, ta = 0.f, tb = sgn * t2.b[c2];
+  for (int w = 0; w < NW; ++w) {
+    tl += red[(w * 2 + 0) * 16 + row];
+    ta += red[(w * 2 + 1) * 16 + row];
+  }
+  for (int r = 0; r < RPT; ++r) tb += bred[r * 16 + row];
+  const float v = tl - eps * ta + tb;
+  const long j = ((long)c2 * H2 + y2) * W2 + x2;
+  if (sgn_neg)
+    U[b * n_relu + off2 + j] = -v;
+  else
+    L[b * n_relu + off2 + j] = v;
+}
+
 // Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q and
 // 4 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 4th tile of 32
 // output features i, K runs over o two at a time.  Epilogue as in the other stages.
@@ -819,15 +977,41 @@ struct Plan {
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+// Kernel for the receptive-field pass 2, or null when the shapes do not qualify.
+using Pass2Kernel = void (*)(DLayer, DLayer, long, const float*, const float*, const float*, long,
+                             const float*, float, float*, float*, long, long);
+Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
+  if (net->L < 3) return nullptr;
+  const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
+  if (t1.kind != LIRPA_CONV2D || t2.kind != LIRPA_CONV2D) return nullptr;
+  if (t2.out_c % 16 || t1.in_c > 8) return nullptr;
+  *nw = t1.in_c;
+  if (t1.k == 4 && t1.stride == 2 && t1.pad == 1) {
+    if (t2.k == 4 && t1.out_c == 8) {
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 8, 3>;
+    }
+    if (t2.k == 4 && t1.out_c == 16) {
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 16, 3>;
+    }
+    if (t2.k == 3 && t1.out_c == 8) {
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 3, 8, 3>;
+    }
+  }
+  return nullptr;
+}
+
 Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   Plan p;
   p.Bc = Bc;
   p.mode = mode;
   const int L = net->L;
   long slab = 0, qpmax = round_up(2 * net->n[1], 64);
+  int nw_unused = 0;
+  const bool win2 = mode == 0 && pass2_kernel_for(net, &nw_unused) != nullptr;
   for (int k = 2; k <= L; ++k) {
     long R = (k < L) ? 2 * net->n[k] : S;
     long qp = round_up(Bc * R, 64);
+    if (k == 2 && win2 && k < L) continue;
     qpmax = std::max(qpmax, qp);
     int mtop = (k < L) ? k - 1 : L;  // slabs hold A over h^(m), m = mtop..1
     for (int m = 1; m <= mtop; ++m) slab = std::max(slab, net->n[m] * qp);
@@ -1064,6 +1248,24 @@ int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, flo
   return LIRPA_OK;
 }
 
+// Returns 1 when the shapes do not qualify (the caller runs the dense pass).
+int pass2_window(const Chunk& c) {
+  const lirpa_net* net = c.net;
+  int nw = 0;
+  Pass2Kernel kern = pass2_kernel_for(net, &nw);
+  if (!kern) return 1;
+  const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
+  long blocks = c.nb * 2 * (t2.out_c / 16) * t2.out_h * t2.out_w;
+  const float* alo = at<float>(c.ws, c.p->off_alo) + net->poff[1];
+  const float* aup = at<float>(c.ws, c.p->off_aup) + net->poff[1];
+  const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
+  return launch_k(tag("pass2_window", 1, 2), c.st, [&] {
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * nw), 0, c.st, dlayer(t1),
+                       dlayer(t2), c.nb, alo, aup, bup, net->pstride, c.x0, c.eps, c.L, c.U,
+                       net->n_relu, net->off[2]);
+  });
+}
+
 int bound_chunk(const Chunk& c, const float* C, float* lb) {
   const lirpa_net* net = c.net;
   const int L = net->L;
@@ -1079,6 +1281,14 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   }
   for (int k = 2; k <= L - 1; ++k) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
+    if (k == 2 && !c.tape) {
+      int e = pass2_window(c);
+      if (e != 1) {
+        if (e) return e;
+        if (int e2 = relax_layer(c, k)) return e2;
+        continue;
+      }
+    }
     Sink s = slab_sink(c, k - 1, at<float>(c.ws, c.p->off_slab0), ldq, R);
     s.tape = tape_of(c, k, k - 1);
     if (int e = launch_k(tag("init_rows", k, k), c.st, [&] {
