@@ -175,7 +175,7 @@ __device__ __forceinline__ void sink_put(const Sink& s, Acc& acc, long i, float 
       acc.beta = fmaf(a, s.b_up[pi], acc.beta);
       ah = a * s.a_up[pi];
     }
-    acc.beta = fmaf(ah, s.bias[i / s.bias_hw], acc.beta);
+    acc.beta = fmaf(ah, s.bias[(unsigned)i / (unsigned)s.bias_hw], acc.beta);
     s.out[i * s.ldq + q] = ah;
   } else {
     acc.lin = fmaf(a, s.x0[i], acc.lin);
@@ -206,7 +206,10 @@ __device__ __forceinline__ void sink_finish(const Sink& s, const Acc& acc, long 
 // Rows +-e_j over h^(k) (j = r mod n_k, sign + for r < n_k): carried through T_k (Eq. 4) they
 // become +-(row j of W_k) over g^(k-1), with bias +-b_k[j].
 template <int MODE>
-__global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, long Q, Sink s) {
+// WT (optional, LINEAR only): the weights transposed, [in_c][out_c], so that the lanes of a
+// wave (consecutive j) read consecutive addresses.
+__global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __restrict__ WT,
+                                                      long Q, Sink s) {
   long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
   if (q >= Q) return;
   long b = q / s.R, r = q % s.R;
@@ -216,7 +219,27 @@ __global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, long Q, Sink s) 
   int hw = t.out_h * t.out_w;
   Acc acc{sgn * t.b[j / hw], 0.f, 0.f};
   if (t.kind == LIRPA_LINEAR) {
-    for (int i = 0; i < t.in_c; ++i) sink_put<MODE>(s, acc, i, sgn * t.W[j * t.in_c + i], q, b);
+    if (WT)
+      for (int i = 0; i < t.in_c; ++i)
+        sink_put<MODE>(s, acc, i, sgn * WT[(long)i * t.out_c + j], q, b);
+    else
+      for (int i = 0; i < t.in_c; ++i)
+        sink_put<MODE>(s, acc, i, sgn * t.W[j * t.in_c + i], q, b);
+  } else if (MODE == MODE_BOUND) {
+    // concretising: only the kernel window contributes
+    int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
+    int y0 = yo * t.stride - t.pad, x0 = xo * t.stride - t.pad;
+    for (int ci = 0; ci < t.in_c; ++ci)
+      for (int ky = 0; ky < t.k; ++ky) {
+        int yi = y0 + ky;
+        if (yi < 0 || yi >= t.in_h) continue;
+        for (int kx = 0; kx < t.k; ++kx) {
+          int xi = x0 + kx;
+          if (xi < 0 || xi >= t.in_w) continue;
+          float a = sgn * t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx];
+          sink_put<MODE>(s, acc, ((long)ci * t.in_h + yi) * t.in_w + xi, a, q, b);
+        }
+      }
   } else {
     int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
     int y0 = yo * t.stride - t.pad, x0 = xo * t.stride - t.pad;
@@ -231,6 +254,15 @@ __global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, long Q, Sink s) 
         }
   }
   sink_finish<MODE>(s, acc, q, b, r, true);
+}
+
+// out[i][o] = W[o][i] for a fully connected layer.
+__global__ void __launch_bounds__(kBlock) k_transpose(const float* __restrict__ W, int nout,
+                                                      int nin, float* __restrict__ out) {
+  long e = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (e >= (long)nout * nin) return;
+  long o = e / nin, i = e % nin;
+  out[i * nout + o] = W[e];
 }
 
 // Spec rows C_s over h^(L) (the property merged into the last layer): written to the slab as
@@ -717,15 +749,16 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
     L[b * n_relu + off2 + j] = v;
 }
 
-// Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q and
-// 4 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 4th tile of 32
-// output features i, K runs over o two at a time.  Epilogue as in the other stages.
+// Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q
+// and 8 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 8th tile of
+// 32 output features i, K runs over o two at a time with the A operand (W, read straight from
+// memory, L2-resident) fetched one group of 8 steps ahead.  Epilogue as in the other stages.
 template <int MODE>
-__global__ void __launch_bounds__(256) k_fcT_mfma(DLayer t, const float* __restrict__ in,
+__global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restrict__ in,
                                                   long ldq, long Q, Sink s) {
   extern __shared__ float lds[];
   float* tile = lds;                            // [out_c][32]
-  float* red = lds + (long)t.out_c * 32;        // [4][3][32]
+  float* red = lds + (long)t.out_c * 32;        // [8][3][32]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int n = lane & 31, h = lane >> 5;
   const long q0 = (long)blockIdx.x * 32;
@@ -734,22 +767,40 @@ __global__ void __launch_bounds__(256) k_fcT_mfma(DLayer t, const float* __restr
   const int nin = t.in_c, nout = t.out_c;
   for (int e = threadIdx.x; e < nout * 8; e += blockDim.x) {
     const int j4 = e & 7, o = e >> 3;
-    *reinterpret_cast<float4*>(tile + o * 32 + j4 * 4) =
-        *reinterpret_cast<const float4*>(in + (long)o * ldq + q0 + j4 * 4);
+    *reinterpret_cast<float4v*>(tile + o * 32 + j4 * 4) =
+        *reinterpret_cast<const float4v*>(in + (long)o * ldq + q0 + j4 * 4);
   }
   __syncthreads();
   Acc sum{0.f, 0.f, 0.f};
   const int KS = (nout + 1) / 2;
+  constexpr int U = 8;
   for (int mt = wave; mt * 32 < nin; mt += nw) {
     floatx16 d;
 #pragma unroll
     for (int r = 0; r < 16; ++r) d[r] = 0.f;
     const int ia = mt * 32 + (lane & 31);
-    for (int k = 0; k < KS; ++k) {
-      const int o = 2 * k + h;
-      const float a = (o < nout && ia < nin) ? t.W[(long)o * nin + ia] : 0.f;
-      const float bv = o < nout ? tile[o * 32 + n] : 0.f;
-      d = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, d, 0, 0, 0);
+    const bool iok = ia < nin;
+    float an[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int o = 2 * u + h;
+      an[u] = (o < nout && iok) ? t.W[(long)o * nin + ia] : 0.f;
+    }
+    for (int k0 = 0; k0 < KS; k0 += U) {
+      float a[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) a[u] = an[u];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int o = 2 * (k0 + U + u) + h;
+        an[u] = (o < nout && iok) ? t.W[(long)o * nin + ia] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int o = 2 * (k0 + u) + h;
+        const float bv = o < nout ? tile[o * 32 + n] : 0.f;
+        d = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u], bv, d, 0, 0, 0);
+      }
     }
     if (q < Q) {
 #pragma unroll
@@ -970,6 +1021,7 @@ struct Plan {
   // mode 1 (gradient): tape[k][m] holds, for pass k, the coefficients over g^(m) before their
   // relaxation (m >= 1) and over x (m = 0), [n_m][qp_k]; adjoints; row weights; forward slabs.
   size_t off_tape[kMaxLayers + 1][kMaxLayers + 1] = {};
+  size_t off_wT[kMaxLayers + 1] = {};  // transposed FC weights of layers 2..L-1 (0 = none)
   size_t off_ga = 0, off_gl = 0, off_gu = 0, off_w = 0, off_za = 0, off_zb = 0, off_G = 0;
   size_t off_lbt = 0, off_grad = 0;
   long fwd_floats = 0;
@@ -1036,6 +1088,11 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
   p.off_slab0 = o; o = align256(o + (size_t)slab * 4);
   p.off_slab1 = o; o = align256(o + (size_t)slab * 4);
+  for (int k = 2; k <= L - 1; ++k)
+    if (net->T[k - 1].kind == LIRPA_LINEAR) {
+      p.off_wT[k] = o;
+      o = align256(o + (size_t)net->n[k] * net->n[k - 1] * 4);
+    }
   if (mode == 1) {
     long fwd = 0;
     for (int k = 2; k <= L; ++k) {
@@ -1137,9 +1194,9 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
   const unsigned nblk32 = (unsigned)((Q + 31) / 32);
   if (t.kind == LIRPA_LINEAR) {
     if (t.out_c <= 448) {
-      size_t lds = ((size_t)t.out_c * 32 + 4 * 3 * 32) * sizeof(float);
+      size_t lds = ((size_t)t.out_c * 32 + 8 * 3 * 32) * sizeof(float);
       return launch_k(tag((std::string("fcT") + sfx).c_str(), m, pass), st, [&] {
-        hipLaunchKernelGGL(k_fcT_mfma<MODE>, dim3(nblk32), dim3(256), lds, st, t, in, ldq, Q, s);
+        hipLaunchKernelGGL(k_fcT_mfma<MODE>, dim3(nblk32), dim3(512), lds, st, t, in, ldq, Q, s);
       });
     }
     return launch_k(tag((std::string("fcT_lane") + sfx).c_str(), m, pass), st, [&] {
@@ -1291,9 +1348,10 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     }
     Sink s = slab_sink(c, k - 1, at<float>(c.ws, c.p->off_slab0), ldq, R);
     s.tape = tape_of(c, k, k - 1);
+    const float* wT = c.p->off_wT[k] ? at<float>(c.ws, c.p->off_wT[k]) : nullptr;
     if (int e = launch_k(tag("init_rows", k, k), c.st, [&] {
           hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
-                             dlayer(net->T[k - 1]), Q, s);
+                             dlayer(net->T[k - 1]), wT, Q, s);
         }))
       return e;
     if (int e = run_stages(c, k, k - 1, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
@@ -1327,10 +1385,23 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
   s.hi = l1u1 + n1;
   s.bstride = 0;
   s.n_half = n1;
-  return launch_k(tag("init_rows_bound", 1, 1), st, [&] {
-    hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
-                       dlayer(net->T[0]), Q, s);
-  });
+  if (int e = launch_k(tag("init_rows_bound", 1, 1), st, [&] {
+        hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
+                           dlayer(net->T[0]), (const float*)nullptr, Q, s);
+      }))
+    return e;
+  // transposed weights of the fully connected layers that start an intermediate pass
+  for (int k = 2; k <= net->L - 1; ++k) {
+    if (!p.off_wT[k]) continue;
+    const lirpa_layer& t = net->T[k - 1];
+    long nel = (long)t.out_c * t.in_c;
+    if (int e = launch_k("transpose", st, [&] {
+          hipLaunchKernelGGL(k_transpose, grid_for(nel), dim3(kBlock), 0, st, t.W, t.out_c,
+                             t.in_c, at<float>(ws, p.off_wT[k]));
+        }))
+      return e;
+  }
+  return LIRPA_OK;
 }
 
 // Gradient of J_b = sum_s lb[b][s] with respect to alpha for every sub-domain of the chunk,
