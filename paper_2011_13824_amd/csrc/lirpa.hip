@@ -130,6 +130,8 @@ DLayer dlayer(const lirpa_layer& t) {
 
 enum { MODE_SLAB = 0, MODE_BOUND = 1 };
 
+typedef float float4v __attribute__((ext_vector_type(4)));
+
 // Where a stage's output row goes.
 //  MODE_SLAB : coefficients over g^(m) are relaxed with layer m's (a_lo, a_up, b_up) of the
 //              row's sub-domain (Eq. 6: non-negative entries take the lower line, negative ones
@@ -256,6 +258,57 @@ __global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __r
   sink_finish<MODE>(s, acc, q, b, r, true);
 }
 
+// Pass initialisation for the rows +-e_j of a fully connected layer k, relaxed onto ReLU layer
+// k-1 (slab sink).  Block: 64 rows x 4 waves; each wave covers a quarter of the coefficients
+// (float4 parameter loads), and the rows' bias terms are summed through LDS in a fixed order.
+__global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __restrict__ WT,
+                                                      long Q, Sink s) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long q = blockIdx.x * 64L + lane;
+  const bool ok = q < Q;
+  const long qq = ok ? q : 0;
+  const long b = qq / s.R, r = qq % s.R;
+  const int nk = t.out_c, nin = t.in_c;
+  const int j = (int)(r % nk);
+  const float sgn = r < nk ? 1.f : -1.f;
+  const int chunk = ((nin + 15) / 16) * 4;
+  const int i0 = w * chunk, i1 = min(nin, i0 + chunk);
+  const long pb = b * s.pstride;
+  const unsigned hw = (unsigned)s.bias_hw;
+  float beta = 0.f;
+  if (ok) {
+    int i = i0;
+    for (; i + 4 <= i1; i += 4) {
+      const float4v lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + i);
+      const float4v up = *reinterpret_cast<const float4v*>(s.a_up + pb + i);
+      const float4v bu = *reinterpret_cast<const float4v*>(s.b_up + pb + i);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float a = sgn * WT[(long)(i + u) * nk + j];
+        const long idx = (long)(i + u) * s.ldq + q;
+        if (s.tape) s.tape[idx] = a;
+        const float ah = a >= 0.f ? a * lo[u] : a * up[u];
+        beta = fmaf(fminf(a, 0.f), bu[u], beta);
+        beta = fmaf(ah, s.bias[(unsigned)(i + u) / hw], beta);
+        s.out[idx] = ah;
+      }
+    }
+    for (; i < i1; ++i) {
+      const float a = sgn * WT[(long)i * nk + j];
+      const long idx = (long)i * s.ldq + q;
+      if (s.tape) s.tape[idx] = a;
+      const float ah = a >= 0.f ? a * s.a_lo[pb + i] : a * s.a_up[pb + i];
+      beta = fmaf(fminf(a, 0.f), s.b_up[pb + i], beta);
+      beta = fmaf(ah, s.bias[(unsigned)i / hw], beta);
+      s.out[idx] = ah;
+    }
+  }
+  red[w][lane] = beta;
+  __syncthreads();
+  if (w == 0 && ok) s.beta[q] = sgn * t.b[j] + ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
 // out[i][o] = W[o][i] for a fully connected layer.
 __global__ void __launch_bounds__(kBlock) k_transpose(const float* __restrict__ W, int nout,
                                                       int nin, float* __restrict__ out) {
@@ -342,7 +395,6 @@ __global__ void __launch_bounds__(kBlock) k_convT(DLayer t, const float* __restr
 // B[l/32][l%32]; accumulator register r of lane l holds D[8(r/4) + 4(l/32) + r%4][l%32].
 // ---------------------------------------------------------------------------------------------
 typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef float float4v __attribute__((ext_vector_type(4)));
 
 // Reduce (beta, lin, l1) of the two lane halves and of the waves of the block, then finish the
 // rows q0..q0+31.  red: LDS scratch of nw*3*32 floats.
@@ -1350,8 +1402,12 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     s.tape = tape_of(c, k, k - 1);
     const float* wT = c.p->off_wT[k] ? at<float>(c.ws, c.p->off_wT[k]) : nullptr;
     if (int e = launch_k(tag("init_rows", k, k), c.st, [&] {
-          hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
-                             dlayer(net->T[k - 1]), wT, Q, s);
+          if (wT)
+            hipLaunchKernelGGL(k_init_fc_rows, dim3((unsigned)((Q + 63) / 64)), dim3(256), 0,
+                               c.st, dlayer(net->T[k - 1]), wT, Q, s);
+          else
+            hipLaunchKernelGGL(k_init_rows<MODE_SLAB>, grid_for(Q), dim3(kBlock), 0, c.st,
+                               dlayer(net->T[k - 1]), wT, Q, s);
         }))
       return e;
     if (int e = run_stages(c, k, k - 1, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
