@@ -140,6 +140,10 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 //  MODE_BOUND: coefficients over the input x are concretised (Eq. 8):
 //              value = A x0 - eps ||A||_1 + beta; row r < n_half goes to lo[b*bstride + r],
 //              a row r >= n_half to hi[b*bstride + r - n_half] negated (an upper bound).
+//              When x0 is null the linear term is already in beta: with A = A1 W1 (A1 the
+//              relaxed coefficients over h^(1)), A x0 + A1 b1 = A1 (W1 x0 + b1), so the
+//              relaxation onto layer 1 dots A1 with z1 = W1 x0 + b1 instead of with b1
+//              (bias_hw == 1 then means a per-neuron bias vector).
 struct Sink {
   float* out;
   long ldq;
@@ -180,7 +184,7 @@ __device__ __forceinline__ void sink_put(const Sink& s, Acc& acc, long i, float 
     acc.beta = fmaf(ah, s.bias[(unsigned)i / (unsigned)s.bias_hw], acc.beta);
     s.out[i * s.ldq + q] = ah;
   } else {
-    acc.lin = fmaf(a, s.x0[i], acc.lin);
+    if (s.x0) acc.lin = fmaf(a, s.x0[i], acc.lin);
     acc.l1 += fabsf(a);
   }
 }
@@ -307,6 +311,32 @@ __global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __r
   red[w][lane] = beta;
   __syncthreads();
   if (w == 0 && ok) s.beta[q] = sgn * t.b[j] + ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+// z1 = W1 x0 + b1: the layer-1 pre-activation at the box centre.
+__global__ void __launch_bounds__(kBlock) k_layer1_at_x0(DLayer t, const float* __restrict__ x0,
+                                                         float* __restrict__ z) {
+  long j = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  const int hw = t.out_h * t.out_w;
+  if (j >= (long)t.out_c * hw) return;
+  float a = t.b[j / hw];
+  if (t.kind == LIRPA_LINEAR) {
+    for (int i = 0; i < t.in_c; ++i) a = fmaf(t.W[j * t.in_c + i], x0[i], a);
+  } else {
+    int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
+    for (int ci = 0; ci < t.in_c; ++ci)
+      for (int ky = 0; ky < t.k; ++ky) {
+        int yi = yo * t.stride - t.pad + ky;
+        if (yi < 0 || yi >= t.in_h) continue;
+        for (int kx = 0; kx < t.k; ++kx) {
+          int xi = xo * t.stride - t.pad + kx;
+          if (xi < 0 || xi >= t.in_w) continue;
+          a = fmaf(t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx],
+                   x0[((long)ci * t.in_h + yi) * t.in_w + xi], a);
+        }
+      }
+  }
+  z[j] = a;
 }
 
 // out[i][o] = W[o][i] for a fully connected layer.
@@ -459,10 +489,12 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   const unsigned b = qok ? q / (unsigned)s.R : 0u;
   float* red = xs + (MODE == MODE_BOUND ? t.in_c * H0 * W0 : 0);  // [NW][3][16]
 
-  if constexpr (MODE == MODE_BOUND) {
+  const bool with_x0 = MODE == MODE_BOUND && s.x0 != nullptr;
+  if (with_x0) {
     const int nx = t.in_c * H0 * W0;
     for (int e = threadIdx.x; e < nx; e += NT) xs[e] = s.x0[e];
   }
+  const bool zvec = MODE == MODE_SLAB && s.bias_hw == 1;  // per-neuron bias (z1)
 
   // A operands, one set per rotation phase: slot (M/4, M%4) of lane l (M = l%16) takes tap
   // ((M/4 - ph*S) mod K, M%4) of co = 4*ks + l/16
@@ -495,21 +527,31 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
     if (!cok[c] || !qok || y < 0 || y >= H0) return;
     const unsigned rowi = ((unsigned)cis[c] * H0 + y) * W0;
     if constexpr (MODE == MODE_BOUND) {
+      if (with_x0) {
 #pragma unroll
-      for (int x = 0; x < W0; ++x) {
-        const float a = vals[x];
-        if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = a;
-        lin = fmaf(a, xs[rowi + x], lin);
-        l1 += fabsf(a);
+        for (int x = 0; x < W0; ++x) {
+          const float a = vals[x];
+          if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = a;
+          lin = fmaf(a, xs[rowi + x], lin);
+          l1 += fabsf(a);
+        }
+      } else {
+#pragma unroll
+        for (int x = 0; x < W0; ++x) {
+          if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = vals[x];
+          l1 += fabsf(vals[x]);
+        }
       }
     } else {
       const long pb = (long)b * s.pstride + rowi;
-      const float bias_c = s.bias[cis[c]];
+      const float bias_c = zvec ? 0.f : s.bias[cis[c]];
 #pragma unroll
       for (int x4 = 0; x4 < W0; x4 += 4) {
         const float4v lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + x4);
         const float4v up = *reinterpret_cast<const float4v*>(s.a_up + pb + x4);
         const float4v bu = *reinterpret_cast<const float4v*>(s.b_up + pb + x4);
+        float4v bz = {bias_c, bias_c, bias_c, bias_c};
+        if (zvec) bz = *reinterpret_cast<const float4v*>(s.bias + rowi + x4);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const float a = vals[x4 + j];
@@ -517,7 +559,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
           if constexpr (TAPE) s.tape[idx] = a;
           const float ah = a >= 0.f ? a * lo[j] : a * up[j];
           beta = fmaf(fminf(a, 0.f), bu[j], beta);
-          beta = fmaf(ah, bias_c, beta);
+          beta = fmaf(ah, bz[j], beta);
           s.out[idx] = ah;
         }
       }
@@ -658,7 +700,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 template <int K1, int S1, int P1, int K2, int C1, int NW>
 __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
-               const float* __restrict__ x0, float eps, float* __restrict__ L,
+               const float* __restrict__ z1, float eps, float* __restrict__ L,
                float* __restrict__ U, long n_relu, long off2) {
   static_assert(C1 % 4 == 0 && K1 <= 4 && K2 <= 4, "unsupported geometry");
   constexpr int KS = C1 / 4;
@@ -700,10 +742,12 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       float v = 0.f;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
         const float w = sgn * t2.W[(((long)c2 * t2.in_c + c1) * t2.k + ky2) * t2.k + kx2];
-        const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
+        const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
+        const long pi = pb + ni;
         v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
         bpart = fmaf(fminf(w, 0.f), b_up[pi], bpart);
-        bpart = fmaf(v, t1.b[c1], bpart);
+        // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
+        bpart = fmaf(v, z1[ni], bpart);
       }
       tile[(c1 * NPOS + pos) * 16 + row] = v;
     }
@@ -730,20 +774,22 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   }
   const int Hi = t1.in_h, Wi = t1.in_w;
   const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;  // footprint origin on the input
-  float lin = 0.f, l1 = 0.f;
+  float l1 = 0.f;
   float acc[WO];
 #pragma unroll
   for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-  auto emit = [&](int yl) {  // local footprint row yl of channel c0
+  const bool inside_x = OX >= 0 && OX + WO <= Wi;
+  auto emit = [&](int yl) {  // local footprint row yl of channel c0: ||.||_1 of the clipped row
     const int y = OY + yl;
     if (!cok || y < 0 || y >= Hi) return;
-    const float* xr = x0 + ((long)c0 * Hi + y) * Wi;
+    if (inside_x) {
 #pragma unroll
-    for (int x = 0; x < WO; ++x) {
-      const int xi = OX + x;
-      if (xi >= 0 && xi < Wi) {
-        lin = fmaf(acc[x], xr[xi], lin);
-        l1 += fabsf(acc[x]);
+      for (int x = 0; x < WO; ++x) l1 += fabsf(acc[x]);
+    } else {
+#pragma unroll
+      for (int x = 0; x < WO; ++x) {
+        const int xi = OX + x;
+        l1 += (xi >= 0 && xi < Wi) ? fabsf(acc[x]) : 0.f;
       }
     }
   };
@@ -775,25 +821,17 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   }
 
   // (3) reduce over lane groups and waves; add the bias terms; write the bound
-  lin += __shfl_xor(lin, 16, 64);
   l1 += __shfl_xor(l1, 16, 64);
-  lin += __shfl_xor(lin, 32, 64);
   l1 += __shfl_xor(l1, 32, 64);
-  if (lane < 16) {
-    red[(wave * 2 + 0) * 16 + lane] = lin;
-    red[(wave * 2 + 1) * 16 + lane] = l1;
-  }
+  if (lane < 16) red[wave * 16 + lane] = l1;
   __syncthreads();
   if (threadIdx.x >= 16) return;
   const int row = threadIdx.x;
   const int c2 = cb * 16 + row;
-  float tl = 0.f, ta = 0.f, tb = sgn * t2.b[c2];
-  for (int w = 0; w < NW; ++w) {
-    tl += red[(w * 2 + 0) * 16 + row];
-    ta += red[(w * 2 + 1) * 16 + row];
-  }
+  float ta = 0.f, tb = sgn * t2.b[c2];
+  for (int w = 0; w < NW; ++w) ta += red[w * 16 + row];
   for (int r = 0; r < RPT; ++r) tb += bred[r * 16 + row];
-  const float v = tl - eps * ta + tb;
+  const float v = tb - eps * ta;
   const long j = ((long)c2 * H2 + y2) * W2 + x2;
   if (sgn_neg)
     U[b * n_relu + off2 + j] = -v;
@@ -1069,6 +1107,7 @@ struct Plan {
   int mode = 0;
   size_t off_l = 0, off_u = 0, off_alo = 0, off_aup = 0, off_bup = 0, off_code = 0;
   size_t off_l1u1 = 0, off_slab0 = 0, off_slab1 = 0, off_beta = 0, total = 0;
+  size_t off_z1 = 0;  // W1 x0 + b1
   long slab_floats = 0, qp_max = 0;
   // mode 1 (gradient): tape[k][m] holds, for pass k, the coefficients over g^(m) before their
   // relaxation (m >= 1) and over x (m = 0), [n_m][qp_k]; adjoints; row weights; forward slabs.
@@ -1137,6 +1176,7 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   p.off_bup = o;  o = align256(o + perp * 4);
   p.off_code = o; o = align256(o + per);
   p.off_l1u1 = o; o = align256(o + 2 * (size_t)net->n[1] * 4);
+  p.off_z1 = o;   o = align256(o + (size_t)net->n[1] * 4);
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
   p.off_slab0 = o; o = align256(o + (size_t)slab * 4);
   p.off_slab1 = o; o = align256(o + (size_t)slab * 4);
@@ -1297,8 +1337,13 @@ Sink slab_sink(const Chunk& c, int m, float* out, long ldq, long R) {
   s.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[m];
   s.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[m];
   s.pstride = net->pstride;
-  s.bias = t.b;
-  s.bias_hw = t.out_h * t.out_w;
+  if (m == 1) {
+    s.bias = at<float>(c.ws, c.p->off_z1);  // layer-1 bias + linear term of the bound
+    s.bias_hw = 1;
+  } else {
+    s.bias = t.b;
+    s.bias_hw = t.out_h * t.out_w;
+  }
   s.beta = at<float>(c.ws, c.p->off_beta);
   s.R = R;
   return s;
@@ -1306,7 +1351,8 @@ Sink slab_sink(const Chunk& c, int m, float* out, long ldq, long R) {
 
 Sink bound_sink(const Chunk& c, long R, float* lo, float* hi, long bstride, long n_half) {
   Sink s{};
-  s.x0 = c.x0;
+  // with a ReLU layer in front of T_1 the linear term was folded into the layer-1 bias (z1)
+  s.x0 = c.net->L >= 2 ? nullptr : c.x0;
   s.eps = c.eps;
   s.beta = at<float>(c.ws, c.p->off_beta);
   s.R = R;
@@ -1370,8 +1416,8 @@ int pass2_window(const Chunk& c) {
   const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
   return launch_k(tag("pass2_window", 1, 2), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * nw), 0, c.st, dlayer(t1),
-                       dlayer(t2), c.nb, alo, aup, bup, net->pstride, c.x0, c.eps, c.L, c.U,
-                       net->n_relu, net->off[2]);
+                       dlayer(t2), c.nb, alo, aup, bup, net->pstride,
+                       at<float>(c.ws, c.p->off_z1), c.eps, c.L, c.U, net->n_relu, net->off[2]);
   });
 }
 
@@ -1444,6 +1490,11 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
   if (int e = launch_k(tag("init_rows_bound", 1, 1), st, [&] {
         hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
                            dlayer(net->T[0]), (const float*)nullptr, Q, s);
+      }))
+    return e;
+  if (int e = launch_k("layer1_at_x0", st, [&] {
+        hipLaunchKernelGGL(k_layer1_at_x0, grid_for(n1), dim3(kBlock), 0, st, dlayer(net->T[0]),
+                           x0, at<float>(ws, p.off_z1));
       }))
     return e;
   // transposed weights of the fully connected layers that start an intermediate pass
