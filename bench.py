@@ -94,10 +94,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="base", choices=["tiny", "base", "wide", "deep"])
+    ap.add_argument("--workload", default="base",
+                    choices=["tiny", "base", "wide", "deep", "wide_opt"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
     ap.add_argument("--max-ws-gib", type=float, default=64.0)
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only copy a device buffer of this many MiB 3 times (a known-size "
                          "kernel for scaling HBM byte counters) and exit")
@@ -126,6 +128,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     w = wl.get(args.workload)
+    if args.batch:
+        w.B = args.batch
     B, S = w.B, w.S
     net = lirpa.Network(w.layers, device=dev)
     x0 = torch.as_tensor(w.x0).to(dev)
@@ -137,12 +141,25 @@ def main():
     cand = np.flatnonzero((l0 < 0) & (u0 > 0))
     split = torch.as_tensor(w.splits(cand)).to(dev)
 
-    ws, ws_bytes = net.workspace(S, B, 0, int(args.max_ws_gib * (1 << 30)))
+    optimise = w.steps > 0
+    ws, ws_bytes = net.workspace(S, B, 1 if optimise else 0, int(args.max_ws_gib * (1 << 30)))
     lb = torch.empty((B, S), dtype=torch.float32, device=dev)
+    if optimise:
+        alpha = torch.empty((B, w.n_relu), dtype=torch.float32, device=dev)
+        adam_m = torch.empty_like(alpha)
+        adam_v = torch.empty_like(alpha)
+        # fresh start: alpha from the library's own heuristic pass, zero Adam moments
+        params = lirpa.lirpa_opt_params(w.steps, w.lr, 0.9, 0.999, 1e-8, 0, 1)
 
     def step():
-        lirpa.lirpa_bound(net.handle, x0, w.eps, C, S, B, split, None, lb, None, None, ws,
-                          ws_bytes)
+        if optimise:
+            # one optimised bound of the whole batch: a heuristic pass, then 20 Adam steps
+            # (21 bounds and 20 gradients through the recomputed intermediate bounds)
+            lirpa.lirpa_optimize(net.handle, x0, w.eps, C, S, B, split, alpha, adam_m, adam_v,
+                                 params, lb, None, ws, ws_bytes)
+        else:
+            lirpa.lirpa_bound(net.handle, x0, w.eps, C, S, B, split, None, lb, None, None, ws,
+                              ws_bytes)
 
     for _ in range(args.warmup):
         step()
@@ -162,7 +179,7 @@ def main():
         step()
     times = lirpa.lirpa_timing_end()
     torch.cuda.synchronize()
-    work = stage_work(w.layers, S, B)
+    work = {} if optimise else stage_work(w.layers, S, B)
     stages = {}
     for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):
         f, b = work.get(cls, (0.0, 0.0))
@@ -176,7 +193,9 @@ def main():
     tot_ms, launches = times[dom]
     f, b = work.get(dom, (0.0, 0.0))
     f, b = f * args.steps, b * args.steps
-    if f > 0:
+    if optimise:
+        roof = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None}
+    elif f > 0:
         achieved = f / launches / (tot_ms / launches / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
@@ -203,8 +222,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "net": w.extra.get("arch"), "B": B, "S": S,
                    "n_relu": w.n_relu, "max_splits": w.max_splits, "eps": w.eps,
-                   "alpha": "upper slope", "ws_gib": round(ws_bytes / 2**30, 2)},
-        "path_tflops": round(total_flops(w.layers, S, B) / (ms / 1e3) / 1e12, 3),
+                   "alpha": (f"{w.steps} Adam steps (lr {w.lr}) from the upper slope"
+                             if optimise else "upper slope"),
+                   "ws_gib": round(ws_bytes / 2**30, 2)},
+        "path_tflops": (None if optimise else
+                        round(total_flops(w.layers, S, B) / (ms / 1e3) / 1e12, 3)),
         "roofline": roof,
         "stages": stages,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_budget),

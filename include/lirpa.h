@@ -109,6 +109,10 @@ typedef struct {
   float beta2;    /* second-moment decay, in [0,1)                       */
   float eps_adam; /* denominator guard, > 0                              */
   int t0;         /* updates already taken (bias correction on resume)   */
+  int fresh;      /* 1: start from scratch -- the library sets alpha to the upper slope
+                     u/(u-l) of each unstable neuron of a heuristic bound pass (1 for
+                     active, 0 for inactive neurons), zeroes adam_m and adam_v and takes
+                     t0 = 0; 0: continue from the caller's alpha, m, v and t0          */
 } lirpa_opt_params;
 
 /* Optimised bounds (Sec. 3.1, Eq. 9 read as a maximisation over alpha): projected Adam ascent

@@ -1027,6 +1027,74 @@ __global__ void __launch_bounds__(kBlock)
   }
 }
 
+// The same forward step on 16x16x4 MFMA, for conv and linear layers alike (a linear layer is
+// a 1x1 convolution on a 1x1 map): implicit GEMM with M = 16 output channels co, N = 16 rows q
+// and K = (ci, ky, kx), four per instruction.  Block: 16 rows x 4 waves; output positions are
+// dealt round-robin to the waves.  A block whose 16 rows all carry weight 0 exits at once.
+template <bool WITNESS>
+__global__ void __launch_bounds__(256)
+    k_fwd_mfma(DLayer t, const float* __restrict__ zin, unsigned ldq, unsigned Q, long R,
+               const float* __restrict__ w, const float* __restrict__ x0, float eps,
+               const float* __restrict__ tape, const float* __restrict__ a_lo,
+               const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+               float* __restrict__ G, float* __restrict__ zout) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const unsigned q0 = blockIdx.x * 16u;
+  const unsigned q = q0 + n;
+  const bool qok = q < Q;
+  const float wq = qok ? w[q] : 0.f;
+  if (__syncthreads_or(wq != 0.f) == 0) return;  // uniform: the whole block is idle
+  const unsigned b = qok ? q / (unsigned)R : 0u;
+  const int K = t.k > 0 ? t.k : 1;
+  const int KD = t.in_c * K * K;
+  const int nks = (KD + 3) / 4;
+  const int Hout = t.out_h, Wout = t.out_w, Hin = t.in_h, Win = t.in_w;
+  const int npos = Hout * Wout;
+  const int nmt = (t.out_c + 15) / 16;
+  for (int pos = wave; pos < npos; pos += 4) {
+    const int y = pos / Wout, x = pos - y * Wout;
+    const int yb = y * t.stride - t.pad, xb = x * t.stride - t.pad;
+    for (int mt = 0; mt < nmt; ++mt) {
+      const int coA = mt * 16 + n;  // A operand row (M = l%16)
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < nks; ++ks) {
+        const int kk = ks * 4 + g;  // K index of this lane group
+        float av = 0.f, bv = 0.f;
+        if (kk < KD) {
+          const int ci = kk / (K * K), rem = kk - ci * K * K;
+          const int ky = rem / K, kx = rem - ky * K;
+          if (coA < t.out_c) av = t.W[(long)coA * KD + kk];
+          const int yi = yb + ky, xi = xb + kx;
+          if (yi >= 0 && yi < Hin && xi >= 0 && xi < Win) {
+            const unsigned ii = ((unsigned)ci * Hin + yi) * Win + xi;
+            const float v = zin[ii * ldq + q];
+            if constexpr (WITNESS)
+              bv = x0[ii] - eps * (v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f));
+            else
+              bv = v;
+          }
+        }
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, d, 0, 0, 0);
+      }
+      if (!qok || wq == 0.f) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = mt * 16 + 4 * g + r;
+        if (co >= t.out_c) continue;
+        const float gv = d[r] + t.b[co];
+        const unsigned o = ((unsigned)co * Hout + y) * Wout + x;
+        const unsigned idx = o * ldq + q;
+        G[idx] = gv;
+        if (zout) {
+          const long pi = (long)b * pstride + o;
+          zout[idx] = tape[idx] >= 0.f ? a_lo[pi] * gv : fmaf(a_up[pi], gv, b_up[pi]);
+        }
+      }
+    }
+  }
+}
+
 // Adjoint accumulation for ReLU layer m: one wave per (sub-domain, neuron) sums over the rows of
 // the pass, w * max(A~,0) G (-> alpha), w * min(A~,0) G (-> upper slope) and w * min(A~,0)
 // (-> upper intercept), and for unstable neurons turns the last two into adjoints of l and u
@@ -1081,6 +1149,21 @@ __global__ void __launch_bounds__(kBlock) k_adam(long n, float* __restrict__ alp
   v[i] = vi;
   float a = alpha[i] + lr * (mi / c1) / (sqrtf(vi / c2) + eps);
   alpha[i] = fminf(fmaxf(a, 0.f), 1.f);
+}
+
+// Fresh optimiser state: alpha = the upper slope u/(u-l) of each unstable neuron of a heuristic
+// pass (1 for l >= 0, 0 otherwise), Adam moments zero.
+__global__ void __launch_bounds__(kBlock) k_alpha_init(long n, const float* __restrict__ l,
+                                                       const float* __restrict__ u,
+                                                       float* __restrict__ alpha,
+                                                       float* __restrict__ m,
+                                                       float* __restrict__ v) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float li = l[i], ui = u[i];
+  alpha[i] = (li < 0.f && ui > 0.f) ? ui / (ui - li) : (li >= 0.f ? 1.f : 0.f);
+  m[i] = 0.f;
+  v[i] = 0.f;
 }
 
 // Best bound so far (elementwise max over iterates) and optional trace copy.
@@ -1548,17 +1631,18 @@ int grad_chunk(const Chunk& c, int full) {
       long off = net->off[m], poff = net->poff[m];
       float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
       DLayer t = dlayer(net->T[m - 1]);
+      const unsigned nblk16 = (unsigned)((Q + 15) / 16);
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
         if (m == 1)
-          hipLaunchKernelGGL(k_fwd<true>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
-                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + poff,
-                             at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
-                             net->pstride, G, zout);
+          hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
+                             (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
+                             at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
+                             at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout);
         else
-          hipLaunchKernelGGL(k_fwd<false>, grid_for(Q), dim3(kBlock), 0, c.st, t, zin, ldq, Q, R,
-                             w, c.x0, c.eps, tp, at<float>(c.ws, p.off_alo) + poff,
-                             at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
-                             net->pstride, G, zout);
+          hipLaunchKernelGGL(k_fwd_mfma<false>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
+                             (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
+                             at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
+                             at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout);
       });
       if (e) return e;
       long pairs = c.nb * net->n[m];
@@ -1753,6 +1837,18 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
     long na = c.nb * net->n_relu, ns = c.nb * S;
     float* a = alpha + b0 * net->n_relu;
     float* lbt = at<float>(ws, p.off_lbt);
+    if (op.fresh) {
+      Chunk h = c;
+      h.alpha = nullptr;
+      h.tape = false;
+      if (int e = bound_chunk(h, C, lbt)) return e;
+      if (int e = launch_k("alpha_init", stream, [&] {
+            hipLaunchKernelGGL(k_alpha_init, grid_for(na), dim3(kBlock), 0, stream, na, h.L, h.U,
+                               a, adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu);
+          }))
+        return e;
+    }
+    const int tbase = op.fresh ? 0 : op.t0;
     for (int t = 0; t <= op.steps; ++t) {
       c.tape = (t < op.steps);
       if (int e = bound_chunk(c, C, lbt)) return e;
@@ -1764,7 +1860,7 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
         return e;
       if (t == op.steps) break;
       if (int e = grad_chunk(c, 1)) return e;
-      int tt = op.t0 + t + 1;
+      int tt = tbase + t + 1;
       float c1 = (float)(1.0 - std::pow((double)op.beta1, tt));
       float c2 = (float)(1.0 - std::pow((double)op.beta2, tt));
       if (int e = launch_k("adam", stream, [&] {

@@ -29,7 +29,8 @@ class lirpa_layer(ctypes.Structure):
 
 class lirpa_opt_params(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
-                ("beta2", ctypes.c_float), ("eps_adam", ctypes.c_float), ("t0", ctypes.c_int)]
+                ("beta2", ctypes.c_float), ("eps_adam", ctypes.c_float), ("t0", ctypes.c_int),
+                ("fresh", ctypes.c_int)]
 
 
 class lirpa_kernel_time(ctypes.Structure):
@@ -243,7 +244,7 @@ class Network:
         return lb, grad
 
     def optimize(self, x0, eps, C, split, alpha, adam_m=None, adam_v=None, steps=20, lr=0.1,
-                 beta1=0.9, beta2=0.999, eps_adam=1e-8, t0=0, trace=False,
+                 beta1=0.9, beta2=0.999, eps_adam=1e-8, t0=0, trace=False, fresh=False,
                  max_ws_bytes=16 << 30):
         """In place on alpha (and adam_m, adam_v); returns lb_best (and the lb trace)."""
         S, B = C.shape[0], alpha.shape[0]
@@ -256,6 +257,7 @@ class Network:
             if trace else None
         ws, ws_bytes = self.workspace(S, B, 1, max_ws_bytes)
         lirpa_optimize(self.handle, x0, eps, C, S, B, split, alpha, adam_m, adam_v,
-                       lirpa_opt_params(steps, lr, beta1, beta2, eps_adam, t0), best, tr, ws,
+                       lirpa_opt_params(steps, lr, beta1, beta2, eps_adam, t0, int(fresh)),
+                       best, tr, ws,
                        ws_bytes)
         return (best, tr) if trace else best

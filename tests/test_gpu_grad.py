@@ -32,11 +32,39 @@ def check_bound(name, got, want):
     assert np.all(excess <= 0), f"{name}: bound off by {excess.max():.3g} beyond tolerance"
 
 
-def check_grad(name, got, want, split):
+def one_sided(rnet, x0, eps, C, split, alpha, b, j, h=1e-5):
+    """Oracle (fp64) left and right derivatives of sum_s lb[b] in alpha[b, j]."""
+    a = alpha[b:b + 1].astype(np.float32)
+    sp = None if split is None else split[b:b + 1]
+    base = ref.bound(rnet, x0, eps, C, sp, a)[0].sum()
+    ap, am = a.copy(), a.copy()
+    ap[0, j] += np.float32(h)
+    am[0, j] -= np.float32(h)
+    right = (ref.bound(rnet, x0, eps, C, sp, ap)[0].sum() - base) / (
+        np.float64(ap[0, j]) - np.float64(a[0, j]))
+    left = (base - ref.bound(rnet, x0, eps, C, sp, am)[0].sum()) / (
+        np.float64(a[0, j]) - np.float64(am[0, j]))
+    return left, right
+
+
+def check_grad(name, got, want, split, kink=None, max_kinks=8):
+    """Normwise gate ||g_gpu - g_ref||_inf <= 1e-4 (1 + ||g_ref||_inf) per sub-domain.
+
+    The bound is piecewise smooth: where an entry of A_x is within rounding of zero, fp32 and
+    fp64 can pick different witness vertices, and both gradients are valid subgradients.  An
+    entry outside the gate must then lie (within the same tolerance) between the oracle's own
+    left and right derivatives (kink(b, j)); at most max_kinks such entries per sub-domain."""
     for b in range(got.shape[0]):
-        ref_inf = np.abs(want[b]).max()
-        err = np.abs(got[b] - want[b]).max()
-        assert err <= 1e-4 * (1 + ref_inf), f"{name}[{b}]: |dg| {err:.3g} vs |g| {ref_inf:.3g}"
+        tol = 1e-4 * (1 + np.abs(want[b]).max())
+        bad = np.flatnonzero(np.abs(got[b] - want[b]) > tol)
+        assert len(bad) <= max_kinks, f"{name}[{b}]: {len(bad)} entries beyond tolerance"
+        for j in bad:
+            assert kink is not None, f"{name}[{b}][{j}]: {got[b, j]} vs {want[b, j]}"
+            lo, hi = sorted(kink(b, j))
+            assert lo - tol <= got[b, j] <= hi + tol, \
+                f"{name}[{b}][{j}]: {got[b, j]:.7g} outside the subgradient range [{lo:.7g}, {hi:.7g}]"
+            print(f"{name}[{b}][{j}]: kink, gpu {got[b, j]:.7g} in [{lo:.7g}, {hi:.7g}], "
+                  f"oracle {want[b, j]:.7g}", flush=True)
     print(f"{name}: max |g_gpu - g_ref| = {np.abs(got - want).max():.3g}", flush=True)
     if split is not None:
         s = split != 0
@@ -59,7 +87,8 @@ def test_grad_tiny(full):
     lb, g = net.bound_grad(dev(w.x0), w.eps, dev(w.C), dev(split), dev(alpha), full=full)
     lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, alpha, full=full)
     check_bound("tiny lb", lb.cpu().double().numpy(), lr)
-    check_grad("tiny grad", g.cpu().double().numpy(), gr, split)
+    kink = (lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, alpha, b, j)) if full else None
+    check_grad("tiny grad", g.cpu().double().numpy(), gr, split, kink)
 
 
 def test_grad_small_conv():
@@ -71,7 +100,8 @@ def test_grad_small_conv():
     lb, g = net.bound_grad(dev(x0), 0.05, dev(C), dev(split), dev(alpha))
     lr, gr = ref.bound_grad(rnet, x0, 0.05, C, split, alpha)
     check_bound("small lb", lb.cpu().double().numpy(), lr)
-    check_grad("small grad", g.cpu().double().numpy(), gr, split)
+    check_grad("small grad", g.cpu().double().numpy(), gr, split,
+               lambda b, j: one_sided(rnet, x0, 0.05, C, split, alpha, b, j))
 
 
 @pytest.mark.parametrize("name", ["base", "deep"])
@@ -82,7 +112,8 @@ def test_grad_conv_nets(name):
     lb, g = net.bound_grad(dev(w.x0), w.eps, dev(w.C), dev(split), dev(alpha))
     lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, alpha)
     check_bound(f"{name} lb", lb.cpu().double().numpy(), lr)
-    check_grad(f"{name} grad", g.cpu().double().numpy(), gr, split)
+    check_grad(f"{name} grad", g.cpu().double().numpy(), gr, split,
+               lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, alpha, b, j))
 
 
 def test_optimize_replay_wide():
@@ -105,7 +136,8 @@ def test_optimize_replay_wide():
         lb, g = net.bound_grad(x0, w.eps, C, sp, alpha)
         lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, a_t.astype(np.float32))
         check_bound(f"step {t} lb", lb.cpu().double().numpy(), lr)
-        check_grad(f"step {t} grad", g.cpu().double().numpy(), gr, split)
+        check_grad(f"step {t} grad", g.cpu().double().numpy(), gr, split,
+                   lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, a_t, b, j))
         if lb0 is None:
             lb0 = lb.cpu().double().numpy()
         best = net.optimize(x0, w.eps, C, sp, alpha, m, v, steps=1, lr=0.1, t0=t)
