@@ -839,6 +839,227 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
     L[b * n_relu + off2 + j] = v;
 }
 
+// Reverse sweep of the receptive-field pass 2.  Layer-1 bounds do not depend on alpha, so the
+// rows of pass 2 only feed d J / d alpha of the layer-1 neurons of their own window:
+// sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
+// the layer-1 relaxation and G_r the layer-1 pre-activation at the row's witness
+// x* = x0 + delta, delta = -eps sign(A_x) (zero outside the footprint), i.e.
+// G_r = z1 + W_1 delta over the window.  One block per 16 rows sharing a window (as in
+// k_pass2_window): it rebuilds the relaxed patch and A_x over the footprint on MFMA, keeps delta
+// in LDS, runs the layer-1 forward over the window on MFMA, reduces the 16 rows' contributions
+// per window neuron and writes them to part[block][c1][pos].  Row weights: w = g_l (sign +) or
+// -g_u (sign -) of the row's layer-2 neuron.
+template <int K1, int S1, int P1, int K2, int C1, int NW>
+__global__ void __launch_bounds__(64 * NW)
+    k_pass2_window_grad(DLayer t1, DLayer t2, const float* __restrict__ a_lo,
+                        const float* __restrict__ a_up, long pstride, float eps,
+                        const float* __restrict__ gl, const float* __restrict__ gu,
+                        const int8_t* __restrict__ code1, long n_relu, long off2,
+                        const float* __restrict__ z1, float* __restrict__ part) {
+  static_assert(C1 % 4 == 0 && C1 <= 16 && K1 == 4, "unsupported geometry");
+  constexpr int KS = C1 / 4;
+  constexpr int NT = 64 * NW;
+  constexpr int NPOS = K2 * K2;
+  constexpr int WO = (K2 - 1) * S1 + K1;
+  constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int NEL = C1 * NPOS * 16;
+  __shared__ float tile[NEL];
+  __shared__ float dl[NW * WO * WO * 16];  // delta over the footprint, [c0][fy][fx][row]
+  __shared__ float wrow[16];
+  __shared__ int active;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, G = lane >> 4;
+  const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
+  const int ncb = C2 / 16;
+  long blk = blockIdx.x;
+  const long blk_id = blk;
+  const int x2 = (int)(blk % W2); blk /= W2;
+  const int y2 = (int)(blk % H2); blk /= H2;
+  const int cb = (int)(blk % ncb); blk /= ncb;
+  const int sgn_neg = (int)(blk % 2); blk /= 2;
+  const long b = blk;
+  const float sgn = sgn_neg ? -1.f : 1.f;
+  const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;
+  const int H1 = t1.out_h, Wd1 = t1.out_w;
+  float* out = part + blk_id * (long)(C1 * NPOS);
+
+  if (threadIdx.x < 16) {
+    const int c2 = cb * 16 + threadIdx.x;
+    const long j = ((long)c2 * H2 + y2) * W2 + x2;
+    const float wv = sgn_neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
+    wrow[threadIdx.x] = wv;
+  }
+  if (threadIdx.x == 0) active = 0;
+  __syncthreads();
+  if (threadIdx.x < 16 && wrow[threadIdx.x] != 0.f) active = 1;
+  __syncthreads();
+  if (!active) {  // no row of this block carries weight: zero contributions
+    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) out[e] = 0.f;
+    return;
+  }
+
+  // (1) relaxed window coefficients (as in the bound)
+  {
+    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
+    const int c2 = cb * 16 + row;
+    const long pb = b * pstride;
+    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
+      const int y1 = Y1 + ky2, x1 = X1 + kx2;
+      float v = 0.f;
+      if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
+        const float w = sgn * t2.W[(((long)c2 * t2.in_c + c1) * t2.k + ky2) * t2.k + kx2];
+        const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
+        v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
+      }
+      tile[(c1 * NPOS + pos) * 16 + row] = v;
+    }
+  }
+  __syncthreads();
+
+  // (2) A_x over the footprint; delta = -eps sign(A_x) into LDS (0 outside the image)
+  const int c0 = wave;
+  const bool cok = c0 < t1.in_c;
+  const int Hi = t1.in_h, Wi = t1.in_w;
+  const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
+  {
+    float wreg[PER][KS];
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER; ++ph) {
+      const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c1 = 4 * ks + G;
+        wreg[ph][ks] = (cok && slot < K1 && kx < K1)
+                           ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
+      }
+    }
+    float acc[WO];
+#pragma unroll
+    for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+    auto emit = [&](int yl) {
+      if (!cok) return;
+      const int y = OY + yl;
+#pragma unroll
+      for (int x = 0; x < WO; ++x) {
+        const int xi = OX + x;
+        const bool in = y >= 0 && y < Hi && xi >= 0 && xi < Wi;
+        const float sv = acc[x] > 0.f ? 1.f : (acc[x] < 0.f ? -1.f : 0.f);
+        dl[((c0 * WO + yl) * WO + x) * 16 + n] = in ? -eps * sv : 0.f;
+      }
+    };
+#pragma unroll
+    for (int j = 0; j < K2; ++j) {
+      const int ph = j % PER;
+#pragma unroll
+      for (int i = 0; i < K2; ++i) {
+        const int pos = j * K2 + i;
+        float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
+                                                  tile[((4 * ks + G) * NPOS + pos) * 16 + n],
+                                                  d, 0, 0, 0);
+#pragma unroll
+        for (int kx2 = 0; kx2 < K1; ++kx2) acc[i * S1 + kx2] += d[kx2];
+      }
+      const int ky = ((G - ph * S1) % K1 + K1) % K1;
+      if (G < K1 && ky < S1) {
+        emit(j * S1 + ky);
+#pragma unroll
+        for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+      }
+    }
+    {
+      const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
+      if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
+    }
+  }
+  __syncthreads();
+
+  // (3) G = z1 + W_1 delta at each window neuron; contributions summed over the 16 rows
+  {
+    const int KD = t1.in_c * K1 * K1;
+    const int nks = (KD + 3) / 4;
+    const int c1A = lane & 15;
+    const float wn = wrow[n];
+    const int c2n = cb * 16 + n;
+    for (int pos = wave; pos < NPOS; pos += NW) {
+      const int j = pos / K2, i = pos - j * K2;
+      const int y1 = Y1 + j, x1 = X1 + i;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < nks; ++ks) {
+        const int kk = ks * 4 + G;
+        float av = 0.f, bv = 0.f;
+        if (kk < KD) {
+          const int cc = kk / (K1 * K1), rem = kk - cc * K1 * K1;
+          const int ky = rem / K1, kx = rem - ky * K1;
+          if (c1A < C1) av = t1.W[(long)c1A * KD + kk];
+          bv = dl[((cc * WO + j * S1 + ky) * WO + i * S1 + kx) * 16 + n];
+        }
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, d, 0, 0, 0);
+      }
+      const bool inmap = y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c1 = 4 * G + r;
+        float cval = 0.f;
+        if (c1 < C1 && inmap) {
+          const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
+          if (code1[b * n_relu + ni] == 5 && wn != 0.f) {
+            const float tv = sgn * t2.W[(((long)c2n * t2.in_c + c1) * t2.k + j) * t2.k + i];
+            cval = wn * fmaxf(tv, 0.f) * (d[r] + z1[ni]);
+          }
+        }
+        cval += __shfl_xor(cval, 8, 64);
+        cval += __shfl_xor(cval, 4, 64);
+        cval += __shfl_xor(cval, 2, 64);
+        cval += __shfl_xor(cval, 1, 64);
+        if (n == 0 && c1 < C1) out[c1 * NPOS + pos] = cval;
+      }
+    }
+  }
+}
+
+// d J / d alpha of layer-1 neuron (c1, y1, x1) from pass 2: the partial sums of every window that
+// covers the neuron, in a fixed order.
+__global__ void __launch_bounds__(kBlock)
+    k_pass2_grad_gather(long nb, DLayer t1, DLayer t2, int NPOS, const float* __restrict__ part,
+                        const int8_t* __restrict__ code1, long n_relu,
+                        float* __restrict__ ga1) {
+  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  const long n1 = (long)t1.out_c * t1.out_h * t1.out_w;
+  if (idx >= nb * n1) return;
+  const long b = idx / n1, ni = idx % n1;
+  if (code1[b * n_relu + ni] != 5) return;
+  const int hw = t1.out_h * t1.out_w;
+  const int c1 = (int)(ni / hw), y1 = (int)((ni / t1.out_w) % t1.out_h), x1 = (int)(ni % t1.out_w);
+  const int H2 = t2.out_h, W2 = t2.out_w, K2 = t2.k, S2 = t2.stride, P2 = t2.pad;
+  const int ncb = t2.out_c / 16;
+  const int C1 = t1.out_c;
+  float acc = 0.f;
+  for (int sg = 0; sg < 2; ++sg)
+    for (int cb = 0; cb < ncb; ++cb)
+      for (int ky2 = 0; ky2 < K2; ++ky2) {
+        const int yn = y1 + P2 - ky2;
+        if (yn < 0 || yn % S2) continue;
+        const int y2 = yn / S2;
+        if (y2 >= H2) continue;
+        for (int kx2 = 0; kx2 < K2; ++kx2) {
+          const int xn = x1 + P2 - kx2;
+          if (xn < 0 || xn % S2) continue;
+          const int x2 = xn / S2;
+          if (x2 >= W2) continue;
+          const long blk = (((b * 2 + sg) * ncb + cb) * H2 + y2) * W2 + x2;
+          acc += part[(blk * C1 + c1) * NPOS + ky2 * K2 + kx2];
+        }
+      }
+  ga1[b * n_relu + ni] += acc;
+}
+
 // Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q
 // and 8 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 8th tile of
 // 32 output features i, K runs over o two at a time with the A operand (W, read straight from
@@ -1197,7 +1418,7 @@ struct Plan {
   size_t off_tape[kMaxLayers + 1][kMaxLayers + 1] = {};
   size_t off_wT[kMaxLayers + 1] = {};  // transposed FC weights of layers 2..L-1 (0 = none)
   size_t off_ga = 0, off_gl = 0, off_gu = 0, off_w = 0, off_za = 0, off_zb = 0, off_G = 0;
-  size_t off_lbt = 0, off_grad = 0;
+  size_t off_lbt = 0, off_grad = 0, off_p2part = 0;
   long fwd_floats = 0;
 };
 
@@ -1226,6 +1447,24 @@ Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
   return nullptr;
 }
 
+using Pass2GradKernel = void (*)(DLayer, DLayer, const float*, const float*, long, float,
+                                 const float*, const float*, const int8_t*, long, long,
+                                 const float*, float*);
+Pass2GradKernel pass2_grad_kernel_for(const lirpa_net* net) {
+  int nw = 0;
+  if (!pass2_kernel_for(net, &nw)) return nullptr;
+  const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
+  if (t2.k == 4 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 4, 8, 3>;
+  if (t2.k == 4 && t1.out_c == 16) return k_pass2_window_grad<4, 2, 1, 4, 16, 3>;
+  if (t2.k == 3 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 3, 8, 3>;
+  return nullptr;
+}
+
+long pass2_blocks(const lirpa_net* net, long nb) {
+  const lirpa_layer& t2 = net->T[1];
+  return nb * 2 * (t2.out_c / 16) * t2.out_h * t2.out_w;
+}
+
 Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   Plan p;
   p.Bc = Bc;
@@ -1233,7 +1472,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   const int L = net->L;
   long slab = 0, qpmax = round_up(2 * net->n[1], 64);
   int nw_unused = 0;
-  const bool win2 = mode == 0 && pass2_kernel_for(net, &nw_unused) != nullptr;
+  const bool win2 = (mode == 0 && pass2_kernel_for(net, &nw_unused) != nullptr) ||
+                    (mode == 1 && pass2_grad_kernel_for(net) != nullptr);
   for (int k = 2; k <= L; ++k) {
     long R = (k < L) ? 2 * net->n[k] : S;
     long qp = round_up(Bc * R, 64);
@@ -1273,6 +1513,14 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
     for (int k = 2; k <= L; ++k) {
       long R = (k < L) ? 2 * net->n[k] : S;
       long qp = round_up(Bc * R, 64);
+      if (k == 2 && win2 && k < L) {
+        // pass 2 is differentiated window by window: partial sums per block and window neuron
+        const lirpa_layer& t2 = net->T[1];
+        const int k2 = t2.k;
+        p.off_p2part = o;
+        o = align256(o + (size_t)pass2_blocks(net, Bc) * net->T[0].out_c * k2 * k2 * 4);
+        continue;
+      }
       for (int m = 0; m <= k - 1; ++m) {
         p.off_tape[k][m] = o;
         o = align256(o + (size_t)net->n[m] * qp * 4);
@@ -1294,8 +1542,10 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   // kernels address a slab with 32-bit element offsets
   long big = std::max(slab, p.fwd_floats);
   if (mode == 1)
-    for (int k = 2; k <= L; ++k)
+    for (int k = 2; k <= L; ++k) {
+      if (k == 2 && win2 && k < L) continue;
       big = std::max(big, net->n[0] * round_up(Bc * ((k < L) ? 2 * net->n[k] : S), 64));
+    }
   if (big >= (1L << 31)) p.total = (size_t)-1;
   return p;
 }
@@ -1519,7 +1769,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   }
   for (int k = 2; k <= L - 1; ++k) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
-    if (k == 2 && !c.tape) {
+    if (k == 2 && (!c.tape || pass2_grad_kernel_for(net))) {
       int e = pass2_window(c);
       if (e != 1) {
         if (e) return e;
@@ -1617,6 +1867,29 @@ int grad_chunk(const Chunk& c, int full) {
       return e;
   for (int P = L; P >= 2; --P) {
     if (!full && P < L) break;
+    if (P == 2 && P < L) {
+      if (Pass2GradKernel gk = pass2_grad_kernel_for(net)) {
+        const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
+        long blocks = pass2_blocks(net, c.nb);
+        float* part = at<float>(c.ws, p.off_p2part);
+        const int8_t* code = at<int8_t>(c.ws, p.off_code);
+        int e = launch_k(tag("pass2_window_grad", 1, 2), c.st, [&] {
+          hipLaunchKernelGGL(gk, dim3((unsigned)blocks), dim3(64 * t1.in_c), 0, c.st, dlayer(t1),
+                             dlayer(t2), at<float>(c.ws, p.off_alo) + net->poff[1],
+                             at<float>(c.ws, p.off_aup) + net->poff[1], net->pstride, c.eps, gl,
+                             gu, code, net->n_relu, net->off[2], at<float>(c.ws, p.off_z1), part);
+        });
+        if (e) return e;
+        long n1 = net->n[1];
+        e = launch_k(tag("pass2_grad_gather", 1, 2), c.st, [&] {
+          hipLaunchKernelGGL(k_pass2_grad_gather, grid_for(c.nb * n1), dim3(kBlock), 0, c.st,
+                             c.nb, dlayer(t1), dlayer(t2), t2.k * t2.k, part, code, net->n_relu,
+                             ga);
+        });
+        if (e) return e;
+        continue;
+      }
+    }
     long R = (P < L) ? 2 * net->n[P] : c.S, Q = c.nb * R, ldq = round_up(Q, 64);
     long offP = (P < L) ? net->off[P] : 0;
     if (int e = launch_k(tag("row_weights", P, P), c.st, [&] {
