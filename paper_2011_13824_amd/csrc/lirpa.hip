@@ -132,6 +132,21 @@ enum { MODE_SLAB = 0, MODE_BOUND = 1 };
 
 typedef float float4v __attribute__((ext_vector_type(4)));
 
+// 16-row tile of a block, XCD-aware.  Workgroups are dispatched round-robin over the 8 XCDs,
+// each with its own L2, and a 16-row tile covers half of a 128-byte line in every slab row: tiles
+// 2k and 2k+1 go to blocks b and b+8, which land on the same XCD, so each line is fetched and
+// written back by one L2.  Grids are padded to a multiple of 16 blocks; blocks past the last
+// tile exit at once.
+__device__ __forceinline__ unsigned xcd_tile(unsigned blk) {
+  return (blk & ~15u) + ((blk & 7u) << 1) + ((blk >> 3) & 1u);
+}
+
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations, not for its
+// outstanding global stores (which __syncthreads() would also drain).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Where a stage's output row goes.
 //  MODE_SLAB : coefficients over g^(m) are relaxed with layer m's (a_lo, a_up, b_up) of the
 //              row's sub-domain (Eq. 6: non-negative entries take the lower line, negative ones
@@ -314,6 +329,13 @@ __global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __r
 }
 
 // z1 = W1 x0 + b1: the layer-1 pre-activation at the box centre.
+// Per-channel bias broadcast to a per-neuron vector.
+__global__ void __launch_bounds__(kBlock) k_bias_fill(long n, int hw, const float* __restrict__ b,
+                                                      float* __restrict__ out) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i < n) out[i] = b[i / hw];
+}
+
 __global__ void __launch_bounds__(kBlock) k_layer1_at_x0(DLayer t, const float* __restrict__ x0,
                                                          float* __restrict__ z) {
   long j = blockIdx.x * (long)blockDim.x + threadIdx.x;
@@ -476,14 +498,18 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   constexpr int KS = CO / 4;
   constexpr int NT = 64 * NW;
   constexpr int PER = (K % S == 0) ? K / S : K;  // rotation period of the tap rows
-  constexpr int TILE = CO * W1 * 16;  // floats per input-row tile
-  constexpr int NV4 = TILE / 4;       // float4 per tile
+  // LDS tile of one input row, [CO][W1][16] with each channel padded to a stride of 16 mod 64
+  // floats, so the four lane groups of a B-operand read (channels 4ks + G) hit disjoint banks
+  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
+  constexpr int TILE = CO * CS;       // floats per input-row tile
+  constexpr int NV4 = CO * W1 * 4;    // float4 per tile
   extern __shared__ float lds[];
   float* tiles = lds;                  // 2 x [CO][W1][16]
   float* xs = lds + 2 * TILE;          // MODE_BOUND: x0 [in_c*H0*W0]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, G = lane >> 4;
-  const unsigned q0 = blockIdx.x * 16u;
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned q = q0 + n;
   const bool qok = q < Q;
   const unsigned b = qok ? q / (unsigned)s.R : 0u;
@@ -494,7 +520,6 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
     const int nx = t.in_c * H0 * W0;
     for (int e = threadIdx.x; e < nx; e += NT) xs[e] = s.x0[e];
   }
-  const bool zvec = MODE == MODE_SLAB && s.bias_hw == 1;  // per-neuron bias (z1)
 
   // A operands, one set per rotation phase: slot (M/4, M%4) of lane l (M = l%16) takes tap
   // ((M/4 - ph*S) mod K, M%4) of co = 4*ks + l/16
@@ -523,6 +548,27 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   }
 
   float beta = 0.f, lin = 0.f, l1 = 0.f;
+  // Relaxation parameters of one output row (MODE_SLAB): loaded before the MFMAs of the step
+  // that completes the row, so their latency hides behind the matrix work.
+  constexpr int NQ = W0 / 4;
+  constexpr int NP = MODE == MODE_SLAB ? NQ : 1;
+  // early loads only where the registers allow it; otherwise just before the row is relaxed
+  constexpr bool EARLY = MODE == MODE_SLAB && CPW == 1 && W0 <= 16;
+  float4v p_lo[CPW][NP], p_up[CPW][NP], p_bu[CPW][NP], p_bz[CPW][NP];
+  auto load_row = [&](int c, int y) {
+    if constexpr (EARLY) {
+      if (!cok[c] || !qok || y < 0 || y >= H0) return;
+      const unsigned rowi = ((unsigned)cis[c] * H0 + y) * W0;
+      const long pb = (long)b * s.pstride + rowi;
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        p_lo[c][i] = *reinterpret_cast<const float4v*>(s.a_lo + pb + 4 * i);
+        p_up[c][i] = *reinterpret_cast<const float4v*>(s.a_up + pb + 4 * i);
+        p_bu[c][i] = *reinterpret_cast<const float4v*>(s.b_up + pb + 4 * i);
+        p_bz[c][i] = *reinterpret_cast<const float4v*>(s.bias + rowi + 4 * i);
+      }
+    }
+  };
   auto emit = [&](int c, int y, const float* vals) {
     if (!cok[c] || !qok || y < 0 || y >= H0) return;
     const unsigned rowi = ((unsigned)cis[c] * H0 + y) * W0;
@@ -544,18 +590,24 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
       }
     } else {
       const long pb = (long)b * s.pstride + rowi;
-      const float bias_c = zvec ? 0.f : s.bias[cis[c]];
 #pragma unroll
-      for (int x4 = 0; x4 < W0; x4 += 4) {
-        const float4v lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + x4);
-        const float4v up = *reinterpret_cast<const float4v*>(s.a_up + pb + x4);
-        const float4v bu = *reinterpret_cast<const float4v*>(s.b_up + pb + x4);
-        float4v bz = {bias_c, bias_c, bias_c, bias_c};
-        if (zvec) bz = *reinterpret_cast<const float4v*>(s.bias + rowi + x4);
+      for (int i = 0; i < NQ; ++i) {
+        float4v lo, up, bu, bz;
+        if constexpr (EARLY) {
+          lo = p_lo[c][i];
+          up = p_up[c][i];
+          bu = p_bu[c][i];
+          bz = p_bz[c][i];
+        } else {
+          lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + 4 * i);
+          up = *reinterpret_cast<const float4v*>(s.a_up + pb + 4 * i);
+          bu = *reinterpret_cast<const float4v*>(s.b_up + pb + 4 * i);
+          bz = *reinterpret_cast<const float4v*>(s.bias + rowi + 4 * i);
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float a = vals[x4 + j];
-          const unsigned idx = (rowi + x4 + j) * ldq + q;
+          const float a = vals[4 * i + j];
+          const unsigned idx = (rowi + 4 * i + j) * ldq + q;
           if constexpr (TAPE) s.tape[idx] = a;
           const float ah = a >= 0.f ? a * lo[j] : a * up[j];
           beta = fmaf(fminf(a, 0.f), bu[j], beta);
@@ -577,10 +629,19 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
     const int co = cx / W1, x1 = cx - co * W1;
     return in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4;
   };
+  auto loff = [&](int v4) {
+    const int cx = v4 >> 2, j4 = v4 & 3;
+    const int co = cx / W1, x1 = cx - co * W1;
+    return co * CS + x1 * 16 + j4 * 4;
+  };
   for (int v4 = threadIdx.x; v4 < NV4; v4 += NT)
-    *reinterpret_cast<float4v*>(tiles + v4 * 4) = *reinterpret_cast<const float4v*>(gaddr(0, v4));
+    *reinterpret_cast<float4v*>(tiles + loff(v4)) = *reinterpret_cast<const float4v*>(gaddr(0, v4));
   __syncthreads();
 
+  // Per input row: (1) issue the loads of the next input tile and of the parameters of the
+  // rows this step completes, (2) the MFMAs, (3) park the next tile in LDS, (4) relax and store
+  // the completed rows, (5) an LDS-only barrier.  No wait inside the loop covers the global
+  // stores of (4).
   constexpr int PF = (NV4 + NT - 1) / NT;  // prefetched float4 per thread
   for (int ybase = 0; ybase < H1; ybase += PER) {
 #pragma unroll
@@ -589,9 +650,12 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
       if (H1 % PER != 0 && y1 >= H1) break;
       const float* tile = tiles + (y1 & 1) * TILE;
       const bool more = y1 + 1 < H1;
+      // this lane group's tap row at this phase; rows with ky < S are complete after it
+      const int ky = ((G - ph * S) % K + K) % K;
+      const bool done = G < K && ky < S;
+      const int yout = y1 * S - P + ky;
       float4v pf[PF];
       {
-        // next input row: loaded now, stored to the other LDS buffer after the MFMAs
         const int yn = more ? y1 + 1 : y1;
 #pragma unroll
         for (int k = 0; k < PF; ++k) {
@@ -599,11 +663,16 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
           pf[k] = *reinterpret_cast<const float4v*>(gaddr(yn, v4));
         }
       }
+      if (EARLY && done) {
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) load_row(c, yout);
+      }
+      if constexpr (EARLY) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int x1 = 0; x1 < W1; ++x1) {
         float bv[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[((4 * ks + G) * W1 + x1) * 16 + n];
+        for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(4 * ks + G) * CS + x1 * 16 + n];
 #pragma unroll
         for (int c = 0; c < CPW; ++c) {
           float4v d = {0.f, 0.f, 0.f, 0.f};
@@ -617,25 +686,23 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
           }
         }
       }
-      // this lane group's tap row at this phase; rows with ky < S are complete
-      const int ky = ((G - ph * S) % K + K) % K;
-      if (G < K && ky < S) {
-#pragma unroll
-        for (int c = 0; c < CPW; ++c) {
-          emit(c, y1 * S - P + ky, acc[c]);
-#pragma unroll
-          for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
-        }
-      }
       if (more) {
         float* nt = tiles + ((y1 + 1) & 1) * TILE;
 #pragma unroll
         for (int k = 0; k < PF; ++k) {
           const int v4 = (int)threadIdx.x + k * NT;
-          if (v4 < NV4) *reinterpret_cast<float4v*>(nt + v4 * 4) = pf[k];
+          if (v4 < NV4) *reinterpret_cast<float4v*>(nt + loff(v4)) = pf[k];
         }
-        __syncthreads();
       }
+      if (done) {
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) {
+          emit(c, yout, acc[c]);
+#pragma unroll
+          for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+        }
+      }
+      if (more) lds_barrier();
     }
   }
   {
@@ -644,7 +711,10 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
     const int ky = ((G - ph_last * S) % K + K) % K;
     if (G < K && ky >= S) {
 #pragma unroll
-      for (int c = 0; c < CPW; ++c) emit(c, (H1 - 1) * S - P + ky, acc[c]);
+      for (int c = 0; c < CPW; ++c) {
+        load_row(c, (H1 - 1) * S - P + ky);
+        emit(c, (H1 - 1) * S - P + ky, acc[c]);
+      }
     }
   }
   // output rows no input row reaches (zero coefficients)
@@ -657,7 +727,10 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 #pragma unroll
       for (int y = YZ; y < H0; ++y)
 #pragma unroll
-        for (int c = 0; c < CPW; ++c) emit(c, y, zero);
+        for (int c = 0; c < CPW; ++c) {
+          load_row(c, y);
+          emit(c, y, zero);
+        }
     }
   }
 
@@ -685,6 +758,254 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   sink_finish<MODE>(s, tot, q, b, q % (unsigned)s.R, false);
 }
 
+// Transposed convolution with the relaxation of layer m-1 fused, on specialised waves.
+//
+// The rotating lane-group MFMA scheme of k_convT_mfma, with the epilogue moved off the matrix
+// waves.  NM = CI / CPW "matrix" waves own CPW output channels each: per input row they read the
+// B operands from the LDS tile, run the MFMAs, and park the output rows that row completes,
+// unrelaxed, in an LDS row buffer.  They also issue every global load of the block -- the next
+// input tile and the relaxation parameters of the rows they complete (staged into LDS one step
+// ahead) -- and no global store.  NS "storer" waves take the parked rows of the previous step:
+// relaxation (Eq. 6), intercept and bias terms of each row, and the stores of the relaxed
+// coefficients; they issue no global load.  So no wave ever waits on a counter that also covers
+// global stores, and the matrix waves never wait on the relaxation's arithmetic.  One LDS-only
+// barrier per input row hands the buffers over (double-buffered).  A block takes 16 rows q
+// spanning at most two sub-domains (R >= 16).
+template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS,
+          bool TAPE>
+__global__ void __launch_bounds__(64 * (CI / CPW + NS))
+    k_convT_relax_ws(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
+  static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % CPW == 0, "geometry");
+  static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
+  constexpr int NM = CI / CPW;                   // matrix waves
+  constexpr int NTM = 64 * NM;
+  constexpr int KS = CO / 4;
+  constexpr int PER = (K % S == 0) ? K / S : K;  // rotation period of the tap rows
+  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
+  constexpr int TILE = CO * CS;
+  constexpr int NV4 = CO * W1 * 4;               // float4 per input tile
+  constexpr int PF = (NV4 + NTM - 1) / NTM;
+  constexpr int RSL = S > K - S ? S : K - S;     // output rows completed per step (max)
+  constexpr int RB = RSL * CI * 16 * 16;         // row buffer: [RSL][CI][16 q][16 x]
+  constexpr int PB = 2 * 4 * RSL * CI * W0;      // parameters: [2 sub-domains][4][RSL][CI][W0]
+  constexpr int NPV4 = PB / 4;
+  constexpr int PP = (NPV4 + NTM - 1) / NTM;
+  extern __shared__ float lds[];
+  float* tiles = lds;              // 2 x TILE
+  float* rows = tiles + 2 * TILE;  // 2 x RB
+  float* pars = rows + 2 * RB;     // 2 x PB
+  float* red = pars + 2 * PB;      // NS x 16
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  const unsigned R = (unsigned)s.R;
+  const unsigned b0 = q0 / R;
+  const unsigned b1 = (min(q0 + 15u, Q - 1u)) / R;  // b0 or b0 + 1
+
+  // output row of slot r at stage e (stage H1: the rows still open after the last input row)
+  auto yrow = [&](int e, int r) { return e < H1 ? e * S - P + r : (H1 - 1) * S - P + S + r; };
+  auto nrows = [&](int e) { return e < H1 ? S : K - S; };
+
+  if (wave < NM) {
+    // ------------------------------------------------------------------ matrix waves
+    const int n = lane & 15, G = lane >> 4;
+    const int tid = threadIdx.x;  // < NTM
+    float wreg[PER][CPW][KS];
+    {
+      const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+      for (int ph = 0; ph < PER; ++ph) {
+        const int ky = ((slot - ph * S) % K + K) % K;
+#pragma unroll
+        for (int c = 0; c < CPW; ++c)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const int co = 4 * ks + G, ci = wave * CPW + c;
+            wreg[ph][c][ks] = (slot < K && kx < K)
+                                  ? t.W[((co * CI + ci) * K + ky) * K + kx] : 0.f;
+          }
+      }
+    }
+    auto gaddr = [&](int y1, int v4) {
+      const int cx = v4 >> 2, j4 = v4 & 3;
+      const int co = cx / W1, x1 = cx - co * W1;
+      return in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4;
+    };
+    auto loff = [&](int v4) {
+      const int cx = v4 >> 2, j4 = v4 & 3;
+      const int co = cx / W1, x1 = cx - co * W1;
+      return co * CS + x1 * 16 + j4 * 4;
+    };
+    // relaxation parameters of stage e: float4 v of [bsel][arr][r][CI][W0/4]
+    auto pload = [&](int e, int v, float4v& out) {
+      const int x4 = v % (W0 / 4);
+      const int c = (v / (W0 / 4)) % CI;
+      const int r = (v / (W0 / 4 * CI)) % RSL;
+      const int arr = (v / (W0 / 4 * CI * RSL)) % 4;
+      const int bsel = v / (W0 / 4 * CI * RSL * 4);
+      const int y = yrow(e, r);
+      out = float4v{0.f, 0.f, 0.f, 0.f};
+      if (r >= nrows(e) || y < 0 || y >= H0 || b0 + bsel > b1) return;
+      const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * x4;
+      const long pb = (long)(b0 + bsel) * s.pstride + rowi;
+      const float* src = arr == 0 ? s.a_lo + pb : arr == 1 ? s.a_up + pb
+                       : arr == 2 ? s.b_up + pb : s.bias + rowi;
+      out = *reinterpret_cast<const float4v*>(src);
+    };
+    auto park = [&](int slot, int r, int c, const float* v) {
+      float* dst = rows + slot * RB + (((r * CI + wave * CPW + c) * 16 + n) * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<float4v*>(dst + 4 * i) =
+            float4v{v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+    };
+
+    for (int v4 = tid; v4 < NV4; v4 += NTM)
+      *reinterpret_cast<float4v*>(tiles + loff(v4)) =
+          *reinterpret_cast<const float4v*>(gaddr(0, v4));
+    lds_barrier();
+
+    float acc[CPW][W0];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c)
+#pragma unroll
+      for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+
+    for (int ybase = 0; ybase < H1; ybase += PER) {
+#pragma unroll
+      for (int ph = 0; ph < PER; ++ph) {
+        const int y1 = ybase + ph;
+        if (H1 % PER != 0 && y1 >= H1) break;
+        const float* tile = tiles + (y1 & 1) * TILE;
+        const bool more = y1 + 1 < H1;
+        float4v pf[PF], pp[PP];
+#pragma unroll
+        for (int k = 0; k < PF; ++k) {
+          const int v4 = min(tid + k * NTM, NV4 - 1);
+          pf[k] = *reinterpret_cast<const float4v*>(gaddr(more ? y1 + 1 : y1, v4));
+        }
+#pragma unroll
+        for (int k = 0; k < PP; ++k) pload(y1, min(tid + k * NTM, NPV4 - 1), pp[k]);
+#pragma unroll
+        for (int x1 = 0; x1 < W1; ++x1) {
+          float bv[KS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(4 * ks + G) * CS + x1 * 16 + n];
+#pragma unroll
+          for (int c = 0; c < CPW; ++c) {
+            float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+              d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+#pragma unroll
+            for (int kx = 0; kx < K; ++kx) {
+              const int col = x1 * S - P + kx;
+              if (col >= 0 && col < W0) acc[c][col] += d[kx];
+            }
+          }
+        }
+        if (more) {
+          float* nt = tiles + ((y1 + 1) & 1) * TILE;
+#pragma unroll
+          for (int k = 0; k < PF; ++k) {
+            const int v4 = tid + k * NTM;
+            if (v4 < NV4) *reinterpret_cast<float4v*>(nt + loff(v4)) = pf[k];
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < PP; ++k) {
+          const int v = tid + k * NTM;
+          if (v < NPV4) *reinterpret_cast<float4v*>(pars + (y1 & 1) * PB + 4 * v) = pp[k];
+        }
+        const int ky = ((G - ph * S) % K + K) % K;
+        if (G < K && ky < S) {
+#pragma unroll
+          for (int c = 0; c < CPW; ++c) {
+            park(y1 & 1, ky, c, acc[c]);
+#pragma unroll
+            for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+          }
+        }
+        lds_barrier();
+      }
+    }
+    // stage H1: the rows still open
+    {
+      float4v pp[PP];
+#pragma unroll
+      for (int k = 0; k < PP; ++k) pload(H1, min(tid + k * NTM, NPV4 - 1), pp[k]);
+      constexpr int ph_last = (H1 - 1) % PER;
+      const int ky = ((G - ph_last * S) % K + K) % K;
+      if (G < K && ky >= S) {
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) park(H1 & 1, ky - S, c, acc[c]);
+      }
+#pragma unroll
+      for (int k = 0; k < PP; ++k) {
+        const int v = tid + k * NTM;
+        if (v < NPV4) *reinterpret_cast<float4v*>(pars + (H1 & 1) * PB + 4 * v) = pp[k];
+      }
+    }
+    lds_barrier();
+    lds_barrier();  // the storers' final reduction
+    return;
+  }
+
+  // -------------------------------------------------------------------- storer waves
+  const int ws = wave - NM;
+  const int qn = lane & 15, xg = lane >> 4;
+  const unsigned q = q0 + qn;
+  const bool qok = q < Q;
+  const int bsel = qok ? (int)(q / R - b0) : 0;
+  float beta = 0.f;
+  auto stage = [&](int e) {
+    const int slot = e & 1;
+    const int nr = nrows(e);
+    for (int it = ws; it < nr * CI; it += NS) {
+      const int r = it / CI, c = it - r * CI;
+      const int y = yrow(e, r);
+      if (y < 0 || y >= H0 || !qok) continue;
+      const float4v a = *reinterpret_cast<const float4v*>(rows + slot * RB +
+                                                          ((r * CI + c) * 16 + qn) * 16 + 4 * xg);
+      const float* pbase = pars + slot * PB + ((bsel * 4) * RSL + r) * CI * W0 + c * W0 + 4 * xg;
+      constexpr int AST = RSL * CI * W0;  // stride between the four parameter arrays
+      const float4v lo = *reinterpret_cast<const float4v*>(pbase);
+      const float4v up = *reinterpret_cast<const float4v*>(pbase + AST);
+      const float4v bu = *reinterpret_cast<const float4v*>(pbase + 2 * AST);
+      const float4v bz = *reinterpret_cast<const float4v*>(pbase + 3 * AST);
+      const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * xg;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const unsigned idx = (rowi + j) * ldq + q;
+        if constexpr (TAPE) s.tape[idx] = a[j];
+        const bool pos = a[j] >= 0.f;
+        const float ah = a[j] * (pos ? lo[j] : up[j]);
+        beta = fmaf(pos ? 0.f : a[j], bu[j], beta);
+        beta = fmaf(ah, bz[j], beta);
+        s.out[idx] = ah;
+      }
+    }
+  };
+  lds_barrier();  // initial tile
+  for (int y1 = 0; y1 < H1; ++y1) {
+    if (y1 > 0) stage(y1 - 1);
+    lds_barrier();
+  }
+  stage(H1 - 1);
+  lds_barrier();
+  stage(H1);
+  beta += __shfl_xor(beta, 16, 64);
+  beta += __shfl_xor(beta, 32, 64);
+  if (lane < 16) red[ws * 16 + lane] = beta;
+  lds_barrier();
+  if (ws != 0 || lane >= 16 || !qok) return;
+  float tot = 0.f;
+  for (int w = 0; w < NS; ++w) tot += red[w * 16 + lane];
+  Acc a{tot, 0.f, 0.f};
+  sink_finish<MODE_SLAB>(s, a, q, q / R, q % R, false);
+}
+
 // Pass 2 restricted to each row's receptive field, when T_2 and T_1 are convolutions.
 // Row +-e_j of h^(2), j = (c2, y2, x2), carried through T_2 is +-W_2[c2] placed on the window
 // (y2*S2 - P2 + ky2, x2*S2 - P2 + kx2) of g^(1) and zero elsewhere, so its image under the
@@ -708,7 +1029,8 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   constexpr int NPOS = K2 * K2;
   constexpr int WO = (K2 - 1) * S1 + K1;           // footprint width on the input
   constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
-  constexpr int NEL = C1 * NPOS * 16;               // relaxed window tile
+  constexpr int CS = NPOS * 16 + (80 - (NPOS * 16) % 64) % 64;  // channel stride, 16 mod 64
+  constexpr int NEL = C1 * CS;                      // relaxed window tile
   constexpr int RPT = NT / 16;                      // threads per row in phase 1
   __shared__ float tile[NEL];
   __shared__ float red[NW * 3 * 16 + RPT * 16];
@@ -749,7 +1071,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
         // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
         bpart = fmaf(v, z1[ni], bpart);
       }
-      tile[(c1 * NPOS + pos) * 16 + row] = v;
+      tile[c1 * CS + pos * 16 + row] = v;
     }
     bred[part * 16 + row] = bpart;
   }
@@ -803,7 +1125,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
-                                                tile[((4 * ks + G) * NPOS + pos) * 16 + n], d,
+                                                tile[(4 * ks + G) * CS + pos * 16 + n], d,
                                                 0, 0, 0);
 #pragma unroll
       for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
@@ -862,7 +1184,8 @@ __global__ void __launch_bounds__(64 * NW)
   constexpr int NPOS = K2 * K2;
   constexpr int WO = (K2 - 1) * S1 + K1;
   constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
-  constexpr int NEL = C1 * NPOS * 16;
+  constexpr int CS = NPOS * 16 + (80 - (NPOS * 16) % 64) % 64;  // channel stride, 16 mod 64
+  constexpr int NEL = C1 * CS;
   __shared__ float tile[NEL];
   __shared__ float dl[NW * WO * WO * 16];  // delta over the footprint, [c0][fy][fx][row]
   __shared__ float wrow[16];
@@ -914,7 +1237,7 @@ __global__ void __launch_bounds__(64 * NW)
         const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
         v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
       }
-      tile[(c1 * NPOS + pos) * 16 + row] = v;
+      tile[c1 * CS + pos * 16 + row] = v;
     }
   }
   __syncthreads();
@@ -961,7 +1284,7 @@ __global__ void __launch_bounds__(64 * NW)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
-                                                  tile[((4 * ks + G) * NPOS + pos) * 16 + n],
+                                                  tile[(4 * ks + G) * CS + pos * 16 + n],
                                                   d, 0, 0, 0);
 #pragma unroll
         for (int kx2 = 0; kx2 < K1; ++kx2) acc[i * S1 + kx2] += d[kx2];
@@ -1261,7 +1584,8 @@ __global__ void __launch_bounds__(256)
                float* __restrict__ G, float* __restrict__ zout) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, g = lane >> 4;
-  const unsigned q0 = blockIdx.x * 16u;
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned q = q0 + n;
   const bool qok = q < Q;
   const float wq = qok ? w[q] : 0.f;
@@ -1411,7 +1735,8 @@ struct Plan {
   int mode = 0;
   size_t off_l = 0, off_u = 0, off_alo = 0, off_aup = 0, off_bup = 0, off_code = 0;
   size_t off_l1u1 = 0, off_slab0 = 0, off_slab1 = 0, off_beta = 0, total = 0;
-  size_t off_z1 = 0;  // W1 x0 + b1
+  size_t off_bz = 0;  // per-neuron bias of every ReLU layer (padded layout, segment m at poff[m])
+  size_t off_z1 = 0;  // its layer-1 segment: W1 x0 + b1
   long slab_floats = 0, qp_max = 0;
   // mode 1 (gradient): tape[k][m] holds, for pass k, the coefficients over g^(m) before their
   // relaxation (m >= 1) and over x (m = 0), [n_m][qp_k]; adjoints; row weights; forward slabs.
@@ -1499,7 +1824,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   p.off_bup = o;  o = align256(o + perp * 4);
   p.off_code = o; o = align256(o + per);
   p.off_l1u1 = o; o = align256(o + 2 * (size_t)net->n[1] * 4);
-  p.off_z1 = o;   o = align256(o + (size_t)net->n[1] * 4);
+  p.off_bz = o;   o = align256(o + (size_t)std::max<long>(net->pstride, net->n[1]) * 4);
+  p.off_z1 = p.off_bz + (size_t)net->poff[1] * 4;
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
   p.off_slab0 = o; o = align256(o + (size_t)slab * 4);
   p.off_slab1 = o; o = align256(o + (size_t)slab * 4);
@@ -1611,6 +1937,35 @@ ConvTKernel<MODE> convT_mfma_for(const DLayer& t, bool tape, int* nwaves) {
   return tape ? convT_mfma_pick<MODE, true>(t, nwaves) : convT_mfma_pick<MODE, false>(t, nwaves);
 }
 
+// Wave-specialised relaxing stage for the 16-wide output geometries; null when not covered.
+// *nwaves: matrix + storer waves; *lds: dynamic LDS bytes.
+template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS>
+ConvTKernel<MODE_SLAB> convT_ws_inst(bool tape, int* nwaves, size_t* lds) {
+  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
+  constexpr int RSL = S > K - S ? S : K - S;
+  *nwaves = CI / CPW + NS;
+  *lds = (size_t)(2 * CO * CS + 2 * RSL * CI * 256 + 2 * 2 * 4 * RSL * CI * W0 + NS * 16) *
+         sizeof(float);
+  return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true>
+              : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false>;
+}
+
+ConvTKernel<MODE_SLAB> convT_ws_for(const DLayer& t, bool tape, int* nwaves, size_t* lds) {
+  const bool g_s2_16 = t.k == 4 && t.stride == 2 && t.pad == 1 && t.out_h == 8 && t.out_w == 8 &&
+                       t.in_h == 16 && t.in_w == 16;
+  const bool g_s1_16 = t.k == 3 && t.stride == 1 && t.pad == 1 && t.out_h == 16 &&
+                       t.out_w == 16 && t.in_h == 16 && t.in_w == 16;
+  if (g_s2_16 && t.in_c == 8 && t.out_c == 16)
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 1, 4>(tape, nwaves, lds);
+  if (g_s2_16 && t.in_c == 8 && t.out_c == 8)
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 8, 8, 1, 4>(tape, nwaves, lds);
+  if (g_s2_16 && t.in_c == 16 && t.out_c == 32)
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4>(tape, nwaves, lds);
+  if (g_s1_16 && t.in_c == 8 && t.out_c == 8)
+    return convT_ws_inst<3, 1, 1, 16, 16, 16, 16, 8, 8, 1, 4>(tape, nwaves, lds);
+  return nullptr;
+}
+
 template <int MODE>
 int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ldq, long Q,
                  const Sink& s, hipStream_t st) {
@@ -1629,9 +1984,28 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
     });
   }
   int nw = 0;
+  if constexpr (MODE == MODE_SLAB) {
+    if (s.R >= 16) {
+      int nwt = 0;
+      size_t lds = 0;
+      if (ConvTKernel<MODE_SLAB> kern = convT_ws_for(t, s.tape != nullptr, &nwt, &lds)) {
+        const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+        if (lds > 65536 &&
+            hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds) != hipSuccess)
+          return fail(LIRPA_EDEVICE, "cannot reserve %zu bytes of LDS", lds);
+        return launch_k(tag("convT_relax", m, pass), st, [&] {
+          hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nwt), lds, st, t, in, (unsigned)ldq,
+                             (unsigned)Q, s);
+        });
+      }
+    }
+  }
   if (ConvTKernel<MODE> kern = convT_mfma_for<MODE>(t, s.tape != nullptr, &nw)) {
-    const unsigned nblk16 = (unsigned)((Q + 15) / 16);
-    size_t lds = (2 * (size_t)t.out_c * t.out_w * 16 + (size_t)nw * 3 * 16 +
+    const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+    const size_t cs = (size_t)t.out_w * 16 + (80 - (t.out_w * 16) % 64) % 64;
+    size_t lds = (2 * (size_t)t.out_c * cs + (size_t)nw * 3 * 16 +
                   (MODE == MODE_BOUND ? (size_t)t.in_c * t.in_h * t.in_w : 0)) * sizeof(float);
     return launch_k(tag((std::string("convT") + sfx).c_str(), m, pass), st, [&] {
       hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, st, t, in, (unsigned)ldq,
@@ -1670,13 +2044,10 @@ Sink slab_sink(const Chunk& c, int m, float* out, long ldq, long R) {
   s.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[m];
   s.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[m];
   s.pstride = net->pstride;
-  if (m == 1) {
-    s.bias = at<float>(c.ws, c.p->off_z1);  // layer-1 bias + linear term of the bound
-    s.bias_hw = 1;
-  } else {
-    s.bias = t.b;
-    s.bias_hw = t.out_h * t.out_w;
-  }
+  // per-neuron bias vector (layer 1: its bias plus the linear term of the bound)
+  s.bias = at<float>(c.ws, c.p->off_bz) + net->poff[m];
+  s.bias_hw = 1;
+  (void)t;
   s.beta = at<float>(c.ws, c.p->off_beta);
   s.R = R;
   return s;
@@ -1830,6 +2201,16 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
                            x0, at<float>(ws, p.off_z1));
       }))
     return e;
+  // per-neuron bias vectors of ReLU layers 2..L-1 (layer 1's is z1, written above)
+  for (int m = 2; m <= net->L - 1; ++m) {
+    const lirpa_layer& t = net->T[m - 1];
+    long nm = net->n[m];
+    if (int e = launch_k("bias_fill", st, [&] {
+          hipLaunchKernelGGL(k_bias_fill, grid_for(nm), dim3(kBlock), 0, st, nm,
+                             t.out_h * t.out_w, t.b, at<float>(ws, p.off_bz) + net->poff[m]);
+        }))
+      return e;
+  }
   // transposed weights of the fully connected layers that start an intermediate pass
   for (int k = 2; k <= net->L - 1; ++k) {
     if (!p.off_wT[k]) continue;
@@ -1904,7 +2285,7 @@ int grad_chunk(const Chunk& c, int full) {
       long off = net->off[m], poff = net->poff[m];
       float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
       DLayer t = dlayer(net->T[m - 1]);
-      const unsigned nblk16 = (unsigned)((Q + 15) / 16);
+      const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
         if (m == 1)
           hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
