@@ -49,6 +49,16 @@ def stage_work(layers, S, B):
         f, b = work.get(cls, (0.0, 0.0))
         work[cls] = (f + flop, b + byt)
 
+    if L >= 3 and layers[0]["kind"] == wl.CONV and layers[1]["kind"] == wl.CONV:
+        # pass 2 restricted to each row's receptive field (launched instead of the dense pass
+        # when the library has a kernel for the shapes): a row +-e_j of h^(2) carries the
+        # C1 x K2 x K2 window of W_2 through the relaxation of layer 1 and T_1^T, each window
+        # entry reaching in_c x K1 x K1 inputs.  Bytes: the layer-1 relaxation parameters read
+        # (3 floats per neuron) and l, u of layer 2 written.
+        t1, t2 = layers[0], layers[1]
+        Q2 = B * 2 * n[2]
+        wmacs = t1["out_c"] * t2["k"] ** 2 * t1["in_c"] * t1["k"] ** 2
+        add("pass2_window[layer1,pass2]", 2.0 * Q2 * wmacs, 4.0 * (3 * B * n[1] + Q2))
     for k in range(2, L + 1):
         R = 2 * n[k] if k < L else S
         Q = B * R
@@ -64,8 +74,9 @@ def stage_work(layers, S, B):
     return work
 
 
-def total_flops(layers, S, B):
-    return sum(f for f, _ in stage_work(layers, S, B).values())
+def path_flops(layers, S, B, launched):
+    """Algorithmic flops of one step over the kernel classes that were launched."""
+    return sum(f for cls, (f, _) in stage_work(layers, S, B).items() if cls in launched)
 
 
 def cpu_baseline(w, budget_s=20.0):
@@ -226,7 +237,7 @@ def main():
                              if optimise else "upper slope"),
                    "ws_gib": round(ws_bytes / 2**30, 2)},
         "path_tflops": (None if optimise else
-                        round(total_flops(w.layers, S, B) / (ms / 1e3) / 1e12, 3)),
+                        round(path_flops(w.layers, S, B, times) / (ms / 1e3) / 1e12, 3)),
         "roofline": roof,
         "stages": stages,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_budget),

@@ -492,7 +492,7 @@ __device__ __forceinline__ void block_finish(const Sink& s, Acc acc, float* red,
 // The y1 loop is unrolled over the rotation period so every register index is static.
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CPW, int NW,
           int MODE, bool TAPE>
-__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, MODE == MODE_BOUND && !TAPE ? 4 : 2)))
 k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
   static_assert(K <= 4 && S <= K && CO % 4 == 0 && W0 % 4 == 0, "unsupported geometry");
   constexpr int KS = CO / 4;
@@ -1051,26 +1051,42 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;  // window origin on g^(1)
   const int H1 = t1.out_h, Wd1 = t1.out_w;
 
-  // (1) relaxed window coefficients of the 16 rows, and their bias terms
+  // (1) relaxed window coefficients of the 16 rows, and their bias terms.  The rows share the
+  // window, so its neurons' relaxation parameters are staged once (zeros outside the map).
+  __shared__ float prm[4][C1 * NPOS];  // a_lo, a_up, b_up, W1 x0 + b1
   {
-    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
-    const int c2 = cb * 16 + row;
-    float bpart = 0.f;
     const long pb = b * pstride;
-    for (int e = part; e < C1 * NPOS; e += RPT) {
+    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) {
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
       const int y1 = Y1 + ky2, x1 = X1 + kx2;
-      float v = 0.f;
+      float lo = 0.f, up = 0.f, bu = 0.f, z = 0.f;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
-        const float w = sgn * t2.W[(((long)c2 * t2.in_c + c1) * t2.k + ky2) * t2.k + kx2];
         const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
-        const long pi = pb + ni;
-        v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
-        bpart = fmaf(fminf(w, 0.f), b_up[pi], bpart);
-        // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
-        bpart = fmaf(v, z1[ni], bpart);
+        lo = a_lo[pb + ni];
+        up = a_up[pb + ni];
+        bu = b_up[pb + ni];
+        z = z1[ni];
       }
+      prm[0][e] = lo;
+      prm[1][e] = up;
+      prm[2][e] = bu;
+      prm[3][e] = z;
+    }
+  }
+  __syncthreads();
+  {
+    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const int c2 = cb * 16 + row;
+    const float* w2 = t2.W + (long)c2 * C1 * NPOS;  // [C1][K2][K2] of output channel c2
+    float bpart = 0.f;
+    for (int e = part; e < C1 * NPOS; e += RPT) {
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      const float w = sgn * w2[e];
+      const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
+      bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
+      // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
+      bpart = fmaf(v, prm[3][e], bpart);
       tile[c1 * CS + pos * 16 + row] = v;
     }
     bred[part * 16 + row] = bpart;
@@ -1222,22 +1238,33 @@ __global__ void __launch_bounds__(64 * NW)
     return;
   }
 
-  // (1) relaxed window coefficients (as in the bound)
+  // (1) relaxed window coefficients (as in the bound; window parameters staged once)
+  __shared__ float prm[2][C1 * NPOS];  // a_lo, a_up (zeros outside the map)
   {
-    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
-    const int c2 = cb * 16 + row;
     const long pb = b * pstride;
-    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
+    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) {
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
       const int y1 = Y1 + ky2, x1 = X1 + kx2;
-      float v = 0.f;
+      float lo = 0.f, up = 0.f;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
-        const float w = sgn * t2.W[(((long)c2 * t2.in_c + c1) * t2.k + ky2) * t2.k + kx2];
         const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
-        v = w >= 0.f ? w * a_lo[pi] : w * a_up[pi];
+        lo = a_lo[pi];
+        up = a_up[pi];
       }
-      tile[c1 * CS + pos * 16 + row] = v;
+      prm[0][e] = lo;
+      prm[1][e] = up;
+    }
+  }
+  __syncthreads();
+  {
+    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
+    const int c2 = cb * 16 + row;
+    const float* w2 = t2.W + (long)c2 * C1 * NPOS;
+    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      const float w = sgn * w2[e];
+      tile[c1 * CS + pos * 16 + row] = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
     }
   }
   __syncthreads();
