@@ -1006,6 +1006,21 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
   sink_finish<MODE_SLAB>(s, a, q, q / R, q % R, false);
 }
 
+// The 16 rows +-e_j of a receptive-field pass-2 block share the window (y2, x2) of one
+// sub-domain.  Output channels C2 a multiple of 16: one sign and 16 consecutive channels (block
+// group g = sign * C2/16 + channel block); C2 = 8: both signs of all 8 channels (row r: sign
+// r / 8, channel r % 8).  Blocks are ordered (sub-domain, group, y2, x2), x2 fastest.
+struct P2Row {
+  int c2;
+  bool neg;
+};
+__device__ __forceinline__ P2Row p2_row(int C2, int g, int r) {
+  if (C2 == 8) return {r & 7, r >= 8};
+  const int ncb = C2 / 16;
+  return {(g % ncb) * 16 + r, g >= ncb};
+}
+__host__ __device__ inline int p2_groups(int C2) { return C2 == 8 ? 1 : 2 * (C2 / 16); }
+
 // Pass 2 restricted to each row's receptive field, when T_2 and T_1 are convolutions.
 // Row +-e_j of h^(2), j = (c2, y2, x2), carried through T_2 is +-W_2[c2] placed on the window
 // (y2*S2 - P2 + ky2, x2*S2 - P2 + kx2) of g^(1) and zero elsewhere, so its image under the
@@ -1038,16 +1053,14 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, G = lane >> 4;
-  // block -> (sub-domain, sign, c2 block, y2, x2)
+  // block -> (sub-domain, row group, y2, x2)
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
-  const int ncb = C2 / 16;
+  const int NG = p2_groups(C2);
   long blk = blockIdx.x;
   const int x2 = (int)(blk % W2); blk /= W2;
   const int y2 = (int)(blk % H2); blk /= H2;
-  const int cb = (int)(blk % ncb); blk /= ncb;
-  const int sgn_neg = (int)(blk % 2); blk /= 2;
+  const int g = (int)(blk % NG); blk /= NG;
   const long b = blk;
-  const float sgn = sgn_neg ? -1.f : 1.f;
   const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;  // window origin on g^(1)
   const int H1 = t1.out_h, Wd1 = t1.out_w;
 
@@ -1077,8 +1090,9 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   __syncthreads();
   {
     const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
-    const int c2 = cb * 16 + row;
-    const float* w2 = t2.W + (long)c2 * C1 * NPOS;  // [C1][K2][K2] of output channel c2
+    const P2Row pr = p2_row(C2, g, row);
+    const float sgn = pr.neg ? -1.f : 1.f;
+    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;  // [C1][K2][K2] of output channel c2
     float bpart = 0.f;
     for (int e = part; e < C1 * NPOS; e += RPT) {
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
@@ -1165,13 +1179,13 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   __syncthreads();
   if (threadIdx.x >= 16) return;
   const int row = threadIdx.x;
-  const int c2 = cb * 16 + row;
-  float ta = 0.f, tb = sgn * t2.b[c2];
+  const P2Row pr = p2_row(C2, g, row);
+  float ta = 0.f, tb = (pr.neg ? -1.f : 1.f) * t2.b[pr.c2];
   for (int w = 0; w < NW; ++w) ta += red[w * 16 + row];
   for (int r = 0; r < RPT; ++r) tb += bred[r * 16 + row];
   const float v = tb - eps * ta;
-  const long j = ((long)c2 * H2 + y2) * W2 + x2;
-  if (sgn_neg)
+  const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
+  if (pr.neg)
     U[b * n_relu + off2 + j] = -v;
   else
     L[b * n_relu + off2 + j] = v;
@@ -1210,23 +1224,21 @@ __global__ void __launch_bounds__(64 * NW)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, G = lane >> 4;
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
-  const int ncb = C2 / 16;
+  const int NG = p2_groups(C2);
   long blk = blockIdx.x;
   const long blk_id = blk;
   const int x2 = (int)(blk % W2); blk /= W2;
   const int y2 = (int)(blk % H2); blk /= H2;
-  const int cb = (int)(blk % ncb); blk /= ncb;
-  const int sgn_neg = (int)(blk % 2); blk /= 2;
+  const int g = (int)(blk % NG); blk /= NG;
   const long b = blk;
-  const float sgn = sgn_neg ? -1.f : 1.f;
   const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;
   const int H1 = t1.out_h, Wd1 = t1.out_w;
   float* out = part + blk_id * (long)(C1 * NPOS);
 
   if (threadIdx.x < 16) {
-    const int c2 = cb * 16 + threadIdx.x;
-    const long j = ((long)c2 * H2 + y2) * W2 + x2;
-    const float wv = sgn_neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
+    const P2Row pr = p2_row(C2, g, threadIdx.x);
+    const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
+    const float wv = pr.neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
     wrow[threadIdx.x] = wv;
   }
   if (threadIdx.x == 0) active = 0;
@@ -1259,8 +1271,9 @@ __global__ void __launch_bounds__(64 * NW)
   __syncthreads();
   {
     const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
-    const int c2 = cb * 16 + row;
-    const float* w2 = t2.W + (long)c2 * C1 * NPOS;
+    const P2Row pr = p2_row(C2, g, row);
+    const float sgn = pr.neg ? -1.f : 1.f;
+    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;
     for (int e = partid; e < C1 * NPOS; e += NT / 16) {
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const float w = sgn * w2[e];
@@ -1336,7 +1349,9 @@ __global__ void __launch_bounds__(64 * NW)
     const int nks = (KD + 3) / 4;
     const int c1A = lane & 15;
     const float wn = wrow[n];
-    const int c2n = cb * 16 + n;
+    const P2Row prn = p2_row(C2, g, n);
+    const int c2n = prn.c2;
+    const float sgn = prn.neg ? -1.f : 1.f;
     for (int pos = wave; pos < NPOS; pos += NW) {
       const int j = pos / K2, i = pos - j * K2;
       const int y1 = Y1 + j, x1 = X1 + i;
@@ -1388,11 +1403,10 @@ __global__ void __launch_bounds__(kBlock)
   const int hw = t1.out_h * t1.out_w;
   const int c1 = (int)(ni / hw), y1 = (int)((ni / t1.out_w) % t1.out_h), x1 = (int)(ni % t1.out_w);
   const int H2 = t2.out_h, W2 = t2.out_w, K2 = t2.k, S2 = t2.stride, P2 = t2.pad;
-  const int ncb = t2.out_c / 16;
+  const int NG = p2_groups(t2.out_c);
   const int C1 = t1.out_c;
   float acc = 0.f;
-  for (int sg = 0; sg < 2; ++sg)
-    for (int cb = 0; cb < ncb; ++cb)
+  for (int g = 0; g < NG; ++g)
       for (int ky2 = 0; ky2 < K2; ++ky2) {
         const int yn = y1 + P2 - ky2;
         if (yn < 0 || yn % S2) continue;
@@ -1403,7 +1417,7 @@ __global__ void __launch_bounds__(kBlock)
           if (xn < 0 || xn % S2) continue;
           const int x2 = xn / S2;
           if (x2 >= W2) continue;
-          const long blk = (((b * 2 + sg) * ncb + cb) * H2 + y2) * W2 + x2;
+          const long blk = ((b * NG + g) * H2 + y2) * W2 + x2;
           acc += part[(blk * C1 + c1) * NPOS + ky2 * K2 + kx2];
         }
       }
@@ -1783,7 +1797,7 @@ Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
   if (net->L < 3) return nullptr;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
   if (t1.kind != LIRPA_CONV2D || t2.kind != LIRPA_CONV2D) return nullptr;
-  if (t2.out_c % 16 || t1.in_c > 8) return nullptr;
+  if ((t2.out_c % 16 && t2.out_c != 8) || t1.in_c > 8) return nullptr;
   *nw = t1.in_c;
   if (t1.k == 4 && t1.stride == 2 && t1.pad == 1) {
     if (t2.k == 4 && t1.out_c == 8) {
@@ -1814,7 +1828,7 @@ Pass2GradKernel pass2_grad_kernel_for(const lirpa_net* net) {
 
 long pass2_blocks(const lirpa_net* net, long nb) {
   const lirpa_layer& t2 = net->T[1];
-  return nb * 2 * (t2.out_c / 16) * t2.out_h * t2.out_w;
+  return nb * p2_groups(t2.out_c) * t2.out_h * t2.out_w;
 }
 
 Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
@@ -2141,7 +2155,7 @@ int pass2_window(const Chunk& c) {
   Pass2Kernel kern = pass2_kernel_for(net, &nw);
   if (!kern) return 1;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
-  long blocks = c.nb * 2 * (t2.out_c / 16) * t2.out_h * t2.out_w;
+  long blocks = pass2_blocks(net, c.nb);
   const float* alo = at<float>(c.ws, c.p->off_alo) + net->poff[1];
   const float* aup = at<float>(c.ws, c.p->off_aup) + net->poff[1];
   const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
