@@ -79,6 +79,26 @@ def path_flops(layers, S, B, launched):
     return sum(f for cls, (f, _) in stage_work(layers, S, B).items() if cls in launched)
 
 
+def traffic_record(workload, kernel):
+    """HBM bytes per launch of a kernel class, as measured by rocprofv3 (FETCH_SIZE and
+    WRITE_SIZE, scaled by a copy of known size) and recorded under profiles/ for this exact
+    library source (sha256 of lirpa.hip); None when no record matches."""
+    import glob
+    import hashlib
+    src = os.path.join(ROOT, "paper_2011_13824_amd", "csrc", "lirpa.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as fh:
+            for line in fh:
+                if not line.startswith("traffic-record: "):
+                    continue
+                rec = json.loads(line[len("traffic-record: "):])
+                if (rec.get("workload"), rec.get("kernel"), rec.get("source_sha256")) == \
+                        (workload, kernel, sha):
+                    return rec["read_bytes"] + rec["write_bytes"]
+    return None
+
+
 def cpu_baseline(w, budget_s=20.0):
     """The fp64 oracle, as it is, on a bounded sample of the same workload recipe."""
     from oracle import ref
@@ -216,7 +236,7 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["avg_launch_ms"] = round(tot_ms / launches, 4)
-    roof["traffic"] = None
+    roof["traffic"] = None if args.batch else traffic_record(w.name, dom)
 
     out = {
         "metric": METRIC,
