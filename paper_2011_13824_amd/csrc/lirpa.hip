@@ -1033,7 +1033,7 @@ __host__ __device__ inline int p2_groups(int C2) { return C2 == 8 ? 1 : 2 * (C2 
 //  (3) concretises the footprint (Eq. 8; positions outside the image are zero padding) and
 //      writes l_j (sign +) or u_j (sign -) of the sub-domain.
 // The result equals the dense pass exactly in arithmetic terms: the skipped products are zeros.
-template <int K1, int S1, int P1, int K2, int C1, int NW>
+template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
 __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                const float* __restrict__ z1, float eps, float* __restrict__ L,
@@ -1042,72 +1042,70 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   constexpr int KS = C1 / 4;
   constexpr int NT = 64 * NW;
   constexpr int NPOS = K2 * K2;
+  constexpr int NE = C1 * NPOS;                      // window entries per row
   constexpr int WO = (K2 - 1) * S1 + K1;           // footprint width on the input
   constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
   constexpr int CS = NPOS * 16 + (80 - (NPOS * 16) % 64) % 64;  // channel stride, 16 mod 64
   constexpr int NEL = C1 * CS;                      // relaxed window tile
   constexpr int RPT = NT / 16;                      // threads per row in phase 1
+  constexpr int NEP = (NE + RPT - 1) / RPT;         // window entries per thread (phase 1)
+  constexpr int NPP = (NE + NT - 1) / NT;           // staged parameters per thread
   __shared__ float tile[NEL];
-  __shared__ float red[NW * 3 * 16 + RPT * 16];
-  float* bred = red + NW * 3 * 16;
+  __shared__ float red[NW * 16 + RPT * 16];
+  __shared__ float prm[4][NE];  // a_lo, a_up, b_up, W1 x0 + b1 of the window (0 outside)
+  float* bred = red + NW * 16;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = lane & 15, G = lane >> 4;
-  // block -> (sub-domain, row group, y2, x2)
+  // block -> (sub-domain, row group, y2, XW consecutive windows along x2)
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
+  const int nxc = W2 / XW;
   long blk = blockIdx.x;
-  const int x2 = (int)(blk % W2); blk /= W2;
+  const int x2c = (int)(blk % nxc); blk /= nxc;
   const int y2 = (int)(blk % H2); blk /= H2;
   const int g = (int)(blk % NG); blk /= NG;
   const long b = blk;
-  const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;  // window origin on g^(1)
+  const int Y1 = y2 * t2.stride - t2.pad;  // window origin on g^(1), rows
   const int H1 = t1.out_h, Wd1 = t1.out_w;
+  const long pb = b * pstride;
 
-  // (1) relaxed window coefficients of the 16 rows, and their bias terms.  The rows share the
-  // window, so its neurons' relaxation parameters are staged once (zeros outside the map).
-  __shared__ float prm[4][C1 * NPOS];  // a_lo, a_up, b_up, W1 x0 + b1
+  // this thread's entries of W_2 (phase 1: row = tid mod 16, entries part, part + RPT, ...),
+  // the same for every window of the block
+  const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
+  const P2Row prw = p2_row(C2, g, row);
+  const float sgn = prw.neg ? -1.f : 1.f;
+  float w2r[NEP];
   {
-    const long pb = b * pstride;
-    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) {
+    const float* w2 = t2.W + (long)prw.c2 * NE;  // [C1][K2][K2] of output channel c2
+#pragma unroll
+    for (int k = 0; k < NEP; ++k) {
+      const int e = part + k * RPT;
+      w2r[k] = e < NE ? sgn * w2[e] : 0.f;
+    }
+  }
+  // relaxation parameters of a window, one neuron per (thread, k)
+  float pn[NPP][4];
+  auto pfetch = [&](int X1) {
+#pragma unroll
+    for (int k = 0; k < NPP; ++k) {
+      const int e = threadIdx.x + k * NT;
+      pn[k][0] = pn[k][1] = pn[k][2] = pn[k][3] = 0.f;
+      if (e >= NE) continue;
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
       const int y1 = Y1 + ky2, x1 = X1 + kx2;
-      float lo = 0.f, up = 0.f, bu = 0.f, z = 0.f;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
         const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
-        lo = a_lo[pb + ni];
-        up = a_up[pb + ni];
-        bu = b_up[pb + ni];
-        z = z1[ni];
+        pn[k][0] = a_lo[pb + ni];
+        pn[k][1] = a_up[pb + ni];
+        pn[k][2] = b_up[pb + ni];
+        pn[k][3] = z1[ni];
       }
-      prm[0][e] = lo;
-      prm[1][e] = up;
-      prm[2][e] = bu;
-      prm[3][e] = z;
     }
-  }
-  __syncthreads();
-  {
-    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
-    const P2Row pr = p2_row(C2, g, row);
-    const float sgn = pr.neg ? -1.f : 1.f;
-    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;  // [C1][K2][K2] of output channel c2
-    float bpart = 0.f;
-    for (int e = part; e < C1 * NPOS; e += RPT) {
-      const int c1 = e / NPOS, pos = e - c1 * NPOS;
-      const float w = sgn * w2[e];
-      const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
-      bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
-      // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
-      bpart = fmaf(v, prm[3][e], bpart);
-      tile[c1 * CS + pos * 16 + row] = v;
-    }
-    bred[part * 16 + row] = bpart;
-  }
-  __syncthreads();
+  };
 
-  // (2) T_1^T on the window, one wave per input channel c0 of T_1
+  // T_1^T weights, one wave per input channel c0 of T_1
   const int c0 = wave;
   const bool cok = c0 < t1.in_c;
   float wreg[PER][KS];
@@ -1125,70 +1123,111 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
     }
   }
   const int Hi = t1.in_h, Wi = t1.in_w;
-  const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;  // footprint origin on the input
-  float l1 = 0.f;
-  float acc[WO];
+  const int OY = Y1 * S1 - P1;  // footprint origin on the input, rows
+
+  pfetch(x2c * XW * t2.stride - t2.pad);
+  for (int xi = 0; xi < XW; ++xi) {
+    const int x2 = x2c * XW + xi;
+    const int X1 = x2 * t2.stride - t2.pad;
+    // (1) stage the window's parameters; fetch the next window's; relaxed coefficients of the
+    // 16 rows and their bias terms
 #pragma unroll
-  for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-  const bool inside_x = OX >= 0 && OX + WO <= Wi;
-  auto emit = [&](int yl) {  // local footprint row yl of channel c0: ||.||_1 of the clipped row
-    const int y = OY + yl;
-    if (!cok || y < 0 || y >= Hi) return;
-    if (inside_x) {
-#pragma unroll
-      for (int x = 0; x < WO; ++x) l1 += fabsf(acc[x]);
-    } else {
-#pragma unroll
-      for (int x = 0; x < WO; ++x) {
-        const int xi = OX + x;
-        l1 += (xi >= 0 && xi < Wi) ? fabsf(acc[x]) : 0.f;
+    for (int k = 0; k < NPP; ++k) {
+      const int e = threadIdx.x + k * NT;
+      if (e < NE) {
+        prm[0][e] = pn[k][0];
+        prm[1][e] = pn[k][1];
+        prm[2][e] = pn[k][2];
+        prm[3][e] = pn[k][3];
       }
     }
-  };
+    __syncthreads();
+    if (xi + 1 < XW) pfetch(X1 + t2.stride);
+    {
+      float bpart = 0.f;
 #pragma unroll
-  for (int j = 0; j < K2; ++j) {
-    const int ph = j % PER;
-#pragma unroll
-    for (int i = 0; i < K2; ++i) {
-      const int pos = j * K2 + i;
-      float4v d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
-                                                tile[(4 * ks + G) * CS + pos * 16 + n], d,
-                                                0, 0, 0);
-#pragma unroll
-      for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+      for (int k = 0; k < NEP; ++k) {
+        const int e = part + k * RPT;
+        if (e >= NE) break;
+        const int c1 = e / NPOS, pos = e - c1 * NPOS;
+        const float w = w2r[k];
+        const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
+        bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
+        // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
+        bpart = fmaf(v, prm[3][e], bpart);
+        tile[c1 * CS + pos * 16 + row] = v;
+      }
+      bred[part * 16 + row] = bpart;
     }
-    const int ky = ((G - ph * S1) % K1 + K1) % K1;
-    if (G < K1 && ky < S1) {
-      emit(j * S1 + ky);
-#pragma unroll
-      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-    }
-  }
-  {
-    const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
-    if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
-  }
+    __syncthreads();
 
-  // (3) reduce over lane groups and waves; add the bias terms; write the bound
-  l1 += __shfl_xor(l1, 16, 64);
-  l1 += __shfl_xor(l1, 32, 64);
-  if (lane < 16) red[wave * 16 + lane] = l1;
-  __syncthreads();
-  if (threadIdx.x >= 16) return;
-  const int row = threadIdx.x;
-  const P2Row pr = p2_row(C2, g, row);
-  float ta = 0.f, tb = (pr.neg ? -1.f : 1.f) * t2.b[pr.c2];
-  for (int w = 0; w < NW; ++w) ta += red[w * 16 + row];
-  for (int r = 0; r < RPT; ++r) tb += bred[r * 16 + row];
-  const float v = tb - eps * ta;
-  const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
-  if (pr.neg)
-    U[b * n_relu + off2 + j] = -v;
-  else
-    L[b * n_relu + off2 + j] = v;
+    // (2) T_1^T on the window
+    const int OX = X1 * S1 - P1;
+    float l1 = 0.f;
+    float acc[WO];
+#pragma unroll
+    for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+    const bool inside_x = OX >= 0 && OX + WO <= Wi;
+    auto emit = [&](int yl) {  // local footprint row yl of channel c0: ||.||_1 of the clipped row
+      const int y = OY + yl;
+      if (!cok || y < 0 || y >= Hi) return;
+      if (inside_x) {
+#pragma unroll
+        for (int x = 0; x < WO; ++x) l1 += fabsf(acc[x]);
+      } else {
+#pragma unroll
+        for (int x = 0; x < WO; ++x) {
+          const int xc = OX + x;
+          l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
+        }
+      }
+    };
+#pragma unroll
+    for (int j = 0; j < K2; ++j) {
+      const int ph = j % PER;
+#pragma unroll
+      for (int i = 0; i < K2; ++i) {
+        const int pos = j * K2 + i;
+        float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
+                                                  tile[(4 * ks + G) * CS + pos * 16 + n], d,
+                                                  0, 0, 0);
+#pragma unroll
+        for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+      }
+      const int ky = ((G - ph * S1) % K1 + K1) % K1;
+      if (G < K1 && ky < S1) {
+        emit(j * S1 + ky);
+#pragma unroll
+        for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+      }
+    }
+    {
+      const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
+      if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
+    }
+
+    // (3) reduce over lane groups and waves; add the bias terms; write the bound
+    l1 += __shfl_xor(l1, 16, 64);
+    l1 += __shfl_xor(l1, 32, 64);
+    if (lane < 16) red[wave * 16 + lane] = l1;
+    __syncthreads();
+    if (threadIdx.x < 16) {
+      const int r = threadIdx.x;
+      const P2Row pr = p2_row(C2, g, r);
+      float ta = 0.f, tb = (pr.neg ? -1.f : 1.f) * t2.b[pr.c2];
+      for (int w = 0; w < NW; ++w) ta += red[w * 16 + r];
+      for (int q = 0; q < RPT; ++q) tb += bred[q * 16 + r];
+      const float v = tb - eps * ta;
+      const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
+      if (pr.neg)
+        U[b * n_relu + off2 + j] = -v;
+      else
+        L[b * n_relu + off2 + j] = v;
+    }
+  }
 }
 
 // Reverse sweep of the receptive-field pass 2.  Layer-1 bounds do not depend on alpha, so the
@@ -1793,21 +1832,24 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Kernel for the receptive-field pass 2, or null when the shapes do not qualify.
 using Pass2Kernel = void (*)(DLayer, DLayer, long, const float*, const float*, const float*, long,
                              const float*, float, float*, float*, long, long);
+constexpr int kP2XW = 4;  // windows per block of the receptive-field pass 2 (along x2)
+
 Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
   if (net->L < 3) return nullptr;
+  if (net->T[1].out_w % kP2XW) return nullptr;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
   if (t1.kind != LIRPA_CONV2D || t2.kind != LIRPA_CONV2D) return nullptr;
   if ((t2.out_c % 16 && t2.out_c != 8) || t1.in_c > 8) return nullptr;
   *nw = t1.in_c;
   if (t1.k == 4 && t1.stride == 2 && t1.pad == 1) {
     if (t2.k == 4 && t1.out_c == 8) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 8, 3>;
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 8, 3, kP2XW>;
     }
     if (t2.k == 4 && t1.out_c == 16) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 16, 3>;
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 16, 3, kP2XW>;
     }
     if (t2.k == 3 && t1.out_c == 8) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 3, 8, 3>;
+      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 3, 8, 3, kP2XW>;
     }
   }
   return nullptr;
@@ -2155,7 +2197,7 @@ int pass2_window(const Chunk& c) {
   Pass2Kernel kern = pass2_kernel_for(net, &nw);
   if (!kern) return 1;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
-  long blocks = pass2_blocks(net, c.nb);
+  long blocks = pass2_blocks(net, c.nb) / kP2XW;
   const float* alo = at<float>(c.ws, c.p->off_alo) + net->poff[1];
   const float* aup = at<float>(c.ws, c.p->off_aup) + net->poff[1];
   const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
