@@ -1006,6 +1006,324 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
   sink_finish<MODE_SLAB>(s, a, q, q / R, q % R, false);
 }
 
+// The last two backward stages of a pass fused: T_2^T with the relaxation of layer 1, then T_1^T
+// with the concretisation (Eq. 6-8), for 16 rows per block.  The coefficients over g^(1) never
+// leave LDS.  Wave roles, all of them stepping through the same barriers t = 0 .. H1 + 2:
+//   matrix waves (one per channel of g^(1)): T_2^T on input row t as in k_convT_relax_ws; the
+//     rows over g^(1) completed at step t ("stage t"; stage H1 = the rows still open after the
+//     last input row) are parked, unrelaxed, in slot t mod 3 of an LDS ring, and the layer-1
+//     relaxation parameters of stage t are staged in LDS; every global load is theirs;
+//   storer waves: relax stage t-1 in place (Eq. 6) and accumulate each row's intercept and bias
+//     terms;
+//   x waves (one per input channel of T_1): T_1^T over the rows of stage t-2, in increasing
+//     order, with the rotating lane-group scheme, accumulating ||A_x||_1 per row.
+// The bound of each row is then beta - eps ||A_x||_1 (the linear term sits in the layer-1 bias).
+template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int NS, int K1,
+          int S1, int P1, int HX, int WX, int C0>
+__global__ void __launch_bounds__(64 * (CI + NS + C0))
+    k_convT2_bound(DLayer t, DLayer t1, const float* __restrict__ in, unsigned ldq, unsigned Q,
+                   Sink s) {
+  static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0, "geometry");
+  static_assert(K1 <= 4 && S1 <= K1 && WX % 4 == 0, "geometry");
+  static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
+  static_assert((H0 - 1) * S1 - P1 + K1 >= HX, "every input row of T_1 is reached");
+  constexpr int NM = CI;                         // matrix waves
+  constexpr int NTM = 64 * NM;
+  constexpr int KS = CO / 4, KS1 = CI / 4;
+  constexpr int PER = (K % S == 0) ? K / S : K;
+  constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
+  constexpr int TILE = CO * CS;
+  constexpr int NV4 = CO * W1 * 4;
+  constexpr int PF = (NV4 + NTM - 1) / NTM;
+  constexpr int RSL = S > K - S ? S : K - S;      // rows per stage (max)
+  constexpr int CS1 = W0 * 16 + (80 - (W0 * 16) % 64) % 64;  // ring: channel stride
+  constexpr int ROWF = CI * CS1;                 // ring: one row over g^(1), [CI][W0][16 q]
+  constexpr int SLOT = RSL * ROWF;
+  constexpr int PB = 2 * 4 * RSL * CI * W0;      // parameters: [2 sub-domains][4][RSL][CI][W0]
+  constexpr int NPV4 = PB / 4;
+  constexpr int PP = (NPV4 + NTM - 1) / NTM;
+  extern __shared__ float lds[];
+  float* tiles = lds;                // 2 x TILE
+  float* ring = tiles + 2 * TILE;    // 3 x SLOT
+  float* pars = ring + 3 * SLOT;     // 2 x PB
+  float* red = pars + 2 * PB;        // (NS + C0) x 16
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  const unsigned R = (unsigned)s.R;
+  const unsigned b0 = q0 / R;
+  const unsigned b1 = (min(q0 + 15u, Q - 1u)) / R;  // b0 or b0 + 1
+  auto yrow = [&](int e, int r) { return e < H1 ? e * S - P + r : (H1 - 1) * S - P + S + r; };
+  auto nrows = [&](int e) { return e < H1 ? S : K - S; };
+  constexpr int NSTEP = H1 + 3;
+
+  if (wave < NM) {
+    // ------------------------------------------------------------------ matrix waves
+    const int n = lane & 15, G = lane >> 4;
+    const int tid = threadIdx.x;
+    float wreg[PER][KS];
+    {
+      const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+      for (int ph = 0; ph < PER; ++ph) {
+        const int ky = ((slot - ph * S) % K + K) % K;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int co = 4 * ks + G;
+          wreg[ph][ks] = (slot < K && kx < K) ? t.W[((co * CI + wave) * K + ky) * K + kx] : 0.f;
+        }
+      }
+    }
+    auto gaddr = [&](int y1, int v4) {
+      const int cx = v4 >> 2, j4 = v4 & 3;
+      const int co = cx / W1, x1 = cx - co * W1;
+      return in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4;
+    };
+    auto loff = [&](int v4) {
+      const int cx = v4 >> 2, j4 = v4 & 3;
+      const int co = cx / W1, x1 = cx - co * W1;
+      return co * CS + x1 * 16 + j4 * 4;
+    };
+    auto pload = [&](int e, int v, float4v& out) {
+      const int x4 = v % (W0 / 4);
+      const int c = (v / (W0 / 4)) % CI;
+      const int r = (v / (W0 / 4 * CI)) % RSL;
+      const int arr = (v / (W0 / 4 * CI * RSL)) % 4;
+      const int bsel = v / (W0 / 4 * CI * RSL * 4);
+      const int y = yrow(e, r);
+      out = float4v{0.f, 0.f, 0.f, 0.f};
+      if (r >= nrows(e) || y < 0 || y >= H0 || b0 + bsel > b1) return;
+      const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * x4;
+      const long pb = (long)(b0 + bsel) * s.pstride + rowi;
+      const float* src = arr == 0 ? s.a_lo + pb : arr == 1 ? s.a_up + pb
+                       : arr == 2 ? s.b_up + pb : s.bias + rowi;
+      out = *reinterpret_cast<const float4v*>(src);
+    };
+    auto park = [&](int t_, int r, const float* v) {
+      float* dst = ring + (t_ % 3) * SLOT + r * ROWF + wave * CS1 + n;
+#pragma unroll
+      for (int x = 0; x < W0; ++x) dst[x * 16] = v[x];
+    };
+
+    for (int v4 = tid; v4 < NV4; v4 += NTM)
+      *reinterpret_cast<float4v*>(tiles + loff(v4)) =
+          *reinterpret_cast<const float4v*>(gaddr(0, v4));
+    lds_barrier();
+
+    float acc[W0];
+#pragma unroll
+    for (int x = 0; x < W0; ++x) acc[x] = 0.f;
+
+    for (int ybase = 0; ybase < H1; ybase += PER) {
+#pragma unroll
+      for (int ph = 0; ph < PER; ++ph) {
+        const int y1 = ybase + ph;
+        if (H1 % PER != 0 && y1 >= H1) break;
+        const float* tile = tiles + (y1 & 1) * TILE;
+        const bool more = y1 + 1 < H1;
+        float4v pf[PF], pp[PP];
+#pragma unroll
+        for (int k = 0; k < PF; ++k) {
+          const int v4 = min(tid + k * NTM, NV4 - 1);
+          pf[k] = *reinterpret_cast<const float4v*>(gaddr(more ? y1 + 1 : y1, v4));
+        }
+#pragma unroll
+        for (int k = 0; k < PP; ++k) pload(y1, min(tid + k * NTM, NPV4 - 1), pp[k]);
+#pragma unroll
+        for (int x1 = 0; x1 < W1; ++x1) {
+          float bv[KS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(4 * ks + G) * CS + x1 * 16 + n];
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks], bv[ks], d, 0, 0, 0);
+#pragma unroll
+          for (int kx = 0; kx < K; ++kx) {
+            const int col = x1 * S - P + kx;
+            if (col >= 0 && col < W0) acc[col] += d[kx];
+          }
+        }
+        if (more) {
+          float* nt = tiles + ((y1 + 1) & 1) * TILE;
+#pragma unroll
+          for (int k = 0; k < PF; ++k) {
+            const int v4 = tid + k * NTM;
+            if (v4 < NV4) *reinterpret_cast<float4v*>(nt + loff(v4)) = pf[k];
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < PP; ++k) {
+          const int v = tid + k * NTM;
+          if (v < NPV4) *reinterpret_cast<float4v*>(pars + (y1 & 1) * PB + 4 * v) = pp[k];
+        }
+        const int ky = ((G - ph * S) % K + K) % K;
+        if (G < K && ky < S) {
+          park(y1, ky, acc);
+#pragma unroll
+          for (int x = 0; x < W0; ++x) acc[x] = 0.f;
+        }
+        lds_barrier();
+      }
+    }
+    {  // step H1: the rows still open, and their parameters
+      float4v pp[PP];
+#pragma unroll
+      for (int k = 0; k < PP; ++k) pload(H1, min(tid + k * NTM, NPV4 - 1), pp[k]);
+      constexpr int ph_last = (H1 - 1) % PER;
+      const int ky = ((G - ph_last * S) % K + K) % K;
+      if (G < K && ky >= S) park(H1, ky - S, acc);
+#pragma unroll
+      for (int k = 0; k < PP; ++k) {
+        const int v = tid + k * NTM;
+        if (v < NPV4) *reinterpret_cast<float4v*>(pars + (H1 & 1) * PB + 4 * v) = pp[k];
+      }
+    }
+    for (int st = H1; st < NSTEP; ++st) lds_barrier();
+    lds_barrier();  // final reduction
+    return;
+  }
+
+  if (wave < NM + NS) {
+    // ------------------------------------------------------------------ storer waves
+    const int ws = wave - NM;
+    const int qn = lane & 15, xg = lane >> 4;
+    const unsigned q = q0 + qn;
+    const bool qok = q < Q;
+    const int bsel = qok ? (int)(q / R - b0) : 0;
+    float beta = 0.f;
+    auto stage = [&](int e) {
+      float* slot = ring + (e % 3) * SLOT;
+      const float* pslot = pars + (e & 1) * PB;
+      const int nr = nrows(e);
+      for (int it = ws; it < nr * CI; it += NS) {
+        const int r = it / CI, c = it - r * CI;
+        const int y = yrow(e, r);
+        if (y < 0 || y >= H0) continue;
+        float* row = slot + r * ROWF + c * CS1 + qn;
+        constexpr int AST = RSL * CI * W0;
+        const float* pbase = pslot + ((bsel * 4) * RSL + r) * CI * W0 + c * W0 + 4 * xg;
+        const float4v lo = *reinterpret_cast<const float4v*>(pbase);
+        const float4v up = *reinterpret_cast<const float4v*>(pbase + AST);
+        const float4v bu = *reinterpret_cast<const float4v*>(pbase + 2 * AST);
+        const float4v bz = *reinterpret_cast<const float4v*>(pbase + 3 * AST);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int x = 4 * xg + j;
+          const float a = row[x * 16];
+          const bool pos = a >= 0.f;
+          const float ah = a * (pos ? lo[j] : up[j]);
+          if (qok) {
+            beta = fmaf(pos ? 0.f : a, bu[j], beta);
+            beta = fmaf(ah, bz[j], beta);
+          }
+          row[x * 16] = ah;
+        }
+      }
+    };
+    lds_barrier();  // initial tile
+    for (int st = 0; st < NSTEP; ++st) {
+      if (st >= 1 && st <= H1 + 1) stage(st - 1);
+      lds_barrier();
+    }
+    beta += __shfl_xor(beta, 16, 64);
+    beta += __shfl_xor(beta, 32, 64);
+    if (lane < 16) red[ws * 16 + lane] = beta;
+    lds_barrier();
+    return;
+  }
+
+  // ---------------------------------------------------------------------- x waves
+  const int xw = wave - NM - NS;  // input channel c0 of T_1
+  const int n = lane & 15, G = lane >> 4;
+  float wreg1[PER1][KS1];
+  {
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER1; ++ph) {
+      const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks) {
+        const int c1 = 4 * ks + G;
+        wreg1[ph][ks] = (slot < K1 && kx < K1) ? t1.W[((c1 * C0 + xw) * K1 + ky) * K1 + kx]
+                                               : 0.f;
+      }
+    }
+  }
+  float acc1[WX];
+#pragma unroll
+  for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+  float l1 = 0.f;
+  auto emit = [&](int yx) {  // output row yx of channel xw: ||.||_1 over the image
+    if (yx < 0 || yx >= HX) return;
+#pragma unroll
+    for (int x = 0; x < WX; ++x) l1 += fabsf(acc1[x]);
+  };
+  // T_1^T over one row y of g^(1), held in `row` ([CI][W0][16 q] with channel stride CS1)
+  auto consume = [&](const float* row, int y) {
+    const int ph = y % PER1;
+    float wa[KS1];
+#pragma unroll
+    for (int ks = 0; ks < KS1; ++ks) {
+      wa[ks] = wreg1[0][ks];
+#pragma unroll
+      for (int p2 = 1; p2 < PER1; ++p2)
+        if (ph == p2) wa[ks] = wreg1[p2][ks];
+    }
+#pragma unroll
+    for (int x1 = 0; x1 < W0; ++x1) {
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], row[(4 * ks + G) * CS1 + x1 * 16 + n],
+                                                d, 0, 0, 0);
+#pragma unroll
+      for (int kx = 0; kx < K1; ++kx) {
+        const int col = x1 * S1 - P1 + kx;
+        if (col >= 0 && col < WX) acc1[col] += d[kx];
+      }
+    }
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    if (G < K1 && ky < S1) {
+      emit(y * S1 - P1 + ky);
+#pragma unroll
+      for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+    }
+  };
+  lds_barrier();  // initial tile
+  for (int st = 0; st < NSTEP; ++st) {
+    if (st >= 2) {
+      const int e = st - 2;
+      const float* slot = ring + (e % 3) * SLOT;
+      const int nr = nrows(e);
+      for (int r = 0; r < nr; ++r) {
+        const int y = yrow(e, r);
+        if (y >= 0 && y < H0) consume(slot + r * ROWF, y);
+      }
+    }
+    lds_barrier();
+  }
+  {  // output rows still open after the last row of g^(1)
+    const int ph = (H0 - 1) % PER1;
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    if (G < K1 && ky >= S1) emit((H0 - 1) * S1 - P1 + ky);
+  }
+  l1 += __shfl_xor(l1, 16, 64);
+  l1 += __shfl_xor(l1, 32, 64);
+  if (lane < 16) red[(NS + xw) * 16 + lane] = l1;
+  lds_barrier();
+  if (xw != 0 || lane >= 16) return;
+  const unsigned q = q0 + lane;
+  if (q >= Q) return;
+  float tb = 0.f, ta = 0.f;
+  for (int w = 0; w < NS; ++w) tb += red[w * 16 + lane];
+  for (int w = 0; w < C0; ++w) ta += red[(NS + w) * 16 + lane];
+  Acc a{tb, 0.f, ta};
+  sink_finish<MODE_BOUND>(s, a, q, q / R, q % R, false);
+}
+
 // The 16 rows +-e_j of a receptive-field pass-2 block share the window (y2, x2) of one
 // sub-domain.  Output channels C2 a multiple of 16: one sign and 16 consecutive channels (block
 // group g = sign * C2/16 + channel block); C2 = 8: both signs of all 8 channels (row r: sign
@@ -2168,12 +2486,67 @@ float* tape_of(const Chunk& c, int pass, int m) {
   return c.tape ? at<float>(c.ws, c.p->off_tape[pass][m]) : nullptr;
 }
 
+// Fused last two stages (T_2^T + relaxation of layer 1, T_1^T + concretisation) when both
+// layers are convolutions of a covered geometry; null otherwise.  *nwaves, *lds as launched.
+using ConvT2Kernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink);
+ConvT2Kernel convT2_bound_for(const lirpa_net* net, int* nwaves, size_t* lds) {
+  if (net->L < 3) return nullptr;
+  const lirpa_layer &a = net->T[0], &t = net->T[1];
+  if (a.kind != LIRPA_CONV2D || t.kind != LIRPA_CONV2D) return nullptr;
+  const bool t1_ok = a.k == 4 && a.stride == 2 && a.pad == 1 && a.in_c == 3 && a.in_h == 32 &&
+                     a.in_w == 32 && a.out_h == 16 && a.out_w == 16 && a.out_c == 8;
+  if (!t1_ok) return nullptr;
+  auto set = [&](int co, int ci, int w1, int k, int s_, int ns) {
+    const int rsl = s_ > k - s_ ? s_ : k - s_;
+    const int cs = w1 * 16 + (80 - (w1 * 16) % 64) % 64;
+    const int cs1 = 16 * 16 + 16;
+    *nwaves = ci + ns + 3;
+    *lds = (size_t)(2 * co * cs + 3 * rsl * ci * cs1 + 2 * 2 * 4 * rsl * ci * 16 + (ns + 3) * 16) *
+           sizeof(float);
+  };
+  // T_2: Conv(8 -> 8, k3, s1, p1), 16x16 -> 16x16 (the Deep shape).  A stride-2 T_2 (Base)
+  // stays on the separate stage kernels: there each x wave carries twice the matrix work of a
+  // T_2 wave per step, and at one block per CU that measured slower than the unfused pair.
+  if (t.k == 3 && t.stride == 1 && t.pad == 1 && t.in_c == 8 && t.out_c == 8 && t.in_h == 16 &&
+      t.out_h == 16 && t.out_w == 16) {
+    set(8, 8, 16, 3, 1, 4);
+    return k_convT2_bound<3, 1, 1, 16, 16, 16, 16, 8, 8, 4, 4, 2, 1, 32, 32, 3>;
+  }
+  return nullptr;
+}
+
 int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, float* lo,
                float* hi, long bstride, long n_half) {
   float* slab[2] = {at<float>(c.ws, c.p->off_slab0), at<float>(c.ws, c.p->off_slab1)};
   int cur = 0;
   for (int m = mtop; m >= 1; --m) {
     int e;
+    if (m == 2 && !c.tape && R >= 16) {
+      int nw = 0;
+      size_t lds = 0;
+      if (ConvT2Kernel kern = convT2_bound_for(c.net, &nw, &lds)) {
+        Sink s = slab_sink(c, 1, nullptr, ldq, R);
+        Sink sb = bound_sink(c, R, lo, hi, bstride, n_half);
+        s.eps = sb.eps;
+        s.x0 = sb.x0;
+        s.lo = sb.lo;
+        s.hi = sb.hi;
+        s.bstride = sb.bstride;
+        s.n_half = sb.n_half;
+        s.ldq = ldq;
+        const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+        if (lds > 65536 &&
+            hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds) != hipSuccess)
+          return fail(LIRPA_EDEVICE, "cannot reserve %zu bytes of LDS", lds);
+        return launch_k(tag("convT2_bound", 2, pass), c.st, [&] {
+          hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, c.st,
+                             dlayer(c.net->T[1]), dlayer(c.net->T[0]), slab[cur], (unsigned)ldq,
+                             (unsigned)Q, s);
+        });
+      }
+    }
     if (m > 1) {
       Sink s = slab_sink(c, m - 1, slab[1 - cur], ldq, R);
       s.tape = tape_of(c, pass, m - 1);
