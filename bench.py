@@ -71,6 +71,12 @@ def stage_work(layers, S, B):
             sfx = "_relax" if m > 1 else "_bound"
             out_bytes = 4.0 * n[m - 1] * Q if m > 1 else 4.0 * Q
             add(f"{kind}{sfx}[layer{m},pass{k}]", 2.0 * Q * macs(t), 4.0 * n[m] * Q + out_bytes)
+        if mtop >= 2 and all(layers[i]["kind"] == wl.CONV for i in (0, 1)):
+            # the last two stages fused in one kernel (launched instead of the pair for the
+            # shapes the library covers): both stages' flops; the slab over h^(2) read and one
+            # float per row written
+            add(f"convT2_bound[layer2,pass{k}]", 2.0 * Q * (macs(layers[1]) + macs(layers[0])),
+                4.0 * n[2] * Q + 4.0 * Q)
     return work
 
 
