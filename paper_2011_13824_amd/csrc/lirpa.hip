@@ -1548,6 +1548,247 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   }
 }
 
+// Pass 3 restricted to each row's receptive field, when T_3, T_2 (stride 1) and T_1 are
+// convolutions.  Row +-e_j of h^(3), j = (c3, y3, x3), carried through T_3 is +-W_3[c3] on the
+// K3 x K3 window of j on g^(2); after the layer-2 relaxation, T_2^T spreads it over a
+// (K3 + K2 - 1)^2 window of g^(1), and after the layer-1 relaxation T_1^T over that window's
+// footprint on x.  One block of 8 waves takes the 16 rows sharing a window (rows as in
+// k_pass2_window, over the channels of h^(3)):
+//  (1) stages the relaxation parameters of both windows (zeros outside the maps),
+//  (2) relaxes the g^(2) window (Eq. 6) with its intercept and bias terms,
+//  (3) applies T_2^T as a gather on 16x16x4 MFMA (M = channels of g^(1), K = (c2, ky, kx)), one
+//      g^(1) window position per wave at a time, and relaxes the result into an LDS tile,
+//  (4) applies T_1^T to that tile with the rotating lane-group scheme (one wave per input
+//      channel of T_1) and concretises (Eq. 8),
+//  (5) writes l_j or u_j.  Arithmetically the dense pass minus products with zero.
+template <int K3, int P3, int K2, int P2, int K1, int S1, int P1, int C1, int C2>
+__global__ void __launch_bounds__(512)
+    k_pass3_window(DLayer t1, DLayer t2, DLayer t3, const float* __restrict__ a_lo,
+                   const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+                   long poff1, long poff2, const float* __restrict__ bias, float eps,
+                   float* __restrict__ L, float* __restrict__ U, long n_relu, long off3) {
+  constexpr int NW = 8, NT = 64 * NW;
+  constexpr int N2 = K3 * K3;               // g^(2) window positions
+  constexpr int W1W = K3 - 1 + K2;          // g^(1) window width (T_2 has stride 1)
+  constexpr int N1 = W1W * W1W;
+  constexpr int E2 = C2 * N2, E1 = C1 * N1;
+  constexpr int WO = (W1W - 1) * S1 + K1;   // footprint width on x
+  constexpr int KD2 = C2 * K2 * K2;         // K of the T_2^T gather
+  constexpr int NKS2 = (KD2 + 3) / 4;
+  constexpr int KS1 = C1 / 4;
+  constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int CS2 = N2 * 16 + (80 - (N2 * 16) % 64) % 64;
+  constexpr int CS1 = N1 * 16 + (80 - (N1 * 16) % 64) % 64;
+  constexpr int RP = NT / 16;               // threads per row in (2)
+  static_assert(C1 % 4 == 0 && C1 <= 16 && K1 <= 4 && K2 <= 4 && K3 <= 4, "geometry");
+  __shared__ float tile2[C2 * CS2];
+  __shared__ float tile1[C1 * CS1];
+  __shared__ float p2s[4][E2];  // a_lo, a_up, b_up, bias of the g^(2) window
+  __shared__ float p1s[4][E1];  // a_lo, a_up, b_up, W1 x0 + b1 of the g^(1) window
+  __shared__ float rb2[RP * 16];  // bias terms of (2), per (part, row)
+  __shared__ float rb1[NW * 2 * 16];  // bias terms of (3), per (wave, lane group, row)
+  __shared__ float rl1[NW * 16];  // ||A_x||_1 partials of (4)
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = lane & 15, G = lane >> 4;
+  const int H3 = t3.out_h, W3 = t3.out_w, C3 = t3.out_c;
+  const int NG = p2_groups(C3);
+  long blk = blockIdx.x;
+  const int x3 = (int)(blk % W3); blk /= W3;
+  const int y3 = (int)(blk % H3); blk /= H3;
+  const int g = (int)(blk % NG); blk /= NG;
+  const long b = blk;
+  const int Y2 = y3 - P3, X2 = x3 - P3;  // g^(2) window origin (T_3 has stride 1)
+  const int Y1 = Y2 - P2, X1 = X2 - P2;  // g^(1) window origin
+  const int H2 = t2.out_h, Wd2 = t2.out_w, H1 = t1.out_h, Wd1 = t1.out_w;
+  const long pb = b * pstride;
+
+  // (1) parameters of both windows
+  for (int e = threadIdx.x; e < E2 + E1; e += NT) {
+    float lo = 0.f, up = 0.f, bu = 0.f, z = 0.f;
+    if (e < E2) {
+      const int c2 = e / N2, p = e - c2 * N2;
+      const int y = Y2 + p / K3, x = X2 + p % K3;
+      if (y >= 0 && y < H2 && x >= 0 && x < Wd2) {
+        const long ni = ((long)c2 * H2 + y) * Wd2 + x;
+        lo = a_lo[pb + poff2 + ni];
+        up = a_up[pb + poff2 + ni];
+        bu = b_up[pb + poff2 + ni];
+        z = bias[poff2 + ni];
+      }
+      p2s[0][e] = lo;
+      p2s[1][e] = up;
+      p2s[2][e] = bu;
+      p2s[3][e] = z;
+    } else {
+      const int f = e - E2;
+      const int c1 = f / N1, p = f - c1 * N1;
+      const int y = Y1 + p / W1W, x = X1 + p % W1W;
+      if (y >= 0 && y < H1 && x >= 0 && x < Wd1) {
+        const long ni = ((long)c1 * H1 + y) * Wd1 + x;
+        lo = a_lo[pb + poff1 + ni];
+        up = a_up[pb + poff1 + ni];
+        bu = b_up[pb + poff1 + ni];
+        z = bias[poff1 + ni];
+      }
+      p1s[0][f] = lo;
+      p1s[1][f] = up;
+      p1s[2][f] = bu;
+      p1s[3][f] = z;
+    }
+  }
+  __syncthreads();
+
+  // (2) relaxed g^(2) window of the 16 rows
+  {
+    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const P2Row pr = p2_row(C3, g, row);
+    const float sgn = pr.neg ? -1.f : 1.f;
+    const float* w3 = t3.W + (long)pr.c2 * E2;  // [C2][K3][K3] of output channel c3
+    float bpart = 0.f;
+    for (int e = part; e < E2; e += RP) {
+      const int c2 = e / N2, p = e - c2 * N2;
+      const float w = sgn * w3[e];
+      const float v = w >= 0.f ? w * p2s[0][e] : w * p2s[1][e];
+      bpart = fmaf(fminf(w, 0.f), p2s[2][e], bpart);
+      bpart = fmaf(v, p2s[3][e], bpart);
+      tile2[c2 * CS2 + p * 16 + row] = v;
+    }
+    rb2[part * 16 + row] = bpart;
+  }
+  __syncthreads();
+
+  // (3) T_2^T: A over the g^(1) window, one position per wave at a time, relaxed into tile1
+  {
+    const int m = lane & 15;  // A operand row: channel c1 of g^(1)
+    float a2[NKS2];
+#pragma unroll
+    for (int ks = 0; ks < NKS2; ++ks) {
+      const int k = 4 * ks + G;
+      a2[ks] = 0.f;
+      if (m < C1 && k < KD2) {
+        const int c2 = k / (K2 * K2), rem = k - c2 * K2 * K2;
+        const int ky = rem / K2, kx = rem - ky * K2;
+        a2[ks] = t2.W[(((long)c2 * C1 + m) * K2 + ky) * K2 + kx];
+      }
+    }
+    float bpart = 0.f;
+    for (int p = wave; p < N1; p += NW) {
+      const int y = p / W1W, x = p - y * W1W;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKS2; ++ks) {
+        const int k = 4 * ks + G;
+        float bv = 0.f;
+        if (k < KD2) {
+          const int c2 = k / (K2 * K2), rem = k - c2 * K2 * K2;
+          const int ky = rem / K2, kx = rem - ky * K2;
+          const int iy = y - ky, ix = x - kx;  // g^(2) window position feeding (y, x)
+          if (iy >= 0 && iy < K3 && ix >= 0 && ix < K3) bv = tile2[c2 * CS2 + (iy * K3 + ix) * 16 + n];
+        }
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a2[ks], bv, d, 0, 0, 0);
+      }
+      if (G * 4 < C1) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int c1 = 4 * G + r;
+          const int e = c1 * N1 + p;
+          const float a = d[r];
+          const float ah = a >= 0.f ? a * p1s[0][e] : a * p1s[1][e];
+          bpart = fmaf(fminf(a, 0.f), p1s[2][e], bpart);
+          // layer-1 bias and the linear term of the concretisation together
+          bpart = fmaf(ah, p1s[3][e], bpart);
+          tile1[c1 * CS1 + p * 16 + n] = ah;
+        }
+      }
+    }
+    if (G < 2) rb1[(wave * 2 + G) * 16 + n] = bpart;
+  }
+  __syncthreads();
+
+  // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
+  {
+    const int c0 = wave;
+    const bool cok = c0 < t1.in_c;
+    float l1 = 0.f;
+    if (cok) {
+      float wreg[PER1][KS1];
+      {
+        const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+        for (int ph = 0; ph < PER1; ++ph) {
+          const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+          for (int ks = 0; ks < KS1; ++ks) {
+            const int c1 = 4 * ks + G;
+            wreg[ph][ks] = (slot < K1 && kx < K1)
+                               ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
+          }
+        }
+      }
+      const int Hi = t1.in_h, Wi = t1.in_w;
+      const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
+      float acc[WO];
+#pragma unroll
+      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+      auto emit = [&](int yl) {
+        const int yy = OY + yl;
+        if (yy < 0 || yy >= Hi) return;
+#pragma unroll
+        for (int x = 0; x < WO; ++x) {
+          const int xc = OX + x;
+          l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
+        }
+      };
+#pragma unroll
+      for (int j = 0; j < W1W; ++j) {
+        const int ph = j % PER1;
+#pragma unroll
+        for (int i = 0; i < W1W; ++i) {
+          const int pos = j * W1W + i;
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS1; ++ks)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                wreg[ph][ks], tile1[(4 * ks + G) * CS1 + pos * 16 + n], d, 0, 0, 0);
+#pragma unroll
+          for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+        }
+        const int ky = ((G - ph * S1) % K1 + K1) % K1;
+        if (G < K1 && ky < S1) {
+          emit(j * S1 + ky);
+#pragma unroll
+          for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+        }
+      }
+      {
+        const int ky = ((G - ((W1W - 1) % PER1) * S1) % K1 + K1) % K1;
+        if (G < K1 && ky >= S1) emit((W1W - 1) * S1 + ky);
+      }
+    }
+    l1 += __shfl_xor(l1, 16, 64);
+    l1 += __shfl_xor(l1, 32, 64);
+    if (lane < 16) rl1[wave * 16 + lane] = l1;
+  }
+  __syncthreads();
+
+  // (5) the bound of each row
+  if (threadIdx.x >= 16) return;
+  const int row = threadIdx.x;
+  const P2Row pr = p2_row(C3, g, row);
+  float tb = (pr.neg ? -1.f : 1.f) * t3.b[pr.c2];
+  for (int q = 0; q < RP; ++q) tb += rb2[q * 16 + row];
+  for (int q = 0; q < NW * 2; ++q) tb += rb1[q * 16 + row];
+  float ta = 0.f;
+  for (int w = 0; w < NW; ++w) ta += rl1[w * 16 + row];
+  const float v = tb - eps * ta;
+  const long j = ((long)pr.c2 * H3 + y3) * W3 + x3;
+  if (pr.neg)
+    U[b * n_relu + off3 + j] = -v;
+  else
+    L[b * n_relu + off3 + j] = v;
+}
+
 // Reverse sweep of the receptive-field pass 2.  Layer-1 bounds do not depend on alpha, so the
 // rows of pass 2 only feed d J / d alpha of the layer-1 neurons of their own window:
 // sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
@@ -2581,6 +2822,37 @@ int pass2_window(const Chunk& c) {
   });
 }
 
+// Kernel for the receptive-field pass 3 (T_3, T_2 stride-1 convolutions over T_1), or null.
+using Pass3Kernel = void (*)(DLayer, DLayer, DLayer, const float*, const float*, const float*,
+                             long, long, long, const float*, float, float*, float*, long, long);
+Pass3Kernel pass3_kernel_for(const lirpa_net* net) {
+  if (net->L < 4) return nullptr;
+  const lirpa_layer &t1 = net->T[0], &t2 = net->T[1], &t3 = net->T[2];
+  if (t1.kind != LIRPA_CONV2D || t2.kind != LIRPA_CONV2D || t3.kind != LIRPA_CONV2D)
+    return nullptr;
+  if (t3.out_c % 16 && t3.out_c != 8) return nullptr;
+  const bool s1 = t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.out_c == 8;
+  const bool s2 = t2.k == 3 && t2.stride == 1 && t2.pad == 1 && t2.out_c == 8;
+  const bool s3 = t3.k == 3 && t3.stride == 1 && t3.pad == 1;
+  if (s1 && s2 && s3 && t1.in_c <= 8) return k_pass3_window<3, 1, 3, 1, 4, 2, 1, 8, 8>;
+  return nullptr;
+}
+
+int pass3_window(const Chunk& c) {
+  const lirpa_net* net = c.net;
+  Pass3Kernel kern = pass3_kernel_for(net);
+  if (!kern) return 1;
+  const lirpa_layer& t3 = net->T[2];
+  long blocks = c.nb * p2_groups(t3.out_c) * t3.out_h * t3.out_w;
+  return launch_k(tag("pass3_window", 1, 3), c.st, [&] {
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(512), 0, c.st, dlayer(net->T[0]),
+                       dlayer(net->T[1]), dlayer(net->T[2]), at<float>(c.ws, c.p->off_alo),
+                       at<float>(c.ws, c.p->off_aup), at<float>(c.ws, c.p->off_bup),
+                       net->pstride, net->poff[1], net->poff[2], at<float>(c.ws, c.p->off_bz),
+                       c.eps, c.L, c.U, net->n_relu, net->off[3]);
+  });
+}
+
 int bound_chunk(const Chunk& c, const float* C, float* lb) {
   const lirpa_net* net = c.net;
   const int L = net->L;
@@ -2598,6 +2870,14 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
     if (k == 2 && (!c.tape || pass2_grad_kernel_for(net))) {
       int e = pass2_window(c);
+      if (e != 1) {
+        if (e) return e;
+        if (int e2 = relax_layer(c, k)) return e2;
+        continue;
+      }
+    }
+    if (k == 3 && !c.tape) {
+      int e = pass3_window(c);
       if (e != 1) {
         if (e) return e;
         if (int e2 = relax_layer(c, k)) return e2;
