@@ -59,6 +59,18 @@ def stage_work(layers, S, B):
         Q2 = B * 2 * n[2]
         wmacs = t1["out_c"] * t2["k"] ** 2 * t1["in_c"] * t1["k"] ** 2
         add("pass2_window[layer1,pass2]", 2.0 * Q2 * wmacs, 4.0 * (3 * B * n[1] + Q2))
+    if L >= 4 and all(layers[i]["kind"] == wl.CONV for i in (0, 1, 2)) \
+            and layers[1]["stride"] == 1 and layers[2]["stride"] == 1:
+        # pass 3 restricted to receptive fields: each of the C2 x K3 x K3 entries of a row's
+        # window on g^(2) reaches C1 x K2 x K2 entries of g^(1), and each of the C1 x W1 x W1
+        # entries of the g^(1) window (W1 = K3 + K2 - 1) reaches in_c x K1 x K1 inputs
+        t1, t2, t3 = layers[0], layers[1], layers[2]
+        Q3 = B * 2 * n[3]
+        w1 = t3["k"] + t2["k"] - 1
+        wmacs = (t2["out_c"] * t3["k"] ** 2 * t1["out_c"] * t2["k"] ** 2
+                 + t1["out_c"] * w1 * w1 * t1["in_c"] * t1["k"] ** 2)
+        add("pass3_window[layer1,pass3]", 2.0 * Q3 * wmacs,
+            4.0 * (3 * B * (n[1] + n[2]) + Q3))
     for k in range(2, L + 1):
         R = 2 * n[k] if k < L else S
         Q = B * R
