@@ -226,13 +226,11 @@ __device__ __forceinline__ void sink_finish(const Sink& s, const Acc& acc, long 
 
 // Rows +-e_j over h^(k) (j = r mod n_k, sign + for r < n_k): carried through T_k (Eq. 4) they
 // become +-(row j of W_k) over g^(k-1), with bias +-b_k[j].
-template <int MODE>
 // WT (optional, LINEAR only): the weights transposed, [in_c][out_c], so that the lanes of a
 // wave (consecutive j) read consecutive addresses.
-__global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __restrict__ WT,
-                                                      long Q, Sink s) {
-  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (q >= Q) return;
+template <int MODE>
+__device__ __forceinline__ void init_row(const DLayer& t, const float* __restrict__ WT,
+                                         const Sink& s, long q) {
   long b = q / s.R, r = q % s.R;
   long nk = (long)t.out_c * t.out_h * t.out_w;
   long j = r % nk;
@@ -275,6 +273,14 @@ __global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __r
         }
   }
   sink_finish<MODE>(s, acc, q, b, r, true);
+}
+
+template <int MODE>
+__global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __restrict__ WT,
+                                                      long Q, Sink s) {
+  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (q >= Q) return;
+  init_row<MODE>(t, WT, s, q);
 }
 
 // Pass initialisation for the rows +-e_j of a fully connected layer k, relaxed onto ReLU layer
@@ -329,18 +335,9 @@ __global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __r
 }
 
 // z1 = W1 x0 + b1: the layer-1 pre-activation at the box centre.
-// Per-channel bias broadcast to a per-neuron vector.
-__global__ void __launch_bounds__(kBlock) k_bias_fill(long n, int hw, const float* __restrict__ b,
-                                                      float* __restrict__ out) {
-  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (i < n) out[i] = b[i / hw];
-}
-
-__global__ void __launch_bounds__(kBlock) k_layer1_at_x0(DLayer t, const float* __restrict__ x0,
-                                                         float* __restrict__ z) {
-  long j = blockIdx.x * (long)blockDim.x + threadIdx.x;
+__device__ __forceinline__ void layer1_at_x0(const DLayer& t, const float* __restrict__ x0,
+                                             float* __restrict__ z, long j) {
   const int hw = t.out_h * t.out_w;
-  if (j >= (long)t.out_c * hw) return;
   float a = t.b[j / hw];
   if (t.kind == LIRPA_LINEAR) {
     for (int i = 0; i < t.in_c; ++i) a = fmaf(t.W[j * t.in_c + i], x0[i], a);
@@ -361,13 +358,57 @@ __global__ void __launch_bounds__(kBlock) k_layer1_at_x0(DLayer t, const float* 
   z[j] = a;
 }
 
-// out[i][o] = W[o][i] for a fully connected layer.
-__global__ void __launch_bounds__(kBlock) k_transpose(const float* __restrict__ W, int nout,
-                                                      int nin, float* __restrict__ out) {
+// Everything a call derives from the network, x0 and eps alone, in one launch: the exact
+// layer-1 bounds (rows +-e_j of h^(1) through T_1, concretised), z1 = W1 x0 + b1, the
+// per-neuron bias vectors of ReLU layers 2..L-1 and the transposed weights of the fully
+// connected layers that start an intermediate pass.  Thread e is dealt to the segments in
+// that order.
+struct SetupJob {
+  DLayer t1;
+  Sink s1;      // layer-1 bound rows (MODE_BOUND sink)
+  long n_rows;  // 2 n1
+  const float* x0;
+  float* z1;
+  long n1;
+  int nfill;
+  long fill_n[kMaxLayers];
+  int fill_hw[kMaxLayers];
+  const float* fill_b[kMaxLayers];
+  float* fill_out[kMaxLayers];
+  int ntr;
+  const float* tr_W[kMaxLayers];
+  int tr_out[kMaxLayers], tr_in[kMaxLayers];
+  float* tr_dst[kMaxLayers];
+};
+
+__global__ void __launch_bounds__(kBlock) k_setup(SetupJob job) {
   long e = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (e >= (long)nout * nin) return;
-  long o = e / nin, i = e % nin;
-  out[i * nout + o] = W[e];
+  if (e < job.n_rows) {
+    init_row<MODE_BOUND>(job.t1, nullptr, job.s1, e);
+    return;
+  }
+  e -= job.n_rows;
+  if (e < job.n1) {
+    layer1_at_x0(job.t1, job.x0, job.z1, e);
+    return;
+  }
+  e -= job.n1;
+  for (int f = 0; f < job.nfill; ++f) {
+    if (e < job.fill_n[f]) {
+      job.fill_out[f][e] = job.fill_b[f][e / job.fill_hw[f]];
+      return;
+    }
+    e -= job.fill_n[f];
+  }
+  for (int k = 0; k < job.ntr; ++k) {
+    const long nel = (long)job.tr_out[k] * job.tr_in[k];
+    if (e < nel) {
+      const long o = e / job.tr_in[k], i = e % job.tr_in[k];
+      job.tr_dst[k][i * job.tr_out[k] + o] = job.tr_W[k][e];
+      return;
+    }
+    e -= nel;
+  }
 }
 
 // Spec rows C_s over h^(L) (the property merged into the last layer): written to the slab as
@@ -2088,9 +2129,11 @@ __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restr
 
 // Relaxation parameters of ReLU layer m for every sub-domain of the chunk (Eq. 5 with the split
 // override of Sec. 3.1, checked in the order: split, u <= 0, l >= 0, unstable).
+// lsh, ush (optional): bounds shared by every sub-domain (layer 1), copied into its rows of l, u.
 __global__ void __launch_bounds__(kBlock)
     k_relax_params(long nb, long nm, long stride, long off, long pstride, long poff,
-                   const float* __restrict__ l, const float* __restrict__ u,
+                   float* __restrict__ l, float* __restrict__ u,
+                   const float* __restrict__ lsh, const float* __restrict__ ush,
                    const int8_t* __restrict__ split, const float* __restrict__ alpha,
                    float* __restrict__ a_lo, float* __restrict__ a_up, float* __restrict__ b_up,
                    int8_t* __restrict__ code) {
@@ -2099,6 +2142,10 @@ __global__ void __launch_bounds__(kBlock)
   long b = idx / nm, j = idx % nm;
   long p = b * stride + off + j;
   long pp = b * pstride + poff + j;
+  if (lsh) {
+    l[p] = lsh[j];
+    u[p] = ush[j];
+  }
   int sp = split ? split[p] : 0;
   float lo = 0.f, up = 0.f, bu = 0.f;
   int c;
@@ -2107,7 +2154,7 @@ __global__ void __launch_bounds__(kBlock)
   } else if (sp < 0) {
     c = 2;
   } else {
-    float lj = l[p], uj = u[p];
+    float lj = lsh ? lsh[j] : l[p], uj = ush ? ush[j] : u[p];
     if (uj <= 0.f) {
       c = 3;
     } else if (lj >= 0.f) {
@@ -2124,18 +2171,6 @@ __global__ void __launch_bounds__(kBlock)
   a_up[pp] = up;
   b_up[pp] = bu;
   code[p] = (int8_t)c;
-}
-
-// Copies the shared layer-1 bounds into every sub-domain's row of l, u.
-__global__ void __launch_bounds__(kBlock) k_bcast_l1(long nb, long n1, long stride,
-                                                     const float* __restrict__ l1,
-                                                     const float* __restrict__ u1,
-                                                     float* __restrict__ l, float* __restrict__ u) {
-  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (idx >= nb * n1) return;
-  long b = idx / n1, j = idx % n1;
-  l[b * stride + j] = l1[j];
-  u[b * stride + j] = u1[j];
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -2709,13 +2744,14 @@ Sink bound_sink(const Chunk& c, long R, float* lo, float* hi, long bstride, long
   return s;
 }
 
-int relax_layer(const Chunk& c, int m) {
+int relax_layer(const Chunk& c, int m, const float* lsh = nullptr, const float* ush = nullptr) {
   const lirpa_net* net = c.net;
   long nm = net->n[m];
   long off = net->off[m];
   return launch_k(tag("relax_params", m, m), c.st, [&] {
     hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
-                       net->n_relu, off, net->pstride, net->poff[m], c.L, c.U, c.split, c.alpha,
+                       net->n_relu, off, net->pstride, net->poff[m], c.L, c.U, lsh, ush,
+                       c.split, c.alpha,
                        at<float>(c.ws, c.p->off_alo), at<float>(c.ws, c.p->off_aup),
                        at<float>(c.ws, c.p->off_bup), at<int8_t>(c.ws, c.p->off_code));
   });
@@ -2858,13 +2894,9 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   const int L = net->L;
   long n1 = net->n[1];
   if (L >= 2) {
+    // layer 1: the shared exact bounds, copied into every sub-domain's rows on the way
     const float* l1u1 = at<float>(c.ws, c.p->off_l1u1);
-    if (int e = launch_k(tag("bcast_l1", 1, 1), c.st, [&] {
-          hipLaunchKernelGGL(k_bcast_l1, grid_for(c.nb * n1), dim3(kBlock), 0, c.st, c.nb, n1,
-                             net->n_relu, l1u1, l1u1 + n1, c.L, c.U);
-        }))
-      return e;
-    if (int e = relax_layer(c, 1)) return e;
+    if (int e = relax_layer(c, 1, l1u1, l1u1 + n1)) return e;
   }
   for (int k = 2; k <= L - 1; ++k) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
@@ -2917,48 +2949,44 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
 // concretised (no relaxation in front of layer 1).
 int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0, float eps,
                   hipStream_t st) {
-  long n1 = net->n[1], R = 2 * n1, Q = R;
+  long n1 = net->n[1], R = 2 * n1;
   float* l1u1 = at<float>(ws, p.off_l1u1);
-  Sink s{};
-  s.x0 = x0;
-  s.eps = eps;
-  s.R = R;
-  s.lo = l1u1;
-  s.hi = l1u1 + n1;
-  s.bstride = 0;
-  s.n_half = n1;
-  if (int e = launch_k(tag("init_rows_bound", 1, 1), st, [&] {
-        hipLaunchKernelGGL(k_init_rows<MODE_BOUND>, grid_for(Q), dim3(kBlock), 0, st,
-                           dlayer(net->T[0]), (const float*)nullptr, Q, s);
-      }))
-    return e;
-  if (int e = launch_k("layer1_at_x0", st, [&] {
-        hipLaunchKernelGGL(k_layer1_at_x0, grid_for(n1), dim3(kBlock), 0, st, dlayer(net->T[0]),
-                           x0, at<float>(ws, p.off_z1));
-      }))
-    return e;
-  // per-neuron bias vectors of ReLU layers 2..L-1 (layer 1's is z1, written above)
-  for (int m = 2; m <= net->L - 1; ++m) {
+  SetupJob job{};
+  job.t1 = dlayer(net->T[0]);
+  job.s1.x0 = x0;
+  job.s1.eps = eps;
+  job.s1.R = R;
+  job.s1.lo = l1u1;
+  job.s1.hi = l1u1 + n1;
+  job.s1.bstride = 0;
+  job.s1.n_half = n1;
+  job.n_rows = R;
+  job.x0 = x0;
+  job.z1 = at<float>(ws, p.off_z1);
+  job.n1 = n1;
+  long total = R + n1;
+  for (int m = 2; m <= net->L - 1; ++m) {  // bias vectors (layer 1's is z1)
     const lirpa_layer& t = net->T[m - 1];
-    long nm = net->n[m];
-    if (int e = launch_k("bias_fill", st, [&] {
-          hipLaunchKernelGGL(k_bias_fill, grid_for(nm), dim3(kBlock), 0, st, nm,
-                             t.out_h * t.out_w, t.b, at<float>(ws, p.off_bz) + net->poff[m]);
-        }))
-      return e;
+    job.fill_n[job.nfill] = net->n[m];
+    job.fill_hw[job.nfill] = t.out_h * t.out_w;
+    job.fill_b[job.nfill] = t.b;
+    job.fill_out[job.nfill] = at<float>(ws, p.off_bz) + net->poff[m];
+    total += net->n[m];
+    ++job.nfill;
   }
-  // transposed weights of the fully connected layers that start an intermediate pass
-  for (int k = 2; k <= net->L - 1; ++k) {
+  for (int k = 2; k <= net->L - 1; ++k) {  // transposed FC weights
     if (!p.off_wT[k]) continue;
     const lirpa_layer& t = net->T[k - 1];
-    long nel = (long)t.out_c * t.in_c;
-    if (int e = launch_k("transpose", st, [&] {
-          hipLaunchKernelGGL(k_transpose, grid_for(nel), dim3(kBlock), 0, st, t.W, t.out_c,
-                             t.in_c, at<float>(ws, p.off_wT[k]));
-        }))
-      return e;
+    job.tr_W[job.ntr] = t.W;
+    job.tr_out[job.ntr] = t.out_c;
+    job.tr_in[job.ntr] = t.in_c;
+    job.tr_dst[job.ntr] = at<float>(ws, p.off_wT[k]);
+    total += (long)t.out_c * t.in_c;
+    ++job.ntr;
   }
-  return LIRPA_OK;
+  return launch_k(tag("setup", 1, 1), st, [&] {
+    hipLaunchKernelGGL(k_setup, grid_for(total), dim3(kBlock), 0, st, job);
+  });
 }
 
 // Gradient of J_b = sum_s lb[b][s] with respect to alpha for every sub-domain of the chunk,
