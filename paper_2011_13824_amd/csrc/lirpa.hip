@@ -814,7 +814,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 // spanning at most two sub-domains (R >= 16).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS,
           bool TAPE>
-__global__ void __launch_bounds__(64 * (CI / CPW + NS))
+__global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 : (CI / CPW + NS <= 12 ? 6 : 1))
     k_convT_relax_ws(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % CPW == 0, "geometry");
   static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
@@ -822,20 +822,25 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
   constexpr int NTM = 64 * NM;
   constexpr int KS = CO / 4;
   constexpr int PER = (K % S == 0) ? K / S : K;  // rotation period of the tap rows
-  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
+  constexpr int CS = W1 * 16;                    // tile: [CO][W1][16 q], no padding
   constexpr int TILE = CO * CS;
   constexpr int NV4 = CO * W1 * 4;               // float4 per input tile
   constexpr int PF = (NV4 + NTM - 1) / NTM;
   constexpr int RSL = S > K - S ? S : K - S;     // output rows completed per step (max)
   constexpr int RB = RSL * CI * 16 * 16;         // row buffer: [RSL][CI][16 q][16 x]
-  constexpr int PB = 2 * 4 * RSL * CI * W0;      // parameters: [2 sub-domains][4][RSL][CI][W0]
+  constexpr int AST = RSL * CI * W0;             // one parameter array of a stage
+  constexpr int PB = 7 * AST;                    // [a_lo, a_up, b_up] x 2 sub-domains + bias
   constexpr int NPV4 = PB / 4;
   constexpr int PP = (NPV4 + NTM - 1) / NTM;
-  extern __shared__ float lds[];
-  float* tiles = lds;              // 2 x TILE
-  float* rows = tiles + 2 * TILE;  // 2 x RB
-  float* pars = rows + 2 * RB;     // 2 x PB
-  float* red = pars + 2 * PB;      // NS x 16
+  static_assert(AST % 256 == 0 && NV4 % 64 == 0, "DMA chunks must be whole waves");
+  // Input tiles and relaxation parameters reach LDS by DMA (global_load_lds), issued by the
+  // matrix waves two steps ahead of their use and waited for, per wave, just before the
+  // barrier that publishes them.  They are issued from inline assembly, so the compiler neither
+  // holds registers for them nor orders other LDS accesses behind them.
+  __shared__ float tiles[3][TILE];
+  __shared__ float rows[2][RB];
+  __shared__ float pars[3][PB];
+  __shared__ float red[NS * 16];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
@@ -868,43 +873,89 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
           }
       }
     }
-    auto gaddr = [&](int y1, int v4) {
-      const int cx = v4 >> 2, j4 = v4 & 3;
-      const int co = cx / W1, x1 = cx - co * W1;
-      return in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4;
+    // 16 bytes per lane from src into LDS at base + 16 * lane (base uniform over the wave)
+    auto dma16 = [&](const float* src, const float* base) {
+      const unsigned lds = __builtin_amdgcn_readfirstlane(
+          (unsigned)(size_t)(__attribute__((address_space(3))) const float*)base);
+      asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                   :: "v"(src), "s"(lds) : "memory", "m0");
     };
-    auto loff = [&](int v4) {
-      const int cx = v4 >> 2, j4 = v4 & 3;
-      const int co = cx / W1, x1 = cx - co * W1;
-      return co * CS + x1 * 16 + j4 * 4;
+    auto dma_tile = [&](float* buf, int y1) {  // input row y1 into buf
+#pragma unroll
+      for (int k = 0; k < PF; ++k) {
+        const int v4 = tid + k * NTM;  // whole waves in or out of range
+        if (v4 < NV4) {
+          const int cx = v4 >> 2, j4 = v4 & 3;
+          const int co = cx / W1, x1 = cx - co * W1;
+          dma16(in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4,
+                buf + 4 * (v4 - lane));
+        }
+      }
     };
-    // relaxation parameters of stage e: float4 v of [bsel][arr][r][CI][W0/4]
-    auto pload = [&](int e, int v, float4v& out) {
-      const int x4 = v % (W0 / 4);
-      const int c = (v / (W0 / 4)) % CI;
-      const int r = (v / (W0 / 4 * CI)) % RSL;
-      const int arr = (v / (W0 / 4 * CI * RSL)) % 4;
-      const int bsel = v / (W0 / 4 * CI * RSL * 4);
-      const int y = yrow(e, r);
-      out = float4v{0.f, 0.f, 0.f, 0.f};
-      if (r >= nrows(e) || y < 0 || y >= H0 || b0 + bsel > b1) return;
-      const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * x4;
-      const long pb = (long)(b0 + bsel) * s.pstride + rowi;
-      const float* src = arr == 0 ? s.a_lo + pb : arr == 1 ? s.a_up + pb
-                       : arr == 2 ? s.b_up + pb : s.bias + rowi;
-      out = *reinterpret_cast<const float4v*>(src);
+    // parameters of stage e into pbuf: float4 v of [arr][RSL][CI][W0/4], arr = 3 bsel + {0,1,2}
+    // for a_lo, a_up, b_up of sub-domain b0 + bsel, arr = 6 for the bias.  Entries of rows
+    // outside the map or of a second sub-domain the block does not have are never read: they
+    // fetch the bias instead.
+    auto dma_pars = [&](float* pbuf, int e) {
+#pragma unroll
+      for (int k = 0; k < PP; ++k) {
+        const int v = tid + k * NTM;
+        if (v < NPV4) {
+          const int x4 = v % (W0 / 4);
+          const int c = (v / (W0 / 4)) % CI;
+          const int r = (v / (W0 / 4 * CI)) % RSL;
+          const int arr = __builtin_amdgcn_readfirstlane(v >> 6) / (AST / 256);
+          const int bsel = arr < 6 ? arr / 3 : 0;
+          const int y = yrow(e, r);
+          const bool ok = r < nrows(e) && y >= 0 && y < H0 && b0 + bsel <= b1;
+          const unsigned rowi = ok ? ((unsigned)c * H0 + y) * W0 + 4 * x4 : 0u;
+          const long pb = (long)(b0 + bsel) * s.pstride + rowi;
+          const float* src = s.bias + rowi;
+          if (ok && arr < 6) {
+            switch (arr % 3) {
+              case 0: src = s.a_lo + pb; break;
+              case 1: src = s.a_up + pb; break;
+              default: src = s.b_up + pb; break;
+            }
+          }
+          dma16(src, pbuf + 4 * (v - lane));
+        }
+      }
     };
+    // DMA instructions this wave issues per call of dma_pars and dma_tile (whole waves)
+    int npw = 0, ntw = 0;
+#pragma unroll
+    for (int k = 0; k < PP; ++k) npw += (wave * 64 + k * NTM < NPV4) ? 1 : 0;
+#pragma unroll
+    for (int k = 0; k < PF; ++k) ntw += (wave * 64 + k * NTM < NV4) ? 1 : 0;
+    // wait until at most n of this wave's DMAs are outstanding (n is uniform, <= PP + PF)
+    auto wait_dma = [](int n) {
+      switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0xF70); break;
+        case 1: __builtin_amdgcn_s_waitcnt(0xF71); break;
+        case 2: __builtin_amdgcn_s_waitcnt(0xF72); break;
+        case 3: __builtin_amdgcn_s_waitcnt(0xF73); break;
+        default: __builtin_amdgcn_s_waitcnt(0xF74); break;
+      }
+    };
+    static_assert(PP + PF <= 4, "wait_dma covers at most four DMAs in flight");
     auto park = [&](int slot, int r, int c, const float* v) {
-      float* dst = rows + slot * RB + (((r * CI + wave * CPW + c) * 16 + n) * 16);
+      float* dst = rows[slot] + (((r * CI + wave * CPW + c) * 16 + n) * 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         *reinterpret_cast<float4v*>(dst + 4 * i) =
             float4v{v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
     };
 
-    for (int v4 = tid; v4 < NV4; v4 += NTM)
-      *reinterpret_cast<float4v*>(tiles + loff(v4)) =
-          *reinterpret_cast<const float4v*>(gaddr(0, v4));
+    // prologue: parameters of stage 0, input rows 0 and 1; row 0 and the parameters landed
+    dma_pars(pars[0], 0);
+    dma_tile(tiles[0], 0);
+    if (H1 > 1) {
+      dma_tile(tiles[1], 1);
+      wait_dma(ntw);
+    } else {
+      wait_dma(0);
+    }
     lds_barrier();
 
     float acc[CPW][W0];
@@ -913,21 +964,20 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
 #pragma unroll
       for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
 
-    for (int ybase = 0; ybase < H1; ybase += PER) {
+    // Step y1: DMA the parameters of stage y1+1 and input row y1+2; MFMAs on row y1; park the
+    // rows it completes; wait for this wave's DMAs of earlier steps (row y1+1, parameters of
+    // stage y1); barrier.  Unrolled over U steps so that the buffer indices are constants.
+    constexpr int U = PER % 3 == 0 ? PER : 3 * PER;
+    for (int ybase = 0; ybase < H1; ybase += U) {
 #pragma unroll
-      for (int ph = 0; ph < PER; ++ph) {
-        const int y1 = ybase + ph;
-        if (H1 % PER != 0 && y1 >= H1) break;
-        const float* tile = tiles + (y1 & 1) * TILE;
-        const bool more = y1 + 1 < H1;
-        float4v pf[PF], pp[PP];
-#pragma unroll
-        for (int k = 0; k < PF; ++k) {
-          const int v4 = min(tid + k * NTM, NV4 - 1);
-          pf[k] = *reinterpret_cast<const float4v*>(gaddr(more ? y1 + 1 : y1, v4));
-        }
-#pragma unroll
-        for (int k = 0; k < PP; ++k) pload(y1, min(tid + k * NTM, NPV4 - 1), pp[k]);
+      for (int u = 0; u < U; ++u) {
+        const int y1 = ybase + u;
+        if (H1 % U != 0 && y1 >= H1) break;
+        const int ph = u % PER;
+        const float* tile = tiles[u % 3];
+        dma_pars(pars[(u + 1) % 3], y1 + 1);
+        const bool more = y1 + 2 < H1;
+        if (more) dma_tile(tiles[(u + 2) % 3], y1 + 2);
 #pragma unroll
         for (int x1 = 0; x1 < W1; ++x1) {
           float bv[KS];
@@ -946,19 +996,6 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
             }
           }
         }
-        if (more) {
-          float* nt = tiles + ((y1 + 1) & 1) * TILE;
-#pragma unroll
-          for (int k = 0; k < PF; ++k) {
-            const int v4 = tid + k * NTM;
-            if (v4 < NV4) *reinterpret_cast<float4v*>(nt + loff(v4)) = pf[k];
-          }
-        }
-#pragma unroll
-        for (int k = 0; k < PP; ++k) {
-          const int v = tid + k * NTM;
-          if (v < NPV4) *reinterpret_cast<float4v*>(pars + (y1 & 1) * PB + 4 * v) = pp[k];
-        }
         const int ky = ((G - ph * S) % K + K) % K;
         if (G < K && ky < S) {
 #pragma unroll
@@ -968,24 +1005,18 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
             for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
           }
         }
+        wait_dma(npw + (more ? ntw : 0));
         lds_barrier();
       }
     }
-    // stage H1: the rows still open
+    // stage H1: the rows still open; its parameters were fetched at the last step
+    wait_dma(0);
     {
-      float4v pp[PP];
-#pragma unroll
-      for (int k = 0; k < PP; ++k) pload(H1, min(tid + k * NTM, NPV4 - 1), pp[k]);
       constexpr int ph_last = (H1 - 1) % PER;
       const int ky = ((G - ph_last * S) % K + K) % K;
       if (G < K && ky >= S) {
 #pragma unroll
         for (int c = 0; c < CPW; ++c) park(H1 & 1, ky - S, c, acc[c]);
-      }
-#pragma unroll
-      for (int k = 0; k < PP; ++k) {
-        const int v = tid + k * NTM;
-        if (v < NPV4) *reinterpret_cast<float4v*>(pars + (H1 & 1) * PB + 4 * v) = pp[k];
       }
     }
     lds_barrier();
@@ -1002,19 +1033,19 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS))
   float beta = 0.f;
   auto stage = [&](int e) {
     const int slot = e & 1;
+    const float* pst = pars[e % 3];
     const int nr = nrows(e);
     for (int it = ws; it < nr * CI; it += NS) {
       const int r = it / CI, c = it - r * CI;
       const int y = yrow(e, r);
       if (y < 0 || y >= H0 || !qok) continue;
-      const float4v a = *reinterpret_cast<const float4v*>(rows + slot * RB +
+      const float4v a = *reinterpret_cast<const float4v*>(rows[slot] +
                                                           ((r * CI + c) * 16 + qn) * 16 + 4 * xg);
-      const float* pbase = pars + slot * PB + ((bsel * 4) * RSL + r) * CI * W0 + c * W0 + 4 * xg;
-      constexpr int AST = RSL * CI * W0;  // stride between the four parameter arrays
-      const float4v lo = *reinterpret_cast<const float4v*>(pbase);
-      const float4v up = *reinterpret_cast<const float4v*>(pbase + AST);
-      const float4v bu = *reinterpret_cast<const float4v*>(pbase + 2 * AST);
-      const float4v bz = *reinterpret_cast<const float4v*>(pbase + 3 * AST);
+      const int off = r * CI * W0 + c * W0 + 4 * xg;
+      const float4v lo = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 0) * AST + off);
+      const float4v up = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 1) * AST + off);
+      const float4v bu = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 2) * AST + off);
+      const float4v bz = *reinterpret_cast<const float4v*>(pst + 6 * AST + off);
       const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * xg;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -2618,11 +2649,8 @@ ConvTKernel<MODE> convT_mfma_for(const DLayer& t, bool tape, int* nwaves) {
 // *nwaves: matrix + storer waves; *lds: dynamic LDS bytes.
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS>
 ConvTKernel<MODE_SLAB> convT_ws_inst(bool tape, int* nwaves, size_t* lds) {
-  constexpr int CS = W1 * 16 + (80 - (W1 * 16) % 64) % 64;
-  constexpr int RSL = S > K - S ? S : K - S;
   *nwaves = CI / CPW + NS;
-  *lds = (size_t)(2 * CO * CS + 2 * RSL * CI * 256 + 2 * 2 * 4 * RSL * CI * W0 + NS * 16) *
-         sizeof(float);
+  *lds = 0;  // all LDS of the kernel is static
   return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true>
               : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false>;
 }
@@ -2633,7 +2661,7 @@ ConvTKernel<MODE_SLAB> convT_ws_for(const DLayer& t, bool tape, int* nwaves, siz
   const bool g_s1_16 = t.k == 3 && t.stride == 1 && t.pad == 1 && t.out_h == 16 &&
                        t.out_w == 16 && t.in_h == 16 && t.in_w == 16;
   if (g_s2_16 && t.in_c == 8 && t.out_c == 16)
-    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 1, 4>(tape, nwaves, lds);
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4>(tape, nwaves, lds);
   if (g_s2_16 && t.in_c == 8 && t.out_c == 8)
     return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 8, 8, 1, 4>(tape, nwaves, lds);
   if (g_s2_16 && t.in_c == 16 && t.out_c == 32)
