@@ -708,7 +708,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 #pragma unroll
         for (int c = 0; c < CPW; ++c) load_row(c, yout);
       }
-      if constexpr (EARLY) __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_barrier(0);  // keep the loads above ahead of the matrix work
 #pragma unroll
       for (int x1 = 0; x1 < W1; ++x1) {
         float bv[KS];
