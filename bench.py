@@ -77,6 +77,14 @@ def stage_work(layers, S, B):
         mtop = k - 1 if k < L else L
         if k < L:
             add(f"init_rows[layer{k},pass{k}]", 0.0, 4.0 * n[k - 1] * Q)
+        if 3 <= k < L and layers[k - 1]["kind"] == wl.FC and layers[k - 2]["kind"] == wl.CONV:
+            # the pass opened at a fully connected layer inside the stage through layer k-1
+            # (launched instead of init_rows + that stage for the shapes the library covers): its
+            # flops; bytes: the rows of W_k and the relaxation of layer k-1 (3 floats per neuron
+            # and sub-domain) read, the relaxed slab over g^(k-2) written
+            t = layers[k - 2]
+            add(f"convT_relax_fc[layer{k - 1},pass{k}]", 2.0 * Q * macs(t),
+                4.0 * (n[k] * n[k - 1] + 3 * B * n[k - 1]) + 4.0 * n[k - 2] * Q)
         for m in range(mtop, 0, -1):
             t = layers[m - 1]
             kind = "fcT" if t["kind"] == wl.FC else "convT"

@@ -179,6 +179,20 @@ struct Sink {
   float* tape;  // optional: the coefficient before relaxation (or over x), [i*ldq + q]
 };
 
+// Input of the first backward stage of a pass that starts at a fully connected layer k (rows
+// +-e_j over h^(k), nk of each sign, R = 2 nk per sub-domain): carried through T_k (Eq. 4) row j
+// becomes +-(row j of W_k) over g^(k-1), which is then relaxed with ReLU layer k-1 (Eq. 6).  A
+// stage through layer k-1 can build these coefficients as it goes instead of reading them from
+// a slab.
+struct FcSrc {
+  const float* W;     // W_k, [nk][nin] (row j contiguous, 16-byte aligned)
+  const float* b;     // b_k, [nk]
+  int nk;
+  const float* a_lo;  // relaxation of ReLU layer k-1 (per sub-domain, stride Sink::pstride)
+  const float* a_up;
+  const float* b_up;
+};
+
 struct Acc {
   float beta, lin, l1;
 };
@@ -812,18 +826,25 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 // global stores, and the matrix waves never wait on the relaxation's arithmetic.  One LDS-only
 // barrier per input row hands the buffers over (double-buffered).  A block takes 16 rows q
 // spanning at most two sub-domains (R >= 16).
+// FC: the stage opens a pass at the fully connected layer above (see FcSrc).  The matrix waves
+// then build each input tile themselves, one step ahead: the rows of W_k and the relaxation of
+// this stage's own layer are loaded into registers before the MFMAs of the current row and
+// turned into relaxed coefficients (with their intercept and bias terms) after them.  The slab
+// that would hold these coefficients is never written or read.
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS,
-          bool TAPE>
+          bool TAPE, bool FC>
 __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 : (CI / CPW + NS <= 12 ? 6 : 1))
-    k_convT_relax_ws(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
+    k_convT_relax_ws(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s,
+                     FcSrc fc) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % CPW == 0, "geometry");
   static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
   constexpr int NM = CI / CPW;                   // matrix waves
   constexpr int NTM = 64 * NM;
   constexpr int KS = CO / 4;
   constexpr int PER = (K % S == 0) ? K / S : K;  // rotation period of the tap rows
-  constexpr int CS = W1 * 16;                    // tile: [CO][W1][16 q], no padding
-  constexpr int TILE = CO * CS;
+  // tile: [W1][CO][16 q], so that the four lane groups of a B-operand read (channels 4ks + G
+  // at one x1) cover 64 consecutive floats
+  constexpr int TILE = W1 * CO * 16;
   constexpr int NV4 = CO * W1 * 4;               // float4 per input tile
   constexpr int PF = (NV4 + NTM - 1) / NTM;
   constexpr int RSL = S > K - S ? S : K - S;     // output rows completed per step (max)
@@ -833,6 +854,11 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   constexpr int NPV4 = PB / 4;
   constexpr int PP = (NPV4 + NTM - 1) / NTM;
   static_assert(AST % 256 == 0 && NV4 % 64 == 0, "DMA chunks must be whole waves");
+  static_assert(!FC || (!TAPE && W1 % 4 == 0), "FC source: bound passes, float4 quads of x1");
+  // FC source: task tk of an input row = (quad qd of four consecutive x1 of channel co, pair of
+  // rows q0 + 2 qp, q0 + 2 qp + 1), qd = t4 * CO + co, tk = 8 qd + qp
+  constexpr int NTASK = CO * W1 / 4 * 8;
+  constexpr int TPL = FC ? (NTASK + NTM - 1) / NTM : 1;
   // Input tiles and relaxation parameters reach LDS by DMA (global_load_lds), issued by the
   // matrix waves two steps ahead of their use and waited for, per wave, just before the
   // barrier that publishes them.  They are issued from inline assembly, so the compiler neither
@@ -841,6 +867,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   __shared__ float rows[2][RB];
   __shared__ float pars[3][PB];
   __shared__ float red[NS * 16];
+  __shared__ float red_fc[FC ? NM * 16 : 1];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
@@ -886,7 +913,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
         const int v4 = tid + k * NTM;  // whole waves in or out of range
         if (v4 < NV4) {
           const int cx = v4 >> 2, j4 = v4 & 3;
-          const int co = cx / W1, x1 = cx - co * W1;
+          const int x1 = cx / CO, co = cx - x1 * CO;
           dma16(in + ((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4,
                 buf + 4 * (v4 - lane));
         }
@@ -939,22 +966,91 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
       }
     };
     static_assert(PP + PF <= 4, "wait_dma covers at most four DMAs in flight");
+    // a parked row of 16 x values holds its float4 i at position i ^ (q >> 2), so that the 16
+    // rows q of one write (64 bytes apart) spread over all banks
     auto park = [&](int slot, int r, int c, const float* v) {
       float* dst = rows[slot] + (((r * CI + wave * CPW + c) * 16 + n) * 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<float4v*>(dst + 4 * i) =
+        *reinterpret_cast<float4v*>(dst + 4 * (i ^ (n >> 2))) =
             float4v{v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+    };
+
+    // FC source: per task, the fixed part of its addresses and its sign (0 for rows past Q)
+    typedef float float2v __attribute__((ext_vector_type(2)));
+    unsigned g_wa[TPL], g_wb[TPL], g_pb[TPL];  // offsets into W_k and the parameter arrays
+    float g_sa[TPL], g_sb[TPL], g_bz[TPL];
+    int g_lds[TPL];
+    bool g_on[TPL];
+    float4v g_xa[TPL], g_xb[TPL], g_lo[TPL], g_up[TPL], g_bu[TPL];
+    float fbeta_a = 0.f, fbeta_b = 0.f;
+    if constexpr (FC) {
+      const unsigned nin = CO * H1 * W1, nk = (unsigned)fc.nk;
+#pragma unroll
+      for (int k = 0; k < TPL; ++k) {
+        const int tk = tid + k * NTM;
+        g_on[k] = tk < NTASK;
+        const int qp = tk & 7, qd = g_on[k] ? tk >> 3 : 0;
+        const int co = qd % CO, t4 = qd / CO;
+        const unsigned qa = q0 + 2u * qp, qb = qa + 1u;
+        const unsigned ra = qa % R, rb = qb % R;
+        g_sa[k] = qa < Q ? (ra < nk ? 1.f : -1.f) : 0.f;
+        g_sb[k] = qb < Q ? (rb < nk ? 1.f : -1.f) : 0.f;
+        const unsigned i0 = (unsigned)co * H1 * W1 + 4u * t4;
+        g_wa[k] = (ra % nk) * nin + i0;
+        g_wb[k] = (rb % nk) * nin + i0;
+        // R is even, so rows 2 qp and 2 qp + 1 share their sub-domain
+        g_pb[k] = (qa < Q ? qa / R : b0) * (unsigned)s.pstride + i0;
+        g_bz[k] = t.b[co];
+        g_lds[k] = (4 * t4 * CO + co) * 16 + 2 * qp;
+      }
+    }
+    auto gen_load = [&](int yg) {
+#pragma unroll
+      for (int k = 0; k < TPL; ++k)
+        if (g_on[k]) {
+          const unsigned o = (unsigned)yg * W1;
+          g_xa[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wa[k] + o));
+          g_xb[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wb[k] + o));
+          g_lo[k] = *reinterpret_cast<const float4v*>(fc.a_lo + (g_pb[k] + o));
+          g_up[k] = *reinterpret_cast<const float4v*>(fc.a_up + (g_pb[k] + o));
+          g_bu[k] = *reinterpret_cast<const float4v*>(fc.b_up + (g_pb[k] + o));
+        }
+    };
+    // relaxation (Eq. 6) of the loaded coefficients into tile buf, with the intercept and bias
+    // terms of rows 2 qp and 2 qp + 1
+    auto gen_store = [&](float* buf) {
+#pragma unroll
+      for (int k = 0; k < TPL; ++k)
+        if (g_on[k]) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a = g_sa[k] * g_xa[k][e], b = g_sb[k] * g_xb[k][e];
+            const float ha = a * (a >= 0.f ? g_lo[k][e] : g_up[k][e]);
+            const float hb = b * (b >= 0.f ? g_lo[k][e] : g_up[k][e]);
+            fbeta_a = fmaf(fminf(a, 0.f), g_bu[k][e], fbeta_a);
+            fbeta_a = fmaf(ha, g_bz[k], fbeta_a);
+            fbeta_b = fmaf(fminf(b, 0.f), g_bu[k][e], fbeta_b);
+            fbeta_b = fmaf(hb, g_bz[k], fbeta_b);
+            *reinterpret_cast<float2v*>(buf + g_lds[k] + e * CO * 16) = float2v{ha, hb};
+          }
+        }
     };
 
     // prologue: parameters of stage 0, input rows 0 and 1; row 0 and the parameters landed
     dma_pars(pars[0], 0);
-    dma_tile(tiles[0], 0);
-    if (H1 > 1) {
-      dma_tile(tiles[1], 1);
-      wait_dma(ntw);
-    } else {
+    if constexpr (FC) {
+      gen_load(0);
+      gen_store(tiles[0]);
       wait_dma(0);
+    } else {
+      dma_tile(tiles[0], 0);
+      if (H1 > 1) {
+        dma_tile(tiles[1], 1);
+        wait_dma(ntw);
+      } else {
+        wait_dma(0);
+      }
     }
     lds_barrier();
 
@@ -977,12 +1073,16 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
         const float* tile = tiles[u % 3];
         dma_pars(pars[(u + 1) % 3], y1 + 1);
         const bool more = y1 + 2 < H1;
-        if (more) dma_tile(tiles[(u + 2) % 3], y1 + 2);
+        if constexpr (FC) {
+          if (y1 + 1 < H1) gen_load(y1 + 1);
+        } else if (more) {
+          dma_tile(tiles[(u + 2) % 3], y1 + 2);
+        }
 #pragma unroll
         for (int x1 = 0; x1 < W1; ++x1) {
           float bv[KS];
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(4 * ks + G) * CS + x1 * 16 + n];
+          for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(x1 * CO + 4 * ks + G) * 16 + n];
 #pragma unroll
           for (int c = 0; c < CPW; ++c) {
             float4v d = {0.f, 0.f, 0.f, 0.f};
@@ -1005,7 +1105,12 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
             for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
           }
         }
-        wait_dma(npw + (more ? ntw : 0));
+        if constexpr (FC) {
+          if (y1 + 1 < H1) gen_store(tiles[(u + 1) % 3]);
+          wait_dma(0);
+        } else {
+          wait_dma(npw + (more ? ntw : 0));
+        }
         lds_barrier();
       }
     }
@@ -1020,6 +1125,18 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
       }
     }
     lds_barrier();
+    if constexpr (FC) {
+      // rows 2 qp, 2 qp + 1 of every task of this wave: lanes qp, qp + 8, ..., qp + 56
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1) {
+        fbeta_a += __shfl_xor(fbeta_a, o, 64);
+        fbeta_b += __shfl_xor(fbeta_b, o, 64);
+      }
+      if (lane < 8) {
+        red_fc[wave * 16 + 2 * lane] = fbeta_a;
+        red_fc[wave * 16 + 2 * lane + 1] = fbeta_b;
+      }
+    }
     lds_barrier();  // the storers' final reduction
     return;
   }
@@ -1039,8 +1156,8 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
       const int r = it / CI, c = it - r * CI;
       const int y = yrow(e, r);
       if (y < 0 || y >= H0 || !qok) continue;
-      const float4v a = *reinterpret_cast<const float4v*>(rows[slot] +
-                                                          ((r * CI + c) * 16 + qn) * 16 + 4 * xg);
+      const float4v a = *reinterpret_cast<const float4v*>(
+          rows[slot] + ((r * CI + c) * 16 + qn) * 16 + 4 * (xg ^ (qn >> 2)));
       const int off = r * CI * W0 + c * W0 + 4 * xg;
       const float4v lo = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 0) * AST + off);
       const float4v up = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 1) * AST + off);
@@ -1074,8 +1191,15 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   if (ws != 0 || lane >= 16 || !qok) return;
   float tot = 0.f;
   for (int w = 0; w < NS; ++w) tot += red[w * 16 + lane];
+  if constexpr (FC) {
+    // the rows' own bias +-b_k[j] and the terms of the relaxation that built them
+    const unsigned r = q % R, nk = (unsigned)fc.nk;
+    float fb = r < nk ? fc.b[r] : -fc.b[r - nk];
+    for (int w = 0; w < NM; ++w) fb += red_fc[w * 16 + lane];
+    tot += fb;
+  }
   Acc a{tot, 0.f, 0.f};
-  sink_finish<MODE_SLAB>(s, a, q, q / R, q % R, false);
+  sink_finish<MODE_SLAB>(s, a, q, q / R, q % R, FC);
 }
 
 // The last two backward stages of a pass fused: T_2^T with the relaxation of layer 1, then T_1^T
@@ -2646,28 +2770,32 @@ ConvTKernel<MODE> convT_mfma_for(const DLayer& t, bool tape, int* nwaves) {
 }
 
 // Wave-specialised relaxing stage for the 16-wide output geometries; null when not covered.
-// *nwaves: matrix + storer waves; *lds: dynamic LDS bytes.
+// fc: the variant that builds its input from the fully connected layer above (bound passes
+// only).  *nwaves: matrix + storer waves; *lds: dynamic LDS bytes.
+using WsKernel = void (*)(DLayer, const float*, unsigned, unsigned, Sink, FcSrc);
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int NS>
-ConvTKernel<MODE_SLAB> convT_ws_inst(bool tape, int* nwaves, size_t* lds) {
+WsKernel convT_ws_inst(bool tape, bool fc, int* nwaves, size_t* lds) {
   *nwaves = CI / CPW + NS;
   *lds = 0;  // all LDS of the kernel is static
-  return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true>
-              : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false>;
+  if (fc) return tape ? nullptr : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false, true>;
+  return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true, false>
+              : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false, false>;
 }
 
-ConvTKernel<MODE_SLAB> convT_ws_for(const DLayer& t, bool tape, int* nwaves, size_t* lds) {
+WsKernel convT_ws_for(const DLayer& t, bool tape, bool fc, int* nwaves, size_t* lds) {
   const bool g_s2_16 = t.k == 4 && t.stride == 2 && t.pad == 1 && t.out_h == 8 && t.out_w == 8 &&
                        t.in_h == 16 && t.in_w == 16;
   const bool g_s1_16 = t.k == 3 && t.stride == 1 && t.pad == 1 && t.out_h == 16 &&
                        t.out_w == 16 && t.in_h == 16 && t.in_w == 16;
   if (g_s2_16 && t.in_c == 8 && t.out_c == 16)
-    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4>(tape, nwaves, lds);
+    return fc ? convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 1, 4>(tape, fc, nwaves, lds)
+              : convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4>(tape, fc, nwaves, lds);
   if (g_s2_16 && t.in_c == 8 && t.out_c == 8)
-    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 8, 8, 1, 4>(tape, nwaves, lds);
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 8, 8, 1, 4>(tape, fc, nwaves, lds);
   if (g_s2_16 && t.in_c == 16 && t.out_c == 32)
-    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4>(tape, nwaves, lds);
-  if (g_s1_16 && t.in_c == 8 && t.out_c == 8)
-    return convT_ws_inst<3, 1, 1, 16, 16, 16, 16, 8, 8, 1, 4>(tape, nwaves, lds);
+    return convT_ws_inst<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4>(tape, fc, nwaves, lds);
+  if (g_s1_16 && t.in_c == 8 && t.out_c == 8 && !fc)
+    return convT_ws_inst<3, 1, 1, 16, 16, 16, 16, 8, 8, 1, 4>(tape, fc, nwaves, lds);
   return nullptr;
 }
 
@@ -2693,16 +2821,11 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
     if (s.R >= 16) {
       int nwt = 0;
       size_t lds = 0;
-      if (ConvTKernel<MODE_SLAB> kern = convT_ws_for(t, s.tape != nullptr, &nwt, &lds)) {
+      if (WsKernel kern = convT_ws_for(t, s.tape != nullptr, false, &nwt, &lds)) {
         const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
-        if (lds > 65536 &&
-            hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)lds) != hipSuccess)
-          return fail(LIRPA_EDEVICE, "cannot reserve %zu bytes of LDS", lds);
         return launch_k(tag("convT_relax", m, pass), st, [&] {
           hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nwt), lds, st, t, in, (unsigned)ldq,
-                             (unsigned)Q, s);
+                             (unsigned)Q, s, FcSrc{});
         });
       }
     }
@@ -2917,6 +3040,37 @@ int pass3_window(const Chunk& c) {
   });
 }
 
+// First stage of a bound pass k that opens at a fully connected layer k over a convolution
+// k-1: the stage through T_{k-1} builds its input rows from W_k and the relaxation of layer k-1
+// itself and writes the rows relaxed onto layer k-2 into slab 0.  Returns 1 when the shapes or
+// alignment do not qualify (the caller runs the pass initialisation and the plain stage).
+int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
+  const lirpa_net* net = c.net;
+  if (c.tape || k < 3 || R < 16 || R % 2) return 1;
+  const lirpa_layer &fl = net->T[k - 1], &cv = net->T[k - 2];
+  if (fl.kind != LIRPA_LINEAR || cv.kind != LIRPA_CONV2D) return 1;
+  if (reinterpret_cast<uintptr_t>(fl.W) % 16) return 1;
+  // parameter offsets of the kernel are 32-bit
+  if ((double)c.nb * net->pstride >= 4.0e9) return 1;
+  int nw = 0;
+  size_t lds = 0;
+  DLayer t = dlayer(cv);
+  WsKernel kern = convT_ws_for(t, false, true, &nw, &lds);
+  if (!kern) return 1;
+  Sink s = slab_sink(c, k - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
+  FcSrc f{fl.W,
+          fl.b,
+          (int)net->n[k],
+          at<float>(c.ws, c.p->off_alo) + net->poff[k - 1],
+          at<float>(c.ws, c.p->off_aup) + net->poff[k - 1],
+          at<float>(c.ws, c.p->off_bup) + net->poff[k - 1]};
+  const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+  return launch_k(tag("convT_relax_fc", k - 1, k), c.st, [&] {
+    hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, c.st, t, nullptr, (unsigned)ldq,
+                       (unsigned)Q, s, f);
+  });
+}
+
 int bound_chunk(const Chunk& c, const float* C, float* lb) {
   const lirpa_net* net = c.net;
   const int L = net->L;
@@ -2940,6 +3094,17 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
       int e = pass3_window(c);
       if (e != 1) {
         if (e) return e;
+        if (int e2 = relax_layer(c, k)) return e2;
+        continue;
+      }
+    }
+    {
+      int e = fc_open_stage(c, k, R, Q, ldq);
+      if (e != 1) {
+        if (e) return e;
+        if (int e2 = run_stages(c, k, k - 2, R, Q, ldq, c.L + net->off[k], c.U + net->off[k],
+                                net->n_relu, nk))
+          return e2;
         if (int e2 = relax_layer(c, k)) return e2;
         continue;
       }
