@@ -547,7 +547,7 @@ __device__ __forceinline__ void block_finish(const Sink& s, Acc acc, float* red,
 // The y1 loop is unrolled over the rotation period so every register index is static.
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CPW, int NW,
           int MODE, bool TAPE>
-__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, MODE == MODE_BOUND && !TAPE ? 4 : 2)))
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(MODE == MODE_BOUND && !TAPE ? (CO <= 8 ? 4 : 3) : 1, MODE == MODE_BOUND && !TAPE ? 8 : 2)))
 k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, Sink s) {
   static_assert(K <= 4 && S <= K && CO % 4 == 0 && W0 % 4 == 0, "unsupported geometry");
   constexpr int KS = CO / 4;
@@ -568,7 +568,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   const unsigned q = q0 + n;
   const bool qok = q < Q;
   const unsigned b = qok ? q / (unsigned)s.R : 0u;
-  float* red = xs + (MODE == MODE_BOUND ? t.in_c * H0 * W0 : 0);  // [NW][3][16]
+  float* red = xs + (MODE == MODE_BOUND && s.x0 ? t.in_c * H0 * W0 : 0);  // [NW][3][16]
 
   const bool with_x0 = MODE == MODE_BOUND && s.x0 != nullptr;
   if (with_x0) {
@@ -678,6 +678,47 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   for (int c = 0; c < CPW; ++c)
 #pragma unroll
     for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+  // Stride 2 (bound stages): the four output columns x1*2 - P + kx of input column x1 do not
+  // overlap those of x1 + 2, so the MFMAs accumulate in place -- one float4 per input column
+  // x1, in two interleaved families (x1 even, x1 odd) -- and a row is summed from the two
+  // families only when it is complete, instead of after every MFMA.
+  constexpr bool DIRECT = MODE == MODE_BOUND && S == 2;
+  constexpr int NB = (W1 + 1) / 2;
+  float4v accd[DIRECT ? CPW : 1][2][DIRECT ? NB : 1];
+  if constexpr (DIRECT) {
+#pragma unroll
+    for (int c = 0; c < CPW; ++c)
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int m = 0; m < NB; ++m) accd[c][f][m] = float4v{0.f, 0.f, 0.f, 0.f};
+  }
+  // row of channel c from the two families (column x: x1 = 2m + f with 4m + kx = x + P - 2f)
+  auto gather = [&](int c, float* vals) {
+    if constexpr (DIRECT) {
+#pragma unroll
+      for (int x = 0; x < W0; ++x) {
+        float v = 0.f;
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+          const int tt = x + P - 2 * f;
+          if (tt >= 0 && (tt >> 2) < NB && 2 * (tt >> 2) + f < W1) v += accd[c][f][tt >> 2][tt & 3];
+        }
+        vals[x] = v;
+      }
+    }
+  };
+  auto reset = [&](int c) {
+    if constexpr (DIRECT) {
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int m = 0; m < NB; ++m) accd[c][f][m] = float4v{0.f, 0.f, 0.f, 0.f};
+    } else {
+#pragma unroll
+      for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+    }
+  };
 
   auto gaddr = [&](int y1, int v4) {
     const int cx = v4 >> 2, j4 = v4 & 3;
@@ -730,14 +771,22 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
         for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(4 * ks + G) * CS + x1 * 16 + n];
 #pragma unroll
         for (int c = 0; c < CPW; ++c) {
-          float4v d = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (DIRECT) {
+            float4v d = accd[c][x1 & 1][x1 >> 1];
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks)
+              d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+            accd[c][x1 & 1][x1 >> 1] = d;
+          } else {
+            float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kx = 0; kx < K; ++kx) {
-            const int col = x1 * S - P + kx;
-            if (col >= 0 && col < W0) acc[c][col] += d[kx];
+            for (int ks = 0; ks < KS; ++ks)
+              d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+#pragma unroll
+            for (int kx = 0; kx < K; ++kx) {
+              const int col = x1 * S - P + kx;
+              if (col >= 0 && col < W0) acc[c][col] += d[kx];
+            }
           }
         }
       }
@@ -752,9 +801,14 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
       if (done) {
 #pragma unroll
         for (int c = 0; c < CPW; ++c) {
-          emit(c, yout, acc[c]);
-#pragma unroll
-          for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+          if constexpr (DIRECT) {
+            float vals[W0];
+            gather(c, vals);
+            emit(c, yout, vals);
+          } else {
+            emit(c, yout, acc[c]);
+          }
+          reset(c);
         }
       }
       if (more) lds_barrier();
@@ -768,7 +822,13 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 #pragma unroll
       for (int c = 0; c < CPW; ++c) {
         load_row(c, (H1 - 1) * S - P + ky);
-        emit(c, (H1 - 1) * S - P + ky, acc[c]);
+        if constexpr (DIRECT) {
+          float vals[W0];
+          gather(c, vals);
+          emit(c, (H1 - 1) * S - P + ky, vals);
+        } else {
+          emit(c, (H1 - 1) * S - P + ky, acc[c]);
+        }
       }
     }
   }
@@ -2221,7 +2281,7 @@ __global__ void __launch_bounds__(kBlock)
 // Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q
 // and 8 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 8th tile of
 // 32 output features i, K runs over o two at a time with the A operand (W, read straight from
-// memory, L2-resident) fetched one group of 8 steps ahead.  Epilogue as in the other stages.
+// memory, L2-resident) fetched one group of 16 steps ahead.  Epilogue as in the other stages.
 template <int MODE>
 __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restrict__ in,
                                                   long ldq, long Q, Sink s) {
@@ -2242,7 +2302,7 @@ __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restr
   __syncthreads();
   Acc sum{0.f, 0.f, 0.f};
   const int KS = (nout + 1) / 2;
-  constexpr int U = 8;
+  constexpr int U = 16;
   for (int mt = wave; mt * 32 < nin; mt += nw) {
     floatx16 d;
 #pragma unroll
@@ -2272,11 +2332,48 @@ __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restr
       }
     }
     if (q < Q) {
+      // accumulator r holds feature i = mt*32 + 8 (r/4) + 4h + r%4: four runs of four
+      // consecutive features.  Every operand of the epilogue is loaded before the first store
+      // (the stores could alias them as far as the compiler knows, so it would not hoist them).
+      auto ld4 = [&](const float* p, int i0) {
+        if (i0 + 4 <= nin) return *reinterpret_cast<const float4v*>(p + i0);
+        float4v v = {0.f, 0.f, 0.f, 0.f};
+        for (int e = 0; e < 4; ++e)
+          if (i0 + e < nin) v[e] = p[i0 + e];
+        return v;
+      };
+      float4v p0[4], p1[4], p2[4], p3[4];
+      const long pb = b * s.pstride;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = mt * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (i < nin) sink_put<MODE>(s, sum, i, d[r], q, b);
+      for (int g = 0; g < 4; ++g) {
+        const int i0 = mt * 32 + 8 * g + 4 * h;
+        if constexpr (MODE == MODE_SLAB) {
+          p0[g] = ld4(s.a_lo + pb, i0);
+          p1[g] = ld4(s.a_up + pb, i0);
+          p2[g] = ld4(s.b_up + pb, i0);
+          p3[g] = ld4(s.bias, i0);  // per-neuron bias vector (bias_hw == 1)
+        } else {
+          p0[g] = s.x0 ? ld4(s.x0, i0) : float4v{0.f, 0.f, 0.f, 0.f};
+        }
       }
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = mt * 32 + 8 * g + 4 * h + e;
+          if (i >= nin) continue;
+          const float a = d[4 * g + e];
+          if (s.tape) s.tape[(long)i * s.ldq + q] = a;
+          if constexpr (MODE == MODE_SLAB) {
+            const float ah = a * (a >= 0.f ? p0[g][e] : p1[g][e]);
+            sum.beta = fmaf(fminf(a, 0.f), p2[g][e], sum.beta);
+            sum.beta = fmaf(ah, p3[g][e], sum.beta);
+            s.out[(long)i * s.ldq + q] = ah;
+          } else {
+            sum.lin = fmaf(a, p0[g][e], sum.lin);
+            sum.l1 += fabsf(a);
+          }
+        }
     }
   }
   block_finish<MODE>(s, sum, red, q0, Q, false);
@@ -2833,8 +2930,10 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
   if (ConvTKernel<MODE> kern = convT_mfma_for<MODE>(t, s.tape != nullptr, &nw)) {
     const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
     const size_t cs = (size_t)t.out_w * 16 + (80 - (t.out_w * 16) % 64) % 64;
+    // x0 is staged in LDS only when the linear term is not folded into the layer-1 bias
     size_t lds = (2 * (size_t)t.out_c * cs + (size_t)nw * 3 * 16 +
-                  (MODE == MODE_BOUND ? (size_t)t.in_c * t.in_h * t.in_w : 0)) * sizeof(float);
+                  (MODE == MODE_BOUND && s.x0 ? (size_t)t.in_c * t.in_h * t.in_w : 0)) *
+                 sizeof(float);
     return launch_k(tag((std::string("convT") + sfx).c_str(), m, pass), st, [&] {
       hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, st, t, in, (unsigned)ldq,
                          (unsigned)Q, s);
