@@ -141,6 +141,19 @@ __device__ __forceinline__ unsigned xcd_tile(unsigned blk) {
   return (blk & ~15u) + ((blk & 7u) << 1) + ((blk >> 3) & 1u);
 }
 
+// Index of the calling wave in its block, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
+// Store v at byte offset boff (< 2^31) from the wave-uniform address row: a buffer store with
+// the base in scalar registers, so no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void store_row(float* row, unsigned boff, float v) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(row, (short)0, 0x7fffffff, 0x00020000);
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), rs, boff, 0, 0);
+}
+
 // Workgroup barrier for LDS traffic only: waits for this wave's LDS operations, not for its
 // outstanding global stores (which __syncthreads() would also drain).
 __device__ __forceinline__ void lds_barrier() {
@@ -303,7 +316,7 @@ __global__ void __launch_bounds__(kBlock) k_init_rows(DLayer t, const float* __r
 __global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __restrict__ WT,
                                                       long Q, Sink s) {
   __shared__ float red[4][64];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = wave_id();
   const long q = blockIdx.x * 64L + lane;
   const bool ok = q < Q;
   const long qq = ok ? q : 0;
@@ -508,7 +521,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 template <int MODE>
 __device__ __forceinline__ void block_finish(const Sink& s, Acc acc, float* red, long q0, long Q,
                                              bool add_beta_from_acc) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id(), nw = blockDim.x >> 6;
   acc.beta += __shfl_xor(acc.beta, 32, 64);
   acc.lin += __shfl_xor(acc.lin, 32, 64);
   acc.l1 += __shfl_xor(acc.l1, 32, 64);
@@ -561,7 +574,7 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
   extern __shared__ float lds[];
   float* tiles = lds;                  // 2 x [CO][W1][16]
   float* xs = lds + 2 * TILE;          // MODE_BOUND: x0 [in_c*H0*W0]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
   if (q0 >= Q) return;  // grid padding, uniform per block
@@ -929,7 +942,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   __shared__ float red[NS * 16];
   __shared__ float red_fc[FC ? NM * 16 : 1];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
   if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned R = (unsigned)s.R;
@@ -1207,6 +1220,10 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   const unsigned q = q0 + qn;
   const bool qok = q < Q;
   const int bsel = qok ? (int)(q / R - b0) : 0;
+  // Rows q0..q0+15 all lie inside the slab's padded width (ldq is a multiple of 64), so rows
+  // past Q are stored too (never read as results) and the stores need no lane mask.  A store
+  // address is a block-uniform row base plus this lane's 32-bit byte offset.
+  const unsigned lane_boff = (4u * xg * ldq + qn) * 4u;
   float beta = 0.f;
   auto stage = [&](int e) {
     const int slot = e & 1;
@@ -1215,7 +1232,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
     for (int it = ws; it < nr * CI; it += NS) {
       const int r = it / CI, c = it - r * CI;
       const int y = yrow(e, r);
-      if (y < 0 || y >= H0 || !qok) continue;
+      if (y < 0 || y >= H0) continue;
       const float4v a = *reinterpret_cast<const float4v*>(
           rows[slot] + ((r * CI + c) * 16 + qn) * 16 + 4 * (xg ^ (qn >> 2)));
       const int off = r * CI * W0 + c * W0 + 4 * xg;
@@ -1223,16 +1240,16 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
       const float4v up = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 1) * AST + off);
       const float4v bu = *reinterpret_cast<const float4v*>(pst + (3 * bsel + 2) * AST + off);
       const float4v bz = *reinterpret_cast<const float4v*>(pst + 6 * AST + off);
-      const unsigned rowi = ((unsigned)c * H0 + y) * W0 + 4 * xg;
+      const unsigned row0 = ((unsigned)c * H0 + y) * W0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const unsigned idx = (rowi + j) * ldq + q;
-        if constexpr (TAPE) s.tape[idx] = a[j];
+        const size_t base = (size_t)(row0 + j) * ldq + q0;  // uniform
+        if constexpr (TAPE) store_row(s.tape + base, lane_boff, a[j]);
         const bool pos = a[j] >= 0.f;
         const float ah = a[j] * (pos ? lo[j] : up[j]);
         beta = fmaf(pos ? 0.f : a[j], bu[j], beta);
         beta = fmaf(ah, bz[j], beta);
-        s.out[idx] = ah;
+        store_row(s.out + base, lane_boff, ah);
       }
     }
   };
@@ -1305,7 +1322,7 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
   float* pars = ring + 3 * SLOT;     // 2 x PB
   float* red = pars + 2 * PB;        // (NS + C0) x 16
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
   if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned R = (unsigned)s.R;
@@ -1629,7 +1646,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   __shared__ float prm[4][NE];  // a_lo, a_up, b_up, W1 x0 + b1 of the window (0 outside)
   float* bred = red + NW * 16;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   // block -> (sub-domain, row group, y2, XW consecutive windows along x2)
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
@@ -1845,7 +1862,7 @@ __global__ void __launch_bounds__(512)
   __shared__ float rb1[NW * 2 * 16];  // bias terms of (3), per (wave, lane group, row)
   __shared__ float rl1[NW * 16];  // ||A_x||_1 partials of (4)
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   const int H3 = t3.out_h, W3 = t3.out_w, C3 = t3.out_c;
   const int NG = p2_groups(C3);
@@ -2075,7 +2092,7 @@ __global__ void __launch_bounds__(64 * NW)
   __shared__ float wrow[16];
   __shared__ int active;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
@@ -2288,7 +2305,7 @@ __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restr
   extern __shared__ float lds[];
   float* tile = lds;                            // [out_c][32]
   float* red = lds + (long)t.out_c * 32;        // [8][3][32]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id(), nw = blockDim.x >> 6;
   const int n = lane & 31, h = lane >> 5;
   const long q0 = (long)blockIdx.x * 32;
   const long q = q0 + n;
@@ -2508,7 +2525,7 @@ __global__ void __launch_bounds__(256)
                const float* __restrict__ tape, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                float* __restrict__ G, float* __restrict__ zout) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, g = lane >> 4;
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
   if (q0 >= Q) return;  // grid padding, uniform per block
