@@ -1652,10 +1652,10 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
   const int nxc = W2 / XW;
-  long blk = blockIdx.x;
-  const int x2c = (int)(blk % nxc); blk /= nxc;
-  const int y2 = (int)(blk % H2); blk /= H2;
-  const int g = (int)(blk % NG); blk /= NG;
+  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  const int x2c = (int)(blk % (unsigned)nxc); blk /= (unsigned)nxc;
+  const int y2 = (int)(blk % (unsigned)H2); blk /= (unsigned)H2;
+  const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
   const long b = blk;
   const int Y1 = y2 * t2.stride - t2.pad;  // window origin on g^(1), rows
   const int H1 = t1.out_h, Wd1 = t1.out_w;
@@ -1866,10 +1866,10 @@ __global__ void __launch_bounds__(512)
   const int n = lane & 15, G = lane >> 4;
   const int H3 = t3.out_h, W3 = t3.out_w, C3 = t3.out_c;
   const int NG = p2_groups(C3);
-  long blk = blockIdx.x;
-  const int x3 = (int)(blk % W3); blk /= W3;
-  const int y3 = (int)(blk % H3); blk /= H3;
-  const int g = (int)(blk % NG); blk /= NG;
+  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  const int x3 = (int)(blk % (unsigned)W3); blk /= (unsigned)W3;
+  const int y3 = (int)(blk % (unsigned)H3); blk /= (unsigned)H3;
+  const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
   const long b = blk;
   const int Y2 = y3 - P3, X2 = x3 - P3;  // g^(2) window origin (T_3 has stride 1)
   const int Y1 = Y2 - P2, X1 = X2 - P2;  // g^(1) window origin
@@ -2096,11 +2096,11 @@ __global__ void __launch_bounds__(64 * NW)
   const int n = lane & 15, G = lane >> 4;
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
-  long blk = blockIdx.x;
+  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
   const long blk_id = blk;
-  const int x2 = (int)(blk % W2); blk /= W2;
-  const int y2 = (int)(blk % H2); blk /= H2;
-  const int g = (int)(blk % NG); blk /= NG;
+  const int x2 = (int)(blk % (unsigned)W2); blk /= (unsigned)W2;
+  const int y2 = (int)(blk % (unsigned)H2); blk /= (unsigned)H2;
+  const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
   const long b = blk;
   const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;
   const int H1 = t1.out_h, Wd1 = t1.out_w;
