@@ -2583,6 +2583,162 @@ __global__ void __launch_bounds__(256)
   }
 }
 
+// Load of a float at byte offset boff (< 2^31) from the wave-uniform address row (buffer load,
+// base in scalar registers).
+__device__ __forceinline__ float load_row(const float* row, unsigned boff) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), (short)0, 0x7fffffff, 0x00020000);
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, boff, 0, 0));
+}
+
+// The witness forward step through a convolution of a covered shape (k <= 4), as a gather-form
+// implicit GEMM on 16x16x4 MFMA: M = 16 output channels, N = 16 rows q, and one K step per
+// (input channel ci, tap row ky) whose four K entries are the tap columns kx = lane group (a
+// column kx >= k carries a zero weight).  So a lane's input column is x*S - P + kx for every K
+// step and the input row and channel of a step are uniform over the wave: each B operand is one
+// buffer load from a uniform slab row at a per-lane offset fixed for the whole output position.
+// Each wave owns one M tile (16 output channels) and holds all its A operands (weights) in
+// registers; output positions are dealt round-robin to the waves of an M tile.  B operands are
+// loaded U K steps at a time, the next chunk (of this or the next output position) issued before
+// the MFMAs of the current one.  With WITNESS, x0 is staged in LDS.  Epilogue as in
+// k_fwd_mfma: G = pre-activation, zout = the row's relaxation line applied.
+template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO, bool WITNESS>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K >= 64 ? 3 : 4, 8)))
+    k_fwd_conv(DLayer t, const float* __restrict__ zin, unsigned ldq, unsigned Q, long R,
+               const float* __restrict__ w, const float* __restrict__ x0, float eps,
+               const float* __restrict__ tape, const float* __restrict__ a_lo,
+               const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+               float* __restrict__ G, float* __restrict__ zout) {
+  static_assert(K <= 4, "tap columns are the four lane groups");
+  constexpr int NKS = CI * K;                // K steps
+  constexpr int NMT = (CO + 15) / 16;        // M tiles
+  static_assert(NMT == 1 || NMT == 2 || NMT == 4, "M tiles are dealt to the 4 waves");
+  constexpr int U = NKS < 8 ? NKS : 8;       // K steps per chunk of B loads
+  constexpr int NCH = (NKS + U - 1) / U;
+  constexpr int NPOS = HO * WO;
+  __shared__ float xs[WITNESS ? CI * HI * WI : 1];
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int n = lane & 15, g = lane >> 4;
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  const unsigned q = q0 + n;
+  const bool qok = q < Q;
+  const float wq = qok ? w[q] : 0.f;
+  if (__syncthreads_or(wq != 0.f) == 0) return;  // uniform: the whole block is idle
+  const unsigned b = qok ? q / (unsigned)R : 0u;
+  const int mt = wave % NMT;
+  float wreg[NKS];
+  {
+    const int co = mt * 16 + n;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const int ci = ks / K, ky = ks % K;
+      wreg[ks] = (co < CO && g < K) ? t.W[((co * CI + ci) * K + ky) * K + g] : 0.f;
+    }
+  }
+  if constexpr (WITNESS) {
+    for (int e = threadIdx.x; e < CI * HI * WI; e += 256) xs[e] = x0[e];
+    __syncthreads();
+  }
+
+  // B operands of chunk c of output position pos into v
+  auto load_chunk = [&](int pos, int c, float* v) {
+    const int y = pos / WO, x = pos - y * WO;
+    const int yb = y * S - P, xi = x * S - P + g;
+    const bool xok = g < K && xi >= 0 && xi < WI;
+    const unsigned boff = ((unsigned)(xok ? xi : 0) * ldq + n) * 4u;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int ks = c * U + u;
+      v[u] = 0.f;
+      if (ks < NKS) {
+        const int ci = ks / K, yi = yb + ks % K;
+        if (yi >= 0 && yi < HI) {  // uniform
+          const unsigned f = ((unsigned)ci * HI + yi) * WI;
+          const float val = load_row(zin + (size_t)f * ldq + q0, boff);
+          if (xok) {
+            if constexpr (WITNESS)
+              v[u] = xs[f + xi] - eps * (val > 0.f ? 1.f : (val < 0.f ? -1.f : 0.f));
+            else
+              v[u] = val;
+          }
+        }
+      }
+    }
+  };
+  constexpr int PSTEP = 4 / NMT;
+  // epilogue operands of an output position (tape and relaxation line of the 4 outputs of this
+  // lane), fetched one position ahead when there is a next layer to feed
+  const bool fz = zout != nullptr && qok && wq != 0.f;
+  float et[4], el[4], eu[4], eb[4];
+  auto load_ep = [&](int p_, float* t_, float* l_, float* u_, float* b_) {
+    const int y = p_ / WO, x = p_ - y * WO;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int co = mt * 16 + 4 * g + r;
+      t_[r] = l_[r] = u_[r] = b_[r] = 0.f;
+      if (fz && co < CO) {
+        const unsigned o = ((unsigned)co * HO + y) * WO + x;
+        const long pi = (long)b * pstride + o;
+        t_[r] = tape[(size_t)o * ldq + q];
+        l_[r] = a_lo[pi];
+        u_[r] = a_up[pi];
+        b_[r] = b_up[pi];
+      }
+    }
+  };
+  float bufA[U], bufB[U];
+  int pos = wave / NMT;
+  if (pos < NPOS) {
+    load_chunk(pos, 0, bufA);
+    load_ep(pos, et, el, eu, eb);
+  }
+  for (; pos < NPOS; pos += PSTEP) {
+    float nt[4], nl[4], nu[4], nb[4];
+    if (pos + PSTEP < NPOS) load_ep(pos + PSTEP, nt, nl, nu, nb);
+    float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      float* cur = (c & 1) ? bufB : bufA;
+      float* nxt = (c & 1) ? bufA : bufB;
+      if (c + 1 < NCH)
+        load_chunk(pos, c + 1, nxt);
+      else if (pos + PSTEP < NPOS)
+        load_chunk(pos + PSTEP, 0, nxt);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ks = c * U + u;
+        if (ks < NKS) d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ks], cur[u], d, 0, 0, 0);
+      }
+    }
+    if constexpr (NCH % 2 == 1) {
+      // the next position's first chunk went to bufB: move it to bufA
+#pragma unroll
+      for (int u = 0; u < U; ++u) bufA[u] = bufB[u];
+    }
+    if (qok && wq != 0.f) {
+      const int y = pos / WO, x = pos - y * WO;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = mt * 16 + 4 * g + r;
+        if (co >= CO) continue;
+        const float gv = d[r] + t.b[co];
+        const unsigned o = ((unsigned)co * HO + y) * WO + x;
+        const size_t idx = (size_t)o * ldq + q;
+        G[idx] = gv;
+        if (zout) zout[idx] = et[r] >= 0.f ? el[r] * gv : fmaf(eu[r], gv, eb[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      et[r] = nt[r];
+      el[r] = nl[r];
+      eu[r] = nu[r];
+      eb[r] = nb[r];
+    }
+  }
+}
+
 // Adjoint accumulation for ReLU layer m: one wave per (sub-domain, neuron) sums over the rows of
 // the pass, w * max(A~,0) G (-> alpha), w * min(A~,0) G (-> upper slope) and w * min(A~,0)
 // (-> upper intercept), and for unstable neurons turns the last two into adjoints of l and u
@@ -3302,6 +3458,31 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
 // after bound_chunk has recorded the tape (passes visited in descending order; the adjoints of
 // l^(P), u^(P) are complete once every later pass has been visited).  full == 0 visits the
 // final pass only (intermediate bounds held fixed).  Result in ga ([nb][n_relu]).
+// Witness forward kernels of the covered convolution shapes (those of the Base, Wide and Deep
+// networks); null for any other layer (the generic k_fwd_mfma runs).
+using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
+                           const float*, float, const float*, const float*, const float*,
+                           const float*, long, float*, float*);
+template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO>
+FwdKernel fwd_conv_inst(bool witness) {
+  return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true>
+                 : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false>;
+}
+FwdKernel fwd_conv_for(const lirpa_layer& t, bool witness) {
+  if (t.kind != LIRPA_CONV2D) return nullptr;
+  auto is = [&](int k, int s_, int p_, int ci, int co, int hi, int ho) {
+    return t.k == k && t.stride == s_ && t.pad == p_ && t.in_c == ci && t.out_c == co &&
+           t.in_h == hi && t.in_w == hi && t.out_h == ho && t.out_w == ho;
+  };
+  if (is(4, 2, 1, 3, 8, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 8, 32, 32, 16, 16>(witness);
+  if (is(4, 2, 1, 3, 16, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 16, 32, 32, 16, 16>(witness);
+  if (is(4, 2, 1, 8, 16, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 16, 16, 16, 8, 8>(witness);
+  if (is(4, 2, 1, 16, 32, 16, 8)) return fwd_conv_inst<4, 2, 1, 16, 32, 16, 16, 8, 8>(witness);
+  if (is(4, 2, 1, 8, 8, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 8, 16, 16, 8, 8>(witness);
+  if (is(3, 1, 1, 8, 8, 16, 16)) return fwd_conv_inst<3, 1, 1, 8, 8, 16, 16, 16, 16>(witness);
+  return nullptr;
+}
+
 int grad_chunk(const Chunk& c, int full) {
   const lirpa_net* net = c.net;
   const Plan& p = *c.p;
@@ -3359,8 +3540,14 @@ int grad_chunk(const Chunk& c, int full) {
       float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
       DLayer t = dlayer(net->T[m - 1]);
       const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+      FwdKernel fk = fwd_conv_for(net->T[m - 1], m == 1);
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
-        if (m == 1)
+        if (fk)
+          hipLaunchKernelGGL(fk, dim3(nblk16), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
+                             (unsigned)Q, R, w, c.x0, c.eps, tp,
+                             at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
+                             at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout);
+        else if (m == 1)
           hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
                              (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
                              at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
