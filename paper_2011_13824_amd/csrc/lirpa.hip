@@ -2121,22 +2121,27 @@ __global__ void __launch_bounds__(64 * NW)
     return;
   }
 
-  // (1) relaxed window coefficients (as in the bound; window parameters staged once)
-  __shared__ float prm[2][C1 * NPOS];  // a_lo, a_up (zeros outside the map)
+  // (1) relaxed window coefficients (as in the bound; window parameters staged once), and per
+  // window neuron z1 and whether it is unstable (zeros outside the map)
+  __shared__ float prm[4][C1 * NPOS];  // a_lo, a_up, z1, unstable (1/0)
   {
     const long pb = b * pstride;
     for (int e = threadIdx.x; e < C1 * NPOS; e += NT) {
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
       const int y1 = Y1 + ky2, x1 = X1 + kx2;
-      float lo = 0.f, up = 0.f;
+      float lo = 0.f, up = 0.f, zz = 0.f, un = 0.f;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
-        const long pi = pb + ((long)c1 * H1 + y1) * Wd1 + x1;
-        lo = a_lo[pi];
-        up = a_up[pi];
+        const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
+        lo = a_lo[pb + ni];
+        up = a_up[pb + ni];
+        zz = z1[ni];
+        un = code1[b * n_relu + ni] == 5 ? 1.f : 0.f;
       }
       prm[0][e] = lo;
       prm[1][e] = up;
+      prm[2][e] = zz;
+      prm[3][e] = un;
     }
   }
   __syncthreads();
@@ -2214,41 +2219,49 @@ __global__ void __launch_bounds__(64 * NW)
   }
   __syncthreads();
 
-  // (3) G = z1 + W_1 delta at each window neuron; contributions summed over the 16 rows
+  // the tile now holds max(A~, 0), the non-negative parts of the unrelaxed window coefficients
   {
-    const int KD = t1.in_c * K1 * K1;
-    const int nks = (KD + 3) / 4;
-    const int c1A = lane & 15;
+    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
+    const P2Row pr = p2_row(C2, g, row);
+    const float sgn = pr.neg ? -1.f : 1.f;
+    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;
+    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      tile[c1 * CS + pos * 16 + row] = fmaxf(sgn * w2[e], 0.f);
+    }
+  }
+  __syncthreads();
+
+  // (3) G = z1 + W_1 delta at each window neuron on MFMA (M = 16 channels c1, N = 16 rows,
+  // one K step per (input channel, tap row) with the tap column as the lane group, so the
+  // footprint entry of a K step is uniform per lane group); contributions summed over the rows
+  {
+    static_assert(K1 == 4, "tap columns are the four lane groups");
+    constexpr int NK1 = NW * K1;  // K steps: in_c == NW
+    float w1r[NK1];
+#pragma unroll
+    for (int ks = 0; ks < NK1; ++ks) {
+      const int cc = ks / K1, ky = ks % K1, c1A = lane & 15;
+      w1r[ks] = (c1A < C1 && cc < t1.in_c)
+                    ? t1.W[(((long)c1A * t1.in_c + cc) * K1 + ky) * K1 + G] : 0.f;
+    }
     const float wn = wrow[n];
-    const P2Row prn = p2_row(C2, g, n);
-    const int c2n = prn.c2;
-    const float sgn = prn.neg ? -1.f : 1.f;
     for (int pos = wave; pos < NPOS; pos += NW) {
       const int j = pos / K2, i = pos - j * K2;
-      const int y1 = Y1 + j, x1 = X1 + i;
       float4v d = {0.f, 0.f, 0.f, 0.f};
-      for (int ks = 0; ks < nks; ++ks) {
-        const int kk = ks * 4 + G;
-        float av = 0.f, bv = 0.f;
-        if (kk < KD) {
-          const int cc = kk / (K1 * K1), rem = kk - cc * K1 * K1;
-          const int ky = rem / K1, kx = rem - ky * K1;
-          if (c1A < C1) av = t1.W[(long)c1A * KD + kk];
-          bv = dl[((cc * WO + j * S1 + ky) * WO + i * S1 + kx) * 16 + n];
-        }
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, d, 0, 0, 0);
+#pragma unroll
+      for (int ks = 0; ks < NK1; ++ks) {
+        const int cc = ks / K1, ky = ks % K1;
+        const float bv = dl[((cc * WO + j * S1 + ky) * WO + i * S1 + G) * 16 + n];
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(w1r[ks], bv, d, 0, 0, 0);
       }
-      const bool inmap = y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int c1 = 4 * G + r;
         float cval = 0.f;
-        if (c1 < C1 && inmap) {
-          const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
-          if (code1[b * n_relu + ni] == 5 && wn != 0.f) {
-            const float tv = sgn * t2.W[(((long)c2n * t2.in_c + c1) * t2.k + j) * t2.k + i];
-            cval = wn * fmaxf(tv, 0.f) * (d[r] + z1[ni]);
-          }
+        if (c1 < C1) {
+          const int e = c1 * NPOS + pos;
+          cval = wn * prm[3][e] * tile[c1 * CS + pos * 16 + n] * (d[r] + prm[2][e]);
         }
         cval += __shfl_xor(cval, 8, 64);
         cval += __shfl_xor(cval, 4, 64);
