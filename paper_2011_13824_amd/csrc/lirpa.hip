@@ -2604,6 +2604,55 @@ __device__ __forceinline__ float load_row(const float* row, unsigned boff) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, boff, 0, 0));
 }
 
+// Sum over each group of 8 consecutive lanes (lanes 8k..8k+7), valid in lanes 8k..8k+3: two
+// butterfly steps inside each quad, then the quad 4 lanes up (DPP, no LDS; a row rotation by r
+// hands lane i the value of lane i - r of its row of 16).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float sum8(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm(1,0,3,2): lane ^ 1
+  v += dpp_f<0x4E>(v);   // quad_perm(2,3,0,1): lane ^ 2
+  v += dpp_f<0x12C>(v);  // row_ror:12: lane i reads lane (i + 4) mod 16 of its row
+  return v;
+}
+
+// Adjoint accumulation for ReLU layer m from the partial sums of the fused witness forward: for
+// each (sub-domain, neuron), the R/8 groups of 8 rows of the sub-domain in increasing order (an
+// order fixed by the rows alone, so the result does not depend on where the sub-domain sits in
+// the chunk), skipping groups without weight; then, for unstable neurons, as k_grad_reduce.
+// Threads run over (sub-domain, position, channel) with the channel fastest, the order of the
+// partial sums.
+__global__ void __launch_bounds__(kBlock)
+    k_grad_gather(long nb, int CO, int NPOS, long R, const float* __restrict__ part,
+                  const unsigned char* __restrict__ gflag, const int8_t* __restrict__ code,
+                  const float* __restrict__ l, const float* __restrict__ u, long n_relu,
+                  float* __restrict__ ga, float* __restrict__ gl, float* __restrict__ gu) {
+  const long nm = (long)CO * NPOS;
+  const long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= nb * nm) return;
+  const long b = idx / nm, oc = idx % nm;
+  const int pos = (int)(oc / CO), co = (int)(oc % CO);
+  const long j = (long)co * NPOS + pos;
+  const long p = b * n_relu + j;
+  if (code[p] != 5) return;
+  const long g0 = b * (R / 8), ng = R / 8;
+  float sa = 0.f, da = 0.f, db = 0.f;
+  for (long k = 0; k < ng; ++k) {
+    if (!gflag[g0 + k]) continue;
+    const float* src = part + (g0 + k) * 3 * nm + oc;
+    sa += src[0];
+    da += src[nm];
+    db += src[2 * nm];
+  }
+  const float lj = l[p], uj = u[p], dd = uj - lj, d2 = dd * dd;
+  ga[p] += sa;
+  gl[p] += (da * uj - db * uj * uj) / d2;
+  gu[p] += (-da * lj + db * lj * lj) / d2;
+}
+
 // The witness forward step through a convolution of a covered shape (k <= 4), as a gather-form
 // implicit GEMM on 16x16x4 MFMA: M = 16 output channels, N = 16 rows q, and one K step per
 // (input channel ci, tap row ky) whose four K entries are the tap columns kx = lane group (a
@@ -2615,18 +2664,21 @@ __device__ __forceinline__ float load_row(const float* row, unsigned boff) {
 // loaded U K steps at a time, the next chunk (of this or the next output position) issued before
 // the MFMAs of the current one.  With WITNESS, x0 is staged in LDS.  Epilogue as in
 // k_fwd_mfma: G = pre-activation, zout = the row's relaxation line applied.
-template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO, bool WITNESS>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K >= 64 ? 3 : 4, 8)))
+template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO, bool WITNESS,
+          bool ZOUT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
+    ZOUT ? (CI * K >= 64 ? 2 : (CI * K >= 24 ? 3 : 4)) : (CI * K >= 64 ? 3 : 4), 8)))
     k_fwd_conv(DLayer t, const float* __restrict__ zin, unsigned ldq, unsigned Q, long R,
                const float* __restrict__ w, const float* __restrict__ x0, float eps,
                const float* __restrict__ tape, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
-               float* __restrict__ G, float* __restrict__ zout) {
+               float* __restrict__ G, float* __restrict__ zout, float* __restrict__ part,
+               unsigned char* __restrict__ gflag) {
   static_assert(K <= 4, "tap columns are the four lane groups");
   constexpr int NKS = CI * K;                // K steps
   constexpr int NMT = (CO + 15) / 16;        // M tiles
   static_assert(NMT == 1 || NMT == 2 || NMT == 4, "M tiles are dealt to the 4 waves");
-  constexpr int U = NKS < 8 ? NKS : 8;       // K steps per chunk of B loads
+  constexpr int U = NKS < 4 ? NKS : 4;       // K steps per chunk of B loads
   constexpr int NCH = (NKS + U - 1) / U;
   constexpr int NPOS = HO * WO;
   __shared__ float xs[WITNESS ? CI * HI * WI : 1];
@@ -2637,6 +2689,15 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K
   const unsigned q = q0 + n;
   const bool qok = q < Q;
   const float wq = qok ? w[q] : 0.f;
+  if (part) {
+    // the two groups of 8 rows of this tile: does any row carry weight
+    const bool live = __syncthreads_or(wq != 0.f && n < 8) != 0;
+    const bool live2 = __syncthreads_or(wq != 0.f && n >= 8) != 0;
+    if (threadIdx.x == 0) {
+      gflag[q0 / 8] = live ? 1 : 0;
+      gflag[q0 / 8 + 1] = live2 ? 1 : 0;
+    }
+  }
   if (__syncthreads_or(wq != 0.f) == 0) return;  // uniform: the whole block is idle
   const unsigned b = qok ? q / (unsigned)R : 0u;
   const int mt = wave % NMT;
@@ -2682,21 +2743,26 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K
   constexpr int PSTEP = 4 / NMT;
   // epilogue operands of an output position (tape and relaxation line of the 4 outputs of this
   // lane), fetched one position ahead when there is a next layer to feed
-  const bool fz = zout != nullptr && qok && wq != 0.f;
-  float et[4], el[4], eu[4], eb[4];
+  // (ZOUT: the output feeds a next layer; part: the adjoint sums are fused)
+  const bool fz = (ZOUT || part != nullptr) && qok && wq != 0.f;
+  constexpr int NE = ZOUT ? 4 : 1;
+  float et[4], el[NE], eu[NE], eb[NE];
   auto load_ep = [&](int p_, float* t_, float* l_, float* u_, float* b_) {
     const int y = p_ / WO, x = p_ - y * WO;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int co = mt * 16 + 4 * g + r;
-      t_[r] = l_[r] = u_[r] = b_[r] = 0.f;
+      t_[r] = 0.f;
+      if constexpr (ZOUT) l_[r] = u_[r] = b_[r] = 0.f;
       if (fz && co < CO) {
         const unsigned o = ((unsigned)co * HO + y) * WO + x;
-        const long pi = (long)b * pstride + o;
         t_[r] = tape[(size_t)o * ldq + q];
-        l_[r] = a_lo[pi];
-        u_[r] = a_up[pi];
-        b_[r] = b_up[pi];
+        if constexpr (ZOUT) {
+          const long pi = (long)b * pstride + o;
+          l_[r] = a_lo[pi];
+          u_[r] = a_up[pi];
+          b_[r] = b_up[pi];
+        }
       }
     }
   };
@@ -2707,7 +2773,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K
     load_ep(pos, et, el, eu, eb);
   }
   for (; pos < NPOS; pos += PSTEP) {
-    float nt[4], nl[4], nu[4], nb[4];
+    float nt[4], nl[NE], nu[NE], nb[NE];
     if (pos + PSTEP < NPOS) load_ep(pos + PSTEP, nt, nl, nu, nb);
     float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -2729,7 +2795,36 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K
 #pragma unroll
       for (int u = 0; u < U; ++u) bufA[u] = bufB[u];
     }
-    if (qok && wq != 0.f) {
+    if (part) {
+      // adjoint terms of the 4 outputs of this lane (rows without weight give exactly 0),
+      // summed over each group of 8 rows: w max(A~,0) G, w min(A~,0) G, w min(A~,0)
+      float4v sa, da, db;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = mt * 16 + 4 * g + r;
+        const float gv = d[r] + (co < CO ? t.b[co] : 0.f);
+        const bool on = fz && co < CO;
+        const float tp = fmaxf(et[r], 0.f), tn = fminf(et[r], 0.f);
+        sa[r] = on ? (wq * tp) * gv : 0.f;
+        da[r] = on ? (wq * tn) * gv : 0.f;
+        db[r] = on ? wq * tn : 0.f;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sa[r] = sum8(sa[r]);
+        da[r] = sum8(da[r]);
+        db[r] = sum8(db[r]);
+      }
+      if ((n & 7) == 0 && mt * 16 + 4 * g < CO) {
+        // [group][term][pos][co]: the 4 channels of this lane are contiguous
+        const size_t grp = q0 / 8 + (n >> 3);
+        float* dst = part + grp * 3 * (NPOS * CO) + (size_t)pos * CO + mt * 16 + 4 * g;
+        *reinterpret_cast<float4v*>(dst) = sa;
+        *reinterpret_cast<float4v*>(dst + NPOS * CO) = da;
+        *reinterpret_cast<float4v*>(dst + 2 * NPOS * CO) = db;
+      }
+    }
+    if (qok && wq != 0.f && (ZOUT || !part)) {
       const int y = pos / WO, x = pos - y * WO;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -2738,13 +2833,14 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CI * K
         const float gv = d[r] + t.b[co];
         const unsigned o = ((unsigned)co * HO + y) * WO + x;
         const size_t idx = (size_t)o * ldq + q;
-        G[idx] = gv;
-        if (zout) zout[idx] = et[r] >= 0.f ? el[r] * gv : fmaf(eu[r], gv, eb[r]);
+        if (!part) G[idx] = gv;
+        if constexpr (ZOUT) zout[idx] = et[r] >= 0.f ? el[r] * gv : fmaf(eu[r], gv, eb[r]);
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      et[r] = nt[r];
+    for (int r = 0; r < 4; ++r) et[r] = nt[r];
+#pragma unroll
+    for (int r = 0; r < NE; ++r) {
       el[r] = nl[r];
       eu[r] = nu[r];
       eb[r] = nb[r];
@@ -2856,6 +2952,9 @@ struct Plan {
   size_t off_wT[kMaxLayers + 1] = {};  // transposed FC weights of layers 2..L-1 (0 = none)
   size_t off_ga = 0, off_gl = 0, off_gu = 0, off_w = 0, off_za = 0, off_zb = 0, off_G = 0;
   size_t off_lbt = 0, off_grad = 0, off_p2part = 0;
+  // adjoint partial sums of the fused witness forward, [Qp/8][3][n_m], and a flag per group of
+  // 8 rows (whether any row of the group carries weight)
+  size_t off_gpart = 0, off_gflag = 0;
   long fwd_floats = 0;
 };
 
@@ -2978,6 +3077,15 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
     p.off_zb = o; o = align256(o + (size_t)fwd * 4);
     p.off_G = o;  o = align256(o + (size_t)fwd * 4);
     p.off_lbt = o; o = align256(o + (size_t)Bc * S * 4);
+    long gpart = 0, gflag = 0;
+    for (int k = 2; k <= L - 1; ++k) {
+      if ((k == 2 && win2) || (2 * net->n[k]) % 8) continue;
+      const long qp8 = round_up(Bc * 2 * net->n[k], 64) / 8;
+      gflag = std::max(gflag, qp8);
+      for (int m = 1; m <= k - 1; ++m) gpart = std::max(gpart, qp8 * 3 * net->n[m]);
+    }
+    p.off_gpart = o; o = align256(o + (size_t)gpart * 4);
+    p.off_gflag = o; o = align256(o + (size_t)gflag);
   }
   p.total = o;
   // kernels address a slab with 32-bit element offsets
@@ -3475,24 +3583,27 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
 // networks); null for any other layer (the generic k_fwd_mfma runs).
 using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
                            const float*, float, const float*, const float*, const float*,
-                           const float*, long, float*, float*);
+                           const float*, long, float*, float*, float*, unsigned char*);
 template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO>
-FwdKernel fwd_conv_inst(bool witness) {
-  return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true>
-                 : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false>;
+FwdKernel fwd_conv_inst(bool witness, bool zout) {
+  if (zout)
+    return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, true>
+                   : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, true>;
+  return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, false>
+                 : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, false>;
 }
-FwdKernel fwd_conv_for(const lirpa_layer& t, bool witness) {
+FwdKernel fwd_conv_for(const lirpa_layer& t, bool witness, bool zout) {
   if (t.kind != LIRPA_CONV2D) return nullptr;
   auto is = [&](int k, int s_, int p_, int ci, int co, int hi, int ho) {
     return t.k == k && t.stride == s_ && t.pad == p_ && t.in_c == ci && t.out_c == co &&
            t.in_h == hi && t.in_w == hi && t.out_h == ho && t.out_w == ho;
   };
-  if (is(4, 2, 1, 3, 8, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 8, 32, 32, 16, 16>(witness);
-  if (is(4, 2, 1, 3, 16, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 16, 32, 32, 16, 16>(witness);
-  if (is(4, 2, 1, 8, 16, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 16, 16, 16, 8, 8>(witness);
-  if (is(4, 2, 1, 16, 32, 16, 8)) return fwd_conv_inst<4, 2, 1, 16, 32, 16, 16, 8, 8>(witness);
-  if (is(4, 2, 1, 8, 8, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 8, 16, 16, 8, 8>(witness);
-  if (is(3, 1, 1, 8, 8, 16, 16)) return fwd_conv_inst<3, 1, 1, 8, 8, 16, 16, 16, 16>(witness);
+  if (is(4, 2, 1, 3, 8, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 8, 32, 32, 16, 16>(witness, zout);
+  if (is(4, 2, 1, 3, 16, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 16, 32, 32, 16, 16>(witness, zout);
+  if (is(4, 2, 1, 8, 16, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 16, 16, 16, 8, 8>(witness, zout);
+  if (is(4, 2, 1, 16, 32, 16, 8)) return fwd_conv_inst<4, 2, 1, 16, 32, 16, 16, 8, 8>(witness, zout);
+  if (is(4, 2, 1, 8, 8, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 8, 16, 16, 8, 8>(witness, zout);
+  if (is(3, 1, 1, 8, 8, 16, 16)) return fwd_conv_inst<3, 1, 1, 8, 8, 16, 16, 16, 16>(witness, zout);
   return nullptr;
 }
 
@@ -3553,13 +3664,18 @@ int grad_chunk(const Chunk& c, int full) {
       float* zout = (m < P - 1) ? zbuf[m % 2] : nullptr;
       DLayer t = dlayer(net->T[m - 1]);
       const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
-      FwdKernel fk = fwd_conv_for(net->T[m - 1], m == 1);
+      FwdKernel fk = fwd_conv_for(net->T[m - 1], m == 1, zout != nullptr);
+      // fused adjoint sums (groups of 8 rows aligned to the sub-domains) where R allows it
+      const bool fused = fk && P < L && R % 8 == 0 && p.off_gpart != 0;
+      float* gpart = fused ? at<float>(c.ws, p.off_gpart) : nullptr;
+      unsigned char* gflag = fused ? at<unsigned char>(c.ws, p.off_gflag) : nullptr;
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
         if (fk)
           hipLaunchKernelGGL(fk, dim3(nblk16), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
                              (unsigned)Q, R, w, c.x0, c.eps, tp,
                              at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
-                             at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout);
+                             at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout, gpart,
+                             gflag);
         else if (m == 1)
           hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
                              (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
@@ -3573,6 +3689,17 @@ int grad_chunk(const Chunk& c, int full) {
       });
       if (e) return e;
       long pairs = c.nb * net->n[m];
+      if (fused) {
+        e = launch_k(tag("grad_gather", m, P), c.st, [&] {
+          hipLaunchKernelGGL(k_grad_gather, grid_for(pairs), dim3(kBlock), 0, c.st, c.nb, t.out_c,
+                             t.out_h * t.out_w, R, gpart, gflag,
+                             at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
+                             net->n_relu, ga + off, gl + off, gu + off);
+        });
+        if (e) return e;
+        zin = zout;
+        continue;
+      }
       e = launch_k(tag("grad_reduce", m, P), c.st, [&] {
         hipLaunchKernelGGL(k_grad_reduce, dim3((unsigned)((pairs + 3) / 4)), dim3(kBlock), 0,
                            c.st, c.nb, net->n[m], R, ldq, w, tp, G,
