@@ -108,11 +108,15 @@ def path_flops(layers, S, B, launched):
 def traffic_record(workload, kernel):
     """HBM bytes per launch of a kernel class, as measured by rocprofv3 (FETCH_SIZE and
     WRITE_SIZE, scaled by a copy of known size) and recorded under profiles/ for this exact
-    library source (sha256 of lirpa.hip); None when no record matches."""
+    library build (sha256 of lirpa.hip followed by build.py); None when no record matches."""
     import glob
     import hashlib
-    src = os.path.join(ROOT, "paper_2011_13824_amd", "csrc", "lirpa.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    pkg = os.path.join(ROOT, "paper_2011_13824_amd")
+    h = hashlib.sha256()
+    for f in (os.path.join(pkg, "csrc", "lirpa.hip"), os.path.join(pkg, "build.py")):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    sha = h.hexdigest()
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         with open(path) as fh:
             for line in fh:
