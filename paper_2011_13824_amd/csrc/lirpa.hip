@@ -2312,12 +2312,12 @@ __global__ void __launch_bounds__(kBlock)
 // and 8 waves; the block's inputs in[.][q0..q0+31] sit in LDS, each wave takes every 8th tile of
 // 32 output features i, K runs over o two at a time with the A operand (W, read straight from
 // memory, L2-resident) fetched one group of 16 steps ahead.  Epilogue as in the other stages.
-template <int MODE>
-__global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restrict__ in,
+template <int MODE, int NWAVE>
+__global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* __restrict__ in,
                                                   long ldq, long Q, Sink s) {
   extern __shared__ float lds[];
   float* tile = lds;                            // [out_c][32]
-  float* red = lds + (long)t.out_c * 32;        // [8][3][32]
+  float* red = lds + (long)t.out_c * 32;        // [NWAVE][3][32]
   const int lane = threadIdx.x & 63, wave = wave_id(), nw = blockDim.x >> 6;
   const int n = lane & 31, h = lane >> 5;
   const long q0 = (long)blockIdx.x * 32;
@@ -2332,7 +2332,7 @@ __global__ void __launch_bounds__(512) k_fcT_mfma(DLayer t, const float* __restr
   __syncthreads();
   Acc sum{0.f, 0.f, 0.f};
   const int KS = (nout + 1) / 2;
-  constexpr int U = 16;
+  constexpr int U = NWAVE > 8 ? 8 : 16;
   for (int mt = wave; mt * 32 < nin; mt += nw) {
     floatx16 d;
 #pragma unroll
@@ -3198,9 +3198,18 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
   const unsigned nblk32 = (unsigned)((Q + 31) / 32);
   if (t.kind == LIRPA_LINEAR) {
     if (t.out_c <= 448) {
-      size_t lds = ((size_t)t.out_c * 32 + 8 * 3 * 32) * sizeof(float);
+      // few row tiles (a final pass): 16 waves per block, so that each wave carries fewer
+      // output tiles in sequence
+      const bool wide = nblk32 <= 256;
+      const int nwv = wide ? 16 : 8;
+      size_t lds = ((size_t)t.out_c * 32 + (size_t)nwv * 3 * 32) * sizeof(float);
       return launch_k(tag((std::string("fcT") + sfx).c_str(), m, pass), st, [&] {
-        hipLaunchKernelGGL(k_fcT_mfma<MODE>, dim3(nblk32), dim3(512), lds, st, t, in, ldq, Q, s);
+        if (wide)
+          hipLaunchKernelGGL((k_fcT_mfma<MODE, 16>), dim3(nblk32), dim3(1024), lds, st, t, in,
+                             ldq, Q, s);
+        else
+          hipLaunchKernelGGL((k_fcT_mfma<MODE, 8>), dim3(nblk32), dim3(512), lds, st, t, in, ldq,
+                             Q, s);
       });
     }
     return launch_k(tag((std::string("fcT_lane") + sfx).c_str(), m, pass), st, [&] {
