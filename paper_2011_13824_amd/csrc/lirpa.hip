@@ -2656,14 +2656,14 @@ __global__ void __launch_bounds__(kBlock)
 // The witness forward step through a convolution of a covered shape (k <= 4), as a gather-form
 // implicit GEMM on 16x16x4 MFMA: M = 16 output channels, N = 16 rows q, and one K step per
 // (input channel ci, tap row ky) whose four K entries are the tap columns kx = lane group (a
-// column kx >= k carries a zero weight).  So a lane's input column is x*S - P + kx for every K
-// step and the input row and channel of a step are uniform over the wave: each B operand is one
-// buffer load from a uniform slab row at a per-lane offset fixed for the whole output position.
-// Each wave owns one M tile (16 output channels) and holds all its A operands (weights) in
-// registers; output positions are dealt round-robin to the waves of an M tile.  B operands are
-// loaded U K steps at a time, the next chunk (of this or the next output position) issued before
-// the MFMAs of the current one.  With WITNESS, x0 is staged in LDS.  Epilogue as in
-// k_fwd_mfma: G = pre-activation, zout = the row's relaxation line applied.
+// column kx >= k carries a zero weight), so the input row and channel of a K step are uniform
+// over the wave.  Output rows are visited in order; the input rows they need sit in an LDS ring
+// ([slot][ci][x][16 rows q], slot = input row mod NSLOT, zero rows for the padding), and the S
+// input rows the next output row adds are loaded into registers at the start of a row and parked
+// in the ring after its MFMAs (with WITNESS, turned into x0 - eps sign(A_x) on the way).  Each
+// wave owns one M tile (16 output channels) and holds all its A operands (weights) in registers;
+// the output positions of a row are dealt to the waves of an M tile.  Epilogue: G =
+// pre-activation, zout = the row's relaxation line applied, or the fused adjoint sums.
 template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO, bool WITNESS,
           bool ZOUT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
@@ -2678,10 +2678,19 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   constexpr int NKS = CI * K;                // K steps
   constexpr int NMT = (CO + 15) / 16;        // M tiles
   static_assert(NMT == 1 || NMT == 2 || NMT == 4, "M tiles are dealt to the 4 waves");
-  constexpr int U = NKS < 4 ? NKS : 4;       // K steps per chunk of B loads
-  constexpr int NCH = (NKS + U - 1) / U;
   constexpr int NPOS = HO * WO;
+  constexpr int PSTEP = 4 / NMT;             // waves per M tile
+  static_assert(WO % PSTEP == 0, "the positions of a row are dealt evenly");
+  constexpr int IPW = WO / PSTEP;            // positions per wave and output row
+  constexpr int ROWF = CI * WI * 16;         // floats of one input row in the ring
+  // K + S slots (one barrier per output row) where they fit in 48 KB, else K (two barriers)
+  constexpr int NSLOT = (K + S) * ROWF * 4 <= 48 * 1024 ? K + S : K;
+  constexpr bool TWO_BAR = NSLOT == K;
+  constexpr int NF4 = S * CI * WI * 4;       // float4 of the S input rows an output row adds
+  constexpr int PFT = (NF4 + 255) / 256;
+  static_assert(K % S == 0 || !TWO_BAR, "prologue chunks fit the ring");
   __shared__ float xs[WITNESS ? CI * HI * WI : 1];
+  __shared__ float ring[NSLOT * ROWF];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, g = lane >> 4;
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
@@ -2715,32 +2724,44 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     __syncthreads();
   }
 
-  // B operands of chunk c of output position pos into v
-  auto load_chunk = [&](int pos, int c, float* v) {
-    const int y = pos / WO, x = pos - y * WO;
-    const int yb = y * S - P, xi = x * S - P + g;
-    const bool xok = g < K && xi >= 0 && xi < WI;
-    const unsigned boff = ((unsigned)(xok ? xi : 0) * ldq + n) * 4u;
+  // input rows ybase .. ybase+S-1 into registers (float4 e = (row j, ci, x, quarter of q))
+  auto slot_of = [](int yi) { return (yi + 8 * NSLOT) % NSLOT; };
+  float4v pf[PFT];
+  auto fetch_rows = [&](int ybase) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int ks = c * U + u;
-      v[u] = 0.f;
-      if (ks < NKS) {
-        const int ci = ks / K, yi = yb + ks % K;
-        if (yi >= 0 && yi < HI) {  // uniform
-          const unsigned f = ((unsigned)ci * HI + yi) * WI;
-          const float val = load_row(zin + (size_t)f * ldq + q0, boff);
-          if (xok) {
-            if constexpr (WITNESS)
-              v[u] = xs[f + xi] - eps * (val > 0.f ? 1.f : (val < 0.f ? -1.f : 0.f));
-            else
-              v[u] = val;
-          }
-        }
+    for (int k = 0; k < PFT; ++k) {
+      const int e = threadIdx.x + k * 256;
+      pf[k] = float4v{0.f, 0.f, 0.f, 0.f};
+      if (e < NF4) {
+        const int j4 = e & 3, fr = e >> 2;
+        const int xi = fr % WI, ci = (fr / WI) % CI, yi = ybase + fr / (WI * CI);
+        if (yi >= 0 && yi < HI)
+          pf[k] = *reinterpret_cast<const float4v*>(
+              zin + (size_t)(((unsigned)ci * HI + yi) * WI + xi) * ldq + q0 + 4 * j4);
       }
     }
   };
-  constexpr int PSTEP = 4 / NMT;
+  // ... and into their ring slots (rows outside the map stay zero)
+  auto park_rows = [&](int ybase) {
+#pragma unroll
+    for (int k = 0; k < PFT; ++k) {
+      const int e = threadIdx.x + k * 256;
+      if (e < NF4) {
+        const int j4 = e & 3, fr = e >> 2;
+        const int xi = fr % WI, ci = (fr / WI) % CI, yi = ybase + fr / (WI * CI);
+        float4v v = pf[k];
+        if constexpr (WITNESS) {
+          if (yi >= 0 && yi < HI) {
+            const float xv = xs[((unsigned)ci * HI + yi) * WI + xi];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj)
+              v[jj] = xv - eps * (v[jj] > 0.f ? 1.f : (v[jj] < 0.f ? -1.f : 0.f));
+          }
+        }
+        *reinterpret_cast<float4v*>(ring + ((slot_of(yi) * CI + ci) * WI + xi) * 16 + 4 * j4) = v;
+      }
+    }
+  };
   // epilogue operands of an output position (tape and relaxation line of the 4 outputs of this
   // lane), fetched one position ahead when there is a next layer to feed
   // (ZOUT: the output feeds a next layer; part: the adjoint sums are fused)
@@ -2766,35 +2787,33 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       }
     }
   };
-  float bufA[U], bufB[U];
-  int pos = wave / NMT;
-  if (pos < NPOS) {
-    load_chunk(pos, 0, bufA);
-    load_ep(pos, et, el, eu, eb);
+  // prologue: the input rows of output row 0, S at a time
+  for (int yb = -P; yb < K - P; yb += S) {
+    fetch_rows(yb);
+    park_rows(yb);
   }
-  for (; pos < NPOS; pos += PSTEP) {
-    float nt[4], nl[NE], nu[NE], nb[NE];
-    if (pos + PSTEP < NPOS) load_ep(pos + PSTEP, nt, nl, nu, nb);
-    float4v d = {0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+  auto pos_of = [&](int y, int k) { return y * WO + wave / NMT + k * PSTEP; };
+  load_ep(pos_of(0, 0), et, el, eu, eb);
+  for (int y = 0; y < HO; ++y) {
+    const int ynew = y * S - P + K;  // first input row output row y + 1 adds
+    if (y + 1 < HO) fetch_rows(ynew);
+#pragma unroll 1
+    for (int k = 0; k < IPW; ++k) {
+      const int pos = pos_of(y, k);
+      const bool has_next = k + 1 < IPW || y + 1 < HO;
+      float nt[4], nl[NE], nu[NE], nb[NE];
+      if (has_next) load_ep(k + 1 < IPW ? pos_of(y, k + 1) : pos_of(y + 1, 0), nt, nl, nu, nb);
+      const int xi = (pos - y * WO) * S - P + g;
+      const bool xok = g < K && xi >= 0 && xi < WI;
+      const float* col = ring + (xok ? xi : 0) * 16 + n;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      float* cur = (c & 1) ? bufB : bufA;
-      float* nxt = (c & 1) ? bufA : bufB;
-      if (c + 1 < NCH)
-        load_chunk(pos, c + 1, nxt);
-      else if (pos + PSTEP < NPOS)
-        load_chunk(pos + PSTEP, 0, nxt);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int ks = c * U + u;
-        if (ks < NKS) d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ks], cur[u], d, 0, 0, 0);
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int ci = ks / K, yi = y * S - P + ks % K;
+        const float bv = xok ? col[(slot_of(yi) * CI + ci) * WI * 16] : 0.f;
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ks], bv, d, 0, 0, 0);
       }
-    }
-    if constexpr (NCH % 2 == 1) {
-      // the next position's first chunk went to bufB: move it to bufA
-#pragma unroll
-      for (int u = 0; u < U; ++u) bufA[u] = bufB[u];
-    }
     if (part) {
       // adjoint terms of the 4 outputs of this lane (rows without weight give exactly 0),
       // summed over each group of 8 rows: w max(A~,0) G, w min(A~,0) G, w min(A~,0)
@@ -2844,6 +2863,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       el[r] = nl[r];
       eu[r] = nu[r];
       eb[r] = nb[r];
+    }
+    }  // positions of row y
+    if (y + 1 < HO) {
+      if constexpr (TWO_BAR) __syncthreads();  // the slots ynew takes are free
+      park_rows(ynew);
+      __syncthreads();
     }
   }
 }
