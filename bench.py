@@ -71,6 +71,21 @@ def stage_work(layers, S, B):
                  + t1["out_c"] * w1 * w1 * t1["in_c"] * t1["k"] ** 2)
         add("pass3_window[layer1,pass3]", 2.0 * Q3 * wmacs,
             4.0 * (3 * B * (n[1] + n[2]) + Q3))
+    if L >= 5 and all(layers[i]["kind"] == wl.CONV for i in (0, 1, 2, 3)) \
+            and layers[1]["stride"] == 1 and layers[2]["stride"] == 1:
+        # pass 4 restricted to receptive fields: the C3 x K4 x K4 entries of a row's window on
+        # g^(3) each reach C2 x K3 x K3 entries of g^(2); the C2 x W2 x W2 entries of that window
+        # (W2 = K4 + K3 - 1) each reach C1 x K2 x K2 of g^(1); the C1 x W1 x W1 entries of the
+        # g^(1) window (W1 = W2 + K2 - 1) each reach in_c x K1 x K1 inputs
+        t1, t2, t3, t4 = layers[0], layers[1], layers[2], layers[3]
+        Q4 = B * 2 * n[4]
+        w2 = t4["k"] + t3["k"] - 1
+        w1 = w2 + t2["k"] - 1
+        wmacs = (t3["out_c"] * t4["k"] ** 2 * t2["out_c"] * t3["k"] ** 2
+                 + t2["out_c"] * w2 * w2 * t1["out_c"] * t2["k"] ** 2
+                 + t1["out_c"] * w1 * w1 * t1["in_c"] * t1["k"] ** 2)
+        add("pass4_window[layer1,pass4]", 2.0 * Q4 * wmacs,
+            4.0 * (3 * B * (n[1] + n[2] + n[3]) + Q4))
     for k in range(2, L + 1):
         R = 2 * n[k] if k < L else S
         Q = B * R

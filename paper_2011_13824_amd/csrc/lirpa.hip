@@ -2062,6 +2062,263 @@ __global__ void __launch_bounds__(512)
     L[b * n_relu + off3 + j] = v;
 }
 
+// Pass 4 restricted to each row's receptive field, when T_4 .. T_1 are convolutions with T_3 and
+// T_2 of stride 1 (the Deep shape).  Row +-e_j of h^(4), j = (c4, y4, x4), carried through T_4
+// is +-W_4[c4] on the K4 x K4 window of j on g^(3); the layer-3 relaxation and T_3^T spread it
+// over a (K4 + K3 - 1)^2 window of g^(2), the layer-2 relaxation and T_2^T over a
+// (K4 + K3 + K2 - 2)^2 window of g^(1), and the layer-1 relaxation and T_1^T over that window's
+// footprint on x.  One block of 8 waves takes the 16 rows sharing a window (rows as in
+// k_pass2_window, over the channels of h^(4)):
+//  (1) stages the relaxation parameters of the three windows (zeros outside the maps),
+//  (2) relaxes the g^(3) window (Eq. 6) with its intercept and bias terms,
+//  (3) applies T_3^T, then T_2^T, as gathers on 16x16x4 MFMA (M = channels, K = (c, ky, kx)),
+//      one window position per wave at a time, relaxing each result into the next LDS tile,
+//  (4) applies T_1^T to the g^(1) tile with the rotating lane-group scheme (one wave per input
+//      channel of T_1) and concretises (Eq. 8),
+//  (5) writes l_j or u_j.  Arithmetically the dense pass minus products with zero.
+template <int K4, int S4, int P4, int K3, int P3, int K2, int P2, int K1, int S1, int P1,
+          int C1, int C2, int C3>
+__global__ void __launch_bounds__(512)
+    k_pass4_window(DLayer t1, DLayer t2, DLayer t3, DLayer t4, const float* __restrict__ a_lo,
+                   const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
+                   long poff1, long poff2, long poff3, const float* __restrict__ bias, float eps,
+                   float* __restrict__ L, float* __restrict__ U, long n_relu, long off4) {
+  constexpr int NW = 8, NT = 64 * NW;
+  constexpr int N3 = K4 * K4;               // g^(3) window positions
+  constexpr int W2W = K4 - 1 + K3;          // g^(2) window width (T_3 has stride 1)
+  constexpr int N2 = W2W * W2W;
+  constexpr int W1W = W2W - 1 + K2;         // g^(1) window width (T_2 has stride 1)
+  constexpr int N1 = W1W * W1W;
+  constexpr int E3 = C3 * N3, E2 = C2 * N2, E1 = C1 * N1;
+  constexpr int WO = (W1W - 1) * S1 + K1;   // footprint width on x
+  constexpr int KD3 = C3 * K3 * K3, NKS3 = (KD3 + 3) / 4;  // K of the T_3^T gather
+  constexpr int KD2 = C2 * K2 * K2, NKS2 = (KD2 + 3) / 4;  // K of the T_2^T gather
+  constexpr int KS1 = C1 / 4;
+  constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int CS3 = N3 * 16 + (80 - (N3 * 16) % 64) % 64;
+  constexpr int CS2 = N2 * 16 + (80 - (N2 * 16) % 64) % 64;
+  constexpr int CS1 = N1 * 16 + (80 - (N1 * 16) % 64) % 64;
+  constexpr int RP = NT / 16;               // threads per row in (2)
+  static_assert(C1 % 4 == 0 && C1 <= 16 && C2 <= 16 && K1 <= 4 && K2 <= 4 && K3 <= 4 &&
+                K4 <= 4, "geometry");
+  // the g^(3) tile is dead once T_3^T has read it, so the g^(1) tile reuses its space
+  __shared__ float tile31[C3 * CS3 > C1 * CS1 ? C3 * CS3 : C1 * CS1];
+  float* const tile3 = tile31;
+  float* const tile1 = tile31;
+  __shared__ float tile2[C2 * CS2];
+  __shared__ float p3s[4][E3];  // a_lo, a_up, b_up, bias of the g^(3) window
+  __shared__ float p2s[4][E2];  // ... of the g^(2) window
+  __shared__ float p1s[4][E1];  // ... of the g^(1) window (bias: W1 x0 + b1)
+  __shared__ float rb3[RP * 16];      // bias terms of (2), per (part, row)
+  __shared__ float rb2[NW * 4 * 16];  // bias terms of (3a), per (wave, lane group, row)
+  __shared__ float rb1[NW * 4 * 16];  // bias terms of (3b)
+  __shared__ float rl1[NW * 16];      // ||A_x||_1 partials of (4)
+
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int n = lane & 15, G = lane >> 4;
+  const int H4 = t4.out_h, W4 = t4.out_w, C4 = t4.out_c;
+  const int NG = p2_groups(C4);
+  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  const int x4 = (int)(blk % (unsigned)W4); blk /= (unsigned)W4;
+  const int y4 = (int)(blk % (unsigned)H4); blk /= (unsigned)H4;
+  const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
+  const long b = blk;
+  const int Y3 = y4 * S4 - P4, X3 = x4 * S4 - P4;  // g^(3) window origin
+  const int Y2 = Y3 - P3, X2 = X3 - P3;            // g^(2) window origin
+  const int Y1 = Y2 - P2, X1 = X2 - P2;            // g^(1) window origin
+  const int H3 = t3.out_h, Wd3 = t3.out_w, H2 = t2.out_h, Wd2 = t2.out_w;
+  const int H1 = t1.out_h, Wd1 = t1.out_w;
+  const long pb = b * pstride;
+
+  // (1) parameters of the three windows
+  auto stage = [&](int e, int Ww, int Y0, int X0, int Hm, int Wm, long poff) {
+    const int c = e / (Ww * Ww), p = e - c * Ww * Ww;
+    const int y = Y0 + p / Ww, x = X0 + p % Ww;
+    float4v v = {0.f, 0.f, 0.f, 0.f};
+    if (y >= 0 && y < Hm && x >= 0 && x < Wm) {
+      const long ni = ((long)c * Hm + y) * Wm + x;
+      v = float4v{a_lo[pb + poff + ni], a_up[pb + poff + ni], b_up[pb + poff + ni],
+                  bias[poff + ni]};
+    }
+    return v;
+  };
+  for (int e = threadIdx.x; e < E3 + E2 + E1; e += NT) {
+    if (e < E3) {
+      const float4v v = stage(e, K4, Y3, X3, H3, Wd3, poff3);
+      p3s[0][e] = v[0]; p3s[1][e] = v[1]; p3s[2][e] = v[2]; p3s[3][e] = v[3];
+    } else if (e < E3 + E2) {
+      const int f = e - E3;
+      const float4v v = stage(f, W2W, Y2, X2, H2, Wd2, poff2);
+      p2s[0][f] = v[0]; p2s[1][f] = v[1]; p2s[2][f] = v[2]; p2s[3][f] = v[3];
+    } else {
+      const int f = e - E3 - E2;
+      const float4v v = stage(f, W1W, Y1, X1, H1, Wd1, poff1);
+      p1s[0][f] = v[0]; p1s[1][f] = v[1]; p1s[2][f] = v[2]; p1s[3][f] = v[3];
+    }
+  }
+  __syncthreads();
+
+  // (2) relaxed g^(3) window of the 16 rows
+  {
+    const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const P2Row pr = p2_row(C4, g, row);
+    const float sgn = pr.neg ? -1.f : 1.f;
+    const float* w4 = t4.W + (long)pr.c2 * E3;  // [C3][K4][K4] of output channel c4
+    float bpart = 0.f;
+    for (int e = part; e < E3; e += RP) {
+      const int c3 = e / N3, p = e - c3 * N3;
+      const float w = sgn * w4[e];
+      const float v = w >= 0.f ? w * p3s[0][e] : w * p3s[1][e];
+      bpart = fmaf(fminf(w, 0.f), p3s[2][e], bpart);
+      bpart = fmaf(v, p3s[3][e], bpart);
+      tile3[c3 * CS3 + p * 16 + row] = v;
+    }
+    rb3[part * 16 + row] = bpart;
+  }
+  __syncthreads();
+
+  // (3) T^T gather from tile `src` (window width SW, channel stride SCS) through the weights of
+  // `tt` (kernel KK, stride 1; NKS <= NKSM steps of 4 entries of K = (c, ky, kx)) into the next
+  // window (width DW, Cd channels), relaxed with the parameters ps (4 arrays, pstr apart) into
+  // `dst`; bias terms into rb[(wave * 4 + G) * 16 + n].  The A operands sit in registers.
+  constexpr int NKSM = NKS3 > NKS2 ? NKS3 : NKS2;
+  auto gather = [&](const DLayer& tt, const float* src, int SW, int SCS, int KK, int NKS, int KD,
+                    float* dst, int DW, int DCS, int Cd, const float* pp, int pstr, float* rb) {
+    const int m = lane & 15;  // A operand row: channel of the destination window
+    float areg[NKSM];
+#pragma unroll
+    for (int ks = 0; ks < NKSM; ++ks) {
+      const int k = 4 * ks + G;
+      areg[ks] = 0.f;
+      if (ks < NKS && k < KD && m < Cd) {
+        const int c = k / (KK * KK), rem = k - c * KK * KK;
+        const int ky = rem / KK, kx = rem - ky * KK;
+        areg[ks] = tt.W[(((long)c * Cd + m) * KK + ky) * KK + kx];
+      }
+    }
+    float bpart = 0.f;
+    const int ND = DW * DW;
+    for (int p = wave; p < ND; p += NW) {
+      const int y = p / DW, x = p - y * DW;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NKSM; ++ks) {
+        if (ks >= NKS) break;
+        const int k = 4 * ks + G;
+        float bv = 0.f;
+        if (k < KD) {
+          const int c = k / (KK * KK), rem = k - c * KK * KK;
+          const int ky = rem / KK, kx = rem - ky * KK;
+          const int iy = y - ky, ix = x - kx;  // source window position feeding (y, x)
+          if (iy >= 0 && iy < SW && ix >= 0 && ix < SW)
+            bv = src[c * SCS + (iy * SW + ix) * 16 + n];
+        }
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[ks], bv, d, 0, 0, 0);
+      }
+      if (G * 4 < Cd) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int c = 4 * G + r;
+          const int e = c * ND + p;
+          const float a = d[r];
+          const float ah = a >= 0.f ? a * pp[e] : a * pp[pstr + e];
+          bpart = fmaf(fminf(a, 0.f), pp[2 * pstr + e], bpart);
+          bpart = fmaf(ah, pp[3 * pstr + e], bpart);
+          dst[c * DCS + p * 16 + n] = ah;
+        }
+      }
+    }
+    rb[(wave * 4 + G) * 16 + n] = bpart;
+  };
+  gather(t3, tile3, K4, CS3, K3, NKS3, KD3, tile2, W2W, CS2, C2, &p2s[0][0], E2, rb2);
+  __syncthreads();
+  gather(t2, tile2, W2W, CS2, K2, NKS2, KD2, tile1, W1W, CS1, C1, &p1s[0][0], E1, rb1);
+  __syncthreads();
+
+  // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
+  {
+    const int c0 = wave;
+    const bool cok = c0 < t1.in_c;
+    float l1 = 0.f;
+    if (cok) {
+      float wreg[PER1][KS1];
+      {
+        const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+        for (int ph = 0; ph < PER1; ++ph) {
+          const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+          for (int ks = 0; ks < KS1; ++ks) {
+            const int c1 = 4 * ks + G;
+            wreg[ph][ks] = (slot < K1 && kx < K1)
+                               ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
+          }
+        }
+      }
+      const int Hi = t1.in_h, Wi = t1.in_w;
+      const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
+      float acc[WO];
+#pragma unroll
+      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+      auto emit = [&](int yl) {
+        const int yy = OY + yl;
+        if (yy < 0 || yy >= Hi) return;
+#pragma unroll
+        for (int x = 0; x < WO; ++x) {
+          const int xc = OX + x;
+          l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
+        }
+      };
+#pragma unroll
+      for (int j = 0; j < W1W; ++j) {
+        const int ph = j % PER1;
+#pragma unroll
+        for (int i = 0; i < W1W; ++i) {
+          const int pos = j * W1W + i;
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS1; ++ks)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                wreg[ph][ks], tile1[(4 * ks + G) * CS1 + pos * 16 + n], d, 0, 0, 0);
+#pragma unroll
+          for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+        }
+        const int ky = ((G - ph * S1) % K1 + K1) % K1;
+        if (G < K1 && ky < S1) {
+          emit(j * S1 + ky);
+#pragma unroll
+          for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+        }
+      }
+      {
+        const int ky = ((G - ((W1W - 1) % PER1) * S1) % K1 + K1) % K1;
+        if (G < K1 && ky >= S1) emit((W1W - 1) * S1 + ky);
+      }
+    }
+    l1 += __shfl_xor(l1, 16, 64);
+    l1 += __shfl_xor(l1, 32, 64);
+    if (lane < 16) rl1[wave * 16 + lane] = l1;
+  }
+  __syncthreads();
+
+  // (5) the bound of each row
+  if (threadIdx.x >= 16) return;
+  const int row = threadIdx.x;
+  const P2Row pr = p2_row(C4, g, row);
+  float tb = (pr.neg ? -1.f : 1.f) * t4.b[pr.c2];
+  for (int q = 0; q < RP; ++q) tb += rb3[q * 16 + row];
+  for (int q = 0; q < NW * 4; ++q) tb += rb2[q * 16 + row];
+  for (int q = 0; q < NW * 4; ++q) tb += rb1[q * 16 + row];
+  float ta = 0.f;
+  for (int w = 0; w < NW; ++w) ta += rl1[w * 16 + row];
+  const float v = tb - eps * ta;
+  const long j = ((long)pr.c2 * H4 + y4) * W4 + x4;
+  if (pr.neg)
+    U[b * n_relu + off4 + j] = -v;
+  else
+    L[b * n_relu + off4 + j] = v;
+}
+
 // Reverse sweep of the receptive-field pass 2.  Layer-1 bounds do not depend on alpha, so the
 // rows of pass 2 only feed d J / d alpha of the layer-1 neurons of their own window:
 // sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
@@ -3498,6 +3755,41 @@ int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
   });
 }
 
+// Kernel for the receptive-field pass 4 (T_4 over the stride-1 T_3, T_2 over T_1; the Deep
+// shape), or null.
+using Pass4Kernel = void (*)(DLayer, DLayer, DLayer, DLayer, const float*, const float*,
+                             const float*, long, long, long, long, const float*, float, float*,
+                             float*, long, long);
+Pass4Kernel pass4_kernel_for(const lirpa_net* net) {
+  if (net->L < 5) return nullptr;
+  const lirpa_layer &t1 = net->T[0], &t2 = net->T[1], &t3 = net->T[2], &t4 = net->T[3];
+  for (const lirpa_layer* t : {&t1, &t2, &t3, &t4})
+    if (t->kind != LIRPA_CONV2D) return nullptr;
+  if (t4.out_c % 16 && t4.out_c != 8) return nullptr;
+  const bool s1 = t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.out_c == 8 && t1.in_c <= 8;
+  const bool s2 = t2.k == 3 && t2.stride == 1 && t2.pad == 1 && t2.out_c == 8;
+  const bool s3 = t3.k == 3 && t3.stride == 1 && t3.pad == 1 && t3.out_c == 8;
+  const bool s4 = t4.k == 4 && t4.stride == 2 && t4.pad == 1;
+  if (s1 && s2 && s3 && s4) return k_pass4_window<4, 2, 1, 3, 1, 3, 1, 4, 2, 1, 8, 8, 8>;
+  return nullptr;
+}
+
+int pass4_window(const Chunk& c) {
+  const lirpa_net* net = c.net;
+  Pass4Kernel kern = pass4_kernel_for(net);
+  if (!kern) return 1;
+  const lirpa_layer& t4 = net->T[3];
+  long blocks = c.nb * p2_groups(t4.out_c) * t4.out_h * t4.out_w;
+  return launch_k(tag("pass4_window", 1, 4), c.st, [&] {
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(512), 0, c.st, dlayer(net->T[0]),
+                       dlayer(net->T[1]), dlayer(net->T[2]), dlayer(net->T[3]),
+                       at<float>(c.ws, c.p->off_alo), at<float>(c.ws, c.p->off_aup),
+                       at<float>(c.ws, c.p->off_bup), net->pstride, net->poff[1], net->poff[2],
+                       net->poff[3], at<float>(c.ws, c.p->off_bz), c.eps, c.L, c.U, net->n_relu,
+                       net->off[4]);
+  });
+}
+
 int bound_chunk(const Chunk& c, const float* C, float* lb) {
   const lirpa_net* net = c.net;
   const int L = net->L;
@@ -3511,6 +3803,14 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     long nk = net->n[k], R = 2 * nk, Q = c.nb * R, ldq = round_up(Q, 64);
     if (k == 2 && (!c.tape || pass2_grad_kernel_for(net))) {
       int e = pass2_window(c);
+      if (e != 1) {
+        if (e) return e;
+        if (int e2 = relax_layer(c, k)) return e2;
+        continue;
+      }
+    }
+    if (k == 4 && !c.tape) {
+      int e = pass4_window(c);
       if (e != 1) {
         if (e) return e;
         if (int e2 = relax_layer(c, k)) return e2;
