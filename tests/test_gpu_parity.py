@@ -93,19 +93,21 @@ def test_small_conv_ragged_batch_with_alpha():
         check("small u", u, ulr)
 
 
-def test_alpha_on_base():
-    w = wl.base()
+@pytest.mark.parametrize("name", ["base", "wide", "deep"])
+def test_alpha_on_conv_nets(name):
+    # random lower slopes through every stage kind, the receptive-field passes included
+    w = wl.get(name)
     rnet = ref.RefNet(w.layers)
     split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=6)
     alpha = np.random.default_rng(3).uniform(0, 1, (6, rnet.n_relu)).astype(np.float32)
     lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split, alpha)
     lr, llr, ulr, code = ref.bound(rnet, w.x0, w.eps, w.C, split, alpha)
-    check("base+alpha lb", lb, lr)
-    check("base+alpha l", l, llr)
-    check("base+alpha u", u, ulr)
+    check(f"{name}+alpha lb", lb, lr)
+    check(f"{name}+alpha l", l, llr)
+    check(f"{name}+alpha u", u, ulr)
 
 
-@pytest.mark.parametrize("name", ["tiny", "base"])
+@pytest.mark.parametrize("name", ["tiny", "base", "wide", "deep"])
 def test_all_split_matches_closed_form(name):
     w = wl.get(name)
     rng = np.random.default_rng(5)
