@@ -927,7 +927,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NS), CI / CPW + NS <= 8 ? 4 :
   constexpr int NPV4 = PB / 4;
   constexpr int PP = (NPV4 + NTM - 1) / NTM;
   static_assert(AST % 256 == 0 && NV4 % 64 == 0, "DMA chunks must be whole waves");
-  static_assert(!FC || (!TAPE && W1 % 4 == 0), "FC source: bound passes, float4 quads of x1");
+  static_assert(!FC || W1 % 4 == 0, "FC source: float4 quads of x1");
   // FC source: task tk of an input row = (quad qd of four consecutive x1 of channel co, pair of
   // rows q0 + 2 qp, q0 + 2 qp + 1), qd = t4 * CO + co, tk = 8 qd + qp
   constexpr int NTASK = CO * W1 / 4 * 8;
@@ -2930,7 +2930,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
                const float* __restrict__ tape, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                float* __restrict__ G, float* __restrict__ zout, float* __restrict__ part,
-               unsigned char* __restrict__ gflag) {
+               unsigned char* __restrict__ gflag, const float* __restrict__ tapeW, int tnk) {
   static_assert(K <= 4, "tap columns are the four lane groups");
   constexpr int NKS = CI * K;                // K steps
   constexpr int NMT = (CO + 15) / 16;        // M tiles
@@ -3034,7 +3034,15 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       if constexpr (ZOUT) l_[r] = u_[r] = b_[r] = 0.f;
       if (fz && co < CO) {
         const unsigned o = ((unsigned)co * HO + y) * WO + x;
-        t_[r] = tape[(size_t)o * ldq + q];
+        if (tapeW) {
+          // the pass's rows over this layer's output are +-W_k[j] (j = r mod nk, sign + for
+          // r < nk): no recorded tape
+          const unsigned ra = q % (unsigned)R, nk = (unsigned)tnk;
+          const float wv = tapeW[(size_t)(ra % nk) * (CO * HO * WO) + o];
+          t_[r] = ra < nk ? wv : -wv;
+        } else {
+          t_[r] = tape[(size_t)o * ldq + q];
+        }
         if constexpr (ZOUT) {
           const long pi = (long)b * pstride + o;
           l_[r] = a_lo[pi];
@@ -3450,7 +3458,9 @@ template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, i
 WsKernel convT_ws_inst(bool tape, bool fc, int* nwaves, size_t* lds) {
   *nwaves = CI / CPW + NS;
   *lds = 0;  // all LDS of the kernel is static
-  if (fc) return tape ? nullptr : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false, true>;
+  if (fc)
+    return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true, true>
+                : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false, true>;
   return tape ? k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, true, false>
               : k_convT_relax_ws<K, S, P, H1, W1, H0, W0, CO, CI, CPW, NS, false, false>;
 }
@@ -3724,24 +3734,68 @@ int pass3_window(const Chunk& c) {
   });
 }
 
+// Witness forward kernels of the covered convolution shapes (those of the Base, Wide and Deep
+// networks); null for any other layer (the generic k_fwd_mfma runs).
+using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
+                           const float*, float, const float*, const float*, const float*,
+                           const float*, long, float*, float*, float*, unsigned char*,
+                           const float*, int);
+template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO>
+FwdKernel fwd_conv_inst(bool witness, bool zout) {
+  if (zout)
+    return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, true>
+                   : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, true>;
+  return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, false>
+                 : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, false>;
+}
+FwdKernel fwd_conv_for(const lirpa_layer& t, bool witness, bool zout) {
+  if (t.kind != LIRPA_CONV2D) return nullptr;
+  auto is = [&](int k, int s_, int p_, int ci, int co, int hi, int ho) {
+    return t.k == k && t.stride == s_ && t.pad == p_ && t.in_c == ci && t.out_c == co &&
+           t.in_h == hi && t.in_w == hi && t.out_h == ho && t.out_w == ho;
+  };
+  if (is(4, 2, 1, 3, 8, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 8, 32, 32, 16, 16>(witness, zout);
+  if (is(4, 2, 1, 3, 16, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 16, 32, 32, 16, 16>(witness, zout);
+  if (is(4, 2, 1, 8, 16, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 16, 16, 16, 8, 8>(witness, zout);
+  if (is(4, 2, 1, 16, 32, 16, 8)) return fwd_conv_inst<4, 2, 1, 16, 32, 16, 16, 8, 8>(witness, zout);
+  if (is(4, 2, 1, 8, 8, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 8, 16, 16, 8, 8>(witness, zout);
+  if (is(3, 1, 1, 8, 8, 16, 16)) return fwd_conv_inst<3, 1, 1, 8, 8, 16, 16, 16, 16>(witness, zout);
+  return nullptr;
+}
+
 // First stage of a bound pass k that opens at a fully connected layer k over a convolution
 // k-1: the stage through T_{k-1} builds its input rows from W_k and the relaxation of layer k-1
 // itself and writes the rows relaxed onto layer k-2 into slab 0.  Returns 1 when the shapes or
 // alignment do not qualify (the caller runs the pass initialisation and the plain stage).
+// Whether pass k (R rows per sub-domain) opens inside the stage through layer k-1.  With a
+// gradient tape the pass then records no tape over g^(k-1): its rows are +-W_k[j] of every
+// sub-domain, and the witness forward through layer k-1 reads them from W_k (which needs the
+// fused forward kernel for that layer).
+bool fc_open_ok(const Chunk& c, int k, long R) {
+  const lirpa_net* net = c.net;
+  if (k < 3 || k >= net->L || R < 16 || R % 2) return false;
+  const lirpa_layer &fl = net->T[k - 1], &cv = net->T[k - 2];
+  if (fl.kind != LIRPA_LINEAR || cv.kind != LIRPA_CONV2D) return false;
+  if (reinterpret_cast<uintptr_t>(fl.W) % 16) return false;
+  // parameter offsets of the kernel are 32-bit
+  if ((double)c.nb * net->pstride >= 4.0e9) return false;
+  int nw = 0;
+  size_t lds = 0;
+  if (!convT_ws_for(dlayer(cv), c.tape, true, &nw, &lds)) return false;
+  if (c.tape && (R % 8 || !c.p->off_gpart || !fwd_conv_for(cv, k - 1 == 1, false))) return false;
+  return true;
+}
+
 int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
   const lirpa_net* net = c.net;
-  if (c.tape || k < 3 || R < 16 || R % 2) return 1;
+  if (!fc_open_ok(c, k, R)) return 1;
   const lirpa_layer &fl = net->T[k - 1], &cv = net->T[k - 2];
-  if (fl.kind != LIRPA_LINEAR || cv.kind != LIRPA_CONV2D) return 1;
-  if (reinterpret_cast<uintptr_t>(fl.W) % 16) return 1;
-  // parameter offsets of the kernel are 32-bit
-  if ((double)c.nb * net->pstride >= 4.0e9) return 1;
   int nw = 0;
   size_t lds = 0;
   DLayer t = dlayer(cv);
-  WsKernel kern = convT_ws_for(t, false, true, &nw, &lds);
-  if (!kern) return 1;
+  WsKernel kern = convT_ws_for(t, c.tape, true, &nw, &lds);
   Sink s = slab_sink(c, k - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
+  s.tape = tape_of(c, k, k - 2);
   FcSrc f{fl.W,
           fl.b,
           (int)net->n[k],
@@ -3913,34 +3967,6 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
 // after bound_chunk has recorded the tape (passes visited in descending order; the adjoints of
 // l^(P), u^(P) are complete once every later pass has been visited).  full == 0 visits the
 // final pass only (intermediate bounds held fixed).  Result in ga ([nb][n_relu]).
-// Witness forward kernels of the covered convolution shapes (those of the Base, Wide and Deep
-// networks); null for any other layer (the generic k_fwd_mfma runs).
-using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
-                           const float*, float, const float*, const float*, const float*,
-                           const float*, long, float*, float*, float*, unsigned char*);
-template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO>
-FwdKernel fwd_conv_inst(bool witness, bool zout) {
-  if (zout)
-    return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, true>
-                   : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, true>;
-  return witness ? k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, true, false>
-                 : k_fwd_conv<K, S, P, CI, CO, HI, WI, HO, WO, false, false>;
-}
-FwdKernel fwd_conv_for(const lirpa_layer& t, bool witness, bool zout) {
-  if (t.kind != LIRPA_CONV2D) return nullptr;
-  auto is = [&](int k, int s_, int p_, int ci, int co, int hi, int ho) {
-    return t.k == k && t.stride == s_ && t.pad == p_ && t.in_c == ci && t.out_c == co &&
-           t.in_h == hi && t.in_w == hi && t.out_h == ho && t.out_w == ho;
-  };
-  if (is(4, 2, 1, 3, 8, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 8, 32, 32, 16, 16>(witness, zout);
-  if (is(4, 2, 1, 3, 16, 32, 16)) return fwd_conv_inst<4, 2, 1, 3, 16, 32, 32, 16, 16>(witness, zout);
-  if (is(4, 2, 1, 8, 16, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 16, 16, 16, 8, 8>(witness, zout);
-  if (is(4, 2, 1, 16, 32, 16, 8)) return fwd_conv_inst<4, 2, 1, 16, 32, 16, 16, 8, 8>(witness, zout);
-  if (is(4, 2, 1, 8, 8, 16, 8)) return fwd_conv_inst<4, 2, 1, 8, 8, 16, 16, 8, 8>(witness, zout);
-  if (is(3, 1, 1, 8, 8, 16, 16)) return fwd_conv_inst<3, 1, 1, 8, 8, 16, 16, 16, 16>(witness, zout);
-  return nullptr;
-}
-
 int grad_chunk(const Chunk& c, int full) {
   const lirpa_net* net = c.net;
   const Plan& p = *c.p;
@@ -4001,6 +4027,10 @@ int grad_chunk(const Chunk& c, int full) {
       FwdKernel fk = fwd_conv_for(net->T[m - 1], m == 1, zout != nullptr);
       // fused adjoint sums (groups of 8 rows aligned to the sub-domains) where R allows it
       const bool fused = fk && P < L && R % 8 == 0 && p.off_gpart != 0;
+      // an FC-opened pass recorded no tape over its first stage's input: rebuild it from W_P
+      const bool wtape = m == P - 1 && fc_open_ok(c, P, R);
+      const float* tapeW = wtape ? net->T[P - 1].W : nullptr;
+      const int tnk = wtape ? (int)net->n[P] : 0;
       float* gpart = fused ? at<float>(c.ws, p.off_gpart) : nullptr;
       unsigned char* gflag = fused ? at<unsigned char>(c.ws, p.off_gflag) : nullptr;
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
@@ -4009,7 +4039,7 @@ int grad_chunk(const Chunk& c, int full) {
                              (unsigned)Q, R, w, c.x0, c.eps, tp,
                              at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
                              at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout, gpart,
-                             gflag);
+                             gflag, tapeW, tnk);
         else if (m == 1)
           hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
                              (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
