@@ -2939,7 +2939,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   constexpr int PSTEP = 4 / NMT;             // waves per M tile
   static_assert(WO % PSTEP == 0, "the positions of a row are dealt evenly");
   constexpr int IPW = WO / PSTEP;            // positions per wave and output row
-  constexpr int ROWF = CI * WI * 16;         // floats of one input row in the ring
+  // a ring row holds the input columns -P .. (WO-1)*S - P + 3 (zero outside the map), so every
+  // lane's column of every K step is in range and needs no test
+  constexpr int XW = (WO - 1) * S + 4;
+  static_assert(P >= 0 && P + WI <= XW, "ring row covers the map");
+  constexpr int ROWF = CI * XW * 16;         // floats of one input row in the ring
   // K + S slots (one barrier per output row) where they fit in 48 KB, else K (two barriers)
   constexpr int NSLOT = (K + S) * ROWF * 4 <= 48 * 1024 ? K + S : K;
   constexpr bool TWO_BAR = NSLOT == K;
@@ -3015,7 +3019,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
               v[jj] = xv - eps * (v[jj] > 0.f ? 1.f : (v[jj] < 0.f ? -1.f : 0.f));
           }
         }
-        *reinterpret_cast<float4v*>(ring + ((slot_of(yi) * CI + ci) * WI + xi) * 16 + 4 * j4) = v;
+        *reinterpret_cast<float4v*>(ring + ((slot_of(yi) * CI + ci) * XW + xi + P) * 16 + 4 * j4) =
+            v;
       }
     }
   };
@@ -3052,7 +3057,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       }
     }
   };
-  // prologue: the input rows of output row 0, S at a time
+  // prologue: the padding columns of every slot are zero for good; the input rows of output
+  // row 0, S at a time
+  for (int e = threadIdx.x; e < NSLOT * CI * XW * 4; e += 256) {
+    const int xr = (e / 4) % XW;
+    if (xr < P || xr >= P + WI) *reinterpret_cast<float4v*>(ring + 4 * e) = float4v{0.f, 0.f, 0.f, 0.f};
+  }
   for (int yb = -P; yb < K - P; yb += S) {
     fetch_rows(yb);
     park_rows(yb);
@@ -3063,20 +3073,22 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   for (int y = 0; y < HO; ++y) {
     const int ynew = y * S - P + K;  // first input row output row y + 1 adds
     if (y + 1 < HO) fetch_rows(ynew);
+    int sb[K];  // ring offsets of the K input rows of output row y (uniform)
+#pragma unroll
+    for (int ky = 0; ky < K; ++ky) sb[ky] = slot_of(y * S - P + ky) * ROWF;
 #pragma unroll 1
     for (int k = 0; k < IPW; ++k) {
       const int pos = pos_of(y, k);
       const bool has_next = k + 1 < IPW || y + 1 < HO;
       float nt[4], nl[NE], nu[NE], nb[NE];
       if (has_next) load_ep(k + 1 < IPW ? pos_of(y, k + 1) : pos_of(y + 1, 0), nt, nl, nu, nb);
-      const int xi = (pos - y * WO) * S - P + g;
-      const bool xok = g < K && xi >= 0 && xi < WI;
-      const float* col = ring + (xok ? xi : 0) * 16 + n;
+      // this lane's ring column (x*S - P + kx, kx = lane group) plus P; a group kx >= K reads
+      // a finite value that meets a zero weight
+      const float* col = ring + ((pos - y * WO) * S + g) * 16 + n;
       float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        const int ci = ks / K, yi = y * S - P + ks % K;
-        const float bv = xok ? col[(slot_of(yi) * CI + ci) * WI * 16] : 0.f;
+        const float bv = col[sb[ks % K] + (ks / K) * XW * 16];
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ks], bv, d, 0, 0, 0);
       }
     if (part) {
