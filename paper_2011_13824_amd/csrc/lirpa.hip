@@ -1931,35 +1931,35 @@ __global__ void __launch_bounds__(512)
   }
   __syncthreads();
 
-  // (3) T_2^T: A over the g^(1) window, one position per wave at a time, relaxed into tile1
+  // (3) T_2^T: A over the g^(1) window, one position per wave at a time, relaxed into tile1.
+  // One K step per (c2, ky) with the tap column kx as the lane group: the source row of a step
+  // is uniform (steps with no source row are skipped) and a lane's source column is fixed for
+  // the whole position.
   {
+    static_assert(K2 <= 4, "tap columns are the four lane groups");
     const int m = lane & 15;  // A operand row: channel c1 of g^(1)
-    float a2[NKS2];
+    float a2[C2 * K2];
 #pragma unroll
-    for (int ks = 0; ks < NKS2; ++ks) {
-      const int k = 4 * ks + G;
-      a2[ks] = 0.f;
-      if (m < C1 && k < KD2) {
-        const int c2 = k / (K2 * K2), rem = k - c2 * K2 * K2;
-        const int ky = rem / K2, kx = rem - ky * K2;
-        a2[ks] = t2.W[(((long)c2 * C1 + m) * K2 + ky) * K2 + kx];
-      }
+    for (int ks = 0; ks < C2 * K2; ++ks) {
+      const int c2 = ks / K2, ky = ks % K2;
+      a2[ks] = (m < C1 && G < K2) ? t2.W[(((long)c2 * C1 + m) * K2 + ky) * K2 + G] : 0.f;
     }
     float bpart = 0.f;
     for (int p = wave; p < N1; p += NW) {
       const int y = p / W1W, x = p - y * W1W;
+      const int ix = x - G;  // g^(2) window column feeding (y, x) through tap column G
+      const bool xok = ix >= 0 && ix < K3;
+      const float* colp = tile2 + (xok ? ix : 0) * 16 + n;
       float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < NKS2; ++ks) {
-        const int k = 4 * ks + G;
-        float bv = 0.f;
-        if (k < KD2) {
-          const int c2 = k / (K2 * K2), rem = k - c2 * K2 * K2;
-          const int ky = rem / K2, kx = rem - ky * K2;
-          const int iy = y - ky, ix = x - kx;  // g^(2) window position feeding (y, x)
-          if (iy >= 0 && iy < K3 && ix >= 0 && ix < K3) bv = tile2[c2 * CS2 + (iy * K3 + ix) * 16 + n];
+      for (int ky = 0; ky < K2; ++ky) {
+        const int iy = y - ky;
+        if (iy < 0 || iy >= K3) continue;  // uniform
+#pragma unroll
+        for (int c2 = 0; c2 < C2; ++c2) {
+          const float bv = xok ? colp[c2 * CS2 + iy * K3 * 16] : 0.f;
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(a2[c2 * K2 + ky], bv, d, 0, 0, 0);
         }
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a2[ks], bv, d, 0, 0, 0);
       }
       if (G * 4 < C1) {
 #pragma unroll
@@ -2177,43 +2177,40 @@ __global__ void __launch_bounds__(512)
   }
   __syncthreads();
 
-  // (3) T^T gather from tile `src` (window width SW, channel stride SCS) through the weights of
-  // `tt` (kernel KK, stride 1; NKS <= NKSM steps of 4 entries of K = (c, ky, kx)) into the next
-  // window (width DW, Cd channels), relaxed with the parameters ps (4 arrays, pstr apart) into
-  // `dst`; bias terms into rb[(wave * 4 + G) * 16 + n].  The A operands sit in registers.
-  constexpr int NKSM = NKS3 > NKS2 ? NKS3 : NKS2;
-  auto gather = [&](const DLayer& tt, const float* src, int SW, int SCS, int KK, int NKS, int KD,
+  // (3) T^T gather from tile `src` (window width SW, channel stride SCS, CS channels) through the
+  // weights of `tt` (kernel KK, stride 1) into the next window (width DW, Cd channels), relaxed
+  // with the parameters pp (4 arrays, pstr apart) into `dst`; bias terms into
+  // rb[(wave * 4 + G) * 16 + n].  One K step per (source channel c, tap row ky) with the tap
+  // column as the lane group (source row uniform, steps without one skipped); the A operands sit
+  // in registers.
+  constexpr int NKSM = (C3 > C2 ? C3 : C2) * (K3 > K2 ? K3 : K2);
+  auto gather = [&](const DLayer& tt, const float* src, int SW, int SCS, int Cs, int KK,
                     float* dst, int DW, int DCS, int Cd, const float* pp, int pstr, float* rb) {
     const int m = lane & 15;  // A operand row: channel of the destination window
     float areg[NKSM];
 #pragma unroll
     for (int ks = 0; ks < NKSM; ++ks) {
-      const int k = 4 * ks + G;
-      areg[ks] = 0.f;
-      if (ks < NKS && k < KD && m < Cd) {
-        const int c = k / (KK * KK), rem = k - c * KK * KK;
-        const int ky = rem / KK, kx = rem - ky * KK;
-        areg[ks] = tt.W[(((long)c * Cd + m) * KK + ky) * KK + kx];
-      }
+      const int c = ks / KK, ky = ks % KK;
+      areg[ks] = (c < Cs && m < Cd && G < KK)
+                     ? tt.W[(((long)c * Cd + m) * KK + ky) * KK + G] : 0.f;
     }
     float bpart = 0.f;
     const int ND = DW * DW;
     for (int p = wave; p < ND; p += NW) {
       const int y = p / DW, x = p - y * DW;
+      const int ix = x - G;  // source window column feeding (y, x) through tap column G
+      const bool xok = ix >= 0 && ix < SW;
+      const float* colp = src + (xok ? ix : 0) * 16 + n;
       float4v d = {0.f, 0.f, 0.f, 0.f};
+      for (int ky = 0; ky < KK; ++ky) {
+        const int iy = y - ky;
+        if (iy < 0 || iy >= SW) continue;  // uniform
 #pragma unroll
-      for (int ks = 0; ks < NKSM; ++ks) {
-        if (ks >= NKS) break;
-        const int k = 4 * ks + G;
-        float bv = 0.f;
-        if (k < KD) {
-          const int c = k / (KK * KK), rem = k - c * KK * KK;
-          const int ky = rem / KK, kx = rem - ky * KK;
-          const int iy = y - ky, ix = x - kx;  // source window position feeding (y, x)
-          if (iy >= 0 && iy < SW && ix >= 0 && ix < SW)
-            bv = src[c * SCS + (iy * SW + ix) * 16 + n];
+        for (int c = 0; c < (C3 > C2 ? C3 : C2); ++c) {
+          if (c >= Cs) break;
+          const float bv = xok ? colp[c * SCS + iy * SW * 16] : 0.f;
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[c * KK + ky], bv, d, 0, 0, 0);
         }
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[ks], bv, d, 0, 0, 0);
       }
       if (G * 4 < Cd) {
 #pragma unroll
@@ -2230,9 +2227,9 @@ __global__ void __launch_bounds__(512)
     }
     rb[(wave * 4 + G) * 16 + n] = bpart;
   };
-  gather(t3, tile3, K4, CS3, K3, NKS3, KD3, tile2, W2W, CS2, C2, &p2s[0][0], E2, rb2);
+  gather(t3, tile3, K4, CS3, C3, K3, tile2, W2W, CS2, C2, &p2s[0][0], E2, rb2);
   __syncthreads();
-  gather(t2, tile2, W2W, CS2, K2, NKS2, KD2, tile1, W1W, CS1, C1, &p1s[0][0], E1, rb1);
+  gather(t2, tile2, W2W, CS2, C2, K2, tile1, W1W, CS1, C1, &p1s[0][0], E1, rb1);
   __syncthreads();
 
   // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
