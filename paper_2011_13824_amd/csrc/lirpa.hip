@@ -1738,15 +1738,17 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       float bpart = 0.f;
 #pragma unroll
       for (int k = 0; k < NEP; ++k) {
+        // (no early exit: the loop unrolls, so w2r is indexed statically)
         const int e = part + k * RPT;
-        if (e >= NE) break;
-        const int c1 = e / NPOS, pos = e - c1 * NPOS;
-        const float w = w2r[k];
-        const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
-        bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
-        // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
-        bpart = fmaf(v, prm[3][e], bpart);
-        tile[c1 * CS + pos * 16 + row] = v;
+        if (e < NE) {
+          const int c1 = e / NPOS, pos = e - c1 * NPOS;
+          const float w = w2r[k];
+          const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
+          bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
+          // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
+          bpart = fmaf(v, prm[3][e], bpart);
+          tile[c1 * CS + pos * 16 + row] = v;
+        }
       }
       bred[part * 16 + row] = bpart;
     }
