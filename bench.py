@@ -100,6 +100,14 @@ def stage_work(layers, S, B):
             t = layers[k - 2]
             add(f"convT_relax_fc[layer{k - 1},pass{k}]", 2.0 * Q * macs(t),
                 4.0 * (n[k] * n[k - 1] + 3 * B * n[k - 1]) + 4.0 * n[k - 2] * Q)
+            if k == 3 and layers[0]["kind"] == wl.CONV:
+                # the whole pass in one kernel (launched instead of the FC-opened stage and the
+                # bound stage for the shapes the library covers): both convolutions' flops;
+                # bytes: the rows of W_3, the relaxations of layers 2 and 1 (3 floats per
+                # neuron and sub-domain, and z1), one float per row written
+                add(f"convT_fc_bound[layer{k - 1},pass{k}]",
+                    2.0 * Q * (macs(t) + macs(layers[0])),
+                    4.0 * (n[k] * n[k - 1] + 3 * B * (n[k - 1] + n[1]) + n[1]) + 4.0 * Q)
         for m in range(mtop, 0, -1):
             t = layers[m - 1]
             kind = "fcT" if t["kind"] == wl.FC else "convT"

@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "lirpa.h"
@@ -1595,6 +1596,413 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
   for (int w = 0; w < C0; ++w) ta += red[(NS + w) * 16 + lane];
   Acc a{tb, 0.f, ta};
   sink_finish<MODE_BOUND>(s, a, q, q / R, q % R, false);
+}
+
+// A pass k that opens at the fully connected layer k (rows +-e_j over h^(k)) with two
+// convolutions T_{k-1} = T_2 and T_1 below it, in one kernel: the rows are built from W_k and
+// relaxed onto layer 2 (Eq. 4, 6), carried through T_2^T (Eq. 7), relaxed onto layer 1 and
+// carried through T_1^T, and concretised (Eq. 8).  16 rows per block; nothing but the bounds
+// reaches global memory.  Wave roles, stepping through the same barriers:
+//   matrix waves (CPW channels of g^(1) each): at step y1 they build the input tile of row
+//     y1 + 1 from W_k (as the FC source of k_convT_relax_ws), run T_2^T on row y1, park the
+//     rows over g^(1) that row completes ("stage y1"; stage H1 = the rows still open after the
+//     last input row), unrelaxed, in slot y1 & 1 of an LDS ring, and stage the layer-1
+//     relaxation of those rows beside them; every global load is theirs;
+//   x waves (one per input channel c0 of T_1): at step e + 1 they relax the rows of stage e as
+//     they read them (Eq. 6; a third of the entries also add their intercept and bias terms)
+//     and carry them through T_1^T with the rotating lane-group scheme, accumulating
+//     ||A_x||_1 per row.
+// The bound of a row is then its bias terms minus eps ||A_x||_1 (the linear term sits in the
+// layer-1 bias).
+template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
+          int S1, int P1, int HX, int WX, int C0>
+__global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_waves_per_eu(4, 8)))
+    k_convT_fc_bound(DLayer t, DLayer t1, unsigned Q, Sink s, FcSrc fc) {
+  static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0 && CI % CPW == 0,
+                "geometry");
+  static_assert(K1 <= 4 && S1 <= K1 && W1 % 4 == 0, "geometry");
+  static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
+  static_assert((H0 - 1) * S1 - P1 + K1 >= HX, "every input row of T_1 is reached");
+  constexpr int NM = CI / CPW;                   // matrix waves
+  constexpr int NTM = 64 * NM;
+  constexpr int KS = CO / 4, KS1 = CI / 4;
+  constexpr int PER = (K % S == 0) ? K / S : K;
+  constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int TILE = W1 * CO * 16;             // input tile [W1][CO][16 q]
+  constexpr int RSL = S > K - S ? S : K - S;     // rows over g^(1) per stage (max)
+  // ring: a row over g^(1) is [CI][W0][16 q] with channel stride CS1; the pads put the four
+  // lane groups of an x-wave read, and the two rows of a park, on different banks
+  constexpr int CS1 = W0 * 16 + 16;
+  constexpr int ROWF = CI * CS1 + 32;
+  constexpr int SLOT = RSL * ROWF;
+  // layer-1 relaxation of a stage, float4 (a_lo, a_up, b_up, z1) per entry:
+  // [2 sub-domains][RSL][CI][W0 (+1 pad)]
+  constexpr int PCS4 = W0 + 1;
+  constexpr int PBS4 = RSL * CI * PCS4 + 2;
+  constexpr int PSLOT4 = 2 * PBS4;
+  constexpr int NPE = 2 * RSL * CI * W0;         // entries staged per stage
+  constexpr int PL = (NPE + NTM - 1) / NTM;
+  constexpr int NTASK = CO * W1 / 4 * 8;         // FC source tasks per input row
+  constexpr int TPL = (NTASK + NTM - 1) / NTM;
+  constexpr int NSTEP = H1 + 2;
+  __shared__ float tiles[2][TILE];
+  __shared__ float ring[2][SLOT];
+  __shared__ float4v pars[2][PSLOT4];
+  __shared__ float red[NM * 16 + 2 * C0 * 16];
+
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  const unsigned R = (unsigned)s.R;
+  const unsigned b0 = q0 / R;
+  const unsigned b1 = (min(q0 + 15u, Q - 1u)) / R;  // b0 or b0 + 1
+  auto yrow = [&](int e, int r) { return e < H1 ? e * S - P + r : (H1 - 1) * S - P + S + r; };
+  auto nrows = [&](int e) { return e < H1 ? S : K - S; };
+
+  if (wave < NM) {
+    // ------------------------------------------------------------------ matrix waves
+    const int n = lane & 15, G = lane >> 4;
+    const int tid = threadIdx.x;  // < NTM
+    float wreg[PER][CPW][KS];
+    {
+      const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+      for (int ph = 0; ph < PER; ++ph) {
+        const int ky = ((slot - ph * S) % K + K) % K;
+#pragma unroll
+        for (int c = 0; c < CPW; ++c)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const int co = 4 * ks + G, ci = wave * CPW + c;
+            wreg[ph][c][ks] = (slot < K && kx < K)
+                                  ? t.W[((co * CI + ci) * K + ky) * K + kx] : 0.f;
+          }
+      }
+    }
+    auto park = [&](int e, int r, int c, const float* v) {
+      float* dst = ring[e & 1] + r * ROWF + (wave * CPW + c) * CS1 + n;
+#pragma unroll
+      for (int x = 0; x < W0; ++x) dst[x * 16] = v[x];
+    };
+    // layer-1 relaxation of stage e: loaded into registers at the start of step e, written to
+    // pars[e & 1] at its end.  Entries of rows outside the map or of a second sub-domain the
+    // block does not have are never read: they load a clamped entry instead, so that the loads
+    // carry no condition (a conditional value would make the wave wait for them at once).
+    float4v pv[PL];
+    auto pl_load = [&](int e) {
+#pragma unroll
+      for (int k = 0; k < PL; ++k) {
+        const int v = min(tid + k * NTM, NPE - 1);
+        const int x = v % W0, c = (v / W0) % CI, r = (v / (W0 * CI)) % RSL;
+        const unsigned b = min(b0 + (unsigned)(v / (W0 * CI * RSL)), b1);
+        const int y = min(max(yrow(e, r), 0), H0 - 1);
+        const unsigned i = ((unsigned)c * H0 + y) * W0 + x;
+        const unsigned pb = b * (unsigned)s.pstride + i;
+        pv[k] = float4v{s.a_lo[pb], s.a_up[pb], s.b_up[pb], s.bias[i]};
+      }
+    };
+    auto pl_store = [&](int e) {
+#pragma unroll
+      for (int k = 0; k < PL; ++k) {
+        const int v = tid + k * NTM;
+        const int x = v % W0, c = (v / W0) % CI, r = (v / (W0 * CI)) % RSL;
+        const int bsel = v / (W0 * CI * RSL);
+        if (v < NPE) pars[e & 1][bsel * PBS4 + (r * CI + c) * PCS4 + x] = pv[k];
+      }
+    };
+
+    // FC source (as in k_convT_relax_ws): task tk of an input row = (quad qd of four
+    // consecutive x1 of channel co, pair of rows q0 + 2 qp, q0 + 2 qp + 1)
+    typedef float float2v __attribute__((ext_vector_type(2)));
+    unsigned g_wa[TPL], g_wb[TPL], g_pb[TPL];
+    float g_sa[TPL], g_sb[TPL], g_bz[TPL];
+    int g_lds[TPL];
+    bool g_on[TPL];
+    float4v g_xa[TPL], g_xb[TPL], g_lo[TPL], g_up[TPL], g_bu[TPL];
+    float fbeta_a = 0.f, fbeta_b = 0.f;
+    {
+      const unsigned nin = CO * H1 * W1, nk = (unsigned)fc.nk;
+#pragma unroll
+      for (int k = 0; k < TPL; ++k) {
+        const int tk = tid + k * NTM;
+        g_on[k] = tk < NTASK;
+        const int qp = tk & 7, qd = g_on[k] ? tk >> 3 : 0;
+        const int co = qd % CO, t4 = qd / CO;
+        const unsigned qa = q0 + 2u * qp, qb = qa + 1u;
+        const unsigned ra = qa % R, rb = qb % R;
+        g_sa[k] = qa < Q ? (ra < nk ? 1.f : -1.f) : 0.f;
+        g_sb[k] = qb < Q ? (rb < nk ? 1.f : -1.f) : 0.f;
+        const unsigned i0 = (unsigned)co * H1 * W1 + 4u * t4;
+        g_wa[k] = (ra % nk) * nin + i0;
+        g_wb[k] = (rb % nk) * nin + i0;
+        // R is even, so rows 2 qp and 2 qp + 1 share their sub-domain
+        g_pb[k] = (qa < Q ? qa / R : b0) * (unsigned)s.pstride + i0;
+        g_bz[k] = t.b[co];
+        g_lds[k] = (4 * t4 * CO + co) * 16 + 2 * qp;
+      }
+    }
+    auto gen_load = [&](int yg) {
+#pragma unroll
+      for (int k = 0; k < TPL; ++k)
+        if (g_on[k]) {
+          const unsigned o = (unsigned)yg * W1;
+          g_xa[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wa[k] + o));
+          g_xb[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wb[k] + o));
+          g_lo[k] = *reinterpret_cast<const float4v*>(fc.a_lo + (g_pb[k] + o));
+          g_up[k] = *reinterpret_cast<const float4v*>(fc.a_up + (g_pb[k] + o));
+          g_bu[k] = *reinterpret_cast<const float4v*>(fc.b_up + (g_pb[k] + o));
+        }
+    };
+    auto gen_store = [&](float* buf) {
+#pragma unroll
+      for (int k = 0; k < TPL; ++k)
+        if (g_on[k]) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a = g_sa[k] * g_xa[k][e], b = g_sb[k] * g_xb[k][e];
+            const float ha = a * (a >= 0.f ? g_lo[k][e] : g_up[k][e]);
+            const float hb = b * (b >= 0.f ? g_lo[k][e] : g_up[k][e]);
+            fbeta_a = fmaf(fminf(a, 0.f), g_bu[k][e], fbeta_a);
+            fbeta_a = fmaf(ha, g_bz[k], fbeta_a);
+            fbeta_b = fmaf(fminf(b, 0.f), g_bu[k][e], fbeta_b);
+            fbeta_b = fmaf(hb, g_bz[k], fbeta_b);
+            *reinterpret_cast<float2v*>(buf + g_lds[k] + e * CO * 16) = float2v{ha, hb};
+          }
+        }
+    };
+
+    gen_load(0);
+    gen_store(tiles[0]);
+    lds_barrier();
+
+    float acc[CPW][W0];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c)
+#pragma unroll
+      for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+
+    for (int ybase = 0; ybase < H1; ybase += 2 * PER) {
+#pragma unroll
+      for (int u = 0; u < 2 * PER; ++u) {
+        const int y1 = ybase + u;
+        if (H1 % (2 * PER) != 0 && y1 >= H1) break;
+        const int ph = u % PER;
+        const float* tile = tiles[u & 1];
+        pl_load(y1);
+        if (y1 + 1 < H1) gen_load(y1 + 1);
+#pragma unroll
+        for (int x1 = 0; x1 < W1; ++x1) {
+          float bv[KS];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) bv[ks] = tile[(x1 * CO + 4 * ks + G) * 16 + n];
+#pragma unroll
+          for (int c = 0; c < CPW; ++c) {
+            float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+              d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][c][ks], bv[ks], d, 0, 0, 0);
+#pragma unroll
+            for (int kx = 0; kx < K; ++kx) {
+              const int col = x1 * S - P + kx;
+              if (col >= 0 && col < W0) acc[c][col] += d[kx];
+            }
+          }
+        }
+        const int ky = ((G - ph * S) % K + K) % K;
+        if (G < K && ky < S) {
+#pragma unroll
+          for (int c = 0; c < CPW; ++c) {
+            park(y1, ky, c, acc[c]);
+#pragma unroll
+            for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
+          }
+        }
+        if (y1 + 1 < H1) gen_store(tiles[(u + 1) & 1]);
+        pl_store(y1);
+        lds_barrier();
+      }
+    }
+    {  // step H1: the rows still open, and their relaxation
+      pl_load(H1);
+      constexpr int ph_last = (H1 - 1) % PER;
+      const int ky = ((G - ph_last * S) % K + K) % K;
+      if (G < K && ky >= S) {
+#pragma unroll
+        for (int c = 0; c < CPW; ++c) park(H1, ky - S, c, acc[c]);
+      }
+      pl_store(H1);
+      lds_barrier();
+    }
+    lds_barrier();  // step H1 + 1
+    // rows 2 qp, 2 qp + 1 of every task of this wave: lanes qp, qp + 8, ..., qp + 56
+#pragma unroll
+    for (int o = 8; o < 64; o <<= 1) {
+      fbeta_a += __shfl_xor(fbeta_a, o, 64);
+      fbeta_b += __shfl_xor(fbeta_b, o, 64);
+    }
+    if (lane < 8) {
+      red[wave * 16 + 2 * lane] = fbeta_a;
+      red[wave * 16 + 2 * lane + 1] = fbeta_b;
+    }
+    lds_barrier();  // final reduction
+    return;
+  }
+
+  // ---------------------------------------------------------------------- x waves
+  static_assert(C0 >= 1 && C0 <= 3, "input channels of T_1");
+  const int xw = wave - NM;  // input channel c0 of T_1
+  const int n = lane & 15, G = lane >> 4;
+  const unsigned q = q0 + n;
+  const int bsel = q < Q ? (int)(q / R - b0) : 0;
+  // the x waves carry the longer chain of each step: they go first when both roles can issue
+  __builtin_amdgcn_s_setprio(2);
+  // The wave of channel xw also adds the intercept and bias terms of the entries at the
+  // columns x1 = xw mod C0; xw is made a constant so that this choice is no branch.
+  auto xrun = [&](auto xb) {
+  constexpr int XB = decltype(xb)::value;
+  float wreg1[PER1][KS1];
+  {
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER1; ++ph) {
+      const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks) {
+        const int c1 = 4 * ks + G;
+        wreg1[ph][ks] = (slot < K1 && kx < K1) ? t1.W[((c1 * C0 + XB) * K1 + ky) * K1 + kx]
+                                               : 0.f;
+      }
+    }
+  }
+  float acc1[WX];
+#pragma unroll
+  for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+  float l1 = 0.f, beta = 0.f;
+  auto emit = [&](int yx) {  // output row yx of channel xw: ||.||_1 over the image
+    if (yx < 0 || yx >= HX) return;
+#pragma unroll
+    for (int x = 0; x < WX; ++x) l1 += fabsf(acc1[x]);
+  };
+  // relaxation and T_1^T of row y over g^(1): coefficients in `row`, relaxation in `prm`
+  // ([CI][W0] float4 with channel stride PCS4, at this lane's sub-domain)
+  auto consume = [&](const float* row, const float4v* prm, int y) {
+    const int ph = y % PER1;
+    float wa[KS1];
+#pragma unroll
+    for (int ks = 0; ks < KS1; ++ks) {
+      wa[ks] = wreg1[0][ks];
+#pragma unroll
+      for (int p2 = 1; p2 < PER1; ++p2)
+        if (ph == p2) wa[ks] = wreg1[p2][ks];
+    }
+    // Three columns in flight: the LDS reads of column x1 + 2 (into buffer (x1 + 2) & 1), the
+    // MFMAs of x1 and the relaxation of x1 + 1, whose reads were issued a column earlier.  The
+    // scheduling barriers keep this order (and the compiler from reading further ahead); the
+    // sums of column x1 are added one column later.  The columns whose bias terms another
+    // wave adds read only a_lo and a_up.
+    typedef float float2v __attribute__((ext_vector_type(2)));
+    float an[2][KS1], hn[KS1];
+    float4v pn[2][KS1];
+    auto fetch = [&](int x1) {
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks) {
+        const int c1 = 4 * ks + G;
+        an[x1 & 1][ks] = row[c1 * CS1 + x1 * 16 + n];
+        if (x1 % C0 == XB) {
+          pn[x1 & 1][ks] = prm[c1 * PCS4 + x1];
+        } else {
+          const float2v h = *reinterpret_cast<const float2v*>(prm + c1 * PCS4 + x1);
+          pn[x1 & 1][ks] = float4v{h[0], h[1], 0.f, 0.f};
+        }
+      }
+    };
+    auto relax = [&](int x1) {
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks) {
+        const float a = an[x1 & 1][ks];
+        const float4v p = pn[x1 & 1][ks];
+        const float ah = a * (a >= 0.f ? p[0] : p[1]);
+        if (x1 % C0 == XB) {
+          beta = fmaf(fminf(a, 0.f), p[2], beta);
+          beta = fmaf(ah, p[3], beta);
+        }
+        hn[ks] = ah;
+      }
+    };
+    auto add = [&](int x1, const float4v& d) {
+#pragma unroll
+      for (int kx = 0; kx < K1; ++kx) {
+        const int col = x1 * S1 - P1 + kx;
+        if (col >= 0 && col < WX) acc1[col] += d[kx];
+      }
+    };
+    fetch(0);
+    fetch(1);
+    relax(0);
+    float4v dp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int x1 = 0; x1 < W0; ++x1) {
+      if (x1 + 2 < W0) fetch(x1 + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS1; ++ks)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], hn[ks], d, 0, 0, 0);
+      if (x1 > 0) add(x1 - 1, dp);
+      if (x1 + 1 < W0) relax(x1 + 1);
+      dp = d;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    add(W0 - 1, dp);
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    if (G < K1 && ky < S1) {
+      emit(y * S1 - P1 + ky);
+#pragma unroll
+      for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+    }
+  };
+  lds_barrier();  // first input tile
+  for (int st = 0; st < NSTEP; ++st) {
+    if (st >= 1) {
+      const int e = st - 1;
+      const float* slot = ring[e & 1];
+      const int nr = nrows(e);
+      for (int r = 0; r < nr; ++r) {
+        const int y = yrow(e, r);
+        if (y >= 0 && y < H0)
+          consume(slot + r * ROWF, pars[e & 1] + bsel * PBS4 + r * CI * PCS4, y);
+      }
+    }
+    lds_barrier();
+  }
+  {  // output rows still open after the last row of g^(1)
+    const int ph = (H0 - 1) % PER1;
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    if (G < K1 && ky >= S1) emit((H0 - 1) * S1 - P1 + ky);
+  }
+  l1 += __shfl_xor(l1, 16, 64);
+  l1 += __shfl_xor(l1, 32, 64);
+  beta += __shfl_xor(beta, 16, 64);
+  beta += __shfl_xor(beta, 32, 64);
+  if (lane < 16) {
+    red[NM * 16 + XB * 16 + lane] = beta;
+    red[NM * 16 + (C0 + XB) * 16 + lane] = l1;
+  }
+  };
+  if (xw == 0) xrun(std::integral_constant<int, 0>());
+  if (C0 > 1 && xw == 1) xrun(std::integral_constant<int, (C0 > 1 ? 1 : 0)>());
+  if (C0 > 2 && xw == 2) xrun(std::integral_constant<int, (C0 > 2 ? 2 : 0)>());
+  lds_barrier();
+  if (xw != 0 || lane >= 16 || q >= Q) return;
+  // the row's own bias +-b_k[j], the terms of the relaxations onto layers 2 and 1
+  const unsigned r = q % R, nk = (unsigned)fc.nk;
+  float tb = r < nk ? fc.b[r] : -fc.b[r - nk];
+  for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
+  for (int w = 0; w < C0; ++w) tb += red[NM * 16 + w * 16 + lane];
+  float ta = 0.f;
+  for (int w = 0; w < C0; ++w) ta += red[NM * 16 + (C0 + w) * 16 + lane];
+  Acc a{tb, 0.f, ta};
+  sink_finish<MODE_BOUND>(s, a, q, q / R, r, true);
 }
 
 // The 16 rows +-e_j of a receptive-field pass-2 block share the window (y2, x2) of one
@@ -3820,6 +4228,55 @@ int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
   });
 }
 
+// Pass 3 of a net whose layers 1 and 2 are convolutions of a covered geometry and whose layer 3
+// is fully connected, bounded without a gradient tape: one kernel from the rows of W_3 to the
+// bounds.  Null otherwise.
+using FcBoundKernel = void (*)(DLayer, DLayer, unsigned, Sink, FcSrc);
+FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves) {
+  if (k != 3 || net->L < 4) return nullptr;
+  const lirpa_layer &fl = net->T[2], &t2 = net->T[1], &t1 = net->T[0];
+  if (fl.kind != LIRPA_LINEAR || t2.kind != LIRPA_CONV2D || t1.kind != LIRPA_CONV2D)
+    return nullptr;
+  const bool t1_ok = t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.in_c == 3 &&
+                     t1.in_h == 32 && t1.in_w == 32 && t1.out_h == 16 && t1.out_w == 16;
+  const bool t2_ok = t2.k == 4 && t2.stride == 2 && t2.pad == 1 && t2.in_h == 16 &&
+                     t2.in_w == 16 && t2.out_h == 8 && t2.out_w == 8;
+  if (!t1_ok || !t2_ok) return nullptr;
+  if (t1.out_c == 8 && t2.in_c == 8 && t2.out_c == 16) {
+    *nwaves = 8 / 2 + 3;
+    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3>;
+  }
+  return nullptr;
+}
+
+// Returns 1 when the pass does not qualify (the caller runs the stages one by one).
+int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
+  const lirpa_net* net = c.net;
+  int nw = 0;
+  FcBoundKernel kern = fc_bound_for(net, k, &nw);
+  if (!kern || c.tape || !fc_open_ok(c, k, R)) return 1;
+  const lirpa_layer& fl = net->T[k - 1];
+  Sink s = slab_sink(c, 1, nullptr, 0, R);  // the relaxation of layer 1 (bias: z1)
+  const Sink sb = bound_sink(c, R, c.L + net->off[k], c.U + net->off[k], net->n_relu, net->n[k]);
+  s.eps = sb.eps;
+  s.x0 = sb.x0;
+  s.lo = sb.lo;
+  s.hi = sb.hi;
+  s.bstride = sb.bstride;
+  s.n_half = sb.n_half;
+  FcSrc f{fl.W,
+          fl.b,
+          (int)net->n[k],
+          at<float>(c.ws, c.p->off_alo) + net->poff[k - 1],
+          at<float>(c.ws, c.p->off_aup) + net->poff[k - 1],
+          at<float>(c.ws, c.p->off_bup) + net->poff[k - 1]};
+  const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+  return launch_k(tag("convT_fc_bound", k - 1, k), c.st, [&] {
+    hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[k - 2]),
+                       dlayer(net->T[0]), (unsigned)Q, s, f);
+  });
+}
+
 // Kernel for the receptive-field pass 4 (T_4 over the stride-1 T_3, T_2 over T_1; the Deep
 // shape), or null.
 using Pass4Kernel = void (*)(DLayer, DLayer, DLayer, DLayer, const float*, const float*,
@@ -3884,6 +4341,14 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     }
     if (k == 3 && !c.tape) {
       int e = pass3_window(c);
+      if (e != 1) {
+        if (e) return e;
+        if (int e2 = relax_layer(c, k)) return e2;
+        continue;
+      }
+    }
+    if (!c.tape) {
+      int e = fc_bound_stage(c, k, R, Q);
       if (e != 1) {
         if (e) return e;
         if (int e2 = relax_layer(c, k)) return e2;
