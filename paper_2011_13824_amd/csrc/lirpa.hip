@@ -1608,15 +1608,18 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 //     rows over g^(1) that row completes ("stage y1"; stage H1 = the rows still open after the
 //     last input row), unrelaxed, in slot y1 & 1 of an LDS ring, and stage the layer-1
 //     relaxation of those rows beside them; every global load is theirs;
-//   x waves (one per input channel c0 of T_1): at step e + 1 they relax the rows of stage e as
-//     they read them (Eq. 6; a third of the entries also add their intercept and bias terms)
-//     and carry them through T_1^T with the rotating lane-group scheme, accumulating
-//     ||A_x||_1 per row.
+//   x waves (NXW of them, each owning a range of output columns of T_1^T over every input
+//     channel): at step e + 1 they relax the rows of stage e as they read them (Eq. 6, each
+//     entry once per wave that reads it, its intercept and bias terms added by one of them)
+//     and carry them through T_1^T with the rotating lane-group scheme, one MFMA chain per
+//     input channel of T_1 on the same relaxed operand, accumulating ||A_x||_1 per row.
+//     Neighbouring column ranges share one input column (their borders are placed so), and
+//     with NXW = NM each SIMD holds one wave of either role.
 // The bound of a row is then its bias terms minus eps ||A_x||_1 (the linear term sits in the
 // layer-1 bias).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
-          int S1, int P1, int HX, int WX, int C0>
-__global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_waves_per_eu(4, 8)))
+          int S1, int P1, int HX, int WX, int C0, int NXW>
+__global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_waves_per_eu(4, 8)))
     k_convT_fc_bound(DLayer t, DLayer t1, unsigned Q, Sink s, FcSrc fc) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0 && CI % CPW == 0,
                 "geometry");
@@ -1648,7 +1651,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_wa
   __shared__ float tiles[2][TILE];
   __shared__ float ring[2][SLOT];
   __shared__ float4v pars[2][PSLOT4];
-  __shared__ float red[NM * 16 + 2 * C0 * 16];
+  __shared__ float red[NM * 16 + 2 * NXW * 16];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
@@ -1849,57 +1852,88 @@ __global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_wa
   }
 
   // ---------------------------------------------------------------------- x waves
-  static_assert(C0 >= 1 && C0 <= 3, "input channels of T_1");
-  const int xw = wave - NM;  // input channel c0 of T_1
+  static_assert(NXW >= 1 && NXW <= 4, "x waves");
+  const int xw = wave - NM;
   const int n = lane & 15, G = lane >> 4;
   const unsigned q = q0 + n;
   const int bsel = q < Q ? (int)(q / R - b0) : 0;
   // the x waves carry the longer chain of each step: they go first when both roles can issue
   __builtin_amdgcn_s_setprio(2);
-  // The wave of channel xw also adds the intercept and bias terms of the entries at the
-  // columns x1 = xw mod C0; xw is made a constant so that this choice is no branch.
+  // Output columns [ob(j), ob(j + 1)) of T_1^T belong to x wave j.  An inner border b with
+  // (b + P1) % S1 == 0 leaves K1 / S1 - 1 input columns to both neighbours.
+  constexpr auto ob = [](int j) {
+    if (j <= 0) return 0;
+    if (j >= NXW) return WX;
+    int b = j * WX / NXW;
+    while ((b + P1) % S1 != 0) --b;
+    return b;
+  };
+  constexpr auto cdiv = [](int a, int b) { return a >= 0 ? (a + b - 1) / b : -((-a) / b); };
+  constexpr auto fdiv = [](int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); };
+  // input columns of wave j: [xlo(j), xhi(j)]; the intercept and bias terms of column x1 are
+  // added by the first wave that reads it
+  constexpr auto xlo = [=](int j) {
+    const int v = cdiv(ob(j) + P1 - K1 + 1, S1);
+    return v < 0 ? 0 : v;
+  };
+  constexpr auto xhi = [=](int j) {
+    const int v = fdiv(ob(j + 1) - 1 + P1, S1);
+    return v > W0 - 1 ? W0 - 1 : v;
+  };
+  // xw is made a constant so that the column ranges are compile-time
   auto xrun = [&](auto xb) {
   constexpr int XB = decltype(xb)::value;
-  float wreg1[PER1][KS1];
+  constexpr int OL = ob(XB), OW = ob(XB + 1) - ob(XB);
+  constexpr int XL = xlo(XB), XH = xhi(XB);
+  constexpr int XC = XB + 1 < NXW ? xlo(XB + 1) : XH + 1;  // bias terms: columns [XL, XC)
+  float wreg1[PER1][C0][KS1];
   {
     const int M = lane & 15, slot = M >> 2, kx = M & 3;
 #pragma unroll
     for (int ph = 0; ph < PER1; ++ph) {
       const int ky = ((slot - ph * S1) % K1 + K1) % K1;
 #pragma unroll
-      for (int ks = 0; ks < KS1; ++ks) {
-        const int c1 = 4 * ks + G;
-        wreg1[ph][ks] = (slot < K1 && kx < K1) ? t1.W[((c1 * C0 + XB) * K1 + ky) * K1 + kx]
-                                               : 0.f;
-      }
+      for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+        for (int ks = 0; ks < KS1; ++ks) {
+          const int c1 = 4 * ks + G;
+          wreg1[ph][c0][ks] = (slot < K1 && kx < K1)
+                                  ? t1.W[((c1 * C0 + c0) * K1 + ky) * K1 + kx] : 0.f;
+        }
     }
   }
-  float acc1[WX];
+  float acc1[C0][OW];
 #pragma unroll
-  for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+  for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+    for (int x = 0; x < OW; ++x) acc1[c0][x] = 0.f;
   float l1 = 0.f, beta = 0.f;
-  auto emit = [&](int yx) {  // output row yx of channel xw: ||.||_1 over the image
+  auto emit = [&](int yx) {  // output row yx over this wave's columns: ||.||_1
     if (yx < 0 || yx >= HX) return;
 #pragma unroll
-    for (int x = 0; x < WX; ++x) l1 += fabsf(acc1[x]);
+    for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+      for (int x = 0; x < OW; ++x) l1 += fabsf(acc1[c0][x]);
   };
   // relaxation and T_1^T of row y over g^(1): coefficients in `row`, relaxation in `prm`
   // ([CI][W0] float4 with channel stride PCS4, at this lane's sub-domain)
   auto consume = [&](const float* row, const float4v* prm, int y) {
     const int ph = y % PER1;
-    float wa[KS1];
+    float wa[C0][KS1];
 #pragma unroll
-    for (int ks = 0; ks < KS1; ++ks) {
-      wa[ks] = wreg1[0][ks];
+    for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
-      for (int p2 = 1; p2 < PER1; ++p2)
-        if (ph == p2) wa[ks] = wreg1[p2][ks];
-    }
-    // Three columns in flight: the LDS reads of column x1 + 2 (into buffer (x1 + 2) & 1), the
-    // MFMAs of x1 and the relaxation of x1 + 1, whose reads were issued a column earlier.  The
+      for (int ks = 0; ks < KS1; ++ks) {
+        wa[c0][ks] = wreg1[0][c0][ks];
+#pragma unroll
+        for (int p2 = 1; p2 < PER1; ++p2)
+          if (ph == p2) wa[c0][ks] = wreg1[p2][c0][ks];
+      }
+    // Three columns in flight: the LDS reads of column x1 + 2 (into buffer x1 & 1), the MFMAs
+    // of x1 and the relaxation of x1 + 1, whose reads were issued a column earlier.  The
     // scheduling barriers keep this order (and the compiler from reading further ahead); the
-    // sums of column x1 are added one column later.  The columns whose bias terms another
-    // wave adds read only a_lo and a_up.
+    // sums of column x1 are added one column later.  Columns whose bias terms another wave
+    // adds read only a_lo and a_up.
     typedef float float2v __attribute__((ext_vector_type(2)));
     float an[2][KS1], hn[KS1];
     float4v pn[2][KS1];
@@ -1908,7 +1942,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_wa
       for (int ks = 0; ks < KS1; ++ks) {
         const int c1 = 4 * ks + G;
         an[x1 & 1][ks] = row[c1 * CS1 + x1 * 16 + n];
-        if (x1 % C0 == XB) {
+        if (x1 < XC) {
           pn[x1 & 1][ks] = prm[c1 * PCS4 + x1];
         } else {
           const float2v h = *reinterpret_cast<const float2v*>(prm + c1 * PCS4 + x1);
@@ -1922,43 +1956,52 @@ __global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_wa
         const float a = an[x1 & 1][ks];
         const float4v p = pn[x1 & 1][ks];
         const float ah = a * (a >= 0.f ? p[0] : p[1]);
-        if (x1 % C0 == XB) {
+        if (x1 < XC) {
           beta = fmaf(fminf(a, 0.f), p[2], beta);
           beta = fmaf(ah, p[3], beta);
         }
         hn[ks] = ah;
       }
     };
-    auto add = [&](int x1, const float4v& d) {
+    auto add = [&](int x1, const float4v* d) {
 #pragma unroll
-      for (int kx = 0; kx < K1; ++kx) {
-        const int col = x1 * S1 - P1 + kx;
-        if (col >= 0 && col < WX) acc1[col] += d[kx];
-      }
+      for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+        for (int kx = 0; kx < K1; ++kx) {
+          const int col = x1 * S1 - P1 + kx - OL;
+          if (col >= 0 && col < OW) acc1[c0][col] += d[c0][kx];
+        }
     };
-    fetch(0);
-    fetch(1);
-    relax(0);
-    float4v dp = {0.f, 0.f, 0.f, 0.f};
+    fetch(XL);
+    if (XL + 1 <= XH) fetch(XL + 1);
+    relax(XL);
+    float4v dp[C0];
 #pragma unroll
-    for (int x1 = 0; x1 < W0; ++x1) {
-      if (x1 + 2 < W0) fetch(x1 + 2);
+    for (int x1 = XL; x1 <= XH; ++x1) {
+      if (x1 + 2 <= XH) fetch(x1 + 2);
       __builtin_amdgcn_sched_barrier(0);
-      float4v d = {0.f, 0.f, 0.f, 0.f};
+      float4v d[C0];
+#pragma unroll
+      for (int c0 = 0; c0 < C0; ++c0) d[c0] = float4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS1; ++ks)
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[ks], hn[ks], d, 0, 0, 0);
-      if (x1 > 0) add(x1 - 1, dp);
-      if (x1 + 1 < W0) relax(x1 + 1);
-      dp = d;
+#pragma unroll
+        for (int c0 = 0; c0 < C0; ++c0)
+          d[c0] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[c0][ks], hn[ks], d[c0], 0, 0, 0);
+      if (x1 > XL) add(x1 - 1, dp);
+      if (x1 + 1 <= XH) relax(x1 + 1);
+#pragma unroll
+      for (int c0 = 0; c0 < C0; ++c0) dp[c0] = d[c0];
       __builtin_amdgcn_sched_barrier(0);
     }
-    add(W0 - 1, dp);
+    add(XH, dp);
     const int ky = ((G - ph * S1) % K1 + K1) % K1;
     if (G < K1 && ky < S1) {
       emit(y * S1 - P1 + ky);
 #pragma unroll
-      for (int x = 0; x < WX; ++x) acc1[x] = 0.f;
+      for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+        for (int x = 0; x < OW; ++x) acc1[c0][x] = 0.f;
     }
   };
   lds_barrier();  // first input tile
@@ -1986,21 +2029,22 @@ __global__ void __launch_bounds__(64 * (CI / CPW + C0)) __attribute__((amdgpu_wa
   beta += __shfl_xor(beta, 32, 64);
   if (lane < 16) {
     red[NM * 16 + XB * 16 + lane] = beta;
-    red[NM * 16 + (C0 + XB) * 16 + lane] = l1;
+    red[NM * 16 + (NXW + XB) * 16 + lane] = l1;
   }
   };
   if (xw == 0) xrun(std::integral_constant<int, 0>());
-  if (C0 > 1 && xw == 1) xrun(std::integral_constant<int, (C0 > 1 ? 1 : 0)>());
-  if (C0 > 2 && xw == 2) xrun(std::integral_constant<int, (C0 > 2 ? 2 : 0)>());
+  if (NXW > 1 && xw == 1) xrun(std::integral_constant<int, (NXW > 1 ? 1 : 0)>());
+  if (NXW > 2 && xw == 2) xrun(std::integral_constant<int, (NXW > 2 ? 2 : 0)>());
+  if (NXW > 3 && xw == 3) xrun(std::integral_constant<int, (NXW > 3 ? 3 : 0)>());
   lds_barrier();
   if (xw != 0 || lane >= 16 || q >= Q) return;
   // the row's own bias +-b_k[j], the terms of the relaxations onto layers 2 and 1
   const unsigned r = q % R, nk = (unsigned)fc.nk;
   float tb = r < nk ? fc.b[r] : -fc.b[r - nk];
   for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
-  for (int w = 0; w < C0; ++w) tb += red[NM * 16 + w * 16 + lane];
+  for (int w = 0; w < NXW; ++w) tb += red[NM * 16 + w * 16 + lane];
   float ta = 0.f;
-  for (int w = 0; w < C0; ++w) ta += red[NM * 16 + (C0 + w) * 16 + lane];
+  for (int w = 0; w < NXW; ++w) ta += red[NM * 16 + (NXW + w) * 16 + lane];
   Acc a{tb, 0.f, ta};
   sink_finish<MODE_BOUND>(s, a, q, q / R, r, true);
 }
@@ -4243,8 +4287,8 @@ FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves) {
                      t2.in_w == 16 && t2.out_h == 8 && t2.out_w == 8;
   if (!t1_ok || !t2_ok) return nullptr;
   if (t1.out_c == 8 && t2.in_c == 8 && t2.out_c == 16) {
-    *nwaves = 8 / 2 + 3;
-    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3>;
+    *nwaves = 8 / 2 + 4;
+    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4>;
   }
   return nullptr;
 }
