@@ -120,6 +120,12 @@ def stage_work(layers, S, B):
             # float per row written
             add(f"convT2_bound[layer2,pass{k}]", 2.0 * Q * (macs(layers[1]) + macs(layers[0])),
                 4.0 * n[2] * Q + 4.0 * Q)
+            # the same pair in the kernel that also runs pass 3 from W_3 (slab source): the same
+            # flops; bytes as above plus the layer-1 relaxation (3 floats per neuron and
+            # sub-domain, and z1)
+            add(f"convT_slab_bound[layer2,pass{k}]",
+                2.0 * Q * (macs(layers[1]) + macs(layers[0])),
+                4.0 * n[2] * Q + 4.0 * Q + 4.0 * (3 * B * n[1] + n[1]))
     return work
 
 

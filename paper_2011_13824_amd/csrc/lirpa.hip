@@ -1598,13 +1598,17 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
   sink_finish<MODE_BOUND>(s, a, q, q / R, q % R, false);
 }
 
-// A pass k that opens at the fully connected layer k (rows +-e_j over h^(k)) with two
-// convolutions T_{k-1} = T_2 and T_1 below it, in one kernel: the rows are built from W_k and
-// relaxed onto layer 2 (Eq. 4, 6), carried through T_2^T (Eq. 7), relaxed onto layer 1 and
-// carried through T_1^T, and concretised (Eq. 8).  16 rows per block; nothing but the bounds
-// reaches global memory.  Wave roles, stepping through the same barriers:
-//   matrix waves (CPW channels of g^(1) each): at step y1 they build the input tile of row
-//     y1 + 1 from W_k (as the FC source of k_convT_relax_ws), run T_2^T on row y1, park the
+// The last two backward stages of a pass, T_2^T (Eq. 7) with the relaxation of layer 1 and
+// T_1^T with the concretisation (Eq. 8), in one kernel, 16 rows per block, for two sources of
+// the rows over g^(2):
+//   FC: pass k opens at the fully connected layer k = 3 (rows +-e_j over h^(3)); the rows are
+//     built from W_3 and relaxed onto layer 2 (Eq. 4, 6) as in k_convT_relax_ws, so nothing
+//     but the bounds reaches global memory;
+//   slab: the rows, already relaxed onto layer 2, are read from a slab [n_2][ldq] (the final
+//     pass), and their running bias from Sink::beta.
+// A block's rows span at most NBS sub-domains.  Wave roles, stepping through the same barriers:
+//   matrix waves (CPW channels of g^(1) each): at step y1 they build (FC) or load (slab) the
+//     input tile of row y1 + 1, run T_2^T on row y1, park the
 //     rows over g^(1) that row completes ("stage y1"; stage H1 = the rows still open after the
 //     last input row), unrelaxed, in slot y1 & 1 of an LDS ring, and stage the layer-1
 //     relaxation of those rows beside them; every global load is theirs;
@@ -1618,9 +1622,10 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 // The bound of a row is then its bias terms minus eps ||A_x||_1 (the linear term sits in the
 // layer-1 bias).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
-          int S1, int P1, int HX, int WX, int C0, int NXW>
+          int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS>
 __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_waves_per_eu(4, 8)))
-    k_convT_fc_bound(DLayer t, DLayer t1, unsigned Q, Sink s, FcSrc fc) {
+    k_convT_fc_bound(DLayer t, DLayer t1, const float* __restrict__ in, unsigned ldq, unsigned Q,
+                     Sink s, FcSrc fc) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0 && CI % CPW == 0,
                 "geometry");
   static_assert(K1 <= 4 && S1 <= K1 && W1 % 4 == 0, "geometry");
@@ -1639,14 +1644,17 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
   constexpr int ROWF = CI * CS1 + 32;
   constexpr int SLOT = RSL * ROWF;
   // layer-1 relaxation of a stage, float4 (a_lo, a_up, b_up, z1) per entry:
-  // [2 sub-domains][RSL][CI][W0 (+1 pad)]
+  // [NBS sub-domains][RSL][CI][W0 (+1 pad)]
+  static_assert(NBS == 2 || NBS == 3, "sub-domains per block");
   constexpr int PCS4 = W0 + 1;
   constexpr int PBS4 = RSL * CI * PCS4 + 2;
-  constexpr int PSLOT4 = 2 * PBS4;
-  constexpr int NPE = 2 * RSL * CI * W0;         // entries staged per stage
+  constexpr int PSLOT4 = NBS * PBS4;
+  constexpr int NPE = NBS * RSL * CI * W0;       // entries staged per stage
   constexpr int PL = (NPE + NTM - 1) / NTM;
   constexpr int NTASK = CO * W1 / 4 * 8;         // FC source tasks per input row
-  constexpr int TPL = (NTASK + NTM - 1) / NTM;
+  constexpr int TPL = FC ? (NTASK + NTM - 1) / NTM : 1;
+  constexpr int NV4 = CO * W1 * 4;               // slab source: float4 per input tile
+  constexpr int PF = FC ? 1 : (NV4 + NTM - 1) / NTM;
   constexpr int NSTEP = H1 + 2;
   __shared__ float tiles[2][TILE];
   __shared__ float ring[2][SLOT];
@@ -1658,7 +1666,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
   if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned R = (unsigned)s.R;
   const unsigned b0 = q0 / R;
-  const unsigned b1 = (min(q0 + 15u, Q - 1u)) / R;  // b0 or b0 + 1
+  const unsigned b1 = (min(q0 + 15u, Q - 1u)) / R;  // b1 - b0 < NBS
   auto yrow = [&](int e, int r) { return e < H1 ? e * S - P + r : (H1 - 1) * S - P + S + r; };
   auto nrows = [&](int e) { return e < H1 ? S : K - S; };
 
@@ -1723,7 +1731,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
     bool g_on[TPL];
     float4v g_xa[TPL], g_xb[TPL], g_lo[TPL], g_up[TPL], g_bu[TPL];
     float fbeta_a = 0.f, fbeta_b = 0.f;
-    {
+    if constexpr (FC) {
       const unsigned nin = CO * H1 * W1, nk = (unsigned)fc.nk;
 #pragma unroll
       for (int k = 0; k < TPL; ++k) {
@@ -1774,8 +1782,35 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
         }
     };
 
-    gen_load(0);
-    gen_store(tiles[0]);
+    // slab source: float4 v of input row y1 (channel co, column x1, four rows q) to registers,
+    // then to the tile
+    float4v sv[PF];
+    auto slab_load = [&](int y1) {
+#pragma unroll
+      for (int k = 0; k < PF; ++k) {
+        const int v4 = min(tid + k * NTM, NV4 - 1);
+        const int cx = v4 >> 2, j4 = v4 & 3;
+        const int x1 = cx / CO, co = cx - x1 * CO;
+        sv[k] = *reinterpret_cast<const float4v*>(
+            in + (size_t)((unsigned)(co * H1 + y1) * W1 + x1) * ldq + q0 + j4 * 4);
+      }
+    };
+    auto slab_store = [&](float* buf) {
+#pragma unroll
+      for (int k = 0; k < PF; ++k) {
+        const int v4 = tid + k * NTM;
+        if (v4 < NV4) *reinterpret_cast<float4v*>(buf + 4 * v4) = sv[k];
+      }
+    };
+    auto src_load = [&](int y1) {
+      if constexpr (FC) gen_load(y1); else slab_load(y1);
+    };
+    auto src_store = [&](float* buf) {
+      if constexpr (FC) gen_store(buf); else slab_store(buf);
+    };
+
+    src_load(0);
+    src_store(tiles[0]);
     lds_barrier();
 
     float acc[CPW][W0];
@@ -1792,7 +1827,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
         const int ph = u % PER;
         const float* tile = tiles[u & 1];
         pl_load(y1);
-        if (y1 + 1 < H1) gen_load(y1 + 1);
+        if (y1 + 1 < H1) src_load(y1 + 1);
 #pragma unroll
         for (int x1 = 0; x1 < W1; ++x1) {
           float bv[KS];
@@ -1820,7 +1855,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
             for (int x = 0; x < W0; ++x) acc[c][x] = 0.f;
           }
         }
-        if (y1 + 1 < H1) gen_store(tiles[(u + 1) & 1]);
+        if (y1 + 1 < H1) src_store(tiles[(u + 1) & 1]);
         pl_store(y1);
         lds_barrier();
       }
@@ -1837,15 +1872,17 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
       lds_barrier();
     }
     lds_barrier();  // step H1 + 1
-    // rows 2 qp, 2 qp + 1 of every task of this wave: lanes qp, qp + 8, ..., qp + 56
+    if constexpr (FC) {
+      // rows 2 qp, 2 qp + 1 of every task of this wave: lanes qp, qp + 8, ..., qp + 56
 #pragma unroll
-    for (int o = 8; o < 64; o <<= 1) {
-      fbeta_a += __shfl_xor(fbeta_a, o, 64);
-      fbeta_b += __shfl_xor(fbeta_b, o, 64);
-    }
-    if (lane < 8) {
-      red[wave * 16 + 2 * lane] = fbeta_a;
-      red[wave * 16 + 2 * lane + 1] = fbeta_b;
+      for (int o = 8; o < 64; o <<= 1) {
+        fbeta_a += __shfl_xor(fbeta_a, o, 64);
+        fbeta_b += __shfl_xor(fbeta_b, o, 64);
+      }
+      if (lane < 8) {
+        red[wave * 16 + 2 * lane] = fbeta_a;
+        red[wave * 16 + 2 * lane + 1] = fbeta_b;
+      }
     }
     lds_barrier();  // final reduction
     return;
@@ -2038,15 +2075,20 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
   if (NXW > 3 && xw == 3) xrun(std::integral_constant<int, (NXW > 3 ? 3 : 0)>());
   lds_barrier();
   if (xw != 0 || lane >= 16 || q >= Q) return;
-  // the row's own bias +-b_k[j], the terms of the relaxations onto layers 2 and 1
-  const unsigned r = q % R, nk = (unsigned)fc.nk;
-  float tb = r < nk ? fc.b[r] : -fc.b[r - nk];
-  for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
+  // FC: the row's own bias +-b_k[j] and the terms of the relaxation onto layer 2 (slab: the
+  // running bias, added by sink_finish); the terms of the relaxation onto layer 1
+  const unsigned r = q % R;
+  float tb = 0.f;
+  if constexpr (FC) {
+    const unsigned nk = (unsigned)fc.nk;
+    tb = r < nk ? fc.b[r] : -fc.b[r - nk];
+    for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
+  }
   for (int w = 0; w < NXW; ++w) tb += red[NM * 16 + w * 16 + lane];
   float ta = 0.f;
   for (int w = 0; w < NXW; ++w) ta += red[NM * 16 + (NXW + w) * 16 + lane];
   Acc a{tb, 0.f, ta};
-  sink_finish<MODE_BOUND>(s, a, q, q / R, r, true);
+  sink_finish<MODE_BOUND>(s, a, q, q / R, r, FC);
 }
 
 // The 16 rows +-e_j of a receptive-field pass-2 block share the window (y2, x2) of one
@@ -4071,6 +4113,29 @@ float* tape_of(const Chunk& c, int pass, int m) {
   return c.tape ? at<float>(c.ws, c.p->off_tape[pass][m]) : nullptr;
 }
 
+// k_convT_fc_bound for layers 1 and 2 of the net when they are convolutions of a covered
+// geometry (fc: rows built from W_3; otherwise read from a slab, with nbs sub-domains per block
+// at most); null otherwise.
+using FcBoundKernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink, FcSrc);
+FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwaves) {
+  if (net->L < 3) return nullptr;
+  const lirpa_layer &t2 = net->T[1], &t1 = net->T[0];
+  if (t2.kind != LIRPA_CONV2D || t1.kind != LIRPA_CONV2D) return nullptr;
+  const bool t1_ok = t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.in_c == 3 &&
+                     t1.in_h == 32 && t1.in_w == 32 && t1.out_h == 16 && t1.out_w == 16;
+  const bool t2_ok = t2.k == 4 && t2.stride == 2 && t2.pad == 1 && t2.in_h == 16 &&
+                     t2.in_w == 16 && t2.out_h == 8 && t2.out_w == 8;
+  if (!t1_ok || !t2_ok) return nullptr;
+  if (t1.out_c == 8 && t2.in_c == 8 && t2.out_c == 16) {
+    *nwaves = 8 / 2 + 4;
+    if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
+    if (nbs == 2)
+      return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
+    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 3>;
+  }
+  return nullptr;
+}
+
 // Fused last two stages (T_2^T + relaxation of layer 1, T_1^T + concretisation) when both
 // layers are convolutions of a covered geometry; null otherwise.  *nwaves, *lds as launched.
 using ConvT2Kernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink);
@@ -4106,6 +4171,26 @@ int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, flo
   int cur = 0;
   for (int m = mtop; m >= 1; --m) {
     int e;
+    if (m == 2 && !c.tape && R >= 8) {
+      // T_2^T, the layer-1 relaxation, T_1^T and the concretisation in one kernel
+      int nw = 0;
+      if (FcBoundKernel kern = conv12_bound_for(c.net, false, R >= 16 ? 2 : 3, &nw)) {
+        Sink s = slab_sink(c, 1, nullptr, ldq, R);
+        const Sink sb = bound_sink(c, R, lo, hi, bstride, n_half);
+        s.eps = sb.eps;
+        s.x0 = sb.x0;
+        s.lo = sb.lo;
+        s.hi = sb.hi;
+        s.bstride = sb.bstride;
+        s.n_half = sb.n_half;
+        const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+        return launch_k(tag("convT_slab_bound", 2, pass), c.st, [&] {
+          hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st,
+                             dlayer(c.net->T[1]), dlayer(c.net->T[0]), slab[cur],
+                             (unsigned)ldq, (unsigned)Q, s, FcSrc{});
+        });
+      }
+    }
     if (m == 2 && !c.tape && R >= 16) {
       int nw = 0;
       size_t lds = 0;
@@ -4272,25 +4357,11 @@ int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
   });
 }
 
-// Pass 3 of a net whose layers 1 and 2 are convolutions of a covered geometry and whose layer 3
-// is fully connected, bounded without a gradient tape: one kernel from the rows of W_3 to the
-// bounds.  Null otherwise.
-using FcBoundKernel = void (*)(DLayer, DLayer, unsigned, Sink, FcSrc);
+// Pass 3 of a net whose layers 1 and 2 are such convolutions and whose layer 3 is fully
+// connected, bounded without a gradient tape: one kernel from the rows of W_3 to the bounds.
 FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves) {
-  if (k != 3 || net->L < 4) return nullptr;
-  const lirpa_layer &fl = net->T[2], &t2 = net->T[1], &t1 = net->T[0];
-  if (fl.kind != LIRPA_LINEAR || t2.kind != LIRPA_CONV2D || t1.kind != LIRPA_CONV2D)
-    return nullptr;
-  const bool t1_ok = t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.in_c == 3 &&
-                     t1.in_h == 32 && t1.in_w == 32 && t1.out_h == 16 && t1.out_w == 16;
-  const bool t2_ok = t2.k == 4 && t2.stride == 2 && t2.pad == 1 && t2.in_h == 16 &&
-                     t2.in_w == 16 && t2.out_h == 8 && t2.out_w == 8;
-  if (!t1_ok || !t2_ok) return nullptr;
-  if (t1.out_c == 8 && t2.in_c == 8 && t2.out_c == 16) {
-    *nwaves = 8 / 2 + 4;
-    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4>;
-  }
-  return nullptr;
+  if (k != 3 || net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
+  return conv12_bound_for(net, true, 2, nwaves);
 }
 
 // Returns 1 when the pass does not qualify (the caller runs the stages one by one).
@@ -4317,7 +4388,7 @@ int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
   return launch_k(tag("convT_fc_bound", k - 1, k), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[k - 2]),
-                       dlayer(net->T[0]), (unsigned)Q, s, f);
+                       dlayer(net->T[0]), nullptr, 0u, (unsigned)Q, s, f);
   });
 }
 
