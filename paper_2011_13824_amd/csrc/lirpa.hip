@@ -362,40 +362,15 @@ __global__ void __launch_bounds__(256) k_init_fc_rows(DLayer t, const float* __r
   if (w == 0 && ok) s.beta[q] = sgn * t.b[j] + ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
-// z1 = W1 x0 + b1: the layer-1 pre-activation at the box centre.
-__device__ __forceinline__ void layer1_at_x0(const DLayer& t, const float* __restrict__ x0,
-                                             float* __restrict__ z, long j) {
-  const int hw = t.out_h * t.out_w;
-  float a = t.b[j / hw];
-  if (t.kind == LIRPA_LINEAR) {
-    for (int i = 0; i < t.in_c; ++i) a = fmaf(t.W[j * t.in_c + i], x0[i], a);
-  } else {
-    int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
-    for (int ci = 0; ci < t.in_c; ++ci)
-      for (int ky = 0; ky < t.k; ++ky) {
-        int yi = yo * t.stride - t.pad + ky;
-        if (yi < 0 || yi >= t.in_h) continue;
-        for (int kx = 0; kx < t.k; ++kx) {
-          int xi = xo * t.stride - t.pad + kx;
-          if (xi < 0 || xi >= t.in_w) continue;
-          a = fmaf(t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx],
-                   x0[((long)ci * t.in_h + yi) * t.in_w + xi], a);
-        }
-      }
-  }
-  z[j] = a;
-}
-
 // Everything a call derives from the network, x0 and eps alone, in one launch: the exact
-// layer-1 bounds (rows +-e_j of h^(1) through T_1, concretised), z1 = W1 x0 + b1, the
-// per-neuron bias vectors of ReLU layers 2..L-1 and the transposed weights of the fully
-// connected layers that start an intermediate pass.  Thread e is dealt to the segments in
-// that order.
+// layer-1 bounds and z1 = W1 x0 + b1, the per-neuron bias vectors of ReLU layers 2..L-1 and the
+// transposed weights of the fully connected layers whose intermediate pass starts from them.
+// Thread e is dealt to the segments in that order; a layer-1 neuron takes 16 threads.
 struct SetupJob {
   DLayer t1;
-  Sink s1;      // layer-1 bound rows (MODE_BOUND sink)
-  long n_rows;  // 2 n1
   const float* x0;
+  float eps;
+  float* l1;    // [n1] lower, then [n1] upper bounds of h^(1)
   float* z1;
   long n1;
   int nfill;
@@ -409,18 +384,51 @@ struct SetupJob {
   float* tr_dst[kMaxLayers];
 };
 
+// Neuron j of h^(1): row +-e_j carried through T_1 is +-W_1[j] (no relaxation in front of
+// layer 1), so its bounds are z1_j -+ eps ||W_1[j]||_1 with z1_j = W_1[j] x0 + b_1[j] (Eq. 8; the
+// taps of a convolution that fall on the zero padding are no entries of the row).  The 16 lanes
+// of a group take every 16th entry and the sums meet in a fixed shuffle tree.
+__device__ __forceinline__ void layer1_neuron(const SetupJob& job, long j, int g) {
+  const DLayer& t = job.t1;
+  float lin = 0.f, l1 = 0.f;
+  if (t.kind == LIRPA_LINEAR) {
+    for (int i = g; i < t.in_c; i += 16) {
+      const float w = t.W[j * t.in_c + i];
+      lin = fmaf(w, job.x0[i], lin);
+      l1 += fabsf(w);
+    }
+  } else {
+    const int hw = t.out_h * t.out_w, kk = t.k * t.k;
+    const int co = (int)(j / hw), yo = (int)((j / t.out_w) % t.out_h), xo = (int)(j % t.out_w);
+    for (int e = g; e < t.in_c * kk; e += 16) {
+      const int ci = e / kk, ky = (e / t.k) % t.k, kx = e % t.k;
+      const int yi = yo * t.stride - t.pad + ky, xi = xo * t.stride - t.pad + kx;
+      if (yi < 0 || yi >= t.in_h || xi < 0 || xi >= t.in_w) continue;
+      const float w = t.W[(long)co * t.in_c * kk + e];
+      lin = fmaf(w, job.x0[((long)ci * t.in_h + yi) * t.in_w + xi], lin);
+      l1 += fabsf(w);
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) {
+    lin += __shfl_xor(lin, o, 64);
+    l1 += __shfl_xor(l1, o, 64);
+  }
+  if (g == 0) {
+    const float z = lin + t.b[j / (t.out_h * t.out_w)];
+    job.z1[j] = z;
+    job.l1[j] = z - job.eps * l1;
+    job.l1[job.n1 + j] = z + job.eps * l1;
+  }
+}
+
 __global__ void __launch_bounds__(kBlock) k_setup(SetupJob job) {
   long e = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (e < job.n_rows) {
-    init_row<MODE_BOUND>(job.t1, nullptr, job.s1, e);
+  if (e < 16 * job.n1) {  // a group of 16 lanes never straddles the segment's end
+    layer1_neuron(job, e >> 4, (int)(e & 15));
     return;
   }
-  e -= job.n_rows;
-  if (e < job.n1) {
-    layer1_at_x0(job.t1, job.x0, job.z1, e);
-    return;
-  }
-  e -= job.n1;
+  e -= 16 * job.n1;
   for (int f = 0; f < job.nfill; ++f) {
     if (e < job.fill_n[f]) {
       job.fill_out[f][e] = job.fill_b[f][e / job.fill_hw[f]];
@@ -4514,22 +4522,15 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
 // concretised (no relaxation in front of layer 1).
 int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0, float eps,
                   hipStream_t st) {
-  long n1 = net->n[1], R = 2 * n1;
-  float* l1u1 = at<float>(ws, p.off_l1u1);
+  long n1 = net->n[1];
   SetupJob job{};
   job.t1 = dlayer(net->T[0]);
-  job.s1.x0 = x0;
-  job.s1.eps = eps;
-  job.s1.R = R;
-  job.s1.lo = l1u1;
-  job.s1.hi = l1u1 + n1;
-  job.s1.bstride = 0;
-  job.s1.n_half = n1;
-  job.n_rows = R;
   job.x0 = x0;
+  job.eps = eps;
+  job.l1 = at<float>(ws, p.off_l1u1);
   job.z1 = at<float>(ws, p.off_z1);
   job.n1 = n1;
-  long total = R + n1;
+  long total = 16 * n1;
   for (int m = 2; m <= net->L - 1; ++m) {  // bias vectors (layer 1's is z1)
     const lirpa_layer& t = net->T[m - 1];
     job.fill_n[job.nfill] = net->n[m];
@@ -4539,8 +4540,15 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
     total += net->n[m];
     ++job.nfill;
   }
-  for (int k = 2; k <= net->L - 1; ++k) {  // transposed FC weights
-    if (!p.off_wT[k]) continue;
+  // transposed FC weights, for the passes that do not open inside the stage below (those read
+  // W_k row by row); that holds for every chunk if it holds for the largest
+  Chunk cp{};
+  cp.net = net;
+  cp.p = &p;
+  cp.nb = p.Bc;
+  cp.tape = p.mode == 1;
+  for (int k = 2; k <= net->L - 1; ++k) {
+    if (!p.off_wT[k] || fc_open_ok(cp, k, 2 * net->n[k])) continue;
     const lirpa_layer& t = net->T[k - 1];
     job.tr_W[job.ntr] = t.W;
     job.tr_out[job.ntr] = t.out_c;
