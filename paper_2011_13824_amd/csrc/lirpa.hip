@@ -3167,6 +3167,112 @@ __global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* 
   block_finish<MODE>(s, sum, red, q0, Q, false);
 }
 
+// The final pass's first two stages when T_L and T_{L-1} are fully connected, 16 rows
+// q = (b, s) per block (NW waves):
+//  (1) row q is the spec row C_s over h^(L) (the property merged into the last layer, Sec. 2.1);
+//      through T_L it becomes C_s W_L over g^(L-1) with bias C_s b_L (Eq. 4).  Its entries are
+//      relaxed onto layer L-1 (Eq. 6) into an LDS tile [j][16 q] with their intercept and bias
+//      terms;
+//  (2) T_{L-1}^T on 16x16x4 MFMA (M = 16 features i of g^(L-2), K = 4 features j, N = 16 rows),
+//      one 16-feature tile per wave at a time with its operands from W_{L-1} (L2-resident); the
+//      results are relaxed onto layer L-2 and stored into the slab, with their terms.
+// The rows' bias goes to Sink::beta (the pass's first stage).  lo1/up1/bu1/bias1: the
+// relaxation of layer L-1; s: that of layer L-2 and the slab.
+template <int NW>
+__global__ void __launch_bounds__(64 * NW)
+    k_final_fc(DLayer tL, DLayer tM, const float* __restrict__ C, int S, long nb, long Q,
+               const float* __restrict__ lo1, const float* __restrict__ up1,
+               const float* __restrict__ bu1, const float* __restrict__ bias1, Sink s) {
+  extern __shared__ float lds[];
+  const int nL = tL.out_c, nj = tM.out_c, ni = tM.in_c;  // n_L, n_{L-1}, n_{L-2}
+  const int KP = (nj + 3) & ~3;
+  float* tile = lds;                 // [KP][16]
+  float* red = lds + KP * 16;        // [NW * 64] terms of (1), then [NW][16] terms of (2)
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const long q0 = (long)blockIdx.x * 16;
+  // (1) thread: row qa = tid & 15, features j = tid >> 4 + k NW 4
+  {
+    const int qa = threadIdx.x & 15;
+    const long q = min(q0 + qa, Q - 1);
+    const long b = q / S;
+    const int sr = (int)(q % S);
+    const long pb = b * s.pstride;
+    float beta = 0.f;
+    for (int j = threadIdx.x >> 4; j < KP; j += NW * 4) {
+      float ah = 0.f;
+      if (j < nj) {
+        float a = 0.f;
+        for (int o = 0; o < nL; ++o) a = fmaf(C[sr * nL + o], tL.W[(long)o * nj + j], a);
+        ah = a * (a >= 0.f ? lo1[pb + j] : up1[pb + j]);
+        beta = fmaf(fminf(a, 0.f), bu1[pb + j], beta);
+        beta = fmaf(ah, bias1[j], beta);
+      }
+      tile[j * 16 + qa] = ah;
+    }
+    red[threadIdx.x] = beta;
+  }
+  __syncthreads();
+  // (2)
+  const int n = lane & 15, G = lane >> 4;
+  const long q = q0 + n;
+  const long b = (q < Q ? q : Q - 1) / S;
+  const long pb = b * s.pstride;
+  float beta = 0.f;
+  const int nk = KP / 4;
+  for (int mt = wave; mt * 16 < ni; mt += NW) {
+    const int ia = mt * 16 + n;  // A operand: feature i of this lane, K index G
+    float4v d = {0.f, 0.f, 0.f, 0.f};
+    int k = 0;
+    for (; k + 8 <= nk; k += 8) {
+      float a[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = 4 * (k + u) + G;
+        a[u] = (j < nj && ia < ni) ? tM.W[(long)j * ni + ia] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], tile[(4 * (k + u) + G) * 16 + n], d, 0,
+                                                 0, 0);
+    }
+    for (; k < nk; ++k) {
+      const int j = 4 * k + G;
+      const float a = (j < nj && ia < ni) ? tM.W[(long)j * ni + ia] : 0.f;
+      d = __builtin_amdgcn_mfma_f32_16x16x4f32(a, tile[j * 16 + n], d, 0, 0, 0);
+    }
+    // lane holds features i0 .. i0 + 3 of row q
+    const int i0 = mt * 16 + 4 * G;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = i0 + r;
+      if (i < ni) {
+        const float a = d[r];
+        const float ah = a * (a >= 0.f ? s.a_lo[pb + i] : s.a_up[pb + i]);
+        beta = fmaf(fminf(a, 0.f), s.b_up[pb + i], beta);
+        beta = fmaf(ah, s.bias[i], beta);
+        s.out[(long)i * s.ldq + q] = ah;
+      }
+    }
+  }
+  // (2)'s terms per row: over the lane groups, then over the waves in order; (1)'s: over the
+  // threads of the row in order
+  beta += __shfl_xor(beta, 16, 64);
+  beta += __shfl_xor(beta, 32, 64);
+  if (lane < 16) red[NW * 64 + wave * 16 + lane] = beta;
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    const long qq = q0 + threadIdx.x;
+    if (qq < Q) {
+      const int sr = (int)(qq % S);
+      float tb = 0.f;
+      for (int o = 0; o < nL; ++o) tb = fmaf(C[sr * nL + o], tL.b[o], tb);
+      for (int t = threadIdx.x; t < NW * 64; t += 16) tb += red[t];
+      for (int w = 0; w < NW; ++w) tb += red[NW * 64 + w * 16 + threadIdx.x];
+      s.beta[qq] = tb;
+    }
+  }
+}
+
 // Relaxation parameters of ReLU layer m for every sub-domain of the chunk (Eq. 5 with the split
 // override of Sec. 3.1, checked in the order: split, u <= 0, l >= 0, unstable).
 // lsh, ush (optional): bounds shared by every sub-domain (layer 1), copied into its rows of l, u.
@@ -4509,6 +4615,26 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   // final pass
   long R = c.S, Q = c.nb * R, ldq = round_up(Q, 64);
   const lirpa_layer& tL = net->T[L - 1];
+  if (!c.tape && L >= 3 && tL.kind == LIRPA_LINEAR && net->T[L - 2].kind == LIRPA_LINEAR) {
+    // the spec rows through T_L and T_{L-1} in one kernel
+    constexpr int NW = 16;
+    Sink s = slab_sink(c, L - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
+    const long nj = net->n[L - 1];
+    const size_t lds = (size_t)(((nj + 3) & ~3L) * 16 + NW * 64 + NW * 16) * sizeof(float);
+    if (lds <= 65536) {
+      const size_t po = (size_t)net->poff[L - 1];
+      if (int e = launch_k(tag("final_fc", L - 1, L), c.st, [&] {
+            hipLaunchKernelGGL(k_final_fc<NW>, dim3((unsigned)((Q + 15) / 16)), dim3(64 * NW),
+                               lds, c.st, dlayer(tL), dlayer(net->T[L - 2]), C, (int)c.S, c.nb,
+                               Q, at<float>(c.ws, c.p->off_alo) + po,
+                               at<float>(c.ws, c.p->off_aup) + po,
+                               at<float>(c.ws, c.p->off_bup) + po,
+                               at<float>(c.ws, c.p->off_bz) + po, s);
+          }))
+        return e;
+      return run_stages(c, L, L - 2, R, Q, ldq, lb, lb, c.S, c.S);
+    }
+  }
   if (int e = launch_k(tag("spec_rows", L, L), c.st, [&] {
         hipLaunchKernelGGL(k_spec_rows, grid_for(Q), dim3(kBlock), 0, c.st, C, net->n[L], tL.b,
                            tL.out_h * tL.out_w, Q, c.S, at<float>(c.ws, c.p->off_slab0), ldq,
