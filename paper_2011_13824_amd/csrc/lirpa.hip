@@ -382,6 +382,12 @@ struct SetupJob {
   const float* tr_W[kMaxLayers];
   int tr_out[kMaxLayers], tr_in[kMaxLayers];
   float* tr_dst[kMaxLayers];
+  // the property merged into the last layer (Sec. 2.1): wsp[s][j] = (C W_L)[s][j], then
+  // wsp[S n_{L-1} + s] = (C b_L)[s]; null when not needed
+  float* wsp;
+  const float* C;
+  DLayer tL;
+  int S;
 };
 
 // Neuron j of h^(1): row +-e_j carried through T_1 is +-W_1[j] (no relaxation in front of
@@ -444,6 +450,22 @@ __global__ void __launch_bounds__(kBlock) k_setup(SetupJob job) {
       return;
     }
     e -= nel;
+  }
+  if (job.wsp) {
+    const int nL = job.tL.out_c, nj = job.tL.in_c;
+    if (e < (long)job.S * nj) {
+      const int sr = (int)(e / nj), j = (int)(e % nj);
+      float a = 0.f;
+      for (int o = 0; o < nL; ++o) a = fmaf(job.C[sr * nL + o], job.tL.W[(long)o * nj + j], a);
+      job.wsp[e] = a;
+      return;
+    }
+    e -= (long)job.S * nj;
+    if (e < job.S) {
+      float a = 0.f;
+      for (int o = 0; o < nL; ++o) a = fmaf(job.C[e * nL + o], job.tL.b[o], a);
+      job.wsp[(long)job.S * nj + e] = a;
+    }
   }
 }
 
@@ -3170,9 +3192,9 @@ __global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* 
 // The final pass's first two stages when T_L and T_{L-1} are fully connected, 16 rows
 // q = (b, s) per block (NW waves):
 //  (1) row q is the spec row C_s over h^(L) (the property merged into the last layer, Sec. 2.1);
-//      through T_L it becomes C_s W_L over g^(L-1) with bias C_s b_L (Eq. 4).  Its entries are
-//      relaxed onto layer L-1 (Eq. 6) into an LDS tile [j][16 q] with their intercept and bias
-//      terms;
+//      through T_L it becomes C_s W_L over g^(L-1) with bias C_s b_L (Eq. 4), both formed once
+//      per call by k_setup (wsp).  Its entries are relaxed onto layer L-1 (Eq. 6) into an LDS
+//      tile [j][16 q] with their intercept and bias terms;
 //  (2) T_{L-1}^T on 16x16x4 MFMA (M = 16 features i of g^(L-2), K = 4 features j, N = 16 rows),
 //      one 16-feature tile per wave at a time with its operands from W_{L-1} (L2-resident); the
 //      results are relaxed onto layer L-2 and stored into the slab, with their terms.
@@ -3180,11 +3202,11 @@ __global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* 
 // relaxation of layer L-1; s: that of layer L-2 and the slab.
 template <int NW>
 __global__ void __launch_bounds__(64 * NW)
-    k_final_fc(DLayer tL, DLayer tM, const float* __restrict__ C, int S, long nb, long Q,
+    k_final_fc(DLayer tM, const float* __restrict__ wsp, int S, long nb, long Q,
                const float* __restrict__ lo1, const float* __restrict__ up1,
                const float* __restrict__ bu1, const float* __restrict__ bias1, Sink s) {
   extern __shared__ float lds[];
-  const int nL = tL.out_c, nj = tM.out_c, ni = tM.in_c;  // n_L, n_{L-1}, n_{L-2}
+  const int nj = tM.out_c, ni = tM.in_c;  // n_{L-1}, n_{L-2}
   const int KP = (nj + 3) & ~3;
   float* tile = lds;                 // [KP][16]
   float* red = lds + KP * 16;        // [NW * 64] terms of (1), then [NW][16] terms of (2)
@@ -3201,8 +3223,7 @@ __global__ void __launch_bounds__(64 * NW)
     for (int j = threadIdx.x >> 4; j < KP; j += NW * 4) {
       float ah = 0.f;
       if (j < nj) {
-        float a = 0.f;
-        for (int o = 0; o < nL; ++o) a = fmaf(C[sr * nL + o], tL.W[(long)o * nj + j], a);
+        const float a = wsp[(long)sr * nj + j];
         ah = a * (a >= 0.f ? lo1[pb + j] : up1[pb + j]);
         beta = fmaf(fminf(a, 0.f), bu1[pb + j], beta);
         beta = fmaf(ah, bias1[j], beta);
@@ -3263,9 +3284,7 @@ __global__ void __launch_bounds__(64 * NW)
   if (threadIdx.x < 16) {
     const long qq = q0 + threadIdx.x;
     if (qq < Q) {
-      const int sr = (int)(qq % S);
-      float tb = 0.f;
-      for (int o = 0; o < nL; ++o) tb = fmaf(C[sr * nL + o], tL.b[o], tb);
+      float tb = wsp[(long)S * nj + qq % S];
       for (int t = threadIdx.x; t < NW * 64; t += 16) tb += red[t];
       for (int w = 0; w < NW; ++w) tb += red[NW * 64 + w * 16 + threadIdx.x];
       s.beta[qq] = tb;
@@ -3852,6 +3871,7 @@ struct Plan {
   int mode = 0;
   size_t off_l = 0, off_u = 0, off_alo = 0, off_aup = 0, off_bup = 0, off_code = 0;
   size_t off_l1u1 = 0, off_slab0 = 0, off_slab1 = 0, off_beta = 0, total = 0;
+  size_t off_wsp = 0;  // C W_L [S][n_{L-1}], then C b_L [S] (L >= 2, T_L fully connected)
   size_t off_bz = 0;  // per-neuron bias of every ReLU layer (padded layout, segment m at poff[m])
   size_t off_z1 = 0;  // its layer-1 segment: W1 x0 + b1
   long slab_floats = 0, qp_max = 0;
@@ -3947,6 +3967,10 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   p.off_bup = o;  o = align256(o + perp * 4);
   p.off_code = o; o = align256(o + per);
   p.off_l1u1 = o; o = align256(o + 2 * (size_t)net->n[1] * 4);
+  if (net->L >= 2 && net->T[net->L - 1].kind == LIRPA_LINEAR) {
+    p.off_wsp = o;
+    o = align256(o + (size_t)S * (net->n[net->L - 1] + 1) * 4);
+  }
   p.off_bz = o;   o = align256(o + (size_t)std::max<long>(net->pstride, net->n[1]) * 4);
   p.off_z1 = p.off_bz + (size_t)net->poff[1] * 4;
   p.off_beta = o; o = align256(o + (size_t)qpmax * 4);
@@ -4615,7 +4639,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   // final pass
   long R = c.S, Q = c.nb * R, ldq = round_up(Q, 64);
   const lirpa_layer& tL = net->T[L - 1];
-  if (!c.tape && L >= 3 && tL.kind == LIRPA_LINEAR && net->T[L - 2].kind == LIRPA_LINEAR) {
+  if (!c.tape && L >= 3 && c.p->off_wsp && net->T[L - 2].kind == LIRPA_LINEAR) {
     // the spec rows through T_L and T_{L-1} in one kernel
     constexpr int NW = 16;
     Sink s = slab_sink(c, L - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
@@ -4625,7 +4649,8 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
       const size_t po = (size_t)net->poff[L - 1];
       if (int e = launch_k(tag("final_fc", L - 1, L), c.st, [&] {
             hipLaunchKernelGGL(k_final_fc<NW>, dim3((unsigned)((Q + 15) / 16)), dim3(64 * NW),
-                               lds, c.st, dlayer(tL), dlayer(net->T[L - 2]), C, (int)c.S, c.nb,
+                               lds, c.st, dlayer(net->T[L - 2]),
+                               at<float>(c.ws, c.p->off_wsp), (int)c.S, c.nb,
                                Q, at<float>(c.ws, c.p->off_alo) + po,
                                at<float>(c.ws, c.p->off_aup) + po,
                                at<float>(c.ws, c.p->off_bup) + po,
@@ -4647,7 +4672,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
 // Exact layer-1 bounds, shared by every sub-domain: rows +-e_j of h^(1) through T_1, then
 // concretised (no relaxation in front of layer 1).
 int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0, float eps,
-                  hipStream_t st) {
+                  const float* C, int S, hipStream_t st) {
   long n1 = net->n[1];
   SetupJob job{};
   job.t1 = dlayer(net->T[0]);
@@ -4682,6 +4707,13 @@ int layer1_bounds(const lirpa_net* net, const Plan& p, void* ws, const float* x0
     job.tr_dst[job.ntr] = at<float>(ws, p.off_wT[k]);
     total += (long)t.out_c * t.in_c;
     ++job.ntr;
+  }
+  if (p.off_wsp) {
+    job.wsp = at<float>(ws, p.off_wsp);
+    job.C = C;
+    job.tL = dlayer(net->T[net->L - 1]);
+    job.S = S;
+    total += (long)S * (net->n[net->L - 1] + 1);
   }
   return launch_k(tag("setup", 1, 1), st, [&] {
     hipLaunchKernelGGL(k_setup, grid_for(total), dim3(kBlock), 0, st, job);
@@ -4927,7 +4959,7 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1).total);
-  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
     if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
@@ -4946,7 +4978,7 @@ int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C,
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1, 1).total);
-  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
     if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
@@ -4974,7 +5006,7 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1, 1).total);
-  if (int e = layer1_bounds(net, p, ws, x0, eps, stream)) return e;
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
     long na = c.nb * net->n_relu, ns = c.nb * S;
