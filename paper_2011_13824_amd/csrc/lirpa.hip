@@ -142,6 +142,15 @@ __device__ __forceinline__ unsigned xcd_tile(unsigned blk) {
   return (blk & ~15u) + ((blk & 7u) << 1) + ((blk >> 3) & 1u);
 }
 
+// Block index of a kernel whose blocks read per-sub-domain data (relaxation parameters): the
+// blocks of XCD x (those with blockIdx.x mod 8 == x) take the contiguous range
+// [x n/8, (x+1) n/8) in order, n = gridDim.x, so the consecutive blocks of one sub-domain
+// fetch its data into one L2 instead of all eight.  Identity when n is not a multiple of 8.
+__device__ __forceinline__ unsigned xcd_range(unsigned blk) {
+  const unsigned n = gridDim.x;
+  return (n & 7u) ? blk : (blk & 7u) * (n >> 3) + (blk >> 3);
+}
+
 // Index of the calling wave in its block, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() {
   return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1692,7 +1701,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
   __shared__ float red[NM * 16 + 2 * NXW * 16];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
-  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  const unsigned q0 = xcd_range(blockIdx.x) * 16u;
   if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned R = (unsigned)s.R;
   const unsigned b0 = q0 / R;
@@ -2176,7 +2185,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
   const int nxc = W2 / XW;
-  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  unsigned blk = xcd_range(blockIdx.x);  // 32-bit: the scalar divisions stay short
   const int x2c = (int)(blk % (unsigned)nxc); blk /= (unsigned)nxc;
   const int y2 = (int)(blk % (unsigned)H2); blk /= (unsigned)H2;
   const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
