@@ -107,6 +107,21 @@ def test_alpha_on_conv_nets(name):
     check(f"{name}+alpha u", u, ulr)
 
 
+@pytest.mark.parametrize("B", [1, 5])
+def test_base_partial_blocks(B):
+    # Base geometry with batches whose row counts leave partial 16-row blocks in every pass
+    # (pass 3: 200 B rows, final pass: 9 B rows), random lower slopes and splits
+    w = wl.base()
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=B)
+    alpha = np.random.default_rng(11 + B).uniform(0, 1, (B, rnet.n_relu)).astype(np.float32)
+    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split, alpha)
+    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, split, alpha)
+    check(f"base B={B} lb", lb, lr)
+    check(f"base B={B} l", l, llr)
+    check(f"base B={B} u", u, ulr)
+
+
 @pytest.mark.parametrize("name", ["tiny", "base", "wide", "deep"])
 def test_all_split_matches_closed_form(name):
     w = wl.get(name)
