@@ -2176,7 +2176,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   constexpr int NPP = (NE + NT - 1) / NT;           // staged parameters per thread
   __shared__ float tile[NEL];
   __shared__ float red[NW * 16 + RPT * 16];
-  __shared__ float prm[4][NE];  // a_lo, a_up, b_up, W1 x0 + b1 of the window (0 outside)
+  __shared__ float4v prm[NE];  // (a_lo, a_up, b_up, W1 x0 + b1) of the window (0 outside)
   float* bred = red + NW * 16;
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -2199,32 +2199,35 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
   const P2Row prw = p2_row(C2, g, row);
   const float sgn = prw.neg ? -1.f : 1.f;
-  float w2r[NEP];
+  // split by sign (relaxed entry = wp a_lo + wn a_up), and the entry's place in the tile
+  float wp[NEP], wn[NEP];
+  int toff[NEP];
   {
     const float* w2 = t2.W + (long)prw.c2 * NE;  // [C1][K2][K2] of output channel c2
 #pragma unroll
     for (int k = 0; k < NEP; ++k) {
       const int e = part + k * RPT;
-      w2r[k] = e < NE ? sgn * w2[e] : 0.f;
+      const float w = e < NE ? sgn * w2[e] : 0.f;
+      wp[k] = fmaxf(w, 0.f);
+      wn[k] = fminf(w, 0.f);
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      toff[k] = c1 * CS + pos * 16 + row;
     }
   }
   // relaxation parameters of a window, one neuron per (thread, k)
-  float pn[NPP][4];
+  float4v pn[NPP];
   auto pfetch = [&](int X1) {
 #pragma unroll
     for (int k = 0; k < NPP; ++k) {
       const int e = threadIdx.x + k * NT;
-      pn[k][0] = pn[k][1] = pn[k][2] = pn[k][3] = 0.f;
+      pn[k] = float4v{0.f, 0.f, 0.f, 0.f};
       if (e >= NE) continue;
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
       const int y1 = Y1 + ky2, x1 = X1 + kx2;
       if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
         const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
-        pn[k][0] = a_lo[pb + ni];
-        pn[k][1] = a_up[pb + ni];
-        pn[k][2] = b_up[pb + ni];
-        pn[k][3] = z1[ni];
+        pn[k] = float4v{a_lo[pb + ni], a_up[pb + ni], b_up[pb + ni], z1[ni]};
       }
     }
   };
@@ -2258,12 +2261,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
 #pragma unroll
     for (int k = 0; k < NPP; ++k) {
       const int e = threadIdx.x + k * NT;
-      if (e < NE) {
-        prm[0][e] = pn[k][0];
-        prm[1][e] = pn[k][1];
-        prm[2][e] = pn[k][2];
-        prm[3][e] = pn[k][3];
-      }
+      if (e < NE) prm[e] = pn[k];
     }
     __syncthreads();
     if (xi + 1 < XW) pfetch(X1 + t2.stride);
@@ -2271,16 +2269,15 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       float bpart = 0.f;
 #pragma unroll
       for (int k = 0; k < NEP; ++k) {
-        // (no early exit: the loop unrolls, so w2r is indexed statically)
+        // (no early exit: the loop unrolls, so the arrays are indexed statically)
         const int e = part + k * RPT;
         if (e < NE) {
-          const int c1 = e / NPOS, pos = e - c1 * NPOS;
-          const float w = w2r[k];
-          const float v = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
-          bpart = fmaf(fminf(w, 0.f), prm[2][e], bpart);
+          const float4v pr = prm[e];
+          const float v = fmaf(wp[k], pr[0], wn[k] * pr[1]);
+          bpart = fmaf(wn[k], pr[2], bpart);
           // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
-          bpart = fmaf(v, prm[3][e], bpart);
-          tile[c1 * CS + pos * 16 + row] = v;
+          bpart = fmaf(v, pr[3], bpart);
+          tile[toff[k]] = v;
         }
       }
       bred[part * 16 + row] = bpart;
