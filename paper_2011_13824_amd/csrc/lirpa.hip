@@ -1699,6 +1699,9 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
   __shared__ float ring[2][SLOT];
   __shared__ float4v pars[2][PSLOT4];
   __shared__ float red[NM * 16 + 2 * NXW * 16];
+  // border exchange of the x waves (see there): [step parity][wave - 1][channel, column][lane]
+  constexpr int NSH = K1 - S1;  // output columns two neighbouring x waves share
+  __shared__ float xb[2][NXW > 1 ? NXW - 1 : 1][C0 * NSH][64];
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const unsigned q0 = xcd_range(blockIdx.x) * 16u;
@@ -1923,45 +1926,36 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
         red[wave * 16 + 2 * lane + 1] = fbeta_b;
       }
     }
+    lds_barrier();  // the x waves' last border exchange
     lds_barrier();  // final reduction
     return;
   }
 
   // ---------------------------------------------------------------------- x waves
   static_assert(NXW >= 1 && NXW <= 4, "x waves");
+  static_assert(W0 % NXW == 0 && NSH > 0, "x-wave column split");
+  static_assert(S <= PER1 && K - S <= PER1, "at most one output row per lane and step");
   const int xw = wave - NM;
   const int n = lane & 15, G = lane >> 4;
   const unsigned q = q0 + n;
   const int bsel = q < Q ? (int)(q / R - b0) : 0;
   // the x waves carry the longer chain of each step: they go first when both roles can issue
   __builtin_amdgcn_s_setprio(2);
-  // Output columns [ob(j), ob(j + 1)) of T_1^T belong to x wave j.  An inner border b with
-  // (b + P1) % S1 == 0 leaves K1 / S1 - 1 input columns to both neighbours.
-  constexpr auto ob = [](int j) {
-    if (j <= 0) return 0;
-    if (j >= NXW) return WX;
-    int b = j * WX / NXW;
-    while ((b + P1) % S1 != 0) --b;
-    return b;
-  };
-  constexpr auto cdiv = [](int a, int b) { return a >= 0 ? (a + b - 1) / b : -((-a) / b); };
-  constexpr auto fdiv = [](int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); };
-  // input columns of wave j: [xlo(j), xhi(j)]; the intercept and bias terms of column x1 are
-  // added by the first wave that reads it
-  constexpr auto xlo = [=](int j) {
-    const int v = cdiv(ob(j) + P1 - K1 + 1, S1);
-    return v < 0 ? 0 : v;
-  };
-  constexpr auto xhi = [=](int j) {
-    const int v = fdiv(ob(j + 1) - 1 + P1, S1);
-    return v > W0 - 1 ? W0 - 1 : v;
-  };
-  // xw is made a constant so that the column ranges are compile-time
-  auto xrun = [&](auto xb) {
-  constexpr int XB = decltype(xb)::value;
-  constexpr int OL = ob(XB), OW = ob(XB + 1) - ob(XB);
-  constexpr int XL = xlo(XB), XH = xhi(XB);
-  constexpr int XC = XB + 1 < NXW ? xlo(XB + 1) : XH + 1;  // bias terms: columns [XL, XC)
+  // x wave j takes the input columns [j W0/NXW, (j+1) W0/NXW) of T_1^T (and adds their
+  // intercept and bias terms).  Their image covers OW output columns from OL on; the first and
+  // last NSH of them are shared with the neighbouring waves.  When a lane completes an output
+  // row it adds |.| of its own columns to ||A_x||_1, publishes its partial sums of the left
+  // shared columns in xb, and keeps those of the right ones; after the next barrier it adds
+  // the right neighbour's published part to them and takes |.|.  A lane completes at most one
+  // output row per step, so one pending row per lane suffices.  xw is made a constant so
+  // that the column ranges are compile-time.
+  auto xrun = [&](auto xb_) {
+  constexpr int XB = decltype(xb_)::value;
+  constexpr int NCX = W0 / NXW;
+  constexpr int XL = XB * NCX, XH = XL + NCX - 1;
+  constexpr int OL = XL * S1 - P1, OW = (NCX - 1) * S1 + K1;
+  constexpr bool HASL = XB > 0, HASR = XB < NXW - 1;
+  static_assert(2 * NSH <= OW, "shared columns");
   float wreg1[PER1][C0][KS1];
   {
     const int M = lane & 15, slot = M >> 2, kx = M & 3;
@@ -1984,16 +1978,37 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
 #pragma unroll
     for (int x = 0; x < OW; ++x) acc1[c0][x] = 0.f;
   float l1 = 0.f, beta = 0.f;
-  auto emit = [&](int yx) {  // output row yx over this wave's columns: ||.||_1
-    if (yx < 0 || yx >= HX) return;
+  float pend[C0 * NSH];  // right shared columns of the pending row
+  bool pend_ok = false;
+  // output row yx completed by this lane (step parity par)
+  auto emit = [&](int yx, int par) {
+    const bool ok = yx >= 0 && yx < HX;
 #pragma unroll
     for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
-      for (int x = 0; x < OW; ++x) l1 += fabsf(acc1[c0][x]);
+      for (int x = 0; x < OW; ++x) {
+        const int g = OL + x;
+        const bool left = HASL && x < NSH, right = HASR && x >= OW - NSH;
+        if (!left && !right && g >= 0 && g < WX && ok) l1 += fabsf(acc1[c0][x]);
+        if (left) xb[par][XB - 1][c0 * NSH + x][lane] = acc1[c0][x];
+        if (right) pend[c0 * NSH + x - (OW - NSH)] = acc1[c0][x];
+        acc1[c0][x] = 0.f;
+      }
+    if (HASR) pend_ok = ok;
+  };
+  // the pending row of the previous step (parity par): add the right neighbour's part
+  auto resolve = [&](int par) {
+    if constexpr (HASR) {
+      if (pend_ok) {
+#pragma unroll
+        for (int v = 0; v < C0 * NSH; ++v) l1 += fabsf(pend[v] + xb[par][XB][v][lane]);
+      }
+      pend_ok = false;
+    }
   };
   // relaxation and T_1^T of row y over g^(1): coefficients in `row`, relaxation in `prm`
   // ([CI][W0] float4 with channel stride PCS4, at this lane's sub-domain)
-  auto consume = [&](const float* row, const float4v* prm, int y) {
+  auto consume = [&](const float* row, const float4v* prm, int y, int par) {
     const int ph = y % PER1;
     float wa[C0][KS1];
 #pragma unroll
@@ -2008,9 +2023,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
     // Three columns in flight: the LDS reads of column x1 + 2 (into buffer x1 & 1), the MFMAs
     // of x1 and the relaxation of x1 + 1, whose reads were issued a column earlier.  The
     // scheduling barriers keep this order (and the compiler from reading further ahead); the
-    // sums of column x1 are added one column later.  Columns whose bias terms another wave
-    // adds read only a_lo and a_up.
-    typedef float float2v __attribute__((ext_vector_type(2)));
+    // sums of column x1 are added one column later.
     float an[2][KS1], hn[KS1];
     float4v pn[2][KS1];
     auto fetch = [&](int x1) {
@@ -2018,12 +2031,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
       for (int ks = 0; ks < KS1; ++ks) {
         const int c1 = 4 * ks + G;
         an[x1 & 1][ks] = row[c1 * CS1 + x1 * 16 + n];
-        if (x1 < XC) {
-          pn[x1 & 1][ks] = prm[c1 * PCS4 + x1];
-        } else {
-          const float2v h = *reinterpret_cast<const float2v*>(prm + c1 * PCS4 + x1);
-          pn[x1 & 1][ks] = float4v{h[0], h[1], 0.f, 0.f};
-        }
+        pn[x1 & 1][ks] = prm[c1 * PCS4 + x1];
       }
     };
     auto relax = [&](int x1) {
@@ -2032,10 +2040,8 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
         const float a = an[x1 & 1][ks];
         const float4v p = pn[x1 & 1][ks];
         const float ah = a * (a >= 0.f ? p[0] : p[1]);
-        if (x1 < XC) {
-          beta = fmaf(fminf(a, 0.f), p[2], beta);
-          beta = fmaf(ah, p[3], beta);
-        }
+        beta = fmaf(fminf(a, 0.f), p[2], beta);
+        beta = fmaf(ah, p[3], beta);
         hn[ks] = ah;
       }
     };
@@ -2043,10 +2049,7 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
 #pragma unroll
       for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
-        for (int kx = 0; kx < K1; ++kx) {
-          const int col = x1 * S1 - P1 + kx - OL;
-          if (col >= 0 && col < OW) acc1[c0][col] += d[c0][kx];
-        }
+        for (int kx = 0; kx < K1; ++kx) acc1[c0][x1 * S1 - P1 + kx - OL] += d[c0][kx];
     };
     fetch(XL);
     if (XL + 1 <= XH) fetch(XL + 1);
@@ -2072,33 +2075,31 @@ __global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_w
     }
     add(XH, dp);
     const int ky = ((G - ph * S1) % K1 + K1) % K1;
-    if (G < K1 && ky < S1) {
-      emit(y * S1 - P1 + ky);
-#pragma unroll
-      for (int c0 = 0; c0 < C0; ++c0)
-#pragma unroll
-        for (int x = 0; x < OW; ++x) acc1[c0][x] = 0.f;
-    }
+    if (G < K1 && ky < S1) emit(y * S1 - P1 + ky, par);
   };
   lds_barrier();  // first input tile
   for (int st = 0; st < NSTEP; ++st) {
     if (st >= 1) {
+      resolve((st - 1) & 1);
       const int e = st - 1;
       const float* slot = ring[e & 1];
       const int nr = nrows(e);
       for (int r = 0; r < nr; ++r) {
         const int y = yrow(e, r);
         if (y >= 0 && y < H0)
-          consume(slot + r * ROWF, pars[e & 1] + bsel * PBS4 + r * CI * PCS4, y);
+          consume(slot + r * ROWF, pars[e & 1] + bsel * PBS4 + r * CI * PCS4, y, st & 1);
       }
     }
     lds_barrier();
   }
+  resolve((NSTEP - 1) & 1);
   {  // output rows still open after the last row of g^(1)
     const int ph = (H0 - 1) % PER1;
     const int ky = ((G - ph * S1) % K1 + K1) % K1;
-    if (G < K1 && ky >= S1) emit((H0 - 1) * S1 - P1 + ky);
+    if (G < K1 && ky >= S1) emit((H0 - 1) * S1 - P1 + ky, NSTEP & 1);
   }
+  lds_barrier();
+  resolve(NSTEP & 1);
   l1 += __shfl_xor(l1, 16, 64);
   l1 += __shfl_xor(l1, 32, 64);
   beta += __shfl_xor(beta, 16, 64);
