@@ -3899,27 +3899,28 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Kernel for the receptive-field pass 2, or null when the shapes do not qualify.
 using Pass2Kernel = void (*)(DLayer, DLayer, long, const float*, const float*, const float*, long,
                              const float*, float, float*, float*, long, long);
-constexpr int kP2XW = 4;  // windows per block of the receptive-field pass 2 (along x2)
+// Windows per block of the receptive-field pass 2 (along x2): 8 when the map width allows it
+// (fewer blocks, each set-up shared by more windows), else 4.
+int p2_xw(const lirpa_net* net) { return net->T[1].out_w % 8 == 0 ? 8 : 4; }
+
+template <int XW>
+Pass2Kernel pass2_kernel_xw(const lirpa_layer& t1, const lirpa_layer& t2) {
+  if (t1.k == 4 && t1.stride == 2 && t1.pad == 1 && t1.in_c == 3) {
+    if (t2.k == 4 && t1.out_c == 8) return k_pass2_window<4, 2, 1, 4, 8, 3, XW>;
+    if (t2.k == 4 && t1.out_c == 16) return k_pass2_window<4, 2, 1, 4, 16, 3, XW>;
+    if (t2.k == 3 && t1.out_c == 8) return k_pass2_window<4, 2, 1, 3, 8, 3, XW>;
+  }
+  return nullptr;
+}
 
 Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
   if (net->L < 3) return nullptr;
-  if (net->T[1].out_w % kP2XW) return nullptr;
+  if (net->T[1].out_w % 4) return nullptr;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
   if (t1.kind != LIRPA_CONV2D || t2.kind != LIRPA_CONV2D) return nullptr;
   if ((t2.out_c % 16 && t2.out_c != 8) || t1.in_c > 8) return nullptr;
   *nw = t1.in_c;
-  if (t1.k == 4 && t1.stride == 2 && t1.pad == 1) {
-    if (t2.k == 4 && t1.out_c == 8) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 8, 3, kP2XW>;
-    }
-    if (t2.k == 4 && t1.out_c == 16) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 4, 16, 3, kP2XW>;
-    }
-    if (t2.k == 3 && t1.out_c == 8) {
-      if (t1.in_c == 3) return k_pass2_window<4, 2, 1, 3, 8, 3, kP2XW>;
-    }
-  }
-  return nullptr;
+  return p2_xw(net) == 8 ? pass2_kernel_xw<8>(t1, t2) : pass2_kernel_xw<4>(t1, t2);
 }
 
 using Pass2GradKernel = void (*)(DLayer, DLayer, const float*, const float*, long, float,
@@ -4385,7 +4386,7 @@ int pass2_window(const Chunk& c) {
   Pass2Kernel kern = pass2_kernel_for(net, &nw);
   if (!kern) return 1;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
-  long blocks = pass2_blocks(net, c.nb) / kP2XW;
+  long blocks = pass2_blocks(net, c.nb) / p2_xw(net);
   const float* alo = at<float>(c.ws, c.p->off_alo) + net->poff[1];
   const float* aup = at<float>(c.ws, c.p->off_aup) + net->poff[1];
   const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
