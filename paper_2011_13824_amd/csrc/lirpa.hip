@@ -1662,7 +1662,8 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 // layer-1 bias).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
           int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS>
-__global__ void __launch_bounds__(64 * (CI / CPW + NXW)) __attribute__((amdgpu_waves_per_eu(4, 8)))
+__global__ void __launch_bounds__(64 * (CI / CPW + NXW))
+__attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
     k_convT_fc_bound(DLayer t, DLayer t1, const float* __restrict__ in, unsigned ldq, unsigned Q,
                      Sink s, FcSrc fc) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0 && CI % CPW == 0,
@@ -4278,6 +4279,13 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
     if (nbs == 2)
       return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
     return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 3>;
+  }
+  // the Wide shape: 8 matrix waves and 4 x waves, one block per CU (the slab source with three
+  // sub-domains per block would not fit in LDS)
+  if (t1.out_c == 16 && t2.in_c == 16 && t2.out_c == 32 && (fc || nbs == 2)) {
+    *nwaves = 16 / 2 + 4;
+    if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
+    return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
   }
   return nullptr;
 }
