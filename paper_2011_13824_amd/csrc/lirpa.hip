@@ -2876,7 +2876,9 @@ __global__ void __launch_bounds__(64 * NW)
   constexpr int CS = NPOS * 16 + (80 - (NPOS * 16) % 64) % 64;  // channel stride, 16 mod 64
   constexpr int NEL = C1 * CS;
   __shared__ float tile[NEL];
-  __shared__ float dl[NW * WO * WO * 16];  // delta over the footprint, [c0][fy][fx][row]
+  // delta / (-eps) = sign(A_x) over the footprint (0 outside the image), [c0][fy][fx][row]; a
+  // byte per entry keeps the block's LDS small enough for more resident blocks
+  __shared__ signed char dl[NW * WO * WO * 16];
   __shared__ float wrow[16];
   __shared__ int active;
 
@@ -2974,8 +2976,8 @@ __global__ void __launch_bounds__(64 * NW)
       for (int x = 0; x < WO; ++x) {
         const int xi = OX + x;
         const bool in = y >= 0 && y < Hi && xi >= 0 && xi < Wi;
-        const float sv = acc[x] > 0.f ? 1.f : (acc[x] < 0.f ? -1.f : 0.f);
-        dl[((c0 * WO + yl) * WO + x) * 16 + n] = in ? -eps * sv : 0.f;
+        const int sv = acc[x] > 0.f ? 1 : (acc[x] < 0.f ? -1 : 0);
+        dl[((c0 * WO + yl) * WO + x) * 16 + n] = (signed char)(in ? sv : 0);
       }
     };
 #pragma unroll
@@ -3020,9 +3022,10 @@ __global__ void __launch_bounds__(64 * NW)
   }
   __syncthreads();
 
-  // (3) G = z1 + W_1 delta at each window neuron on MFMA (M = 16 channels c1, N = 16 rows,
-  // one K step per (input channel, tap row) with the tap column as the lane group, so the
-  // footprint entry of a K step is uniform per lane group); contributions summed over the rows
+  // (3) G = z1 + W_1 delta = z1 - eps W_1 sign(A_x) at each window neuron, W_1 sign(A_x) on MFMA
+  // (M = 16 channels c1, N = 16 rows, one K step per (input channel, tap row) with the tap
+  // column as the lane group, so the footprint entry of a K step is uniform per lane group);
+  // contributions summed over the rows
   {
     static_assert(K1 == 4, "tap columns are the four lane groups");
     constexpr int NK1 = NW * K1;  // K steps: in_c == NW
@@ -3040,7 +3043,7 @@ __global__ void __launch_bounds__(64 * NW)
 #pragma unroll
       for (int ks = 0; ks < NK1; ++ks) {
         const int cc = ks / K1, ky = ks % K1;
-        const float bv = dl[((cc * WO + j * S1 + ky) * WO + i * S1 + G) * 16 + n];
+        const float bv = (float)dl[((cc * WO + j * S1 + ky) * WO + i * S1 + G) * 16 + n];
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(w1r[ks], bv, d, 0, 0, 0);
       }
 #pragma unroll
@@ -3049,7 +3052,7 @@ __global__ void __launch_bounds__(64 * NW)
         float cval = 0.f;
         if (c1 < C1) {
           const int e = c1 * NPOS + pos;
-          cval = wn * prm[3][e] * tile[c1 * CS + pos * 16 + n] * (d[r] + prm[2][e]);
+          cval = wn * prm[3][e] * tile[c1 * CS + pos * 16 + n] * fmaf(-eps, d[r], prm[2][e]);
         }
         cval += __shfl_xor(cval, 8, 64);
         cval += __shfl_xor(cval, 4, 64);
