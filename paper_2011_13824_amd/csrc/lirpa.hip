@@ -2380,8 +2380,6 @@ __global__ void __launch_bounds__(512)
   constexpr int N1 = W1W * W1W;
   constexpr int E2 = C2 * N2, E1 = C1 * N1;
   constexpr int WO = (W1W - 1) * S1 + K1;   // footprint width on x
-  constexpr int KD2 = C2 * K2 * K2;         // K of the T_2^T gather
-  constexpr int NKS2 = (KD2 + 3) / 4;
   constexpr int KS1 = C1 / 4;
   constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
   constexpr int CS2 = N2 * 16 + (80 - (N2 * 16) % 64) % 64;
@@ -2625,8 +2623,6 @@ __global__ void __launch_bounds__(512)
   constexpr int N1 = W1W * W1W;
   constexpr int E3 = C3 * N3, E2 = C2 * N2, E1 = C1 * N1;
   constexpr int WO = (W1W - 1) * S1 + K1;   // footprint width on x
-  constexpr int KD3 = C3 * K3 * K3, NKS3 = (KD3 + 3) / 4;  // K of the T_3^T gather
-  constexpr int KD2 = C2 * K2 * K2, NKS2 = (KD2 + 3) / 4;  // K of the T_2^T gather
   constexpr int KS1 = C1 / 4;
   constexpr int PER1 = (K1 % S1 == 0) ? K1 / S1 : K1;
   constexpr int CS3 = N3 * 16 + (80 - (N3 * 16) % 64) % 64;
@@ -3488,14 +3484,6 @@ __global__ void __launch_bounds__(256)
       }
     }
   }
-}
-
-// Load of a float at byte offset boff (< 2^31) from the wave-uniform address row (buffer load,
-// base in scalar registers).
-__device__ __forceinline__ float load_row(const float* row, unsigned boff) {
-  const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), (short)0, 0x7fffffff, 0x00020000);
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, boff, 0, 0));
 }
 
 // Sum over each group of 8 consecutive lanes (lanes 8k..8k+7), valid in lanes 8k..8k+3: two
