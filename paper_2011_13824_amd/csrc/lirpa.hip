@@ -257,6 +257,24 @@ __device__ __forceinline__ void sink_finish(const Sink& s, const Acc& acc, long 
   }
 }
 
+// Relaxation of one ReLU neuron with bounds l <= u (Eq. 5 with the split override of Sec. 3.1,
+// checked in the order: split, u <= 0, l >= 0, unstable): lower slope a_lo (alpha when given,
+// else the upper slope), upper line a_up x + b_up, and the stability code (1 split active,
+// 2 split inactive, 3 inactive, 4 active, 5 unstable).
+struct Relax1 {
+  float lo, up, bu;
+  int code;
+};
+__device__ __forceinline__ Relax1 relax_neuron(float l, float u, int sp, const float* alpha) {
+  if (sp > 0) return {1.f, 1.f, 0.f, 1};
+  if (sp < 0) return {0.f, 0.f, 0.f, 2};
+  if (u <= 0.f) return {0.f, 0.f, 0.f, 3};
+  if (l >= 0.f) return {1.f, 1.f, 0.f, 4};
+  const float d = u - l;
+  const float up = u / d;
+  return {alpha ? *alpha : up, up, -(u * l) / d, 5};
+}
+
 // ---------------------------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------------------------
@@ -2132,22 +2150,22 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   sink_finish<MODE_BOUND>(s, a, q, q / R, r, FC);
 }
 
-// The 16 rows +-e_j of a receptive-field pass-2 block share the window (y2, x2) of one
-// sub-domain.  Output channels C2 a multiple of 16: one sign and 16 consecutive channels (block
-// group g = sign * C2/16 + channel block); C2 = 8: both signs of all 8 channels (row r: sign
-// r / 8, channel r % 8).  Blocks are ordered (sub-domain, group, y2, x2), x2 fastest.
+// The 16 rows +-e_j of a receptive-field block share the window (y2, x2) of one sub-domain:
+// both signs of 8 consecutive output channels (block group g: channels 8g .. 8g + 7; row r:
+// sign r / 8, channel 8g + r % 8), so rows r and r + 8 give l and u of one neuron.  C2 is a
+// multiple of 8.  Blocks are ordered (sub-domain, group, y2, x2), x2 fastest.
 struct P2Row {
   int c2;
   bool neg;
 };
 __device__ __forceinline__ P2Row p2_row(int C2, int g, int r) {
-  if (C2 == 8) return {r & 7, r >= 8};
-  const int ncb = C2 / 16;
-  return {(g % ncb) * 16 + r, g >= ncb};
+  (void)C2;
+  return {g * 8 + (r & 7), r >= 8};
 }
-__host__ __device__ inline int p2_groups(int C2) { return C2 == 8 ? 1 : 2 * (C2 / 16); }
+__host__ __device__ inline int p2_groups(int C2) { return C2 / 8; }
 
-// Pass 2 restricted to each row's receptive field, when T_2 and T_1 are convolutions.
+// Pass 2 restricted to each row's receptive field, when T_2 and T_1 are convolutions.  (The
+// kernel also writes the relaxation of layer 2, as k_relax_params would from its bounds.)
 // Row +-e_j of h^(2), j = (c2, y2, x2), carried through T_2 is +-W_2[c2] placed on the window
 // (y2*S2 - P2 + ky2, x2*S2 - P2 + kx2) of g^(1) and zero elsewhere, so its image under the
 // relaxation of layer 1 and T_1^T is confined to that window's footprint on the input.  One
@@ -2163,7 +2181,9 @@ template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
 __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                const float* __restrict__ z1, float eps, float* __restrict__ L,
-               float* __restrict__ U, long n_relu, long off2) {
+               float* __restrict__ U, long n_relu, long off2, const int8_t* __restrict__ split,
+               const float* __restrict__ alpha, float* __restrict__ lo2, float* __restrict__ up2,
+               float* __restrict__ bu2, int8_t* __restrict__ code2) {
   static_assert(C1 % 4 == 0 && K1 <= 4 && K2 <= 4, "unsupported geometry");
   constexpr int KS = C1 / 4;
   constexpr int NT = 64 * NW;
@@ -2179,6 +2199,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   __shared__ float tile[NEL];
   __shared__ float red[NW * 16 + RPT * 16];
   __shared__ float4v prm[NE];  // (a_lo, a_up, b_up, W1 x0 + b1) of the window (0 outside)
+  __shared__ float vb[XW][16];  // the rows' bounds, written out once per block
   float* bred = red + NW * 16;
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -2345,13 +2366,24 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       float ta = 0.f, tb = (pr.neg ? -1.f : 1.f) * t2.b[pr.c2];
       for (int w = 0; w < NW; ++w) ta += red[w * 16 + r];
       for (int q = 0; q < RPT; ++q) tb += bred[q * 16 + r];
-      const float v = tb - eps * ta;
-      const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
-      if (pr.neg)
-        U[b * n_relu + off2 + j] = -v;
-      else
-        L[b * n_relu + off2 + j] = v;
+      vb[xi][r] = tb - eps * ta;
     }
+  }
+  // l and u of the block's 8 neurons in each of its XW windows (rows r and r + 8 are +-e_j of
+  // one neuron), and their relaxation for the passes above: XW consecutive neurons per channel
+  __syncthreads();
+  if (threadIdx.x < 8 * XW) {
+    const int cc = threadIdx.x / XW, xi = threadIdx.x - cc * XW;
+    const long j = ((long)(g * 8 + cc) * H2 + y2) * W2 + x2c * XW + xi;
+    const long pi = b * n_relu + off2 + j;
+    const float l = vb[xi][cc], u = -vb[xi][cc + 8];
+    L[pi] = l;
+    U[pi] = u;
+    const Relax1 rx = relax_neuron(l, u, split ? split[pi] : 0, alpha ? alpha + pi : nullptr);
+    lo2[b * pstride + j] = rx.lo;
+    up2[b * pstride + j] = rx.up;
+    bu2[b * pstride + j] = rx.bu;
+    code2[pi] = (int8_t)rx.code;
   }
 }
 
@@ -3318,31 +3350,13 @@ __global__ void __launch_bounds__(kBlock)
     l[p] = lsh[j];
     u[p] = ush[j];
   }
-  int sp = split ? split[p] : 0;
-  float lo = 0.f, up = 0.f, bu = 0.f;
-  int c;
-  if (sp > 0) {
-    lo = 1.f; up = 1.f; c = 1;
-  } else if (sp < 0) {
-    c = 2;
-  } else {
-    float lj = lsh ? lsh[j] : l[p], uj = ush ? ush[j] : u[p];
-    if (uj <= 0.f) {
-      c = 3;
-    } else if (lj >= 0.f) {
-      lo = 1.f; up = 1.f; c = 4;
-    } else {
-      float d = uj - lj;
-      up = uj / d;
-      bu = -(uj * lj) / d;
-      lo = alpha ? alpha[p] : up;
-      c = 5;
-    }
-  }
-  a_lo[pp] = lo;
-  a_up[pp] = up;
-  b_up[pp] = bu;
-  code[p] = (int8_t)c;
+  const int sp = split ? split[p] : 0;
+  const float lj = lsh ? lsh[j] : l[p], uj = ush ? ush[j] : u[p];
+  const Relax1 r = relax_neuron(lj, uj, sp, alpha ? alpha + p : nullptr);
+  a_lo[pp] = r.lo;
+  a_up[pp] = r.up;
+  b_up[pp] = r.bu;
+  code[p] = (int8_t)r.code;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -3890,7 +3904,8 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 // Kernel for the receptive-field pass 2, or null when the shapes do not qualify.
 using Pass2Kernel = void (*)(DLayer, DLayer, long, const float*, const float*, const float*, long,
-                             const float*, float, float*, float*, long, long);
+                             const float*, float, float*, float*, long, long, const int8_t*,
+                             const float*, float*, float*, float*, int8_t*);
 // Windows per block of the receptive-field pass 2 (along x2): 8 when the map width allows it
 // (fewer blocks, each set-up shared by more windows), else 4.
 int p2_xw(const lirpa_net* net) { return net->T[1].out_w % 8 == 0 ? 8 : 4; }
@@ -4389,10 +4404,14 @@ int pass2_window(const Chunk& c) {
   const float* alo = at<float>(c.ws, c.p->off_alo) + net->poff[1];
   const float* aup = at<float>(c.ws, c.p->off_aup) + net->poff[1];
   const float* bup = at<float>(c.ws, c.p->off_bup) + net->poff[1];
+  const size_t p2 = (size_t)net->poff[2];
   return launch_k(tag("pass2_window", 1, 2), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * nw), 0, c.st, dlayer(t1),
                        dlayer(t2), c.nb, alo, aup, bup, net->pstride,
-                       at<float>(c.ws, c.p->off_z1), c.eps, c.L, c.U, net->n_relu, net->off[2]);
+                       at<float>(c.ws, c.p->off_z1), c.eps, c.L, c.U, net->n_relu, net->off[2],
+                       c.split, c.alpha, at<float>(c.ws, c.p->off_alo) + p2,
+                       at<float>(c.ws, c.p->off_aup) + p2, at<float>(c.ws, c.p->off_bup) + p2,
+                       at<int8_t>(c.ws, c.p->off_code));
   });
 }
 
@@ -4586,8 +4605,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     if (k == 2 && (!c.tape || pass2_grad_kernel_for(net))) {
       int e = pass2_window(c);
       if (e != 1) {
-        if (e) return e;
-        if (int e2 = relax_layer(c, k)) return e2;
+        if (e) return e;  // (the kernel also wrote the relaxation of layer 2)
         continue;
       }
     }
