@@ -214,6 +214,15 @@ struct FcSrc {
   const float* a_lo;  // relaxation of ReLU layer k-1 (per sub-domain, stride Sink::pstride)
   const float* a_up;
   const float* b_up;
+  // k_convT_fc_bound only (rows interleaved: row 2j is +e_j, row 2j + 1 is -e_j): the
+  // relaxation of layer k it writes from the bounds (as k_relax_params would)
+  const int8_t* split;  // per sub-domain, stride n_relu, at the layer's offset off
+  const float* alpha;
+  float* r_lo;          // per sub-domain, stride Sink::pstride
+  float* r_up;
+  float* r_bu;
+  int8_t* code;         // stride n_relu, at offset off
+  long n_relu, off;
 };
 
 struct Acc {
@@ -1802,11 +1811,13 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         const int co = qd % CO, t4 = qd / CO;
         const unsigned qa = q0 + 2u * qp, qb = qa + 1u;
         const unsigned ra = qa % R, rb = qb % R;
-        g_sa[k] = qa < Q ? (ra < nk ? 1.f : -1.f) : 0.f;
-        g_sb[k] = qb < Q ? (rb < nk ? 1.f : -1.f) : 0.f;
+        // rows 2 qp, 2 qp + 1 are +e_j, -e_j of one neuron j (R is even): one row of W_k
+        (void)nk;
+        g_sa[k] = qa < Q ? 1.f : 0.f;
+        g_sb[k] = qb < Q ? -1.f : 0.f;
         const unsigned i0 = (unsigned)co * H1 * W1 + 4u * t4;
-        g_wa[k] = (ra % nk) * nin + i0;
-        g_wb[k] = (rb % nk) * nin + i0;
+        g_wa[k] = (ra >> 1) * nin + i0;
+        g_wb[k] = g_wa[k];
         // R is even, so rows 2 qp and 2 qp + 1 share their sub-domain
         g_pb[k] = (qa < Q ? qa / R : b0) * (unsigned)s.pstride + i0;
         g_bz[k] = t.b[co];
@@ -1819,7 +1830,7 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         if (g_on[k]) {
           const unsigned o = (unsigned)yg * W1;
           g_xa[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wa[k] + o));
-          g_xb[k] = *reinterpret_cast<const float4v*>(fc.W + (g_wb[k] + o));
+          g_xb[k] = g_xa[k];
           g_lo[k] = *reinterpret_cast<const float4v*>(fc.a_lo + (g_pb[k] + o));
           g_up[k] = *reinterpret_cast<const float4v*>(fc.a_up + (g_pb[k] + o));
           g_bu[k] = *reinterpret_cast<const float4v*>(fc.b_up + (g_pb[k] + o));
@@ -2133,21 +2144,40 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   if (NXW > 2 && xw == 2) xrun(std::integral_constant<int, (NXW > 2 ? 2 : 0)>());
   if (NXW > 3 && xw == 3) xrun(std::integral_constant<int, (NXW > 3 ? 3 : 0)>());
   lds_barrier();
-  if (xw != 0 || lane >= 16 || q >= Q) return;
+  if (xw != 0 || lane >= 16) return;
   // FC: the row's own bias +-b_k[j] and the terms of the relaxation onto layer 2 (slab: the
   // running bias, added by sink_finish); the terms of the relaxation onto layer 1
   const unsigned r = q % R;
   float tb = 0.f;
   if constexpr (FC) {
-    const unsigned nk = (unsigned)fc.nk;
-    tb = r < nk ? fc.b[r] : -fc.b[r - nk];
+    const float bj = fc.b[(r >> 1) % (unsigned)fc.nk];
+    tb = (r & 1) ? -bj : bj;
     for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
   }
   for (int w = 0; w < NXW; ++w) tb += red[NM * 16 + w * 16 + lane];
   float ta = 0.f;
   for (int w = 0; w < NXW; ++w) ta += red[NM * 16 + (NXW + w) * 16 + lane];
-  Acc a{tb, 0.f, ta};
-  sink_finish<MODE_BOUND>(s, a, q, q / R, r, FC);
+  if constexpr (FC) {
+    // rows 2j, 2j + 1 (lanes 2i, 2i + 1) give l_j and -u_j; then the relaxation of layer k
+    const float v = tb - s.eps * ta;
+    const float vn = __shfl_xor(v, 1, 64);
+    if (q >= Q || (r & 1)) return;  // (Q is even: row q + 1 exists)
+    const unsigned b = q / R, jj = r >> 1;
+    s.lo[b * s.bstride + jj] = v;
+    s.hi[b * s.bstride + jj] = -vn;
+    const long pi = (long)b * fc.n_relu + fc.off + jj;
+    const Relax1 rx = relax_neuron(v, -vn, fc.split ? fc.split[pi] : 0,
+                                   fc.alpha ? fc.alpha + pi : nullptr);
+    const long pp = (long)b * s.pstride + jj;
+    fc.r_lo[pp] = rx.lo;
+    fc.r_up[pp] = rx.up;
+    fc.r_bu[pp] = rx.bu;
+    fc.code[pi] = (int8_t)rx.code;
+  } else {
+    if (q >= Q) return;
+    Acc a{tb, 0.f, ta};
+    sink_finish<MODE_BOUND>(s, a, q, q / R, r, false);
+  }
 }
 
 // The 16 rows +-e_j of a receptive-field block share the window (y2, x2) of one sub-domain:
@@ -4543,12 +4573,21 @@ int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   s.hi = sb.hi;
   s.bstride = sb.bstride;
   s.n_half = sb.n_half;
-  FcSrc f{fl.W,
-          fl.b,
-          (int)net->n[k],
-          at<float>(c.ws, c.p->off_alo) + net->poff[k - 1],
-          at<float>(c.ws, c.p->off_aup) + net->poff[k - 1],
-          at<float>(c.ws, c.p->off_bup) + net->poff[k - 1]};
+  FcSrc f{};
+  f.W = fl.W;
+  f.b = fl.b;
+  f.nk = (int)net->n[k];
+  f.a_lo = at<float>(c.ws, c.p->off_alo) + net->poff[k - 1];
+  f.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[k - 1];
+  f.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[k - 1];
+  f.split = c.split;
+  f.alpha = c.alpha;
+  f.r_lo = at<float>(c.ws, c.p->off_alo) + net->poff[k];
+  f.r_up = at<float>(c.ws, c.p->off_aup) + net->poff[k];
+  f.r_bu = at<float>(c.ws, c.p->off_bup) + net->poff[k];
+  f.code = at<int8_t>(c.ws, c.p->off_code);
+  f.n_relu = net->n_relu;
+  f.off = net->off[k];
   const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
   return launch_k(tag("convT_fc_bound", k - 1, k), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[k - 2]),
@@ -4628,8 +4667,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     if (!c.tape) {
       int e = fc_bound_stage(c, k, R, Q);
       if (e != 1) {
-        if (e) return e;
-        if (int e2 = relax_layer(c, k)) return e2;
+        if (e) return e;  // (the kernel also wrote the relaxation of layer k)
         continue;
       }
     }
