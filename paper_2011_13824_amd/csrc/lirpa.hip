@@ -182,6 +182,11 @@ __device__ __forceinline__ void lds_barrier() {
 //              relaxed coefficients over h^(1)), A x0 + A1 b1 = A1 (W1 x0 + b1), so the
 //              relaxation onto layer 1 dots A1 with z1 = W1 x0 + b1 instead of with b1
 //              (bias_hw == 1 then means a per-neuron bias vector).
+// Sign of a coefficient as stored in the gradient tape over x: -1, 0 or +1.
+__device__ __forceinline__ int8_t sign8(float a) {
+  return (int8_t)(a > 0.f ? 1 : (a < 0.f ? -1 : 0));
+}
+
 struct Sink {
   float* out;
   long ldq;
@@ -199,7 +204,10 @@ struct Sink {
   float* hi;
   long bstride;
   long n_half;
-  float* tape;  // optional: the coefficient before relaxation (or over x), [i*ldq + q]
+  float* tape;  // optional: the coefficient before relaxation (relaxing stages), [i*ldq + q]
+  // optional (concretising stages): the sign of the coefficient over x, the only part of it
+  // the witness x* = x0 - eps sign(A_x) of the gradient needs, one byte per entry [i*ldq + q]
+  int8_t* tsign;
 };
 
 // Input of the first backward stage of a pass that starts at a fully connected layer k (rows
@@ -232,7 +240,11 @@ struct Acc {
 template <int MODE>
 __device__ __forceinline__ void sink_put(const Sink& s, Acc& acc, long i, float a, long q,
                                          long b) {
-  if (s.tape) s.tape[i * s.ldq + q] = a;
+  if constexpr (MODE == MODE_SLAB) {
+    if (s.tape) s.tape[i * s.ldq + q] = a;
+  } else {
+    if (s.tsign) s.tsign[i * s.ldq + q] = sign8(a);
+  }
   if constexpr (MODE == MODE_SLAB) {
     long pi = b * s.pstride + i;
     float ah;
@@ -274,6 +286,7 @@ struct Relax1 {
   float lo, up, bu;
   int code;
 };
+
 __device__ __forceinline__ Relax1 relax_neuron(float l, float u, int sp, const float* alpha) {
   if (sp > 0) return {1.f, 1.f, 0.f, 1};
   if (sp < 0) return {0.f, 0.f, 0.f, 2};
@@ -712,14 +725,14 @@ k_convT_mfma(DLayer t, const float* __restrict__ in, unsigned ldq, unsigned Q, S
 #pragma unroll
         for (int x = 0; x < W0; ++x) {
           const float a = vals[x];
-          if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = a;
+          if constexpr (TAPE) s.tsign[(rowi + x) * ldq + q] = sign8(a);
           lin = fmaf(a, xs[rowi + x], lin);
           l1 += fabsf(a);
         }
       } else {
 #pragma unroll
         for (int x = 0; x < W0; ++x) {
-          if constexpr (TAPE) s.tape[(rowi + x) * ldq + q] = vals[x];
+          if constexpr (TAPE) s.tsign[(rowi + x) * ldq + q] = sign8(vals[x]);
           l1 += fabsf(vals[x]);
         }
       }
@@ -3242,7 +3255,11 @@ __global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* 
           const int i = mt * 32 + 8 * g + 4 * h + e;
           if (i >= nin) continue;
           const float a = d[4 * g + e];
-          if (s.tape) s.tape[(long)i * s.ldq + q] = a;
+          if constexpr (MODE == MODE_SLAB) {
+            if (s.tape) s.tape[(long)i * s.ldq + q] = a;
+          } else {
+            if (s.tsign) s.tsign[(long)i * s.ldq + q] = sign8(a);
+          }
           if constexpr (MODE == MODE_SLAB) {
             const float ah = a * (a >= 0.f ? p0[g][e] : p1[g][e]);
             sum.beta = fmaf(fminf(a, 0.f), p2[g][e], sum.beta);
@@ -3416,53 +3433,11 @@ __global__ void __launch_bounds__(kBlock) k_row_weights(long Q, long R, long nP,
 // that function is the network with each ReLU replaced, per row, by the line the backward pass
 // chose for it (lower line where the row's coefficient was >= 0, upper line otherwise).
 // G = W_m z + b_m is the pre-activation along that network; z_out = chosen line applied to G.
-// WITNESS: the input z is built on the fly from the tape of A_x.
-template <bool WITNESS>
-__global__ void __launch_bounds__(kBlock)
-    k_fwd(DLayer t, const float* __restrict__ zin, long ldq, long Q, long R,
-          const float* __restrict__ w, const float* __restrict__ x0, float eps,
-          const float* __restrict__ tape, const float* __restrict__ a_lo,
-          const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
-          float* __restrict__ G, float* __restrict__ zout) {
-  long q = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (q >= Q || w[q] == 0.f) return;
-  long b = q / R;
-  auto in = [&](long i) -> float {
-    float v = zin[i * ldq + q];
-    if constexpr (WITNESS) return x0[i] - eps * (v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f));
-    return v;
-  };
-  const int hw = t.out_h * t.out_w;
-  const long nout = (long)t.out_c * hw;
-  for (long o = 0; o < nout; ++o) {
-    float g = t.b[o / hw];
-    if (t.kind == LIRPA_LINEAR) {
-      for (int i = 0; i < t.in_c; ++i) g = fmaf(t.W[o * t.in_c + i], in(i), g);
-    } else {
-      int co = (int)(o / hw), yo = (int)((o / t.out_w) % t.out_h), xo = (int)(o % t.out_w);
-      for (int ci = 0; ci < t.in_c; ++ci)
-        for (int ky = 0; ky < t.k; ++ky) {
-          int yi = yo * t.stride - t.pad + ky;
-          if (yi < 0 || yi >= t.in_h) continue;
-          for (int kx = 0; kx < t.k; ++kx) {
-            int xi = xo * t.stride - t.pad + kx;
-            if (xi < 0 || xi >= t.in_w) continue;
-            g = fmaf(t.W[(((long)co * t.in_c + ci) * t.k + ky) * t.k + kx],
-                     in(((long)ci * t.in_h + yi) * t.in_w + xi), g);
-          }
-        }
-    }
-    G[o * ldq + q] = g;
-    if (zout) {
-      long pi = b * pstride + o;
-      float tv = tape[o * ldq + q];
-      zout[o * ldq + q] = tv >= 0.f ? a_lo[pi] * g : fmaf(a_up[pi], g, b_up[pi]);
-    }
-  }
-}
-
-// The same forward step on 16x16x4 MFMA, for conv and linear layers alike (a linear layer is
-// a 1x1 convolution on a 1x1 map): implicit GEMM with M = 16 output channels co, N = 16 rows q
+// WITNESS: the input z is built on the fly from the sign tape of A_x; the input pointer then
+// holds one int8_t sign per entry, [i][ldq].
+//
+// On 16x16x4 MFMA, for conv and linear layers alike (a linear layer is a 1x1 convolution on a
+// 1x1 map): implicit GEMM with M = 16 output channels co, N = 16 rows q
 // and K = (ci, ky, kx), four per instruction.  Block: 16 rows x 4 waves; output positions are
 // dealt round-robin to the waves.  A block whose 16 rows all carry weight 0 exits at once.
 template <bool WITNESS>
@@ -3503,11 +3478,10 @@ __global__ void __launch_bounds__(256)
           const int yi = yb + ky, xi = xb + kx;
           if (yi >= 0 && yi < Hin && xi >= 0 && xi < Win) {
             const unsigned ii = ((unsigned)ci * Hin + yi) * Win + xi;
-            const float v = zin[ii * ldq + q];
             if constexpr (WITNESS)
-              bv = x0[ii] - eps * (v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f));
+              bv = x0[ii] - eps * (float)reinterpret_cast<const int8_t*>(zin)[(size_t)ii * ldq + q];
             else
-              bv = v;
+              bv = zin[ii * ldq + q];
           }
         }
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, d, 0, 0, 0);
@@ -3656,6 +3630,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
 
   // input rows ybase .. ybase+S-1 into registers (float4 e = (row j, ci, x, quarter of q))
   auto slot_of = [](int yi) { return (yi + 8 * NSLOT) % NSLOT; };
+  // (WITNESS: the four rows' signs of the sign tape, one 32-bit word, in pf[k][0])
   float4v pf[PFT];
   auto fetch_rows = [&](int ybase) {
 #pragma unroll
@@ -3665,9 +3640,14 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       if (e < NF4) {
         const int j4 = e & 3, fr = e >> 2;
         const int xi = fr % WI, ci = (fr / WI) % CI, yi = ybase + fr / (WI * CI);
-        if (yi >= 0 && yi < HI)
-          pf[k] = *reinterpret_cast<const float4v*>(
-              zin + (size_t)(((unsigned)ci * HI + yi) * WI + xi) * ldq + q0 + 4 * j4);
+        if (yi >= 0 && yi < HI) {
+          const size_t at = (size_t)(((unsigned)ci * HI + yi) * WI + xi) * ldq + q0 + 4 * j4;
+          if constexpr (WITNESS)
+            pf[k][0] = __builtin_bit_cast(
+                float, *reinterpret_cast<const int*>(reinterpret_cast<const int8_t*>(zin) + at));
+          else
+            pf[k] = *reinterpret_cast<const float4v*>(zin + at);
+        }
       }
     }
   };
@@ -3683,9 +3663,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
         if constexpr (WITNESS) {
           if (yi >= 0 && yi < HI) {
             const float xv = xs[((unsigned)ci * HI + yi) * WI + xi];
+            const int sw = __builtin_bit_cast(int, pf[k][0]);
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj)
-              v[jj] = xv - eps * (v[jj] > 0.f ? 1.f : (v[jj] < 0.f ? -1.f : 0.f));
+              v[jj] = xv - eps * (float)(int8_t)(sw >> (8 * jj));
           }
         }
         *reinterpret_cast<float4v*>(ring + ((slot_of(yi) * CI + ci) * XW + xi + P) * 16 + 4 * j4) =
@@ -4040,8 +4021,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
         continue;
       }
       for (int m = 0; m <= k - 1; ++m) {
-        p.off_tape[k][m] = o;
-        o = align256(o + (size_t)net->n[m] * qp * 4);
+        p.off_tape[k][m] = o;  // over x: signs, one byte per entry
+        o = align256(o + (size_t)net->n[m] * qp * (m == 0 ? 1 : 4));
         if (m >= 1) fwd = std::max(fwd, net->n[m] * qp);
       }
     }
@@ -4210,7 +4191,8 @@ int launch_stage(const lirpa_net* net, int m, int pass, const float* in, long ld
       }
     }
   }
-  if (ConvTKernel<MODE> kern = convT_mfma_for<MODE>(t, s.tape != nullptr, &nw)) {
+  const bool tape = MODE == MODE_SLAB ? s.tape != nullptr : s.tsign != nullptr;
+  if (ConvTKernel<MODE> kern = convT_mfma_for<MODE>(t, tape, &nw)) {
     const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
     const size_t cs = (size_t)t.out_w * 16 + (80 - (t.out_w * 16) % 64) % 64;
     // x0 is staged in LDS only when the linear term is not folded into the layer-1 bias
@@ -4294,6 +4276,10 @@ int relax_layer(const Chunk& c, int m, const float* lsh = nullptr, const float* 
 // spec rows when mtop == L), ending with the concretisation into (lo, hi).
 float* tape_of(const Chunk& c, int pass, int m) {
   return c.tape ? at<float>(c.ws, c.p->off_tape[pass][m]) : nullptr;
+}
+// the pass's sign tape over x (one byte per entry, in the place of its tape over layer 0)
+int8_t* tsign_of(const Chunk& c, int pass) {
+  return c.tape ? at<int8_t>(c.ws, c.p->off_tape[pass][0]) : nullptr;
 }
 
 // k_convT_fc_bound for layers 1 and 2 of the net when they are convolutions of a covered
@@ -4415,7 +4401,7 @@ int run_stages(const Chunk& c, int pass, int mtop, long R, long Q, long ldq, flo
     } else {
       Sink s = bound_sink(c, R, lo, hi, bstride, n_half);
       s.ldq = ldq;
-      s.tape = tape_of(c, pass, 0);
+      s.tsign = tsign_of(c, pass);
       e = launch_stage<MODE_BOUND>(c.net, m, pass, slab[cur], ldq, Q, s, c.st);
     }
     if (e) return e;
@@ -4836,7 +4822,9 @@ int grad_chunk(const Chunk& c, int full) {
                              net->n_relu, offP, (int)(P == L), gl, gu, w);
         }))
       return e;
-    const float* zin = tape_of(c, P, 0);
+    // the first layer's input is the witness, built from the pass's sign tape (bytes; the
+    // forward kernels with WITNESS read their input pointer as int8_t)
+    const float* zin = reinterpret_cast<const float*>(tsign_of(c, P));
     float* zbuf[2] = {za, zb};
     for (int m = 1; m <= P - 1; ++m) {
       const float* tp = tape_of(c, P, m);
