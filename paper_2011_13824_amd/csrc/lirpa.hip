@@ -1710,6 +1710,7 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
                 "geometry");
   static_assert(K1 <= 4 && S1 <= K1 && W1 % 4 == 0, "geometry");
   static_assert((H1 - 1) * S - P + K >= H0, "every output row is reached by an input row");
+  static_assert((W1 - 1) * S - P + K >= W0 && P < K, "every output column is reached");
   static_assert((H0 - 1) * S1 - P1 + K1 >= HX, "every input row of T_1 is reached");
   constexpr int NM = CI / CPW;                   // matrix waves
   constexpr int NTM = 64 * NM;
@@ -2350,12 +2351,13 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
     }
     __syncthreads();
 
-    // (2) T_1^T on the window
+    // (2) T_1^T on the window.  A lane's row of acc restarts after the lane emits it: the
+    // first contribution of the next window row to each column then scales the old value by
+    // keep = 0 (instead of clearing the row; every column is reached in every window row).
     const int OX = X1 * S1 - P1;
     float l1 = 0.f;
     float acc[WO];
-#pragma unroll
-    for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+    float keep = 1.f;
     const bool inside_x = OX >= 0 && OX + WO <= Wi;
     auto emit = [&](int yl) {  // local footprint row yl of channel c0: ||.||_1 of the clipped row
       const int y = OY + yl;
@@ -2384,14 +2386,20 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
                                                   tile[(4 * ks + G) * CS + pos * 16 + n], d,
                                                   0, 0, 0);
 #pragma unroll
-        for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
+        for (int kx = 0; kx < K1; ++kx) {
+          float& a = acc[i * S1 + kx];
+          if (i > 0 && kx < K1 - S1)
+            a += d[kx];
+          else if (j == 0)
+            a = d[kx];
+          else
+            a = fmaf(a, keep, d[kx]);
+        }
       }
       const int ky = ((G - ph * S1) % K1 + K1) % K1;
-      if (G < K1 && ky < S1) {
-        emit(j * S1 + ky);
-#pragma unroll
-        for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-      }
+      const bool done = G < K1 && ky < S1;
+      if (done) emit(j * S1 + ky);
+      keep = done ? 0.f : 1.f;
     }
     {
       const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
@@ -3286,7 +3294,8 @@ __global__ void __launch_bounds__(64 * NWAVE) k_fcT_mfma(DLayer t, const float* 
 //      results are relaxed onto layer L-2 and stored into the slab, with their terms.
 // The rows' bias goes to Sink::beta (the pass's first stage).  lo1/up1/bu1/bias1: the
 // relaxation of layer L-1; s: that of layer L-2 and the slab.
-template <int NW>
+// NK = ceil(n_{L-1} / 4) k-steps.
+template <int NW, int NK>
 __global__ void __launch_bounds__(64 * NW)
     k_final_fc(DLayer tM, const float* __restrict__ wsp, int S, long nb, long Q,
                const float* __restrict__ lo1, const float* __restrict__ up1,
@@ -3319,34 +3328,37 @@ __global__ void __launch_bounds__(64 * NW)
     red[threadIdx.x] = beta;
   }
   __syncthreads();
-  // (2)
+  // (2) A tile's operands are loaded at once: the column of W_{L-1} (one entry per k-step;
+  // entries j >= n_{L-1} read a clamped row and meet zeros of the LDS tile) and the four
+  // neurons' relaxation as float4.
   const int n = lane & 15, G = lane >> 4;
   const long q = q0 + n;
   const long b = (q < Q ? q : Q - 1) / S;
   const long pb = b * s.pstride;
   float beta = 0.f;
-  const int nk = KP / 4;
-  for (int mt = wave; mt * 16 < ni; mt += NW) {
-    const int ia = mt * 16 + n;  // A operand: feature i of this lane, K index G
+  struct Ops {
+    float a[NK];
+    float4v lo, up, bu, bz;
+  };
+  auto load = [&](int mt, Ops& o) {
+    const int ia = min(mt * 16 + n, ni - 1);
+    const float* w = tM.W + (long)G * ni + ia;
+    // 4 k + G < 4 (NK - 1) < n_{L-1} for k < NK - 1
+#pragma unroll
+    for (int k = 0; k < NK - 1; ++k) o.a[k] = w[(long)4 * k * ni];
+    o.a[NK - 1] = tM.W[(long)min(4 * (NK - 1) + G, nj - 1) * ni + ia];
+    // within the padded segment round_up(ni, 4); a clamped quad has no neuron i < ni
+    const long i0 = min(mt * 16 + 4 * G, ((ni + 3) & ~3) - 4);
+    o.lo = *reinterpret_cast<const float4v*>(s.a_lo + pb + i0);
+    o.up = *reinterpret_cast<const float4v*>(s.a_up + pb + i0);
+    o.bu = *reinterpret_cast<const float4v*>(s.b_up + pb + i0);
+    o.bz = *reinterpret_cast<const float4v*>(s.bias + i0);
+  };
+  auto compute = [&](int mt, const Ops& o) {
     float4v d = {0.f, 0.f, 0.f, 0.f};
-    int k = 0;
-    for (; k + 8 <= nk; k += 8) {
-      float a[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = 4 * (k + u) + G;
-        a[u] = (j < nj && ia < ni) ? tM.W[(long)j * ni + ia] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], tile[(4 * (k + u) + G) * 16 + n], d, 0,
-                                                 0, 0);
-    }
-    for (; k < nk; ++k) {
-      const int j = 4 * k + G;
-      const float a = (j < nj && ia < ni) ? tM.W[(long)j * ni + ia] : 0.f;
-      d = __builtin_amdgcn_mfma_f32_16x16x4f32(a, tile[j * 16 + n], d, 0, 0, 0);
-    }
+    for (int k = 0; k < NK; ++k)
+      d = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[k], tile[(4 * k + G) * 16 + n], d, 0, 0, 0);
     // lane holds features i0 .. i0 + 3 of row q
     const int i0 = mt * 16 + 4 * G;
 #pragma unroll
@@ -3354,12 +3366,18 @@ __global__ void __launch_bounds__(64 * NW)
       const int i = i0 + r;
       if (i < ni) {
         const float a = d[r];
-        const float ah = a * (a >= 0.f ? s.a_lo[pb + i] : s.a_up[pb + i]);
-        beta = fmaf(fminf(a, 0.f), s.b_up[pb + i], beta);
-        beta = fmaf(ah, s.bias[i], beta);
+        const float ah = a * (a >= 0.f ? o.lo[r] : o.up[r]);
+        beta = fmaf(fminf(a, 0.f), o.bu[r], beta);
+        beta = fmaf(ah, o.bz[r], beta);
         s.out[(long)i * s.ldq + q] = ah;
       }
     }
+  };
+  const int ntile = (ni + 15) / 16;
+  for (int mt = wave; mt < ntile; mt += NW) {
+    Ops o;
+    load(mt, o);
+    compute(mt, o);
   }
   // (2)'s terms per row: over the lane groups, then over the waves in order; (1)'s: over the
   // threads of the row in order
@@ -4694,10 +4712,21 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     Sink s = slab_sink(c, L - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
     const long nj = net->n[L - 1];
     const size_t lds = (size_t)(((nj + 3) & ~3L) * 16 + NW * 64 + NW * 16) * sizeof(float);
-    if (lds <= 65536) {
+    // k-steps of the kernel: ceil(n_{L-1} / 4) for the instantiated sizes
+    auto fkern = [&]() -> void (*)(DLayer, const float*, int, long, long, const float*,
+                                   const float*, const float*, const float*, Sink) {
+      switch ((nj + 3) / 4) {
+        case 8: return k_final_fc<NW, 8>;
+        case 16: return k_final_fc<NW, 16>;
+        case 25: return k_final_fc<NW, 25>;
+        case 32: return k_final_fc<NW, 32>;
+        default: return nullptr;
+      }
+    };
+    if (lds <= 65536 && fkern()) {
       const size_t po = (size_t)net->poff[L - 1];
       if (int e = launch_k(tag("final_fc", L - 1, L), c.st, [&] {
-            hipLaunchKernelGGL(k_final_fc<NW>, dim3((unsigned)((Q + 15) / 16)), dim3(64 * NW),
+            hipLaunchKernelGGL(fkern(), dim3((unsigned)((Q + 15) / 16)), dim3(64 * NW),
                                lds, c.st, dlayer(net->T[L - 2]),
                                at<float>(c.ws, c.p->off_wsp), (int)c.S, c.nb,
                                Q, at<float>(c.ws, c.p->off_alo) + po,
