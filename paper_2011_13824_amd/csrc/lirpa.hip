@@ -2052,17 +2052,23 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   };
   // relaxation and T_1^T of row y over g^(1): coefficients in `row`, relaxation in `prm`
   // ([CI][W0] float4 with channel stride PCS4, at this lane's sub-domain)
-  auto consume = [&](const float* row, const float4v* prm, int y, int par) {
-    const int ph = y % PER1;
+  // (phc: the phase y mod PER1 when it is a compile-time constant, else -1)
+  auto consume = [&](const float* row, const float4v* prm, int y, int par, auto phc) {
+    constexpr int PHC = decltype(phc)::value;
+    const int ph = PHC >= 0 ? PHC : y % PER1;
     float wa[C0][KS1];
 #pragma unroll
     for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
       for (int ks = 0; ks < KS1; ++ks) {
-        wa[c0][ks] = wreg1[0][c0][ks];
+        if constexpr (PHC >= 0) {
+          wa[c0][ks] = wreg1[PHC][c0][ks];
+        } else {
+          wa[c0][ks] = wreg1[0][c0][ks];
 #pragma unroll
-        for (int p2 = 1; p2 < PER1; ++p2)
-          if (ph == p2) wa[c0][ks] = wreg1[p2][c0][ks];
+          for (int p2 = 1; p2 < PER1; ++p2)
+            if (ph == p2) wa[c0][ks] = wreg1[p2][c0][ks];
+        }
       }
     // Three columns in flight: the LDS reads of column x1 + 2 (into buffer x1 & 1), the MFMAs
     // of x1 and the relaxation of x1 + 1, whose reads were issued a column earlier.  The
@@ -2128,11 +2134,20 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
       const int e = st - 1;
       const float* slot = ring[e & 1];
       const int nr = nrows(e);
-      for (int r = 0; r < nr; ++r) {
+      // row r of a step has y = (multiple of S) - P + r: its phase is fixed when PER1 | S
+      auto row_r = [&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        constexpr int PHC = S % PER1 == 0 ? ((r - P) % PER1 + PER1) % PER1 : -1;
         const int y = yrow(e, r);
-        if (y >= 0 && y < H0)
-          consume(slot + r * ROWF, pars[e & 1] + bsel * PBS4 + r * CI * PCS4, y, st & 1);
-      }
+        if (r < nr && y >= 0 && y < H0)
+          consume(slot + r * ROWF, pars[e & 1] + bsel * PBS4 + r * CI * PCS4, y, st & 1,
+                  std::integral_constant<int, PHC>());
+      };
+      static_assert(RSL <= 4, "rows per step");
+      row_r(std::integral_constant<int, 0>());
+      if constexpr (RSL > 1) row_r(std::integral_constant<int, 1>());
+      if constexpr (RSL > 2) row_r(std::integral_constant<int, 2>());
+      if constexpr (RSL > 3) row_r(std::integral_constant<int, 3>());
     }
     lds_barrier();
   }
