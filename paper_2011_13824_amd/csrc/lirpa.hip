@@ -2949,13 +2949,16 @@ __global__ void __launch_bounds__(512)
 // sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
 // the layer-1 relaxation and G_r the layer-1 pre-activation at the row's witness
 // x* = x0 + delta, delta = -eps sign(A_x) (zero outside the footprint), i.e.
-// G_r = z1 + W_1 delta over the window.  One block per 16 rows sharing a window (as in
-// k_pass2_window): it rebuilds the relaxed patch and A_x over the footprint on MFMA, keeps delta
-// in LDS, runs the layer-1 forward over the window on MFMA, reduces the 16 rows' contributions
-// per window neuron and writes them to part[block][c1][pos].  Row weights: w = g_l (sign +) or
-// -g_u (sign -) of the row's layer-2 neuron.
-template <int K1, int S1, int P1, int K2, int C1, int NW>
-__global__ void __launch_bounds__(64 * NW)
+// G_r = z1 + W_1 delta over the window.  A block takes the 16 rows of k_pass2_window (one
+// sub-domain, eight channels, both signs) in XW consecutive windows along x2; per window it
+// rebuilds the relaxed patch and A_x over the footprint on MFMA, keeps delta in LDS, runs the
+// layer-1 forward over the window on MFMA, reduces the 16 rows' contributions per window neuron
+// and writes them to part[window][c1][pos] (windows numbered (b, group, y2, x2)).  The weights
+// are loaded once per block and the next window's relaxation while this one is computed.  Row
+// weights: w = g_l (sign +) or -g_u (sign -) of the row's layer-2 neuron; a window none of whose
+// rows carries weight writes zeros.
+template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 3 : 4, 8)))
     k_pass2_window_grad(DLayer t1, DLayer t2, const float* __restrict__ a_lo,
                         const float* __restrict__ a_up, long pstride, float eps,
                         const float* __restrict__ gl, const float* __restrict__ gu,
@@ -2965,90 +2968,68 @@ __global__ void __launch_bounds__(64 * NW)
   constexpr int KS = C1 / 4;
   constexpr int NT = 64 * NW;
   constexpr int NPOS = K2 * K2;
+  constexpr int NE = C1 * NPOS;                      // window entries
   constexpr int WO = (K2 - 1) * S1 + K1;
   constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
   constexpr int CS = NPOS * 16 + (80 - (NPOS * 16) % 64) % 64;  // channel stride, 16 mod 64
   constexpr int NEL = C1 * CS;
+  constexpr int RPT = NT / 16;                       // threads per row in the tile fills
+  constexpr int NEP = (NE + RPT - 1) / RPT;          // tile entries per thread
+  constexpr int NPP = (NE + NT - 1) / NT;            // staged window entries per thread
+  static_assert(16 * XW <= NT, "row weights of the block's windows");
   __shared__ float tile[NEL];
   // delta / (-eps) = sign(A_x) over the footprint (0 outside the image), [c0][fy][fx][row]; a
-  // byte per entry keeps the block's LDS small enough for more resident blocks
+  // byte per entry keeps the block's LDS small
   __shared__ signed char dl[NW * WO * WO * 16];
-  __shared__ float wrow[16];
-  __shared__ int active;
+  __shared__ float wrow[XW][16];
+  __shared__ float4v prm[NE];  // a_lo, a_up, z1, unstable (1/0) of the window (0 outside)
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   const int H2 = t2.out_h, W2 = t2.out_w, C2 = t2.out_c;
   const int NG = p2_groups(C2);
-  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
-  const long blk_id = blk;
-  const int x2 = (int)(blk % (unsigned)W2); blk /= (unsigned)W2;
+  const int nxc = W2 / XW;
+  unsigned blk = xcd_range(blockIdx.x);  // 32-bit: the scalar divisions stay short
+  const int x2c = (int)(blk % (unsigned)nxc); blk /= (unsigned)nxc;
   const int y2 = (int)(blk % (unsigned)H2); blk /= (unsigned)H2;
   const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
   const long b = blk;
-  const int Y1 = y2 * t2.stride - t2.pad, X1 = x2 * t2.stride - t2.pad;
+  const long win0 = ((b * NG + g) * H2 + y2) * W2 + (long)x2c * XW;  // first window's number
+  const int Y1 = y2 * t2.stride - t2.pad;
   const int H1 = t1.out_h, Wd1 = t1.out_w;
-  float* out = part + blk_id * (long)(C1 * NPOS);
+  const long pb = b * pstride;
 
-  if (threadIdx.x < 16) {
-    const P2Row pr = p2_row(C2, g, threadIdx.x);
-    const long j = ((long)pr.c2 * H2 + y2) * W2 + x2;
-    const float wv = pr.neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
-    wrow[threadIdx.x] = wv;
-  }
-  if (threadIdx.x == 0) active = 0;
-  __syncthreads();
-  if (threadIdx.x < 16 && wrow[threadIdx.x] != 0.f) active = 1;
-  __syncthreads();
-  if (!active) {  // no row of this block carries weight: zero contributions
-    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) out[e] = 0.f;
-    return;
+  if (threadIdx.x < 16 * XW) {
+    const int xi = threadIdx.x >> 4, r = threadIdx.x & 15;
+    const P2Row pr = p2_row(C2, g, r);
+    const long j = ((long)pr.c2 * H2 + y2) * W2 + x2c * XW + xi;
+    wrow[xi][r] = pr.neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
   }
 
-  // (1) relaxed window coefficients (as in the bound; window parameters staged once), and per
-  // window neuron z1 and whether it is unstable (zeros outside the map)
-  __shared__ float prm[4][C1 * NPOS];  // a_lo, a_up, z1, unstable (1/0)
+  // this thread's entries of W_2 for the tile fills (row = tid mod 16, entries part,
+  // part + RPT, ...), signed by the row, the same for every window
+  const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
+  float wv[NEP];
   {
-    const long pb = b * pstride;
-    for (int e = threadIdx.x; e < C1 * NPOS; e += NT) {
-      const int c1 = e / NPOS, pos = e - c1 * NPOS;
-      const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
-      const int y1 = Y1 + ky2, x1 = X1 + kx2;
-      float lo = 0.f, up = 0.f, zz = 0.f, un = 0.f;
-      if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
-        const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
-        lo = a_lo[pb + ni];
-        up = a_up[pb + ni];
-        zz = z1[ni];
-        un = code1[b * n_relu + ni] == 5 ? 1.f : 0.f;
-      }
-      prm[0][e] = lo;
-      prm[1][e] = up;
-      prm[2][e] = zz;
-      prm[3][e] = un;
-    }
-  }
-  __syncthreads();
-  {
-    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
     const P2Row pr = p2_row(C2, g, row);
     const float sgn = pr.neg ? -1.f : 1.f;
-    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;
-    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
-      const int c1 = e / NPOS, pos = e - c1 * NPOS;
-      const float w = sgn * w2[e];
-      tile[c1 * CS + pos * 16 + row] = w >= 0.f ? w * prm[0][e] : w * prm[1][e];
+    const float* w2 = t2.W + (long)pr.c2 * NE;
+#pragma unroll
+    for (int k = 0; k < NEP; ++k) {
+      const int e = partid + k * RPT;
+      wv[k] = e < NE ? sgn * w2[e] : 0.f;
     }
   }
-  __syncthreads();
-
-  // (2) A_x over the footprint; delta = -eps sign(A_x) into LDS (0 outside the image)
+  auto toff = [&](int k) {  // tile place of the thread's entry k
+    const int e = partid + k * RPT;
+    const int c1 = e / NPOS, pos = e - c1 * NPOS;
+    return c1 * CS + pos * 16 + row;
+  };
+  // T_1^T weights (step 2), one wave per input channel c0 of T_1
   const int c0 = wave;
   const bool cok = c0 < t1.in_c;
-  const int Hi = t1.in_h, Wi = t1.in_w;
-  const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
+  float wreg[PER][KS];
   {
-    float wreg[PER][KS];
     const int M = lane & 15, slot = M >> 2, kx = M & 3;
 #pragma unroll
     for (int ph = 0; ph < PER; ++ph) {
@@ -3060,101 +3041,158 @@ __global__ void __launch_bounds__(64 * NW)
                            ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
       }
     }
-    float acc[WO];
+  }
+  // W_1 weights (step 3): M = 16 channels c1, one K step per (input channel, tap row) with the
+  // tap column as the lane group
+  static_assert(K1 == 4, "tap columns are the four lane groups");
+  constexpr int NK1 = NW * K1;  // K steps: in_c == NW
+  float w1r[NK1];
 #pragma unroll
-    for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-    auto emit = [&](int yl) {
-      if (!cok) return;
-      const int y = OY + yl;
+  for (int ks = 0; ks < NK1; ++ks) {
+    const int cc = ks / K1, ky = ks % K1, c1A = lane & 15;
+    w1r[ks] = (c1A < C1 && cc < t1.in_c)
+                  ? t1.W[(((long)c1A * t1.in_c + cc) * K1 + ky) * K1 + G] : 0.f;
+  }
+  const int Hi = t1.in_h, Wi = t1.in_w;
+  const int OY = Y1 * S1 - P1;
+
+  // relaxation of a window, one entry per (thread, k), fetched a window ahead
+  float4v pn[NPP];
+  auto pfetch = [&](int X1) {
 #pragma unroll
-      for (int x = 0; x < WO; ++x) {
-        const int xi = OX + x;
-        const bool in = y >= 0 && y < Hi && xi >= 0 && xi < Wi;
-        const int sv = acc[x] > 0.f ? 1 : (acc[x] < 0.f ? -1 : 0);
-        dl[((c0 * WO + yl) * WO + x) * 16 + n] = (signed char)(in ? sv : 0);
+    for (int k = 0; k < NPP; ++k) {
+      const int e = threadIdx.x + k * NT;
+      pn[k] = float4v{0.f, 0.f, 0.f, 0.f};
+      if (e >= NE) continue;
+      const int c1 = e / NPOS, pos = e - c1 * NPOS;
+      const int ky2 = pos / K2, kx2 = pos - ky2 * K2;
+      const int y1 = Y1 + ky2, x1 = X1 + kx2;
+      if (y1 >= 0 && y1 < H1 && x1 >= 0 && x1 < Wd1) {
+        const long ni = ((long)c1 * H1 + y1) * Wd1 + x1;
+        pn[k] = float4v{a_lo[pb + ni], a_up[pb + ni], z1[ni],
+                        code1[b * n_relu + ni] == 5 ? 1.f : 0.f};
       }
-    };
+    }
+  };
+  pfetch(x2c * XW * t2.stride - t2.pad);
+  __syncthreads();  // wrow
+
+  for (int xi = 0; xi < XW; ++xi) {
+    const int x2 = x2c * XW + xi;
+    const int X1 = x2 * t2.stride - t2.pad;
+    float* out = part + (win0 + xi) * (long)NE;
+    bool active = false;
 #pragma unroll
-    for (int j = 0; j < K2; ++j) {
-      const int ph = j % PER;
+    for (int r = 0; r < 16; ++r) active |= wrow[xi][r] != 0.f;
+    if (!active) {  // uniform: no row of this window carries weight
+      for (int e = threadIdx.x; e < NE; e += NT) out[e] = 0.f;
+      if (xi + 1 < XW) pfetch(X1 + t2.stride);
+      continue;
+    }
+    // (1) stage the window's relaxation; fetch the next window's; relaxed window coefficients
 #pragma unroll
-      for (int i = 0; i < K2; ++i) {
-        const int pos = j * K2 + i;
+    for (int k = 0; k < NPP; ++k) {
+      const int e = threadIdx.x + k * NT;
+      if (e < NE) prm[e] = pn[k];
+    }
+    __syncthreads();
+    if (xi + 1 < XW) pfetch(X1 + t2.stride);
+#pragma unroll
+    for (int k = 0; k < NEP; ++k) {
+      const int e = partid + k * RPT;
+      if (e < NE) {
+        const float4v pr = prm[e];
+        tile[toff(k)] = wv[k] >= 0.f ? wv[k] * pr[0] : wv[k] * pr[1];
+      }
+    }
+    __syncthreads();
+
+    // (2) A_x over the footprint; delta = -eps sign(A_x) into LDS (0 outside the image)
+    const int OX = X1 * S1 - P1;
+    {
+      float acc[WO];
+#pragma unroll
+      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+      auto emit = [&](int yl) {
+        if (!cok) return;
+        const int y = OY + yl;
+#pragma unroll
+        for (int x = 0; x < WO; ++x) {
+          const int xc = OX + x;
+          const bool in = y >= 0 && y < Hi && xc >= 0 && xc < Wi;
+          const int sv = acc[x] > 0.f ? 1 : (acc[x] < 0.f ? -1 : 0);
+          dl[((c0 * WO + yl) * WO + x) * 16 + n] = (signed char)(in ? sv : 0);
+        }
+      };
+#pragma unroll
+      for (int j = 0; j < K2; ++j) {
+        const int ph = j % PER;
+#pragma unroll
+        for (int i = 0; i < K2; ++i) {
+          const int pos = j * K2 + i;
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
+                                                    tile[(4 * ks + G) * CS + pos * 16 + n],
+                                                    d, 0, 0, 0);
+#pragma unroll
+          for (int kx2 = 0; kx2 < K1; ++kx2) acc[i * S1 + kx2] += d[kx2];
+        }
+        const int ky = ((G - ph * S1) % K1 + K1) % K1;
+        if (G < K1 && ky < S1) {
+          emit(j * S1 + ky);
+#pragma unroll
+          for (int x = 0; x < WO; ++x) acc[x] = 0.f;
+        }
+      }
+      {
+        const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
+        if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
+      }
+    }
+    __syncthreads();
+
+    // the tile now holds max(A~, 0), the non-negative parts of the unrelaxed window coefficients
+#pragma unroll
+    for (int k = 0; k < NEP; ++k) {
+      const int e = partid + k * RPT;
+      if (e < NE) tile[toff(k)] = fmaxf(wv[k], 0.f);
+    }
+    __syncthreads();
+
+    // (3) G = z1 + W_1 delta = z1 - eps W_1 sign(A_x) at each window neuron, W_1 sign(A_x) on
+    // MFMA (the footprint entry of a K step is uniform per lane group); contributions summed
+    // over the rows
+    {
+      const float wn = wrow[xi][n];
+      for (int pos = wave; pos < NPOS; pos += NW) {
+        const int j = pos / K2, i = pos - j * K2;
         float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
-                                                  tile[(4 * ks + G) * CS + pos * 16 + n],
-                                                  d, 0, 0, 0);
-#pragma unroll
-        for (int kx2 = 0; kx2 < K1; ++kx2) acc[i * S1 + kx2] += d[kx2];
-      }
-      const int ky = ((G - ph * S1) % K1 + K1) % K1;
-      if (G < K1 && ky < S1) {
-        emit(j * S1 + ky);
-#pragma unroll
-        for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-      }
-    }
-    {
-      const int ky = ((G - ((K2 - 1) % PER) * S1) % K1 + K1) % K1;
-      if (G < K1 && ky >= S1) emit((K2 - 1) * S1 + ky);
-    }
-  }
-  __syncthreads();
-
-  // the tile now holds max(A~, 0), the non-negative parts of the unrelaxed window coefficients
-  {
-    const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
-    const P2Row pr = p2_row(C2, g, row);
-    const float sgn = pr.neg ? -1.f : 1.f;
-    const float* w2 = t2.W + (long)pr.c2 * C1 * NPOS;
-    for (int e = partid; e < C1 * NPOS; e += NT / 16) {
-      const int c1 = e / NPOS, pos = e - c1 * NPOS;
-      tile[c1 * CS + pos * 16 + row] = fmaxf(sgn * w2[e], 0.f);
-    }
-  }
-  __syncthreads();
-
-  // (3) G = z1 + W_1 delta = z1 - eps W_1 sign(A_x) at each window neuron, W_1 sign(A_x) on MFMA
-  // (M = 16 channels c1, N = 16 rows, one K step per (input channel, tap row) with the tap
-  // column as the lane group, so the footprint entry of a K step is uniform per lane group);
-  // contributions summed over the rows
-  {
-    static_assert(K1 == 4, "tap columns are the four lane groups");
-    constexpr int NK1 = NW * K1;  // K steps: in_c == NW
-    float w1r[NK1];
-#pragma unroll
-    for (int ks = 0; ks < NK1; ++ks) {
-      const int cc = ks / K1, ky = ks % K1, c1A = lane & 15;
-      w1r[ks] = (c1A < C1 && cc < t1.in_c)
-                    ? t1.W[(((long)c1A * t1.in_c + cc) * K1 + ky) * K1 + G] : 0.f;
-    }
-    const float wn = wrow[n];
-    for (int pos = wave; pos < NPOS; pos += NW) {
-      const int j = pos / K2, i = pos - j * K2;
-      float4v d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < NK1; ++ks) {
-        const int cc = ks / K1, ky = ks % K1;
-        const float bv = (float)dl[((cc * WO + j * S1 + ky) * WO + i * S1 + G) * 16 + n];
-        d = __builtin_amdgcn_mfma_f32_16x16x4f32(w1r[ks], bv, d, 0, 0, 0);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c1 = 4 * G + r;
-        float cval = 0.f;
-        if (c1 < C1) {
-          const int e = c1 * NPOS + pos;
-          cval = wn * prm[3][e] * tile[c1 * CS + pos * 16 + n] * fmaf(-eps, d[r], prm[2][e]);
+        for (int ks = 0; ks < NK1; ++ks) {
+          const int cc = ks / K1, ky = ks % K1;
+          const float bv = (float)dl[((cc * WO + j * S1 + ky) * WO + i * S1 + G) * 16 + n];
+          d = __builtin_amdgcn_mfma_f32_16x16x4f32(w1r[ks], bv, d, 0, 0, 0);
         }
-        cval += __shfl_xor(cval, 8, 64);
-        cval += __shfl_xor(cval, 4, 64);
-        cval += __shfl_xor(cval, 2, 64);
-        cval += __shfl_xor(cval, 1, 64);
-        if (n == 0 && c1 < C1) out[c1 * NPOS + pos] = cval;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int c1 = 4 * G + r;
+          float cval = 0.f;
+          if (c1 < C1) {
+            const int e = c1 * NPOS + pos;
+            const float4v pr = prm[e];
+            cval = wn * pr[3] * tile[c1 * CS + pos * 16 + n] * fmaf(-eps, d[r], pr[2]);
+          }
+          cval += __shfl_xor(cval, 8, 64);
+          cval += __shfl_xor(cval, 4, 64);
+          cval += __shfl_xor(cval, 2, 64);
+          cval += __shfl_xor(cval, 1, 64);
+          if (n == 0 && c1 < C1) out[c1 * NPOS + pos] = cval;
+        }
       }
     }
+    __syncthreads();  // prm, tile and dl are refilled by the next window
   }
 }
 
@@ -3981,9 +4019,16 @@ Pass2GradKernel pass2_grad_kernel_for(const lirpa_net* net) {
   int nw = 0;
   if (!pass2_kernel_for(net, &nw)) return nullptr;
   const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
-  if (t2.k == 4 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 4, 8, 3>;
-  if (t2.k == 4 && t1.out_c == 16) return k_pass2_window_grad<4, 2, 1, 4, 16, 3>;
-  if (t2.k == 3 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 3, 8, 3>;
+  // windows per block: those of k_pass2_window
+  if (p2_xw(net) == 8) {
+    if (t2.k == 4 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 4, 8, 3, 8>;
+    if (t2.k == 4 && t1.out_c == 16) return k_pass2_window_grad<4, 2, 1, 4, 16, 3, 8>;
+    if (t2.k == 3 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 3, 8, 3, 8>;
+  } else {
+    if (t2.k == 4 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 4, 8, 3, 4>;
+    if (t2.k == 4 && t1.out_c == 16) return k_pass2_window_grad<4, 2, 1, 4, 16, 3, 4>;
+    if (t2.k == 3 && t1.out_c == 8) return k_pass2_window_grad<4, 2, 1, 3, 8, 3, 4>;
+  }
   return nullptr;
 }
 
@@ -4839,7 +4884,7 @@ int grad_chunk(const Chunk& c, int full) {
     if (P == 2 && P < L) {
       if (Pass2GradKernel gk = pass2_grad_kernel_for(net)) {
         const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
-        long blocks = pass2_blocks(net, c.nb);
+        long blocks = pass2_blocks(net, c.nb) / p2_xw(net);  // windows / windows per block
         float* part = at<float>(c.ws, p.off_p2part);
         const int8_t* code = at<int8_t>(c.ws, p.off_code);
         int e = launch_k(tag("pass2_window_grad", 1, 2), c.st, [&] {
