@@ -107,6 +107,29 @@ def test_alpha_on_conv_nets(name):
     check(f"{name}+alpha u", u, ulr)
 
 
+@pytest.mark.parametrize("widths", [(20, 30), (40, 64), (50, 99), (30, 128), (6, 7)])
+def test_closing_linear_widths(widths):
+    # the final pass's two closing Linear layers at widths that take every k-step count of the
+    # fused kernel (n_{L-1} = 30, 64, 99, 128: a clamped last k-step when it is not a multiple
+    # of 4; n_{L-2} not a multiple of 16: a clamped relaxation quad) and the generic path (7)
+    n2, n3 = widths
+    layers = wl.random_net([wl.conv(2, 6, 3, 3, 2, 1), wl.fc(27, n2), wl.fc(n2, n3),
+                            wl.fc(n3, 4)], 31 + n3)
+    rng = np.random.default_rng(n3)
+    x0 = rng.uniform(0, 1, wl.n_in(layers[0])).astype(np.float32)
+    C = wl.margin_spec(4, 1)
+    rnet = ref.RefNet(layers)
+    B = 23
+    split = wl.make_splits(B, rnet.n_relu, 6, n3, ref.root_unstable(rnet, x0, 0.05, C))
+    alpha = rng.uniform(0, 1, (B, rnet.n_relu)).astype(np.float32)
+    for a in (None, alpha):
+        lb, l, u = gpu_bound(layers, x0, 0.05, C, split, a)
+        lr, llr, ulr, _ = ref.bound(rnet, x0, 0.05, C, split, a)
+        check(f"fc{n2}-{n3} lb", lb, lr)
+        check(f"fc{n2}-{n3} l", l, llr)
+        check(f"fc{n2}-{n3} u", u, ulr)
+
+
 @pytest.mark.parametrize("B", [1, 5])
 def test_base_partial_blocks(B):
     # Base geometry with batches whose row counts leave partial 16-row blocks in every pass
