@@ -2496,7 +2496,7 @@ __global__ void __launch_bounds__(512)
   const int n = lane & 15, G = lane >> 4;
   const int H3 = t3.out_h, W3 = t3.out_w, C3 = t3.out_c;
   const int NG = p2_groups(C3);
-  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  unsigned blk = xcd_range(blockIdx.x);  // 32-bit: the scalar divisions stay short
   const int x3 = (int)(blk % (unsigned)W3); blk /= (unsigned)W3;
   const int y3 = (int)(blk % (unsigned)H3); blk /= (unsigned)H3;
   const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
@@ -2746,7 +2746,7 @@ __global__ void __launch_bounds__(512)
   const int n = lane & 15, G = lane >> 4;
   const int H4 = t4.out_h, W4 = t4.out_w, C4 = t4.out_c;
   const int NG = p2_groups(C4);
-  unsigned blk = blockIdx.x;  // 32-bit: the scalar divisions stay short
+  unsigned blk = xcd_range(blockIdx.x);  // 32-bit: the scalar divisions stay short
   const int x4 = (int)(blk % (unsigned)W4); blk /= (unsigned)W4;
   const int y4 = (int)(blk % (unsigned)H4); blk /= (unsigned)H4;
   const int g = (int)(blk % (unsigned)NG); blk /= (unsigned)NG;
