@@ -2016,11 +2016,23 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         }
     }
   }
-  float acc1[C0][OW];
+  // The output columns (x1 - XL) S1 + kx of input column x1 do not overlap those of x1 + 2
+  // (K1 = 2 S1), so each input column accumulates in place, as the MFMA's C operand, in one of
+  // two families of float4 (x1 - XL even: ev, odd: od); a column of the output row is the sum
+  // of its two family entries, formed when the row is emitted.
+  static_assert(K1 == 2 * S1 && NCX % 2 == 0, "two column families");
+  constexpr int NF = NCX / 2;
+  float4v ev[C0][NF], od[C0][NF];
 #pragma unroll
   for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
-    for (int x = 0; x < OW; ++x) acc1[c0][x] = 0.f;
+    for (int m = 0; m < NF; ++m) ev[c0][m] = od[c0][m] = float4v{0.f, 0.f, 0.f, 0.f};
+  auto colv = [&](int c0, int x) {  // output column x (local) of channel c0
+    float v = 0.f;
+    if (x / K1 < NF) v = ev[c0][x / K1][x % K1];
+    if (x >= S1 && (x - S1) / K1 < NF) v += od[c0][(x - S1) / K1][(x - S1) % K1];
+    return v;
+  };
   float l1 = 0.f, beta = 0.f;
   float pend[C0 * NSH];  // right shared columns of the pending row
   bool pend_ok = false;
@@ -2033,11 +2045,15 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
       for (int x = 0; x < OW; ++x) {
         const int g = OL + x;
         const bool left = HASL && x < NSH, right = HASR && x >= OW - NSH;
-        if (!left && !right && g >= 0 && g < WX && ok) l1 += fabsf(acc1[c0][x]);
-        if (left) xb[par][XB - 1][c0 * NSH + x][lane] = acc1[c0][x];
-        if (right) pend[c0 * NSH + x - (OW - NSH)] = acc1[c0][x];
-        acc1[c0][x] = 0.f;
+        const float a = colv(c0, x);
+        if (!left && !right && g >= 0 && g < WX && ok) l1 += fabsf(a);
+        if (left) xb[par][XB - 1][c0 * NSH + x][lane] = a;
+        if (right) pend[c0 * NSH + x - (OW - NSH)] = a;
       }
+#pragma unroll
+    for (int c0 = 0; c0 < C0; ++c0)
+#pragma unroll
+      for (int m = 0; m < NF; ++m) ev[c0][m] = od[c0][m] = float4v{0.f, 0.f, 0.f, 0.f};
     if (HASR) pend_ok = ok;
   };
   // the pending row of the previous step (parity par): add the right neighbour's part
@@ -2095,35 +2111,24 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         hn[ks] = ah;
       }
     };
-    auto add = [&](int x1, const float4v* d) {
-#pragma unroll
-      for (int c0 = 0; c0 < C0; ++c0)
-#pragma unroll
-        for (int kx = 0; kx < K1; ++kx) acc1[c0][x1 * S1 - P1 + kx - OL] += d[c0][kx];
-    };
     fetch(XL);
     if (XL + 1 <= XH) fetch(XL + 1);
     relax(XL);
-    float4v dp[C0];
 #pragma unroll
     for (int x1 = XL; x1 <= XH; ++x1) {
       if (x1 + 2 <= XH) fetch(x1 + 2);
       __builtin_amdgcn_sched_barrier(0);
-      float4v d[C0];
-#pragma unroll
-      for (int c0 = 0; c0 < C0; ++c0) d[c0] = float4v{0.f, 0.f, 0.f, 0.f};
+      const int u = x1 - XL;
 #pragma unroll
       for (int ks = 0; ks < KS1; ++ks)
 #pragma unroll
-        for (int c0 = 0; c0 < C0; ++c0)
-          d[c0] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[c0][ks], hn[ks], d[c0], 0, 0, 0);
-      if (x1 > XL) add(x1 - 1, dp);
+        for (int c0 = 0; c0 < C0; ++c0) {
+          float4v& a = (u % 2 == 0) ? ev[c0][u / 2] : od[c0][u / 2];
+          a = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[c0][ks], hn[ks], a, 0, 0, 0);
+        }
       if (x1 + 1 <= XH) relax(x1 + 1);
-#pragma unroll
-      for (int c0 = 0; c0 < C0; ++c0) dp[c0] = d[c0];
       __builtin_amdgcn_sched_barrier(0);
     }
-    add(XH, dp);
     const int ky = ((G - ph * S1) % K1 + K1) % K1;
     if (G < K1 && ky < S1) emit(y * S1 - P1 + ky, par);
   };
