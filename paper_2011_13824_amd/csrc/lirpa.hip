@@ -3915,6 +3915,42 @@ __global__ void __launch_bounds__(kBlock)
   gu[p] += (-da * lj + db * lj * lj) / d2;
 }
 
+// The same accumulation when the pass has few rows per sub-domain (R <= 64, e.g. the spec rows
+// of the final pass): one wave per (sub-domain, 64 consecutive neurons), a lane per neuron
+// summing its R rows in order.  The row weights are uniform over the wave and the adjoint
+// updates of the wave are contiguous.
+__global__ void __launch_bounds__(kBlock)
+    k_grad_reduce_rows(long nb, long nm, long R, long ldq, const float* __restrict__ w,
+                       const float* __restrict__ tape, const float* __restrict__ G,
+                       const int8_t* __restrict__ code, const float* __restrict__ l,
+                       const float* __restrict__ u, long n_relu, float* __restrict__ ga,
+                       float* __restrict__ gl, float* __restrict__ gu) {
+  const long nw = (nm + 63) / 64;  // waves per sub-domain
+  const long wv = blockIdx.x * (long)(blockDim.x / 64) + threadIdx.x / 64;
+  if (wv >= nb * nw) return;  // uniform per wave
+  const long b = wv / nw, j = (wv % nw) * 64 + (threadIdx.x & 63);
+  if (j >= nm) return;
+  float sa = 0.f, da = 0.f, db = 0.f;
+  const float* tj = tape + j * ldq;
+  const float* gj = G + j * ldq;
+  for (long r = 0; r < R; ++r) {
+    const long q = b * R + r;
+    const float wr = w[q];
+    if (wr == 0.f) continue;  // uniform per wave
+    const float tv = tj[q], g = gj[q];
+    const float tp = fmaxf(tv, 0.f), tn = fminf(tv, 0.f);
+    sa = fmaf(wr * tp, g, sa);
+    da = fmaf(wr * tn, g, da);
+    db = fmaf(wr, tn, db);
+  }
+  const long p = b * n_relu + j;
+  if (code[p] != 5) return;
+  float lj = l[p], uj = u[p], d = uj - lj, d2 = d * d;
+  ga[p] += sa;
+  gl[p] += (da * uj - db * uj * uj) / d2;
+  gu[p] += (-da * lj + db * lj * lj) / d2;
+}
+
 // Projected Adam ascent step (bias-corrected), alpha clipped to [0, 1].
 __global__ void __launch_bounds__(kBlock) k_adam(long n, float* __restrict__ alpha,
                                                  float* __restrict__ m, float* __restrict__ v,
@@ -4967,10 +5003,18 @@ int grad_chunk(const Chunk& c, int full) {
         continue;
       }
       e = launch_k(tag("grad_reduce", m, P), c.st, [&] {
-        hipLaunchKernelGGL(k_grad_reduce, dim3((unsigned)((pairs + 3) / 4)), dim3(kBlock), 0,
-                           c.st, c.nb, net->n[m], R, ldq, w, tp, G,
-                           at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off, net->n_relu,
-                           ga + off, gl + off, gu + off);
+        if (R <= 64) {
+          const long waves = c.nb * ((net->n[m] + 63) / 64);
+          hipLaunchKernelGGL(k_grad_reduce_rows, dim3((unsigned)((waves + 3) / 4)), dim3(kBlock),
+                             0, c.st, c.nb, net->n[m], R, ldq, w, tp, G,
+                             at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
+                             net->n_relu, ga + off, gl + off, gu + off);
+        } else {
+          hipLaunchKernelGGL(k_grad_reduce, dim3((unsigned)((pairs + 3) / 4)), dim3(kBlock), 0,
+                             c.st, c.nb, net->n[m], R, ldq, w, tp, G,
+                             at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
+                             net->n_relu, ga + off, gl + off, gu + off);
+        }
       });
       if (e) return e;
       zin = zout;
