@@ -3538,15 +3538,18 @@ __global__ void __launch_bounds__(256)
   const int Hout = t.out_h, Wout = t.out_w, Hin = t.in_h, Win = t.in_w;
   const int npos = Hout * Wout;
   const int nmt = (t.out_c + 15) / 16;
-  for (int pos = wave; pos < npos; pos += 4) {
+  // work items (output position, 16-channel M tile) dealt to the 4 waves, so that a layer with
+  // one position (Linear) keeps every wave busy; the operands of 8 K steps are loaded at once
+  for (int it = wave; it < npos * nmt; it += 4) {
+    const int pos = it / nmt, mt = it - pos * nmt;
     const int y = pos / Wout, x = pos - y * Wout;
     const int yb = y * t.stride - t.pad, xb = x * t.stride - t.pad;
-    for (int mt = 0; mt < nmt; ++mt) {
+    {
       const int coA = mt * 16 + n;  // A operand row (M = l%16)
-      float4v d = {0.f, 0.f, 0.f, 0.f};
-      for (int ks = 0; ks < nks; ++ks) {
+      auto operands = [&](int ks, float& av, float& bv) {
         const int kk = ks * 4 + g;  // K index of this lane group
-        float av = 0.f, bv = 0.f;
+        av = 0.f;
+        bv = 0.f;
         if (kk < KD) {
           const int ci = kk / (K * K), rem = kk - ci * K * K;
           const int ky = rem / K, kx = rem - ky * K;
@@ -3560,6 +3563,19 @@ __global__ void __launch_bounds__(256)
               bv = zin[ii * ldq + q];
           }
         }
+      };
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+      int ks = 0;
+      for (; ks + 8 <= nks; ks += 8) {
+        float av[8], bv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) operands(ks + u, av[u], bv[u]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], d, 0, 0, 0);
+      }
+      for (; ks < nks; ++ks) {
+        float av, bv;
+        operands(ks, av, bv);
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, d, 0, 0, 0);
       }
       if (!qok || wq == 0.f) continue;
