@@ -86,6 +86,18 @@ def stage_work(layers, S, B):
                  + t1["out_c"] * w1 * w1 * t1["in_c"] * t1["k"] ** 2)
         add("pass4_window[layer1,pass4]", 2.0 * Q4 * wmacs,
             4.0 * (3 * B * (n[1] + n[2] + n[3]) + Q4))
+    for m in range(1, L):
+        # relaxation parameters of layer m (elementwise): l, u read or, for layer 1, copied from
+        # the shared bounds and written (8 bytes), the split byte read, (a_lo, a_up, b_up) and
+        # the stability code written (13 bytes) per neuron and sub-domain
+        add(f"relax_params[layer{m},pass{m}]", 0.0, 22.0 * B * n[m])
+    if L >= 3 and layers[L - 2]["kind"] == wl.FC:
+        # the final pass's spec rows through T_L and T_{L-1} in one kernel: T_{L-1}^T's flops;
+        # bytes: the relaxations of layers L-1 and L-2 read (3 floats per neuron and
+        # sub-domain), the relaxed slab over g^(L-2) written
+        Qf = B * S
+        add(f"final_fc[layer{L - 1},pass{L}]", 2.0 * Qf * macs(layers[L - 2]),
+            4.0 * 3 * B * (n[L - 1] + n[L - 2]) + 4.0 * n[L - 2] * Qf)
     for k in range(2, L + 1):
         R = 2 * n[k] if k < L else S
         Q = B * R
