@@ -98,6 +98,14 @@ def stage_work(layers, S, B):
         Qf = B * S
         add(f"final_fc[layer{L - 1},pass{L}]", 2.0 * Qf * macs(layers[L - 2]),
             4.0 * 3 * B * (n[L - 1] + n[L - 2]) + 4.0 * n[L - 2] * Qf)
+    if L == 4 and layers[2]["kind"] == wl.FC and all(layers[i]["kind"] == wl.CONV for i in (0, 1)):
+        # the whole final pass in one kernel (launched for the shapes the library covers): the
+        # spec rows through T_3^T, T_2^T and T_1^T; bytes: the relaxations of layers 1 to 3
+        # read (3 floats per neuron and sub-domain), W_3 and z1, one float per row written
+        Qf = B * S
+        add(f"spec_bound[layer2,pass{L}]",
+            2.0 * Qf * (macs(layers[2]) + macs(layers[1]) + macs(layers[0])),
+            4.0 * (3 * B * (n[1] + n[2] + n[3]) + n[3] * n[2] + n[1]) + 4.0 * Qf)
     for k in range(2, L + 1):
         R = 2 * n[k] if k < L else S
         Q = B * R

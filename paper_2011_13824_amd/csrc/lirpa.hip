@@ -231,6 +231,11 @@ struct FcSrc {
   float* r_bu;
   int8_t* code;         // stride n_relu, at offset off
   long n_relu, off;
+  // spec source of k_convT_fc_bound (the final pass from the merged spec rows): b holds
+  // C W_L [S][nk] followed by C b_L [S]; r_lo, r_up, r_bu the relaxation of layer L-1 (read);
+  // a_lo, a_up, b_up that of layer L-2; the two layers' bias vectors
+  const float* sbias_k = nullptr;   // layer L-2
+  const float* sbias_k1 = nullptr;  // layer L-1
 };
 
 struct Acc {
@@ -1701,9 +1706,9 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 // The bound of a row is then its bias terms minus eps ||A_x||_1 (the linear term sits in the
 // layer-1 bias).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
-          int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS>
+          int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS, int SPEC = 0>
 __global__ void __launch_bounds__(64 * (CI / CPW + NXW))
-__attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
+__attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3), 8)))
     k_convT_fc_bound(DLayer t, DLayer t1, const float* __restrict__ in, unsigned ldq, unsigned Q,
                      Sink s, FcSrc fc) {
   static_assert(W0 == 16 && K <= 4 && S <= K && CO % 4 == 0 && CI % 4 == 0 && CI % CPW == 0,
@@ -1727,6 +1732,11 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   // layer-1 relaxation of a stage, float4 (a_lo, a_up, b_up, z1) per entry:
   // [NBS sub-domains][RSL][CI][W0 (+1 pad)]
   static_assert(NBS == 2 || NBS == 3, "sub-domains per block");
+  static_assert(SPEC == 0 || !FC, "the spec source replaces the slab source");
+  constexpr int NMT_S = CO * W1 / 16;  // spec source: 16-entry tiles of an input row
+  static_assert(SPEC == 0 || (NMT_S % (CI / CPW) == 0 && W1 % 4 == 0), "spec tiles per wave");
+  static_assert(SPEC == 0 || NMT_S / (CI / CPW) <= 2, "spec operands: two tiles per wave");
+  constexpr int TPW_S = SPEC > 0 ? NMT_S / (CI / CPW) : 1;
   constexpr int PCS4 = W0 + 1;
   constexpr int PBS4 = RSL * CI * PCS4 + 2;
   constexpr int PSLOT4 = NBS * PBS4;
@@ -1741,6 +1751,9 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   __shared__ float ring[2][SLOT];
   __shared__ float4v pars[2][PSLOT4];
   __shared__ float red[NM * 16 + 2 * NXW * 16];
+  // spec source: each matrix wave's copy of the block's rows relaxed onto layer L-1, the MFMA
+  // B operand [4 SPEC][16 rows]
+  __shared__ float vts[SPEC > 0 ? NM : 1][SPEC > 0 ? SPEC * 64 : 1];
   // border exchange of the x waves (see there): [step parity][wave - 1][channel, column][lane]
   constexpr int NSH = K1 - S1;  // output columns two neighbouring x waves share
   __shared__ float xb[2][NXW > 1 ? NXW - 1 : 1][C0 * NSH][64];
@@ -1888,11 +1901,94 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         if (v4 < NV4) *reinterpret_cast<float4v*>(buf + 4 * v4) = sv[k];
       }
     };
+    // Spec source (final pass, rows q = (b, s) of the spec merged into the last layer): the
+    // row over g^(L-1) is C_s W_L relaxed onto layer L-1 (Eq. 6), built once per wave in LDS;
+    // each input row of T_2^T (entries (co, y1, x1) of g^(L-2)) is that row through W_{L-1}^T
+    // on MFMA (M = 16 entries, K = 4 features j, N = 16 rows; TPW_S entry tiles per wave, their
+    // operands loaded at the start of the step) relaxed onto layer L-2 into the input tile.
+    // The rows' intercept and bias terms of both relaxations, and C_s b_L, go to sbeta.
+    float sbeta = 0.f;
+    float sa[SPEC > 0 ? SPEC : 1];  // the first tile's A operands, loaded a step ahead
+    int spec_y1 = 0;                // the input row they belong to
+    const unsigned qs = min(q0 + (unsigned)n, Q - 1u);  // this lane's row (clamped)
+    const unsigned bs = qs / R;
+    if constexpr (SPEC > 0) {
+      float* vt = vts[wave];
+      const int nj = fc.nk;
+      const unsigned sn = qs - bs * R;
+      const long pb3 = (long)bs * s.pstride;
+#pragma unroll 5
+      for (int k = 0; k < SPEC; ++k) {
+        const int j = 4 * k + G;
+        float ah = 0.f;
+        if (j < nj) {
+          const float a = fc.b[(long)sn * nj + j];
+          ah = a * (a >= 0.f ? fc.r_lo[pb3 + j] : fc.r_up[pb3 + j]);
+          if (wave == 0) {
+            sbeta = fmaf(fminf(a, 0.f), fc.r_bu[pb3 + j], sbeta);
+            sbeta = fmaf(ah, fc.sbias_k1[j], sbeta);
+          }
+        }
+        vt[j * 16 + n] = ah;
+      }
+      if (wave == 0 && G == 0) sbeta += fc.b[(long)R * nj + sn];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wave's own LDS rows
+    }
+    // A operands of entry tile mt of input row y1 (4 k + G < 4 (SPEC - 1) < nj for
+    // k < SPEC - 1; the last k-step is clamped, its rows j >= nj meet zeros of the LDS rows)
+    auto spec_a = [&](int mt, int y1, float* a) {
+      const int nj = fc.nk, nin = CO * H1 * W1;
+      const int e = mt * 16 + (lane & 15);  // A operand row: entry e = (co, x1)
+      const int i = ((e / W1) * H1 + y1) * W1 + e % W1;
+      const float* w = fc.W + (long)G * nin + i;
+#pragma unroll
+      for (int k = 0; k < SPEC - 1; ++k) a[k] = w[(long)4 * k * nin];
+      a[SPEC - 1] = fc.W[(long)min(4 * (SPEC - 1) + G, nj - 1) * nin + i];
+    };
+    auto spec_load = [&](int y1) {
+      if constexpr (SPEC > 0) {
+        spec_a(wave, y1, sa);
+        spec_y1 = y1;
+      }
+    };
+    auto spec_store = [&](float* buf) {
+      if constexpr (SPEC > 0) {
+        const float* vt = vts[wave];
+        const long pb2 = (long)bs * s.pstride;
+        float sb[SPEC];  // the other tiles' operands, loaded here
+#pragma unroll
+        for (int t = 0; t < TPW_S; ++t) {
+          const int mt = wave + NM * t;
+          if (t + 1 < TPW_S) spec_a(mt + NM, spec_y1, sb);
+          // this lane's four D entries: consecutive x1 of one channel
+          const int e0 = mt * 16 + 4 * G;
+          const int i0 = ((e0 / W1) * H1 + spec_y1) * W1 + e0 % W1;
+          const float4v p_lo = *reinterpret_cast<const float4v*>(fc.a_lo + pb2 + i0);
+          const float4v p_up = *reinterpret_cast<const float4v*>(fc.a_up + pb2 + i0);
+          const float4v p_bu = *reinterpret_cast<const float4v*>(fc.b_up + pb2 + i0);
+          const float4v p_bz = *reinterpret_cast<const float4v*>(fc.sbias_k + i0);
+          float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int k = 0; k < SPEC; ++k)
+            d = __builtin_amdgcn_mfma_f32_16x16x4f32(t == 0 ? sa[k] : sb[k],
+                                                     vt[(4 * k + G) * 16 + n], d, 0, 0, 0);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int e = mt * 16 + 4 * G + r;
+            const float a = d[r];
+            const float ah = a * (a >= 0.f ? p_lo[r] : p_up[r]);
+            sbeta = fmaf(fminf(a, 0.f), p_bu[r], sbeta);
+            sbeta = fmaf(ah, p_bz[r], sbeta);
+            buf[((e % W1) * CO + e / W1) * 16 + n] = ah;
+          }
+        }
+      }
+    };
     auto src_load = [&](int y1) {
-      if constexpr (FC) gen_load(y1); else slab_load(y1);
+      if constexpr (SPEC > 0) spec_load(y1); else if constexpr (FC) gen_load(y1); else slab_load(y1);
     };
     auto src_store = [&](float* buf) {
-      if constexpr (FC) gen_store(buf); else slab_store(buf);
+      if constexpr (SPEC > 0) spec_store(buf); else if constexpr (FC) gen_store(buf); else slab_store(buf);
     };
 
     src_load(0);
@@ -1969,6 +2065,12 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
         red[wave * 16 + 2 * lane] = fbeta_a;
         red[wave * 16 + 2 * lane + 1] = fbeta_b;
       }
+    }
+    if constexpr (SPEC > 0) {
+      // row n's terms: lanes n, n + 16, n + 32, n + 48 of the wave
+      sbeta += __shfl_xor(sbeta, 16, 64);
+      sbeta += __shfl_xor(sbeta, 32, 64);
+      if (lane < 16) red[wave * 16 + lane] = sbeta;
     }
     lds_barrier();  // the x waves' last border exchange
     lds_barrier();  // final reduction
@@ -2188,6 +2290,9 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
     tb = (r & 1) ? -bj : bj;
     for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
   }
+  if constexpr (SPEC > 0) {
+    for (int w = 0; w < NM; ++w) tb += red[w * 16 + lane];
+  }
   for (int w = 0; w < NXW; ++w) tb += red[NM * 16 + w * 16 + lane];
   float ta = 0.f;
   for (int w = 0; w < NXW; ++w) ta += red[NM * 16 + (NXW + w) * 16 + lane];
@@ -2210,7 +2315,8 @@ __attribute__((amdgpu_waves_per_eu(CI / CPW + NXW <= 8 ? 4 : 3, 8)))
   } else {
     if (q >= Q) return;
     Acc a{tb, 0.f, ta};
-    sink_finish<MODE_BOUND>(s, a, q, q / R, r, false);
+    // (spec source: no running bias from an earlier stage)
+    sink_finish<MODE_BOUND>(s, a, q, q / R, r, SPEC > 0);
   }
 }
 
@@ -4476,7 +4582,10 @@ int8_t* tsign_of(const Chunk& c, int pass) {
 // geometry (fc: rows built from W_3; otherwise read from a slab, with nbs sub-domains per block
 // at most); null otherwise.
 using FcBoundKernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink, FcSrc);
-FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwaves) {
+// (spec: the variant that takes the final pass's spec rows from C W_L through a closing
+// Linear layer of 97..100 features; Base geometry, three sub-domains per block)
+FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwaves,
+                               bool spec = false) {
   if (net->L < 3) return nullptr;
   const lirpa_layer &t2 = net->T[1], &t1 = net->T[0];
   if (t2.kind != LIRPA_CONV2D || t1.kind != LIRPA_CONV2D) return nullptr;
@@ -4487,6 +4596,15 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
   if (!t1_ok || !t2_ok) return nullptr;
   if (t1.out_c == 8 && t2.in_c == 8 && t2.out_c == 16) {
     *nwaves = 8 / 2 + 4;
+    if (spec) {
+      // one g^(1) channel per matrix wave: 8 matrix waves, so that each takes one entry tile
+      // of the spec source, its operands loaded a whole step ahead
+      *nwaves = 8 + 4;
+      return fc || nbs != 3
+                 ? nullptr
+                 : k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 1, 4, 2, 1, 32, 32, 3, 4, false, 3,
+                                    25>;
+    }
     if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
     if (nbs == 2)
       return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
@@ -4494,7 +4612,7 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
   }
   // the Wide shape: 8 matrix waves and 4 x waves, one block per CU (the slab source with three
   // sub-domains per block would not fit in LDS)
-  if (t1.out_c == 16 && t2.in_c == 16 && t2.out_c == 32 && (fc || nbs == 2)) {
+  if (t1.out_c == 16 && t2.in_c == 16 && t2.out_c == 32 && (fc || nbs == 2) && !spec) {
     *nwaves = 16 / 2 + 4;
     if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
     return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
@@ -4878,6 +4996,41 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
   // final pass
   long R = c.S, Q = c.nb * R, ldq = round_up(Q, 64);
   const lirpa_layer& tL = net->T[L - 1];
+  if (!c.tape && L == 4 && c.p->off_wsp && net->T[2].kind == LIRPA_LINEAR && R >= 8 &&
+      (net->n[3] + 3) / 4 == 25) {
+    // the whole final pass in one kernel: the spec rows through T_4 (k_setup's C W_4), their
+    // relaxation onto layer 3, T_3^T on MFMA and the relaxation onto layer 2 built into the
+    // conv kernel's input tile, then T_2^T, the layer-1 relaxation, T_1^T and the
+    // concretisation (Base geometry)
+    int nw = 0;
+    if (FcBoundKernel kern = conv12_bound_for(net, false, 3, &nw, /*spec=*/true)) {
+      Sink s = slab_sink(c, 1, nullptr, ldq, R);
+      const Sink sb = bound_sink(c, R, lb, lb, c.S, c.S);
+      s.eps = sb.eps;
+      s.x0 = sb.x0;
+      s.lo = sb.lo;
+      s.hi = sb.hi;
+      s.bstride = sb.bstride;
+      s.n_half = sb.n_half;
+      FcSrc f{};
+      f.W = net->T[2].W;
+      f.b = at<float>(c.ws, c.p->off_wsp);
+      f.nk = (int)net->n[3];
+      f.a_lo = at<float>(c.ws, c.p->off_alo) + net->poff[2];
+      f.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[2];
+      f.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[2];
+      f.r_lo = at<float>(c.ws, c.p->off_alo) + net->poff[3];
+      f.r_up = at<float>(c.ws, c.p->off_aup) + net->poff[3];
+      f.r_bu = at<float>(c.ws, c.p->off_bup) + net->poff[3];
+      f.sbias_k = at<float>(c.ws, c.p->off_bz) + net->poff[2];
+      f.sbias_k1 = at<float>(c.ws, c.p->off_bz) + net->poff[3];
+      const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
+      return launch_k(tag("spec_bound", 2, L), c.st, [&] {
+        hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[1]),
+                           dlayer(net->T[0]), nullptr, (unsigned)ldq, (unsigned)Q, s, f);
+      });
+    }
+  }
   if (!c.tape && L >= 3 && c.p->off_wsp && net->T[L - 2].kind == LIRPA_LINEAR) {
     // the spec rows through T_L and T_{L-1} in one kernel
     constexpr int NW = 16;
