@@ -1922,8 +1922,10 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
         const int j = 4 * k + G;
         float ah = 0.f;
         if (j < nj) {
+          // both slopes loaded, so that no load waits for the coefficient's sign
           const float a = fc.b[(long)sn * nj + j];
-          ah = a * (a >= 0.f ? fc.r_lo[pb3 + j] : fc.r_up[pb3 + j]);
+          const float lo = fc.r_lo[pb3 + j], up = fc.r_up[pb3 + j];
+          ah = a * (a >= 0.f ? lo : up);
           if (wave == 0) {
             sbeta = fmaf(fminf(a, 0.f), fc.r_bu[pb3 + j], sbeta);
             sbeta = fmaf(ah, fc.sbias_k1[j], sbeta);
