@@ -1,8 +1,9 @@
 #!/usr/bin/env python
 """Throughput of batched LiRPA sub-domain bounds on one MI355X.
 
-One step = one lirpa_bound call over the whole batch of the workload (default: the Base conv
-net, 400 sub-domains, 9 margin specs): layer-1 bounds, every intermediate pass (rows +-e_j of
+One step = one lirpa_bound call over the whole batch of the workload (default: the base conv
+net Conv(3->8, k4 s2 p1)-Conv(8->16, k4 s2 p1)-FC(1024->100)-FC(100->10) on 3x32x32 inputs,
+400 sub-domains, 9 margin specs): layer-1 bounds, every intermediate pass (rows +-e_j of
 each hidden layer, per sub-domain under its own splits) and the final pass, each backward stage
 with its relaxation or concretisation fused.  Inputs are synthetic and resident in HBM before
 the timed region.  Prints one JSON line.

@@ -2806,7 +2806,7 @@ __global__ void __launch_bounds__(512)
 }
 
 // Pass 4 restricted to each row's receptive field, when T_4 .. T_1 are convolutions with T_3 and
-// T_2 of stride 1 (the Deep shape).  Row +-e_j of h^(4), j = (c4, y4, x4), carried through T_4
+// T_2 of stride 1 (e.g. k4 s2, k3 s1, k3 s1 over 8 channels).  Row +-e_j of h^(4), j = (c4, y4, x4), carried through T_4
 // is +-W_4[c4] on the K4 x K4 window of j on g^(3); the layer-3 relaxation and T_3^T spread it
 // over a (K4 + K3 - 1)^2 window of g^(2), the layer-2 relaxation and T_2^T over a
 // (K4 + K3 + K2 - 2)^2 window of g^(1), and the layer-1 relaxation and T_1^T over that window's
@@ -4358,8 +4358,9 @@ using ConvTKernel = void (*)(DLayer, const float*, unsigned, unsigned, Sink);
 
 // Block size limit per instantiation: 256 threads (one wave per SIMD, so the unified register
 // file can hold the 32-wide ring of accumulators) for in_c <= 8, else 512.
-// Geometry / channel combinations with an MFMA kernel (those of the Base, Wide and Deep
-// shapes); everything else uses the per-lane gather kernel.  One wave per channel ci, two
+// Geometry / channel combinations with an MFMA kernel (k4 s2 p1 from 3 to 8 or 16 channels on
+// 32x32, k4 s2 p1 from 8 or 16 to 16 or 32 channels on 16x16, k3 s1 p1 8 to 8 on 16x16);
+// everything else uses the per-lane gather kernel.  One wave per channel ci, two
 // channels per wave above 8.
 template <int MODE, bool TAPE>
 ConvTKernel<MODE> convT_mfma_pick(const DLayer& t, int* nwaves) {
@@ -4396,8 +4397,9 @@ ConvTKernel<MODE> convT_mfma_pick(const DLayer& t, int* nwaves) {
   return nullptr;
 }
 
-// Geometry / channel combinations with an MFMA kernel (those of the Base, Wide and Deep
-// shapes); everything else uses the per-lane gather kernel.  One wave per channel ci, two
+// Geometry / channel combinations with an MFMA kernel (k4 s2 p1 from 3 to 8 or 16 channels on
+// 32x32, k4 s2 p1 from 8 or 16 to 16 or 32 channels on 16x16, k3 s1 p1 8 to 8 on 16x16);
+// everything else uses the per-lane gather kernel.  One wave per channel ci, two
 // channels per wave above 8.
 template <int MODE>
 ConvTKernel<MODE> convT_mfma_for(const DLayer& t, bool tape, int* nwaves) {
@@ -4585,7 +4587,7 @@ int8_t* tsign_of(const Chunk& c, int pass) {
 // at most); null otherwise.
 using FcBoundKernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink, FcSrc);
 // (spec: the variant that takes the final pass's spec rows from C W_L through a closing
-// Linear layer of 97..100 features; Base geometry, three sub-domains per block)
+// Linear layer of 97..100 features; conv 3 -> 8 -> 16 channels, three sub-domains per block)
 FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwaves,
                                bool spec = false) {
   if (net->L < 3) return nullptr;
@@ -4612,7 +4614,7 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
       return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
     return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 3>;
   }
-  // the Wide shape: 8 matrix waves and 4 x waves, one block per CU (the slab source with three
+  // 3 -> 16 -> 32 channels: 8 matrix waves and 4 x waves, one block per CU (the slab source with three
   // sub-domains per block would not fit in LDS)
   if (t1.out_c == 16 && t2.in_c == 16 && t2.out_c == 32 && (fc || nbs == 2) && !spec) {
     *nwaves = 16 / 2 + 4;
@@ -4640,7 +4642,7 @@ ConvT2Kernel convT2_bound_for(const lirpa_net* net, int* nwaves, size_t* lds) {
     *lds = (size_t)(2 * co * cs + 3 * rsl * ci * cs1 + 2 * 2 * 4 * rsl * ci * 16 + (ns + 3) * 16) *
            sizeof(float);
   };
-  // T_2: Conv(8 -> 8, k3, s1, p1), 16x16 -> 16x16 (the Deep shape).  A stride-2 T_2 (Base)
+  // T_2: Conv(8 -> 8, k3, s1, p1), 16x16 -> 16x16.  A stride-2 T_2 (8 -> 16 channels)
   // stays on the separate stage kernels: there each x wave carries twice the matrix work of a
   // T_2 wave per step, and at one block per CU that measured slower than the unfused pair.
   if (t.k == 3 && t.stride == 1 && t.pad == 1 && t.in_c == 8 && t.out_c == 8 && t.in_h == 16 &&
@@ -4772,8 +4774,8 @@ int pass3_window(const Chunk& c) {
   });
 }
 
-// Witness forward kernels of the covered convolution shapes (those of the Base, Wide and Deep
-// networks); null for any other layer (the generic k_fwd_mfma runs).
+// Witness forward kernels of the covered convolution shapes (the k4 s2 p1 and k3 s1 p1 layers
+// of the convolution kernels); null for any other layer (the generic k_fwd_mfma runs).
 using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
                            const float*, float, const float*, const float*, const float*,
                            const float*, long, float*, float*, float*, unsigned char*,
@@ -4891,8 +4893,8 @@ int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   });
 }
 
-// Kernel for the receptive-field pass 4 (T_4 over the stride-1 T_3, T_2 over T_1; the Deep
-// shape), or null.
+// Kernel for the receptive-field pass 4 (T_4 over the stride-1 T_3, T_2 over T_1, 8 channels
+// each), or null.
 using Pass4Kernel = void (*)(DLayer, DLayer, DLayer, DLayer, const float*, const float*,
                              const float*, long, long, long, long, const float*, float, float*,
                              float*, long, long);
@@ -5003,7 +5005,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
     // the whole final pass in one kernel: the spec rows through T_4 (k_setup's C W_4), their
     // relaxation onto layer 3, T_3^T on MFMA and the relaxation onto layer 2 built into the
     // conv kernel's input tile, then T_2^T, the layer-1 relaxation, T_1^T and the
-    // concretisation (Base geometry)
+    // concretisation (conv 3 -> 8 -> 16 channels on 32x32, then a Linear layer of 97..100)
     int nw = 0;
     if (FcBoundKernel kern = conv12_bound_for(net, false, 3, &nw, /*spec=*/true)) {
       Sink s = slab_sink(c, 1, nullptr, ldq, R);
