@@ -1751,9 +1751,8 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
   __shared__ float ring[2][SLOT];
   __shared__ float4v pars[2][PSLOT4];
   __shared__ float red[NM * 16 + 2 * NXW * 16];
-  // spec source: each matrix wave's copy of the block's rows relaxed onto layer L-1, the MFMA
-  // B operand [4 SPEC][16 rows]
-  __shared__ float vts[SPEC > 0 ? NM : 1][SPEC > 0 ? SPEC * 64 : 1];
+  // spec source: the block's rows relaxed onto layer L-1, the MFMA B operand [4 SPEC][16 rows]
+  __shared__ float vts[SPEC > 0 ? SPEC * 64 : 1];
   // border exchange of the x waves (see there): [step parity][wave - 1][channel, column][lane]
   constexpr int NSH = K1 - S1;  // output columns two neighbouring x waves share
   __shared__ float xb[2][NXW > 1 ? NXW - 1 : 1][C0 * NSH][64];
@@ -1913,12 +1912,15 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
     const unsigned qs = min(q0 + (unsigned)n, Q - 1u);  // this lane's row (clamped)
     const unsigned bs = qs / R;
     if constexpr (SPEC > 0) {
-      float* vt = vts[wave];
+      // the matrix waves share the rows: wave w relaxes k-steps w, w + NM, ... (each feature
+      // j once, its terms in the wave's sbeta); a barrier of both roles follows
       const int nj = fc.nk;
       const unsigned sn = qs - bs * R;
       const long pb3 = (long)bs * s.pstride;
-#pragma unroll 5
-      for (int k = 0; k < SPEC; ++k) {
+#pragma unroll
+      for (int t = 0; t < (SPEC + NM - 1) / NM; ++t) {
+        const int k = wave + t * NM;
+        if (k >= SPEC) break;  // uniform
         const int j = 4 * k + G;
         float ah = 0.f;
         if (j < nj) {
@@ -1926,15 +1928,13 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
           const float a = fc.b[(long)sn * nj + j];
           const float lo = fc.r_lo[pb3 + j], up = fc.r_up[pb3 + j];
           ah = a * (a >= 0.f ? lo : up);
-          if (wave == 0) {
-            sbeta = fmaf(fminf(a, 0.f), fc.r_bu[pb3 + j], sbeta);
-            sbeta = fmaf(ah, fc.sbias_k1[j], sbeta);
-          }
+          sbeta = fmaf(fminf(a, 0.f), fc.r_bu[pb3 + j], sbeta);
+          sbeta = fmaf(ah, fc.sbias_k1[j], sbeta);
         }
-        vt[j * 16 + n] = ah;
+        vts[j * 16 + n] = ah;
       }
       if (wave == 0 && G == 0) sbeta += fc.b[(long)R * nj + sn];
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wave's own LDS rows
+      lds_barrier();  // the rows (matched by the x waves' first barrier of the spec source)
     }
     // A operands of entry tile mt of input row y1 (4 k + G < 4 (SPEC - 1) < nj for
     // k < SPEC - 1; the last k-step is clamped, its rows j >= nj meet zeros of the LDS rows)
@@ -1955,7 +1955,7 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
     };
     auto spec_store = [&](float* buf) {
       if constexpr (SPEC > 0) {
-        const float* vt = vts[wave];
+        const float* vt = vts;
         const long pb2 = (long)bs * s.pstride;
         float sb[SPEC];  // the other tiles' operands, loaded here
 #pragma unroll
@@ -2236,6 +2236,7 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
     const int ky = ((G - ph * S1) % K1 + K1) % K1;
     if (G < K1 && ky < S1) emit(y * S1 - P1 + ky, par);
   };
+  if constexpr (SPEC > 0) lds_barrier();  // the matrix waves' spec rows
   lds_barrier();  // first input tile
   for (int st = 0; st < NSTEP; ++st) {
     if (st >= 1) {
