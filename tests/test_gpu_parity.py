@@ -145,6 +145,26 @@ def test_base_partial_blocks(B):
     check(f"base B={B} u", u, ulr)
 
 
+@pytest.mark.parametrize("S", [3, 8, 16])
+def test_base_spec_counts(S):
+    # Base geometry with S spec rows per sub-domain: the one-kernel final pass for S >= 8
+    # (16-row blocks spanning up to three sub-domains; 16 = one sub-domain a block) and the
+    # two-kernel final pass below that
+    w = wl.base()
+    rnet = ref.RefNet(w.layers)
+    rng = np.random.default_rng(40 + S)
+    C = rng.standard_normal((S, 10)).astype(np.float32)
+    B = 7
+    split = wl.make_splits(B, rnet.n_relu, 6, 40 + S, ref.root_unstable(rnet, w.x0, w.eps, C))
+    alpha = rng.uniform(0, 1, (B, rnet.n_relu)).astype(np.float32)
+    for a in (None, alpha):
+        lb, l, u = gpu_bound(w.layers, w.x0, w.eps, C, split, a)
+        lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, C, split, a)
+        check(f"base S={S} lb", lb, lr)
+        check(f"base S={S} l", l, llr)
+        check(f"base S={S} u", u, ulr)
+
+
 @pytest.mark.parametrize("name", ["tiny", "base", "wide", "deep"])
 def test_all_split_matches_closed_form(name):
     w = wl.get(name)
