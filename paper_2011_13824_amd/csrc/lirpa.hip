@@ -1836,7 +1836,7 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
         const int qp = tk & 7, qd = g_on[k] ? tk >> 3 : 0;
         const int co = qd % CO, t4 = qd / CO;
         const unsigned qa = q0 + 2u * qp, qb = qa + 1u;
-        const unsigned ra = qa % R, rb = qb % R;
+        const unsigned ra = qa % R;
         // rows 2 qp, 2 qp + 1 are +e_j, -e_j of one neuron j (R is even): one row of W_k
         (void)nk;
         g_sa[k] = qa < Q ? 1.f : 0.f;
@@ -4837,12 +4837,13 @@ int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
   WsKernel kern = convT_ws_for(t, c.tape, true, &nw, &lds);
   Sink s = slab_sink(c, k - 2, at<float>(c.ws, c.p->off_slab0), ldq, R);
   s.tape = tape_of(c, k, k - 2);
-  FcSrc f{fl.W,
-          fl.b,
-          (int)net->n[k],
-          at<float>(c.ws, c.p->off_alo) + net->poff[k - 1],
-          at<float>(c.ws, c.p->off_aup) + net->poff[k - 1],
-          at<float>(c.ws, c.p->off_bup) + net->poff[k - 1]};
+  FcSrc f{};
+  f.W = fl.W;
+  f.b = fl.b;
+  f.nk = (int)net->n[k];
+  f.a_lo = at<float>(c.ws, c.p->off_alo) + net->poff[k - 1];
+  f.a_up = at<float>(c.ws, c.p->off_aup) + net->poff[k - 1];
+  f.b_up = at<float>(c.ws, c.p->off_bup) + net->poff[k - 1];
   const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
   return launch_k(tag("convT_relax_fc", k - 1, k), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), lds, c.st, t, nullptr, (unsigned)ldq,
