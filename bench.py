@@ -269,8 +269,8 @@ def main():
             lirpa.lirpa_optimize(net.handle, x0, w.eps, C, S, B, split, alpha, adam_m, adam_v,
                                  params, lb, None, ws, ws_bytes)
         else:
-            lirpa.lirpa_bound(net.handle, x0, w.eps, C, S, B, split, None, lb, None, None, ws,
-                              ws_bytes)
+            lirpa.lirpa_bound(net.handle, x0, w.eps, C, S, B, split, None, lb, None, None,
+                              None, ws, ws_bytes)
 
     for _ in range(args.warmup):
         step()

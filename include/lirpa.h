@@ -14,14 +14,22 @@
  *   borrowed by a lirpa_net, which must outlive it).  The library never allocates or frees
  *   device memory: every scratch buffer comes from the caller's workspace `ws`.
  * - Calls validate their arguments on the host, enqueue kernels on `stream` and return without
- *   synchronising.  Return 0 (LIRPA_OK) on success, a negative lirpa_status otherwise; on error
- *   nothing is enqueued and lirpa_last_error() returns a thread-local message.
+ *   synchronising.  Return 0 (LIRPA_OK) on success, a negative lirpa_status otherwise, and
+ *   lirpa_last_error() returns a thread-local message.  On EINVAL, ENOMEM, EUNSUPPORTED and
+ *   EDATA nothing is enqueued.  On EDEVICE (a launch or runtime call failed part-way) the work
+ *   of the call up to the failure may already be enqueued: the outputs, and the in/out
+ *   optimiser state (alpha, adam_m, adam_v) of lirpa_optimize, are then undefined.
  * - Flattening is C order: a conv activation is [C][H][W]; a Linear layer after a conv reads the
  *   flattened [C][H][W] vector.  Per-neuron arrays (split, alpha, l, u, gradients) concatenate
  *   the ReLU layers 1..L-1 in layer order: n_relu = sum_{m<L} n_m values per sub-domain.
- * - Floating point is fp32 (round to nearest).  Device contents are not validated: a split
- *   value outside {-1, 0, 1} or an alpha outside [0, 1] gives undefined (but memory-safe)
- *   results.
+ * - Floating point is fp32 (round to nearest).  Device contents are not validated by default: a
+ *   split value outside {-1, 0, 1} or an alpha outside [0, 1] gives undefined (but
+ *   memory-safe) results.  With the environment variable LIRPA_VALIDATE=1 every call also
+ *   enqueues a read-only check of its device inputs (split in {-1, 0, 1} as the split
+ *   constraints of Sec. 3.1 require, alpha in [0, 1] as Eq. 5 requires, x0 and C finite);
+ *   the findings are reported by the NEXT call on the same device, which then synchronises
+ *   its stream, returns LIRPA_EDATA without enqueuing anything, names the offending input in
+ *   lirpa_last_error() and clears the findings.
  */
 #ifndef LIRPA_H_
 #define LIRPA_H_
@@ -40,7 +48,9 @@ typedef enum {
   LIRPA_EINVAL = -1,      /* bad argument: shape, null pointer, eps, S, B            */
   LIRPA_ENOMEM = -2,      /* the workspace cannot hold even one sub-domain            */
   LIRPA_EDEVICE = -3,     /* a HIP launch or runtime call failed                      */
-  LIRPA_EUNSUPPORTED = -4 /* a layer shape outside the supported set                  */
+  LIRPA_EUNSUPPORTED = -4, /* a layer shape outside the supported set                 */
+  LIRPA_EDATA = -5         /* LIRPA_VALIDATE=1: the previous call's device inputs were
+                              out of range (see the conventions above)                 */
 } lirpa_status;
 
 typedef enum { LIRPA_LINEAR = 0, LIRPA_CONV2D = 1 } lirpa_layer_kind;
@@ -63,19 +73,23 @@ typedef struct {
 
 typedef struct lirpa_net lirpa_net; /* opaque host object */
 
-/* Build a network from n_layers >= 1 layers (copied; W/b pointers borrowed).  EINVAL if the
+/* The network f of Sec. 2.1: affine layers T_1..T_L with a ReLU after each but the last.
+ * Build it from n_layers >= 1 layers (copied; W/b pointers borrowed).  EINVAL if the
  * chain is inconsistent (n_in of T_m != n_out of T_{m-1}, a conv output size that does not
  * follow the formula above, null W/b) and EUNSUPPORTED for shapes the kernels do not handle
  * (kernel size > 7, stride > 4, more than 32 layers). */
 int lirpa_net_create(const lirpa_layer* layers, int n_layers, lirpa_net** out);
 void lirpa_net_destroy(lirpa_net* net);
 
-/* n_relu = sum over ReLU layers of their sizes; -1 for a null net. */
+/* n_relu = sum over the ReLU layers 1..L-1 of Sec. 2.1 of their sizes; -1 for a null net. */
 int64_t lirpa_net_num_relu(const lirpa_net* net);
 
 /* Workspace bytes for one call processing up to B_chunk sub-domains at a time with S spec
- * rows.  mode 0 = lirpa_bound, 1 = lirpa_bound_grad / lirpa_optimize.  A call given a
- * smaller workspace processes its batch in chunks of as many sub-domains as fit. */
+ * rows (the batch of sub-domains of Sec. 3.3 is bounded by memory).  mode 0 = lirpa_bound,
+ * 1 = lirpa_bound_grad / lirpa_optimize.  A call given a smaller workspace processes its
+ * batch in chunks of as many sub-domains as fit.  Returns 0 for invalid arguments and
+ * SIZE_MAX when a chunk of B_chunk sub-domains cannot run at all (one bound-matrix slab would
+ * exceed 2^31 floats, the kernels' 32-bit element offsets); a call then uses smaller chunks. */
 size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode);
 
 /* Batched bound (Sec. 2.3 Eq. 2-7, concretised by Eq. 8; split constraints of Sec. 3.1).
@@ -89,10 +103,14 @@ size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode)
  *                         under sub-domain b's splits
  *   l_out, u_out [B][n_relu] optional out: intermediate pre-activation bounds (layer-1 bounds
  *                         are exact; split neurons report their bounds before the split)
+ *   code_out [B][n_relu]  optional out: the case of Eq. 5 / Sec. 3.1 each neuron's relaxation
+ *                         took, checked in this order: 1 split active (split +1), 2 split
+ *                         inactive (split -1), 3 inactive (u <= 0), 4 active (l >= 0),
+ *                         5 unstable (l < 0 < u)
  * Intermediate bounds of every layer are recomputed per sub-domain under its own splits. */
 int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
                 const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
-                void* ws, size_t ws_bytes, hipStream_t stream);
+                int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* As lirpa_bound, plus grad[b][:] = d(sum_s lb[b][s]) / d alpha[b][:] (alpha required).
  * full != 0 differentiates through the recomputed intermediate bounds (Sec. 3.1: they depend on

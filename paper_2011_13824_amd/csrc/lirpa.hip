@@ -23,6 +23,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <type_traits>
@@ -4167,6 +4168,34 @@ __global__ void __launch_bounds__(kBlock) k_zero(long n, float* __restrict__ p) 
 }
 
 // ---------------------------------------------------------------------------------------------
+// Input check (LIRPA_VALIDATE=1)
+// ---------------------------------------------------------------------------------------------
+// Findings of the check of a call's device inputs, one word per kind: [0] a split value outside
+// {-1, 0, 1} (Sec. 3.1 split constraints), [1] an alpha outside [0, 1] or not a number (Eq. 5),
+// [2] a non-finite x0, [3] a non-finite spec entry.  Each device holds its own copy; a finding
+// is recorded by plain stores of 1 (idempotent, no atomics) and read and cleared by the host.
+__device__ unsigned int g_check[4];
+
+__global__ void __launch_bounds__(kBlock)
+    k_check_inputs(long n_split, const int8_t* __restrict__ split, long n_alpha,
+                   const float* __restrict__ alpha, long n_x0, const float* __restrict__ x0,
+                   long n_C, const float* __restrict__ C) {
+  const long stride = (long)gridDim.x * blockDim.x;
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_split; i += stride) {
+    const int v = split[i];
+    if (v < -1 || v > 1) g_check[0] = 1u;
+  }
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_alpha; i += stride) {
+    const float a = alpha[i];
+    if (!(a >= 0.f && a <= 1.f)) g_check[1] = 1u;
+  }
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_x0; i += stride)
+    if (!isfinite(x0[i])) g_check[2] = 1u;
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_C; i += stride)
+    if (!isfinite(C[i])) g_check[3] = 1u;
+}
+
+// ---------------------------------------------------------------------------------------------
 // Workspace plan
 // ---------------------------------------------------------------------------------------------
 struct Plan {
@@ -4245,6 +4274,10 @@ long pass2_blocks(const lirpa_net* net, long nb) {
   return nb * p2_groups(t2.out_c) * t2.out_h * t2.out_w;
 }
 
+// Whether bound mode (no gradient tape) runs pass k, 2 <= k < L, in one kernel that keeps the
+// pass's coefficients on chip: such a pass needs no bound-matrix slab.
+bool pass_on_chip(const lirpa_net* net, int k, long Bc);
+
 Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   Plan p;
   p.Bc = Bc;
@@ -4259,6 +4292,7 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
     long qp = round_up(Bc * R, 64);
     if (k == 2 && win2 && k < L) continue;
     qpmax = std::max(qpmax, qp);
+    if (mode == 0 && k < L && pass_on_chip(net, k, Bc)) continue;
     int mtop = (k < L) ? k - 1 : L;  // slabs hold A over h^(m), m = mtop..1
     for (int m = 1; m <= mtop; ++m) slab = std::max(slab, net->n[m] * qp);
   }
@@ -4914,6 +4948,21 @@ Pass4Kernel pass4_kernel_for(const lirpa_net* net) {
   return nullptr;
 }
 
+bool pass_on_chip(const lirpa_net* net, int k, long Bc) {
+  // the same choices, in the same order, as bound_chunk makes for a chunk without a tape
+  int nw = 0;
+  if (k == 2) return pass2_kernel_for(net, &nw) != nullptr;
+  if (k == 4 && pass4_kernel_for(net)) return true;
+  if (k == 3 && pass3_kernel_for(net)) return true;
+  if (!fc_bound_for(net, k, &nw)) return false;
+  // fc_open_ok holds for every chunk of at most Bc sub-domains when it holds for Bc
+  Chunk c{};
+  c.net = net;
+  c.nb = Bc;
+  c.tape = false;
+  return fc_open_ok(c, k, 2 * net->n[k]);
+}
+
 int pass4_window(const Chunk& c) {
   const lirpa_net* net = c.net;
   Pass4Kernel kern = pass4_kernel_for(net);
@@ -5302,6 +5351,44 @@ int copy_d2d(void* dst, const void* src, size_t bytes, hipStream_t st) {
   return LIRPA_OK;
 }
 
+bool validate_on() {
+  const char* v = std::getenv("LIRPA_VALIDATE");
+  return v && v[0] == '1' && v[1] == '\0';
+}
+
+// With LIRPA_VALIDATE=1: report (LIRPA_EDATA) and clear what the check kernels of earlier calls
+// on this device found.  Synchronises the stream.
+int validate_report(hipStream_t st) {
+  if (!validate_on()) return LIRPA_OK;
+  unsigned int f[4] = {0, 0, 0, 0};
+  if (hipMemcpyFromSymbolAsync(f, HIP_SYMBOL(g_check), sizeof f, 0, hipMemcpyDeviceToHost, st) !=
+          hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return fail(LIRPA_EDEVICE, "reading the input-check findings failed");
+  if (!(f[0] | f[1] | f[2] | f[3])) return LIRPA_OK;
+  const unsigned int zero[4] = {0, 0, 0, 0};
+  if (hipMemcpyToSymbolAsync(HIP_SYMBOL(g_check), zero, sizeof zero, 0, hipMemcpyHostToDevice,
+                             st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return fail(LIRPA_EDEVICE, "clearing the input-check findings failed");
+  return fail(LIRPA_EDATA, "an earlier call's device inputs were out of range:%s%s%s%s",
+              f[0] ? " split value outside {-1,0,1};" : "",
+              f[1] ? " alpha outside [0,1];" : "", f[2] ? " non-finite x0;" : "",
+              f[3] ? " non-finite C;" : "");
+}
+
+// With LIRPA_VALIDATE=1: enqueue the read-only check of this call's device inputs.
+int validate_enqueue(const lirpa_net* net, const float* x0, const float* C, int S, int B,
+                     const int8_t* split, const float* alpha, hipStream_t st) {
+  if (!validate_on()) return LIRPA_OK;
+  const long n = (long)B * net->n_relu;
+  const long nC = (long)S * net->n[net->L];
+  return launch_k("check_inputs", st, [&] {
+    hipLaunchKernelGGL(k_check_inputs, dim3(1024), dim3(kBlock), 0, st, split ? n : 0L, split,
+                       alpha ? n : 0L, alpha, net->n[0], x0, nC, C);
+  });
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
@@ -5368,7 +5455,7 @@ size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode)
 
 int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
                 const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
-                void* ws, size_t ws_bytes, hipStream_t stream) {
+                int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
   if (!lb) return fail(LIRPA_EINVAL, "lb is null");
   if ((l_out == nullptr) != (u_out == nullptr))
@@ -5378,10 +5465,16 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1).total);
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
   if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
     if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
+    if (code_out && net->n_relu)
+      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
+                           (size_t)c.nb * net->n_relu, stream))
+        return e;
   }
   return LIRPA_OK;
 }
@@ -5397,6 +5490,8 @@ int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C,
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1, 1).total);
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
   if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
@@ -5425,6 +5520,10 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1, 1).total);
+  if (int e = validate_report(stream)) return e;
+  // alpha is an input only when the call continues from the caller's state
+  if (int e = validate_enqueue(net, x0, C, S, B, split, op.fresh ? nullptr : alpha, stream))
+    return e;
   if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);

@@ -16,7 +16,8 @@ import torch
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "liblirpa.so")
 
-LIRPA_OK, LIRPA_EINVAL, LIRPA_ENOMEM, LIRPA_EDEVICE, LIRPA_EUNSUPPORTED = 0, -1, -2, -3, -4
+LIRPA_OK, LIRPA_EINVAL, LIRPA_ENOMEM, LIRPA_EDEVICE, LIRPA_EUNSUPPORTED, LIRPA_EDATA = \
+    0, -1, -2, -3, -4, -5
 LINEAR, CONV2D = 0, 1
 
 
@@ -63,7 +64,7 @@ def load() -> ctypes.CDLL:
     L.lirpa_net_num_relu.restype = ctypes.c_int64
     L.lirpa_workspace_bytes.argtypes = [P, i, i, i]
     L.lirpa_workspace_bytes.restype = sz
-    L.lirpa_bound.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, sz, P]
+    L.lirpa_bound.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, sz, P]
     L.lirpa_bound.restype = i
     L.lirpa_bound_grad.argtypes = [P, P, f, P, i, i, P, P, i, P, P, P, sz, P]
     L.lirpa_bound_grad.restype = i
@@ -151,14 +152,15 @@ def lirpa_workspace_bytes(net, S, B_chunk, mode=0) -> int:
     return int(load().lirpa_workspace_bytes(net, S, B_chunk, mode))
 
 
-def lirpa_bound(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, ws, ws_bytes,
-                stream=None):
+def lirpa_bound(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out, ws,
+                ws_bytes, stream=None):
     _check(load().lirpa_bound(net, _dev(x0, torch.float32, "x0"), float(eps),
                               _dev(C, torch.float32, "C"), int(S), int(B),
                               _dev(split, torch.int8, "split"),
                               _dev(alpha, torch.float32, "alpha"),
                               _dev(lb, torch.float32, "lb"), _dev(l_out, torch.float32, "l_out"),
-                              _dev(u_out, torch.float32, "u_out"), _dev(ws, None, "ws"),
+                              _dev(u_out, torch.float32, "u_out"),
+                              _dev(code_out, torch.int8, "code_out"), _dev(ws, None, "ws"),
                               int(ws_bytes), _stream(stream)))
 
 
@@ -219,20 +221,25 @@ class Network:
         return self._ws, need
 
     def bound(self, x0, eps, C, split=None, alpha=None, B=None, want_lu=False, ws=None,
-              ws_bytes=None, max_ws_bytes=16 << 30):
+              ws_bytes=None, max_ws_bytes=16 << 30, want_codes=False):
         S = C.shape[0]
         if B is None:
             B = split.shape[0] if split is not None else (alpha.shape[0] if alpha is not None
                                                             else 1)
         lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
-        l = u = None
+        l = u = code = None
         if want_lu:
             l = torch.empty((B, self.n_relu), dtype=torch.float32, device=self.device)
             u = torch.empty_like(l)
+        if want_codes:
+            code = torch.empty((B, self.n_relu), dtype=torch.int8, device=self.device)
         if ws is None:
             ws, ws_bytes = self.workspace(S, B, 0, max_ws_bytes)
-        lirpa_bound(self.handle, x0, eps, C, S, B, split, alpha, lb, l, u, ws, ws_bytes)
-        return (lb, l, u) if want_lu else lb
+        lirpa_bound(self.handle, x0, eps, C, S, B, split, alpha, lb, l, u, code, ws, ws_bytes)
+        out = (lb, l, u) if want_lu else (lb,)
+        if want_codes:
+            out = out + (code,)
+        return out if len(out) > 1 else lb
 
     def bound_grad(self, x0, eps, C, split, alpha, full=True, max_ws_bytes=16 << 30):
         S, B = C.shape[0], alpha.shape[0]

@@ -97,7 +97,8 @@ def test_bound_validates_before_launching(L):
                  ws=P, ws_bytes=need * 4)
         a.update(kw)
         return L.lirpa_bound(h, a["x0"], a["eps"], a["C"], a["S"], a["B"], a["split"],
-                             a["alpha"], a["lb"], a["l"], a["u"], a["ws"], a["ws_bytes"], None)
+                             a["alpha"], a["lb"], a["l"], a["u"], None, a["ws"], a["ws_bytes"],
+                             None)
 
     assert call(S=0) == lirpa.LIRPA_EINVAL
     assert call(B=0) == lirpa.LIRPA_EINVAL
@@ -111,7 +112,7 @@ def test_bound_validates_before_launching(L):
     assert call(l=P) == lirpa.LIRPA_EINVAL          # l without u
     assert call(ws_bytes=need - 1) == lirpa.LIRPA_ENOMEM
     assert "workspace" in lirpa.lirpa_last_error()
-    assert L.lirpa_bound(None, P, 0.1, P, 1, 1, None, None, P, None, None, P, need,
+    assert L.lirpa_bound(None, P, 0.1, P, 1, 1, None, None, P, None, None, None, P, need,
                          None) == lirpa.LIRPA_EINVAL
     L.lirpa_net_destroy(h)
 
@@ -120,4 +121,24 @@ def test_workspace_chunking_is_monotone(L):
     rc, h = _create(L, _fake_layers(wl.ARCHS["wide"]))
     sizes = [L.lirpa_workspace_bytes(h, 9, b, 0) for b in (1, 2, 3, 64, 1024)]
     assert all(x < y for x, y in zip(sizes, sizes[1:]))
+    L.lirpa_net_destroy(h)
+
+
+@pytest.mark.parametrize("arch,B", [("base", 400), ("wide", 1024), ("deep", 1024),
+                                    ("wide", 2048)])
+def test_full_batches_fit_one_chunk(L, arch, B):
+    # bound mode reserves no bound-matrix slab for the passes that run on chip (receptive-field
+    # and fused pass kernels), so every full batch of the benchmark runs as one chunk
+    rc, h = _create(L, _fake_layers(wl.ARCHS[arch]))
+    need = L.lirpa_workspace_bytes(h, 9, B, 0)
+    assert 0 < need < 8 << 30, need
+    L.lirpa_net_destroy(h)
+
+
+def test_workspace_sentinel_for_unaddressable_chunks(L):
+    # gradient mode of the deep net at B = 1024 needs a tape slab over 2^31 floats: the
+    # documented SIZE_MAX, while smaller chunks have a real size
+    rc, h = _create(L, _fake_layers(wl.ARCHS["deep"]))
+    assert L.lirpa_workspace_bytes(h, 9, 1024, 1) == 2**64 - 1
+    assert 0 < L.lirpa_workspace_bytes(h, 9, 64, 1) < 2**40
     L.lirpa_net_destroy(h)

@@ -118,6 +118,10 @@ def test_grad_conv_nets(name):
                lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, alpha, b, j))
 
 
+# least share of the unstable neurons of the sampled C4 sub-domains whose final alpha lies within
+# 1e-3 of the oracle's own fp64 trajectory
+ALPHA_AGREE = 0.95
+
 # optimiser parameters as the library receives them (fp32)
 ADAM = {k: float(np.float32(x)) for k, x in
         (("lr", 0.1), ("beta1", 0.9), ("beta2", 0.999), ("eps_adam", 1e-8))}
@@ -166,6 +170,46 @@ def test_optimize_steps_wide():
                lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, a_fin, b, j))
 
 
+def test_adam_step_replay_wide():
+    """One projected Adam step of the library, replayed in fp64 from the library's own state.
+
+    alpha, m, v are taken from the GPU after t steps, and g = d(sum_s lb)/d alpha from
+    lirpa_bound_grad at that alpha (the same kernels, chunking and reduction order as the
+    gradient the optimiser consumes, so the same values).  The library's next step must equal
+    the bias-corrected Adam update of its own inputs, clipped to [0, 1], to within fp32
+    rounding: m, v to 1e-6 of their terms, alpha to 1e-6.  (A numpy replay of a textbook step,
+    not the oracle.)"""
+    w = wl.wide_opt()
+    B = 4
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=B)
+    net = lirpa.Network(w.layers)
+    x0, C, sp = dev(w.x0), dev(w.C), dev(split)
+    alpha = torch.empty((B, w.n_relu), dtype=torch.float32, device="cuda")
+    m, v = torch.empty_like(alpha), torch.empty_like(alpha)
+    net.optimize(x0, w.eps, C, sp, alpha, m, v, steps=1, lr=ADAM["lr"], fresh=True)
+    b1, b2, lr, ea = ADAM["beta1"], ADAM["beta2"], ADAM["lr"], ADAM["eps_adam"]
+    for t in (1, 2, 3, 4):
+        a_t, m_t, v_t = (x.cpu().double().numpy() for x in (alpha, m, v))
+        _, g = net.bound_grad(x0, w.eps, C, sp, alpha)
+        g = g.cpu().double().numpy()
+        net.optimize(x0, w.eps, C, sp, alpha, m, v, steps=1, lr=lr, t0=t, fresh=False)
+        m_r = b1 * m_t + (1 - b1) * g
+        v_r = b2 * v_t + (1 - b2) * g * g
+        a_r = np.clip(a_t + lr * (m_r / (1 - b1 ** (t + 1))) /
+                      (np.sqrt(v_r / (1 - b2 ** (t + 1))) + ea), 0.0, 1.0)
+        got = {k: x.cpu().double().numpy() for k, x in (("alpha", alpha), ("m", m), ("v", v))}
+        tols = {"m": 1e-6 * (np.abs(b1 * m_t) + np.abs((1 - b1) * g)) + 1e-30,
+                "v": 1e-6 * v_r + 1e-30, "alpha": 1e-6}
+        moved = int((np.abs(got["alpha"] - a_t) > 0).sum())
+        for k, want in (("m", m_r), ("v", v_r), ("alpha", a_r)):
+            d = np.abs(got[k] - want)
+            print(f"step {t + 1} {k}: max |gpu - replay| = {d.max():.3g} "
+                  f"({moved} alphas moved)", flush=True)
+            assert np.all(d <= tols[k]), f"step {t + 1} {k}: off by {d.max():.3g}"
+        assert moved > 0
+
+
 def test_optimize_full_batch_sampled():
     """The alpha-optimised Wide workload at its full batch, in the benchmark's launch
     configuration (one call: fresh start, 20 Adam steps, one chunk).  A sample of sub-domains is
@@ -191,15 +235,25 @@ def test_optimize_full_batch_sampled():
     assert a.min() >= 0 and a.max() <= 1
     assert np.all(best >= trace[0]) and best.mean() > trace[0].mean()
     rng = np.random.default_rng(11)
-    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 10, replace=False)]))
-    _, l, u, _ = ref.bound(rnet, w.x0, w.eps, w.C, split[idx])
+    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(np.arange(1, B - 1), 14,
+                                                           replace=False)]))
+    assert idx.size == 16
+    _, l, u, code = ref.bound(rnet, w.x0, w.eps, w.C, split[idx])
     r = ref.optimize(rnet, w.x0, w.eps, w.C, split[idx], heuristic_alpha(l, u), w.steps, **ADAM)
     for t in range(w.steps + 1):
         check_bound(f"iterate {t}", trace[t, idx], r["lb_trace"][t])
     check_bound("best", best[idx], r["lb_best"])
+    # final alphas of the neurons unstable at the root: fp32 and fp64 trajectories may part where
+    # a gradient entry sits at a kink of the piecewise-linear bound (both one-sided derivatives
+    # are valid); the rest agree
+    unst = code == ref.ST_UNSTABLE
     d = np.abs(a[idx] - r["alpha"])
-    print(f"alpha: max |gpu - oracle| = {d.max():.3g}, {(d > 1e-3).sum()} of {d.size} "
-          f"beyond 1e-3", flush=True)
+    du = d[unst]
+    frac = float((du <= 1e-3).mean())
+    print(f"alpha: max |gpu - oracle| = {du.max():.3g}, {(du > 1e-3).sum()} of {du.size} "
+          f"unstable neurons beyond 1e-3 (agreeing: {frac:.4%}), median {np.median(du):.3g}",
+          flush=True)
+    assert frac >= ALPHA_AGREE, f"alpha: only {frac:.4%} of unstable neurons within 1e-3"
     X = H.box_samples(w.x0, w.eps, 2000, np.random.default_rng(1))
     for b in idx[:4]:
         vals = H.torch_forward(w.layers, X, split[b]) @ w.C.T.astype(np.float64)

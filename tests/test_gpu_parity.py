@@ -2,7 +2,13 @@
 
 Tolerance (fp32 GPU vs fp64 oracle): |gpu - ref| <= 1e-4 + 1e-4 |ref| for every bound, and for
 the intermediate bounds l, u.  Full-size batches run on the GPU exactly as the benchmark runs
-them; the oracle recomputes a sample of their sub-domains one by one."""
+them, and the oracle recomputes every one of their sub-domains.
+
+Stability codes (which case of Eq. 5 / the split constraints of Sec. 3.1 each neuron took) are
+compared byte for byte: on every split neuron, and on every free neuron whose oracle bounds l, u
+are both farther from 0 than the bound tolerance (closer than that, fp32 rounding may decide the
+sign either way).  Every GPU code must also be the one the relaxation table gives for the GPU's
+own l, u and split."""
 import numpy as np
 import pytest
 import torch
@@ -29,12 +35,14 @@ def dev(a):
 
 
 def gpu_bound(layers, x0, eps, C, split=None, alpha=None, B=None, max_ws_bytes=16 << 30,
-              net=None):
+              net=None, codes=False):
     net = net or lirpa.Network(layers)
-    lb, l, u = net.bound(dev(x0), eps, dev(C), dev(split), dev(alpha), B=B, want_lu=True,
-                         max_ws_bytes=max_ws_bytes)
+    out = net.bound(dev(x0), eps, dev(C), dev(split), dev(alpha), B=B, want_lu=True,
+                    max_ws_bytes=max_ws_bytes, want_codes=True)
     torch.cuda.synchronize()
-    return (lb.cpu().double().numpy(), l.cpu().double().numpy(), u.cpu().double().numpy())
+    lb, l, u, code = out
+    res = (lb.cpu().double().numpy(), l.cpu().double().numpy(), u.cpu().double().numpy())
+    return res + (code.cpu().numpy(),) if codes else res
 
 
 def check(name, got, want):
@@ -45,15 +53,40 @@ def check(name, got, want):
     assert np.all(excess <= 0), f"{name}: exceeds tolerance by {excess.max():.3g}"
 
 
+def table_codes(l, u, split):
+    """The relaxation case of each neuron from its own bounds and split (checked in the order
+    split, u <= 0, l >= 0, unstable; codes 1..5 as in the header)."""
+    sp = np.zeros(l.shape, dtype=np.int8) if split is None else split
+    return np.select([sp > 0, sp < 0, u <= 0, l >= 0], [1, 2, 3, 4], 5).astype(np.int8)
+
+
+def check_codes(name, code, code_ref, l, u, l_ref, u_ref, split):
+    """Byte-identical codes on split neurons and on neurons whose oracle bounds are clear of 0;
+    every GPU code consistent with the GPU's own l, u (fp32 as computed)."""
+    own = table_codes(l.astype(np.float32), u.astype(np.float32), split)
+    assert np.array_equal(code, own), f"{name}: a code disagrees with the GPU's own l, u"
+    clear = (np.abs(l_ref) > ATOL + RTOL * np.abs(l_ref)) & \
+        (np.abs(u_ref) > ATOL + RTOL * np.abs(u_ref))
+    sure = clear if split is None else (clear | (split != 0))
+    diff = (code != code_ref) & sure
+    print(f"{name}: codes identical on {int(sure.sum())} of {code.size} neurons "
+          f"({int((~sure).sum())} within rounding of 0), split neurons "
+          f"{0 if split is None else int((split != 0).sum())}", flush=True)
+    assert not diff.any(), f"{name}: {int(diff.sum())} codes differ from the oracle"
+    if split is not None:
+        assert np.all(code[split > 0] == 1) and np.all(code[split < 0] == 2)
+
+
 def test_tiny_every_subdomain():
     w = wl.tiny()
     rnet = ref.RefNet(w.layers)
     split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C))
-    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split)
-    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, split)
+    lb, l, u, code = gpu_bound(w.layers, w.x0, w.eps, w.C, split, codes=True)
+    lr, llr, ulr, cr = ref.bound(rnet, w.x0, w.eps, w.C, split)
     check("tiny lb", lb, lr)
     check("tiny l", l, llr)
     check("tiny u", u, ulr)
+    check_codes("tiny codes", code, cr, l, u, llr, ulr, split)
 
 
 # the benchmark's workspace cap: every full batch here runs as one chunk, as it does there
@@ -61,19 +94,26 @@ BENCH_WS_BYTES = 64 << 30
 
 
 @pytest.mark.parametrize("name", ["base", "wide", "deep"])
-def test_full_size_batches_sampled(name):
+def test_full_size_batches(name):
     w = wl.get(name)
     B = w.B
     rnet = ref.RefNet(w.layers)
     split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C))
     print(f"{name}: B={B} S={w.S} n_relu={w.n_relu}", flush=True)
-    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split, max_ws_bytes=BENCH_WS_BYTES)
-    rng = np.random.default_rng(7)
-    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 14, replace=False)]))
-    lr, llr, ulr, _ = ref.bound(rnet, w.x0, w.eps, w.C, split[idx])
-    check(f"{name} lb", lb[idx], lr)
-    check(f"{name} l", l[idx], llr)
-    check(f"{name} u", u[idx], ulr)
+    net = lirpa.Network(w.layers)
+    need = lirpa.lirpa_workspace_bytes(net.handle, w.S, B, 0)
+    assert need <= BENCH_WS_BYTES, f"{name}: the whole batch does not fit one chunk ({need} B)"
+    lb, l, u, code = gpu_bound(w.layers, w.x0, w.eps, w.C, split, max_ws_bytes=BENCH_WS_BYTES,
+                               net=net, codes=True)
+    # the oracle on every sub-domain, in slices so that progress shows
+    for b0 in range(0, B, 256):
+        sl = slice(b0, min(B, b0 + 256))
+        lr, llr, ulr, cr = ref.bound(rnet, w.x0, w.eps, w.C, split[sl])
+        check(f"{name}[{b0}:{sl.stop}] lb", lb[sl], lr)
+        check(f"{name}[{b0}:{sl.stop}] l", l[sl], llr)
+        check(f"{name}[{b0}:{sl.stop}] u", u[sl], ulr)
+        check_codes(f"{name}[{b0}:{sl.stop}] codes", code[sl], cr, l[sl], u[sl], llr, ulr,
+                    split[sl])
 
 
 def test_small_conv_ragged_batch_with_alpha():
@@ -86,11 +126,12 @@ def test_small_conv_ragged_batch_with_alpha():
     split = wl.make_splits(B, rnet.n_relu, 5, 21, ref.root_unstable(rnet, x0, 0.05, C))
     alpha = rng.uniform(0, 1, (B, rnet.n_relu)).astype(np.float32)
     for a in (None, alpha):
-        lb, l, u = gpu_bound(layers, x0, 0.05, C, split, a)
-        lr, llr, ulr, _ = ref.bound(rnet, x0, 0.05, C, split, a)
+        lb, l, u, code = gpu_bound(layers, x0, 0.05, C, split, a, codes=True)
+        lr, llr, ulr, cr = ref.bound(rnet, x0, 0.05, C, split, a)
         check("small lb", lb, lr)
         check("small l", l, llr)
         check("small u", u, ulr)
+        check_codes("small codes", code, cr, l, u, llr, ulr, split)
 
 
 @pytest.mark.parametrize("name", ["base", "wide", "deep"])
@@ -100,11 +141,12 @@ def test_alpha_on_conv_nets(name):
     rnet = ref.RefNet(w.layers)
     split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=6)
     alpha = np.random.default_rng(3).uniform(0, 1, (6, rnet.n_relu)).astype(np.float32)
-    lb, l, u = gpu_bound(w.layers, w.x0, w.eps, w.C, split, alpha)
-    lr, llr, ulr, code = ref.bound(rnet, w.x0, w.eps, w.C, split, alpha)
+    lb, l, u, code = gpu_bound(w.layers, w.x0, w.eps, w.C, split, alpha, codes=True)
+    lr, llr, ulr, cr = ref.bound(rnet, w.x0, w.eps, w.C, split, alpha)
     check(f"{name}+alpha lb", lb, lr)
     check(f"{name}+alpha l", l, llr)
     check(f"{name}+alpha u", u, ulr)
+    check_codes(f"{name}+alpha codes", code, cr, l, u, llr, ulr, split)
 
 
 @pytest.mark.parametrize("widths", [(20, 30), (40, 64), (50, 99), (30, 128), (6, 7)])
@@ -170,7 +212,9 @@ def test_all_split_matches_closed_form(name):
     w = wl.get(name)
     rng = np.random.default_rng(5)
     split = rng.choice(np.array([-1, 1], dtype=np.int8), size=(3, w.n_relu))
-    lb, _, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split)
+    lb, _, _, code = gpu_bound(w.layers, w.x0, w.eps, w.C, split, codes=True)
+    # every neuron split: the codes are the split directions, exactly
+    assert np.array_equal(code, np.where(split > 0, 1, 2).astype(np.int8))
     for b in range(3):
         M, c = H.affine_map_of_split_net(w.layers, split[b])
         check(f"{name} all-split", lb[b], H.box_min_of_affine(w.C, M, c, w.x0, w.eps))
@@ -224,3 +268,43 @@ def test_chunking_permutation_determinism():
     perm = np.random.default_rng(1).permutation(B)
     lb4, _, _ = gpu_bound(w.layers, w.x0, w.eps, w.C, split[perm], net=net)
     assert np.array_equal(lb4, lb1[perm]), "sub-domain order changed results"
+
+
+def test_validate_reports_bad_inputs(monkeypatch):
+    """LIRPA_VALIDATE=1: a call with out-of-range device inputs (memory-safe, undefined results)
+    is reported by the next call as LIRPA_EDATA, which enqueues nothing and clears the report;
+    without the variable nothing is checked."""
+    w = wl.tiny()
+    rnet = ref.RefNet(w.layers)
+    split = w.splits(ref.root_unstable(rnet, w.x0, w.eps, w.C), B=8)
+    net = lirpa.Network(w.layers)
+    x0, C, sp = dev(w.x0), dev(w.C), dev(split)
+    alpha = dev(np.full((8, w.n_relu), 0.5, dtype=np.float32))
+
+    def call(x0_=x0, sp_=sp, al_=alpha):
+        lb = net.bound(x0_, w.eps, C, sp_, al_)
+        torch.cuda.synchronize()
+        return lb
+
+    monkeypatch.setenv("LIRPA_VALIDATE", "1")
+    call()
+    call()  # nothing to report
+    bad_split = split.copy()
+    bad_split[3, 5] = 2
+    bad_alpha = np.full((8, w.n_relu), 0.5, dtype=np.float32)
+    bad_alpha[7, 0] = 1.5
+    bad_x0 = w.x0.copy()
+    bad_x0[1] = np.nan
+    for what, kw in (("split", dict(sp_=dev(bad_split))), ("alpha", dict(al_=dev(bad_alpha))),
+                     ("x0", dict(x0_=dev(bad_x0)))):
+        call(**kw)  # enqueued; its check runs on the device
+        with pytest.raises(lirpa.LirpaError) as ei:
+            call()
+        assert ei.value.code == lirpa.LIRPA_EDATA and what in str(ei.value), str(ei.value)
+        print(f"validate: {ei.value}", flush=True)
+        lb = call()  # the report was cleared
+        want, *_ = ref.bound(rnet, w.x0, w.eps, w.C, split, np.full((8, w.n_relu), 0.5))
+        check("validate lb after a report", lb.cpu().double().numpy(), want)
+    monkeypatch.delenv("LIRPA_VALIDATE")
+    call(sp_=dev(bad_split))
+    call()  # not checked, not reported

@@ -176,6 +176,67 @@ def test_one_neuron_triangle_closed_form(v, alpha):
 
 
 # ----------------------------------------------------------------------------------------------
+# A layer-2 intermediate bound over unstable layer-1 neurons (Eq. 4-8), derived by hand.
+# ----------------------------------------------------------------------------------------------
+def two_hidden_net():
+    """x in R^2; h1 = [x1 - x2 - 0.5, 2 x2 + 1]; h2 = g1_a - 2 g1_b + 0.25; f = g2 - 1."""
+    layers = [dict(wl.fc(2, 2), W=np.array([[1, -1], [0, 2]], np.float32),
+                   b=np.array([-0.5, 1], np.float32)),
+              dict(wl.fc(2, 1), W=np.array([[1, -2]], np.float32),
+                   b=np.array([0.25], np.float32)),
+              dict(wl.fc(1, 1), W=np.array([[1]], np.float32), b=np.array([-1], np.float32))]
+    return layers, np.array([0.5, -0.25], np.float32), 0.5
+
+
+@pytest.mark.parametrize("alpha", [None, (0.0, 0.0, 0.0), (1.0, 1.0, 1.0), (0.25, 0.5, 0.75)])
+def test_two_hidden_layer_intermediate_bound_closed_form(alpha):
+    """Worked by hand from Eq. 4-8 with x0 = (0.5, -0.25), eps = 0.5 (box [0,1] x [-0.75,0.25]).
+
+    Layer 1 (exact): h1_a in [-0.75, 1.25] (a_up = 0.625, b_up = 0.46875), h1_b in [-0.5, 1.5]
+    (a_up = 0.75, b_up = 0.375); both unstable.
+    Pass 2, row +e over h2: coefficients (1, -2) over g1; a takes its lower line (slope alpha_a),
+    b its upper line (slope 0.75, intercept -2 * 0.375); through T_1: A_x = (alpha_a,
+    -alpha_a - 3), beta = -2 - alpha_a / 2; concretised: l2 = -2.75 - 0.75 alpha_a.
+    Row -e: coefficients (-1, 2); a takes its upper line, b its lower line (slope alpha_b);
+    A_x = (-0.625, 0.625 + 4 alpha_b), beta = -0.40625 + 2 alpha_b; lb = -1.5 - alpha_b, so
+    u2 = 1.5 + alpha_b.  Layer 2 is unstable.  Final pass, spec 1 over f = g2 - 1: the
+    coefficient 1 over g2 takes the lower line (slope alpha_2), which scales the row +e, so
+    lb = -1 + alpha_2 (-2.75 - 0.75 alpha_a).  The heuristic alpha is each neuron's a_up."""
+    layers, x0, eps = two_hidden_net()
+    net = ref.RefNet(layers)
+    C = np.array([[1.0]], np.float32)
+    al = None if alpha is None else np.array([alpha], np.float32)
+    lb, l, u, code = ref.bound(net, x0, eps, C, alpha=al, B=1)
+    np.testing.assert_allclose(l[0, :2], [-0.75, -0.5], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(u[0, :2], [1.25, 1.5], rtol=0, atol=1e-15)
+    a_a, a_b = (0.625, 0.75) if alpha is None else (np.float64(al[0, 0]), np.float64(al[0, 1]))
+    l2, u2 = -2.75 - 0.75 * a_a, 1.5 + a_b
+    np.testing.assert_allclose([l[0, 2], u[0, 2]], [l2, u2], rtol=0, atol=1e-14)
+    assert list(code[0]) == [ref.ST_UNSTABLE] * 3
+    a_2 = u2 / (u2 - l2) if alpha is None else np.float64(al[0, 2])
+    np.testing.assert_allclose(lb[0, 0], -1 + a_2 * (-2.75 - 0.75 * a_a), rtol=0, atol=1e-14)
+    # every bound is sound: h2 and f sampled over the box
+    X = H.box_samples(x0, eps, 20000, np.random.default_rng(0))
+    out, pre = H.torch_forward(layers, X, return_pre=True)
+    assert l2 <= pre[:, 2].min() + 1e-12 and pre[:, 2].max() <= u2 + 1e-12
+    assert lb[0, 0] <= out[:, 0].min() + 1e-12
+
+
+def test_ref_forward_matches_torch():
+    """The oracle's plain forward evaluation of f_s (split ReLUs replaced by the identity or 0)
+    against torch's conv2d / linear in fp64, with and without a split vector."""
+    layers = wl.random_net(H.small_conv_arch(), 3)
+    net = ref.RefNet(layers)
+    rng = np.random.default_rng(3)
+    X = rng.uniform(-1, 1, (7, wl.n_in(layers[0])))
+    np.testing.assert_allclose(ref.forward(net, X), H.torch_forward(layers, X), rtol=1e-12,
+                               atol=1e-12)
+    split = rng.choice(np.array([-1, 0, 1], np.int8), size=net.n_relu)
+    np.testing.assert_allclose(ref.forward(net, X, split), H.torch_forward(layers, X, split),
+                               rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------------------------
 # App. A.1: the paper's worked counter-example.
 # ----------------------------------------------------------------------------------------------
 def _a1_net():
