@@ -112,6 +112,19 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
                 const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
                 int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* lirpa_bound for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same computation and outputs, with
+ * no workspace argument.  Its workspace is the library's own scratch array of 128 MiB per
+ * device (a static device array, held from the time the library is loaded on the device until
+ * the process ends); the call allocates and frees nothing.  A batch whose workspace exceeds it
+ * runs in chunks of as many sub-domains as fit (results are identical to any other chunking).
+ * LIRPA_ENOMEM when one sub-domain alone needs more than 128 MiB.  Every call on a device
+ * shares that device's array and leaves its contents behind: calls that overlap on one device
+ * (from several streams or threads) race and give undefined results. */
+int lirpa_bound_noalloc(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                        const int8_t* split, const float* alpha, float* lb, float* l_out,
+                        float* u_out, int8_t* code_out, hipStream_t stream);
+
 /* As lirpa_bound, plus grad[b][:] = d(sum_s lb[b][s]) / d alpha[b][:] (alpha required).
  * full != 0 differentiates through the recomputed intermediate bounds (Sec. 3.1: they depend on
  * the alphas of earlier layers); full == 0 holds them fixed.  Split and stable neurons get

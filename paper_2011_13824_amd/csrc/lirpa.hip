@@ -25,6 +25,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <type_traits>
 #include <vector>
@@ -101,6 +102,21 @@ long n_out_of(const lirpa_layer& t) { return (long)t.out_c * t.out_h * t.out_w; 
 long round_up(long x, long m) { return (x + m - 1) / m * m; }
 
 }  // namespace
+
+// Findings of the check of a call's device inputs (LIRPA_VALIDATE=1), one word per kind: [0] a
+// split value outside {-1, 0, 1} (Sec. 3.1 split constraints), [1] an alpha outside [0, 1] or not
+// a number (Eq. 5), [2] a non-finite x0, [3] a non-finite spec entry.  Each device holds its own
+// copy; a finding is recorded by plain stores of 1 (idempotent, no atomics) and read and cleared
+// by the host through the symbol.
+static __device__ unsigned int g_check[4];
+
+// Scratch array of lirpa_bound_noalloc, the workspace of callers that cannot allocate device
+// memory.  Each device holds its own copy from the time the library is loaded on it until the
+// process ends.  Host code never passes the array's name to a kernel or a copy (it is a host-side
+// stand-in there): it takes the device address of the current device's copy, looked up once per
+// device with hipGetSymbolAddress (scratch_address()).
+constexpr size_t kScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 struct lirpa_net {
   std::vector<lirpa_layer> T;  // T[0..L-1] = T_1..T_L
@@ -4170,12 +4186,6 @@ __global__ void __launch_bounds__(kBlock) k_zero(long n, float* __restrict__ p) 
 // ---------------------------------------------------------------------------------------------
 // Input check (LIRPA_VALIDATE=1)
 // ---------------------------------------------------------------------------------------------
-// Findings of the check of a call's device inputs, one word per kind: [0] a split value outside
-// {-1, 0, 1} (Sec. 3.1 split constraints), [1] an alpha outside [0, 1] or not a number (Eq. 5),
-// [2] a non-finite x0, [3] a non-finite spec entry.  Each device holds its own copy; a finding
-// is recorded by plain stores of 1 (idempotent, no atomics) and read and cleared by the host.
-__device__ unsigned int g_check[4];
-
 __global__ void __launch_bounds__(kBlock)
     k_check_inputs(long n_split, const int8_t* __restrict__ split, long n_alpha,
                    const float* __restrict__ alpha, long n_x0, const float* __restrict__ x0,
@@ -5302,14 +5312,19 @@ int grad_chunk(const Chunk& c, int full) {
   return LIRPA_OK;
 }
 
-int check_common(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
-                 void* ws) {
+int check_args(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B) {
   if (!net) return fail(LIRPA_EINVAL, "net is null");
   if (!x0) return fail(LIRPA_EINVAL, "x0 is null");
   if (!C) return fail(LIRPA_EINVAL, "C is null");
   if (S < 1) return fail(LIRPA_EINVAL, "S must be >= 1 (got %d)", S);
   if (B < 1) return fail(LIRPA_EINVAL, "B must be >= 1 (got %d)", B);
   if (!std::isfinite(eps) || eps < 0.f) return fail(LIRPA_EINVAL, "eps must be finite and >= 0");
+  return LIRPA_OK;
+}
+
+int check_common(const lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                 void* ws) {
+  if (int e = check_args(net, x0, eps, C, S, B)) return e;
   if (!ws) return fail(LIRPA_EINVAL, "workspace is null");
   return LIRPA_OK;
 }
@@ -5389,6 +5404,47 @@ int validate_enqueue(const lirpa_net* net, const float* x0, const float* C, int 
   });
 }
 
+
+// lirpa_bound on a workspace that holds chunks of Bc sub-domains (plan p).
+int bound_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float eps, const float* C,
+              int S, int B, const int8_t* split, const float* alpha, float* lb, float* l_out,
+              float* u_out, int8_t* code_out, void* ws, hipStream_t stream) {
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
+    if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
+    if (code_out && net->n_relu)
+      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
+                           (size_t)c.nb * net->n_relu, stream))
+        return e;
+  }
+  return LIRPA_OK;
+}
+
+constexpr int kMaxDevices = 64;
+void* g_scratch_addr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+// The current device's copy of the scratch array, looked up once per device.
+int scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+    return fail(LIRPA_EDEVICE, "hipGetDevice failed");
+  if (dev >= kMaxDevices) return fail(LIRPA_EUNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+      return fail(LIRPA_EDEVICE, "hipGetSymbolAddress of the scratch array failed on device %d",
+                  dev);
+    g_scratch_addr[dev] = ptr;
+  }
+  *out = g_scratch_addr[dev];
+  return LIRPA_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
@@ -5465,18 +5521,29 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
   if (Bc < 1)
     return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
                 make_plan(net, S, 1).total);
-  if (int e = validate_report(stream)) return e;
-  if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
-  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
-  for (long b0 = 0; b0 < B; b0 += Bc) {
-    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
-    if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
-    if (code_out && net->n_relu)
-      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
-                           (size_t)c.nb * net->n_relu, stream))
-        return e;
-  }
-  return LIRPA_OK;
+  return bound_run(net, p, Bc, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out, ws,
+                   stream);
+}
+
+int lirpa_bound_noalloc(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                        const int8_t* split, const float* alpha, float* lb, float* l_out,
+                        float* u_out, int8_t* code_out, hipStream_t stream) {
+  // host checks first: a rejected call touches no device
+  if (int e = check_args(net, x0, eps, C, S, B)) return e;
+  if (!lb) return fail(LIRPA_EINVAL, "lb is null");
+  if ((l_out == nullptr) != (u_out == nullptr))
+    return fail(LIRPA_EINVAL, "l_out and u_out must both be given or both be null");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, kScratchBytes, &p);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM,
+                "one sub-domain needs %zu bytes of workspace, beyond the library's scratch array "
+                "of %zu MiB; call lirpa_bound with a workspace",
+                make_plan(net, S, 1).total, kScratchBytes >> 20);
+  void* ws = nullptr;
+  if (int e = scratch_address(&ws)) return e;
+  return bound_run(net, p, Bc, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out, ws,
+                   stream);
 }
 
 int lirpa_bound_grad(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,

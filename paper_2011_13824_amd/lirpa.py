@@ -40,7 +40,8 @@ class lirpa_kernel_time(ctypes.Structure):
 
 
 SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
-           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_grad", "lirpa_optimize",
+           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_noalloc", "lirpa_bound_grad",
+           "lirpa_optimize",
            "lirpa_timing_begin", "lirpa_timing_end", "lirpa_last_error")
 
 _lib = None
@@ -66,6 +67,8 @@ def load() -> ctypes.CDLL:
     L.lirpa_workspace_bytes.restype = sz
     L.lirpa_bound.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, sz, P]
     L.lirpa_bound.restype = i
+    L.lirpa_bound_noalloc.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P]
+    L.lirpa_bound_noalloc.restype = i
     L.lirpa_bound_grad.argtypes = [P, P, f, P, i, i, P, P, i, P, P, P, sz, P]
     L.lirpa_bound_grad.restype = i
     L.lirpa_optimize.argtypes = [P, P, f, P, i, i, P, P, P, P, ctypes.POINTER(lirpa_opt_params),
@@ -162,6 +165,18 @@ def lirpa_bound(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out,
                               _dev(u_out, torch.float32, "u_out"),
                               _dev(code_out, torch.int8, "code_out"), _dev(ws, None, "ws"),
                               int(ws_bytes), _stream(stream)))
+
+
+def lirpa_bound_noalloc(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out,
+                        stream=None):
+    _check(load().lirpa_bound_noalloc(net, _dev(x0, torch.float32, "x0"), float(eps),
+                                      _dev(C, torch.float32, "C"), int(S), int(B),
+                                      _dev(split, torch.int8, "split"),
+                                      _dev(alpha, torch.float32, "alpha"),
+                                      _dev(lb, torch.float32, "lb"),
+                                      _dev(l_out, torch.float32, "l_out"),
+                                      _dev(u_out, torch.float32, "u_out"),
+                                      _dev(code_out, torch.int8, "code_out"), _stream(stream)))
 
 
 def lirpa_bound_grad(net, x0, eps, C, S, B, split, alpha, full, lb, grad, ws, ws_bytes,
