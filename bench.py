@@ -1,12 +1,14 @@
 #!/usr/bin/env python
 """Throughput of batched LiRPA sub-domain bounds on one MI355X.
 
-One step = one lirpa_bound call over the whole batch of the workload (default: the base conv
-net Conv(3->8, k4 s2 p1)-Conv(8->16, k4 s2 p1)-FC(1024->100)-FC(100->10) on 3x32x32 inputs,
-400 sub-domains, 9 margin specs): layer-1 bounds, every intermediate pass (rows +-e_j of
-each hidden layer, per sub-domain under its own splits) and the final pass, each backward stage
-with its relaxation or concretisation fused.  Inputs are synthetic and resident in HBM before
-the timed region.  Prints one JSON line.
+Default workload: alpha-optimised bounds of the wide conv net Conv(3->16, k4 s2 p1)-Conv(16->32,
+k4 s2 p1)-FC(2048->100)-FC(100->10) on 3x32x32 inputs, 2048 sub-domains with up to 16 splits
+each, 9 margin specs.  One step = one lirpa_optimize call over the whole batch: a heuristic bound
+pass, then 20 projected Adam steps on the lower slopes (each a bound with every intermediate
+pass recomputed under the sub-domain's splits and its gradient through those bounds), the best
+bound of the 21 iterates kept.  --workload picks the plain-bound workloads instead (one step =
+one lirpa_bound call: layer-1 bounds, every intermediate pass and the final pass).  Inputs are
+synthetic and resident in HBM before the timed region.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -150,9 +152,46 @@ def stage_work(layers, S, B):
     return work
 
 
-def path_flops(layers, S, B, launched):
-    """Algorithmic flops of one step over the kernel classes that were launched."""
-    return sum(f for cls, (f, _) in stage_work(layers, S, B).items() if cls in launched)
+def grad_work(layers, S, B):
+    """Algorithmic work per launch of the reverse-sweep kernel classes: {class: (flop, bytes)}.
+
+    Pass P (rows Q = B*R) is swept from its witnesses forward.  The witness forward through
+    layer m costs 2 * Q * MACs(T_m) flops; its bytes are its input per row (the sign of A_x, one
+    byte per input, for m = 1; the relaxed activations over g^(m-1) otherwise), the recorded
+    coefficients over g^(m) and its output over g^(m) (4 bytes per entry each).  The adjoint
+    sums read per (sub-domain, neuron) what the forward left (3 floats per group of 8 rows).
+    The receptive-field pass 2 rebuilds each row's relaxed window and its A_x on MFMA and runs
+    W_1 over the window's witness: twice the window flops of the bound pass; bytes: the layer-1
+    relaxation read (3 floats per neuron and sub-domain) and one partial sum written per
+    (window, window neuron)."""
+    from paper_2011_13824_amd import workloads as wl
+    L = len(layers)
+    n = [wl.n_in(layers[0])] + [wl.n_out(t) for t in layers]
+
+    def macs(t):
+        if t["kind"] == wl.CONV:
+            return wl.n_out(t) * t["in_c"] * t["k"] * t["k"]
+        return t["out_c"] * t["in_c"]
+
+    work = {}
+    for P in range(L, 1, -1):
+        R = S if P == L else 2 * n[P]
+        Q = B * R
+        if P == 2 and P < L and layers[0]["kind"] == wl.CONV and layers[1]["kind"] == wl.CONV:
+            t1, t2 = layers[0], layers[1]
+            wmacs = t1["out_c"] * t2["k"] ** 2 * t1["in_c"] * t1["k"] ** 2
+            parts = B * (t2["out_c"] // 8) * t2["out_h"] * t2["out_w"] * t1["out_c"] * t2["k"] ** 2
+            work["pass2_window_grad[layer1,pass2]"] = (4.0 * Q * wmacs,
+                                                       4.0 * (3 * B * n[1] + parts))
+            work["pass2_grad_gather[layer1,pass2]"] = (0.0, 4.0 * (parts + 3 * B * n[1]))
+            continue
+        for m in range(1, P):
+            t = layers[m - 1]
+            inb = n[0] * Q if m == 1 else 4.0 * n[m - 1] * Q
+            work[f"fwd[layer{m},pass{P}]"] = (2.0 * Q * macs(t), inb + 8.0 * n[m] * Q)
+            work[f"grad_gather[layer{m},pass{P}]"] = (0.0, 12.0 * n[m] * Q / 8 + 12.0 * B * n[m])
+            work[f"grad_reduce[layer{m},pass{P}]"] = (0.0, 8.0 * n[m] * Q + 12.0 * B * n[m])
+    return work
 
 
 def traffic_record(workload, kernel):
@@ -186,6 +225,21 @@ def cpu_baseline(w, budget_s=20.0):
     rnet = ref.RefNet(w.layers)
     cand = ref.root_unstable(rnet, w.x0, w.eps, w.C)
     split = w.splits(cand)
+    if w.steps > 0:
+        # the same work per sub-domain as the GPU step: a heuristic bound pass for the fresh
+        # start, then the projected Adam loop (a bound and a gradient per step, one more bound)
+        n = min(16, w.B)
+        t0 = time.perf_counter()
+        _, l, u, _ = ref.bound(rnet, w.x0, w.eps, w.C, split[:n], nthreads=threads)
+        a0 = np.where((l < 0) & (u > 0), u / np.where(u - l > 0, u - l, 1),
+                      np.where(l >= 0, 1.0, 0.0))
+        ref.optimize(rnet, w.x0, w.eps, w.C, split[:n], a0, w.steps, lr=w.lr, nthreads=threads)
+        dt = time.perf_counter() - t0
+        return {"value": round(n / dt, 4), "unit": "subdomains/s", "cores": threads,
+                "kind": "oracle",
+                "sample": f"first {n} of the {w.B} sub-domains of the {w.name} batch, heuristic "
+                          f"start and {w.steps} Adam steps (fp64 C oracle, OpenMP, "
+                          f"{dt:.1f} s wall)"}
     probe = min(8, w.B)
     t0 = time.perf_counter()
     ref.bound(rnet, w.x0, w.eps, w.C, split[:probe], nthreads=threads)
@@ -205,7 +259,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="base",
+    ap.add_argument("--workload", default="wide_opt",
                     choices=["tiny", "base", "wide", "deep", "wide_opt"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle time")
@@ -290,11 +344,13 @@ def main():
         step()
     times = lirpa.lirpa_timing_end()
     torch.cuda.synchronize()
-    work = {} if optimise else stage_work(w.layers, S, B)
+    work = stage_work(w.layers, S, B)
+    if optimise:
+        work.update(grad_work(w.layers, S, B))
     stages = {}
     for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):
         f, b = work.get(cls, (0.0, 0.0))
-        f, b = f * args.steps, b * args.steps
+        f, b = f * launches, b * launches
         sec = tot_ms / 1e3
         stages[cls] = {"ms_per_step": round(tot_ms / args.steps, 4),
                        "launches_per_step": launches / args.steps,
@@ -303,10 +359,8 @@ def main():
     dom = max(times, key=lambda c: times[c][0])
     tot_ms, launches = times[dom]
     f, b = work.get(dom, (0.0, 0.0))
-    f, b = f * args.steps, b * args.steps
-    if optimise:
-        roof = {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None}
-    elif f > 0:
+    f, b = f * launches, b * launches
+    if f > 0 and (b == 0 or f / b >= PEAK_FP32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)):
         achieved = f / launches / (tot_ms / launches / 1e3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_TFLOPS, 4)}
@@ -336,8 +390,8 @@ def main():
                    "alpha": (f"{w.steps} Adam steps (lr {w.lr}) from the upper slope"
                              if optimise else "upper slope"),
                    "ws_gib": round(ws_bytes / 2**30, 2)},
-        "path_tflops": (None if optimise else
-                        round(path_flops(w.layers, S, B, times) / (ms / 1e3) / 1e12, 3)),
+        "path_tflops": round(sum(work.get(c, (0.0, 0.0))[0] * times[c][1] for c in times)
+                             / args.steps / (ms / 1e3) / 1e12, 3),
         "roofline": roof,
         "stages": stages,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(w, args.cpu_budget),

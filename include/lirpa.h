@@ -86,7 +86,8 @@ int64_t lirpa_net_num_relu(const lirpa_net* net);
 
 /* Workspace bytes for one call processing up to B_chunk sub-domains at a time with S spec
  * rows (the batch of sub-domains of Sec. 3.3 is bounded by memory).  mode 0 = lirpa_bound,
- * 1 = lirpa_bound_grad / lirpa_optimize.  A call given a smaller workspace processes its
+ * 1 = lirpa_bound_grad / lirpa_optimize, 2 = lirpa_bound_ul, 3 = lirpa_optimize_ul (other
+ * values: 0).  A call given a smaller workspace processes its
  * batch in chunks of as many sub-domains as fit.  Returns 0 for invalid arguments and
  * SIZE_MAX when a chunk of B_chunk sub-domains cannot run at all (one bound-matrix slab would
  * exceed 2^31 floats, the kernels' 32-bit element offsets); a call then uses smaller chunks. */
@@ -125,6 +126,18 @@ int lirpa_bound_noalloc(lirpa_net* net, const float* x0, float eps, const float*
                         const int8_t* split, const float* alpha, float* lb, float* l_out,
                         float* u_out, int8_t* code_out, hipStream_t stream);
 
+/* Lower AND upper bounds of the spec rows, the pair (f_lo, f_hi) of Eq. 8 that Algorithm 1's
+ * bounding step returns for every sub-domain:
+ *   lb[b][s] <= min_{x in box} (C f_b(x))_s   and   ub[b][s] >= max_{x in box} (C f_b(x))_s,
+ * ub being max_x of the upper linear function U, computed as -(the lower bound of the rows -C).
+ * The intermediate passes (and their l, u, codes) are those of lirpa_bound and are shared by
+ * both sides; the final pass bounds the 2S rows [C; -C].  alpha (optional) is the lower slope of
+ * both sides.  Arguments as in lirpa_bound; lb, ub [B][S] out; workspace mode 2. */
+int lirpa_bound_ul(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                   const int8_t* split, const float* alpha, float* lb, float* ub, float* l_out,
+                   float* u_out, int8_t* code_out, void* ws, size_t ws_bytes,
+                   hipStream_t stream);
+
 /* As lirpa_bound, plus grad[b][:] = d(sum_s lb[b][s]) / d alpha[b][:] (alpha required).
  * full != 0 differentiates through the recomputed intermediate bounds (Sec. 3.1: they depend on
  * the alphas of earlier layers); full == 0 holds them fixed.  Split and stable neurons get
@@ -156,6 +169,18 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
                    const int8_t* split, float* alpha, float* adam_m, float* adam_v,
                    const lirpa_opt_params* params, float* lb_best, float* lb_trace, void* ws,
                    size_t ws_bytes, hipStream_t stream);
+
+/* Optimised lower AND upper bounds (Eq. 9, each side read as the tightest sound bound: f_lo =
+ * max over alpha of min_x L, f_hi = min over alpha of max_x U).  The two sides are optimised
+ * with separate slopes, as the intermediate bounds depend on them: alpha_lo, m_lo, v_lo drive
+ * lb_best exactly as lirpa_optimize does for C; alpha_up, m_up, v_up drive ub_best, which is
+ * -(lirpa_optimize's lb_best for the rows -C).  All [B][n_relu] in/out, lb_best and ub_best
+ * [B][S] out; params as in lirpa_optimize (shared by both sides); workspace mode 3. */
+int lirpa_optimize_ul(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                      const int8_t* split, float* alpha_lo, float* m_lo, float* v_lo,
+                      float* alpha_up, float* m_up, float* v_up, const lirpa_opt_params* params,
+                      float* lb_best, float* ub_best, void* ws, size_t ws_bytes,
+                      hipStream_t stream);
 
 /* Kernel timing, for profiling harnesses.  Between lirpa_timing_begin() and
  * lirpa_timing_end() every kernel the calls of this thread enqueue is bracketed by a pair of

@@ -4183,6 +4183,36 @@ __global__ void __launch_bounds__(kBlock) k_zero(long n, float* __restrict__ p) 
   if (i < n) p[i] = 0.f;
 }
 
+// Spec rows of an upper bound (Eq. 8: max_x U = -min_x of the lower function of -C): out holds
+// [C; -C] (both = 1) or -C alone, [rows][nL].
+__global__ void __launch_bounds__(kBlock) k_spec_pm(long n, const float* __restrict__ C,
+                                                    float* __restrict__ out, int both) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  if (both) {
+    out[i] = C[i];
+    out[n + i] = -C[i];
+  } else {
+    out[i] = -C[i];
+  }
+}
+
+// Bounds of the rows [C; -C] of nb sub-domains ([nb][2S]) into lb = the C rows and
+// ub = -(the -C rows), [nb][S] each.
+__global__ void __launch_bounds__(kBlock) k_split_ul(long nb, long S, const float* __restrict__ lb2,
+                                                     float* __restrict__ lb, float* __restrict__ ub) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= nb * S) return;
+  const long b = i / S, s_ = i % S;
+  lb[i] = lb2[b * 2 * S + s_];
+  ub[i] = -lb2[b * 2 * S + S + s_];
+}
+
+__global__ void __launch_bounds__(kBlock) k_negate(long n, float* __restrict__ p) {
+  long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = -p[i];
+}
+
 // ---------------------------------------------------------------------------------------------
 // Input check (LIRPA_VALIDATE=1)
 // ---------------------------------------------------------------------------------------------
@@ -4227,6 +4257,9 @@ struct Plan {
   // 8 rows (whether any row of the group carries weight)
   size_t off_gpart = 0, off_gflag = 0;
   long fwd_floats = 0;
+  // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
+  // the [Bc][2S] bounds of those rows before they are split into lb and ub
+  size_t off_spec = 0, off_lb2 = 0;
 };
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -5329,14 +5362,33 @@ int check_common(const lirpa_net* net, const float* x0, float eps, const float* 
   return LIRPA_OK;
 }
 
+// Workspace plan of a call kind: 0 lirpa_bound, 1 lirpa_bound_grad / lirpa_optimize,
+// 2 lirpa_bound_ul (the final pass bounds the 2S rows [C; -C]), 3 lirpa_optimize_ul (the
+// optimiser's plan and the rows -C).
+Plan plan_for(const lirpa_net* net, long S, long Bc, int mode) {
+  if (mode <= 1) return make_plan(net, S, Bc, mode);
+  Plan p = make_plan(net, mode == 2 ? 2 * S : S, Bc, mode == 2 ? 0 : 1);
+  if (p.total == (size_t)-1) return p;
+  const long nL = net->n[net->L];
+  size_t o = p.total;
+  p.off_spec = o;
+  o = align256(o + (size_t)(mode == 2 ? 2 : 1) * S * nL * 4);
+  if (mode == 2) {
+    p.off_lb2 = o;
+    o = align256(o + (size_t)Bc * 2 * S * 4);
+  }
+  p.total = o;
+  return p;
+}
+
 // Largest chunk whose workspace fits.
 long fit_chunk(const lirpa_net* net, long S, long B, size_t ws_bytes, Plan* out, int mode = 0) {
   long lo = 0, hi = B;
   while (lo < hi) {
     long mid = (lo + hi + 1) / 2;
-    if (make_plan(net, S, mid, mode).total <= ws_bytes) lo = mid; else hi = mid - 1;
+    if (plan_for(net, S, mid, mode).total <= ws_bytes) lo = mid; else hi = mid - 1;
   }
-  if (lo > 0) *out = make_plan(net, S, lo, mode);
+  if (lo > 0) *out = plan_for(net, S, lo, mode);
   return lo;
 }
 
@@ -5445,6 +5497,63 @@ int scratch_address(void** out) {
   return LIRPA_OK;
 }
 
+
+int check_opt_params(const lirpa_opt_params& op) {
+  if (op.steps < 0 || op.t0 < 0 || !(op.lr >= 0.f) || !(op.beta1 >= 0.f && op.beta1 < 1.f) ||
+      !(op.beta2 >= 0.f && op.beta2 < 1.f) || !(op.eps_adam > 0.f))
+    return fail(LIRPA_EINVAL, "bad optimiser parameters");
+  return LIRPA_OK;
+}
+
+// lirpa_optimize on a workspace that holds chunks of Bc sub-domains (plan p, gradient mode).
+int optimize_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float eps,
+                 const float* C, int S, int B, const int8_t* split, float* alpha, float* adam_m,
+                 float* adam_v, const lirpa_opt_params& op, float* lb_best, float* lb_trace,
+                 void* ws, hipStream_t stream) {
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
+    long na = c.nb * net->n_relu, ns = c.nb * S;
+    float* a = alpha + b0 * net->n_relu;
+    float* lbt = at<float>(ws, p.off_lbt);
+    if (op.fresh) {
+      Chunk h = c;
+      h.alpha = nullptr;
+      h.tape = false;
+      if (int e = bound_chunk(h, C, lbt)) return e;
+      if (int e = launch_k("alpha_init", stream, [&] {
+            hipLaunchKernelGGL(k_alpha_init, grid_for(na), dim3(kBlock), 0, stream, na, h.L, h.U,
+                               a, adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu);
+          }))
+        return e;
+    }
+    const int tbase = op.fresh ? 0 : op.t0;
+    for (int t = 0; t <= op.steps; ++t) {
+      c.tape = (t < op.steps);
+      if (int e = bound_chunk(c, C, lbt)) return e;
+      float* tr = lb_trace ? lb_trace + ((long)t * B + b0) * S : nullptr;
+      if (int e = launch_k("best", stream, [&] {
+            hipLaunchKernelGGL(k_best, grid_for(ns), dim3(kBlock), 0, stream, ns, lbt,
+                               lb_best + b0 * S, tr, (int)(t == 0));
+          }))
+        return e;
+      if (t == op.steps) break;
+      if (int e = grad_chunk(c, 1)) return e;
+      int tt = tbase + t + 1;
+      float c1 = (float)(1.0 - std::pow((double)op.beta1, tt));
+      float c2 = (float)(1.0 - std::pow((double)op.beta2, tt));
+      if (int e = launch_k("adam", stream, [&] {
+            hipLaunchKernelGGL(k_adam, grid_for(na), dim3(kBlock), 0, stream, na, a,
+                               adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu,
+                               at<float>(ws, p.off_ga), op.lr, op.beta1, op.beta2, op.eps_adam,
+                               c1, c2);
+          }))
+        return e;
+    }
+  }
+  return LIRPA_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
@@ -5505,8 +5614,8 @@ void lirpa_net_destroy(lirpa_net* net) { delete net; }
 int64_t lirpa_net_num_relu(const lirpa_net* net) { return net ? net->n_relu : -1; }
 
 size_t lirpa_workspace_bytes(const lirpa_net* net, int S, int B_chunk, int mode) {
-  if (!net || S < 1 || B_chunk < 1 || (mode != 0 && mode != 1)) return 0;
-  return make_plan(net, S, B_chunk, mode).total;
+  if (!net || S < 1 || B_chunk < 1 || mode < 0 || mode > 3) return 0;
+  return plan_for(net, S, B_chunk, mode).total;
 }
 
 int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
@@ -5578,10 +5687,7 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
   if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
   if (!alpha || !adam_m || !adam_v || !params || !lb_best)
     return fail(LIRPA_EINVAL, "alpha, adam_m, adam_v, params and lb_best must be given");
-  const lirpa_opt_params& op = *params;
-  if (op.steps < 0 || op.t0 < 0 || !(op.lr >= 0.f) || !(op.beta1 >= 0.f && op.beta1 < 1.f) ||
-      !(op.beta2 >= 0.f && op.beta2 < 1.f) || !(op.eps_adam > 0.f))
-    return fail(LIRPA_EINVAL, "bad optimiser parameters");
+  if (int e = check_opt_params(*params)) return e;
   Plan p;
   long Bc = fit_chunk(net, S, B, ws_bytes, &p, 1);
   if (Bc < 1)
@@ -5589,50 +5695,94 @@ int lirpa_optimize(lirpa_net* net, const float* x0, float eps, const float* C, i
                 make_plan(net, S, 1, 1).total);
   if (int e = validate_report(stream)) return e;
   // alpha is an input only when the call continues from the caller's state
-  if (int e = validate_enqueue(net, x0, C, S, B, split, op.fresh ? nullptr : alpha, stream))
+  if (int e = validate_enqueue(net, x0, C, S, B, split, params->fresh ? nullptr : alpha, stream))
     return e;
-  if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
+  return optimize_run(net, p, Bc, x0, eps, C, S, B, split, alpha, adam_m, adam_v, *params,
+                      lb_best, lb_trace, ws, stream);
+}
+
+int lirpa_bound_ul(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                   const int8_t* split, const float* alpha, float* lb, float* ub, float* l_out,
+                   float* u_out, int8_t* code_out, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!lb || !ub) return fail(LIRPA_EINVAL, "lb and ub must be given");
+  if ((l_out == nullptr) != (u_out == nullptr))
+    return fail(LIRPA_EINVAL, "l_out and u_out must both be given or both be null");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p, 2);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                plan_for(net, S, 1, 2).total);
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
+  const long nL = net->n[net->L];
+  float* C2 = at<float>(ws, p.off_spec);
+  if (int e = launch_k("spec_pm", stream, [&] {
+        hipLaunchKernelGGL(k_spec_pm, grid_for((long)S * nL), dim3(kBlock), 0, stream,
+                           (long)S * nL, C, C2, 1);
+      }))
+    return e;
+  // the intermediate passes are shared; the final pass bounds the 2S rows [C; -C]
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C2, 2 * S, stream)) return e;
+  float* lb2 = at<float>(ws, p.off_lb2);
   for (long b0 = 0; b0 < B; b0 += Bc) {
-    Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, nullptr, nullptr, stream);
-    long na = c.nb * net->n_relu, ns = c.nb * S;
-    float* a = alpha + b0 * net->n_relu;
-    float* lbt = at<float>(ws, p.off_lbt);
-    if (op.fresh) {
-      Chunk h = c;
-      h.alpha = nullptr;
-      h.tape = false;
-      if (int e = bound_chunk(h, C, lbt)) return e;
-      if (int e = launch_k("alpha_init", stream, [&] {
-            hipLaunchKernelGGL(k_alpha_init, grid_for(na), dim3(kBlock), 0, stream, na, h.L, h.U,
-                               a, adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu);
-          }))
+    Chunk c = make_chunk(net, p, ws, x0, eps, 2 * S, B, b0, split, alpha, l_out, u_out, stream);
+    if (int e = bound_chunk(c, C2, lb2)) return e;
+    if (int e = launch_k("split_ul", stream, [&] {
+          hipLaunchKernelGGL(k_split_ul, grid_for(c.nb * S), dim3(kBlock), 0, stream, c.nb,
+                             (long)S, lb2, lb + b0 * S, ub + b0 * S);
+        }))
+      return e;
+    if (code_out && net->n_relu)
+      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
+                           (size_t)c.nb * net->n_relu, stream))
         return e;
-    }
-    const int tbase = op.fresh ? 0 : op.t0;
-    for (int t = 0; t <= op.steps; ++t) {
-      c.tape = (t < op.steps);
-      if (int e = bound_chunk(c, C, lbt)) return e;
-      float* tr = lb_trace ? lb_trace + ((long)t * B + b0) * S : nullptr;
-      if (int e = launch_k("best", stream, [&] {
-            hipLaunchKernelGGL(k_best, grid_for(ns), dim3(kBlock), 0, stream, ns, lbt,
-                               lb_best + b0 * S, tr, (int)(t == 0));
-          }))
-        return e;
-      if (t == op.steps) break;
-      if (int e = grad_chunk(c, 1)) return e;
-      int tt = tbase + t + 1;
-      float c1 = (float)(1.0 - std::pow((double)op.beta1, tt));
-      float c2 = (float)(1.0 - std::pow((double)op.beta2, tt));
-      if (int e = launch_k("adam", stream, [&] {
-            hipLaunchKernelGGL(k_adam, grid_for(na), dim3(kBlock), 0, stream, na, a,
-                               adam_m + b0 * net->n_relu, adam_v + b0 * net->n_relu,
-                               at<float>(ws, p.off_ga), op.lr, op.beta1, op.beta2, op.eps_adam,
-                               c1, c2);
-          }))
-        return e;
-    }
   }
   return LIRPA_OK;
+}
+
+int lirpa_optimize_ul(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                      const int8_t* split, float* alpha_lo, float* m_lo, float* v_lo,
+                      float* alpha_up, float* m_up, float* v_up, const lirpa_opt_params* params,
+                      float* lb_best, float* ub_best, void* ws, size_t ws_bytes,
+                      hipStream_t stream) {
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!alpha_lo || !m_lo || !v_lo || !alpha_up || !m_up || !v_up || !params || !lb_best ||
+      !ub_best)
+    return fail(LIRPA_EINVAL, "both sides' alpha, m, v, params, lb_best and ub_best must be given");
+  if (int e = check_opt_params(*params)) return e;
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p, 3);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                plan_for(net, S, 1, 3).total);
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, C, S, B, split, params->fresh ? nullptr : alpha_lo,
+                               stream))
+    return e;
+  if (!params->fresh)
+    if (int e = validate_enqueue(net, x0, C, S, B, nullptr, alpha_up, stream)) return e;
+  // lower side: maximise lb of C over alpha_lo
+  if (int e = optimize_run(net, p, Bc, x0, eps, C, S, B, split, alpha_lo, m_lo, v_lo, *params,
+                           lb_best, nullptr, ws, stream))
+    return e;
+  // upper side: maximise lb of -C over alpha_up, i.e. minimise ub = -lb(-C) (Eq. 9 read as the
+  // tightest sound upper bound)
+  const long nL = net->n[net->L];
+  float* Cn = at<float>(ws, p.off_spec);
+  if (int e = launch_k("spec_pm", stream, [&] {
+        hipLaunchKernelGGL(k_spec_pm, grid_for((long)S * nL), dim3(kBlock), 0, stream,
+                           (long)S * nL, C, Cn, 0);
+      }))
+    return e;
+  if (int e = optimize_run(net, p, Bc, x0, eps, Cn, S, B, split, alpha_up, m_up, v_up, *params,
+                           ub_best, nullptr, ws, stream))
+    return e;
+  return launch_k("negate", stream, [&] {
+    hipLaunchKernelGGL(k_negate, grid_for((long)B * S), dim3(kBlock), 0, stream, (long)B * S,
+                       ub_best);
+  });
 }
 
 int lirpa_timing_begin(void) {

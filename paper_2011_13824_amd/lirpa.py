@@ -40,8 +40,8 @@ class lirpa_kernel_time(ctypes.Structure):
 
 
 SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
-           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_noalloc", "lirpa_bound_grad",
-           "lirpa_optimize",
+           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_noalloc", "lirpa_bound_ul",
+           "lirpa_bound_grad", "lirpa_optimize", "lirpa_optimize_ul",
            "lirpa_timing_begin", "lirpa_timing_end", "lirpa_last_error")
 
 _lib = None
@@ -69,6 +69,11 @@ def load() -> ctypes.CDLL:
     L.lirpa_bound.restype = i
     L.lirpa_bound_noalloc.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P]
     L.lirpa_bound_noalloc.restype = i
+    L.lirpa_bound_ul.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, P, sz, P]
+    L.lirpa_bound_ul.restype = i
+    L.lirpa_optimize_ul.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P,
+                                    ctypes.POINTER(lirpa_opt_params), P, P, P, sz, P]
+    L.lirpa_optimize_ul.restype = i
     L.lirpa_bound_grad.argtypes = [P, P, f, P, i, i, P, P, i, P, P, P, sz, P]
     L.lirpa_bound_grad.restype = i
     L.lirpa_optimize.argtypes = [P, P, f, P, i, i, P, P, P, P, ctypes.POINTER(lirpa_opt_params),
@@ -179,6 +184,33 @@ def lirpa_bound_noalloc(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, c
                                       _dev(code_out, torch.int8, "code_out"), _stream(stream)))
 
 
+def lirpa_bound_ul(net, x0, eps, C, S, B, split, alpha, lb, ub, l_out, u_out, code_out, ws,
+                   ws_bytes, stream=None):
+    _check(load().lirpa_bound_ul(net, _dev(x0, torch.float32, "x0"), float(eps),
+                                 _dev(C, torch.float32, "C"), int(S), int(B),
+                                 _dev(split, torch.int8, "split"),
+                                 _dev(alpha, torch.float32, "alpha"),
+                                 _dev(lb, torch.float32, "lb"), _dev(ub, torch.float32, "ub"),
+                                 _dev(l_out, torch.float32, "l_out"),
+                                 _dev(u_out, torch.float32, "u_out"),
+                                 _dev(code_out, torch.int8, "code_out"), _dev(ws, None, "ws"),
+                                 int(ws_bytes), _stream(stream)))
+
+
+def lirpa_optimize_ul(net, x0, eps, C, S, B, split, alpha_lo, m_lo, v_lo, alpha_up, m_up, v_up,
+                      params, lb_best, ub_best, ws, ws_bytes, stream=None):
+    p = params if isinstance(params, lirpa_opt_params) else lirpa_opt_params(**params)
+    f32 = torch.float32
+    _check(load().lirpa_optimize_ul(net, _dev(x0, f32, "x0"), float(eps), _dev(C, f32, "C"),
+                                    int(S), int(B), _dev(split, torch.int8, "split"),
+                                    _dev(alpha_lo, f32, "alpha_lo"), _dev(m_lo, f32, "m_lo"),
+                                    _dev(v_lo, f32, "v_lo"), _dev(alpha_up, f32, "alpha_up"),
+                                    _dev(m_up, f32, "m_up"), _dev(v_up, f32, "v_up"),
+                                    ctypes.byref(p), _dev(lb_best, f32, "lb_best"),
+                                    _dev(ub_best, f32, "ub_best"), _dev(ws, None, "ws"),
+                                    int(ws_bytes), _stream(stream)))
+
+
 def lirpa_bound_grad(net, x0, eps, C, S, B, split, alpha, full, lb, grad, ws, ws_bytes,
                      stream=None):
     _check(load().lirpa_bound_grad(net, _dev(x0, torch.float32, "x0"), float(eps),
@@ -255,6 +287,40 @@ class Network:
         if want_codes:
             out = out + (code,)
         return out if len(out) > 1 else lb
+
+    def bound_ul(self, x0, eps, C, split=None, alpha=None, B=None, max_ws_bytes=16 << 30):
+        """(lb, ub) [B, S] of the spec rows: Eq. 8's lower and upper bounds in one call."""
+        S = C.shape[0]
+        if B is None:
+            B = split.shape[0] if split is not None else (alpha.shape[0] if alpha is not None
+                                                            else 1)
+        lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        ub = torch.empty_like(lb)
+        ws, ws_bytes = self.workspace(S, B, 2, max_ws_bytes)
+        lirpa_bound_ul(self.handle, x0, eps, C, S, B, split, alpha, lb, ub, None, None, None, ws,
+                       ws_bytes)
+        return lb, ub
+
+    def optimize_ul(self, x0, eps, C, split, B=None, steps=20, lr=0.1, beta1=0.9, beta2=0.999,
+                    eps_adam=1e-8, max_ws_bytes=16 << 30, state=None):
+        """Optimised (lb_best, ub_best) from a fresh start (state None) or from the state dict a
+        previous call returned (alpha, m, v of both sides, t0); returns (lb, ub, state)."""
+        S = C.shape[0]
+        B = split.shape[0] if B is None else B
+        fresh = state is None
+        if fresh:
+            state = {k: torch.empty((B, self.n_relu), dtype=torch.float32, device=self.device)
+                     for k in ("alpha_lo", "m_lo", "v_lo", "alpha_up", "m_up", "v_up")}
+            state["t0"] = 0
+        lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        ub = torch.empty_like(lb)
+        ws, ws_bytes = self.workspace(S, B, 3, max_ws_bytes)
+        lirpa_optimize_ul(self.handle, x0, eps, C, S, B, split, state["alpha_lo"], state["m_lo"],
+                          state["v_lo"], state["alpha_up"], state["m_up"], state["v_up"],
+                          lirpa_opt_params(steps, lr, beta1, beta2, eps_adam, state["t0"],
+                                           int(fresh)), lb, ub, ws, ws_bytes)
+        state = dict(state, t0=state["t0"] + steps)
+        return lb, ub, state
 
     def bound_grad(self, x0, eps, C, split, alpha, full=True, max_ws_bytes=16 << 30):
         S, B = C.shape[0], alpha.shape[0]
