@@ -182,6 +182,62 @@ int lirpa_optimize_ul(lirpa_net* net, const float* x0, float eps, const float* C
                       float* lb_best, float* ub_best, void* ws, size_t ws_bytes,
                       hipStream_t stream);
 
+/* Branch and bound over sub-domains (Algorithm 1, Sec. 3.3-3.4) with the bounding steps above
+ * and without its LP fallback: for the single property c^T f(x) >= 0 over the box,
+ *   line 2   optimised LiRPA at the root (root_steps Adam steps; 0 = the heuristic slopes);
+ *   line 5   batch_pick_out: the `batch` unverified sub-domains with the lowest f_lo (ties: the
+ *            earlier record) leave the set P;
+ *   line 6   batch_split: each is split on one unstable, unsplit ReLU neuron into a child with it
+ *            forced active (+1) and one forced inactive (-1);
+ *   line 7   the 2 batch children are bounded in one batch, each from its parent's slopes
+ *            (`steps` Adam steps; f_hi at the slopes the lower side ends with);
+ *   line 8   Domain_Filter drops the children with f_lo >= 0 (verified), the others join P;
+ *   lines 9-10  f_lo, f_hi = the minima over P.
+ * The neuron to split is chosen by a stand-in rule (BaBSR's score is not given in the paper):
+ * the largest intercept -l u / (u - l) of the upper relaxation line of Eq. 5 under the
+ * sub-domain's own bounds, the lowest flat index on ties.  The set P lives in the workspace;
+ * the loop reads a small summary from the device once per iteration, so this call synchronises
+ * `stream` and returns when the search has ended:
+ *   LIRPA_BAB_VERIFIED        P is empty: every sub-domain has f_lo >= 0 (the property holds);
+ *   LIRPA_BAB_VIOLATED        a sub-domain's f_hi < 0 (Algorithm 1's loop condition: every point
+ *                             of it violates the property, if its splits are feasible -- the
+ *                             check the paper leaves to LP);
+ *   LIRPA_BAB_UNKNOWN_STUCK   a picked sub-domain has no unstable neuron left to split;
+ *   LIRPA_BAB_UNKNOWN_LIMIT   P outgrew max_domains (the paper's eta) or max_iters were run;
+ * the last two are where the paper switches to LP.  c is [n_L] on the device. */
+typedef enum {
+  LIRPA_BAB_VERIFIED = 1,
+  LIRPA_BAB_VIOLATED = 2,
+  LIRPA_BAB_UNKNOWN_STUCK = 3,
+  LIRPA_BAB_UNKNOWN_LIMIT = 4
+} lirpa_bab_status;
+
+typedef struct {
+  int batch;        /* n of Algorithm 1: sub-domains picked per iteration, 1..1024      */
+  int max_domains;  /* eta: largest |P| before stopping; max_domains + batch <= 16384   */
+  int max_iters;    /* iteration limit, >= 0                                            */
+  int root_steps;   /* Adam steps at the root (the paper takes 100)                     */
+  int steps;        /* Adam steps for every new sub-domain (the paper takes 10)         */
+  float lr, beta1, beta2, eps_adam; /* as in lirpa_opt_params                           */
+} lirpa_bab_params;
+
+typedef struct {
+  int status;               /* a lirpa_bab_status                                         */
+  float f_lo, f_hi;         /* global bounds at exit: the minima over P (over the verified  */
+                            /* sub-domains when P is empty)                                 */
+  int iterations;           /* loop iterations run                                          */
+  int64_t domains_bounded;  /* sub-domains bounded, the root included                       */
+  int domains_left;         /* |P| at exit                                                  */
+} lirpa_bab_result;
+
+/* Workspace bytes of lirpa_bab (0 for invalid arguments, SIZE_MAX as in
+ * lirpa_workspace_bytes). */
+size_t lirpa_bab_workspace_bytes(const lirpa_net* net, const lirpa_bab_params* params);
+
+int lirpa_bab(lirpa_net* net, const float* x0, float eps, const float* c,
+              const lirpa_bab_params* params, lirpa_bab_result* result, void* ws,
+              size_t ws_bytes, hipStream_t stream);
+
 /* Kernel timing, for profiling harnesses.  Between lirpa_timing_begin() and
  * lirpa_timing_end() every kernel the calls of this thread enqueue is bracketed by a pair of
  * hipEvents recorded on the call's own stream.  lirpa_timing_end() waits for those events and

@@ -4213,6 +4213,246 @@ __global__ void __launch_bounds__(kBlock) k_negate(long n, float* __restrict__ p
   if (i < n) p[i] = -p[i];
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// Branch and bound (Algorithm 1 without the LP fallback)
+// ---------------------------------------------------------------------------------------------
+// The set P of unverified sub-domains lives on the device as a store of records: split mask
+// [n_relu] int8, slopes alpha [n_relu], f_lo, f_hi and the neuron to split next.  The batch of
+// children of an iteration has the same layout.
+
+// Branching stand-in (BaBSR's score is not given in the paper): the unstable, unsplit neuron
+// with the largest intercept -l u / (u - l) of its upper relaxation line (Eq. 5) under the
+// sub-domain's own bounds; the lowest flat index on ties; -1 when none is left.  One block per
+// sub-domain.
+__global__ void __launch_bounds__(kBlock)
+    k_bab_branch(long n_relu, const float* __restrict__ l, const float* __restrict__ u,
+                 const int8_t* __restrict__ code, int* __restrict__ branch) {
+  __shared__ float bs[kBlock];
+  __shared__ int bj[kBlock];
+  const long b = blockIdx.x;
+  float best = -INFINITY;
+  int jb = -1;
+  for (long j = threadIdx.x; j < n_relu; j += kBlock) {
+    const long p = b * n_relu + j;
+    if (code[p] != 5) continue;
+    const float lj = l[p], uj = u[p];
+    const float sc = -(lj * uj) / (uj - lj);
+    if (sc > best) {  // j increases within a thread: the first maximum is kept
+      best = sc;
+      jb = (int)j;
+    }
+  }
+  bs[threadIdx.x] = best;
+  bj[threadIdx.x] = jb;
+  __syncthreads();
+  for (int o = kBlock / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      const float s2 = bs[threadIdx.x + o];
+      const int j2 = bj[threadIdx.x + o];
+      if (j2 >= 0 && (bj[threadIdx.x] < 0 || s2 > bs[threadIdx.x] ||
+                      (s2 == bs[threadIdx.x] && j2 < bj[threadIdx.x]))) {
+        bs[threadIdx.x] = s2;
+        bj[threadIdx.x] = j2;
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) branch[b] = bj[0];
+}
+
+// Summary of P read by the host after every iteration.
+struct BabSummary {
+  int count;     // |P|
+  int stuck;     // a sub-domain among the next batch has no neuron left to split
+  float f_lo;    // min over P of the lower bounds (Algorithm 1, line 9)
+  float f_hi;    // min over P of the upper bounds (line 10)
+  float leaf_lo; // min lower bound of the verified sub-domains dropped so far
+  float leaf_hi; // min upper bound of those
+  int pad[2];
+};
+
+__device__ __forceinline__ unsigned int ordered_bits(float f) {
+  const unsigned int b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// batch_pick_out (line 5): one block sorts the N = sum->count records of P by (f_lo, slot)
+// ascending with a bitonic network in LDS (N rounded up to a power of two, at most the LDS the
+// launch reserved) and writes the order to perm; then fills the summary (stuck looks at the
+// first min(batch, N) records).
+__global__ void __launch_bounds__(1024)
+    k_bab_sort(int batch, const float* __restrict__ lo, const float* __restrict__ hi,
+               const int* __restrict__ branch, int* __restrict__ perm,
+               BabSummary* __restrict__ sum) {
+  extern __shared__ unsigned long long keys[];
+  __shared__ float red[1024];
+  __shared__ int stk[1024];
+  const int tid = threadIdx.x;
+  const int N = sum->count;
+  int npad = 1;
+  while (npad < N) npad <<= 1;
+  for (int i = tid; i < npad; i += 1024)
+    keys[i] = i < N ? ((unsigned long long)ordered_bits(lo[i]) << 32) | (unsigned)i
+                    : ~0ull;
+  __syncthreads();
+  for (int k = 2; k <= npad; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < npad; i += 1024) {
+        const int ix = i ^ j;
+        if (ix > i) {
+          const unsigned long long a = keys[i], c = keys[ix];
+          const bool up = (i & k) == 0;
+          if ((a > c) == up) {
+            keys[i] = c;
+            keys[ix] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  float mh = INFINITY;
+  int st = 0;
+  const int kb = min(batch, N);
+  for (int i = tid; i < N; i += 1024) {
+    const int slot = (int)(keys[i] & 0xffffffffu);
+    perm[i] = slot;
+    mh = fminf(mh, hi[slot]);
+    if (i < kb && branch[slot] < 0) st = 1;
+  }
+  red[tid] = mh;
+  stk[tid] = st;
+  __syncthreads();
+  for (int o = 512; o > 0; o >>= 1) {
+    if (tid < o) {
+      red[tid] = fminf(red[tid], red[tid + o]);
+      stk[tid] |= stk[tid + o];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    sum->count = N;
+    sum->stuck = stk[0];
+    sum->f_lo = N > 0 ? lo[(int)(keys[0] & 0xffffffffu)] : INFINITY;
+    sum->f_hi = red[0];
+  }
+}
+
+// batch_split (line 6): child 2i of the i-th picked record forces its branching neuron active
+// (+1), child 2i + 1 inactive (-1); both start from the parent's slopes.
+__global__ void __launch_bounds__(kBlock)
+    k_bab_children(long k, long n_relu, const int* __restrict__ perm,
+                   const int8_t* __restrict__ smask, const float* __restrict__ salpha,
+                   const int* __restrict__ sbranch, int8_t* __restrict__ cmask,
+                   float* __restrict__ calpha) {
+  const long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= 2 * k * n_relu) return;
+  const long c = idx / n_relu, j = idx % n_relu;
+  const long par = perm[c >> 1];
+  const int8_t v = smask[par * n_relu + j];
+  cmask[idx] = j == sbranch[par] ? (int8_t)((c & 1) ? -1 : 1) : v;
+  if (calpha) calpha[idx] = salpha[par * n_relu + j];
+}
+
+// The records of P that were not picked (perm[k..N)) into the other store buffer, in order.
+__global__ void __launch_bounds__(kBlock)
+    k_bab_gather(long nrest, long k, long n_relu, const int* __restrict__ perm,
+                 const int8_t* __restrict__ smask, const float* __restrict__ salpha,
+                 const float* __restrict__ slo, const float* __restrict__ shi,
+                 const int* __restrict__ sbranch, int8_t* __restrict__ dmask,
+                 float* __restrict__ dalpha, float* __restrict__ dlo, float* __restrict__ dhi,
+                 int* __restrict__ dbranch) {
+  const long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= nrest * n_relu) return;
+  const long r = idx / n_relu, j = idx % n_relu;
+  const long src = perm[k + r];
+  dmask[idx] = smask[src * n_relu + j];
+  if (dalpha) dalpha[idx] = salpha[src * n_relu + j];
+  if (j == 0) {
+    dlo[r] = slo[src];
+    dhi[r] = shi[src];
+    dbranch[r] = sbranch[src];
+  }
+}
+
+// Domain_Filter (line 8): children with f_lo >= 0 are verified and dropped (their bounds kept
+// in the summary's leaf minima); the others get consecutive slots from N0 on, in child order.
+// One block; nc <= 2048.
+__global__ void __launch_bounds__(1024)
+    k_bab_filter(int nc, int N0, const float* __restrict__ clo, const float* __restrict__ chi,
+                 int* __restrict__ dst, BabSummary* __restrict__ sum) {
+  __shared__ int cnt[1024];
+  __shared__ float rl[1024], rh[1024];
+  const int tid = threadIdx.x;
+  const int c0 = 2 * tid, c1 = 2 * tid + 1;
+  const bool k0 = c0 < nc && !(clo[c0] >= 0.f), k1 = c1 < nc && !(clo[c1] >= 0.f);
+  float ll = INFINITY, lh = INFINITY;
+  if (c0 < nc && !k0) { ll = clo[c0]; lh = chi[c0]; }
+  if (c1 < nc && !k1) { ll = fminf(ll, clo[c1]); lh = fminf(lh, chi[c1]); }
+  cnt[tid] = (int)k0 + (int)k1;
+  rl[tid] = ll;
+  rh[tid] = lh;
+  __syncthreads();
+  // inclusive scan (Hillis-Steele) of the kept counts; minima of the dropped bounds
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int v = tid >= o ? cnt[tid - o] : 0;
+    __syncthreads();
+    cnt[tid] += v;
+    __syncthreads();
+  }
+  for (int o = 512; o > 0; o >>= 1) {
+    if (tid < o) {
+      rl[tid] = fminf(rl[tid], rl[tid + o]);
+      rh[tid] = fminf(rh[tid], rh[tid + o]);
+    }
+    __syncthreads();
+  }
+  const int before = cnt[tid] - (int)k0 - (int)k1;
+  if (c0 < nc) dst[c0] = k0 ? N0 + before : -1;
+  if (c1 < nc) dst[c1] = k1 ? N0 + before + (int)k0 : -1;
+  if (tid == 0) {
+    sum->leaf_lo = fminf(sum->leaf_lo, rl[0]);
+    sum->leaf_hi = fminf(sum->leaf_hi, rh[0]);
+    sum->count = N0 + cnt[1023];
+  }
+}
+
+// Kept children into their slots of P.
+__global__ void __launch_bounds__(kBlock)
+    k_bab_insert(long nc, long n_relu, const int* __restrict__ dst,
+                 const int8_t* __restrict__ cmask, const float* __restrict__ calpha,
+                 const float* __restrict__ clo, const float* __restrict__ chi,
+                 const int* __restrict__ cbranch, int8_t* __restrict__ smask,
+                 float* __restrict__ salpha, float* __restrict__ slo, float* __restrict__ shi,
+                 int* __restrict__ sbranch) {
+  const long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (idx >= nc * n_relu) return;
+  const long c = idx / n_relu, j = idx % n_relu;
+  const int d = dst[c];
+  if (d < 0) return;
+  smask[(long)d * n_relu + j] = cmask[idx];
+  if (salpha) salpha[(long)d * n_relu + j] = calpha[idx];
+  if (j == 0) {
+    slo[d] = clo[c];
+    shi[d] = chi[c];
+    sbranch[d] = cbranch[c];
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_fill_i8(long n, int8_t* __restrict__ p, int v) {
+  const long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = (int8_t)v;
+}
+
+__global__ void k_bab_summary_init(BabSummary* sum) {
+  sum->count = 0;
+  sum->stuck = 0;
+  sum->f_lo = INFINITY;
+  sum->f_hi = INFINITY;
+  sum->leaf_lo = INFINITY;
+  sum->leaf_hi = INFINITY;
+}
+
 // ---------------------------------------------------------------------------------------------
 // Input check (LIRPA_VALIDATE=1)
 // ---------------------------------------------------------------------------------------------
@@ -5554,6 +5794,258 @@ int optimize_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float 
   return LIRPA_OK;
 }
 
+
+// lirpa_bound_ul on a workspace that holds chunks of Bc sub-domains (plan p, mode 2).
+int bound_ul_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float eps,
+                 const float* C, int S, int B, const int8_t* split, const float* alpha, float* lb,
+                 float* ub, float* l_out, float* u_out, int8_t* code_out, void* ws,
+                 hipStream_t stream) {
+  const long nL = net->n[net->L];
+  float* C2 = at<float>(ws, p.off_spec);
+  if (int e = launch_k("spec_pm", stream, [&] {
+        hipLaunchKernelGGL(k_spec_pm, grid_for((long)S * nL), dim3(kBlock), 0, stream,
+                           (long)S * nL, C, C2, 1);
+      }))
+    return e;
+  // the intermediate passes are shared; the final pass bounds the 2S rows [C; -C]
+  if (int e = layer1_bounds(net, p, ws, x0, eps, C2, 2 * S, stream)) return e;
+  float* lb2 = at<float>(ws, p.off_lb2);
+  for (long b0 = 0; b0 < B; b0 += Bc) {
+    Chunk c = make_chunk(net, p, ws, x0, eps, 2 * S, B, b0, split, alpha, l_out, u_out, stream);
+    if (int e = bound_chunk(c, C2, lb2)) return e;
+    if (int e = launch_k("split_ul", stream, [&] {
+          hipLaunchKernelGGL(k_split_ul, grid_for(c.nb * S), dim3(kBlock), 0, stream, c.nb,
+                             (long)S, lb2, lb + b0 * S, ub + b0 * S);
+        }))
+      return e;
+    if (code_out && net->n_relu)
+      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
+                           (size_t)c.nb * net->n_relu, stream))
+        return e;
+  }
+  return LIRPA_OK;
+}
+
+
+// Branch and bound workspace: two store buffers for P, the order of P, the batch of children,
+// the summary, and a region for the bounding calls on the children.
+struct BabPlan {
+  long cap = 0, nc = 0;  // store capacity, children per iteration (2 batch)
+  bool alpha = false;     // slopes carried per record (some optimisation is asked for)
+  size_t smask[2] = {}, salpha[2] = {}, slo[2] = {}, shi[2] = {}, sbr[2] = {};
+  size_t perm = 0, cmask = 0, calpha = 0, cm = 0, cv = 0, clo = 0, chi = 0, clbu = 0;
+  size_t cl = 0, cu = 0, ccode = 0, cbr = 0, cdst = 0, sum = 0, inner = 0;
+  size_t inner_bytes = 0, total = 0;
+};
+
+BabPlan bab_plan(const lirpa_net* net, const lirpa_bab_params& bp) {
+  BabPlan q;
+  const long n = net->n_relu;
+  q.cap = (long)bp.max_domains + bp.batch;
+  q.nc = 2L * bp.batch;
+  q.alpha = bp.root_steps > 0 || bp.steps > 0;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at_ = o;
+    o = align256(o + bytes);
+    return at_;
+  };
+  for (int i = 0; i < 2; ++i) {
+    q.smask[i] = take((size_t)q.cap * n);
+    if (q.alpha) q.salpha[i] = take((size_t)q.cap * n * 4);
+    q.slo[i] = take((size_t)q.cap * 4);
+    q.shi[i] = take((size_t)q.cap * 4);
+    q.sbr[i] = take((size_t)q.cap * 4);
+  }
+  q.perm = take((size_t)q.cap * 4);
+  q.cmask = take((size_t)q.nc * n);
+  if (q.alpha) {
+    q.calpha = take((size_t)q.nc * n * 4);
+    q.cm = take((size_t)q.nc * n * 4);
+    q.cv = take((size_t)q.nc * n * 4);
+  }
+  q.clo = take((size_t)q.nc * 4);
+  q.chi = take((size_t)q.nc * 4);
+  q.clbu = take((size_t)q.nc * 4);
+  q.cl = take((size_t)q.nc * n * 4);
+  q.cu = take((size_t)q.nc * n * 4);
+  q.ccode = take((size_t)q.nc * n);
+  q.cbr = take((size_t)q.nc * 4);
+  q.cdst = take((size_t)q.nc * 4);
+  q.sum = take(sizeof(BabSummary));
+  const size_t ul = plan_for(net, 1, q.nc, 2).total;
+  const size_t op = q.alpha ? plan_for(net, 1, q.nc, 1).total : 0;
+  q.inner_bytes = std::max(ul, op);
+  q.inner = o;
+  q.total = (ul == (size_t)-1 || op == (size_t)-1) ? (size_t)-1 : o + q.inner_bytes;
+  return q;
+}
+
+int check_bab_params(const lirpa_bab_params& bp) {
+  if (bp.batch < 1 || bp.batch > 1024) return fail(LIRPA_EINVAL, "batch must be in 1..1024");
+  if (bp.max_domains < 1 || (long)bp.max_domains + bp.batch > 16384)
+    return fail(LIRPA_EINVAL, "max_domains must be >= 1 with max_domains + batch <= 16384");
+  if (bp.max_iters < 0 || bp.root_steps < 0 || bp.steps < 0)
+    return fail(LIRPA_EINVAL, "max_iters, root_steps and steps must be >= 0");
+  if (!(bp.lr >= 0.f) || !(bp.beta1 >= 0.f && bp.beta1 < 1.f) ||
+      !(bp.beta2 >= 0.f && bp.beta2 < 1.f) || !(bp.eps_adam > 0.f))
+    return fail(LIRPA_EINVAL, "bad optimiser parameters");
+  return LIRPA_OK;
+}
+
+// Bound nb children (masks at q.cmask, slopes at q.calpha): lower bounds into q.clo, upper
+// bounds into q.chi, their l, u, codes and the neuron each would split next.  steps > 0
+// optimises the slopes from where they are (fresh: from the heuristic start) first.
+int bab_bound_children(lirpa_net* net, const BabPlan& q, void* ws, const float* x0, float eps,
+                       const float* c, long nb, int steps, bool fresh,
+                       const lirpa_bab_params& bp, hipStream_t st) {
+  void* inner = at<char>(ws, q.inner);
+  int8_t* mask = at<int8_t>(ws, q.cmask);
+  float* alpha = q.alpha ? at<float>(ws, q.calpha) : nullptr;
+  float* lo = at<float>(ws, q.clo);
+  if (q.alpha && (steps > 0 || fresh)) {
+    Plan p;
+    const long Bc = fit_chunk(net, 1, nb, q.inner_bytes, &p, 1);
+    if (Bc < 1) return fail(LIRPA_ENOMEM, "branch and bound: inner workspace too small");
+    const long na = nb * net->n_relu;
+    for (size_t off : {q.cm, q.cv})
+      if (int e = launch_k("zero", st, [&] {
+            hipLaunchKernelGGL(k_zero, grid_for(na), dim3(kBlock), 0, st, na, at<float>(ws, off));
+          }))
+        return e;
+    lirpa_opt_params op{steps, bp.lr, bp.beta1, bp.beta2, bp.eps_adam, 0, fresh ? 1 : 0};
+    if (int e = optimize_run(net, p, Bc, x0, eps, c, 1, (int)nb, mask, alpha,
+                             at<float>(ws, q.cm), at<float>(ws, q.cv), op, lo, nullptr, inner,
+                             st))
+      return e;
+  }
+  // the upper bound (and l, u, codes) at the slopes the lower side ended with
+  Plan p;
+  const long Bc = fit_chunk(net, 1, nb, q.inner_bytes, &p, 2);
+  if (Bc < 1) return fail(LIRPA_ENOMEM, "branch and bound: inner workspace too small");
+  const bool opt = q.alpha && (steps > 0 || fresh);
+  if (int e = bound_ul_run(net, p, Bc, x0, eps, c, 1, (int)nb, mask, alpha,
+                           opt ? at<float>(ws, q.clbu) : lo, at<float>(ws, q.chi),
+                           at<float>(ws, q.cl), at<float>(ws, q.cu), at<int8_t>(ws, q.ccode),
+                           inner, st))
+    return e;
+  return launch_k("bab_branch", st, [&] {
+    hipLaunchKernelGGL(k_bab_branch, dim3((unsigned)nb), dim3(kBlock), 0, st, net->n_relu,
+                       at<float>(ws, q.cl), at<float>(ws, q.cu), at<int8_t>(ws, q.ccode),
+                       at<int>(ws, q.cbr));
+  });
+}
+
+// Domain_Filter and insertion of nc bounded children into store buffer `cur` holding N records,
+// then batch_pick_out's sort of the new P; the summary is copied to *hs (the loop's one
+// synchronisation per iteration).
+int bab_insert_sort(lirpa_net* net, const BabPlan& q, void* ws, int cur, long N, long nc,
+                    const lirpa_bab_params& bp, BabSummary* hs, hipStream_t st) {
+  BabSummary* sum = at<BabSummary>(ws, q.sum);
+  const long n = net->n_relu;
+  if (int e = launch_k("bab_filter", st, [&] {
+        hipLaunchKernelGGL(k_bab_filter, dim3(1), dim3(1024), 0, st, (int)nc, (int)N,
+                           at<float>(ws, q.clo), at<float>(ws, q.chi), at<int>(ws, q.cdst), sum);
+      }))
+    return e;
+  if (int e = launch_k("bab_insert", st, [&] {
+        hipLaunchKernelGGL(k_bab_insert, grid_for(nc * n), dim3(kBlock), 0, st, nc, n,
+                           at<int>(ws, q.cdst), at<int8_t>(ws, q.cmask),
+                           q.alpha ? at<float>(ws, q.calpha) : nullptr, at<float>(ws, q.clo),
+                           at<float>(ws, q.chi), at<int>(ws, q.cbr), at<int8_t>(ws, q.smask[cur]),
+                           q.alpha ? at<float>(ws, q.salpha[cur]) : nullptr,
+                           at<float>(ws, q.slo[cur]), at<float>(ws, q.shi[cur]),
+                           at<int>(ws, q.sbr[cur]));
+      }))
+    return e;
+  long npad = 1;
+  while (npad < q.cap) npad <<= 1;
+  const size_t lds = (size_t)npad * sizeof(unsigned long long);
+  if (lds > 65536 &&
+      hipFuncSetAttribute(reinterpret_cast<const void*>(k_bab_sort),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(LIRPA_EDEVICE, "cannot reserve %zu bytes of LDS for the sort", lds);
+  if (int e = launch_k("bab_sort", st, [&] {
+        hipLaunchKernelGGL(k_bab_sort, dim3(1), dim3(1024), lds, st, bp.batch,
+                           at<float>(ws, q.slo[cur]), at<float>(ws, q.shi[cur]),
+                           at<int>(ws, q.sbr[cur]), at<int>(ws, q.perm), sum);
+      }))
+    return e;
+  if (hipMemcpyAsync(hs, sum, sizeof *hs, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return fail(LIRPA_EDEVICE, "branch and bound: reading the summary failed");
+  return LIRPA_OK;
+}
+
+int bab_run(lirpa_net* net, const BabPlan& q, const float* x0, float eps, const float* c,
+            const lirpa_bab_params& bp, lirpa_bab_result* res, void* ws, hipStream_t st) {
+  const long n = net->n_relu;
+  BabSummary hs{};
+  // line 2: the root (no split), optimised from the heuristic start when asked
+  if (int e = launch_k("bab_init", st, [&] {
+        hipLaunchKernelGGL(k_fill_i8, grid_for(n), dim3(kBlock), 0, st, n,
+                           at<int8_t>(ws, q.cmask), 0);
+        hipLaunchKernelGGL(k_bab_summary_init, dim3(1), dim3(1), 0, st,
+                           at<BabSummary>(ws, q.sum));
+      }))
+    return e;
+  if (int e = bab_bound_children(net, q, ws, x0, eps, c, 1, bp.root_steps, true, bp, st))
+    return e;
+  int cur = 0;
+  long N = 0;
+  // line 3: P = the root unless it is verified already
+  if (int e = bab_insert_sort(net, q, ws, cur, N, 1, bp, &hs, st)) return e;
+  N = hs.count;
+  res->domains_bounded = 1;
+  res->iterations = 0;
+  for (;;) {
+    int status = 0;
+    if (N == 0) status = LIRPA_BAB_VERIFIED;
+    else if (hs.f_hi < 0.f) status = LIRPA_BAB_VIOLATED;
+    else if (N > bp.max_domains || res->iterations >= bp.max_iters) status = LIRPA_BAB_UNKNOWN_LIMIT;
+    else if (hs.stuck) status = LIRPA_BAB_UNKNOWN_STUCK;
+    if (status) {
+      res->status = status;
+      res->f_lo = N == 0 ? hs.leaf_lo : hs.f_lo;
+      res->f_hi = N == 0 ? hs.leaf_hi : hs.f_hi;
+      res->domains_left = (int)N;
+      return LIRPA_OK;
+    }
+    // lines 5-6: pick the k lowest records (perm[0..k)), split each into two children; the rest
+    // move to the other store buffer in order
+    const long k = std::min<long>(bp.batch, N);
+    if (int e = launch_k("bab_children", st, [&] {
+          hipLaunchKernelGGL(k_bab_children, grid_for(2 * k * n), dim3(kBlock), 0, st, k, n,
+                             at<int>(ws, q.perm), at<int8_t>(ws, q.smask[cur]),
+                             q.alpha ? at<float>(ws, q.salpha[cur]) : nullptr,
+                             at<int>(ws, q.sbr[cur]), at<int8_t>(ws, q.cmask),
+                             q.alpha ? at<float>(ws, q.calpha) : nullptr);
+        }))
+      return e;
+    const long rest = N - k;
+    if (rest > 0)
+      if (int e = launch_k("bab_gather", st, [&] {
+            hipLaunchKernelGGL(k_bab_gather, grid_for(rest * n), dim3(kBlock), 0, st, rest, k, n,
+                               at<int>(ws, q.perm), at<int8_t>(ws, q.smask[cur]),
+                               q.alpha ? at<float>(ws, q.salpha[cur]) : nullptr,
+                               at<float>(ws, q.slo[cur]), at<float>(ws, q.shi[cur]),
+                               at<int>(ws, q.sbr[cur]), at<int8_t>(ws, q.smask[1 - cur]),
+                               q.alpha ? at<float>(ws, q.salpha[1 - cur]) : nullptr,
+                               at<float>(ws, q.slo[1 - cur]), at<float>(ws, q.shi[1 - cur]),
+                               at<int>(ws, q.sbr[1 - cur]));
+          }))
+        return e;
+    cur = 1 - cur;
+    // line 7: (optimised) LiRPA on the 2k children, from their parents' slopes
+    if (int e = bab_bound_children(net, q, ws, x0, eps, c, 2 * k, bp.steps, false, bp, st))
+      return e;
+    res->domains_bounded += 2 * k;
+    // lines 8-10
+    if (int e = bab_insert_sort(net, q, ws, cur, rest, 2 * k, bp, &hs, st)) return e;
+    N = hs.count;
+    ++res->iterations;
+  }
+}
 }  // namespace
 
 // ---------------------------------------------------------------------------------------------
@@ -5716,30 +6208,8 @@ int lirpa_bound_ul(lirpa_net* net, const float* x0, float eps, const float* C, i
                 plan_for(net, S, 1, 2).total);
   if (int e = validate_report(stream)) return e;
   if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
-  const long nL = net->n[net->L];
-  float* C2 = at<float>(ws, p.off_spec);
-  if (int e = launch_k("spec_pm", stream, [&] {
-        hipLaunchKernelGGL(k_spec_pm, grid_for((long)S * nL), dim3(kBlock), 0, stream,
-                           (long)S * nL, C, C2, 1);
-      }))
-    return e;
-  // the intermediate passes are shared; the final pass bounds the 2S rows [C; -C]
-  if (int e = layer1_bounds(net, p, ws, x0, eps, C2, 2 * S, stream)) return e;
-  float* lb2 = at<float>(ws, p.off_lb2);
-  for (long b0 = 0; b0 < B; b0 += Bc) {
-    Chunk c = make_chunk(net, p, ws, x0, eps, 2 * S, B, b0, split, alpha, l_out, u_out, stream);
-    if (int e = bound_chunk(c, C2, lb2)) return e;
-    if (int e = launch_k("split_ul", stream, [&] {
-          hipLaunchKernelGGL(k_split_ul, grid_for(c.nb * S), dim3(kBlock), 0, stream, c.nb,
-                             (long)S, lb2, lb + b0 * S, ub + b0 * S);
-        }))
-      return e;
-    if (code_out && net->n_relu)
-      if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
-                           (size_t)c.nb * net->n_relu, stream))
-        return e;
-  }
-  return LIRPA_OK;
+  return bound_ul_run(net, p, Bc, x0, eps, C, S, B, split, alpha, lb, ub, l_out, u_out, code_out,
+                      ws, stream);
 }
 
 int lirpa_optimize_ul(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
@@ -5783,6 +6253,27 @@ int lirpa_optimize_ul(lirpa_net* net, const float* x0, float eps, const float* C
     hipLaunchKernelGGL(k_negate, grid_for((long)B * S), dim3(kBlock), 0, stream, (long)B * S,
                        ub_best);
   });
+}
+
+size_t lirpa_bab_workspace_bytes(const lirpa_net* net, const lirpa_bab_params* params) {
+  if (!net || !params || check_bab_params(*params)) return 0;
+  return bab_plan(net, *params).total;
+}
+
+int lirpa_bab(lirpa_net* net, const float* x0, float eps, const float* c,
+              const lirpa_bab_params* params, lirpa_bab_result* result, void* ws,
+              size_t ws_bytes, hipStream_t stream) {
+  if (int e = check_common(net, x0, eps, c, 1, 1, ws)) return e;
+  if (!params || !result) return fail(LIRPA_EINVAL, "params and result must be given");
+  if (int e = check_bab_params(*params)) return e;
+  const BabPlan q = bab_plan(net, *params);
+  if (q.total > ws_bytes)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes, branch and bound needs %zu", ws_bytes,
+                q.total);
+  if (int e = validate_report(stream)) return e;
+  if (int e = validate_enqueue(net, x0, c, 1, 1, nullptr, nullptr, stream)) return e;
+  *result = lirpa_bab_result{};
+  return bab_run(net, q, x0, eps, c, *params, result, ws, stream);
 }
 
 int lirpa_timing_begin(void) {

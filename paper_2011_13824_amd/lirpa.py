@@ -34,6 +34,22 @@ class lirpa_opt_params(ctypes.Structure):
                 ("fresh", ctypes.c_int)]
 
 
+class lirpa_bab_params(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int), ("max_domains", ctypes.c_int),
+                ("max_iters", ctypes.c_int), ("root_steps", ctypes.c_int),
+                ("steps", ctypes.c_int), ("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps_adam", ctypes.c_float)]
+
+
+class lirpa_bab_result(ctypes.Structure):
+    _fields_ = [("status", ctypes.c_int), ("f_lo", ctypes.c_float), ("f_hi", ctypes.c_float),
+                ("iterations", ctypes.c_int), ("domains_bounded", ctypes.c_int64),
+                ("domains_left", ctypes.c_int)]
+
+
+BAB_VERIFIED, BAB_VIOLATED, BAB_UNKNOWN_STUCK, BAB_UNKNOWN_LIMIT = 1, 2, 3, 4
+
+
 class lirpa_kernel_time(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("total_ms", ctypes.c_double),
                 ("launches", ctypes.c_int64)]
@@ -42,6 +58,7 @@ class lirpa_kernel_time(ctypes.Structure):
 SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
            "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_noalloc", "lirpa_bound_ul",
            "lirpa_bound_grad", "lirpa_optimize", "lirpa_optimize_ul",
+           "lirpa_bab_workspace_bytes", "lirpa_bab",
            "lirpa_timing_begin", "lirpa_timing_end", "lirpa_last_error")
 
 _lib = None
@@ -74,6 +91,11 @@ def load() -> ctypes.CDLL:
     L.lirpa_optimize_ul.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P,
                                     ctypes.POINTER(lirpa_opt_params), P, P, P, sz, P]
     L.lirpa_optimize_ul.restype = i
+    L.lirpa_bab_workspace_bytes.argtypes = [P, ctypes.POINTER(lirpa_bab_params)]
+    L.lirpa_bab_workspace_bytes.restype = sz
+    L.lirpa_bab.argtypes = [P, P, f, P, ctypes.POINTER(lirpa_bab_params),
+                            ctypes.POINTER(lirpa_bab_result), P, sz, P]
+    L.lirpa_bab.restype = i
     L.lirpa_bound_grad.argtypes = [P, P, f, P, i, i, P, P, i, P, P, P, sz, P]
     L.lirpa_bound_grad.restype = i
     L.lirpa_optimize.argtypes = [P, P, f, P, i, i, P, P, P, P, ctypes.POINTER(lirpa_opt_params),
@@ -211,6 +233,20 @@ def lirpa_optimize_ul(net, x0, eps, C, S, B, split, alpha_lo, m_lo, v_lo, alpha_
                                     int(ws_bytes), _stream(stream)))
 
 
+def lirpa_bab_workspace_bytes(net, params) -> int:
+    return int(load().lirpa_bab_workspace_bytes(net, ctypes.byref(params)))
+
+
+def lirpa_bab(net, x0, eps, c, params, ws, ws_bytes, stream=None):
+    """Runs the search (the call synchronises the stream); returns the lirpa_bab_result."""
+    res = lirpa_bab_result()
+    _check(load().lirpa_bab(net, _dev(x0, torch.float32, "x0"), float(eps),
+                            _dev(c, torch.float32, "c"), ctypes.byref(params),
+                            ctypes.byref(res), _dev(ws, None, "ws"), int(ws_bytes),
+                            _stream(stream)))
+    return res
+
+
 def lirpa_bound_grad(net, x0, eps, C, S, B, split, alpha, full, lb, grad, ws, ws_bytes,
                      stream=None):
     _check(load().lirpa_bound_grad(net, _dev(x0, torch.float32, "x0"), float(eps),
@@ -321,6 +357,16 @@ class Network:
                                            int(fresh)), lb, ub, ws, ws_bytes)
         state = dict(state, t0=state["t0"] + steps)
         return lb, ub, state
+
+    def bab(self, x0, eps, c, batch=64, max_domains=4000, max_iters=30, root_steps=0, steps=0,
+            lr=0.1, beta1=0.9, beta2=0.999, eps_adam=1e-8):
+        """Branch and bound on c^T f(x) >= 0; returns a dict of the lirpa_bab_result fields."""
+        p = lirpa_bab_params(batch, max_domains, max_iters, root_steps, steps, lr, beta1, beta2,
+                             eps_adam)
+        need = lirpa_bab_workspace_bytes(self.handle, p)
+        ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        r = lirpa_bab(self.handle, x0, eps, c, p, ws, need)
+        return {k: getattr(r, k) for k, _ in lirpa_bab_result._fields_}
 
     def bound_grad(self, x0, eps, C, split, alpha, full=True, max_ws_bytes=16 << 30):
         S, B = C.shape[0], alpha.shape[0]
