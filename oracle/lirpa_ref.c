@@ -275,6 +275,11 @@ typedef struct {
   int S, B;
   const int8_t* split; /* [B][n_relu] or NULL */
   const float* alpha;  /* [B][n_relu] or NULL */
+  /* [B][n_relu] or NULL: intermediate bounds of each sub-domain's parent, intersected with its
+   * own (the paper is silent on reusing them; this is the reading that a parent's bounds hold
+   * on its children, which are subsets of it) */
+  const float* l_par;
+  const float* u_par;
   relaxset* rs;        /* [B] */
 } problem;
 
@@ -318,6 +323,13 @@ static int compute_relaxations(problem* p) {
         memcpy(p->rs[b].l + o, p->rs[0].l + o, sizeof(double) * nk);
         memcpy(p->rs[b].u + o, p->rs[0].u + o, sizeof(double) * nk);
       }
+    if (p->l_par)
+      for (int b = 0; b < p->B; ++b)
+        for (long j = 0; j < nk; ++j) {
+          long i = (long)b * ni->n_relu + o + j;
+          p->rs[b].l[o + j] = fmax(p->rs[b].l[o + j], (double)p->l_par[i]);
+          p->rs[b].u[o + j] = fmin(p->rs[b].u[o + j], (double)p->u_par[i]);
+        }
     for (int b = 0; b < p->B; ++b)
       relax_layer(ni, k, p->split ? p->split + (long)b * ni->n_relu : NULL,
                   p->alpha ? p->alpha + (long)b * ni->n_relu : NULL, &p->rs[b]);
@@ -404,14 +416,17 @@ long ref_num_relu(const ref_layer* T, int L) {
  * under the split constraints of b.  alpha == NULL selects the heuristic lower slope.
  * l_out, u_out, code_out (optional, [B][n_relu]) receive the intermediate bounds and
  * stability codes. */
-int ref_bound(const ref_layer* T, int L, const float* x0, float eps, const float* C, int S,
-              int B, const int8_t* split, const float* alpha, double* lb, double* l_out,
-              double* u_out, signed char* code_out, int nthreads) {
+static int bound_impl(const ref_layer* T, int L, const float* x0, float eps, const float* C,
+                      int S, int B, const int8_t* split, const float* alpha,
+                      const float* l_par, const float* u_par, double* lb, double* l_out,
+                      double* u_out, signed char* code_out, int nthreads) {
   set_threads(nthreads);
   problem p;
   memset(&p, 0, sizeof p);
   double* x0d = NULL;
   int e = problem_init(&p, T, L, x0, eps, C, S, B, split, alpha, &x0d);
+  p.l_par = l_par;
+  p.u_par = u_par;
   if (!e) e = compute_relaxations(&p);
   if (!e) e = final_pass(&p, lb);
   if (!e)
@@ -423,6 +438,26 @@ int ref_bound(const ref_layer* T, int L, const float* x0, float eps, const float
     }
   problem_free(&p, x0d);
   return e;
+}
+
+int ref_bound(const ref_layer* T, int L, const float* x0, float eps, const float* C, int S,
+              int B, const int8_t* split, const float* alpha, double* lb, double* l_out,
+              double* u_out, signed char* code_out, int nthreads) {
+  return bound_impl(T, L, x0, eps, C, S, B, split, alpha, NULL, NULL, lb, l_out, u_out,
+                    code_out, nthreads);
+}
+
+/* ref_bound with each sub-domain's intermediate bounds intersected, layer by layer before its
+ * relaxation, with its parent's l_par, u_par ([B][n_relu], fp32): l = max(l, l_par),
+ * u = min(u, u_par).  The result bounds min over the sub-domain itself (not over the box of
+ * the split network), and l_out, u_out report the intersected bounds. */
+int ref_bound_child(const ref_layer* T, int L, const float* x0, float eps, const float* C,
+                    int S, int B, const int8_t* split, const float* alpha, const float* l_par,
+                    const float* u_par, double* lb, double* l_out, double* u_out,
+                    signed char* code_out, int nthreads) {
+  if (!l_par || !u_par) return REF_EINVAL;
+  return bound_impl(T, L, x0, eps, C, S, B, split, alpha, l_par, u_par, lb, l_out, u_out,
+                    code_out, nthreads);
 }
 
 /* The final linear lower-bounding functions L_s(x) = A_s x + beta_s of one sub-domain

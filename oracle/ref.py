@@ -48,6 +48,7 @@ def lib():
         L.ref_num_relu.argtypes = [_P, i]
         L.ref_num_relu.restype = l
         L.ref_bound.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, _P, _P, _P, _P, i]
+        L.ref_bound_child.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, _P, _P, _P, _P, _P, _P, i]
         L.ref_bound_grad.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, i, _P, _P, i]
         L.ref_optimize.argtypes = [_P, i, _P, f, _P, i, i, _P, _P, _P, _P, i, d, d, d, d, i, _P,
                                    _P, i]
@@ -56,8 +57,9 @@ def lib():
         L.ref_layer_T.argtypes = [_P, _P, l, _P]
         L.ref_layer_fwd.argtypes = [_P, _P, l, _P]
         L.ref_relax.argtypes = [d, d, i, i, d, _P]
-        for fn in ("ref_bound", "ref_bound_grad", "ref_optimize", "ref_linear_bound_fn",
-                   "ref_forward", "ref_layer_T", "ref_layer_fwd", "ref_relax"):
+        for fn in ("ref_bound", "ref_bound_child", "ref_bound_grad", "ref_optimize",
+                   "ref_linear_bound_fn", "ref_forward", "ref_layer_T", "ref_layer_fwd",
+                   "ref_relax"):
             getattr(L, fn).restype = i
         _lib = L
     return _lib
@@ -115,6 +117,21 @@ def bound(net: RefNet, x0, eps, C, split=None, alpha=None, B=None, nthreads=0):
     _check(lib().ref_bound(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S, B, _ptr(split),
                            _ptr(alpha), _ptr(lb), _ptr(l), _ptr(u), _ptr(code), nthreads),
            "ref_bound")
+    return lb, l, u, code
+
+
+def bound_child(net: RefNet, x0, eps, C, split, alpha, l_par, u_par, nthreads=0):
+    """bound() with each layer's bounds intersected with the parent's l_par, u_par [B,n_relu]."""
+    x0, C, split, alpha = _f32(x0), _f32(C), _i8(split), _f32(alpha)
+    l_par, u_par = _f32(l_par), _f32(u_par)
+    B, S = l_par.shape[0], C.shape[0]
+    lb = np.zeros((B, S))
+    l = np.zeros((B, net.n_relu))
+    u = np.zeros((B, net.n_relu))
+    code = np.zeros((B, net.n_relu), dtype=np.int8)
+    _check(lib().ref_bound_child(net.arr, net.L, _ptr(x0), float(eps), _ptr(C), S, B,
+                                 _ptr(split), _ptr(alpha), _ptr(l_par), _ptr(u_par), _ptr(lb),
+                                 _ptr(l), _ptr(u), _ptr(code), nthreads), "ref_bound_child")
     return lb, l, u, code
 
 
