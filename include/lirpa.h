@@ -113,6 +113,20 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
                 const int8_t* split, const float* alpha, float* lb, float* l_out, float* u_out,
                 int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* lirpa_bound for sub-domains split from a parent whose intermediate bounds are known: every
+ * layer's bounds l, u of a sub-domain are intersected with its parent's before the layer is
+ * relaxed, l = max(l, l_parent), u = min(u, u_parent).  The paper is silent on reusing them
+ * (Sec. 3.1 split constraints, Eq. 9); the reading taken is that a child is a subset of its
+ * parent, so the parent's bounds hold on it.  The bound then holds over the sub-domain itself
+ * (the box under its split constraints) rather than over the whole box of the split network.
+ * Sub-domain b's parent bounds are row b of l_parent, u_parent [B][n_relu] (fp32; e.g. the
+ * l_out, u_out of the call that bounded the parent); l_out, u_out report the intersected
+ * bounds.  Other arguments as in lirpa_bound (workspace mode 0). */
+int lirpa_bound_child(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                      const int8_t* split, const float* alpha, const float* l_parent,
+                      const float* u_parent, float* lb, float* l_out, float* u_out,
+                      int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* lirpa_bound for callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc): the same computation and outputs, with
  * no workspace argument.  Its workspace is the library's own scratch array of 128 MiB per

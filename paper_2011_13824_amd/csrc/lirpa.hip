@@ -248,6 +248,8 @@ struct FcSrc {
   float* r_bu;
   int8_t* code;         // stride n_relu, at offset off
   long n_relu, off;
+  const float* lpar;    // parent bounds (stride n_relu, at offset off) or null
+  const float* upar;
   // spec source of k_convT_fc_bound (the final pass from the merged spec rows): b holds
   // C W_L [S][nk] followed by C b_L [S]; r_lo, r_up, r_bu the relaxation of layer L-1 (read);
   // a_lo, a_up, b_up that of layer L-2; the two layers' bias vectors
@@ -317,6 +319,17 @@ __device__ __forceinline__ Relax1 relax_neuron(float l, float u, int sp, const f
   const float d = u - l;
   const float up = u / d;
   return {alpha ? *alpha : up, up, -(u * l) / d, 5};
+}
+
+// A sub-domain's bounds of one neuron intersected with its parent's (lp, up at index i, both
+// null when no parent bounds are given): a child is a subset of its parent, so the parent's
+// bounds hold on it.
+__device__ __forceinline__ void parent_clip(float& l, float& u, const float* lp, const float* up,
+                                            long i) {
+  if (lp) {
+    l = fmaxf(l, lp[i]);
+    u = fminf(u, up[i]);
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -2322,10 +2335,12 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
     const float vn = __shfl_xor(v, 1, 64);
     if (q >= Q || (r & 1)) return;  // (Q is even: row q + 1 exists)
     const unsigned b = q / R, jj = r >> 1;
-    s.lo[b * s.bstride + jj] = v;
-    s.hi[b * s.bstride + jj] = -vn;
     const long pi = (long)b * fc.n_relu + fc.off + jj;
-    const Relax1 rx = relax_neuron(v, -vn, fc.split ? fc.split[pi] : 0,
+    float lv = v, uv = -vn;
+    parent_clip(lv, uv, fc.lpar, fc.upar, pi);
+    s.lo[b * s.bstride + jj] = lv;
+    s.hi[b * s.bstride + jj] = uv;
+    const Relax1 rx = relax_neuron(lv, uv, fc.split ? fc.split[pi] : 0,
                                    fc.alpha ? fc.alpha + pi : nullptr);
     const long pp = (long)b * s.pstride + jj;
     fc.r_lo[pp] = rx.lo;
@@ -2373,7 +2388,8 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
                const float* __restrict__ z1, float eps, float* __restrict__ L,
                float* __restrict__ U, long n_relu, long off2, const int8_t* __restrict__ split,
                const float* __restrict__ alpha, float* __restrict__ lo2, float* __restrict__ up2,
-               float* __restrict__ bu2, int8_t* __restrict__ code2) {
+               float* __restrict__ bu2, int8_t* __restrict__ code2, const float* __restrict__ lpar,
+               const float* __restrict__ upar) {
   static_assert(C1 % 4 == 0 && K1 <= 4 && K2 <= 4, "unsupported geometry");
   constexpr int KS = C1 / 4;
   constexpr int NT = 64 * NW;
@@ -2573,7 +2589,8 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
     const int cc = threadIdx.x / XW, xi = threadIdx.x - cc * XW;
     const long j = ((long)(g * 8 + cc) * H2 + y2) * W2 + x2c * XW + xi;
     const long pi = b * n_relu + off2 + j;
-    const float l = vb[xi][cc], u = -vb[xi][cc + 8];
+    float l = vb[xi][cc], u = -vb[xi][cc + 8];
+    parent_clip(l, u, lpar, upar, pi);
     L[pi] = l;
     U[pi] = u;
     const Relax1 rx = relax_neuron(l, u, split ? split[pi] : 0, alpha ? alpha + pi : nullptr);
@@ -3589,18 +3606,20 @@ __global__ void __launch_bounds__(kBlock)
                    const float* __restrict__ lsh, const float* __restrict__ ush,
                    const int8_t* __restrict__ split, const float* __restrict__ alpha,
                    float* __restrict__ a_lo, float* __restrict__ a_up, float* __restrict__ b_up,
-                   int8_t* __restrict__ code) {
+                   int8_t* __restrict__ code, const float* __restrict__ lpar,
+                   const float* __restrict__ upar) {
   long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
   if (idx >= nb * nm) return;
   long b = idx / nm, j = idx % nm;
   long p = b * stride + off + j;
   long pp = b * pstride + poff + j;
-  if (lsh) {
-    l[p] = lsh[j];
-    u[p] = ush[j];
-  }
   const int sp = split ? split[p] : 0;
-  const float lj = lsh ? lsh[j] : l[p], uj = ush ? ush[j] : u[p];
+  float lj = lsh ? lsh[j] : l[p], uj = ush ? ush[j] : u[p];
+  parent_clip(lj, uj, lpar, upar, p);
+  if (lsh || lpar) {
+    l[p] = lj;
+    u[p] = uj;
+  }
   const Relax1 r = relax_neuron(lj, uj, sp, alpha ? alpha + p : nullptr);
   a_lo[pp] = r.lo;
   a_up[pp] = r.up;
@@ -3616,7 +3635,8 @@ __global__ void __launch_bounds__(kBlock)
                     const float* __restrict__ lsh, const float* __restrict__ ush,
                     const int8_t* __restrict__ split, const float* __restrict__ alpha,
                     float* __restrict__ a_lo, float* __restrict__ a_up, float* __restrict__ b_up,
-                    int8_t* __restrict__ code) {
+                    int8_t* __restrict__ code, const float* __restrict__ lpar,
+                    const float* __restrict__ upar) {
   long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
   if (idx >= nb * nm4) return;
   long b = idx / nm4, j = (idx % nm4) * 4;
@@ -3626,11 +3646,22 @@ __global__ void __launch_bounds__(kBlock)
   if (lsh) {
     lv = *reinterpret_cast<const float4v*>(lsh + j);
     uv = *reinterpret_cast<const float4v*>(ush + j);
-    *reinterpret_cast<float4v*>(l + p) = lv;
-    *reinterpret_cast<float4v*>(u + p) = uv;
   } else {
     lv = *reinterpret_cast<const float4v*>(l + p);
     uv = *reinterpret_cast<const float4v*>(u + p);
+  }
+  if (lpar) {
+    const float4v pl = *reinterpret_cast<const float4v*>(lpar + p);
+    const float4v pu = *reinterpret_cast<const float4v*>(upar + p);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      lv[r] = fmaxf(lv[r], pl[r]);
+      uv[r] = fminf(uv[r], pu[r]);
+    }
+  }
+  if (lsh || lpar) {
+    *reinterpret_cast<float4v*>(l + p) = lv;
+    *reinterpret_cast<float4v*>(u + p) = uv;
   }
   const int sp4 = split ? *reinterpret_cast<const int*>(split + p) : 0;
   float4v lo, up, bu;
@@ -4507,7 +4538,8 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Kernel for the receptive-field pass 2, or null when the shapes do not qualify.
 using Pass2Kernel = void (*)(DLayer, DLayer, long, const float*, const float*, const float*, long,
                              const float*, float, float*, float*, long, long, const int8_t*,
-                             const float*, float*, float*, float*, int8_t*);
+                             const float*, float*, float*, float*, int8_t*, const float*,
+                             const float*);
 // Windows per block of the receptive-field pass 2 (along x2): 8 when the map width allows it
 // (fewer blocks, each set-up shared by more windows), else 4.
 int p2_xw(const lirpa_net* net) { return net->T[1].out_w % 8 == 0 ? 8 : 4; }
@@ -4828,6 +4860,8 @@ struct Chunk {
   const float* alpha;
   hipStream_t st;
   bool tape = false;   // record the gradient tape (mode-1 plan)
+  const float* lp = nullptr;  // the parent sub-domains' l, u (chunk's first row) or null
+  const float* up = nullptr;
 };
 
 // Sink that relaxes onto ReLU layer m and stores into `out`.
@@ -4872,21 +4906,22 @@ int relax_layer(const Chunk& c, int m, const float* lsh = nullptr, const float* 
   const bool vec4 = nm % 4 == 0 && net->n_relu % 4 == 0 && off % 4 == 0 &&
                     net->pstride % 4 == 0 && net->poff[m] % 4 == 0 && al(c.L, 16) &&
                     al(c.U, 16) && al(lsh, 16) && al(ush, 16) && al(c.alpha, 16) &&
-                    al(c.split, 4) && al(c.ws, 256);
+                    al(c.split, 4) && al(c.ws, 256) && al(c.lp, 16) && al(c.up, 16);
   return launch_k(tag("relax_params", m, m), c.st, [&] {
     if (vec4) {
       hipLaunchKernelGGL(k_relax_params4, grid_for(c.nb * (nm / 4)), dim3(kBlock), 0, c.st,
                          c.nb, nm / 4, net->n_relu, off, net->pstride, net->poff[m], c.L, c.U,
                          lsh, ush, c.split, c.alpha, at<float>(c.ws, c.p->off_alo),
                          at<float>(c.ws, c.p->off_aup), at<float>(c.ws, c.p->off_bup),
-                         at<int8_t>(c.ws, c.p->off_code));
+                         at<int8_t>(c.ws, c.p->off_code), c.lp, c.up);
       return;
     }
     hipLaunchKernelGGL(k_relax_params, grid_for(c.nb * nm), dim3(kBlock), 0, c.st, c.nb, nm,
                        net->n_relu, off, net->pstride, net->poff[m], c.L, c.U, lsh, ush,
                        c.split, c.alpha,
                        at<float>(c.ws, c.p->off_alo), at<float>(c.ws, c.p->off_aup),
-                       at<float>(c.ws, c.p->off_bup), at<int8_t>(c.ws, c.p->off_code));
+                       at<float>(c.ws, c.p->off_bup), at<int8_t>(c.ws, c.p->off_code), c.lp,
+                       c.up);
   });
 }
 
@@ -5057,7 +5092,7 @@ int pass2_window(const Chunk& c) {
                        at<float>(c.ws, c.p->off_z1), c.eps, c.L, c.U, net->n_relu, net->off[2],
                        c.split, c.alpha, at<float>(c.ws, c.p->off_alo) + p2,
                        at<float>(c.ws, c.p->off_aup) + p2, at<float>(c.ws, c.p->off_bup) + p2,
-                       at<int8_t>(c.ws, c.p->off_code));
+                       at<int8_t>(c.ws, c.p->off_code), c.lp, c.up);
   });
 }
 
@@ -5205,6 +5240,8 @@ int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   f.code = at<int8_t>(c.ws, c.p->off_code);
   f.n_relu = net->n_relu;
   f.off = net->off[k];
+  f.lpar = c.lp;
+  f.upar = c.up;
   const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
   return launch_k(tag("convT_fc_bound", k - 1, k), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[k - 2]),
@@ -5700,12 +5737,17 @@ int validate_enqueue(const lirpa_net* net, const float* x0, const float* C, int 
 // lirpa_bound on a workspace that holds chunks of Bc sub-domains (plan p).
 int bound_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float eps, const float* C,
               int S, int B, const int8_t* split, const float* alpha, float* lb, float* l_out,
-              float* u_out, int8_t* code_out, void* ws, hipStream_t stream) {
+              float* u_out, int8_t* code_out, void* ws, hipStream_t stream,
+              const float* l_par = nullptr, const float* u_par = nullptr) {
   if (int e = validate_report(stream)) return e;
   if (int e = validate_enqueue(net, x0, C, S, B, split, alpha, stream)) return e;
   if (int e = layer1_bounds(net, p, ws, x0, eps, C, S, stream)) return e;
   for (long b0 = 0; b0 < B; b0 += Bc) {
     Chunk c = make_chunk(net, p, ws, x0, eps, S, B, b0, split, alpha, l_out, u_out, stream);
+    if (l_par) {
+      c.lp = l_par + b0 * net->n_relu;
+      c.up = u_par + b0 * net->n_relu;
+    }
     if (int e = bound_chunk(c, C, lb + b0 * S)) return e;
     if (code_out && net->n_relu)
       if (int e = copy_d2d(code_out + b0 * net->n_relu, at<int8_t>(ws, p.off_code),
@@ -6124,6 +6166,24 @@ int lirpa_bound(lirpa_net* net, const float* x0, float eps, const float* C, int 
                 make_plan(net, S, 1).total);
   return bound_run(net, p, Bc, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out, ws,
                    stream);
+}
+
+int lirpa_bound_child(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,
+                      const int8_t* split, const float* alpha, const float* l_parent,
+                      const float* u_parent, float* lb, float* l_out, float* u_out,
+                      int8_t* code_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (int e = check_common(net, x0, eps, C, S, B, ws)) return e;
+  if (!lb) return fail(LIRPA_EINVAL, "lb is null");
+  if (!l_parent || !u_parent) return fail(LIRPA_EINVAL, "l_parent and u_parent must be given");
+  if ((l_out == nullptr) != (u_out == nullptr))
+    return fail(LIRPA_EINVAL, "l_out and u_out must both be given or both be null");
+  Plan p;
+  long Bc = fit_chunk(net, S, B, ws_bytes, &p);
+  if (Bc < 1)
+    return fail(LIRPA_ENOMEM, "workspace of %zu bytes holds no sub-domain (need %zu)", ws_bytes,
+                make_plan(net, S, 1).total);
+  return bound_run(net, p, Bc, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out, ws,
+                   stream, l_parent, u_parent);
 }
 
 int lirpa_bound_noalloc(lirpa_net* net, const float* x0, float eps, const float* C, int S, int B,

@@ -56,7 +56,8 @@ class lirpa_kernel_time(ctypes.Structure):
 
 
 SYMBOLS = ("lirpa_net_create", "lirpa_net_destroy", "lirpa_net_num_relu",
-           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_noalloc", "lirpa_bound_ul",
+           "lirpa_workspace_bytes", "lirpa_bound", "lirpa_bound_child", "lirpa_bound_noalloc",
+           "lirpa_bound_ul",
            "lirpa_bound_grad", "lirpa_optimize", "lirpa_optimize_ul",
            "lirpa_bab_workspace_bytes", "lirpa_bab",
            "lirpa_timing_begin", "lirpa_timing_end", "lirpa_last_error")
@@ -84,6 +85,8 @@ def load() -> ctypes.CDLL:
     L.lirpa_workspace_bytes.restype = sz
     L.lirpa_bound.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, sz, P]
     L.lirpa_bound.restype = i
+    L.lirpa_bound_child.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, P, P, sz, P]
+    L.lirpa_bound_child.restype = i
     L.lirpa_bound_noalloc.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P]
     L.lirpa_bound_noalloc.restype = i
     L.lirpa_bound_ul.argtypes = [P, P, f, P, i, i, P, P, P, P, P, P, P, P, sz, P]
@@ -192,6 +195,18 @@ def lirpa_bound(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out,
                               _dev(u_out, torch.float32, "u_out"),
                               _dev(code_out, torch.int8, "code_out"), _dev(ws, None, "ws"),
                               int(ws_bytes), _stream(stream)))
+
+
+def lirpa_bound_child(net, x0, eps, C, S, B, split, alpha, l_parent, u_parent, lb, l_out, u_out,
+                      code_out, ws, ws_bytes, stream=None):
+    f32 = torch.float32
+    _check(load().lirpa_bound_child(net, _dev(x0, f32, "x0"), float(eps), _dev(C, f32, "C"),
+                                    int(S), int(B), _dev(split, torch.int8, "split"),
+                                    _dev(alpha, f32, "alpha"), _dev(l_parent, f32, "l_parent"),
+                                    _dev(u_parent, f32, "u_parent"), _dev(lb, f32, "lb"),
+                                    _dev(l_out, f32, "l_out"), _dev(u_out, f32, "u_out"),
+                                    _dev(code_out, torch.int8, "code_out"), _dev(ws, None, "ws"),
+                                    int(ws_bytes), _stream(stream)))
 
 
 def lirpa_bound_noalloc(net, x0, eps, C, S, B, split, alpha, lb, l_out, u_out, code_out,
@@ -323,6 +338,18 @@ class Network:
         if want_codes:
             out = out + (code,)
         return out if len(out) > 1 else lb
+
+    def bound_child(self, x0, eps, C, split, alpha, l_parent, u_parent, max_ws_bytes=16 << 30):
+        """(lb, l, u, codes) with every layer's bounds intersected with the parent's."""
+        S, B = C.shape[0], l_parent.shape[0]
+        lb = torch.empty((B, S), dtype=torch.float32, device=self.device)
+        l = torch.empty((B, self.n_relu), dtype=torch.float32, device=self.device)
+        u = torch.empty_like(l)
+        code = torch.empty((B, self.n_relu), dtype=torch.int8, device=self.device)
+        ws, ws_bytes = self.workspace(S, B, 0, max_ws_bytes)
+        lirpa_bound_child(self.handle, x0, eps, C, S, B, split, alpha, l_parent, u_parent, lb, l,
+                          u, code, ws, ws_bytes)
+        return lb, l, u, code
 
     def bound_ul(self, x0, eps, C, split=None, alpha=None, B=None, max_ws_bytes=16 << 30):
         """(lb, ub) [B, S] of the spec rows: Eq. 8's lower and upper bounds in one call."""
