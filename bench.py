@@ -185,6 +185,15 @@ def grad_work(layers, S, B):
                                                        4.0 * (3 * B * n[1] + parts))
             work["pass2_grad_gather[layer1,pass2]"] = (0.0, 4.0 * (parts + 3 * B * n[1]))
             continue
+        if P == 3 and P < L and all(layers[i]["kind"] == wl.CONV for i in (0, 1)) \
+                and layers[2]["kind"] == wl.FC:
+            # both convolutions of pass 3's witness forward in one kernel (launched for the
+            # shapes the library covers): their flops; bytes: the signs of A_x (one byte per
+            # input), the recorded coefficients over g^(1), the adjoint partial sums of both
+            # layers (3 floats per neuron and group of 8 rows)
+            work[f"fwd12[layer1,pass{P}]"] = (
+                2.0 * Q * (macs(layers[0]) + macs(layers[1])),
+                n[0] * Q + 4.0 * n[1] * Q + 12.0 * (n[1] + n[2]) * Q / 8)
         for m in range(1, P):
             t = layers[m - 1]
             inb = n[0] * Q if m == 1 else 4.0 * n[m - 1] * Q

@@ -3810,6 +3810,331 @@ __device__ __forceinline__ float sum8(float v) {
   return v;
 }
 
+// Sum of v over the 8 rows of a position in k_fwd_conv12's layout: the lane's four rows are
+// summed in place, then with the four rows of the lane 16 away (v_permlane16_swap exchanges rows
+// 0 <-> 1 and 2 <-> 3 of 16 lanes; with the same value in both operands, the two results are
+// the lane's own and its partner's value).
+__device__ __forceinline__ float sum_rows8(const float4v& v) {
+  const float own = (v[0] + v[1]) + (v[2] + v[3]);
+  const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(own), __float_as_uint(own),
+                                                   false, false);
+  return __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+}
+
+// The witness forward of a pass opened at a Linear layer T_3 over two convolutions
+// T_1: Conv(3 -> C1, k4 s2 p1, 32x32 -> 16x16) and T_2: Conv(C1 -> C2, k4 s2 p1, 16x16 -> 8x8)
+// (pass 3 of the Base and Wide nets), both layers in one kernel, with the adjoint sums of both
+// layers fused.  One block (4 waves) takes one group of 8 rows q of the pass, which lie in one
+// sub-domain (R is a multiple of 8).  It runs x* = x0 - eps sign(A_x) through T_1 (G_1, the
+// adjoint terms of layer 1 against the recorded coefficients A~_1, then the row's relaxation
+// line z_1), keeps z_1 in an LDS ring instead of writing it out, and runs z_1 through T_2 (G_2,
+// the adjoint terms of layer 2 against A~_2 = +-W_3[j], the row's own coefficients).
+// Both convolutions are gather-form implicit GEMMs on 16x16x4 MFMA with the activations as the
+// A operand: M = the 8 rows at two output positions (m = 8 p + row), N = 16 output channels,
+// one K step per (input channel, tap row) with the tap column as the lane group.  A lane then
+// holds four rows (4 (g & 1) .. + 3, position g >> 1) of one output channel n: its adjoint
+// terms are summed over the rows in place and once across lanes (sum_rows8), its z_1 values
+// are one 16-byte LDS store, and its recorded coefficients one 16-byte read.
+// Schedule over the output rows y2 of T_2: conv2 row y2 reads z_1 rows 2 y2 - 1 .. 2 y2 + 2
+// (ring of 4 slots, row mod 4); then conv1 computes z_1 rows 2 y2 + 3 and 2 y2 + 4 into the two
+// slots conv2 just finished with, from x* rows 4 y2 + 5 .. 4 y2 + 10 (ring of 6 slots, row
+// mod 6).  While conv2 runs, the block fetches with coalesced 16-byte loads what conv1 will
+// need -- the four new x* rows (signs and x0), and for its two rows the recorded coefficients
+// A~_1 and the layer-1 relaxation -- and parks them in LDS.  Rows outside a map are zero slots
+// (the convolutions' zero padding).  Adjoint sums are written as k_fwd_conv writes them
+// ([group][term][position][channel]).  The LDS footprint lets two blocks share a CU, so one
+// block's barriers overlap the other's work.  No load carries a per-lane condition (such a
+// value makes the wave wait for it at once): out-of-map rows and rows past Q read clamped,
+// in-bounds entries that are zeroed or meet a zero weight where they are used.
+template <int C1, int C2>
+__global__ void __launch_bounds__(256, 2)
+    k_fwd_conv12(DLayer t1, DLayer t2, const int8_t* __restrict__ sgn, unsigned ldq, unsigned Q,
+                 unsigned R, const float* __restrict__ w, const float* __restrict__ x0, float eps,
+                 const float* __restrict__ tape1, const float* __restrict__ a_lo,
+                 const float* __restrict__ a_up, const float* __restrict__ b_up,
+                 unsigned pstride, const float* __restrict__ W3, unsigned nk,
+                 float* __restrict__ part1, float* __restrict__ part2,
+                 unsigned char* __restrict__ gflag) {
+  constexpr int C0 = 3, K = 4, S = 2, HX = 32, H1 = 16, H2 = 8;
+  constexpr int N1 = C1 * H1 * H1, N2 = C2 * H2 * H2;
+  constexpr int XW1 = (H1 - 1) * S + K;  // x* ring columns: x = -1 .. 32
+  constexpr int XW2 = (H2 - 1) * S + K;  // z_1 ring columns: x1 = -1 .. 16
+  constexpr int XROW = C0 * XW1 * 8, ZROW = C1 * XW2 * 8;
+  constexpr int NX = 6, NZ = 4;          // ring slots
+  constexpr int NKS1 = C0 * K, NKS2 = C1 * K;
+  constexpr int NMT2 = C2 / 16;          // channel tiles of T_2
+  static_assert(C1 == 8 || C1 == 16, "T_1 output channels");
+  static_assert(C2 == 16 || C2 == 32, "T_2 output channels");
+  // conv1 epilogue operands of the two rows of an iteration: relaxation [row][a_lo, a_up, b_up]
+  // [x1][channel] and coefficients [row][x1][channel][q]
+  constexpr int EPP = 2 * 3 * H1 * C1, EPT = 2 * H1 * C1 * 8;
+  __shared__ __attribute__((aligned(16))) float xr[NX * XROW];
+  __shared__ __attribute__((aligned(16))) float zr[NZ * ZROW];
+  __shared__ float ep_p[EPP];
+  __shared__ __attribute__((aligned(16))) float ep_t[EPT];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const int qr = n & 7, pp = n >> 3;  // A operand: this lane's row and position of a pair
+  const int qb = 4 * (g & 1), pd = g >> 1;  // D: this lane's first row and position
+  const unsigned grp = xcd_range(blockIdx.x);
+  const unsigned q0 = grp * 8u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  // the lane's four D rows: weight, sign and row of W_3 of each (rows past Q: weight 0)
+  float wq[4], tsg[4];
+  const float* w3r[4];
+  bool any = false;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const unsigned q = q0 + qb + r;
+    const bool ok = q < Q;
+    wq[r] = ok ? w[min(q, Q - 1)] : 0.f;
+    const unsigned ra = q % R;
+    tsg[r] = !ok ? 0.f : (ra < nk ? 1.f : -1.f);
+    w3r[r] = W3 + (size_t)(ra % nk) * N2;
+    any |= wq[r] != 0.f;
+  }
+  {
+    const bool live = __syncthreads_or(any) != 0;
+    if (tid == 0) gflag[grp] = live ? 1 : 0;
+    if (!live) return;  // uniform: the whole block is idle
+  }
+  const unsigned b = q0 / R;  // the group's sub-domain
+  const int mt2 = wave % NMT2;
+
+  // B operands: lane (n, g) holds W[co = n][ci][ky][kx = g] per K step (ci, ky); the bias of
+  // this lane's output channel
+  float w1r[NKS1], w2r[NKS2];
+#pragma unroll
+  for (int ks = 0; ks < NKS1; ++ks)
+    w1r[ks] = n < C1 ? t1.W[((n * C0 + ks / K) * K + ks % K) * K + g] : 0.f;
+#pragma unroll
+  for (int ks = 0; ks < NKS2; ++ks)
+    w2r[ks] = t2.W[(((mt2 * 16 + n) * C1 + ks / K) * K + ks % K) * K + g];
+  const float b1 = n < C1 ? t1.b[n] : 0.f;
+  const int co2 = mt2 * 16 + n;
+  const float b2 = t2.b[co2];
+
+  auto xslot = [](int yi) { return (yi + 6 * NX) % NX; };
+  auto zslot = [](int y1) { return (y1 + 4 * NZ) % NZ; };
+
+  // pad columns of every slot, and the z_1 row -1 (slot 3), are zero for good
+  for (int e = tid; e < NX * C0 * 2 * 8; e += 256) {
+    const int qq = e & 7, side = (e >> 3) & 1, sc = e >> 4;
+    xr[(sc * XW1 + (side ? XW1 - 1 : 0)) * 8 + qq] = 0.f;
+  }
+  for (int e = tid; e < NZ * C1 * 2 * 8; e += 256) {
+    const int qq = e & 7, side = (e >> 3) & 1, sc = e >> 4;
+    zr[(sc * XW2 + (side ? XW2 - 1 : 0)) * 8 + qq] = 0.f;
+  }
+  for (int e = tid; e < ZROW; e += 256) zr[zslot(-1) * ZROW + e] = 0.f;
+
+  // x* rows, 4 at a time: element e = (row j, channel ci, column x, half h of the 8 rows); the
+  // signs of 4 rows are one 32-bit word of the byte tape
+  constexpr int NXE = 4 * C0 * HX * 2;
+  constexpr int XPT = NXE / 256;
+  static_assert(NXE % 256 == 0, "whole x* elements per thread");
+  int sw[XPT];
+  float sx[XPT];
+  auto fetch_x = [&](int yfirst) {
+#pragma unroll
+    for (int k = 0; k < XPT; ++k) {
+      const int e = tid + k * 256;
+      const int h = e & 1, x = (e >> 1) % HX, ci = (e >> 1) / HX % C0;
+      const int yc = min(max(yfirst + e / (2 * C0 * HX), 0), HX - 1);
+      sw[k] = *reinterpret_cast<const int*>(
+          sgn + (size_t)((ci * HX + yc) * HX + x) * ldq + q0 + 4 * h);
+      sx[k] = x0[(ci * HX + yc) * HX + x];
+    }
+  };
+  auto park_x = [&](int yfirst) {
+#pragma unroll
+    for (int k = 0; k < XPT; ++k) {
+      const int e = tid + k * 256;
+      const int h = e & 1, x = (e >> 1) % HX, ci = (e >> 1) / HX % C0;
+      const int yi = yfirst + e / (2 * C0 * HX);
+      const bool in = yi >= 0 && yi < HX;
+      float4v v;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        v[jj] = in ? sx[k] - eps * (float)(int8_t)(sw[k] >> (8 * jj)) : 0.f;
+      *reinterpret_cast<float4v*>(xr + ((xslot(yi) * C0 + ci) * XW1 + x + 1) * 8 + 4 * h) = v;
+    }
+  };
+  // conv1 epilogue operands of rows ya, ya + 1 (a row past the map reads row H1 - 1: unused):
+  // relaxation element e = (row, param, channel, quad of x1), coefficient element
+  // e = (row, channel, x1, half of the 8 rows q), each one 16-byte load
+  constexpr int NPE = 2 * 3 * C1 * 4, NTE = 2 * C1 * H1 * 2;
+  constexpr int PPT = (NPE + 255) / 256, TPT = NTE / 256;
+  static_assert(NTE % 256 == 0, "whole coefficient elements per thread");
+  float4v pv[PPT], tv[TPT];
+  auto fetch_ep = [&](int ya) {
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+      const int e = min(tid + k * 256, NPE - 1);
+      const int x4 = e & 3, c = (e >> 2) % C1, pr = (e >> 2) / C1 % 3, r2 = e / (4 * C1 * 3);
+      const int y1 = min(ya + r2, H1 - 1);
+      const float* src = pr == 0 ? a_lo : (pr == 1 ? a_up : b_up);
+      pv[k] = *reinterpret_cast<const float4v*>(src + (size_t)b * pstride +
+                                                (c * H1 + y1) * H1 + 4 * x4);
+    }
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+      const int e = tid + k * 256;
+      const int h = e & 1, x1 = (e >> 1) % H1, c = (e >> 1) / H1 % C1, r2 = e / (2 * H1 * C1);
+      const int y1 = min(ya + r2, H1 - 1);
+      tv[k] = *reinterpret_cast<const float4v*>(
+          tape1 + (size_t)((c * H1 + y1) * H1 + x1) * ldq + q0 + 4 * h);
+    }
+  };
+  auto park_ep = [&]() {
+#pragma unroll
+    for (int k = 0; k < PPT; ++k) {
+      const int e = tid + k * 256;
+      if (NPE % 256 == 0 || e < NPE) {
+        const int x4 = e & 3, c = (e >> 2) % C1, pr = (e >> 2) / C1 % 3, r2 = e / (4 * C1 * 3);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ep_p[((r2 * 3 + pr) * H1 + 4 * x4 + i) * C1 + c] = pv[k][i];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < TPT; ++k) {
+      const int e = tid + k * 256;
+      const int h = e & 1, x1 = (e >> 1) % H1, c = (e >> 1) / H1 % C1, r2 = e / (2 * H1 * C1);
+      *reinterpret_cast<float4v*>(ep_t + ((r2 * H1 + x1) * C1 + c) * 8 + 4 * h) = tv[k];
+    }
+  };
+
+  // one T_1 position pair (row y1 = ya + r2, columns 2 xp, 2 xp + 1)
+  auto conv1_pos = [&](int y1, int r2, int xp) {
+    const float* xb[K];
+#pragma unroll
+    for (int ky = 0; ky < K; ++ky)
+      xb[ky] = xr + xslot(2 * y1 - 1 + ky) * XROW + (2 * (2 * xp + pp) + g) * 8 + qr;
+    float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NKS1; ++ks)
+      d = __builtin_amdgcn_mfma_f32_16x16x4f32(xb[ks % K][(ks / K) * XW1 * 8], w1r[ks], d, 0, 0,
+                                               0);
+    const int x1 = 2 * xp + pd;
+    const int c = min(n, C1 - 1);  // (lanes of channels past C1 read a valid entry, unused)
+    const float4v tt = *reinterpret_cast<const float4v*>(ep_t + ((r2 * H1 + x1) * C1 + c) * 8 + qb);
+    const float lo = ep_p[((r2 * 3 + 0) * H1 + x1) * C1 + c];
+    const float up = ep_p[((r2 * 3 + 1) * H1 + x1) * C1 + c];
+    const float bu = ep_p[((r2 * 3 + 2) * H1 + x1) * C1 + c];
+    float4v ta, tb, tc, z;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float gv = d[r] + b1;
+      // a row without weight (rows past Q included) gets zero terms and z_1 = 0
+      const float t = wq[r] != 0.f ? tt[r] : 0.f;
+      const float tp = fmaxf(t, 0.f), tn = fminf(t, 0.f);
+      ta[r] = (wq[r] * tp) * gv;
+      tb[r] = (wq[r] * tn) * gv;
+      tc[r] = wq[r] * tn;
+      z[r] = wq[r] == 0.f ? 0.f : (t >= 0.f ? lo * gv : fmaf(up, gv, bu));
+    }
+    if (n < C1)
+      *reinterpret_cast<float4v*>(zr + ((zslot(y1) * C1 + n) * XW2 + x1 + 1) * 8 + qb) = z;
+    const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
+    if ((g & 1) == 0 && n < C1) {
+      float* dst = part1 + (size_t)grp * 3 * N1 + (size_t)(y1 * H1 + x1) * C1 + n;
+      dst[0] = sa;
+      dst[N1] = da;
+      dst[2 * N1] = db;
+    }
+  };
+  // a T_1 row: 8 position pairs, pairs wave and wave + 4
+  auto conv1_row = [&](int y1, int r2) {
+    if (y1 >= H1) {
+      // the z_1 row below the map: zeros
+      for (int e2 = tid; e2 < ZROW; e2 += 256) zr[zslot(y1) * ZROW + e2] = 0.f;
+      return;
+    }
+    conv1_pos(y1, r2, wave);
+    conv1_pos(y1, r2, wave + 4);
+  };
+  // a T_2 row: 4 position pairs times NMT2 channel tiles, NMT2 per wave
+  constexpr int P2W = NMT2;
+  auto xp2 = [&](int k) { return wave / NMT2 + k * (4 / NMT2); };
+  // this lane's entries of the rows' coefficients over g^(2), +-W_3[j] at (co2, y2, x2)
+  auto load_tw = [&](int y2, float4v* tw) {
+#pragma unroll
+    for (int k = 0; k < P2W; ++k) {
+      const int o = (co2 * H2 + y2) * H2 + 2 * xp2(k) + pd;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) tw[k][r] = tsg[r] * w3r[r][o];
+    }
+  };
+  auto conv2_pos = [&](int y2, int xp, const float4v& tw) {
+    const float* zb[K];
+#pragma unroll
+    for (int ky = 0; ky < K; ++ky)
+      zb[ky] = zr + zslot(2 * y2 - 1 + ky) * ZROW + (2 * (2 * xp + pp) + g) * 8 + qr;
+    float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NKS2; ++ks)
+      d = __builtin_amdgcn_mfma_f32_16x16x4f32(zb[ks % K][(ks / K) * XW2 * 8], w2r[ks], d, 0, 0,
+                                               0);
+    float4v ta, tb, tc;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float gv = d[r] + b2;
+      const float tp = fmaxf(tw[r], 0.f), tn = fminf(tw[r], 0.f);
+      ta[r] = (wq[r] * tp) * gv;
+      tb[r] = (wq[r] * tn) * gv;
+      tc[r] = wq[r] * tn;
+    }
+    const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
+    if ((g & 1) == 0) {
+      const int x2 = 2 * xp + pd;
+      float* dst = part2 + (size_t)grp * 3 * N2 + (size_t)(y2 * H2 + x2) * C2 + co2;
+      dst[0] = sa;
+      dst[N2] = da;
+      dst[2 * N2] = db;
+    }
+  };
+
+  // prologue: z_1 row 0 (epilogue operands of rows 0, 1), then rows 1, 2
+  fetch_x(-1);
+  fetch_ep(0);
+  park_x(-1);
+  park_ep();
+  __syncthreads();
+  conv1_row(0, 0);
+  fetch_x(3);
+  __syncthreads();  // x* row 0's slot is free
+  park_x(3);
+  __syncthreads();
+  conv1_row(1, 1);
+  fetch_ep(2);
+  __syncthreads();  // the staged operands of rows 0, 1 are consumed
+  park_ep();
+  __syncthreads();
+  conv1_row(2, 0);
+  __syncthreads();
+
+  for (int y2 = 0; y2 < H2; ++y2) {
+    const int ya = 2 * y2 + 3, yb = 2 * y2 + 4;  // z_1 rows this iteration adds
+    const bool more = ya < H1 + 1;               // (row 16 is the zero row)
+    float4v tw[P2W];
+    load_tw(y2, tw);
+    if (more) {
+      fetch_x(4 * y2 + 7);
+      fetch_ep(ya);
+    }
+#pragma unroll
+    for (int k = 0; k < P2W; ++k) conv2_pos(y2, xp2(k), tw[k]);
+    if (!more) break;
+    park_x(4 * y2 + 7);
+    park_ep();
+    __syncthreads();  // staged rows visible; every wave is done with the z_1 slots it overwrites
+    conv1_row(ya, 0);
+    conv1_row(yb, 1);
+    __syncthreads();  // z_1 rows visible to the next conv2 row; staged operands consumed
+  }
+}
+
 // Adjoint accumulation for ReLU layer m from the partial sums of the fused witness forward: for
 // each (sub-domain, neuron), the R/8 groups of 8 rows of the sub-domain in increasing order (an
 // order fixed by the rows alone, so the result does not depend on where the sub-domain sits in
@@ -4527,6 +4852,7 @@ struct Plan {
   // adjoint partial sums of the fused witness forward, [Qp/8][3][n_m], and a flag per group of
   // 8 rows (whether any row of the group carries weight)
   size_t off_gpart = 0, off_gflag = 0;
+  size_t off_gpart2 = 0;  // layer-2 partial sums of the fused two-layer witness forward
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -4592,6 +4918,27 @@ long pass2_blocks(const lirpa_net* net, long nb) {
 // Whether bound mode (no gradient tape) runs pass k, 2 <= k < L, in one kernel that keeps the
 // pass's coefficients on chip: such a pass needs no bound-matrix slab.
 bool pass_on_chip(const lirpa_net* net, int k, long Bc);
+
+// The fused two-layer witness forward of pass 3 (k_fwd_conv12) for a net whose T_1 is
+// Conv(3 -> C1, k4 s2 p1, 32x32), T_2 Conv(C1 -> C2, k4 s2 p1, 16x16) and T_3 Linear, with
+// (C1, C2) = (8, 16) or (16, 32); null otherwise.
+using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
+                             const float*, const float*, float, const float*, const float*,
+                             const float*, const float*, unsigned, const float*, unsigned, float*,
+                             float*, unsigned char*);
+Fwd12Kernel fwd12_for(const lirpa_net* net) {
+  if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
+  const lirpa_layer &a = net->T[0], &t = net->T[1];
+  if (a.kind != LIRPA_CONV2D || t.kind != LIRPA_CONV2D) return nullptr;
+  const bool ga = a.k == 4 && a.stride == 2 && a.pad == 1 && a.in_c == 3 && a.in_h == 32 &&
+                  a.in_w == 32 && a.out_h == 16 && a.out_w == 16;
+  const bool gt = t.k == 4 && t.stride == 2 && t.pad == 1 && t.in_h == 16 && t.in_w == 16 &&
+                  t.out_h == 8 && t.out_w == 8;
+  if (!ga || !gt) return nullptr;
+  if (a.out_c == 8 && t.out_c == 16) return k_fwd_conv12<8, 16>;
+  if (a.out_c == 16 && t.out_c == 32) return k_fwd_conv12<16, 32>;
+  return nullptr;
+}
 
 Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
   Plan p;
@@ -4680,6 +5027,11 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
     }
     p.off_gpart = o; o = align256(o + (size_t)gpart * 4);
     p.off_gflag = o; o = align256(o + (size_t)gflag);
+    if (fwd12_for(net)) {
+      // pass 3's layer-2 partial sums, written by the same kernel as its layer-1 sums
+      p.off_gpart2 = o;
+      o = align256(o + (size_t)(round_up(Bc * 2 * net->n[3], 64) / 8) * 3 * net->n[2] * 4);
+    }
   }
   p.total = o;
   // kernels address a slab with 32-bit element offsets
@@ -5551,6 +5903,40 @@ int grad_chunk(const Chunk& c, int full) {
                              net->n_relu, offP, (int)(P == L), gl, gu, w);
         }))
       return e;
+    if (P == 3 && P < L && R % 8 == 0 && p.off_gpart && p.off_gpart2 && fc_open_ok(c, P, R)) {
+      if (Fwd12Kernel fk = fwd12_for(net)) {
+        // both convolutions of pass 3's witness forward in one kernel, then both layers' sums
+        const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
+        float* part1 = at<float>(c.ws, p.off_gpart);
+        float* part2 = at<float>(c.ws, p.off_gpart2);
+        unsigned char* gflag = at<unsigned char>(c.ws, p.off_gflag);
+        const unsigned nblk8 = (unsigned)round_up((Q + 7) / 8, 8);
+        if (int e = launch_k(tag("fwd12", 1, P), c.st, [&] {
+              hipLaunchKernelGGL(fk, dim3(nblk8), dim3(256), 0, c.st, dlayer(t1), dlayer(t2),
+                                 tsign_of(c, P), (unsigned)ldq, (unsigned)Q, (unsigned)R, w,
+                                 c.x0, c.eps, tape_of(c, P, 1),
+                                 at<float>(c.ws, p.off_alo) + net->poff[1],
+                                 at<float>(c.ws, p.off_aup) + net->poff[1],
+                                 at<float>(c.ws, p.off_bup) + net->poff[1],
+                                 (unsigned)net->pstride, net->T[2].W, (unsigned)net->n[3], part1,
+                                 part2, gflag);
+            }))
+          return e;
+        for (int m = 1; m <= 2; ++m) {
+          const lirpa_layer& t = net->T[m - 1];
+          const long off = net->off[m];
+          if (int e = launch_k(tag("grad_gather", m, P), c.st, [&] {
+                hipLaunchKernelGGL(k_grad_gather, grid_for(c.nb * net->n[m]), dim3(kBlock), 0,
+                                   c.st, c.nb, t.out_c, t.out_h * t.out_w, R,
+                                   m == 1 ? part1 : part2, gflag,
+                                   at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
+                                   net->n_relu, ga + off, gl + off, gu + off);
+              }))
+            return e;
+        }
+        continue;
+      }
+    }
     // the first layer's input is the witness, built from the pass's sign tape (bytes; the
     // forward kernels with WITNESS read their input pointer as int8_t)
     const float* zin = reinterpret_cast<const float*>(tsign_of(c, P));
