@@ -3859,7 +3859,10 @@ __global__ void __launch_bounds__(256, 2)
   constexpr int N1 = C1 * H1 * H1, N2 = C2 * H2 * H2;
   constexpr int XW1 = (H1 - 1) * S + K;  // x* ring columns: x = -1 .. 32
   constexpr int XW2 = (H2 - 1) * S + K;  // z_1 ring columns: x1 = -1 .. 16
-  constexpr int XROW = C0 * XW1 * 8, ZROW = C1 * XW2 * 8;
+  // z_1 ring channel stride: 4 floats of padding put the 16-byte stores of the 16 channels of a
+  // position on distinct banks
+  constexpr int ZCS = XW2 * 8 + 4;
+  constexpr int XROW = C0 * XW1 * 8, ZROW = C1 * ZCS;
   constexpr int NX = 6, NZ = 4;          // ring slots
   constexpr int NKS1 = C0 * K, NKS2 = C1 * K;
   constexpr int NMT2 = C2 / 16;          // channel tiles of T_2
@@ -3925,7 +3928,7 @@ __global__ void __launch_bounds__(256, 2)
   }
   for (int e = tid; e < NZ * C1 * 2 * 8; e += 256) {
     const int qq = e & 7, side = (e >> 3) & 1, sc = e >> 4;
-    zr[(sc * XW2 + (side ? XW2 - 1 : 0)) * 8 + qq] = 0.f;
+    zr[sc * ZCS + (side ? XW2 - 1 : 0) * 8 + qq] = 0.f;
   }
   for (int e = tid; e < ZROW; e += 256) zr[zslot(-1) * ZROW + e] = 0.f;
 
@@ -3962,9 +3965,10 @@ __global__ void __launch_bounds__(256, 2)
     }
   };
   // conv1 epilogue operands of rows ya, ya + 1 (a row past the map reads row H1 - 1: unused):
-  // relaxation element e = (row, param, channel, quad of x1), coefficient element
-  // e = (row, channel, x1, half of the 8 rows q), each one 16-byte load
-  constexpr int NPE = 2 * 3 * C1 * 4, NTE = 2 * C1 * H1 * 2;
+  // relaxation element e = (row, param, quad of x1, channel), coefficient element
+  // e = (row, x1, channel, half of the 8 rows q), each one 16-byte load; consecutive threads
+  // take consecutive channels, so that their LDS stores fall on distinct banks
+  constexpr int NPE = 2 * 3 * 4 * C1, NTE = 2 * H1 * C1 * 2;
   constexpr int PPT = (NPE + 255) / 256, TPT = NTE / 256;
   static_assert(NTE % 256 == 0, "whole coefficient elements per thread");
   float4v pv[PPT], tv[TPT];
@@ -3972,7 +3976,7 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
     for (int k = 0; k < PPT; ++k) {
       const int e = min(tid + k * 256, NPE - 1);
-      const int x4 = e & 3, c = (e >> 2) % C1, pr = (e >> 2) / C1 % 3, r2 = e / (4 * C1 * 3);
+      const int c = e % C1, x4 = (e / C1) & 3, pr = e / (4 * C1) % 3, r2 = e / (4 * C1 * 3);
       const int y1 = min(ya + r2, H1 - 1);
       const float* src = pr == 0 ? a_lo : (pr == 1 ? a_up : b_up);
       pv[k] = *reinterpret_cast<const float4v*>(src + (size_t)b * pstride +
@@ -3981,7 +3985,7 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
       const int e = tid + k * 256;
-      const int h = e & 1, x1 = (e >> 1) % H1, c = (e >> 1) / H1 % C1, r2 = e / (2 * H1 * C1);
+      const int h = e & 1, c = (e >> 1) % C1, x1 = (e >> 1) / C1 % H1, r2 = e / (2 * H1 * C1);
       const int y1 = min(ya + r2, H1 - 1);
       tv[k] = *reinterpret_cast<const float4v*>(
           tape1 + (size_t)((c * H1 + y1) * H1 + x1) * ldq + q0 + 4 * h);
@@ -3992,7 +3996,7 @@ __global__ void __launch_bounds__(256, 2)
     for (int k = 0; k < PPT; ++k) {
       const int e = tid + k * 256;
       if (NPE % 256 == 0 || e < NPE) {
-        const int x4 = e & 3, c = (e >> 2) % C1, pr = (e >> 2) / C1 % 3, r2 = e / (4 * C1 * 3);
+        const int c = e % C1, x4 = (e / C1) & 3, pr = e / (4 * C1) % 3, r2 = e / (4 * C1 * 3);
 #pragma unroll
         for (int i = 0; i < 4; ++i) ep_p[((r2 * 3 + pr) * H1 + 4 * x4 + i) * C1 + c] = pv[k][i];
       }
@@ -4000,7 +4004,7 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
       const int e = tid + k * 256;
-      const int h = e & 1, x1 = (e >> 1) % H1, c = (e >> 1) / H1 % C1, r2 = e / (2 * H1 * C1);
+      const int h = e & 1, c = (e >> 1) % C1, x1 = (e >> 1) / C1 % H1, r2 = e / (2 * H1 * C1);
       *reinterpret_cast<float4v*>(ep_t + ((r2 * H1 + x1) * C1 + c) * 8 + 4 * h) = tv[k];
     }
   };
@@ -4035,7 +4039,7 @@ __global__ void __launch_bounds__(256, 2)
       z[r] = wq[r] == 0.f ? 0.f : (t >= 0.f ? lo * gv : fmaf(up, gv, bu));
     }
     if (n < C1)
-      *reinterpret_cast<float4v*>(zr + ((zslot(y1) * C1 + n) * XW2 + x1 + 1) * 8 + qb) = z;
+      *reinterpret_cast<float4v*>(zr + zslot(y1) * ZROW + n * ZCS + (x1 + 1) * 8 + qb) = z;
     const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
     if ((g & 1) == 0 && n < C1) {
       float* dst = part1 + (size_t)grp * 3 * N1 + (size_t)(y1 * H1 + x1) * C1 + n;
@@ -4074,8 +4078,7 @@ __global__ void __launch_bounds__(256, 2)
     float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < NKS2; ++ks)
-      d = __builtin_amdgcn_mfma_f32_16x16x4f32(zb[ks % K][(ks / K) * XW2 * 8], w2r[ks], d, 0, 0,
-                                               0);
+      d = __builtin_amdgcn_mfma_f32_16x16x4f32(zb[ks % K][(ks / K) * ZCS], w2r[ks], d, 0, 0, 0);
     float4v ta, tb, tc;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
