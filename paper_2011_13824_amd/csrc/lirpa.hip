@@ -3097,14 +3097,16 @@ __global__ void __launch_bounds__(512)
 // sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
 // the layer-1 relaxation and G_r the layer-1 pre-activation at the row's witness
 // x* = x0 + delta, delta = -eps sign(A_x) (zero outside the footprint), i.e.
-// G_r = z1 + W_1 delta over the window.  A block takes the 16 rows of k_pass2_window (one
-// sub-domain, eight channels, both signs) in XW consecutive windows along x2; per window it
-// rebuilds the relaxed patch and A_x over the footprint on MFMA, keeps delta in LDS, runs the
-// layer-1 forward over the window on MFMA, reduces the 16 rows' contributions per window neuron
-// and writes them to part[window][c1][pos] (windows numbered (b, group, y2, x2)).  The weights
-// are loaded once per block and the next window's relaxation while this one is computed.  Row
-// weights: w = g_l (sign +) or -g_u (sign -) of the row's layer-2 neuron; a window none of whose
-// rows carries weight writes zeros.
+// G_r = z1 + W_1 delta over the window.  Only rows with a nonzero weight contribute, and at an
+// unstable-sparse layer 2 they are few, so the rows of a position are compacted: of the 2 C2
+// rows +-e_(c2, y2, x2) (taken in the order (c2, sign)), the live ones are numbered in that
+// order and slot s of the position takes live rows 16 s .. 16 s + 15 (slots past the last live
+// row carry weight 0).  A block takes slot s of XW consecutive positions along x2 of one
+// sub-domain; per window it rebuilds the relaxed patch and A_x over the footprint on MFMA,
+// keeps delta in LDS, runs the layer-1 forward over the window on MFMA, reduces the 16 rows'
+// contributions per window neuron and writes them to part[window][c1][pos] (windows numbered
+// (b, slot, y2, x2)).  A window without live rows writes zeros.  Row weights: w = g_l (sign +)
+// or -g_u (sign -) of the row's layer-2 neuron.
 template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 3 : 4, 8)))
     k_pass2_window_grad(DLayer t1, DLayer t2, const float* __restrict__ a_lo,
@@ -3130,6 +3132,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
   // byte per entry keeps the block's LDS small
   __shared__ signed char dl[NW * WO * WO * 16];
   __shared__ float wrow[XW][16];
+  __shared__ unsigned short rid[XW][16];  // the slot's rows: 2 c2 + (sign -)
   __shared__ float4v prm[NE];  // a_lo, a_up, z1, unstable (1/0) of the window (0 outside)
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -3147,27 +3150,47 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
   const int H1 = t1.out_h, Wd1 = t1.out_w;
   const long pb = b * pstride;
 
-  if (threadIdx.x < 16 * XW) {
-    const int xi = threadIdx.x >> 4, r = threadIdx.x & 15;
-    const P2Row pr = p2_row(C2, g, r);
-    const long j = ((long)pr.c2 * H2 + y2) * W2 + x2c * XW + xi;
-    wrow[xi][r] = pr.neg ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
+  // slot g of each position: one wave per position numbers the live rows by ballot
+  for (int xi = wave; xi < XW; xi += NW) {
+    int base = 0;
+    for (int c0r = 0; c0r < 2 * C2; c0r += 64) {
+      const int ci = c0r + lane, c2 = ci >> 1;
+      float wgt = 0.f;
+      if (ci < 2 * C2) {
+        const long j = ((long)c2 * H2 + y2) * W2 + x2c * XW + xi;
+        wgt = (ci & 1) ? -gu[b * n_relu + off2 + j] : gl[b * n_relu + off2 + j];
+      }
+      const bool live = wgt != 0.f;
+      const unsigned long long m = __ballot(live);
+      const int r = base + (int)__builtin_amdgcn_mbcnt_hi(
+                               (unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u)) -
+                    16 * g;
+      if (live && r >= 0 && r < 16) {
+        wrow[xi][r] = wgt;
+        rid[xi][r] = (unsigned short)ci;
+      }
+      base += __popcll(m);
+    }
+    if (lane < 16 && 16 * g + lane >= base) {  // past the last live row
+      wrow[xi][lane] = 0.f;
+      rid[xi][lane] = 0;
+    }
   }
 
   // this thread's entries of W_2 for the tile fills (row = tid mod 16, entries part,
-  // part + RPT, ...), signed by the row, the same for every window
+  // part + RPT, ...), signed by the row; the rows differ from window to window
   const int row = threadIdx.x & 15, partid = threadIdx.x >> 4;
   float wv[NEP];
-  {
-    const P2Row pr = p2_row(C2, g, row);
-    const float sgn = pr.neg ? -1.f : 1.f;
-    const float* w2 = t2.W + (long)pr.c2 * NE;
+  auto wload = [&](int xi) {
+    const int ci = rid[xi][row];
+    const float sgn = (ci & 1) ? -1.f : 1.f;
+    const float* w2 = t2.W + (long)(ci >> 1) * NE;
 #pragma unroll
     for (int k = 0; k < NEP; ++k) {
       const int e = partid + k * RPT;
       wv[k] = e < NE ? sgn * w2[e] : 0.f;
     }
-  }
+  };
   auto toff = [&](int k) {  // tile place of the thread's entry k
     const int e = partid + k * RPT;
     const int c1 = e / NPOS, pos = e - c1 * NPOS;
@@ -3238,6 +3261,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
       continue;
     }
     // (1) stage the window's relaxation; fetch the next window's; relaxed window coefficients
+    wload(xi);
 #pragma unroll
     for (int k = 0; k < NPP; ++k) {
       const int e = threadIdx.x + k * NT;
