@@ -1735,8 +1735,13 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 //     with NXW = NM each SIMD holds one wave of either role.
 // The bound of a row is then its bias terms minus eps ||A_x||_1 (the linear term sits in the
 // layer-1 bias).
+// TAPE (FC source, for the reverse sweep): the matrix waves also store each parked row over
+// g^(1), unrelaxed, to Sink::tape, and the x waves the sign of each entry of A_x to Sink::tsign,
+// both [entry][ldq] with the block's 16 rows contiguous (rows past Q included: they lie inside
+// the padded width ldq, and hold zeros).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
-          int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS, int SPEC = 0>
+          int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS, int SPEC = 0,
+          bool TAPE = false>
 __global__ void __launch_bounds__(64 * (CI / CPW + NXW))
 __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3), 8)))
     k_convT_fc_bound(DLayer t, DLayer t1, const float* __restrict__ in, unsigned ldq, unsigned Q,
@@ -1763,6 +1768,7 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
   // [NBS sub-domains][RSL][CI][W0 (+1 pad)]
   static_assert(NBS == 2 || NBS == 3, "sub-domains per block");
   static_assert(SPEC == 0 || !FC, "the spec source replaces the slab source");
+  static_assert(!TAPE || FC, "tapes are written for the FC source only");
   constexpr int NMT_S = CO * W1 / 16;  // spec source: 16-entry tiles of an input row
   static_assert(SPEC == 0 || (NMT_S % (CI / CPW) == 0 && W1 % 4 == 0), "spec tiles per wave");
   static_assert(SPEC == 0 || NMT_S / (CI / CPW) <= 2, "spec operands: two tiles per wave");
@@ -1820,6 +1826,21 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
       float* dst = ring[e & 1] + r * ROWF + (wave * CPW + c) * CS1 + n;
 #pragma unroll
       for (int x = 0; x < W0; ++x) dst[x * 16] = v[x];
+      if constexpr (TAPE) {
+        // buffer stores: a block-uniform base (the channel's plane) and a 32-bit lane offset
+        const int y = yrow(e, r);
+        if (y >= 0 && y < H0) {
+          float* plane = s.tape + (size_t)(wave * CPW + c) * (H0 * W0) * ldq + q0;
+          const unsigned boff = ((unsigned)y * W0 * ldq + (unsigned)n) * 4u;
+#pragma unroll
+          for (int x = 0; x < W0; ++x) {
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc(plane, (short)0, 0x7fffffff, 0x00020000);
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[x]), rs, boff,
+                                                  (unsigned)x * ldq * 4u, 0);
+          }
+        }
+      }
     };
     // layer-1 relaxation of stage e: loaded into registers at the start of step e, written to
     // pars[e & 1] at its end.  Entries of rows outside the map or of a second sub-domain the
@@ -2170,6 +2191,19 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
   float l1 = 0.f, beta = 0.f;
   float pend[C0 * NSH];  // right shared columns of the pending row
   bool pend_ok = false;
+  int pend_y = 0;
+  // TAPE: the sign of entry (c0, yx, g) of this lane's row
+  // (lane offset: the row yx and the lane's q; the uniform part, channel and column, goes in
+  // the scalar offset, so that no per-column address stays live in vector registers)
+  auto put_sign = [&](int c0, int yx, int g, float a) {
+    if constexpr (TAPE) {
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc(s.tsign + q0, (short)0, 0x7fffffff, 0x00020000);
+      const unsigned voff = (unsigned)(yx * WX) * ldq + (unsigned)n;
+      const unsigned soff = (unsigned)(c0 * HX * WX + g) * ldq;
+      __builtin_amdgcn_raw_buffer_store_b8((unsigned char)sign8(a), rs, voff, soff, 0);
+    }
+  };
   // output row yx completed by this lane (step parity par)
   auto emit = [&](int yx, int par) {
     const bool ok = yx >= 0 && yx < HX;
@@ -2180,7 +2214,10 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
         const int g = OL + x;
         const bool left = HASL && x < NSH, right = HASR && x >= OW - NSH;
         const float a = colv(c0, x);
-        if (!left && !right && g >= 0 && g < WX && ok) l1 += fabsf(a);
+        if (!left && !right && g >= 0 && g < WX && ok) {
+          l1 += fabsf(a);
+          put_sign(c0, yx, g, a);
+        }
         if (left) xb[par][XB - 1][c0 * NSH + x][lane] = a;
         if (right) pend[c0 * NSH + x - (OW - NSH)] = a;
       }
@@ -2188,14 +2225,21 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
     for (int c0 = 0; c0 < C0; ++c0)
 #pragma unroll
       for (int m = 0; m < NF; ++m) ev[c0][m] = od[c0][m] = float4v{0.f, 0.f, 0.f, 0.f};
-    if (HASR) pend_ok = ok;
+    if (HASR) {
+      pend_ok = ok;
+      pend_y = yx;
+    }
   };
   // the pending row of the previous step (parity par): add the right neighbour's part
   auto resolve = [&](int par) {
     if constexpr (HASR) {
       if (pend_ok) {
 #pragma unroll
-        for (int v = 0; v < C0 * NSH; ++v) l1 += fabsf(pend[v] + xb[par][XB][v][lane]);
+        for (int v = 0; v < C0 * NSH; ++v) {
+          const float a = pend[v] + xb[par][XB][v][lane];
+          l1 += fabsf(a);
+          put_sign(v / NSH, pend_y, OL + OW - NSH + v % NSH, a);
+        }
       }
       pend_ok = false;
     }
@@ -3711,9 +3755,9 @@ __global__ void __launch_bounds__(kBlock)
 
 // Row weights of pass P: 1 for the spec rows of the final pass (J = sum_s lb_s); for pass P < L
 // the adjoints of the bounds it produced: row +e_j carries g_l[j], row -e_j carries -g_u[j]
-// (u_j = -lb of that row).
+// (u_j = -lb of that row); the two signs in halves of R, or interleaved (inter).
 __global__ void __launch_bounds__(kBlock) k_row_weights(long Q, long R, long nP, long n_relu,
-                                                        long offP, int final_pass,
+                                                        long offP, int final_pass, int inter,
                                                         const float* __restrict__ gl,
                                                         const float* __restrict__ gu,
                                                         float* __restrict__ w) {
@@ -3724,7 +3768,10 @@ __global__ void __launch_bounds__(kBlock) k_row_weights(long Q, long R, long nP,
     return;
   }
   long b = q / R, r = q % R;
-  w[q] = r < nP ? gl[b * n_relu + offP + r] : -gu[b * n_relu + offP + (r - nP)];
+  if (inter)  // rows 2j, 2j + 1: +e_j, -e_j
+    w[q] = (r & 1) ? -gu[b * n_relu + offP + (r >> 1)] : gl[b * n_relu + offP + (r >> 1)];
+  else
+    w[q] = r < nP ? gl[b * n_relu + offP + r] : -gu[b * n_relu + offP + (r - nP)];
 }
 
 // Forward step of the witness pass through layer m for every row with a non-zero weight.
@@ -3876,7 +3923,7 @@ __global__ void __launch_bounds__(256, 2)
                  unsigned R, const float* __restrict__ w, const float* __restrict__ x0, float eps,
                  const float* __restrict__ tape1, const float* __restrict__ a_lo,
                  const float* __restrict__ a_up, const float* __restrict__ b_up,
-                 unsigned pstride, const float* __restrict__ W3, unsigned nk,
+                 unsigned pstride, const float* __restrict__ W3, unsigned nk, unsigned inter,
                  float* __restrict__ part1, float* __restrict__ part2,
                  unsigned char* __restrict__ gflag) {
   constexpr int C0 = 3, K = 4, S = 2, HX = 32, H1 = 16, H2 = 8;
@@ -3916,9 +3963,11 @@ __global__ void __launch_bounds__(256, 2)
     const unsigned q = q0 + qb + r;
     const bool ok = q < Q;
     wq[r] = ok ? w[min(q, Q - 1)] : 0.f;
+    // row ra of the sub-domain: +-e_j, the signs in two halves or interleaved (inter)
     const unsigned ra = q % R;
-    tsg[r] = !ok ? 0.f : (ra < nk ? 1.f : -1.f);
-    w3r[r] = W3 + (size_t)(ra % nk) * N2;
+    const bool neg = inter ? (ra & 1u) != 0 : ra >= nk;
+    tsg[r] = !ok ? 0.f : (neg ? -1.f : 1.f);
+    w3r[r] = W3 + (size_t)(inter ? ra >> 1 : ra % nk) * N2;
     any |= wq[r] != 0.f;
   }
   {
@@ -4951,8 +5000,8 @@ bool pass_on_chip(const lirpa_net* net, int k, long Bc);
 // (C1, C2) = (8, 16) or (16, 32); null otherwise.
 using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
                              const float*, const float*, float, const float*, const float*,
-                             const float*, const float*, unsigned, const float*, unsigned, float*,
-                             float*, unsigned char*);
+                             const float*, const float*, unsigned, const float*, unsigned,
+                             unsigned, float*, float*, unsigned char*);
 Fwd12Kernel fwd12_for(const lirpa_net* net) {
   if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
   const lirpa_layer &a = net->T[0], &t = net->T[1];
@@ -5319,9 +5368,10 @@ int8_t* tsign_of(const Chunk& c, int pass) {
 // at most); null otherwise.
 using FcBoundKernel = void (*)(DLayer, DLayer, const float*, unsigned, unsigned, Sink, FcSrc);
 // (spec: the variant that takes the final pass's spec rows from C W_L through a closing
-// Linear layer of 97..100 features; conv 3 -> 8 -> 16 channels, three sub-domains per block)
+// Linear layer of 97..100 features; conv 3 -> 8 -> 16 channels, three sub-domains per block;
+// tape: the FC variant that also writes the reverse sweep's tape over g^(1) and sign tape)
 FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwaves,
-                               bool spec = false) {
+                               bool spec = false, bool tape = false) {
   if (net->L < 3) return nullptr;
   const lirpa_layer &t2 = net->T[1], &t1 = net->T[0];
   if (t2.kind != LIRPA_CONV2D || t1.kind != LIRPA_CONV2D) return nullptr;
@@ -5341,6 +5391,9 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
                  : k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 1, 4, 2, 1, 32, 32, 3, 4, false, 3,
                                     25>;
     }
+    if (fc && tape)
+      return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, true, 2, 0,
+                              true>;
     if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
     if (nbs == 2)
       return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 16, 8, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
@@ -5350,6 +5403,9 @@ FcBoundKernel conv12_bound_for(const lirpa_net* net, bool fc, int nbs, int* nwav
   // sub-domains per block would not fit in LDS)
   if (t1.out_c == 16 && t2.in_c == 16 && t2.out_c == 32 && (fc || nbs == 2) && !spec) {
     *nwaves = 16 / 2 + 4;
+    if (fc && tape)
+      return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, true, 2, 0,
+                              true>;
     if (fc) return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, true, 2>;
     return k_convT_fc_bound<4, 2, 1, 8, 8, 16, 16, 32, 16, 2, 4, 2, 1, 32, 32, 3, 4, false, 2>;
   }
@@ -5584,17 +5640,31 @@ int fc_open_stage(const Chunk& c, int k, long R, long Q, long ldq) {
 
 // Pass 3 of a net whose layers 1 and 2 are such convolutions and whose layer 3 is fully
 // connected, bounded without a gradient tape: one kernel from the rows of W_3 to the bounds.
-FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves) {
+FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves, bool tape = false) {
   if (k != 3 || net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
-  return conv12_bound_for(net, true, 2, nwaves);
+  return conv12_bound_for(net, true, 2, nwaves, false, tape);
+}
+
+// Whether pass k of a gradient chunk runs as one tape-writing k_convT_fc_bound.  Its rows are
+// then interleaved (row 2j: +e_j, row 2j + 1: -e_j) and the reverse sweep of the pass runs
+// k_fwd_conv12, which reads the two tapes that kernel writes.
+bool fused_tape_pass(const Chunk& c, int k, long R) {
+  int nw = 0;
+  // the kernel's tape stores take 32-bit byte offsets within a channel plane of g^(1) and
+  // within the sign tape
+  const double ldq = (double)round_up(c.nb * R, 64);
+  if (4.0 * 256 * ldq >= 2147483647.0 || 3072.0 * ldq >= 2147483647.0) return false;
+  return c.tape && k == 3 && R % 8 == 0 && fc_open_ok(c, k, R) && c.p->off_gpart &&
+         c.p->off_gpart2 && fwd12_for(c.net) && fc_bound_for(c.net, k, &nw, true);
 }
 
 // Returns 1 when the pass does not qualify (the caller runs the stages one by one).
 int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   const lirpa_net* net = c.net;
   int nw = 0;
-  FcBoundKernel kern = fc_bound_for(net, k, &nw);
-  if (!kern || c.tape || !fc_open_ok(c, k, R)) return 1;
+  const bool tape = c.tape;
+  FcBoundKernel kern = fc_bound_for(net, k, &nw, tape);
+  if (!kern || !fc_open_ok(c, k, R) || (tape && !fused_tape_pass(c, k, R))) return 1;
   const lirpa_layer& fl = net->T[k - 1];
   Sink s = slab_sink(c, 1, nullptr, 0, R);  // the relaxation of layer 1 (bias: z1)
   const Sink sb = bound_sink(c, R, c.L + net->off[k], c.U + net->off[k], net->n_relu, net->n[k]);
@@ -5621,10 +5691,15 @@ int fc_bound_stage(const Chunk& c, int k, long R, long Q) {
   f.off = net->off[k];
   f.lpar = c.lp;
   f.upar = c.up;
+  const long ldq = round_up(Q, 64);
+  if (tape) {
+    s.tape = tape_of(c, k, 1);
+    s.tsign = tsign_of(c, k);
+  }
   const unsigned nblk16 = (unsigned)round_up((Q + 15) / 16, 16);
   return launch_k(tag("convT_fc_bound", k - 1, k), c.st, [&] {
     hipLaunchKernelGGL(kern, dim3(nblk16), dim3(64 * nw), 0, c.st, dlayer(net->T[k - 2]),
-                       dlayer(net->T[0]), nullptr, 0u, (unsigned)Q, s, f);
+                       dlayer(net->T[0]), nullptr, tape ? (unsigned)ldq : 0u, (unsigned)Q, s, f);
   });
 }
 
@@ -5712,7 +5787,7 @@ int bound_chunk(const Chunk& c, const float* C, float* lb) {
         continue;
       }
     }
-    if (!c.tape) {
+    {
       int e = fc_bound_stage(c, k, R, Q);
       if (e != 1) {
         if (e) return e;  // (the kernel also wrote the relaxation of layer k)
@@ -5925,9 +6000,11 @@ int grad_chunk(const Chunk& c, int full) {
     }
     long R = (P < L) ? 2 * net->n[P] : c.S, Q = c.nb * R, ldq = round_up(Q, 64);
     long offP = (P < L) ? net->off[P] : 0;
+    // rows of a pass bounded by the tape-writing k_convT_fc_bound are interleaved
+    const bool inter = P < L && fused_tape_pass(c, P, R);
     if (int e = launch_k(tag("row_weights", P, P), c.st, [&] {
           hipLaunchKernelGGL(k_row_weights, grid_for(Q), dim3(kBlock), 0, c.st, Q, R, net->n[P],
-                             net->n_relu, offP, (int)(P == L), gl, gu, w);
+                             net->n_relu, offP, (int)(P == L), (int)inter, gl, gu, w);
         }))
       return e;
     if (P == 3 && P < L && R % 8 == 0 && p.off_gpart && p.off_gpart2 && fc_open_ok(c, P, R)) {
@@ -5945,8 +6022,8 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_alo) + net->poff[1],
                                  at<float>(c.ws, p.off_aup) + net->poff[1],
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
-                                 (unsigned)net->pstride, net->T[2].W, (unsigned)net->n[3], part1,
-                                 part2, gflag);
+                                 (unsigned)net->pstride, net->T[2].W, (unsigned)net->n[3],
+                                 (unsigned)inter, part1, part2, gflag);
             }))
           return e;
         for (int m = 1; m <= 2; ++m) {
@@ -5964,6 +6041,8 @@ int grad_chunk(const Chunk& c, int full) {
         continue;
       }
     }
+    if (inter)  // (fused_tape_pass implies every condition of the branch above)
+      return fail(LIRPA_EUNSUPPORTED, "pass %d: interleaved rows without k_fwd_conv12", P);
     // the first layer's input is the witness, built from the pass's sign tape (bytes; the
     // forward kernels with WITNESS read their input pointer as int8_t)
     const float* zin = reinterpret_cast<const float*>(tsign_of(c, P));
