@@ -4186,6 +4186,9 @@ __global__ void __launch_bounds__(256, 2)
   fetch_ep(2);
   __syncthreads();  // the staged operands of rows 0, 1 are consumed
   park_ep();
+  // the operands of the first iteration's conv1 rows: in flight during row 2 and conv2 row 0
+  fetch_x(7);
+  fetch_ep(3);
   __syncthreads();
   conv1_row(2, 0);
   __syncthreads();
@@ -4195,15 +4198,16 @@ __global__ void __launch_bounds__(256, 2)
     const bool more = ya < H1 + 1;               // (row 16 is the zero row)
     float4v tw[P2W];
     load_tw(y2, tw);
-    if (more) {
-      fetch_x(4 * y2 + 7);
-      fetch_ep(ya);
-    }
 #pragma unroll
     for (int k = 0; k < P2W; ++k) conv2_pos(y2, xp2(k), tw[k]);
     if (!more) break;
     park_x(4 * y2 + 7);
     park_ep();
+    // the next iteration's operands: in flight during this iteration's conv1 and the next conv2
+    if (ya + 2 < H1 + 1) {
+      fetch_x(4 * y2 + 11);
+      fetch_ep(ya + 2);
+    }
     __syncthreads();  // staged rows visible; every wave is done with the z_1 slots it overwrites
     conv1_row(ya, 0);
     conv1_row(yb, 1);
