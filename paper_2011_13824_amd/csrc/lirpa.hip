@@ -4536,39 +4536,69 @@ __global__ void __launch_bounds__(kBlock)
 }
 
 // The same accumulation when the pass has few rows per sub-domain (R <= 64, e.g. the spec rows
-// of the final pass): one wave per (sub-domain, 64 consecutive neurons), a lane per neuron
-// summing its R rows in order.  The row weights are uniform over the wave and the adjoint
-// updates of the wave are contiguous.
-__global__ void __launch_bounds__(kBlock)
-    k_grad_reduce_rows(long nb, long nm, long R, long ldq, const float* __restrict__ w,
-                       const float* __restrict__ tape, const float* __restrict__ G,
-                       const int8_t* __restrict__ code, const float* __restrict__ l,
-                       const float* __restrict__ u, long n_relu, float* __restrict__ ga,
-                       float* __restrict__ gl, float* __restrict__ gu) {
-  const long nw = (nm + 63) / 64;  // waves per sub-domain
-  const long wv = blockIdx.x * (long)(blockDim.x / 64) + threadIdx.x / 64;
-  if (wv >= nb * nw) return;  // uniform per wave
-  const long b = wv / nw, j = (wv % nw) * 64 + (threadIdx.x & 63);
-  if (j >= nm) return;
-  float sa = 0.f, da = 0.f, db = 0.f;
-  const float* tj = tape + j * ldq;
-  const float* gj = G + j * ldq;
-  for (long r = 0; r < R; ++r) {
-    const long q = b * R + r;
-    const float wr = w[q];
-    if (wr == 0.f) continue;  // uniform per wave
-    const float tv = tj[q], g = gj[q];
-    const float tp = fmaxf(tv, 0.f), tn = fminf(tv, 0.f);
-    sa = fmaf(wr * tp, g, sa);
-    da = fmaf(wr * tn, g, da);
-    db = fmaf(wr, tn, db);
+// of the final pass).  The tape and G are [neuron][ldq] with a sub-domain's rows contiguous, so a
+// block takes 64 consecutive neurons and SPW = min(floor(64 / R), 16) consecutive sub-domains:
+// for each neuron, lane l of a wave reads row q0 + l of the window (coalesced along q), forms
+// the row's three terms, and lane s < SPW then sums the R terms of sub-domain b0 + s in row
+// order from the wave's LDS scratch.  The block's results are written out with the neurons fastest.  Rows
+// with weight 0 contribute nothing and are not read (their G may never have been written).
+__global__ void __launch_bounds__(256)
+    k_grad_reduce_seg(long nb, long nm, long R, long ldq, const float* __restrict__ w,
+                      const float* __restrict__ tape, const float* __restrict__ G,
+                      const int8_t* __restrict__ code, const float* __restrict__ l,
+                      const float* __restrict__ u, long n_relu, float* __restrict__ ga,
+                      float* __restrict__ gl, float* __restrict__ gu) {
+  __shared__ float scr[4][3][64];  // per wave: the window's row terms
+  __shared__ float res[3][16][65];  // [term][sub-domain slot][neuron] (+1: no bank conflicts)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int SPW = (int)(R >= 4 ? 64 / R : 16), QW = SPW * (int)R;
+  const long njt = (nm + 63) / 64;
+  const long j0 = (long)(blockIdx.x % njt) * 64;
+  const long b0 = (long)(blockIdx.x / njt) * SPW;
+  const long q = b0 * R + lane;
+  const bool qok = lane < QW && b0 + lane / R < nb;
+  const float wq = qok ? w[q] : 0.f;
+  for (int jj = 0; jj < 16; ++jj) {
+    const int jl = wave * 16 + jj;
+    const long j = j0 + jl;
+    float ca = 0.f, cd = 0.f, cb = 0.f;
+    if (j < nm && wq != 0.f) {
+      const float tv = tape[j * ldq + q], g = G[j * ldq + q];
+      const float tp = fmaxf(tv, 0.f), tn = fminf(tv, 0.f);
+      ca = (wq * tp) * g;
+      cd = (wq * tn) * g;
+      cb = wq * tn;
+    }
+    scr[wave][0][lane] = ca;
+    scr[wave][1][lane] = cd;
+    scr[wave][2][lane] = cb;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wave's LDS writes are done
+    if (lane < SPW) {
+      float sa = 0.f, da = 0.f, db = 0.f;
+      for (int r = 0; r < (int)R; ++r) {
+        sa += scr[wave][0][lane * R + r];
+        da += scr[wave][1][lane * R + r];
+        db += scr[wave][2][lane * R + r];
+      }
+      res[0][lane][jl] = sa;
+      res[1][lane][jl] = da;
+      res[2][lane][jl] = db;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // scr read before the next writes
   }
-  const long p = b * n_relu + j;
-  if (code[p] != 5) return;
-  float lj = l[p], uj = u[p], d = uj - lj, d2 = d * d;
-  ga[p] += sa;
-  gl[p] += (da * uj - db * uj * uj) / d2;
-  gu[p] += (-da * lj + db * lj * lj) / d2;
+  __syncthreads();
+  for (int e = threadIdx.x; e < SPW * 64; e += 256) {
+    const int sl = e >> 6, jl = e & 63;
+    const long b = b0 + sl, j = j0 + jl;
+    if (b >= nb || j >= nm) continue;
+    const long p = b * n_relu + j;
+    if (code[p] != 5) continue;
+    const float sa = res[0][sl][jl], da = res[1][sl][jl], db = res[2][sl][jl];
+    const float lj = l[p], uj = u[p], d = uj - lj, d2 = d * d;
+    ga[p] += sa;
+    gl[p] += (da * uj - db * uj * uj) / d2;
+    gu[p] += (-da * lj + db * lj * lj) / d2;
+  }
 }
 
 // Projected Adam ascent step (bias-corrected), alpha clipped to [0, 1].
@@ -6099,8 +6129,9 @@ int grad_chunk(const Chunk& c, int full) {
       }
       e = launch_k(tag("grad_reduce", m, P), c.st, [&] {
         if (R <= 64) {
-          const long waves = c.nb * ((net->n[m] + 63) / 64);
-          hipLaunchKernelGGL(k_grad_reduce_rows, dim3((unsigned)((waves + 3) / 4)), dim3(kBlock),
+          const long spw = R >= 4 ? 64 / R : 16;
+          const long blocks = ((net->n[m] + 63) / 64) * ((c.nb + spw - 1) / spw);
+          hipLaunchKernelGGL(k_grad_reduce_seg, dim3((unsigned)blocks), dim3(256),
                              0, c.st, c.nb, net->n[m], R, ldq, w, tp, G,
                              at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
                              net->n_relu, ga + off, gl + off, gu + off);
