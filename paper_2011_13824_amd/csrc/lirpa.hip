@@ -3866,6 +3866,106 @@ __global__ void __launch_bounds__(256)
   }
 }
 
+// The witness forward step through a Linear layer past the first (its input z is a
+// [in][ldq] slab), as a GEMM on 16x16x4 MFMA: M = 16 outputs o, N = 16 rows q, K = inputs.
+// Block: 64 rows (one N tile per wave) and every output (MT tiles of 16 per wave).  K runs in
+// chunks of 32 staged in LDS, the inputs as [k][q] and the weights as [o][k], double-buffered:
+// the next chunk's global loads are issued before the current chunk's MFMAs and parked after
+// them.  Epilogue as in k_fwd_mfma; rows without weight (and rows past Q, which read the
+// slab's padding) are computed but never stored.  in_c is a multiple of 4.
+template <int MT>
+__global__ void __launch_bounds__(256)
+    k_fwd_fc(DLayer t, const float* __restrict__ zin, unsigned ldq, unsigned Q, long R,
+             const float* __restrict__ w, const float* __restrict__ tape,
+             const float* __restrict__ a_lo, const float* __restrict__ a_up,
+             const float* __restrict__ b_up, long pstride, float* __restrict__ G,
+             float* __restrict__ zout) {
+  constexpr int KC = 32;
+  constexpr int ZS = 80;       // row stride of the input chunk: the 4 lane groups' reads of a
+                               // K step fall on distinct banks
+  constexpr int WS = KC + 4;   // row stride of the weight chunk (likewise for the 16 outputs)
+  constexpr int NW4 = MT * 16 * KC / 4;         // float4 of a weight chunk
+  constexpr int WPT = (NW4 + 255) / 256;
+  __shared__ __attribute__((aligned(16))) float zs[2][KC * ZS];
+  __shared__ __attribute__((aligned(16))) float ws[2][MT * 16 * WS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const unsigned q0 = xcd_range(blockIdx.x) * 64u;
+  if (q0 >= Q) return;  // grid padding, uniform per block
+  const unsigned q = q0 + 16u * wave + n;
+  const float wq = q < Q ? w[q] : 0.f;
+  if (__syncthreads_or(wq != 0.f) == 0) return;  // uniform: the whole block is idle
+  const int nin = t.in_c, nout = t.out_c;
+  const int nch = (nin + KC - 1) / KC;
+  float4v zr[2], wr[WPT];
+  auto fetch = [&](int c) {
+    const int k0 = c * KC;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {  // inputs: 32 x 64 floats, float4 e = (k, quarter of 16 rows)
+      const int e = tid + 256 * k, kk = e >> 4, q4 = e & 15;
+      zr[k] = k0 + kk < nin
+                  ? *reinterpret_cast<const float4v*>(zin + (size_t)(k0 + kk) * ldq + q0 + 4 * q4)
+                  : float4v{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int k = 0; k < WPT; ++k) {  // weights: MT 16 x 32 floats, float4 e = (o, k quarter)
+      const int e = tid + 256 * k, o = e >> 3, k4 = e & 7;
+      wr[k] = (e < NW4 && o < nout && k0 + 4 * k4 < nin)
+                  ? *reinterpret_cast<const float4v*>(t.W + (size_t)o * nin + k0 + 4 * k4)
+                  : float4v{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  auto park = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int e = tid + 256 * k, kk = e >> 4, q4 = e & 15;
+      *reinterpret_cast<float4v*>(&zs[buf][kk * ZS + 4 * q4]) = zr[k];
+    }
+#pragma unroll
+    for (int k = 0; k < WPT; ++k) {
+      const int e = tid + 256 * k, o = e >> 3, k4 = e & 7;
+      if (e < NW4) *reinterpret_cast<float4v*>(&ws[buf][o * WS + 4 * k4]) = wr[k];
+    }
+  };
+  float4v d[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) d[mt] = float4v{0.f, 0.f, 0.f, 0.f};
+  fetch(0);
+  park(0);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nch) fetch(c + 1);
+#pragma unroll
+    for (int ks = 0; ks < KC / 4; ++ks) {
+      const float bv = zs[buf][(4 * ks + g) * ZS + 16 * wave + n];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        d[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(ws[buf][(mt * 16 + n) * WS + 4 * ks + g], bv,
+                                                     d[mt], 0, 0, 0);
+    }
+    if (c + 1 < nch) park(buf ^ 1);
+    __syncthreads();
+  }
+  // lane (n, g) holds outputs mt 16 + 4 g + r of row q
+  if (q >= Q || wq == 0.f) return;
+  const long b = q / R;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int o = mt * 16 + 4 * g + r;
+      if (o >= nout) continue;
+      const float gv = d[mt][r] + t.b[o];
+      const size_t idx = (size_t)o * ldq + q;
+      G[idx] = gv;
+      if (zout) {
+        const long pi = b * pstride + o;
+        zout[idx] = tape[idx] >= 0.f ? a_lo[pi] * gv : fmaf(a_up[pi], gv, b_up[pi]);
+      }
+    }
+}
+
 // Sum over each group of 8 consecutive lanes (lanes 8k..8k+7), valid in lanes 8k..8k+3: two
 // butterfly steps inside each quad, then the quad 4 lanes up (DPP, no LDS; a row rotation by r
 // hands lane i the value of lane i - r of its row of 16).
@@ -6096,8 +6196,29 @@ int grad_chunk(const Chunk& c, int full) {
       const int tnk = wtape ? (int)net->n[P] : 0;
       float* gpart = fused ? at<float>(c.ws, p.off_gpart) : nullptr;
       unsigned char* gflag = fused ? at<unsigned char>(c.ws, p.off_gflag) : nullptr;
+      // a Linear layer past the first: the GEMM kernel (up to 128 outputs)
+      const lirpa_layer& tl = net->T[m - 1];
+      const bool fc_gemm = !fk && m > 1 && tl.kind == LIRPA_LINEAR && tl.in_c % 4 == 0 &&
+                           tl.out_c <= 128;
       int e = launch_k(tag("fwd", m, P), c.st, [&] {
-        if (fk)
+        if (fc_gemm) {
+          auto kf = k_fwd_fc<8>;
+          switch ((tl.out_c + 15) / 16) {
+            case 1: kf = k_fwd_fc<1>; break;
+            case 2: kf = k_fwd_fc<2>; break;
+            case 3: kf = k_fwd_fc<3>; break;
+            case 4: kf = k_fwd_fc<4>; break;
+            case 5: kf = k_fwd_fc<5>; break;
+            case 6: kf = k_fwd_fc<6>; break;
+            case 7: kf = k_fwd_fc<7>; break;
+            default: break;
+          }
+          const unsigned nblk64 = (unsigned)round_up((Q + 63) / 64, 8);
+          hipLaunchKernelGGL(kf, dim3(nblk64), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
+                             (unsigned)Q, R, w, tp, at<float>(c.ws, p.off_alo) + poff,
+                             at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
+                             net->pstride, G, zout);
+        } else if (fk)
           hipLaunchKernelGGL(fk, dim3(nblk16), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
                              (unsigned)Q, R, w, c.x0, c.eps, tp,
                              at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
