@@ -2645,6 +2645,69 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   }
 }
 
+// T^T of a stride-1 convolution (kernel KK <= 3, Cs source channels) as a gather onto a window
+// of 8 destination channels, DW x DW positions, from a source window SW x SW: the 16 rows of a
+// block are the N dimension, and the 16 M lanes take the 8 channels at two neighbouring
+// positions (x0, x0 + 1) of a destination row, whose tap columns together span the four K
+// lanes of a step (source column x0 + 1 - G for lane group G: tap G - 1 for x0, tap G for
+// x0 + 1), so one MFMA serves both positions.  One K step per (source channel, tap row), the
+// source row uniform (steps without one are skipped); position pairs are dealt to the waves.
+// Each result is relaxed (Eq. 6) with pp = (a_lo, a_up, b_up, bias), pstr apart, written to
+// dst[c][p][row], and its intercept and bias terms are summed into the returned value.
+// Source and destination tiles: [channel][position][16 rows], channel strides SCS and DCS.
+template <int Cs, int KK, int SW, int DW, int NW>
+__device__ __forceinline__ float gather_pair8(const float* __restrict__ W, const float* src,
+                                              int SCS, float* dst, int DCS, const float* pp,
+                                              int pstr) {
+  static_assert(KK <= 3, "two positions' tap columns fit the four K lanes");
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int n = lane & 15, G = lane >> 4;
+  const int cm = n & 7, pm = n >> 3;  // A operand row: destination channel and position
+  const int kx = G - 1 + pm;
+  float areg[Cs * KK];
+#pragma unroll
+  for (int ks = 0; ks < Cs * KK; ++ks) {
+    const int c = ks / KK, ky = ks % KK;
+    areg[ks] = (kx >= 0 && kx < KK) ? W[((c * 8 + cm) * KK + ky) * KK + kx] : 0.f;
+  }
+  constexpr int NP = (DW + 1) / 2;  // position pairs per destination row
+  constexpr int ND = DW * DW;
+  float bpart = 0.f;
+  for (int pi = wave; pi < DW * NP; pi += NW) {
+    const int y = pi / NP, x0 = 2 * (pi - y * NP);
+    const int ix = x0 + 1 - G;
+    const bool xok = ix >= 0 && ix < SW;
+    const float* colp = src + (xok ? ix : 0) * 16 + n;
+    float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ky = 0; ky < KK; ++ky) {
+      const int iy = y - ky;
+      if (iy < 0 || iy >= SW) continue;  // uniform
+#pragma unroll
+      for (int c = 0; c < Cs; ++c) {
+        const float bv = xok ? colp[c * SCS + iy * SW * 16] : 0.f;
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[c * KK + ky], bv, d, 0, 0, 0);
+      }
+    }
+    // lane (n, G) holds rows n of channels 4 (G & 1) + r at position x0 + (G >> 1)
+    const int x = x0 + (G >> 1);
+    if (x < DW) {
+      const int p = y * DW + x;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = 4 * (G & 1) + r;
+        const int e = c * ND + p;
+        const float a = d[r];
+        const float ah = a >= 0.f ? a * pp[e] : a * pp[pstr + e];
+        bpart = fmaf(fminf(a, 0.f), pp[2 * pstr + e], bpart);
+        bpart = fmaf(ah, pp[3 * pstr + e], bpart);
+        dst[c * DCS + p * 16 + n] = ah;
+      }
+    }
+  }
+  return bpart;
+}
+
 // Pass 3 restricted to each row's receptive field, when T_3, T_2 (stride 1) and T_1 are
 // convolutions.  Row +-e_j of h^(3), j = (c3, y3, x3), carried through T_3 is +-W_3[c3] on the
 // K3 x K3 window of j on g^(2); after the layer-2 relaxation, T_2^T spreads it over a
@@ -2681,7 +2744,7 @@ __global__ void __launch_bounds__(512)
   __shared__ float p2s[4][E2];  // a_lo, a_up, b_up, bias of the g^(2) window
   __shared__ float p1s[4][E1];  // a_lo, a_up, b_up, W1 x0 + b1 of the g^(1) window
   __shared__ float rb2[RP * 16];  // bias terms of (2), per (part, row)
-  __shared__ float rb1[NW * 2 * 16];  // bias terms of (3), per (wave, lane group, row)
+  __shared__ float rb1[NW * 4 * 16];  // bias terms of (3), per (wave, lane group, row)
   __shared__ float rl1[NW * 16];  // ||A_x||_1 partials of (4)
 
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -2753,51 +2816,12 @@ __global__ void __launch_bounds__(512)
   }
   __syncthreads();
 
-  // (3) T_2^T: A over the g^(1) window, one position per wave at a time, relaxed into tile1.
-  // One K step per (c2, ky) with the tap column kx as the lane group: the source row of a step
-  // is uniform (steps with no source row are skipped) and a lane's source column is fixed for
-  // the whole position.
+  // (3) T_2^T: A over the g^(1) window, two positions per MFMA, relaxed into tile1
   {
-    static_assert(K2 <= 4, "tap columns are the four lane groups");
-    const int m = lane & 15;  // A operand row: channel c1 of g^(1)
-    float a2[C2 * K2];
-#pragma unroll
-    for (int ks = 0; ks < C2 * K2; ++ks) {
-      const int c2 = ks / K2, ky = ks % K2;
-      a2[ks] = (m < C1 && G < K2) ? t2.W[(((long)c2 * C1 + m) * K2 + ky) * K2 + G] : 0.f;
-    }
-    float bpart = 0.f;
-    for (int p = wave; p < N1; p += NW) {
-      const int y = p / W1W, x = p - y * W1W;
-      const int ix = x - G;  // g^(2) window column feeding (y, x) through tap column G
-      const bool xok = ix >= 0 && ix < K3;
-      const float* colp = tile2 + (xok ? ix : 0) * 16 + n;
-      float4v d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ky = 0; ky < K2; ++ky) {
-        const int iy = y - ky;
-        if (iy < 0 || iy >= K3) continue;  // uniform
-#pragma unroll
-        for (int c2 = 0; c2 < C2; ++c2) {
-          const float bv = xok ? colp[c2 * CS2 + iy * K3 * 16] : 0.f;
-          d = __builtin_amdgcn_mfma_f32_16x16x4f32(a2[c2 * K2 + ky], bv, d, 0, 0, 0);
-        }
-      }
-      if (G * 4 < C1) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int c1 = 4 * G + r;
-          const int e = c1 * N1 + p;
-          const float a = d[r];
-          const float ah = a >= 0.f ? a * p1s[0][e] : a * p1s[1][e];
-          bpart = fmaf(fminf(a, 0.f), p1s[2][e], bpart);
-          // layer-1 bias and the linear term of the concretisation together
-          bpart = fmaf(ah, p1s[3][e], bpart);
-          tile1[c1 * CS1 + p * 16 + n] = ah;
-        }
-      }
-    }
-    if (G < 2) rb1[(wave * 2 + G) * 16 + n] = bpart;
+    static_assert(C1 == 8, "the position-pair gather takes 8 channels");
+    const float bpart = gather_pair8<C2, K2, K3, W1W, NW>(t2.W, tile2, CS2, tile1, CS1,
+                                                          &p1s[0][0], E1);
+    rb1[(wave * 4 + G) * 16 + n] = bpart;
   }
   __syncthreads();
 
@@ -2873,7 +2897,7 @@ __global__ void __launch_bounds__(512)
   const P2Row pr = p2_row(C3, g, row);
   float tb = (pr.neg ? -1.f : 1.f) * t3.b[pr.c2];
   for (int q = 0; q < RP; ++q) tb += rb2[q * 16 + row];
-  for (int q = 0; q < NW * 2; ++q) tb += rb1[q * 16 + row];
+  for (int q = 0; q < NW * 4; ++q) tb += rb1[q * 16 + row];
   float ta = 0.f;
   for (int w = 0; w < NW; ++w) ta += rl1[w * 16 + row];
   const float v = tb - eps * ta;
@@ -2997,59 +3021,14 @@ __global__ void __launch_bounds__(512)
   }
   __syncthreads();
 
-  // (3) T^T gather from tile `src` (window width SW, channel stride SCS, CS channels) through the
-  // weights of `tt` (kernel KK, stride 1) into the next window (width DW, Cd channels), relaxed
-  // with the parameters pp (4 arrays, pstr apart) into `dst`; bias terms into
-  // rb[(wave * 4 + G) * 16 + n].  One K step per (source channel c, tap row ky) with the tap
-  // column as the lane group (source row uniform, steps without one skipped); the A operands sit
-  // in registers.
-  constexpr int NKSM = (C3 > C2 ? C3 : C2) * (K3 > K2 ? K3 : K2);
-  auto gather = [&](const DLayer& tt, const float* src, int SW, int SCS, int Cs, int KK,
-                    float* dst, int DW, int DCS, int Cd, const float* pp, int pstr, float* rb) {
-    const int m = lane & 15;  // A operand row: channel of the destination window
-    float areg[NKSM];
-#pragma unroll
-    for (int ks = 0; ks < NKSM; ++ks) {
-      const int c = ks / KK, ky = ks % KK;
-      areg[ks] = (c < Cs && m < Cd && G < KK)
-                     ? tt.W[(((long)c * Cd + m) * KK + ky) * KK + G] : 0.f;
-    }
-    float bpart = 0.f;
-    const int ND = DW * DW;
-    for (int p = wave; p < ND; p += NW) {
-      const int y = p / DW, x = p - y * DW;
-      const int ix = x - G;  // source window column feeding (y, x) through tap column G
-      const bool xok = ix >= 0 && ix < SW;
-      const float* colp = src + (xok ? ix : 0) * 16 + n;
-      float4v d = {0.f, 0.f, 0.f, 0.f};
-      for (int ky = 0; ky < KK; ++ky) {
-        const int iy = y - ky;
-        if (iy < 0 || iy >= SW) continue;  // uniform
-#pragma unroll
-        for (int c = 0; c < (C3 > C2 ? C3 : C2); ++c) {
-          if (c >= Cs) break;
-          const float bv = xok ? colp[c * SCS + iy * SW * 16] : 0.f;
-          d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[c * KK + ky], bv, d, 0, 0, 0);
-        }
-      }
-      if (G * 4 < Cd) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int c = 4 * G + r;
-          const int e = c * ND + p;
-          const float a = d[r];
-          const float ah = a >= 0.f ? a * pp[e] : a * pp[pstr + e];
-          bpart = fmaf(fminf(a, 0.f), pp[2 * pstr + e], bpart);
-          bpart = fmaf(ah, pp[3 * pstr + e], bpart);
-          dst[c * DCS + p * 16 + n] = ah;
-        }
-      }
-    }
-    rb[(wave * 4 + G) * 16 + n] = bpart;
-  };
-  gather(t3, tile3, K4, CS3, C3, K3, tile2, W2W, CS2, C2, &p2s[0][0], E2, rb2);
+  // (3) T_3^T, then T_2^T, as position-pair gathers (two destination positions per MFMA),
+  // each result relaxed into the next tile
+  static_assert(C2 == 8 && C1 == 8, "the position-pair gather takes 8 channels");
+  rb2[(wave * 4 + G) * 16 + n] =
+      gather_pair8<C3, K3, K4, W2W, NW>(t3.W, tile3, CS3, tile2, CS2, &p2s[0][0], E2);
   __syncthreads();
-  gather(t2, tile2, W2W, CS2, C2, K2, tile1, W1W, CS1, C1, &p1s[0][0], E1, rb1);
+  rb1[(wave * 4 + G) * 16 + n] =
+      gather_pair8<C2, K2, W2W, W1W, NW>(t2.W, tile2, CS2, tile1, CS1, &p1s[0][0], E1);
   __syncthreads();
 
   // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
