@@ -6425,10 +6425,15 @@ int optimize_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float 
     long na = c.nb * net->n_relu, ns = c.nb * S;
     float* a = alpha + b0 * net->n_relu;
     float* lbt = at<float>(ws, p.off_lbt);
+    // A fresh start bounds with the heuristic lower slopes u/(u-l) and sets alpha to them; the
+    // bound at t = 0 (alpha at those values, every layer's l and u recomputed from layer 1 up)
+    // then repeats that bound operation for operation.  So with steps to take, the heuristic
+    // bound records the tape and serves as the t = 0 iterate.
+    const bool t0_done = op.fresh && op.steps > 0;
     if (op.fresh) {
       Chunk h = c;
       h.alpha = nullptr;
-      h.tape = false;
+      h.tape = t0_done;
       if (int e = bound_chunk(h, C, lbt)) return e;
       if (int e = launch_k("alpha_init", stream, [&] {
             hipLaunchKernelGGL(k_alpha_init, grid_for(na), dim3(kBlock), 0, stream, na, h.L, h.U,
@@ -6439,7 +6444,8 @@ int optimize_run(lirpa_net* net, const Plan& p, long Bc, const float* x0, float 
     const int tbase = op.fresh ? 0 : op.t0;
     for (int t = 0; t <= op.steps; ++t) {
       c.tape = (t < op.steps);
-      if (int e = bound_chunk(c, C, lbt)) return e;
+      if (!(t == 0 && t0_done))
+        if (int e = bound_chunk(c, C, lbt)) return e;
       float* tr = lb_trace ? lb_trace + ((long)t * B + b0) * S : nullptr;
       if (int e = launch_k("best", stream, [&] {
             hipLaunchKernelGGL(k_best, grid_for(ns), dim3(kBlock), 0, stream, ns, lbt,
