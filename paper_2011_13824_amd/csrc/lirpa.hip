@@ -3115,6 +3115,22 @@ __global__ void __launch_bounds__(512)
     L[b * n_relu + off4 + j] = v;
 }
 
+// Sum of v over the 16 lanes of each row of the wave, by DPP (row rotations by 8 and 4, then the
+// quad permutations that swap lane pairs 2 and 1 apart): no LDS round trip.  Every lane ends
+// with its row's total, each in its own order of additions, so one fixed lane is read.
+__device__ __forceinline__ float row_sum16(float v) {
+  auto dpp = [](float x, auto ctrl) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                         0, __builtin_bit_cast(int, x), decltype(ctrl)::value,
+                                         0xF, 0xF, false));
+  };
+  v += dpp(v, std::integral_constant<int, 0x128>());  // row_ror:8
+  v += dpp(v, std::integral_constant<int, 0x124>());  // row_ror:4
+  v += dpp(v, std::integral_constant<int, 0x4E>());   // quad_perm(2,3,0,1): lane ^ 2
+  v += dpp(v, std::integral_constant<int, 0xB1>());   // quad_perm(1,0,3,2): lane ^ 1
+  return v;
+}
+
 // Reverse sweep of the receptive-field pass 2.  Layer-1 bounds do not depend on alpha, so the
 // rows of pass 2 only feed d J / d alpha of the layer-1 neurons of their own window:
 // sum over rows of w_r max(A~_r, 0) G_r, where A~_r = +-W_2[c2] is the row's coefficient before
@@ -3379,10 +3395,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
             const float4v pr = prm[e];
             cval = wn * pr[3] * tile[c1 * CS + pos * 16 + n] * fmaf(-eps, d[r], pr[2]);
           }
-          cval += __shfl_xor(cval, 8, 64);
-          cval += __shfl_xor(cval, 4, 64);
-          cval += __shfl_xor(cval, 2, 64);
-          cval += __shfl_xor(cval, 1, 64);
+          cval = row_sum16(cval);
           if (n == 0 && c1 < C1) out[c1 * NPOS + pos] = cval;
         }
       }
