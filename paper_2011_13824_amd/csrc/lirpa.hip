@@ -3951,9 +3951,10 @@ __global__ void __launch_bounds__(256)
       const float gv = d[mt][r] + t.b[o];
       const size_t idx = (size_t)o * ldq + q;
       G[idx] = gv;
-      if (zout) {
+      if (zout) {  // both lines, then a select (no branch around the loads)
         const long pi = b * pstride + o;
-        zout[idx] = tape[idx] >= 0.f ? a_lo[pi] * gv : fmaf(a_up[pi], gv, b_up[pi]);
+        const float zl = a_lo[pi] * gv, zu = fmaf(a_up[pi], gv, b_up[pi]);
+        zout[idx] = tape[idx] >= 0.f ? zl : zu;
       }
     }
 }
@@ -4137,15 +4138,22 @@ __global__ void __launch_bounds__(256, 2)
   constexpr int PPT = (NPE + 255) / 256, TPT = NTE / 256;
   static_assert(NTE % 256 == 0, "whole coefficient elements per thread");
   float4v pv[PPT], tv[TPT];
+  // this thread's relaxation array per element (a_lo, a_up or b_up), chosen once: a per-lane
+  // pointer select in the loop compiles to branches
+  const float* psrc[PPT];
+#pragma unroll
+  for (int k = 0; k < PPT; ++k) {
+    const int e = min(tid + k * 256, NPE - 1);
+    const int pr = e / (4 * C1) % 3;
+    psrc[k] = (pr == 0 ? a_lo : (pr == 1 ? a_up : b_up)) + (size_t)b * pstride;
+  }
   auto fetch_ep = [&](int ya) {
 #pragma unroll
     for (int k = 0; k < PPT; ++k) {
       const int e = min(tid + k * 256, NPE - 1);
-      const int c = e % C1, x4 = (e / C1) & 3, pr = e / (4 * C1) % 3, r2 = e / (4 * C1 * 3);
+      const int c = e % C1, x4 = (e / C1) & 3, r2 = e / (4 * C1 * 3);
       const int y1 = min(ya + r2, H1 - 1);
-      const float* src = pr == 0 ? a_lo : (pr == 1 ? a_up : b_up);
-      pv[k] = *reinterpret_cast<const float4v*>(src + (size_t)b * pstride +
-                                                (c * H1 + y1) * H1 + 4 * x4);
+      pv[k] = *reinterpret_cast<const float4v*>(psrc[k] + (c * H1 + y1) * H1 + 4 * x4);
     }
 #pragma unroll
     for (int k = 0; k < TPT; ++k) {
@@ -4201,7 +4209,10 @@ __global__ void __launch_bounds__(256, 2)
       ta[r] = (wq[r] * tp) * gv;
       tb[r] = (wq[r] * tn) * gv;
       tc[r] = wq[r] * tn;
-      z[r] = wq[r] == 0.f ? 0.f : (t >= 0.f ? lo * gv : fmaf(up, gv, bu));
+      // both lines computed and selected (no branch): the z_1 of a row without weight is 0
+      const float zl = lo * gv, zu = fmaf(up, gv, bu);
+      const float zs = t >= 0.f ? zl : zu;
+      z[r] = wq[r] != 0.f ? zs : 0.f;
     }
     if (n < C1)
       *reinterpret_cast<float4v*>(zr + zslot(y1) * ZROW + n * ZCS + (x1 + 1) * 8 + qb) = z;
@@ -4568,7 +4579,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
         const unsigned o = ((unsigned)co * HO + y) * WO + x;
         const size_t idx = (size_t)o * ldq + q;
         if (!part) G[idx] = gv;
-        if constexpr (ZOUT) zout[idx] = et[r] >= 0.f ? el[r] * gv : fmaf(eu[r], gv, eb[r]);
+        if constexpr (ZOUT) {  // both lines, then a select (no branch)
+          const float zl = el[r] * gv, zu = fmaf(eu[r], gv, eb[r]);
+          zout[idx] = et[r] >= 0.f ? zl : zu;
+        }
       }
     }
 #pragma unroll
