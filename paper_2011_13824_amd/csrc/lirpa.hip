@@ -2544,7 +2544,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       for (int k = 0; k < NEP; ++k) {
         // (no early exit: the loop unrolls, so the arrays are indexed statically)
         const int e = part + k * RPT;
-        if (e < NE) {
+        if (k + 1 < NEP || e < NE) {  // (only the last k can fall past NE)
           const float4v pr = prm[e];
           const float v = fmaf(wp[k], pr[0], wn[k] * pr[1]);
           bpart = fmaf(wn[k], pr[2], bpart);
@@ -3311,9 +3311,9 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
 #pragma unroll
     for (int k = 0; k < NEP; ++k) {
       const int e = partid + k * RPT;
-      if (e < NE) {
+      if (k + 1 < NEP || e < NE) {  // (only the last k can fall past NE)
         const float4v pr = prm[e];
-        tile[toff(k)] = wv[k] >= 0.f ? wv[k] * pr[0] : wv[k] * pr[1];
+        tile[toff(k)] = wv[k] * (wv[k] >= 0.f ? pr[0] : pr[1]);
       }
     }
     __syncthreads();
@@ -3368,7 +3368,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
 #pragma unroll
     for (int k = 0; k < NEP; ++k) {
       const int e = partid + k * RPT;
-      if (e < NE) tile[toff(k)] = fmaxf(wv[k], 0.f);
+      if (k + 1 < NEP || e < NE) tile[toff(k)] = fmaxf(wv[k], 0.f);
     }
     __syncthreads();
 
