@@ -152,7 +152,7 @@ def stage_work(layers, S, B):
     return work
 
 
-def grad_work(layers, S, B):
+def grad_work(layers, S, B, l2=None):
     """Algorithmic work per launch of the reverse-sweep kernel classes: {class: (flop, bytes)}.
 
     Pass P (rows Q = B*R) is swept from its witnesses forward.  The witness forward through
@@ -163,7 +163,14 @@ def grad_work(layers, S, B):
     The receptive-field pass 2 rebuilds each row's relaxed window and its A_x on MFMA and runs
     W_1 over the window's witness: twice the window flops of the bound pass; bytes: the layer-1
     relaxation read (3 floats per neuron and sub-domain) and one partial sum written per
-    (window, window neuron)."""
+    (window, window neuron).
+
+    The fused two-layer forward of pass 3 needs T_2 only at the layer-2 neurons that are
+    unstable (elsewhere the adjoint terms it feeds are not used); with 32 channels it computes
+    just those (in tiles of 16 channels per pair of positions).  l2 = (fraction of layer-2
+    neurons unstable, fraction of the dense T_2 tiles computed), from the batch's stability
+    codes: its algorithmic flops count T_2 at the unstable neurons only, and the executed MFMA
+    flops (the tiles computed) are returned under the key "executed"."""
     from paper_2011_13824_amd import workloads as wl
     L = len(layers)
     n = [wl.n_in(layers[0])] + [wl.n_out(t) for t in layers]
@@ -181,7 +188,9 @@ def grad_work(layers, S, B):
             t1, t2 = layers[0], layers[1]
             wmacs = t1["out_c"] * t2["k"] ** 2 * t1["in_c"] * t1["k"] ** 2
             parts = B * (t2["out_c"] // 8) * t2["out_h"] * t2["out_w"] * t1["out_c"] * t2["k"] ** 2
-            work["pass2_window_grad[layer1,pass2]"] = (4.0 * Q * wmacs,
+            # (only the rows of unstable layer-2 neurons carry weight, and only those are run)
+            f2 = l2[0] if l2 is not None else 1.0
+            work["pass2_window_grad[layer1,pass2]"] = (4.0 * Q * wmacs * f2,
                                                        4.0 * (3 * B * n[1] + parts))
             work["pass2_grad_gather[layer1,pass2]"] = (0.0, 4.0 * (parts + 3 * B * n[1]))
             continue
@@ -191,9 +200,14 @@ def grad_work(layers, S, B):
             # shapes the library covers): their flops; bytes: the signs of A_x (one byte per
             # input), the recorded coefficients over g^(1), the adjoint partial sums of both
             # layers (3 floats per neuron and group of 8 rows)
+            f2, tiles = (1.0, 1.0)
+            if layers[1]["out_c"] == 32 and l2 is not None:
+                f2, tiles = l2
             work[f"fwd12[layer1,pass{P}]"] = (
-                2.0 * Q * (macs(layers[0]) + macs(layers[1])),
+                2.0 * Q * (macs(layers[0]) + f2 * macs(layers[1])),
                 n[0] * Q + 4.0 * n[1] * Q + 12.0 * (n[1] + n[2]) * Q / 8)
+            work.setdefault("executed", {})[f"fwd12[layer1,pass{P}]"] = \
+                2.0 * Q * (macs(layers[0]) + tiles * macs(layers[1]))
         for m in range(1, P):
             t = layers[m - 1]
             inb = n[0] * Q if m == 1 else 4.0 * n[m - 1] * Q
@@ -201,6 +215,26 @@ def grad_work(layers, S, B):
             work[f"grad_gather[layer{m},pass{P}]"] = (0.0, 12.0 * n[m] * Q / 8 + 12.0 * B * n[m])
             work[f"grad_reduce[layer{m},pass{P}]"] = (0.0, 8.0 * n[m] * Q + 12.0 * B * n[m])
     return work
+
+
+def layer2_stats(net, x0, w, C, split, alpha):
+    """(fraction of layer-2 neurons unstable, fraction of the dense T_2 tiles the fused pass-3
+    forward computes) over the batch at the given slopes, or None when T_2 is not a
+    convolution.  The second is 1 unless T_2 has 32 channels on an 8x8 map: then a tile is 16
+    channels at a pair of positions (x, x + 1) of one row, and a pair takes ceil(n / 16)
+    tiles, at least one, for its n channels unstable at either position."""
+    t2 = w.layers[1]
+    if t2.get("kind") != 1:
+        return None
+    from paper_2011_13824_amd import workloads as wl
+    off2, n2 = wl.n_out(w.layers[0]), wl.n_out(t2)
+    _, code = net.bound(x0, w.eps, C, split=split, alpha=alpha, want_codes=True)
+    u = code[:, off2:off2 + n2].cpu().numpy() == 5
+    if t2["out_c"] != 32 or (t2["out_h"], t2["out_w"]) != (8, 8):
+        return float(u.mean()), 1.0
+    per_pair = u.reshape(-1, 32, 8, 4, 2).any(axis=4).sum(axis=1)  # [B, 8 rows, 4 pairs]
+    tiles = np.maximum(1, (per_pair + 15) // 16)
+    return float(u.mean()), float(tiles.mean() / 2.0)
 
 
 def traffic_record(workload, kernel):
@@ -354,8 +388,10 @@ def main():
     times = lirpa.lirpa_timing_end()
     torch.cuda.synchronize()
     work = stage_work(w.layers, S, B)
+    executed = {}
     if optimise:
-        work.update(grad_work(w.layers, S, B))
+        work.update(grad_work(w.layers, S, B, layer2_stats(net, x0, w, C, split, alpha)))
+        executed = work.pop("executed", {})
     stages = {}
     for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):
         f, b = work.get(cls, (0.0, 0.0))
@@ -365,6 +401,8 @@ def main():
                        "launches_per_step": launches / args.steps,
                        "tflops": round(f / sec / 1e12, 3) if f else None,
                        "gbs": round(b / sec / 1e9, 1) if b else None}
+        if cls in executed:
+            stages[cls]["executed_tflops"] = round(executed[cls] * launches / sec / 1e12, 3)
     dom = max(times, key=lambda c: times[c][0])
     tot_ms, launches = times[dom]
     f, b = work.get(dom, (0.0, 0.0))
@@ -379,6 +417,9 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["avg_launch_ms"] = round(tot_ms / launches, 4)
+    if dom in executed:
+        # the MFMA work the kernel actually issues (it skips T_2 where nothing uses it)
+        roof["executed_tflops"] = round(executed[dom] / (tot_ms / launches / 1e3) / 1e12, 3)
     roof["traffic"] = None if args.batch else traffic_record(w.name, dom)
 
     out = {

@@ -1737,8 +1737,9 @@ __global__ void __launch_bounds__(64 * (CI + NS + C0))
 // layer-1 bias).
 // TAPE (FC source, for the reverse sweep): the matrix waves also store each parked row over
 // g^(1), unrelaxed, to Sink::tape, and the x waves the sign of each entry of A_x to Sink::tsign,
-// both [entry][ldq] with the block's 16 rows contiguous (rows past Q included: they lie inside
-// the padded width ldq, and hold zeros).
+// both blocked by groups of 8 rows, [q / 8][entry][q % 8], so that the reverse sweep, which
+// takes 8 rows at a time, reads contiguous memory (rows past Q included: they lie inside the
+// padded width ldq, and hold zeros).
 template <int K, int S, int P, int H1, int W1, int H0, int W0, int CO, int CI, int CPW, int K1,
           int S1, int P1, int HX, int WX, int C0, int NXW, bool FC, int NBS, int SPEC = 0,
           bool TAPE = false>
@@ -1827,17 +1828,21 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
 #pragma unroll
       for (int x = 0; x < W0; ++x) dst[x * 16] = v[x];
       if constexpr (TAPE) {
-        // buffer stores: a block-uniform base (the channel's plane) and a 32-bit lane offset
+        // buffer stores: a block-uniform base (the channel's plane in the block's first group
+        // of 8 rows), the lane's row group, row and map row as the lane offset, the column as
+        // the scalar offset
         const int y = yrow(e, r);
         if (y >= 0 && y < H0) {
-          float* plane = s.tape + (size_t)(wave * CPW + c) * (H0 * W0) * ldq + q0;
-          const unsigned boff = ((unsigned)y * W0 * ldq + (unsigned)n) * 4u;
+          constexpr unsigned NG = CI * H0 * W0 * 8;  // floats of one group of 8 rows
+          float* plane = s.tape + (size_t)(q0 >> 3) * NG + (size_t)(wave * CPW + c) * (H0 * W0 * 8);
+          const unsigned boff =
+              ((unsigned)(n >> 3) * NG + (unsigned)(n & 7) + (unsigned)y * (W0 * 8)) * 4u;
 #pragma unroll
           for (int x = 0; x < W0; ++x) {
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc(plane, (short)0, 0x7fffffff, 0x00020000);
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[x]), rs, boff,
-                                                  (unsigned)x * ldq * 4u, 0);
+                                                  (unsigned)x * 32u, 0);
           }
         }
       }
@@ -2193,14 +2198,16 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
   bool pend_ok = false;
   int pend_y = 0;
   // TAPE: the sign of entry (c0, yx, g) of this lane's row
-  // (lane offset: the row yx and the lane's q; the uniform part, channel and column, goes in
-  // the scalar offset, so that no per-column address stays live in vector registers)
+  // (lane offset: the lane's row group and row and the row yx; the uniform part, channel and
+  // column, goes in the scalar offset, so that no per-column address stays live in vector
+  // registers)
   auto put_sign = [&](int c0, int yx, int g, float a) {
     if constexpr (TAPE) {
-      const __amdgpu_buffer_rsrc_t rs =
-          __builtin_amdgcn_make_buffer_rsrc(s.tsign + q0, (short)0, 0x7fffffff, 0x00020000);
-      const unsigned voff = (unsigned)(yx * WX) * ldq + (unsigned)n;
-      const unsigned soff = (unsigned)(c0 * HX * WX + g) * ldq;
+      constexpr unsigned NG = C0 * HX * WX * 8;  // bytes of one group of 8 rows
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          s.tsign + (size_t)(q0 >> 3) * NG, (short)0, 0x7fffffff, 0x00020000);
+      const unsigned voff = (unsigned)(n >> 3) * NG + (unsigned)(n & 7) + (unsigned)(yx * WX * 8);
+      const unsigned soff = (unsigned)(c0 * HX * WX + g) * 8u;
       __builtin_amdgcn_raw_buffer_store_b8((unsigned char)sign8(a), rs, voff, soff, 0);
     }
   };
@@ -3974,6 +3981,33 @@ __device__ __forceinline__ float sum8(float v) {
   return v;
 }
 
+// A copy of a k x k convolution's weights with the two tap indices exchanged,
+// Wt[co][ci][kx][ky] = W[co][ci][ky][kx], so that the taps of one column are contiguous.
+__global__ void __launch_bounds__(kBlock)
+    k_taps_swap(long n, int k, const float* __restrict__ W, float* __restrict__ Wt) {
+  const long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const long kk = (long)k * k, base = i / kk * kk;
+  const int ky = (int)(i % kk) / k, kx = (int)(i % k);
+  Wt[base + (long)kx * k + ky] = W[i];
+}
+
+// Position of the k-th set bit (k counted from 0) of m, for k < popcount(m): a binary search
+// over halves, quarters, ... of the word, by the popcount of each lower part (no branch).
+__device__ __forceinline__ int kth_bit(unsigned m, int k) {
+  int pos = 0;
+#pragma unroll
+  for (int w = 16; w >= 1; w >>= 1) {
+    const unsigned low = m & ((1u << w) - 1u);
+    const int c = __builtin_popcount(low);
+    const bool up = k >= c;
+    k = up ? k - c : k;
+    pos += up ? w : 0;
+    m = up ? m >> w : low;
+  }
+  return pos;
+}
+
 // Sum of v over the 8 rows of a position in k_fwd_conv12's layout: the lane's four rows are
 // summed in place, then with the four rows of the lane 16 away (v_permlane16_swap exchanges rows
 // 0 <-> 1 and 2 <-> 3 of 16 lanes; with the same value in both operands, the two results are
@@ -4004,7 +4038,10 @@ __device__ __forceinline__ float sum_rows8(const float4v& v) {
 // slots conv2 just finished with, from x* rows 4 y2 + 5 .. 4 y2 + 10 (ring of 6 slots, row
 // mod 6).  While conv2 runs, the block fetches with coalesced 16-byte loads what conv1 will
 // need -- the four new x* rows (signs and x0), and for its two rows the recorded coefficients
-// A~_1 and the layer-1 relaxation -- and parks them in LDS.  Rows outside a map are zero slots
+// A~_1 and the layer-1 relaxation -- and parks them in LDS.  The two tapes (the signs of A_x
+// and A~_1, both written by k_convT_fc_bound) are blocked by groups of 8 rows,
+// [q / 8][entry][q % 8], so the group's entries of a row are one contiguous run.  Rows outside
+// a map are zero slots
 // (the convolutions' zero padding).  Adjoint sums are written as k_fwd_conv writes them
 // ([group][term][position][channel]).  The LDS footprint lets two blocks share a CU, so one
 // block's barriers overlap the other's work.  No load carries a per-lane condition (such a
@@ -4017,7 +4054,9 @@ __global__ void __launch_bounds__(256, 2)
                  const float* __restrict__ tape1, const float* __restrict__ a_lo,
                  const float* __restrict__ a_up, const float* __restrict__ b_up,
                  unsigned pstride, const float* __restrict__ W3, unsigned nk, unsigned inter,
-                 float* __restrict__ part1, float* __restrict__ part2,
+                 const int8_t* __restrict__ code2, unsigned n_relu,
+                 const float* __restrict__ W2t, float* __restrict__ part1,
+                 float* __restrict__ part2,
                  unsigned char* __restrict__ gflag) {
   constexpr int C0 = 3, K = 4, S = 2, HX = 32, H1 = 16, H2 = 8;
   constexpr int N1 = C1 * H1 * H1, N2 = C2 * H2 * H2;
@@ -4032,6 +4071,11 @@ __global__ void __launch_bounds__(256, 2)
   constexpr int NMT2 = C2 / 16;          // channel tiles of T_2
   static_assert(C1 == 8 || C1 == 16, "T_1 output channels");
   static_assert(C2 == 16 || C2 == 32, "T_2 output channels");
+  // With 32 channels, conv2 runs only where its adjoint terms are used: at the layer-2 neurons
+  // that are unstable in the block's sub-domain.  Wave w takes position pair w of each row; the
+  // channels unstable at either position of the pair are packed into tiles of 16 (one tile for
+  // up to 16 such channels, two above), and lane n of a tile computes the n-th of them.
+  constexpr bool GATHER = C2 == 32;
   // conv1 epilogue operands of the two rows of an iteration: relaxation [row][a_lo, a_up, b_up]
   // [x1][channel] and coefficients [row][x1][channel][q]
   constexpr int EPP = 2 * 3 * H1 * C1, EPT = 2 * H1 * C1 * 8;
@@ -4072,17 +4116,58 @@ __global__ void __launch_bounds__(256, 2)
   const int mt2 = wave % NMT2;
 
   // B operands: lane (n, g) holds W[co = n][ci][ky][kx = g] per K step (ci, ky); the bias of
-  // this lane's output channel
+  // this lane's output channel.  (GATHER: the conv2 operands of the wave's next tile, loaded
+  // per tile.)
   float w1r[NKS1], w2r[NKS2];
 #pragma unroll
   for (int ks = 0; ks < NKS1; ++ks)
     w1r[ks] = n < C1 ? t1.W[((n * C0 + ks / K) * K + ks % K) * K + g] : 0.f;
+  if constexpr (!GATHER) {
 #pragma unroll
-  for (int ks = 0; ks < NKS2; ++ks)
-    w2r[ks] = t2.W[(((mt2 * 16 + n) * C1 + ks / K) * K + ks % K) * K + g];
+    for (int ks = 0; ks < NKS2; ++ks)
+      w2r[ks] = t2.W[(((mt2 * 16 + n) * C1 + ks / K) * K + ks % K) * K + g];
+  }
   const float b1 = n < C1 ? t1.b[n] : 0.f;
-  const int co2 = mt2 * 16 + n;
-  const float b2 = t2.b[co2];
+  int co2 = mt2 * 16 + n;
+  float b2 = GATHER ? 0.f : t2.b[co2];
+  // (GATHER: a lane past the tile's last channel repeats that channel, computes the same
+  // values and stores them to the same place)
+  // layer-2 stability codes of the sub-domain; the code of (channel lane & 31, position
+  // 2 wave + (lane >> 5)) of a row
+  const int8_t* cd2 = code2 + (size_t)b * n_relu + (lane & 31) * (H2 * H2) + 2 * wave + (lane >> 5);
+  // tile t of mask m (row y2): this lane's channel and bias, its conv2 operands and its
+  // coefficients over g^(2).  Lane group g = kx loads the four taps ky = 0..3 of tap column g of
+  // each input channel as one 16-byte quad of the tap-swapped weights, which are the operands
+  // of K steps (ci, ky) in registers 4 ci + ky.
+  float4v tw;
+  auto tile_load = [&](unsigned m, int t, int y2) {
+    const int cnt = __builtin_popcount(m);
+    const int k = n + 16 * t;
+    co2 = kth_bit(m, min(k, cnt - 1));
+    b2 = t2.b[co2];
+    const float4v* wp = reinterpret_cast<const float4v*>(W2t + (size_t)co2 * (C1 * K * K)) + g;
+#pragma unroll
+    for (int ci = 0; ci < C1; ++ci) {
+      const float4v v = wp[ci * K];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w2r[ci * K + j] = v[j];
+    }
+    const int o = (co2 * H2 + y2) * H2 + 2 * wave + pd;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) tw[r] = w3r[r][o];  // (times the row's sign where used)
+  };
+  // the unstable channels of the wave's pair in each row (wave-uniform masks, read once)
+  unsigned um[H2];
+  if constexpr (GATHER) {
+    int8_t cd[H2];
+#pragma unroll
+    for (int y = 0; y < H2; ++y) cd[y] = cd2[y * H2];
+#pragma unroll
+    for (int y = 0; y < H2; ++y) {
+      const unsigned long long m = __ballot(cd[y] == 5);
+      um[y] = (unsigned)m | (unsigned)(m >> 32);
+    }
+  }
 
   auto xslot = [](int yi) { return (yi + 6 * NX) % NX; };
   auto zslot = [](int y1) { return (y1 + 4 * NZ) % NZ; };
@@ -4112,7 +4197,8 @@ __global__ void __launch_bounds__(256, 2)
       const int h = e & 1, x = (e >> 1) % HX, ci = (e >> 1) / HX % C0;
       const int yc = min(max(yfirst + e / (2 * C0 * HX), 0), HX - 1);
       sw[k] = *reinterpret_cast<const int*>(
-          sgn + (size_t)((ci * HX + yc) * HX + x) * ldq + q0 + 4 * h);
+          sgn + (size_t)(q0 / 8) * (C0 * HX * HX * 8) + (size_t)((ci * HX + yc) * HX + x) * 8 +
+          4 * h);
       sx[k] = x0[(ci * HX + yc) * HX + x];
     }
   };
@@ -4161,7 +4247,7 @@ __global__ void __launch_bounds__(256, 2)
       const int h = e & 1, c = (e >> 1) % C1, x1 = (e >> 1) / C1 % H1, r2 = e / (2 * H1 * C1);
       const int y1 = min(ya + r2, H1 - 1);
       tv[k] = *reinterpret_cast<const float4v*>(
-          tape1 + (size_t)((c * H1 + y1) * H1 + x1) * ldq + q0 + 4 * h);
+          tape1 + (size_t)(q0 / 8) * (N1 * 8) + (size_t)((c * H1 + y1) * H1 + x1) * 8 + 4 * h);
     }
   };
   auto park_ep = [&]() {
@@ -4216,8 +4302,11 @@ __global__ void __launch_bounds__(256, 2)
     }
     if (n < C1)
       *reinterpret_cast<float4v*>(zr + zslot(y1) * ZROW + n * ZCS + (x1 + 1) * 8 + qb) = z;
+    // (lane groups g and g ^ 1 hold the same sums: with 16 channels every lane stores, the same
+    // value as its partner to the same place, so that no store is under a branch and later
+    // memory waits count exactly the operations before them)
     const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
-    if ((g & 1) == 0 && n < C1) {
+    if (C1 == 16 || ((g & 1) == 0 && n < C1)) {
       float* dst = part1 + (size_t)grp * 3 * N1 + (size_t)(y1 * H1 + x1) * C1 + n;
       dst[0] = sa;
       dst[N1] = da;
@@ -4275,6 +4364,7 @@ __global__ void __launch_bounds__(256, 2)
   };
 
   // prologue: z_1 row 0 (epilogue operands of rows 0, 1), then rows 1, 2
+  if constexpr (GATHER) tile_load(um[0], 0, 0);
   fetch_x(-1);
   fetch_ep(0);
   park_x(-1);
@@ -4299,11 +4389,41 @@ __global__ void __launch_bounds__(256, 2)
   for (int y2 = 0; y2 < H2; ++y2) {
     const int ya = 2 * y2 + 3, yb = 2 * y2 + 4;  // z_1 rows this iteration adds
     const bool more = ya < H1 + 1;               // (row 16 is the zero row)
-    float4v tw[P2W];
-    load_tw(y2, tw);
+    if constexpr (GATHER) {
+      unsigned umask = um[0];
 #pragma unroll
-    for (int k = 0; k < P2W; ++k) conv2_pos(y2, xp2(k), tw[k]);
+      for (int y = 1; y < H2; ++y) umask = y2 == y ? um[y] : umask;
+      // tile 0 always runs (with no unstable channel it computes channel 0, which no one
+      // reads), so that the code from here to the barrier has no branch around a memory
+      // operation and its memory waits count exactly the operations before them
+      auto tile = [&]() {
+        float4v tws;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) tws[r] = tsg[r] * tw[r];
+        conv2_pos(y2, wave, tws);
+      };
+      tile();
+      if (__builtin_popcount(umask) > 16) {
+        // (the tiles of a pair share their A operands: a compiler barrier keeps them read per
+        // tile rather than held in registers across the tiles)
+        asm volatile("" ::: "memory");
+        tile_load(umask, 1, y2);
+        tile();
+      }
+    } else {
+      float4v tw[P2W];
+      load_tw(y2, tw);
+#pragma unroll
+      for (int k = 0; k < P2W; ++k) conv2_pos(y2, xp2(k), tw[k]);
+    }
     if (!more) break;
+    if constexpr (GATHER) {
+      // the next row's first tile: its loads are in flight during this iteration's conv1
+      unsigned un = um[1];
+#pragma unroll
+      for (int y = 2; y < H2; ++y) un = y2 + 1 == y ? um[y] : un;
+      tile_load(un, 0, y2 + 1);
+    }
     park_x(4 * y2 + 7);
     park_ep();
     // the next iteration's operands: in flight during this iteration's conv1 and the next conv2
@@ -5069,6 +5189,7 @@ struct Plan {
   // 8 rows (whether any row of the group carries weight)
   size_t off_gpart = 0, off_gflag = 0;
   size_t off_gpart2 = 0;  // layer-2 partial sums of the fused two-layer witness forward
+  size_t off_w2t = 0;     // its copy of T_2's weights with the tap indices exchanged
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -5141,7 +5262,8 @@ bool pass_on_chip(const lirpa_net* net, int k, long Bc);
 using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
                              const float*, const float*, float, const float*, const float*,
                              const float*, const float*, unsigned, const float*, unsigned,
-                             unsigned, float*, float*, unsigned char*);
+                             unsigned, const int8_t*, unsigned, const float*, float*, float*,
+                             unsigned char*);
 Fwd12Kernel fwd12_for(const lirpa_net* net) {
   if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
   const lirpa_layer &a = net->T[0], &t = net->T[1];
@@ -5247,6 +5369,9 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
       // pass 3's layer-2 partial sums, written by the same kernel as its layer-1 sums
       p.off_gpart2 = o;
       o = align256(o + (size_t)(round_up(Bc * 2 * net->n[3], 64) / 8) * 3 * net->n[2] * 4);
+      const lirpa_layer& t2 = net->T[1];
+      p.off_w2t = o;
+      o = align256(o + (size_t)t2.out_c * t2.in_c * t2.k * t2.k * 4);
     }
   }
   p.total = o;
@@ -5790,10 +5915,6 @@ FcBoundKernel fc_bound_for(const lirpa_net* net, int k, int* nwaves, bool tape =
 // k_fwd_conv12, which reads the two tapes that kernel writes.
 bool fused_tape_pass(const Chunk& c, int k, long R) {
   int nw = 0;
-  // the kernel's tape stores take 32-bit byte offsets within a channel plane of g^(1) and
-  // within the sign tape
-  const double ldq = (double)round_up(c.nb * R, 64);
-  if (4.0 * 256 * ldq >= 2147483647.0 || 3072.0 * ldq >= 2147483647.0) return false;
   return c.tape && k == 3 && R % 8 == 0 && fc_open_ok(c, k, R) && c.p->off_gpart &&
          c.p->off_gpart2 && fwd12_for(c.net) && fc_bound_for(c.net, k, &nw, true);
 }
@@ -6154,6 +6275,14 @@ int grad_chunk(const Chunk& c, int full) {
         float* part1 = at<float>(c.ws, p.off_gpart);
         float* part2 = at<float>(c.ws, p.off_gpart2);
         unsigned char* gflag = at<unsigned char>(c.ws, p.off_gflag);
+        // T_2's weights with the tap indices exchanged (the kernel's per-tile operand loads)
+        float* w2t = at<float>(c.ws, p.off_w2t);
+        const long nw2 = (long)t2.out_c * t2.in_c * t2.k * t2.k;
+        if (int e = launch_k(tag("taps_swap", 2, P), c.st, [&] {
+              hipLaunchKernelGGL(k_taps_swap, grid_for(nw2), dim3(kBlock), 0, c.st, nw2, t2.k,
+                                 t2.W, w2t);
+            }))
+          return e;
         const unsigned nblk8 = (unsigned)round_up((Q + 7) / 8, 8);
         if (int e = launch_k(tag("fwd12", 1, P), c.st, [&] {
               hipLaunchKernelGGL(fk, dim3(nblk8), dim3(256), 0, c.st, dlayer(t1), dlayer(t2),
@@ -6163,7 +6292,8 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_aup) + net->poff[1],
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
                                  (unsigned)net->pstride, net->T[2].W, (unsigned)net->n[3],
-                                 (unsigned)inter, part1, part2, gflag);
+                                 (unsigned)inter, at<int8_t>(c.ws, p.off_code) + net->off[2],
+                                 (unsigned)net->n_relu, w2t, part1, part2, gflag);
             }))
           return e;
         for (int m = 1; m <= 2; ++m) {
