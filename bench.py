@@ -220,9 +220,10 @@ def grad_work(layers, S, B, l2=None):
 def layer2_stats(net, x0, w, C, split, alpha):
     """(fraction of layer-2 neurons unstable, fraction of the dense T_2 tiles the fused pass-3
     forward computes) over the batch at the given slopes, or None when T_2 is not a
-    convolution.  The second is 1 unless T_2 has 32 channels on an 8x8 map: then a tile is 16
-    channels at a pair of positions (x, x + 1) of one row, and a pair takes ceil(n / 16)
-    tiles, at least one, for its n channels unstable at either position."""
+    convolution.  The second is 1 unless T_2 has 32 channels on an 8x8 map: then a row's 8
+    positions are paired by their number of unstable channels (most with fewest, ties by
+    position), a tile is 16 channels at a pair, and a pair takes ceil(n / 16) tiles, at least
+    one, for its n channels unstable at either position."""
     t2 = w.layers[1]
     if t2.get("kind") != 1:
         return None
@@ -232,7 +233,12 @@ def layer2_stats(net, x0, w, C, split, alpha):
     u = code[:, off2:off2 + n2].cpu().numpy() == 5
     if t2["out_c"] != 32 or (t2["out_h"], t2["out_w"]) != (8, 8):
         return float(u.mean()), 1.0
-    per_pair = u.reshape(-1, 32, 8, 4, 2).any(axis=4).sum(axis=1)  # [B, 8 rows, 4 pairs]
+    u = u.reshape(-1, 32, 8, 8).transpose(0, 2, 3, 1)  # [B, row, position, channel]
+    key = u.sum(axis=3) * 8 + np.arange(8)  # unique per position
+    order = np.argsort(key, axis=2)  # positions by rank
+    lo = np.take_along_axis(u, order[:, :, :4, None], axis=2)
+    hi = np.take_along_axis(u, order[:, :, ::-1][:, :, :4, None], axis=2)
+    per_pair = (lo | hi).sum(axis=3)  # [B, row, pair]
     tiles = np.maximum(1, (per_pair + 15) // 16)
     return float(u.mean()), float(tiles.mean() / 2.0)
 

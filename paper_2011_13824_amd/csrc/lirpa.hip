@@ -3992,6 +3992,18 @@ __global__ void __launch_bounds__(kBlock)
   Wt[base + (long)kx * k + ky] = W[i];
 }
 
+// A copy of a Linear layer's weights over a C x HW input with the input index reordered
+// channel-last: Wc[j][p C + c] = W[j][c HW + p], so that the entries of one input position
+// over all channels are contiguous.
+__global__ void __launch_bounds__(kBlock)
+    k_fc_chlast(long n, int C, int HW, const float* __restrict__ W, float* __restrict__ Wc) {
+  const long i = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const long nin = (long)C * HW, j = i / nin;
+  const int k = (int)(i % nin), c = k / HW, pos = k % HW;
+  Wc[j * nin + (long)pos * C + c] = W[i];
+}
+
 // Position of the k-th set bit (k counted from 0) of m, for k < popcount(m): a binary search
 // over halves, quarters, ... of the word, by the popcount of each lower part (no branch).
 __device__ __forceinline__ int kth_bit(unsigned m, int k) {
@@ -4072,9 +4084,12 @@ __global__ void __launch_bounds__(256, 2)
   static_assert(C1 == 8 || C1 == 16, "T_1 output channels");
   static_assert(C2 == 16 || C2 == 32, "T_2 output channels");
   // With 32 channels, conv2 runs only where its adjoint terms are used: at the layer-2 neurons
-  // that are unstable in the block's sub-domain.  Wave w takes position pair w of each row; the
-  // channels unstable at either position of the pair are packed into tiles of 16 (one tile for
-  // up to 16 such channels, two above), and lane n of a tile computes the n-th of them.
+  // that are unstable in the block's sub-domain.  The 8 positions of a row are paired, the one
+  // with the most unstable channels with the one with the fewest and so on (so that a pair
+  // rarely has more than 16), and wave w takes pair w; the channels unstable at either position
+  // of its pair are packed into tiles of 16 (one tile for up to 16 such channels, two above),
+  // and lane n of a tile computes the n-th of them.  W3 is then the channel-last copy of W_3
+  // (k_fc_chlast), whose entries of one position are contiguous.
   constexpr bool GATHER = C2 == 32;
   // conv1 epilogue operands of the two rows of an iteration: relaxation [row][a_lo, a_up, b_up]
   // [x1][channel] and coefficients [row][x1][channel][q]
@@ -4132,15 +4147,12 @@ __global__ void __launch_bounds__(256, 2)
   float b2 = GATHER ? 0.f : t2.b[co2];
   // (GATHER: a lane past the tile's last channel repeats that channel, computes the same
   // values and stores them to the same place)
-  // layer-2 stability codes of the sub-domain; the code of (channel lane & 31, position
-  // 2 wave + (lane >> 5)) of a row
-  const int8_t* cd2 = code2 + (size_t)b * n_relu + (lane & 31) * (H2 * H2) + 2 * wave + (lane >> 5);
   // tile t of mask m (row y2): this lane's channel and bias, its conv2 operands and its
   // coefficients over g^(2).  Lane group g = kx loads the four taps ky = 0..3 of tap column g of
   // each input channel as one 16-byte quad of the tap-swapped weights, which are the operands
   // of K steps (ci, ky) in registers 4 ci + ky.
   float4v tw;
-  auto tile_load = [&](unsigned m, int t, int y2) {
+  auto tile_load = [&](unsigned m, int t, int y2, int xa, int xb) {
     const int cnt = __builtin_popcount(m);
     const int k = n + 16 * t;
     co2 = kth_bit(m, min(k, cnt - 1));
@@ -4152,20 +4164,52 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
       for (int j = 0; j < 4; ++j) w2r[ci * K + j] = v[j];
     }
-    const int o = (co2 * H2 + y2) * H2 + 2 * wave + pd;
+    const int o = (y2 * H2 + (pd ? xb : xa)) * C2 + co2;
 #pragma unroll
     for (int r = 0; r < 4; ++r) tw[r] = w3r[r][o];  // (times the row's sign where used)
   };
-  // the unstable channels of the wave's pair in each row (wave-uniform masks, read once)
-  unsigned um[H2];
+  // each row's pair of positions (xa | xb << 3) for this wave and the channels unstable at
+  // either of them (wave-uniform, from the sub-domain's layer-2 stability codes, read once:
+  // lane c and c + 32 read channel c of two rows, one byte per position), kept in LDS
+  __shared__ unsigned gsel[GATHER ? 4 : 1][H2][2];
   if constexpr (GATHER) {
-    int8_t cd[H2];
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int8_t* cc = code2 + (size_t)b * n_relu + (lane & 31) * (H2 * H2) + (lane >> 5) * H2;
+    int8_t cd[H2 / 2][H2];
 #pragma unroll
-    for (int y = 0; y < H2; ++y) cd[y] = cd2[y * H2];
+    for (int yy = 0; yy < H2 / 2; ++yy)
 #pragma unroll
-    for (int y = 0; y < H2; ++y) {
-      const unsigned long long m = __ballot(cd[y] == 5);
-      um[y] = (unsigned)m | (unsigned)(m >> 32);
+      for (int x = 0; x < H2; ++x) cd[yy][x] = cc[2 * yy * H2 + x];
+#pragma unroll
+    for (int yy = 0; yy < H2 / 2; ++yy) {
+      unsigned m[2][H2];
+#pragma unroll
+      for (int x = 0; x < H2; ++x) {
+        const unsigned long long bm = __ballot(cd[yy][x] == 5);
+        m[0][x] = (unsigned)bm;
+        m[1][x] = (unsigned)(bm >> 32);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // rank of each position by (count, position); this wave's pair: ranks wv and 7 - wv
+        int key[H2];
+#pragma unroll
+        for (int x = 0; x < H2; ++x) key[x] = __builtin_popcount(m[h][x]) * H2 + x;
+        int xa = 0, xb = 0;
+        unsigned ma = 0u, mb = 0u;
+#pragma unroll
+        for (int x = 0; x < H2; ++x) {
+          int rk = 0;
+#pragma unroll
+          for (int x2 = 0; x2 < H2; ++x2) rk += key[x2] < key[x] ? 1 : 0;
+          xa = rk == wv ? x : xa;
+          ma = rk == wv ? m[h][x] : ma;
+          xb = rk == H2 - 1 - wv ? x : xb;
+          mb = rk == H2 - 1 - wv ? m[h][x] : mb;
+        }
+        gsel[wave][2 * yy + h][0] = ma | mb;
+        gsel[wave][2 * yy + h][1] = (unsigned)xa | ((unsigned)xb << 3);
+      }
     }
   }
 
@@ -4335,11 +4379,12 @@ __global__ void __launch_bounds__(256, 2)
       for (int r = 0; r < 4; ++r) tw[k][r] = tsg[r] * w3r[r][o];
     }
   };
-  auto conv2_pos = [&](int y2, int xp, const float4v& tw) {
+  // a T_2 position pair (xa, xb) of row y2 (A operand rows 0..7 at xa, 8..15 at xb)
+  auto conv2_pos = [&](int y2, int xa, int xb, const float4v& tw) {
     const float* zb[K];
 #pragma unroll
     for (int ky = 0; ky < K; ++ky)
-      zb[ky] = zr + zslot(2 * y2 - 1 + ky) * ZROW + (2 * (2 * xp + pp) + g) * 8 + qr;
+      zb[ky] = zr + zslot(2 * y2 - 1 + ky) * ZROW + (2 * (pp ? xb : xa) + g) * 8 + qr;
     float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < NKS2; ++ks)
@@ -4355,7 +4400,7 @@ __global__ void __launch_bounds__(256, 2)
     }
     const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
     if ((g & 1) == 0) {
-      const int x2 = 2 * xp + pd;
+      const int x2 = pd ? xb : xa;
       float* dst = part2 + (size_t)grp * 3 * N2 + (size_t)(y2 * H2 + x2) * C2 + co2;
       dst[0] = sa;
       dst[N2] = da;
@@ -4364,7 +4409,11 @@ __global__ void __launch_bounds__(256, 2)
   };
 
   // prologue: z_1 row 0 (epilogue operands of rows 0, 1), then rows 1, 2
-  if constexpr (GATHER) tile_load(um[0], 0, 0);
+  if constexpr (GATHER) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane(gsel[wave][0][0]);
+    const unsigned s0 = __builtin_amdgcn_readfirstlane(gsel[wave][0][1]);
+    tile_load(m0, 0, 0, s0 & 7, s0 >> 3);
+  }
   fetch_x(-1);
   fetch_ep(0);
   park_x(-1);
@@ -4390,9 +4439,9 @@ __global__ void __launch_bounds__(256, 2)
     const int ya = 2 * y2 + 3, yb = 2 * y2 + 4;  // z_1 rows this iteration adds
     const bool more = ya < H1 + 1;               // (row 16 is the zero row)
     if constexpr (GATHER) {
-      unsigned umask = um[0];
-#pragma unroll
-      for (int y = 1; y < H2; ++y) umask = y2 == y ? um[y] : umask;
+      const unsigned umask = __builtin_amdgcn_readfirstlane(gsel[wave][y2][0]);
+      const unsigned sel = __builtin_amdgcn_readfirstlane(gsel[wave][y2][1]);
+      const int xa = sel & 7, xb = sel >> 3;
       // tile 0 always runs (with no unstable channel it computes channel 0, which no one
       // reads), so that the code from here to the barrier has no branch around a memory
       // operation and its memory waits count exactly the operations before them
@@ -4400,29 +4449,28 @@ __global__ void __launch_bounds__(256, 2)
         float4v tws;
 #pragma unroll
         for (int r = 0; r < 4; ++r) tws[r] = tsg[r] * tw[r];
-        conv2_pos(y2, wave, tws);
+        conv2_pos(y2, xa, xb, tws);
       };
       tile();
       if (__builtin_popcount(umask) > 16) {
         // (the tiles of a pair share their A operands: a compiler barrier keeps them read per
         // tile rather than held in registers across the tiles)
         asm volatile("" ::: "memory");
-        tile_load(umask, 1, y2);
+        tile_load(umask, 1, y2, xa, xb);
         tile();
       }
     } else {
       float4v tw[P2W];
       load_tw(y2, tw);
 #pragma unroll
-      for (int k = 0; k < P2W; ++k) conv2_pos(y2, xp2(k), tw[k]);
+      for (int k = 0; k < P2W; ++k) conv2_pos(y2, 2 * xp2(k), 2 * xp2(k) + 1, tw[k]);
     }
     if (!more) break;
     if constexpr (GATHER) {
       // the next row's first tile: its loads are in flight during this iteration's conv1
-      unsigned un = um[1];
-#pragma unroll
-      for (int y = 2; y < H2; ++y) un = y2 + 1 == y ? um[y] : un;
-      tile_load(un, 0, y2 + 1);
+      const unsigned un = __builtin_amdgcn_readfirstlane(gsel[wave][y2 + 1][0]);
+      const unsigned sn = __builtin_amdgcn_readfirstlane(gsel[wave][y2 + 1][1]);
+      tile_load(un, 0, y2 + 1, sn & 7, sn >> 3);
     }
     park_x(4 * y2 + 7);
     park_ep();
@@ -5190,6 +5238,7 @@ struct Plan {
   size_t off_gpart = 0, off_gflag = 0;
   size_t off_gpart2 = 0;  // layer-2 partial sums of the fused two-layer witness forward
   size_t off_w2t = 0;     // its copy of T_2's weights with the tap indices exchanged
+  size_t off_w3c = 0;     // and of T_3's weights with the input index channel-last
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -5372,6 +5421,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
       const lirpa_layer& t2 = net->T[1];
       p.off_w2t = o;
       o = align256(o + (size_t)t2.out_c * t2.in_c * t2.k * t2.k * 4);
+      p.off_w3c = o;
+      o = align256(o + (size_t)net->T[2].out_c * net->T[2].in_c * 4);
     }
   }
   p.total = o;
@@ -6283,6 +6334,19 @@ int grad_chunk(const Chunk& c, int full) {
                                  t2.W, w2t);
             }))
           return e;
+        // with 32 channels the kernel reads T_3's weights channel-last
+        const float* w3 = net->T[2].W;
+        if (t2.out_c == 32) {
+          float* w3c = at<float>(c.ws, p.off_w3c);
+          const lirpa_layer& t3 = net->T[2];
+          const long nw3 = (long)t3.out_c * t3.in_c;
+          if (int e = launch_k(tag("fc_chlast", 3, P), c.st, [&] {
+                hipLaunchKernelGGL(k_fc_chlast, grid_for(nw3), dim3(kBlock), 0, c.st, nw3,
+                                   t2.out_c, t2.out_h * t2.out_w, t3.W, w3c);
+              }))
+            return e;
+          w3 = w3c;
+        }
         const unsigned nblk8 = (unsigned)round_up((Q + 7) / 8, 8);
         if (int e = launch_k(tag("fwd12", 1, P), c.st, [&] {
               hipLaunchKernelGGL(fk, dim3(nblk8), dim3(256), 0, c.st, dlayer(t1), dlayer(t2),
@@ -6291,7 +6355,7 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_alo) + net->poff[1],
                                  at<float>(c.ws, p.off_aup) + net->poff[1],
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
-                                 (unsigned)net->pstride, net->T[2].W, (unsigned)net->n[3],
+                                 (unsigned)net->pstride, w3, (unsigned)net->n[3],
                                  (unsigned)inter, at<int8_t>(c.ws, p.off_code) + net->off[2],
                                  (unsigned)net->n_relu, w2t, part1, part2, gflag);
             }))
