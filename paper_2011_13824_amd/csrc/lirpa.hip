@@ -4168,6 +4168,22 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
     for (int r = 0; r < 4; ++r) tw[r] = w3r[r][o];  // (times the row's sign where used)
   };
+  // the tile after the current one: its channel, bias and coefficients now, its conv2 operands
+  // (from the returned quads) one input channel at a time during the current tile's MFMAs, into
+  // the registers those MFMAs have just read, so that the loads overlap the MFMA chain
+  int co2n = 0;
+  float b2n = 0.f;
+  float4v twn;
+  auto next_setup = [&](unsigned m, int t, int y2, int xa, int xb) {
+    const int cnt = __builtin_popcount(m);
+    const int k = n + 16 * t;
+    co2n = kth_bit(m, min(k, cnt - 1));
+    b2n = t2.b[co2n];
+    const int o = (y2 * H2 + (pd ? xb : xa)) * C2 + co2n;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) twn[r] = w3r[r][o];
+    return reinterpret_cast<const float4v*>(W2t + (size_t)co2n * (C1 * K * K)) + g;
+  };
   // each row's pair of positions (xa | xb << 3) for this wave and the channels unstable at
   // either of them (wave-uniform, from the sub-domain's layer-2 stability codes, read once:
   // lane c and c + 32 read channel c of two rows, one byte per position), kept in LDS
@@ -4380,15 +4396,27 @@ __global__ void __launch_bounds__(256, 2)
     }
   };
   // a T_2 position pair (xa, xb) of row y2 (A operand rows 0..7 at xa, 8..15 at xb)
-  auto conv2_pos = [&](int y2, int xa, int xb, const float4v& tw) {
+  // (GATHER: wpn, the next tile's operand quads, loaded into w2r as its entries are used)
+  auto conv2_pos = [&](int y2, int xa, int xb, const float4v& tw, const float4v* wpn) {
     const float* zb[K];
 #pragma unroll
     for (int ky = 0; ky < K; ++ky)
       zb[ky] = zr + zslot(2 * y2 - 1 + ky) * ZROW + (2 * (pp ? xb : xa) + g) * 8 + qr;
     float4v d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < NKS2; ++ks)
-      d = __builtin_amdgcn_mfma_f32_16x16x4f32(zb[ks % K][(ks / K) * ZCS], w2r[ks], d, 0, 0, 0);
+    for (int ci = 0; ci < C1; ++ci) {
+#pragma unroll
+      for (int ky = 0; ky < K; ++ky)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(zb[ky][ci * ZCS], w2r[ci * K + ky], d, 0, 0, 0);
+      if constexpr (GATHER) {
+        const float4v v = wpn[ci * K];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w2r[ci * K + j] = v[j];
+        // (keep each load behind the four MFMAs that free its registers, not bunched at the end)
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+    }
     float4v ta, tb, tc;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -4445,33 +4473,37 @@ __global__ void __launch_bounds__(256, 2)
       // tile 0 always runs (with no unstable channel it computes channel 0, which no one
       // reads), so that the code from here to the barrier has no branch around a memory
       // operation and its memory waits count exactly the operations before them
-      auto tile = [&]() {
+      const bool two = __builtin_popcount(umask) > 16;
+      const int yn = min(y2 + 1, H2 - 1);  // (the last row fetches its own first tile again)
+      const unsigned un = __builtin_amdgcn_readfirstlane(gsel[wave][yn][0]);
+      const unsigned sn = __builtin_amdgcn_readfirstlane(gsel[wave][yn][1]);
+      auto tile = [&](const float4v* wpn) {
         float4v tws;
 #pragma unroll
         for (int r = 0; r < 4; ++r) tws[r] = tsg[r] * tw[r];
-        conv2_pos(y2, xa, xb, tws);
+        conv2_pos(y2, xa, xb, tws, wpn);
+        co2 = co2n;
+        b2 = b2n;
+        tw = twn;
       };
-      tile();
-      if (__builtin_popcount(umask) > 16) {
+      {
+        // the tile after this one: the row's second, else the next row's first
+        const unsigned mn = two ? umask : un, snx = two ? sel : sn;
+        tile(next_setup(mn, two ? 1 : 0, two ? y2 : yn, snx & 7, snx >> 3));
+      }
+      if (two) {
         // (the tiles of a pair share their A operands: a compiler barrier keeps them read per
         // tile rather than held in registers across the tiles)
         asm volatile("" ::: "memory");
-        tile_load(umask, 1, y2, xa, xb);
-        tile();
+        tile(next_setup(un, 0, yn, sn & 7, sn >> 3));
       }
     } else {
       float4v tw[P2W];
       load_tw(y2, tw);
 #pragma unroll
-      for (int k = 0; k < P2W; ++k) conv2_pos(y2, 2 * xp2(k), 2 * xp2(k) + 1, tw[k]);
+      for (int k = 0; k < P2W; ++k) conv2_pos(y2, 2 * xp2(k), 2 * xp2(k) + 1, tw[k], nullptr);
     }
     if (!more) break;
-    if constexpr (GATHER) {
-      // the next row's first tile: its loads are in flight during this iteration's conv1
-      const unsigned un = __builtin_amdgcn_readfirstlane(gsel[wave][y2 + 1][0]);
-      const unsigned sn = __builtin_amdgcn_readfirstlane(gsel[wave][y2 + 1][1]);
-      tile_load(un, 0, y2 + 1, sn & 7, sn >> 3);
-    }
     park_x(4 * y2 + 7);
     park_ep();
     // the next iteration's operands: in flight during this iteration's conv1 and the next conv2
