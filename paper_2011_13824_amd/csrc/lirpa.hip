@@ -3151,15 +3151,17 @@ __device__ __forceinline__ float row_sum16(float v) {
 // sub-domain; per window it rebuilds the relaxed patch and A_x over the footprint on MFMA,
 // keeps delta in LDS, runs the layer-1 forward over the window on MFMA, reduces the 16 rows'
 // contributions per window neuron and writes them to part[window][c1][pos] (windows numbered
-// (b, slot, y2, x2)).  A window without live rows writes zeros.  Row weights: w = g_l (sign +)
-// or -g_u (sign -) of the row's layer-2 neuron.
+// (b, slot, y2, x2)).  pflag[window] says whether the window has a live row; a window without
+// writes nothing else, and a block whose windows have none stops after numbering them.  Row
+// weights: w = g_l (sign +) or -g_u (sign -) of the row's layer-2 neuron.
 template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 3 : 4, 8)))
     k_pass2_window_grad(DLayer t1, DLayer t2, const float* __restrict__ a_lo,
                         const float* __restrict__ a_up, long pstride, float eps,
                         const float* __restrict__ gl, const float* __restrict__ gu,
                         const int8_t* __restrict__ code1, long n_relu, long off2,
-                        const float* __restrict__ z1, float* __restrict__ part) {
+                        const float* __restrict__ z1, float* __restrict__ part,
+                        unsigned char* __restrict__ pflag) {
   static_assert(C1 % 4 == 0 && C1 <= 16 && K1 == 4, "unsupported geometry");
   constexpr int KS = C1 / 4;
   constexpr int NT = 64 * NW;
@@ -3221,6 +3223,21 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
       wrow[xi][lane] = 0.f;
       rid[xi][lane] = 0;
     }
+  }
+  __syncthreads();  // wrow, rid
+  {
+    bool any = false;
+#pragma unroll
+    for (int xi = 0; xi < XW; ++xi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) any |= wrow[xi][r] != 0.f;
+    if (threadIdx.x < XW) {
+      bool live = false;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) live |= wrow[threadIdx.x][r] != 0.f;
+      pflag[win0 + threadIdx.x] = live ? 1 : 0;
+    }
+    if (!any) return;  // uniform: no window of the block has a live row
   }
 
   // this thread's entries of W_2 for the tile fills (row = tid mod 16, entries part,
@@ -3292,7 +3309,6 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
     }
   };
   pfetch(x2c * XW * t2.stride - t2.pad);
-  __syncthreads();  // wrow
 
   for (int xi = 0; xi < XW; ++xi) {
     const int x2 = x2c * XW + xi;
@@ -3301,8 +3317,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
     bool active = false;
 #pragma unroll
     for (int r = 0; r < 16; ++r) active |= wrow[xi][r] != 0.f;
-    if (!active) {  // uniform: no row of this window carries weight
-      for (int e = threadIdx.x; e < NE; e += NT) out[e] = 0.f;
+    if (!active) {  // uniform: no row of this window carries weight (its flag says so)
       if (xi + 1 < XW) pfetch(X1 + t2.stride);
       continue;
     }
@@ -3415,6 +3430,7 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
 // covers the neuron, in a fixed order.
 __global__ void __launch_bounds__(kBlock)
     k_pass2_grad_gather(long nb, DLayer t1, DLayer t2, int NPOS, const float* __restrict__ part,
+                        const unsigned char* __restrict__ pflag,
                         const int8_t* __restrict__ code1, long n_relu,
                         float* __restrict__ ga1) {
   long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
@@ -3427,22 +3443,25 @@ __global__ void __launch_bounds__(kBlock)
   const int H2 = t2.out_h, W2 = t2.out_w, K2 = t2.k, S2 = t2.stride, P2 = t2.pad;
   const int NG = p2_groups(t2.out_c);
   const int C1 = t1.out_c;
+  // the windows covering (y1, x1): taps ky2 = (y1 + P2) mod S2, + S2, ... (the same for x);
+  // the order (g, ky2, kx2) is fixed by the neuron alone
+  const int ry = (y1 + P2) % S2, rx = (x1 + P2) % S2;
   float acc = 0.f;
   for (int g = 0; g < NG; ++g)
-      for (int ky2 = 0; ky2 < K2; ++ky2) {
-        const int yn = y1 + P2 - ky2;
-        if (yn < 0 || yn % S2) continue;
-        const int y2 = yn / S2;
-        if (y2 >= H2) continue;
-        for (int kx2 = 0; kx2 < K2; ++kx2) {
-          const int xn = x1 + P2 - kx2;
-          if (xn < 0 || xn % S2) continue;
-          const int x2 = xn / S2;
-          if (x2 >= W2) continue;
-          const long blk = ((b * NG + g) * H2 + y2) * W2 + x2;
-          acc += part[(blk * C1 + c1) * NPOS + ky2 * K2 + kx2];
-        }
+    for (int ky2 = ry; ky2 < K2; ky2 += S2) {
+      const int yn = y1 + P2 - ky2;
+      if (yn < 0) break;  // (yn falls as ky2 grows)
+      const int y2 = yn / S2;
+      if (y2 >= H2) continue;
+      for (int kx2 = rx; kx2 < K2; kx2 += S2) {
+        const int xn = x1 + P2 - kx2;
+        if (xn < 0) break;
+        const int x2 = xn / S2;
+        if (x2 >= W2) continue;
+        const long blk = ((b * NG + g) * H2 + y2) * W2 + x2;
+        if (pflag[blk]) acc += part[(blk * C1 + c1) * NPOS + ky2 * K2 + kx2];
       }
+    }
   ga1[b * n_relu + ni] += acc;
 }
 
@@ -5264,7 +5283,7 @@ struct Plan {
   size_t off_tape[kMaxLayers + 1][kMaxLayers + 1] = {};
   size_t off_wT[kMaxLayers + 1] = {};  // transposed FC weights of layers 2..L-1 (0 = none)
   size_t off_ga = 0, off_gl = 0, off_gu = 0, off_w = 0, off_za = 0, off_zb = 0, off_G = 0;
-  size_t off_lbt = 0, off_grad = 0, off_p2part = 0;
+  size_t off_lbt = 0, off_grad = 0, off_p2part = 0, off_p2flag = 0;
   // adjoint partial sums of the fused witness forward, [Qp/8][3][n_m], and a flag per group of
   // 8 rows (whether any row of the group carries weight)
   size_t off_gpart = 0, off_gflag = 0;
@@ -5310,7 +5329,7 @@ Pass2Kernel pass2_kernel_for(const lirpa_net* net, int* nw) {
 
 using Pass2GradKernel = void (*)(DLayer, DLayer, const float*, const float*, long, float,
                                  const float*, const float*, const int8_t*, long, long,
-                                 const float*, float*);
+                                 const float*, float*, unsigned char*);
 Pass2GradKernel pass2_grad_kernel_for(const lirpa_net* net) {
   int nw = 0;
   if (!pass2_kernel_for(net, &nw)) return nullptr;
@@ -5419,6 +5438,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
         const int k2 = t2.k;
         p.off_p2part = o;
         o = align256(o + (size_t)pass2_blocks(net, Bc) * net->T[0].out_c * k2 * k2 * 4);
+        p.off_p2flag = o;  // one byte per window: has a live row
+        o = align256(o + (size_t)pass2_blocks(net, Bc));
         continue;
       }
       for (int m = 0; m <= k - 1; ++m) {
@@ -6324,19 +6345,21 @@ int grad_chunk(const Chunk& c, int full) {
         const lirpa_layer &t1 = net->T[0], &t2 = net->T[1];
         long blocks = pass2_blocks(net, c.nb) / p2_xw(net);  // windows / windows per block
         float* part = at<float>(c.ws, p.off_p2part);
+        unsigned char* pflag = at<unsigned char>(c.ws, p.off_p2flag);
         const int8_t* code = at<int8_t>(c.ws, p.off_code);
         int e = launch_k(tag("pass2_window_grad", 1, 2), c.st, [&] {
           hipLaunchKernelGGL(gk, dim3((unsigned)blocks), dim3(64 * t1.in_c), 0, c.st, dlayer(t1),
                              dlayer(t2), at<float>(c.ws, p.off_alo) + net->poff[1],
                              at<float>(c.ws, p.off_aup) + net->poff[1], net->pstride, c.eps, gl,
-                             gu, code, net->n_relu, net->off[2], at<float>(c.ws, p.off_z1), part);
+                             gu, code, net->n_relu, net->off[2], at<float>(c.ws, p.off_z1), part,
+                             pflag);
         });
         if (e) return e;
         long n1 = net->n[1];
         e = launch_k(tag("pass2_grad_gather", 1, 2), c.st, [&] {
           hipLaunchKernelGGL(k_pass2_grad_gather, grid_for(c.nb * n1), dim3(kBlock), 0, c.st,
-                             c.nb, dlayer(t1), dlayer(t2), t2.k * t2.k, part, code, net->n_relu,
-                             ga);
+                             c.nb, dlayer(t1), dlayer(t2), t2.k * t2.k, part, pflag, code,
+                             net->n_relu, ga);
         });
         if (e) return e;
         continue;
