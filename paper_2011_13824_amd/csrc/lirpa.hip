@@ -4074,7 +4074,8 @@ __device__ __forceinline__ float sum_rows8(const float4v& v) {
 // [q / 8][entry][q % 8], so the group's entries of a row are one contiguous run.  Rows outside
 // a map are zero slots
 // (the convolutions' zero padding).  Adjoint sums are written as k_fwd_conv writes them
-// ([group][term][position][channel]).  The LDS footprint lets two blocks share a CU, so one
+// ([group][term][position][channel]); with 32 channels on T_2 the layer-1 sums go only to the
+// unstable neurons, by their rank in the sub-domain ([group][rank][term], k_grad_gather_c).  The LDS footprint lets two blocks share a CU, so one
 // block's barriers overlap the other's work.  No load carries a per-lane condition (such a
 // value makes the wave wait for it at once): out-of-map rows and rows past Q read clamped,
 // in-bounds entries that are zeroed or meet a zero weight where they are used.
@@ -4086,7 +4087,8 @@ __global__ void __launch_bounds__(256, 2)
                  const float* __restrict__ a_up, const float* __restrict__ b_up,
                  unsigned pstride, const float* __restrict__ W3, unsigned nk, unsigned inter,
                  const int8_t* __restrict__ code2, unsigned n_relu,
-                 const float* __restrict__ W2t, float* __restrict__ part1,
+                 const int* __restrict__ kidx1, const float* __restrict__ W2t,
+                 float* __restrict__ part1,
                  float* __restrict__ part2,
                  unsigned char* __restrict__ gflag) {
   constexpr int C0 = 3, K = 4, S = 2, HX = 32, H1 = 16, H2 = 8;
@@ -4112,10 +4114,14 @@ __global__ void __launch_bounds__(256, 2)
   constexpr bool GATHER = C2 == 32;
   // conv1 epilogue operands of the two rows of an iteration: relaxation [row][a_lo, a_up, b_up]
   // [x1][channel] and coefficients [row][x1][channel][q]
+  // (GATHER: a fourth, the neuron's rank among the sub-domain's unstable layer-1 neurons, or -1,
+  // staged as 16 bits in ep_k, so that two blocks still share a CU)
+  constexpr int NPR = GATHER ? 4 : 3;
   constexpr int EPP = 2 * 3 * H1 * C1, EPT = 2 * H1 * C1 * 8;
   __shared__ __attribute__((aligned(16))) float xr[NX * XROW];
   __shared__ __attribute__((aligned(16))) float zr[NZ * ZROW];
   __shared__ float ep_p[EPP];
+  __shared__ short ep_k[GATHER ? 2 * H1 * C1 : 1];
   __shared__ __attribute__((aligned(16))) float ep_t[EPT];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -4299,7 +4305,7 @@ __global__ void __launch_bounds__(256, 2)
   // relaxation element e = (row, param, quad of x1, channel), coefficient element
   // e = (row, x1, channel, half of the 8 rows q), each one 16-byte load; consecutive threads
   // take consecutive channels, so that their LDS stores fall on distinct banks
-  constexpr int NPE = 2 * 3 * 4 * C1, NTE = 2 * H1 * C1 * 2;
+  constexpr int NPE = 2 * NPR * 4 * C1, NTE = 2 * H1 * C1 * 2;
   constexpr int PPT = (NPE + 255) / 256, TPT = NTE / 256;
   static_assert(NTE % 256 == 0, "whole coefficient elements per thread");
   float4v pv[PPT], tv[TPT];
@@ -4309,14 +4315,15 @@ __global__ void __launch_bounds__(256, 2)
 #pragma unroll
   for (int k = 0; k < PPT; ++k) {
     const int e = min(tid + k * 256, NPE - 1);
-    const int pr = e / (4 * C1) % 3;
-    psrc[k] = (pr == 0 ? a_lo : (pr == 1 ? a_up : b_up)) + (size_t)b * pstride;
+    const int pr = e / (4 * C1) % NPR;
+    psrc[k] = pr == 3 ? reinterpret_cast<const float*>(kidx1) + (size_t)b * N1
+                      : (pr == 0 ? a_lo : (pr == 1 ? a_up : b_up)) + (size_t)b * pstride;
   }
   auto fetch_ep = [&](int ya) {
 #pragma unroll
     for (int k = 0; k < PPT; ++k) {
       const int e = min(tid + k * 256, NPE - 1);
-      const int c = e % C1, x4 = (e / C1) & 3, r2 = e / (4 * C1 * 3);
+      const int c = e % C1, x4 = (e / C1) & 3, r2 = e / (4 * C1 * NPR);
       const int y1 = min(ya + r2, H1 - 1);
       pv[k] = *reinterpret_cast<const float4v*>(psrc[k] + (c * H1 + y1) * H1 + 4 * x4);
     }
@@ -4334,9 +4341,16 @@ __global__ void __launch_bounds__(256, 2)
     for (int k = 0; k < PPT; ++k) {
       const int e = tid + k * 256;
       if (NPE % 256 == 0 || e < NPE) {
-        const int c = e % C1, x4 = (e / C1) & 3, pr = e / (4 * C1) % 3, r2 = e / (4 * C1 * 3);
+        const int c = e % C1, x4 = (e / C1) & 3, pr = e / (4 * C1) % NPR,
+                  r2 = e / (4 * C1 * NPR);
+        if (GATHER && pr == 3) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ep_p[((r2 * 3 + pr) * H1 + 4 * x4 + i) * C1 + c] = pv[k][i];
+          for (int i = 0; i < 4; ++i)
+            ep_k[(r2 * H1 + 4 * x4 + i) * C1 + c] = (short)__float_as_int(pv[k][i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ep_p[((r2 * 3 + pr) * H1 + 4 * x4 + i) * C1 + c] = pv[k][i];
+        }
       }
     }
 #pragma unroll
@@ -4381,11 +4395,18 @@ __global__ void __launch_bounds__(256, 2)
     }
     if (n < C1)
       *reinterpret_cast<float4v*>(zr + zslot(y1) * ZROW + n * ZCS + (x1 + 1) * 8 + qb) = z;
-    // (lane groups g and g ^ 1 hold the same sums: with 16 channels every lane stores, the same
-    // value as its partner to the same place, so that no store is under a branch and later
-    // memory waits count exactly the operations before them)
     const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
-    if (C1 == 16 || ((g & 1) == 0 && n < C1)) {
+    if constexpr (GATHER) {
+      // only the unstable neurons' sums are used: at the neuron's rank in the sub-domain,
+      // [group][rank][3] (k_grad_gather_c)
+      const int kr = ep_k[(r2 * H1 + x1) * C1 + c];
+      if ((g & 1) == 0 && kr >= 0) {
+        float* dst = part1 + ((size_t)grp * N1 + kr) * 3;
+        dst[0] = sa;
+        dst[1] = da;
+        dst[2] = db;
+      }
+    } else if ((g & 1) == 0 && n < C1) {
       float* dst = part1 + (size_t)grp * 3 * N1 + (size_t)(y1 * H1 + x1) * C1 + n;
       dst[0] = sa;
       dst[N1] = da;
@@ -4537,6 +4558,69 @@ __global__ void __launch_bounds__(256, 2)
   }
 }
 
+// The unstable neurons of a layer, numbered per sub-domain in neuron order: kidx[b][j] = the
+// rank of neuron j among the sub-domain's unstable neurons (-1 if it is not unstable),
+// list[b][k] = the neuron of rank k, cnt[b] = their number.  One block per sub-domain.
+__global__ void __launch_bounds__(256)
+    k_unstable_index(int n, const int8_t* __restrict__ code, long n_relu, int* __restrict__ kidx,
+                     int* __restrict__ list, int* __restrict__ cnt) {
+  __shared__ int wsum[4];
+  const long b = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int base = 0;
+  for (int j0 = 0; j0 < n; j0 += 256) {
+    const int j = j0 + threadIdx.x;
+    const bool un = j < n && code[b * n_relu + j] == 5;
+    const unsigned long long m = __ballot(un);
+    const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int off = base;
+    for (int w = 0; w < wave; ++w) off += wsum[w];
+    const int k = off + below;
+    if (j < n) kidx[b * n + j] = un ? k : -1;
+    if (un) list[b * n + k] = j;
+    base += wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();  // wsum is rewritten by the next chunk
+  }
+  if (threadIdx.x == 0) cnt[b] = base;
+}
+
+// k_grad_gather over compacted partial sums: part[(b (R / 8) + k8) n_m + k][3] holds the sums of
+// the unstable neuron of rank k (k_unstable_index) for group k8 of sub-domain b.  A block per
+// sub-domain, a thread per rank: the same sums in the same group order as k_grad_gather, from
+// contiguous memory.
+__global__ void __launch_bounds__(kBlock)
+    k_grad_gather_c(long nm, long R, const float* __restrict__ part,
+                    const unsigned char* __restrict__ gflag, const int* __restrict__ list,
+                    const int* __restrict__ cnt, const float* __restrict__ l,
+                    const float* __restrict__ u, long n_relu, float* __restrict__ ga,
+                    float* __restrict__ gl, float* __restrict__ gu) {
+  const long b = blockIdx.x;
+  const int nk = cnt[b];
+  const long ng = R / 8, g0 = b * ng;
+  for (int k = threadIdx.x; k < nk; k += blockDim.x) {
+    const long p = b * n_relu + list[b * nm + k];
+    // (flags as in k_grad_gather)
+    float sa = 0.f, da = 0.f, db = 0.f;
+    const float* src = part + (g0 * nm + k) * 3;
+#pragma unroll 5
+    for (long k8 = 0; k8 < ng; ++k8) {
+      const bool on = gflag[g0 + k8] != 0;
+      const float* e = src + k8 * nm * 3;
+      const float a0 = e[0], a1 = e[1], a2 = e[2];
+      sa += on ? a0 : 0.f;
+      da += on ? a1 : 0.f;
+      db += on ? a2 : 0.f;
+    }
+    const float lj = l[p], uj = u[p], dd = uj - lj, d2 = dd * dd;
+    ga[p] += sa;
+    gl[p] += (da * uj - db * uj * uj) / d2;
+    gu[p] += (-da * lj + db * lj * lj) / d2;
+  }
+}
+
 // Adjoint accumulation for ReLU layer m from the partial sums of the fused witness forward: for
 // each (sub-domain, neuron), the R/8 groups of 8 rows of the sub-domain in increasing order (an
 // order fixed by the rows alone, so the result does not depend on where the sub-domain sits in
@@ -4557,13 +4641,18 @@ __global__ void __launch_bounds__(kBlock)
   const long p = b * n_relu + j;
   if (code[p] != 5) return;
   const long g0 = b * (R / 8), ng = R / 8;
+  // every group's entries are loaded (in bounds, possibly stale where the group had no weight)
+  // and a group without weight adds nothing: no load waits for a flag, so the loads of several
+  // groups are in flight together
   float sa = 0.f, da = 0.f, db = 0.f;
+#pragma unroll 5
   for (long k = 0; k < ng; ++k) {
-    if (!gflag[g0 + k]) continue;
+    const bool on = gflag[g0 + k] != 0;
     const float* src = part + (g0 + k) * 3 * nm + oc;
-    sa += src[0];
-    da += src[nm];
-    db += src[2 * nm];
+    const float a0 = src[0], a1 = src[nm], a2 = src[2 * nm];
+    sa += on ? a0 : 0.f;
+    da += on ? a1 : 0.f;
+    db += on ? a2 : 0.f;
   }
   const float lj = l[p], uj = u[p], dd = uj - lj, d2 = dd * dd;
   ga[p] += sa;
@@ -5290,6 +5379,7 @@ struct Plan {
   size_t off_gpart2 = 0;  // layer-2 partial sums of the fused two-layer witness forward
   size_t off_w2t = 0;     // its copy of T_2's weights with the tap indices exchanged
   size_t off_w3c = 0;     // and of T_3's weights with the input index channel-last
+  size_t off_kidx1 = 0, off_list1 = 0, off_cnt1 = 0;  // its unstable layer-1 neurons' ranks
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -5362,8 +5452,8 @@ bool pass_on_chip(const lirpa_net* net, int k, long Bc);
 using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
                              const float*, const float*, float, const float*, const float*,
                              const float*, const float*, unsigned, const float*, unsigned,
-                             unsigned, const int8_t*, unsigned, const float*, float*, float*,
-                             unsigned char*);
+                             unsigned, const int8_t*, unsigned, const int*, const float*,
+                             float*, float*, unsigned char*);
 Fwd12Kernel fwd12_for(const lirpa_net* net) {
   if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
   const lirpa_layer &a = net->T[0], &t = net->T[1];
@@ -5476,6 +5566,12 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
       o = align256(o + (size_t)t2.out_c * t2.in_c * t2.k * t2.k * 4);
       p.off_w3c = o;
       o = align256(o + (size_t)net->T[2].out_c * net->T[2].in_c * 4);
+      p.off_kidx1 = o;
+      o = align256(o + (size_t)Bc * net->n[1] * 4);
+      p.off_list1 = o;
+      o = align256(o + (size_t)Bc * net->n[1] * 4);
+      p.off_cnt1 = o;
+      o = align256(o + (size_t)Bc * 4);
     }
   }
   p.total = o;
@@ -6389,9 +6485,19 @@ int grad_chunk(const Chunk& c, int full) {
                                  t2.W, w2t);
             }))
           return e;
-        // with 32 channels the kernel reads T_3's weights channel-last
+        // with 32 channels the kernel reads T_3's weights channel-last, and writes its layer-1
+        // sums for the unstable neurons only, at their ranks
         const float* w3 = net->T[2].W;
+        int* kidx1 = at<int>(c.ws, p.off_kidx1);
+        int* list1 = at<int>(c.ws, p.off_list1);
+        int* cnt1 = at<int>(c.ws, p.off_cnt1);
         if (t2.out_c == 32) {
+          if (int e = launch_k(tag("unstable_index", 1, P), c.st, [&] {
+                hipLaunchKernelGGL(k_unstable_index, dim3((unsigned)c.nb), dim3(256), 0, c.st,
+                                   (int)net->n[1], at<int8_t>(c.ws, p.off_code) + net->off[1],
+                                   net->n_relu, kidx1, list1, cnt1);
+              }))
+            return e;
           float* w3c = at<float>(c.ws, p.off_w3c);
           const lirpa_layer& t3 = net->T[2];
           const long nw3 = (long)t3.out_c * t3.in_c;
@@ -6412,18 +6518,24 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
                                  (unsigned)net->pstride, w3, (unsigned)net->n[3],
                                  (unsigned)inter, at<int8_t>(c.ws, p.off_code) + net->off[2],
-                                 (unsigned)net->n_relu, w2t, part1, part2, gflag);
+                                 (unsigned)net->n_relu, kidx1, w2t, part1, part2, gflag);
             }))
           return e;
         for (int m = 1; m <= 2; ++m) {
           const lirpa_layer& t = net->T[m - 1];
           const long off = net->off[m];
           if (int e = launch_k(tag("grad_gather", m, P), c.st, [&] {
-                hipLaunchKernelGGL(k_grad_gather, grid_for(c.nb * net->n[m]), dim3(kBlock), 0,
-                                   c.st, c.nb, t.out_c, t.out_h * t.out_w, R,
-                                   m == 1 ? part1 : part2, gflag,
-                                   at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
-                                   net->n_relu, ga + off, gl + off, gu + off);
+                if (m == 1 && t2.out_c == 32)
+                  hipLaunchKernelGGL(k_grad_gather_c, dim3((unsigned)c.nb), dim3(kBlock), 0,
+                                     c.st, net->n[1], R, part1, gflag, list1, cnt1,
+                                     c.L + off, c.U + off, net->n_relu, ga + off, gl + off,
+                                     gu + off);
+                else
+                  hipLaunchKernelGGL(k_grad_gather, grid_for(c.nb * net->n[m]), dim3(kBlock),
+                                     0, c.st, c.nb, t.out_c, t.out_h * t.out_w, R,
+                                     m == 1 ? part1 : part2, gflag,
+                                     at<int8_t>(c.ws, p.off_code) + off, c.L + off, c.U + off,
+                                     net->n_relu, ga + off, gl + off, gu + off);
               }))
             return e;
         }
