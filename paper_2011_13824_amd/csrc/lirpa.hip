@@ -4074,8 +4074,8 @@ __device__ __forceinline__ float sum_rows8(const float4v& v) {
 // [q / 8][entry][q % 8], so the group's entries of a row are one contiguous run.  Rows outside
 // a map are zero slots
 // (the convolutions' zero padding).  Adjoint sums are written as k_fwd_conv writes them
-// ([group][term][position][channel]); with 32 channels on T_2 the layer-1 sums go only to the
-// unstable neurons, by their rank in the sub-domain ([group][rank][term], k_grad_gather_c).  The LDS footprint lets two blocks share a CU, so one
+// ([group][term][position][channel]); with 32 channels on T_2 the sums of both layers go only to
+// the unstable neurons, by their rank in the sub-domain ([group][rank][term], k_grad_gather_c).  The LDS footprint lets two blocks share a CU, so one
 // block's barriers overlap the other's work.  No load carries a per-lane condition (such a
 // value makes the wave wait for it at once): out-of-map rows and rows past Q read clamped,
 // in-bounds entries that are zeroed or meet a zero weight where they are used.
@@ -4087,7 +4087,8 @@ __global__ void __launch_bounds__(256, 2)
                  const float* __restrict__ a_up, const float* __restrict__ b_up,
                  unsigned pstride, const float* __restrict__ W3, unsigned nk, unsigned inter,
                  const int8_t* __restrict__ code2, unsigned n_relu,
-                 const int* __restrict__ kidx1, const float* __restrict__ W2t,
+                 const int* __restrict__ kidx1, const int* __restrict__ kidx2,
+                 const float* __restrict__ W2t,
                  float* __restrict__ part1,
                  float* __restrict__ part2,
                  unsigned char* __restrict__ gflag) {
@@ -4177,6 +4178,8 @@ __global__ void __launch_bounds__(256, 2)
   // each input channel as one 16-byte quad of the tap-swapped weights, which are the operands
   // of K steps (ci, ky) in registers 4 ci + ky.
   float4v tw;
+  // (k2: the rank of the lane's layer-2 neuron among the sub-domain's unstable ones, or -1)
+  int k2 = -1, k2n = -1;
   auto tile_load = [&](unsigned m, int t, int y2, int xa, int xb) {
     const int cnt = __builtin_popcount(m);
     const int k = n + 16 * t;
@@ -4192,6 +4195,7 @@ __global__ void __launch_bounds__(256, 2)
     const int o = (y2 * H2 + (pd ? xb : xa)) * C2 + co2;
 #pragma unroll
     for (int r = 0; r < 4; ++r) tw[r] = w3r[r][o];  // (times the row's sign where used)
+    k2 = kidx2[(size_t)b * N2 + (co2 * H2 + y2) * H2 + (pd ? xb : xa)];
   };
   // the tile after the current one: its channel, bias and coefficients now, its conv2 operands
   // (from the returned quads) one input channel at a time during the current tile's MFMAs, into
@@ -4207,6 +4211,7 @@ __global__ void __launch_bounds__(256, 2)
     const int o = (y2 * H2 + (pd ? xb : xa)) * C2 + co2n;
 #pragma unroll
     for (int r = 0; r < 4; ++r) twn[r] = w3r[r][o];
+    k2n = kidx2[(size_t)b * N2 + (co2n * H2 + y2) * H2 + (pd ? xb : xa)];
     return reinterpret_cast<const float4v*>(W2t + (size_t)co2n * (C1 * K * K)) + g;
   };
   // each row's pair of positions (xa | xb << 3) for this wave and the channels unstable at
@@ -4467,7 +4472,15 @@ __global__ void __launch_bounds__(256, 2)
       tc[r] = wq[r] * tn;
     }
     const float sa = sum_rows8(ta), da = sum_rows8(tb), db = sum_rows8(tc);
-    if ((g & 1) == 0) {
+    if constexpr (GATHER) {
+      // the unstable neurons' sums at their ranks, [group][rank][3], as the layer-1 sums
+      if ((g & 1) == 0 && k2 >= 0) {
+        float* dst = part2 + ((size_t)grp * N2 + k2) * 3;
+        dst[0] = sa;
+        dst[1] = da;
+        dst[2] = db;
+      }
+    } else if ((g & 1) == 0) {
       const int x2 = pd ? xb : xa;
       float* dst = part2 + (size_t)grp * 3 * N2 + (size_t)(y2 * H2 + x2) * C2 + co2;
       dst[0] = sa;
@@ -4525,6 +4538,7 @@ __global__ void __launch_bounds__(256, 2)
         co2 = co2n;
         b2 = b2n;
         tw = twn;
+        k2 = k2n;
       };
       {
         // the tile after this one: the row's second, else the next row's first
@@ -5380,6 +5394,7 @@ struct Plan {
   size_t off_w2t = 0;     // its copy of T_2's weights with the tap indices exchanged
   size_t off_w3c = 0;     // and of T_3's weights with the input index channel-last
   size_t off_kidx1 = 0, off_list1 = 0, off_cnt1 = 0;  // its unstable layer-1 neurons' ranks
+  size_t off_kidx2 = 0, off_list2 = 0, off_cnt2 = 0;  // and layer-2 neurons'
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -5452,8 +5467,8 @@ bool pass_on_chip(const lirpa_net* net, int k, long Bc);
 using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
                              const float*, const float*, float, const float*, const float*,
                              const float*, const float*, unsigned, const float*, unsigned,
-                             unsigned, const int8_t*, unsigned, const int*, const float*,
-                             float*, float*, unsigned char*);
+                             unsigned, const int8_t*, unsigned, const int*, const int*,
+                             const float*, float*, float*, unsigned char*);
 Fwd12Kernel fwd12_for(const lirpa_net* net) {
   if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
   const lirpa_layer &a = net->T[0], &t = net->T[1];
@@ -5571,6 +5586,12 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
       p.off_list1 = o;
       o = align256(o + (size_t)Bc * net->n[1] * 4);
       p.off_cnt1 = o;
+      o = align256(o + (size_t)Bc * 4);
+      p.off_kidx2 = o;
+      o = align256(o + (size_t)Bc * net->n[2] * 4);
+      p.off_list2 = o;
+      o = align256(o + (size_t)Bc * net->n[2] * 4);
+      p.off_cnt2 = o;
       o = align256(o + (size_t)Bc * 4);
     }
   }
@@ -6491,13 +6512,18 @@ int grad_chunk(const Chunk& c, int full) {
         int* kidx1 = at<int>(c.ws, p.off_kidx1);
         int* list1 = at<int>(c.ws, p.off_list1);
         int* cnt1 = at<int>(c.ws, p.off_cnt1);
+        int* kidx2 = at<int>(c.ws, p.off_kidx2);
+        int* list2 = at<int>(c.ws, p.off_list2);
+        int* cnt2 = at<int>(c.ws, p.off_cnt2);
         if (t2.out_c == 32) {
-          if (int e = launch_k(tag("unstable_index", 1, P), c.st, [&] {
-                hipLaunchKernelGGL(k_unstable_index, dim3((unsigned)c.nb), dim3(256), 0, c.st,
-                                   (int)net->n[1], at<int8_t>(c.ws, p.off_code) + net->off[1],
-                                   net->n_relu, kidx1, list1, cnt1);
-              }))
-            return e;
+          for (int m = 1; m <= 2; ++m)
+            if (int e = launch_k(tag("unstable_index", m, P), c.st, [&] {
+                  hipLaunchKernelGGL(k_unstable_index, dim3((unsigned)c.nb), dim3(256), 0, c.st,
+                                     (int)net->n[m], at<int8_t>(c.ws, p.off_code) + net->off[m],
+                                     net->n_relu, m == 1 ? kidx1 : kidx2, m == 1 ? list1 : list2,
+                                     m == 1 ? cnt1 : cnt2);
+                }))
+              return e;
           float* w3c = at<float>(c.ws, p.off_w3c);
           const lirpa_layer& t3 = net->T[2];
           const long nw3 = (long)t3.out_c * t3.in_c;
@@ -6518,18 +6544,18 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
                                  (unsigned)net->pstride, w3, (unsigned)net->n[3],
                                  (unsigned)inter, at<int8_t>(c.ws, p.off_code) + net->off[2],
-                                 (unsigned)net->n_relu, kidx1, w2t, part1, part2, gflag);
+                                 (unsigned)net->n_relu, kidx1, kidx2, w2t, part1, part2, gflag);
             }))
           return e;
         for (int m = 1; m <= 2; ++m) {
           const lirpa_layer& t = net->T[m - 1];
           const long off = net->off[m];
           if (int e = launch_k(tag("grad_gather", m, P), c.st, [&] {
-                if (m == 1 && t2.out_c == 32)
+                if (t2.out_c == 32)
                   hipLaunchKernelGGL(k_grad_gather_c, dim3((unsigned)c.nb), dim3(kBlock), 0,
-                                     c.st, net->n[1], R, part1, gflag, list1, cnt1,
-                                     c.L + off, c.U + off, net->n_relu, ga + off, gl + off,
-                                     gu + off);
+                                     c.st, net->n[m], R, m == 1 ? part1 : part2, gflag,
+                                     m == 1 ? list1 : list2, m == 1 ? cnt1 : cnt2, c.L + off,
+                                     c.U + off, net->n_relu, ga + off, gl + off, gu + off);
                 else
                   hipLaunchKernelGGL(k_grad_gather, grid_for(c.nb * net->n[m]), dim3(kBlock),
                                      0, c.st, c.nb, t.out_c, t.out_h * t.out_w, R,
