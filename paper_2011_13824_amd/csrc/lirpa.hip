@@ -4694,7 +4694,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
                const float* __restrict__ tape, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                float* __restrict__ G, float* __restrict__ zout, float* __restrict__ part,
-               unsigned char* __restrict__ gflag, const float* __restrict__ tapeW, int tnk) {
+               unsigned char* __restrict__ gflag, const float* __restrict__ tapeW, int tnk,
+               int ns) {
   static_assert(K <= 4, "tap columns are the four lane groups");
   constexpr int NKS = CI * K;                // K steps
   constexpr int NMT = (CO + 15) / 16;        // M tiles
@@ -4718,7 +4719,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
   __shared__ float ring[NSLOT * ROWF];
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, g = lane >> 4;
-  const unsigned q0 = xcd_tile(blockIdx.x) * 16u;
+  // ns = 2: two blocks per 16-row tile, each over half of the output rows (more blocks for a
+  // small batch of rows)
+  const unsigned q0 = xcd_tile(ns == 2 ? blockIdx.x >> 1 : blockIdx.x) * 16u;
+  const int y_lo = ns == 2 ? (int)(blockIdx.x & 1u) * (HO / 2) : 0;
+  const int y_hi = ns == 2 ? y_lo + HO / 2 : HO;
   if (q0 >= Q) return;  // grid padding, uniform per block
   const unsigned q = q0 + n;
   const bool qok = q < Q;
@@ -4834,23 +4839,23 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
     const int xr = (e / 4) % XW;
     if (xr < P || xr >= P + WI) *reinterpret_cast<float4v*>(ring + 4 * e) = float4v{0.f, 0.f, 0.f, 0.f};
   }
-  for (int yb = -P; yb < K - P; yb += S) {
+  for (int yb = y_lo * S - P; yb < y_lo * S + K - P; yb += S) {
     fetch_rows(yb);
     park_rows(yb);
   }
   __syncthreads();
   auto pos_of = [&](int y, int k) { return y * WO + wave / NMT + k * PSTEP; };
-  load_ep(pos_of(0, 0), et, el, eu, eb);
-  for (int y = 0; y < HO; ++y) {
+  load_ep(pos_of(y_lo, 0), et, el, eu, eb);
+  for (int y = y_lo; y < y_hi; ++y) {
     const int ynew = y * S - P + K;  // first input row output row y + 1 adds
-    if (y + 1 < HO) fetch_rows(ynew);
+    if (y + 1 < y_hi) fetch_rows(ynew);
     int sb[K];  // ring offsets of the K input rows of output row y (uniform)
 #pragma unroll
     for (int ky = 0; ky < K; ++ky) sb[ky] = slot_of(y * S - P + ky) * ROWF;
 #pragma unroll 1
     for (int k = 0; k < IPW; ++k) {
       const int pos = pos_of(y, k);
-      const bool has_next = k + 1 < IPW || y + 1 < HO;
+      const bool has_next = k + 1 < IPW || y + 1 < y_hi;
       float nt[4], nl[NE], nu[NE], nb[NE];
       if (has_next) load_ep(k + 1 < IPW ? pos_of(y, k + 1) : pos_of(y + 1, 0), nt, nl, nu, nb);
       // this lane's ring column (x*S - P + kx, kx = lane group) plus P; a group kx >= K reads
@@ -4916,7 +4921,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(
       eb[r] = nb[r];
     }
     }  // positions of row y
-    if (y + 1 < HO) {
+    if (y + 1 < y_hi) {
       if constexpr (TWO_BAR) __syncthreads();  // the slots ynew takes are free
       park_rows(ynew);
       __syncthreads();
@@ -6053,7 +6058,7 @@ int pass3_window(const Chunk& c) {
 using FwdKernel = void (*)(DLayer, const float*, unsigned, unsigned, long, const float*,
                            const float*, float, const float*, const float*, const float*,
                            const float*, long, float*, float*, float*, unsigned char*,
-                           const float*, int);
+                           const float*, int, int);
 template <int K, int S, int P, int CI, int CO, int HI, int WI, int HO, int WO>
 FwdKernel fwd_conv_inst(bool witness, bool zout) {
   if (zout)
@@ -6611,12 +6616,16 @@ int grad_chunk(const Chunk& c, int full) {
                              (unsigned)Q, R, w, tp, at<float>(c.ws, p.off_alo) + poff,
                              at<float>(c.ws, p.off_aup) + poff, at<float>(c.ws, p.off_bup) + poff,
                              net->pstride, G, zout);
-        } else if (fk)
-          hipLaunchKernelGGL(fk, dim3(nblk16), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
+        } else if (fk) {
+          // a small batch of rows (the final pass) splits each tile's output rows over two
+          // blocks, so that the grid fills the GPU in whole rounds
+          const int ns = (nblk16 < 4096 && t.out_h % 2 == 0) ? 2 : 1;
+          hipLaunchKernelGGL(fk, dim3(nblk16 * ns), dim3(256), 0, c.st, t, zin, (unsigned)ldq,
                              (unsigned)Q, R, w, c.x0, c.eps, tp,
                              at<float>(c.ws, p.off_alo) + poff, at<float>(c.ws, p.off_aup) + poff,
                              at<float>(c.ws, p.off_bup) + poff, net->pstride, G, zout, gpart,
-                             gflag, tapeW, tnk);
+                             gflag, tapeW, tnk, ns);
+        }
         else if (m == 1)
           hipLaunchKernelGGL(k_fwd_mfma<true>, dim3(nblk16), dim3(256), 0, c.st, t, zin,
                              (unsigned)ldq, (unsigned)Q, R, w, c.x0, c.eps, tp,
