@@ -4991,11 +4991,23 @@ __global__ void __launch_bounds__(256)
   const long q = b0 * R + lane;
   const bool qok = lane < QW && b0 + lane / R < nb;
   const float wq = qok ? w[q] : 0.f;
+  // the lane's row's neuron j is unstable in its sub-domain: only those rows' terms are used, so
+  // only those rows are read (the codes of the wave's 16 neurons, first)
+  bool un[16];
+  {
+    const long bq = qok ? b0 + lane / R : b0;
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      const long j = min(j0 + wave * 16 + jj, nm - 1);
+      un[jj] = code[bq * n_relu + j] == 5;
+    }
+  }
+#pragma unroll
   for (int jj = 0; jj < 16; ++jj) {
     const int jl = wave * 16 + jj;
     const long j = j0 + jl;
     float ca = 0.f, cd = 0.f, cb = 0.f;
-    if (j < nm && wq != 0.f) {
+    if (j < nm && wq != 0.f && un[jj]) {
       const float tv = tape[j * ldq + q], g = G[j * ldq + q];
       const float tp = fmaxf(tv, 0.f), tn = fminf(tv, 0.f);
       ca = (wq * tp) * g;
