@@ -2410,6 +2410,8 @@ __attribute__((amdgpu_waves_per_eu(SPEC > 0 ? 2 : (CI / CPW + NXW <= 8 ? 4 : 3),
 // both signs of 8 consecutive output channels (block group g: channels 8g .. 8g + 7; row r:
 // sign r / 8, channel 8g + r % 8), so rows r and r + 8 give l and u of one neuron.  C2 is a
 // multiple of 8.  Blocks are ordered (sub-domain, group, y2, x2), x2 fastest.
+__host__ __device__ constexpr int cgcd(int a, int b) { return b ? cgcd(b, a % b) : a; }
+
 struct P2Row {
   int c2;
   bool neg;
@@ -2434,7 +2436,7 @@ __host__ __device__ inline int p2_groups(int C2) { return C2 / 8; }
 //      writes l_j (sign +) or u_j (sign -) of the sub-domain.
 // The result equals the dense pass exactly in arithmetic terms: the skipped products are zeros.
 template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
-__global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 4 : 6, 8))) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                const float* __restrict__ z1, float eps, float* __restrict__ L,
                float* __restrict__ U, long n_relu, long off2, const int8_t* __restrict__ split,
@@ -2479,9 +2481,12 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
   const int row = threadIdx.x & 15, part = threadIdx.x >> 4;
   const P2Row prw = p2_row(C2, g, row);
   const float sgn = prw.neg ? -1.f : 1.f;
-  // split by sign (relaxed entry = wp a_lo + wn a_up), and the entry's place in the tile
+  // split by sign (relaxed entry = wp a_lo + wn a_up), and the entry's place in the tile.
+  // Entries k and k + TP lie TS channels apart at the same position, so only the first TP
+  // places are held; the others are those plus a constant (an immediate LDS offset).
+  constexpr int TP = NPOS / cgcd(RPT, NPOS), TS = TP * RPT / NPOS;
   float wp[NEP], wn[NEP];
-  int toff[NEP];
+  int toff[TP];
   {
     const float* w2 = t2.W + (long)prw.c2 * NE;  // [C1][K2][K2] of output channel c2
 #pragma unroll
@@ -2490,6 +2495,10 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
       const float w = e < NE ? sgn * w2[e] : 0.f;
       wp[k] = fmaxf(w, 0.f);
       wn[k] = fminf(w, 0.f);
+    }
+#pragma unroll
+    for (int k = 0; k < TP; ++k) {
+      const int e = part + k * RPT;
       const int c1 = e / NPOS, pos = e - c1 * NPOS;
       toff[k] = c1 * CS + pos * 16 + row;
     }
@@ -2557,7 +2566,7 @@ __global__ void __launch_bounds__(64 * NW) k_pass2_window(DLayer t1, DLayer t2, 
           bpart = fmaf(wn[k], pr[2], bpart);
           // layer-1 bias and the linear term of the concretisation together: v (W1 x0 + b1)
           bpart = fmaf(v, pr[3], bpart);
-          tile[toff[k]] = v;
+          tile[toff[k % TP] + (k / TP) * TS * CS] = v;
         }
       }
       bred[part * 16 + row] = bpart;
@@ -3254,11 +3263,17 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
       wv[k] = e < NE ? sgn * w2[e] : 0.f;
     }
   };
-  auto toff = [&](int k) {  // tile place of the thread's entry k
+  // tile place of the thread's entry k: entries k and k + TP lie TS channels apart at the same
+  // position, so only the first TP places are held (the rest add an immediate LDS offset)
+  constexpr int TP = NPOS / cgcd(RPT, NPOS), TS = TP * RPT / NPOS;
+  int tbase[TP];
+#pragma unroll
+  for (int k = 0; k < TP; ++k) {
     const int e = partid + k * RPT;
     const int c1 = e / NPOS, pos = e - c1 * NPOS;
-    return c1 * CS + pos * 16 + row;
-  };
+    tbase[k] = c1 * CS + pos * 16 + row;
+  }
+  auto toff = [&](int k) { return tbase[k % TP] + (k / TP) * TS * CS; };
   // T_1^T weights (step 2), one wave per input channel c0 of T_1
   const int c0 = wave;
   const bool cok = c0 < t1.in_c;
