@@ -152,7 +152,7 @@ def stage_work(layers, S, B):
     return work
 
 
-def grad_work(layers, S, B, l2=None):
+def grad_work(layers, S, B, l2=None, fr=None):
     """Algorithmic work per launch of the reverse-sweep kernel classes: {class: (flop, bytes)}.
 
     Pass P (rows Q = B*R) is swept from its witnesses forward.  The witness forward through
@@ -170,7 +170,12 @@ def grad_work(layers, S, B, l2=None):
     just those (in tiles of 16 channels per pair of positions).  l2 = (fraction of layer-2
     neurons unstable, fraction of the dense T_2 tiles computed), from the batch's stability
     codes: its algorithmic flops count T_2 at the unstable neurons only, and the executed MFMA
-    flops (the tiles computed) are returned under the key "executed"."""
+    flops (the tiles computed) are returned under the key "executed".
+
+    fr[m - 1] is the fraction of layer-m neurons unstable over the batch.  Only unstable neurons
+    get adjoint terms, so the gathers read the partial sums of those neurons alone, the
+    segmented reduction (R <= 64 rows per sub-domain) reads only their rows, and with 32
+    channels on T_2 the fused pass-3 forward writes only their partial sums."""
     from paper_2011_13824_amd import workloads as wl
     L = len(layers)
     n = [wl.n_in(layers[0])] + [wl.n_out(t) for t in layers]
@@ -180,6 +185,7 @@ def grad_work(layers, S, B, l2=None):
             return wl.n_out(t) * t["in_c"] * t["k"] * t["k"]
         return t["out_c"] * t["in_c"]
 
+    fr = [1.0] * L if fr is None else list(fr) + [1.0] * (L - len(fr))
     work = {}
     for P in range(L, 1, -1):
         R = S if P == L else 2 * n[P]
@@ -201,19 +207,23 @@ def grad_work(layers, S, B, l2=None):
             # input), the recorded coefficients over g^(1), the adjoint partial sums of both
             # layers (3 floats per neuron and group of 8 rows)
             f2, tiles = (1.0, 1.0)
-            if layers[1]["out_c"] == 32 and l2 is not None:
+            compact = layers[1]["out_c"] == 32
+            if compact and l2 is not None:
                 f2, tiles = l2
+            sums = fr[0] * n[1] + fr[1] * n[2] if compact else n[1] + n[2]
             work[f"fwd12[layer1,pass{P}]"] = (
                 2.0 * Q * (macs(layers[0]) + f2 * macs(layers[1])),
-                n[0] * Q + 4.0 * n[1] * Q + 12.0 * (n[1] + n[2]) * Q / 8)
+                n[0] * Q + 4.0 * n[1] * Q + 12.0 * sums * Q / 8)
             work.setdefault("executed", {})[f"fwd12[layer1,pass{P}]"] = \
                 2.0 * Q * (macs(layers[0]) + tiles * macs(layers[1]))
         for m in range(1, P):
             t = layers[m - 1]
             inb = n[0] * Q if m == 1 else 4.0 * n[m - 1] * Q
             work[f"fwd[layer{m},pass{P}]"] = (2.0 * Q * macs(t), inb + 8.0 * n[m] * Q)
-            work[f"grad_gather[layer{m},pass{P}]"] = (0.0, 12.0 * n[m] * Q / 8 + 12.0 * B * n[m])
-            work[f"grad_reduce[layer{m},pass{P}]"] = (0.0, 8.0 * n[m] * Q + 12.0 * B * n[m])
+            nu = fr[m - 1] * n[m]  # unstable neurons per sub-domain
+            work[f"grad_gather[layer{m},pass{P}]"] = (0.0, 12.0 * nu * Q / 8 + 12.0 * B * nu)
+            rows = nu if R <= 64 else n[m]  # (the segmented reduction skips stable neurons)
+            work[f"grad_reduce[layer{m},pass{P}]"] = (0.0, 8.0 * rows * Q + 12.0 * B * nu)
     return work
 
 
@@ -241,6 +251,20 @@ def layer2_stats(net, x0, w, C, split, alpha):
     per_pair = (lo | hi).sum(axis=3)  # [B, row, pair]
     tiles = np.maximum(1, (per_pair + 15) // 16)
     return float(u.mean()), float(tiles.mean() / 2.0)
+
+
+def unstable_fractions(net, x0, w, C, split, alpha):
+    """Fraction of the neurons of each ReLU layer that are unstable over the batch at the
+    given slopes, from the library's stability codes."""
+    from paper_2011_13824_amd import workloads as wl
+    _, code = net.bound(x0, w.eps, C, split=split, alpha=alpha, want_codes=True)
+    u = code.cpu().numpy() == 5
+    fr, off = [], 0
+    for t in w.layers[:-1]:
+        k = wl.n_out(t)
+        fr.append(float(u[:, off:off + k].mean()))
+        off += k
+    return fr
 
 
 def traffic_record(workload, kernel):
@@ -396,7 +420,8 @@ def main():
     work = stage_work(w.layers, S, B)
     executed = {}
     if optimise:
-        work.update(grad_work(w.layers, S, B, layer2_stats(net, x0, w, C, split, alpha)))
+        work.update(grad_work(w.layers, S, B, layer2_stats(net, x0, w, C, split, alpha),
+                              unstable_fractions(net, x0, w, C, split, alpha)))
         executed = work.pop("executed", {})
     stages = {}
     for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):
