@@ -198,7 +198,12 @@ def grad_work(layers, S, B, l2=None, fr=None):
             f2 = l2[0] if l2 is not None else 1.0
             work["pass2_window_grad[layer1,pass2]"] = (4.0 * Q * wmacs * f2,
                                                        4.0 * (3 * B * n[1] + parts))
-            work["pass2_grad_gather[layer1,pass2]"] = (0.0, 4.0 * (parts + 3 * B * n[1]))
+            # the gather reads every layer-1 code (a byte) and, for an unstable neuron, one
+            # partial per covering window (NG groups x (K2 / S2)^2 taps) and its gradient entry
+            taps = (t2["k"] + t2["stride"] - 1) // t2["stride"]
+            cover = (t2["out_c"] // 8) * taps * taps
+            work["pass2_grad_gather[layer1,pass2]"] = (
+                0.0, B * n[1] * (1.0 + fr[0] * (4.0 * cover + 8.0)))
             continue
         if P == 3 and P < L and all(layers[i]["kind"] == wl.CONV for i in (0, 1)) \
                 and layers[2]["kind"] == wl.FC:

@@ -56,6 +56,10 @@ def test_unstable_fractions_scale_only_the_sparse_reads(layers):
     macs1, macs2 = N1 * 3 * 16, N2 * 16 * 16
     assert work["fwd12[layer1,pass3]"][0] == pytest.approx(2.0 * Q3 * (macs1 + 0.25 * macs2))
     assert work["executed"]["fwd12[layer1,pass3]"] == pytest.approx(2.0 * Q3 * (macs1 + 0.5 * macs2))
+    # pass-2 gather: every layer-1 code, then for an unstable neuron the partials of the windows
+    # covering it (4 row groups of 8 channels x 2 x 2 taps) and its gradient entry
+    assert work["pass2_grad_gather[layer1,pass2]"][1] == pytest.approx(
+        B * N1 * (1.0 + 0.1 * (4.0 * 16 + 8.0)))
     # the witness forwards themselves do not change
     for k in ("fwd[layer1,pass4]", "fwd[layer2,pass4]", "pass2_window_grad[layer1,pass2]"):
         assert work[k] == dense[k]
