@@ -2661,6 +2661,14 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
   }
 }
 
+// LDS slot of channel c (0..7) in a tile the position-pair gather writes: bits 1 and 2 of c
+// exchanged (an involution).  The gather's lane groups store channels c and c + 4 at two
+// positions; with channel strides of 16 mod 64 banks, c and c + 4 would share banks, their
+// slots lie two strides (32 banks) apart.
+__host__ __device__ constexpr int slot8(int c) {
+  return (c & ~6) | ((c & 2) << 1) | ((c & 4) >> 1);
+}
+
 // T^T of a stride-1 convolution (kernel KK <= 3, Cs source channels) as a gather onto a window
 // of 8 destination channels, DW x DW positions, from a source window SW x SW: the 16 rows of a
 // block are the N dimension, and the 16 M lanes take the 8 channels at two neighbouring
@@ -2668,23 +2676,28 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1
 // lanes of a step (source column x0 + 1 - G for lane group G: tap G - 1 for x0, tap G for
 // x0 + 1), so one MFMA serves both positions.  One K step per (source channel, tap row), the
 // source row uniform (steps without one are skipped); position pairs are dealt to the waves.
-// Each result is relaxed (Eq. 6) with pp = (a_lo, a_up, b_up, bias), pstr apart, written to
-// dst[c][p][row], and its intercept and bias terms are summed into the returned value.
-// Source and destination tiles: [channel][position][16 rows], channel strides SCS and DCS.
-template <int Cs, int KK, int SW, int DW, int NW>
+// Each result is relaxed (Eq. 6) with pp[e] = (a_lo, a_up, b_up, bias), written to
+// dst[slot8(c)][p][row], and its intercept and bias terms are summed into the returned value.
+// Source and destination tiles: [channel slot][position][16 rows], channel strides SCS and DCS
+// (16 mod 64 banks); the source's channels sit at slot8(c) when SRC_SLOT, else at c.
+template <int Cs, int KK, int SW, int DW, int NW, bool SRC_SLOT>
 __device__ __forceinline__ float gather_pair8(const float* __restrict__ W, const float* src,
-                                              int SCS, float* dst, int DCS, const float* pp,
-                                              int pstr) {
+                                              int SCS, float* dst, int DCS, const float4v* pp) {
   static_assert(KK <= 3, "two positions' tap columns fit the four K lanes");
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int n = lane & 15, G = lane >> 4;
   const int cm = n & 7, pm = n >> 3;  // A operand row: destination channel and position
   const int kx = G - 1 + pm;
+  // (every lane loads from an in-range tap column, so the loads carry no branch; a lane whose
+  // column lies outside the kernel then takes a zero weight)
+  const bool kok = kx >= 0 && kx < KK;
+  const float* wl = W + cm * KK * KK + min(max(kx, 0), KK - 1);
   float areg[Cs * KK];
 #pragma unroll
   for (int ks = 0; ks < Cs * KK; ++ks) {
     const int c = ks / KK, ky = ks % KK;
-    areg[ks] = (kx >= 0 && kx < KK) ? W[((c * 8 + cm) * KK + ky) * KK + kx] : 0.f;
+    const float v = wl[(c * 8 * KK + ky) * KK];
+    areg[ks] = kok ? v : 0.f;
   }
   constexpr int NP = (DW + 1) / 2;  // position pairs per destination row
   constexpr int ND = DW * DW;
@@ -2701,7 +2714,7 @@ __device__ __forceinline__ float gather_pair8(const float* __restrict__ W, const
       if (iy < 0 || iy >= SW) continue;  // uniform
 #pragma unroll
       for (int c = 0; c < Cs; ++c) {
-        const float bv = xok ? colp[c * SCS + iy * SW * 16] : 0.f;
+        const float bv = xok ? colp[(SRC_SLOT ? slot8(c) : c) * SCS + iy * SW * 16] : 0.f;
         d = __builtin_amdgcn_mfma_f32_16x16x4f32(areg[c * KK + ky], bv, d, 0, 0, 0);
       }
     }
@@ -2712,12 +2725,12 @@ __device__ __forceinline__ float gather_pair8(const float* __restrict__ W, const
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int c = 4 * (G & 1) + r;
-        const int e = c * ND + p;
+        const float4v q = pp[c * ND + p];
         const float a = d[r];
-        const float ah = a >= 0.f ? a * pp[e] : a * pp[pstr + e];
-        bpart = fmaf(fminf(a, 0.f), pp[2 * pstr + e], bpart);
-        bpart = fmaf(ah, pp[3 * pstr + e], bpart);
-        dst[c * DCS + p * 16 + n] = ah;
+        const float ah = a >= 0.f ? a * q[0] : a * q[1];
+        bpart = fmaf(fminf(a, 0.f), q[2], bpart);
+        bpart = fmaf(ah, q[3], bpart);
+        dst[slot8(c) * DCS + p * 16 + n] = ah;
       }
     }
   }
@@ -2757,8 +2770,8 @@ __global__ void __launch_bounds__(512)
   static_assert(C1 % 4 == 0 && C1 <= 16 && K1 <= 4 && K2 <= 4 && K3 <= 4, "geometry");
   __shared__ float tile2[C2 * CS2];
   __shared__ float tile1[C1 * CS1];
-  __shared__ float p2s[4][E2];  // a_lo, a_up, b_up, bias of the g^(2) window
-  __shared__ float p1s[4][E1];  // a_lo, a_up, b_up, W1 x0 + b1 of the g^(1) window
+  __shared__ float4v p2s[E2];  // (a_lo, a_up, b_up, bias) of the g^(2) window
+  __shared__ float4v p1s[E1];  // (a_lo, a_up, b_up, W1 x0 + b1) of the g^(1) window
   __shared__ float rb2[RP * 16];  // bias terms of (2), per (part, row)
   __shared__ float rb1[NW * 4 * 16];  // bias terms of (3), per (wave, lane group, row)
   __shared__ float rl1[NW * 16];  // ||A_x||_1 partials of (4)
@@ -2790,10 +2803,7 @@ __global__ void __launch_bounds__(512)
         bu = b_up[pb + poff2 + ni];
         z = bias[poff2 + ni];
       }
-      p2s[0][e] = lo;
-      p2s[1][e] = up;
-      p2s[2][e] = bu;
-      p2s[3][e] = z;
+      p2s[e] = float4v{lo, up, bu, z};
     } else {
       const int f = e - E2;
       const int c1 = f / N1, p = f - c1 * N1;
@@ -2805,10 +2815,7 @@ __global__ void __launch_bounds__(512)
         bu = b_up[pb + poff1 + ni];
         z = bias[poff1 + ni];
       }
-      p1s[0][f] = lo;
-      p1s[1][f] = up;
-      p1s[2][f] = bu;
-      p1s[3][f] = z;
+      p1s[f] = float4v{lo, up, bu, z};
     }
   }
   __syncthreads();
@@ -2823,9 +2830,10 @@ __global__ void __launch_bounds__(512)
     for (int e = part; e < E2; e += RP) {
       const int c2 = e / N2, p = e - c2 * N2;
       const float w = sgn * w3[e];
-      const float v = w >= 0.f ? w * p2s[0][e] : w * p2s[1][e];
-      bpart = fmaf(fminf(w, 0.f), p2s[2][e], bpart);
-      bpart = fmaf(v, p2s[3][e], bpart);
+      const float4v q = p2s[e];
+      const float v = w >= 0.f ? w * q[0] : w * q[1];
+      bpart = fmaf(fminf(w, 0.f), q[2], bpart);
+      bpart = fmaf(v, q[3], bpart);
       tile2[c2 * CS2 + p * 16 + row] = v;
     }
     rb2[part * 16 + row] = bpart;
@@ -2835,8 +2843,8 @@ __global__ void __launch_bounds__(512)
   // (3) T_2^T: A over the g^(1) window, two positions per MFMA, relaxed into tile1
   {
     static_assert(C1 == 8, "the position-pair gather takes 8 channels");
-    const float bpart = gather_pair8<C2, K2, K3, W1W, NW>(t2.W, tile2, CS2, tile1, CS1,
-                                                          &p1s[0][0], E1);
+    const float bpart =
+        gather_pair8<C2, K2, K3, W1W, NW, false>(t2.W, tile2, CS2, tile1, CS1, p1s);
     rb1[(wave * 4 + G) * 16 + n] = bpart;
   }
   __syncthreads();
@@ -2855,7 +2863,7 @@ __global__ void __launch_bounds__(512)
           const int ky = ((slot - ph * S1) % K1 + K1) % K1;
 #pragma unroll
           for (int ks = 0; ks < KS1; ++ks) {
-            const int c1 = 4 * ks + G;
+            const int c1 = slot8(4 * ks + G);  // (the tile holds channel slots)
             wreg[ph][ks] = (slot < K1 && kx < K1)
                                ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
           }
@@ -2966,9 +2974,9 @@ __global__ void __launch_bounds__(512)
   float* const tile3 = tile31;
   float* const tile1 = tile31;
   __shared__ float tile2[C2 * CS2];
-  __shared__ float p3s[4][E3];  // a_lo, a_up, b_up, bias of the g^(3) window
-  __shared__ float p2s[4][E2];  // ... of the g^(2) window
-  __shared__ float p1s[4][E1];  // ... of the g^(1) window (bias: W1 x0 + b1)
+  __shared__ float4v p3s[E3];  // (a_lo, a_up, b_up, bias) of the g^(3) window
+  __shared__ float4v p2s[E2];  // ... of the g^(2) window
+  __shared__ float4v p1s[E1];  // ... of the g^(1) window (bias: W1 x0 + b1)
   __shared__ float rb3[RP * 16];      // bias terms of (2), per (part, row)
   __shared__ float rb2[NW * 4 * 16];  // bias terms of (3a), per (wave, lane group, row)
   __shared__ float rb1[NW * 4 * 16];  // bias terms of (3b)
@@ -3005,15 +3013,15 @@ __global__ void __launch_bounds__(512)
   for (int e = threadIdx.x; e < E3 + E2 + E1; e += NT) {
     if (e < E3) {
       const float4v v = stage(e, K4, Y3, X3, H3, Wd3, poff3);
-      p3s[0][e] = v[0]; p3s[1][e] = v[1]; p3s[2][e] = v[2]; p3s[3][e] = v[3];
+      p3s[e] = v;
     } else if (e < E3 + E2) {
       const int f = e - E3;
       const float4v v = stage(f, W2W, Y2, X2, H2, Wd2, poff2);
-      p2s[0][f] = v[0]; p2s[1][f] = v[1]; p2s[2][f] = v[2]; p2s[3][f] = v[3];
+      p2s[f] = v;
     } else {
       const int f = e - E3 - E2;
       const float4v v = stage(f, W1W, Y1, X1, H1, Wd1, poff1);
-      p1s[0][f] = v[0]; p1s[1][f] = v[1]; p1s[2][f] = v[2]; p1s[3][f] = v[3];
+      p1s[f] = v;
     }
   }
   __syncthreads();
@@ -3028,9 +3036,10 @@ __global__ void __launch_bounds__(512)
     for (int e = part; e < E3; e += RP) {
       const int c3 = e / N3, p = e - c3 * N3;
       const float w = sgn * w4[e];
-      const float v = w >= 0.f ? w * p3s[0][e] : w * p3s[1][e];
-      bpart = fmaf(fminf(w, 0.f), p3s[2][e], bpart);
-      bpart = fmaf(v, p3s[3][e], bpart);
+      const float4v q = p3s[e];
+      const float v = w >= 0.f ? w * q[0] : w * q[1];
+      bpart = fmaf(fminf(w, 0.f), q[2], bpart);
+      bpart = fmaf(v, q[3], bpart);
       tile3[c3 * CS3 + p * 16 + row] = v;
     }
     rb3[part * 16 + row] = bpart;
@@ -3041,10 +3050,10 @@ __global__ void __launch_bounds__(512)
   // each result relaxed into the next tile
   static_assert(C2 == 8 && C1 == 8, "the position-pair gather takes 8 channels");
   rb2[(wave * 4 + G) * 16 + n] =
-      gather_pair8<C3, K3, K4, W2W, NW>(t3.W, tile3, CS3, tile2, CS2, &p2s[0][0], E2);
+      gather_pair8<C3, K3, K4, W2W, NW, false>(t3.W, tile3, CS3, tile2, CS2, p2s);
   __syncthreads();
   rb1[(wave * 4 + G) * 16 + n] =
-      gather_pair8<C2, K2, W2W, W1W, NW>(t2.W, tile2, CS2, tile1, CS1, &p1s[0][0], E1);
+      gather_pair8<C2, K2, W2W, W1W, NW, true>(t2.W, tile2, CS2, tile1, CS1, p1s);
   __syncthreads();
 
   // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
@@ -3061,7 +3070,7 @@ __global__ void __launch_bounds__(512)
           const int ky = ((slot - ph * S1) % K1 + K1) % K1;
 #pragma unroll
           for (int ks = 0; ks < KS1; ++ks) {
-            const int c1 = 4 * ks + G;
+            const int c1 = slot8(4 * ks + G);  // (the tile holds channel slots)
             wreg[ph][ks] = (slot < K1 && kx < K1)
                                ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
           }
