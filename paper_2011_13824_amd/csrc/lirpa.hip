@@ -2737,6 +2737,87 @@ __device__ __forceinline__ float gather_pair8(const float* __restrict__ W, const
   return bpart;
 }
 
+// T_1^T over a W x W window tile of g^(1) ([channel slot][position][16 rows], 8 slots at
+// stride CS, channel slot8(c) at slot c) for input channel c0 of T_1, with the rotating
+// lane-group scheme of k_pass2_window, and the L1 norm of the result over the window's footprint
+// on x (origin OY, OX; positions outside the image are zero padding): this lane's part of
+// ||A_x||_1 of row n (Eq. 8).  A lane's row of acc restarts after the lane emits it: the next
+// window row's first contribution to each column scales the old value by keep = 0 (every
+// column is reached in every window row), and a footprint inside the image horizontally is
+// summed without a per-column test.
+template <int W, int K1, int S1, int KS, int CS>
+__device__ __forceinline__ float t1t_window_l1(const DLayer& t1, int c0, const float* tile,
+                                               int OY, int OX) {
+  constexpr int PER = (K1 % S1 == 0) ? K1 / S1 : K1;
+  constexpr int WO = (W - 1) * S1 + K1;  // footprint width on x
+  const int lane = threadIdx.x & 63, n = lane & 15, G = lane >> 4;
+  float wreg[PER][KS];
+  {
+    const int M = lane & 15, slot = M >> 2, kx = M & 3;
+#pragma unroll
+    for (int ph = 0; ph < PER; ++ph) {
+      const int ky = ((slot - ph * S1) % K1 + K1) % K1;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int c1 = slot8(4 * ks + G);  // (the tile holds channel slots)
+        wreg[ph][ks] = (slot < K1 && kx < K1)
+                           ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
+      }
+    }
+  }
+  const int Hi = t1.in_h, Wi = t1.in_w;
+  const bool inside_x = OX >= 0 && OX + WO <= Wi;
+  float l1 = 0.f, keep = 1.f;
+  float acc[WO];
+  auto emit = [&](int yl) {  // footprint row yl: ||.||_1 of the clipped row
+    const int y = OY + yl;
+    if (y < 0 || y >= Hi) return;
+    if (inside_x) {
+#pragma unroll
+      for (int x = 0; x < WO; ++x) l1 += fabsf(acc[x]);
+    } else {
+#pragma unroll
+      for (int x = 0; x < WO; ++x) {
+        const int xc = OX + x;
+        l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
+      }
+    }
+  };
+#pragma unroll
+  for (int j = 0; j < W; ++j) {
+    const int ph = j % PER;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      const int pos = j * W + i;
+      float4v d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        d = __builtin_amdgcn_mfma_f32_16x16x4f32(wreg[ph][ks],
+                                                tile[(4 * ks + G) * CS + pos * 16 + n], d, 0,
+                                                0, 0);
+#pragma unroll
+      for (int kx = 0; kx < K1; ++kx) {
+        float& a = acc[i * S1 + kx];
+        if (i > 0 && kx < K1 - S1)
+          a += d[kx];
+        else if (j == 0)
+          a = d[kx];
+        else
+          a = fmaf(a, keep, d[kx]);
+      }
+    }
+    const int ky = ((G - ph * S1) % K1 + K1) % K1;
+    const bool done = G < K1 && ky < S1;
+    if (done) emit(j * S1 + ky);
+    keep = done ? 0.f : 1.f;
+  }
+  {
+    const int ky = ((G - ((W - 1) % PER) * S1) % K1 + K1) % K1;
+    if (G < K1 && ky >= S1) emit((W - 1) * S1 + ky);
+  }
+  return l1;
+}
+
 // Pass 3 restricted to each row's receptive field, when T_3, T_2 (stride 1) and T_1 are
 // convolutions.  Row +-e_j of h^(3), j = (c3, y3, x3), carried through T_3 is +-W_3[c3] on the
 // K3 x K3 window of j on g^(2); after the layer-2 relaxation, T_2^T spreads it over a
@@ -2851,70 +2932,14 @@ __global__ void __launch_bounds__(512)
 
   // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
   {
-    const int c0 = wave;
-    const bool cok = c0 < t1.in_c;
-    float l1 = 0.f;
-    if (cok) {
-      float wreg[PER1][KS1];
-      {
-        const int M = lane & 15, slot = M >> 2, kx = M & 3;
-#pragma unroll
-        for (int ph = 0; ph < PER1; ++ph) {
-          const int ky = ((slot - ph * S1) % K1 + K1) % K1;
-#pragma unroll
-          for (int ks = 0; ks < KS1; ++ks) {
-            const int c1 = slot8(4 * ks + G);  // (the tile holds channel slots)
-            wreg[ph][ks] = (slot < K1 && kx < K1)
-                               ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
-          }
-        }
-      }
-      const int Hi = t1.in_h, Wi = t1.in_w;
-      const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
-      float acc[WO];
-#pragma unroll
-      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-      auto emit = [&](int yl) {
-        const int yy = OY + yl;
-        if (yy < 0 || yy >= Hi) return;
-#pragma unroll
-        for (int x = 0; x < WO; ++x) {
-          const int xc = OX + x;
-          l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
-        }
-      };
-#pragma unroll
-      for (int j = 0; j < W1W; ++j) {
-        const int ph = j % PER1;
-#pragma unroll
-        for (int i = 0; i < W1W; ++i) {
-          const int pos = j * W1W + i;
-          float4v d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < KS1; ++ks)
-            d = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                wreg[ph][ks], tile1[(4 * ks + G) * CS1 + pos * 16 + n], d, 0, 0, 0);
-#pragma unroll
-          for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
-        }
-        const int ky = ((G - ph * S1) % K1 + K1) % K1;
-        if (G < K1 && ky < S1) {
-          emit(j * S1 + ky);
-#pragma unroll
-          for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-        }
-      }
-      {
-        const int ky = ((G - ((W1W - 1) % PER1) * S1) % K1 + K1) % K1;
-        if (G < K1 && ky >= S1) emit((W1W - 1) * S1 + ky);
-      }
-    }
+    float l1 = wave < t1.in_c ? t1t_window_l1<W1W, K1, S1, KS1, CS1>(t1, wave, tile1,
+                                                                    Y1 * S1 - P1, X1 * S1 - P1)
+                              : 0.f;
     l1 += __shfl_xor(l1, 16, 64);
     l1 += __shfl_xor(l1, 32, 64);
     if (lane < 16) rl1[wave * 16 + lane] = l1;
   }
   __syncthreads();
-
   // (5) the bound of each row
   if (threadIdx.x >= 16) return;
   const int row = threadIdx.x;
@@ -3058,70 +3083,14 @@ __global__ void __launch_bounds__(512)
 
   // (4) T_1^T over the g^(1) window, one wave per input channel c0 of T_1
   {
-    const int c0 = wave;
-    const bool cok = c0 < t1.in_c;
-    float l1 = 0.f;
-    if (cok) {
-      float wreg[PER1][KS1];
-      {
-        const int M = lane & 15, slot = M >> 2, kx = M & 3;
-#pragma unroll
-        for (int ph = 0; ph < PER1; ++ph) {
-          const int ky = ((slot - ph * S1) % K1 + K1) % K1;
-#pragma unroll
-          for (int ks = 0; ks < KS1; ++ks) {
-            const int c1 = slot8(4 * ks + G);  // (the tile holds channel slots)
-            wreg[ph][ks] = (slot < K1 && kx < K1)
-                               ? t1.W[(((long)c1 * t1.in_c + c0) * K1 + ky) * K1 + kx] : 0.f;
-          }
-        }
-      }
-      const int Hi = t1.in_h, Wi = t1.in_w;
-      const int OY = Y1 * S1 - P1, OX = X1 * S1 - P1;
-      float acc[WO];
-#pragma unroll
-      for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-      auto emit = [&](int yl) {
-        const int yy = OY + yl;
-        if (yy < 0 || yy >= Hi) return;
-#pragma unroll
-        for (int x = 0; x < WO; ++x) {
-          const int xc = OX + x;
-          l1 += (xc >= 0 && xc < Wi) ? fabsf(acc[x]) : 0.f;
-        }
-      };
-#pragma unroll
-      for (int j = 0; j < W1W; ++j) {
-        const int ph = j % PER1;
-#pragma unroll
-        for (int i = 0; i < W1W; ++i) {
-          const int pos = j * W1W + i;
-          float4v d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < KS1; ++ks)
-            d = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                wreg[ph][ks], tile1[(4 * ks + G) * CS1 + pos * 16 + n], d, 0, 0, 0);
-#pragma unroll
-          for (int kx = 0; kx < K1; ++kx) acc[i * S1 + kx] += d[kx];
-        }
-        const int ky = ((G - ph * S1) % K1 + K1) % K1;
-        if (G < K1 && ky < S1) {
-          emit(j * S1 + ky);
-#pragma unroll
-          for (int x = 0; x < WO; ++x) acc[x] = 0.f;
-        }
-      }
-      {
-        const int ky = ((G - ((W1W - 1) % PER1) * S1) % K1 + K1) % K1;
-        if (G < K1 && ky >= S1) emit((W1W - 1) * S1 + ky);
-      }
-    }
+    float l1 = wave < t1.in_c ? t1t_window_l1<W1W, K1, S1, KS1, CS1>(t1, wave, tile1,
+                                                                    Y1 * S1 - P1, X1 * S1 - P1)
+                              : 0.f;
     l1 += __shfl_xor(l1, 16, 64);
     l1 += __shfl_xor(l1, 32, 64);
     if (lane < 16) rl1[wave * 16 + lane] = l1;
   }
   __syncthreads();
-
   // (5) the bound of each row
   if (threadIdx.x >= 16) return;
   const int row = threadIdx.x;
