@@ -4079,7 +4079,7 @@ __global__ void __launch_bounds__(256, 2)
                  const float* __restrict__ tape1, const float* __restrict__ a_lo,
                  const float* __restrict__ a_up, const float* __restrict__ b_up,
                  unsigned pstride, const float* __restrict__ W3, unsigned nk, unsigned inter,
-                 const int8_t* __restrict__ code2, unsigned n_relu,
+                 const unsigned* __restrict__ psel,
                  const int* __restrict__ kidx1, const int* __restrict__ kidx2,
                  const float* __restrict__ W2t,
                  float* __restrict__ part1,
@@ -4208,48 +4208,10 @@ __global__ void __launch_bounds__(256, 2)
     return reinterpret_cast<const float4v*>(W2t + (size_t)co2n * (C1 * K * K)) + g;
   };
   // each row's pair of positions (xa | xb << 3) for this wave and the channels unstable at
-  // either of them (wave-uniform, from the sub-domain's layer-2 stability codes, read once:
-  // lane c and c + 32 read channel c of two rows, one byte per position), kept in LDS
+  // either of them (wave-uniform, k_pair_select), kept in LDS
   __shared__ unsigned gsel[GATHER ? 4 : 1][H2][2];
   if constexpr (GATHER) {
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
-    const int8_t* cc = code2 + (size_t)b * n_relu + (lane & 31) * (H2 * H2) + (lane >> 5) * H2;
-    int8_t cd[H2 / 2][H2];
-#pragma unroll
-    for (int yy = 0; yy < H2 / 2; ++yy)
-#pragma unroll
-      for (int x = 0; x < H2; ++x) cd[yy][x] = cc[2 * yy * H2 + x];
-#pragma unroll
-    for (int yy = 0; yy < H2 / 2; ++yy) {
-      unsigned m[2][H2];
-#pragma unroll
-      for (int x = 0; x < H2; ++x) {
-        const unsigned long long bm = __ballot(cd[yy][x] == 5);
-        m[0][x] = (unsigned)bm;
-        m[1][x] = (unsigned)(bm >> 32);
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        // rank of each position by (count, position); this wave's pair: ranks wv and 7 - wv
-        int key[H2];
-#pragma unroll
-        for (int x = 0; x < H2; ++x) key[x] = __builtin_popcount(m[h][x]) * H2 + x;
-        int xa = 0, xb = 0;
-        unsigned ma = 0u, mb = 0u;
-#pragma unroll
-        for (int x = 0; x < H2; ++x) {
-          int rk = 0;
-#pragma unroll
-          for (int x2 = 0; x2 < H2; ++x2) rk += key[x2] < key[x] ? 1 : 0;
-          xa = rk == wv ? x : xa;
-          ma = rk == wv ? m[h][x] : ma;
-          xb = rk == H2 - 1 - wv ? x : xb;
-          mb = rk == H2 - 1 - wv ? m[h][x] : mb;
-        }
-        gsel[wave][2 * yy + h][0] = ma | mb;
-        gsel[wave][2 * yy + h][1] = (unsigned)xa | ((unsigned)xb << 3);
-      }
-    }
+    if (lane < 2 * H2) (&gsel[wave][0][0])[lane] = psel[((size_t)b * 4 + wave) * (2 * H2) + lane];
   }
 
   auto xslot = [](int yi) { return (yi + 6 * NX) % NX; };
@@ -4592,6 +4554,61 @@ __global__ void __launch_bounds__(256)
     __syncthreads();  // wsum is rewritten by the next chunk
   }
   if (threadIdx.x == 0) cnt[b] = base;
+}
+
+// The position pairs of k_fwd_conv12's layer-2 tiles (T_2 with 32 channels on an 8 x 8 map), the
+// same for every group of rows of a sub-domain, so found once per sub-domain: for wave w of that
+// kernel and map row y, sel[b][w][y] = (the channels unstable at either position of the wave's
+// pair, xa | xb << 3).  The 8 positions of a row are ranked by (number of unstable channels,
+// position) and wave w takes ranks w and 7 - w.  One block of 4 waves per sub-domain, wave w
+// for pairs w; the stability codes are read once (lane c and c + 32 read channel c of two rows,
+// one byte per position) and counted by ballot.
+__global__ void __launch_bounds__(256)
+    k_pair_select(const int8_t* __restrict__ code2, unsigned n_relu, unsigned* __restrict__ sel) {
+  constexpr int H2 = 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned b = blockIdx.x;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int8_t* cc = code2 + (size_t)b * n_relu + (lane & 31) * (H2 * H2) + (lane >> 5) * H2;
+  int8_t cd[H2 / 2][H2];
+#pragma unroll
+  for (int yy = 0; yy < H2 / 2; ++yy)
+#pragma unroll
+    for (int x = 0; x < H2; ++x) cd[yy][x] = cc[2 * yy * H2 + x];
+  unsigned* out = sel + ((size_t)b * 4 + wv) * (2 * H2);
+#pragma unroll
+  for (int yy = 0; yy < H2 / 2; ++yy) {
+    unsigned m[2][H2];
+#pragma unroll
+    for (int x = 0; x < H2; ++x) {
+      const unsigned long long bm = __ballot(cd[yy][x] == 5);
+      m[0][x] = (unsigned)bm;
+      m[1][x] = (unsigned)(bm >> 32);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      // rank of each position by (count, position); this wave's pair: ranks wv and 7 - wv
+      int key[H2];
+#pragma unroll
+      for (int x = 0; x < H2; ++x) key[x] = __builtin_popcount(m[h][x]) * H2 + x;
+      int xa = 0, xb = 0;
+      unsigned ma = 0u, mb = 0u;
+#pragma unroll
+      for (int x = 0; x < H2; ++x) {
+        int rk = 0;
+#pragma unroll
+        for (int x2 = 0; x2 < H2; ++x2) rk += key[x2] < key[x] ? 1 : 0;
+        xa = rk == wv ? x : xa;
+        ma = rk == wv ? m[h][x] : ma;
+        xb = rk == H2 - 1 - wv ? x : xb;
+        mb = rk == H2 - 1 - wv ? m[h][x] : mb;
+      }
+      if (lane == 0) {
+        out[(2 * yy + h) * 2] = ma | mb;
+        out[(2 * yy + h) * 2 + 1] = (unsigned)xa | ((unsigned)xb << 3);
+      }
+    }
+  }
 }
 
 // k_grad_gather over compacted partial sums: part[(b (R / 8) + k8) n_m + k][3] holds the sums of
@@ -5405,6 +5422,7 @@ struct Plan {
   size_t off_w3c = 0;     // and of T_3's weights with the input index channel-last
   size_t off_kidx1 = 0, off_list1 = 0, off_cnt1 = 0;  // its unstable layer-1 neurons' ranks
   size_t off_kidx2 = 0, off_list2 = 0, off_cnt2 = 0;  // and layer-2 neurons'
+  size_t off_psel = 0;  // its position pairs of layer-2 tiles per sub-domain
   long fwd_floats = 0;
   // lower and upper bounds in one call: the spec rows [C; -C] (or -C alone) and, for the bound,
   // the [Bc][2S] bounds of those rows before they are split into lb and ub
@@ -5477,7 +5495,7 @@ bool pass_on_chip(const lirpa_net* net, int k, long Bc);
 using Fwd12Kernel = void (*)(DLayer, DLayer, const int8_t*, unsigned, unsigned, unsigned,
                              const float*, const float*, float, const float*, const float*,
                              const float*, const float*, unsigned, const float*, unsigned,
-                             unsigned, const int8_t*, unsigned, const int*, const int*,
+                             unsigned, const unsigned*, const int*, const int*,
                              const float*, float*, float*, unsigned char*);
 Fwd12Kernel fwd12_for(const lirpa_net* net) {
   if (net->L < 4 || net->T[2].kind != LIRPA_LINEAR) return nullptr;
@@ -5603,6 +5621,8 @@ Plan make_plan(const lirpa_net* net, long S, long Bc, int mode = 0) {
       o = align256(o + (size_t)Bc * net->n[2] * 4);
       p.off_cnt2 = o;
       o = align256(o + (size_t)Bc * 4);
+      p.off_psel = o;  // k_pair_select's [Bc][4][H2][2] words (H2 = 8)
+      o = align256(o + (size_t)Bc * 4 * 8 * 2 * 4);
     }
   }
   p.total = o;
@@ -6525,6 +6545,7 @@ int grad_chunk(const Chunk& c, int full) {
         int* kidx2 = at<int>(c.ws, p.off_kidx2);
         int* list2 = at<int>(c.ws, p.off_list2);
         int* cnt2 = at<int>(c.ws, p.off_cnt2);
+        unsigned* psel = at<unsigned>(c.ws, p.off_psel);
         if (t2.out_c == 32) {
           for (int m = 1; m <= 2; ++m)
             if (int e = launch_k(tag("unstable_index", m, P), c.st, [&] {
@@ -6534,6 +6555,12 @@ int grad_chunk(const Chunk& c, int full) {
                                      m == 1 ? cnt1 : cnt2);
                 }))
               return e;
+          if (int e = launch_k(tag("pair_select", 2, P), c.st, [&] {
+                hipLaunchKernelGGL(k_pair_select, dim3((unsigned)c.nb), dim3(256), 0, c.st,
+                                   at<int8_t>(c.ws, p.off_code) + net->off[2],
+                                   (unsigned)net->n_relu, psel);
+              }))
+            return e;
           float* w3c = at<float>(c.ws, p.off_w3c);
           const lirpa_layer& t3 = net->T[2];
           const long nw3 = (long)t3.out_c * t3.in_c;
@@ -6553,8 +6580,7 @@ int grad_chunk(const Chunk& c, int full) {
                                  at<float>(c.ws, p.off_aup) + net->poff[1],
                                  at<float>(c.ws, p.off_bup) + net->poff[1],
                                  (unsigned)net->pstride, w3, (unsigned)net->n[3],
-                                 (unsigned)inter, at<int8_t>(c.ws, p.off_code) + net->off[2],
-                                 (unsigned)net->n_relu, kidx1, kidx2, w2t, part1, part2, gflag);
+                                 (unsigned)inter, psel, kidx1, kidx2, w2t, part1, part2, gflag);
             }))
           return e;
         for (int m = 1; m <= 2; ++m) {
