@@ -2436,7 +2436,11 @@ __host__ __device__ inline int p2_groups(int C2) { return C2 / 8; }
 //      writes l_j (sign +) or u_j (sign -) of the sub-domain.
 // The result equals the dense pass exactly in arithmetic terms: the skipped products are zeros.
 template <int K1, int S1, int P1, int K2, int C1, int NW, int XW>
-__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 4 : 6, 8))) k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
+// (with 8 windows per block the kernel fits 80 VGPRs with 8 channels on T_1, 128 with 16, one
+// more wave per SIMD than it would take unhinted; with 4 it would spill, so it is left alone)
+__global__ void __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(XW == 8 ? (C1 >= 16 ? 4 : 6) : 1, 8)))
+    k_pass2_window(DLayer t1, DLayer t2, long nb, const float* __restrict__ a_lo,
                const float* __restrict__ a_up, const float* __restrict__ b_up, long pstride,
                const float* __restrict__ z1, float eps, float* __restrict__ L,
                float* __restrict__ U, long n_relu, long off2, const int8_t* __restrict__ split,
