@@ -28,7 +28,7 @@ PEAK_FP32_TFLOPS = 157.3   # MI355X dense fp32 (MFMA)
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
 
 
-def stage_work(layers, S, B):
+def stage_work(layers, S, B, fr=None):
     """Algorithmic work of one step per kernel class: {class: (flop, bytes)}.
 
     A backward stage through layer m carries Q = B*R rows (R = 2 n_k for pass k, S for the final
@@ -92,8 +92,11 @@ def stage_work(layers, S, B):
     for m in range(1, L):
         # relaxation parameters of layer m (elementwise): l, u read or, for layer 1, copied from
         # the shared bounds and written (8 bytes), the split byte read, (a_lo, a_up, b_up) and
-        # the stability code written (13 bytes) per neuron and sub-domain
-        add(f"relax_params[layer{m},pass{m}]", 0.0, 22.0 * B * n[m])
+        # the stability code written (13 bytes) per neuron and sub-domain; with optimised
+        # slopes (fr = the fraction of the layer's neurons unstable), alpha read (4 bytes) for
+        # the unstable neurons, the only ones whose slope is free
+        fa = 0.0 if fr is None else fr[m - 1]
+        add(f"relax_params[layer{m},pass{m}]", 0.0, (22.0 + 4.0 * fa) * B * n[m])
     if L >= 3 and layers[L - 2]["kind"] == wl.FC:
         # the final pass's spec rows through T_L and T_{L-1} in one kernel: T_{L-1}^T's flops;
         # bytes: the relaxations of layers L-1 and L-2 read (3 floats per neuron and
@@ -422,11 +425,11 @@ def main():
         step()
     times = lirpa.lirpa_timing_end()
     torch.cuda.synchronize()
-    work = stage_work(w.layers, S, B)
+    fr = unstable_fractions(net, x0, w, C, split, alpha) if optimise else None
+    work = stage_work(w.layers, S, B, fr)
     executed = {}
     if optimise:
-        work.update(grad_work(w.layers, S, B, layer2_stats(net, x0, w, C, split, alpha),
-                              unstable_fractions(net, x0, w, C, split, alpha)))
+        work.update(grad_work(w.layers, S, B, layer2_stats(net, x0, w, C, split, alpha), fr))
         executed = work.pop("executed", {})
     stages = {}
     for cls, (tot_ms, launches) in sorted(times.items(), key=lambda kv: -kv[1][0]):

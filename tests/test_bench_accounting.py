@@ -71,3 +71,13 @@ def test_pass_rows_above_the_segment_limit_read_every_neuron(layers):
     work = bench.grad_work(layers, S, B, None, [0.1, 0.25, 0.8])
     Q3 = B * 2 * N3
     assert work["grad_reduce[layer1,pass3]"][1] == pytest.approx(8.0 * N1 * Q3 + 12.0 * B * 0.1 * N1)
+
+
+def test_relax_params_reads_alpha_of_unstable_neurons_only(layers):
+    # l, u (8), split (1), a_lo, a_up, b_up and the code (13) per neuron; alpha (4) only where
+    # the neuron is unstable, since every other neuron's slope is fixed
+    plain = bench.stage_work(layers, S, B)
+    opt = bench.stage_work(layers, S, B, [0.1, 0.25, 0.8])
+    assert plain["relax_params[layer1,pass1]"][1] == pytest.approx(22.0 * B * N1)
+    assert opt["relax_params[layer1,pass1]"][1] == pytest.approx((22.0 + 0.4) * B * N1)
+    assert opt["relax_params[layer2,pass2]"][1] == pytest.approx((22.0 + 1.0) * B * N2)
