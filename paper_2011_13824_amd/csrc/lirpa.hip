@@ -3426,25 +3426,18 @@ __attribute__((amdgpu_waves_per_eu(C1 >= 16 ? 3 : 4, 8)))
   }
 }
 
-// d J / d alpha of layer-1 neuron (c1, y1, x1) from pass 2: the partial sums of every window that
-// covers the neuron, in a fixed order.
-__global__ void __launch_bounds__(kBlock)
-    k_pass2_grad_gather(long nb, DLayer t1, DLayer t2, int NPOS, const float* __restrict__ part,
-                        const unsigned char* __restrict__ pflag,
-                        const int8_t* __restrict__ code1, long n_relu,
-                        float* __restrict__ ga1) {
-  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  const long n1 = (long)t1.out_c * t1.out_h * t1.out_w;
-  if (idx >= nb * n1) return;
-  const long b = idx / n1, ni = idx % n1;
-  if (code1[b * n_relu + ni] != 5) return;
+// The sum for neuron ni = (c1, y1, x1) of sub-domain b: the flagged partials of the windows that
+// cover it, in the order (g, ky2, kx2), which the neuron alone fixes.
+__device__ __forceinline__ float p2_gather_neuron(long b, long ni, const DLayer& t1,
+                                                  const DLayer& t2, int NPOS,
+                                                  const float* __restrict__ part,
+                                                  const unsigned char* __restrict__ pflag) {
   const int hw = t1.out_h * t1.out_w;
   const int c1 = (int)(ni / hw), y1 = (int)((ni / t1.out_w) % t1.out_h), x1 = (int)(ni % t1.out_w);
   const int H2 = t2.out_h, W2 = t2.out_w, K2 = t2.k, S2 = t2.stride, P2 = t2.pad;
   const int NG = p2_groups(t2.out_c);
   const int C1 = t1.out_c;
-  // the windows covering (y1, x1): taps ky2 = (y1 + P2) mod S2, + S2, ... (the same for x);
-  // the order (g, ky2, kx2) is fixed by the neuron alone
+  // the windows covering (y1, x1): taps ky2 = (y1 + P2) mod S2, + S2, ... (the same for x)
   const int ry = (y1 + P2) % S2, rx = (x1 + P2) % S2;
   float acc = 0.f;
   for (int g = 0; g < NG; ++g)
@@ -3462,7 +3455,37 @@ __global__ void __launch_bounds__(kBlock)
         if (pflag[blk]) acc += part[(blk * C1 + c1) * NPOS + ky2 * K2 + kx2];
       }
     }
-  ga1[b * n_relu + ni] += acc;
+  return acc;
+}
+
+// d J / d alpha of layer-1 neuron (c1, y1, x1) from pass 2: the partial sums of every window that
+// covers the neuron, in a fixed order; a thread per (sub-domain, neuron).
+__global__ void __launch_bounds__(kBlock)
+    k_pass2_grad_gather(long nb, DLayer t1, DLayer t2, int NPOS, const float* __restrict__ part,
+                        const unsigned char* __restrict__ pflag,
+                        const int8_t* __restrict__ code1, long n_relu,
+                        float* __restrict__ ga1) {
+  long idx = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  const long n1 = (long)t1.out_c * t1.out_h * t1.out_w;
+  if (idx >= nb * n1) return;
+  const long b = idx / n1, ni = idx % n1;
+  if (code1[b * n_relu + ni] != 5) return;
+  ga1[b * n_relu + ni] += p2_gather_neuron(b, ni, t1, t2, NPOS, part, pflag);
+}
+
+// The same over the sub-domain's unstable layer-1 neurons listed by k_unstable_index
+// (list[b][k], cnt[b]): a block per sub-domain, a thread per listed neuron, the same sums.
+__global__ void __launch_bounds__(kBlock)
+    k_pass2_grad_gather_c(DLayer t1, DLayer t2, int NPOS, const float* __restrict__ part,
+                          const unsigned char* __restrict__ pflag, const int* __restrict__ list,
+                          const int* __restrict__ cnt, long n1, long n_relu,
+                          float* __restrict__ ga1) {
+  const long b = blockIdx.x;
+  const int m = cnt[b];
+  for (int k = threadIdx.x; k < m; k += blockDim.x) {
+    const long ni = list[b * n1 + k];
+    ga1[b * n_relu + ni] += p2_gather_neuron(b, ni, t1, t2, NPOS, part, pflag);
+  }
 }
 
 // Linear^T as a GEMM on 32x32x2 MFMA: out[i][q] = sum_o W[o][i] in[o][q].  Block: 32 rows q
@@ -6492,6 +6515,7 @@ int grad_chunk(const Chunk& c, int full) {
           hipLaunchKernelGGL(k_zero, grid_for(per), dim3(kBlock), 0, c.st, per, g);
         }))
       return e;
+  bool have_list1 = false;  // k_unstable_index has listed the layer-1 neurons of this chunk
   for (int P = L; P >= 2; --P) {
     if (!full && P < L) break;
     if (P == 2 && P < L) {
@@ -6511,9 +6535,15 @@ int grad_chunk(const Chunk& c, int full) {
         if (e) return e;
         long n1 = net->n[1];
         e = launch_k(tag("pass2_grad_gather", 1, 2), c.st, [&] {
-          hipLaunchKernelGGL(k_pass2_grad_gather, grid_for(c.nb * n1), dim3(kBlock), 0, c.st,
-                             c.nb, dlayer(t1), dlayer(t2), t2.k * t2.k, part, pflag, code,
-                             net->n_relu, ga);
+          if (have_list1)  // the sub-domains' unstable layer-1 neurons are listed (pass 3)
+            hipLaunchKernelGGL(k_pass2_grad_gather_c, dim3((unsigned)c.nb), dim3(kBlock), 0,
+                               c.st, dlayer(t1), dlayer(t2), t2.k * t2.k, part, pflag,
+                               at<int>(c.ws, p.off_list1), at<int>(c.ws, p.off_cnt1), n1,
+                               net->n_relu, ga);
+          else
+            hipLaunchKernelGGL(k_pass2_grad_gather, grid_for(c.nb * n1), dim3(kBlock), 0, c.st,
+                               c.nb, dlayer(t1), dlayer(t2), t2.k * t2.k, part, pflag, code,
+                               net->n_relu, ga);
         });
         if (e) return e;
         continue;
@@ -6554,6 +6584,7 @@ int grad_chunk(const Chunk& c, int full) {
         int* cnt2 = at<int>(c.ws, p.off_cnt2);
         unsigned* psel = at<unsigned>(c.ws, p.off_psel);
         if (t2.out_c == 32) {
+          have_list1 = true;  // (pass 2's gather below takes the layer-1 list too)
           for (int m = 1; m <= 2; ++m)
             if (int e = launch_k(tag("unstable_index", m, P), c.st, [&] {
                   hipLaunchKernelGGL(k_unstable_index, dim3((unsigned)c.nb), dim3(256), 0, c.st,
