@@ -5134,6 +5134,20 @@ __global__ void __launch_bounds__(kBlock) k_zero(long n, float* __restrict__ p) 
   if (i < n) p[i] = 0.f;
 }
 
+// Three 16-byte-aligned arrays of n floats cleared in one launch, four floats per store.
+__global__ void __launch_bounds__(kBlock)
+    k_zero3(long n, float* __restrict__ a, float* __restrict__ b, float* __restrict__ c) {
+  const long i = (blockIdx.x * (long)blockDim.x + threadIdx.x) * 4;
+  if (i + 4 <= n) {
+    const float4v z = {0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<float4v*>(a + i) = z;
+    *reinterpret_cast<float4v*>(b + i) = z;
+    *reinterpret_cast<float4v*>(c + i) = z;
+  } else {
+    for (long k = i; k < n; ++k) a[k] = b[k] = c[k] = 0.f;
+  }
+}
+
 // Spec rows of an upper bound (Eq. 8: max_x U = -min_x of the lower function of -C): out holds
 // [C; -C] (both = 1) or -C alone, [rows][nL].
 __global__ void __launch_bounds__(kBlock) k_spec_pm(long n, const float* __restrict__ C,
@@ -6510,11 +6524,12 @@ int grad_chunk(const Chunk& c, int full) {
   float* za = at<float>(c.ws, p.off_za);
   float* zb = at<float>(c.ws, p.off_zb);
   float* G = at<float>(c.ws, p.off_G);
-  for (float* g : {ga, gl, gu})
-    if (int e = launch_k("zero", c.st, [&] {
-          hipLaunchKernelGGL(k_zero, grid_for(per), dim3(kBlock), 0, c.st, per, g);
-        }))
-      return e;
+  // (workspace regions: 256-byte aligned)
+  if (int e = launch_k("zero", c.st, [&] {
+        hipLaunchKernelGGL(k_zero3, grid_for((per + 3) / 4), dim3(kBlock), 0, c.st, per, ga, gl,
+                           gu);
+      }))
+    return e;
   bool have_list1 = false;  // k_unstable_index has listed the layer-1 neurons of this chunk
   for (int P = L; P >= 2; --P) {
     if (!full && P < L) break;
