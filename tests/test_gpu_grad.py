@@ -118,6 +118,21 @@ def test_grad_conv_nets(name):
                lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, alpha, b, j))
 
 
+@pytest.mark.parametrize("B", [1, 3])
+def test_grad_wide_small_batches(B):
+    # one sub-domain, and three (600 rows of pass 3: 75 groups of 8), through the per-sub-domain
+    # set-up of the fused pass-3 forward (unstable-neuron lists, position pairs) and the listed
+    # pass-2 gather
+    w = wl.get("wide")
+    rnet, split, alpha = setup(w.layers, w.x0, w.eps, w.C, B, w.max_splits, 11 + B)
+    net = lirpa.Network(w.layers)
+    lb, g = net.bound_grad(dev(w.x0), w.eps, dev(w.C), dev(split), dev(alpha))
+    lr, gr = ref.bound_grad(rnet, w.x0, w.eps, w.C, split, alpha)
+    check_bound(f"wide B={B} lb", lb.cpu().double().numpy(), lr)
+    check_grad(f"wide B={B} grad", g.cpu().double().numpy(), gr, split,
+               lambda b, j: one_sided(rnet, w.x0, w.eps, w.C, split, alpha, b, j))
+
+
 # least share of the unstable neurons of the sampled C4 sub-domains whose final alpha lies within
 # 1e-3 of the oracle's own fp64 trajectory
 ALPHA_AGREE = 0.95
